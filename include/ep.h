@@ -1,0 +1,210 @@
+/*
+ * ep.h -- C ABI of the MI355X expert-parallel dispatch/combine library (libep.so).
+ *
+ * One GPU is one rank of an expert-parallel (EP) group of R ranks.  A MoE layer's
+ * router has picked k of E experts per token; experts are placed contiguously, rank r
+ * holding experts [r*L, (r+1)*L) with L = E/R.  The library computes this rank's share
+ * of the layer's communication (Lee et al., "Efficient Expert-Parallel Communication on
+ * PCIe-Connected Consumer GPUs"):
+ *
+ *   ep_dispatch_layout  counts, prefix offsets and the packed row of every (token, slot),
+ *                       grouping rows by destination rank, then expert, then token
+ *                       (Sec. 4.3: tokens are grouped by the experts that consume them;
+ *                       Sec. 4.5: routing-aware transfer of only the rows each
+ *                       destination needs).
+ *   ep_dispatch         packs the token rows into that contiguous layout (Sec. 2.2:
+ *                       a DMA engine moves only contiguous regions, so a kernel packs
+ *                       routing-dependent rows first) and, with host staging, moves the
+ *                       packed buffer to a pinned host bounce buffer on a DMA (SDMA)
+ *                       stream in fixed chunks, raising one completion flag per chunk in
+ *                       host memory (Sec. 4.3 DMA offload; Sec. 4.4 flags kept apart
+ *                       from the payload).
+ *   ep_combine          waits for the peers' completion flags (one polling lane per
+ *                       sender, with pauses between polls: Sec. 4.4), moves the returned
+ *                       rows host->device on a second DMA stream, and reduces each
+ *                       token's k returned rows, weighted by its gates, in fp32 back into
+ *                       token order on the GPU (Sec. 4.3: the reduction stays on the GPU
+ *                       because a DMA engine cannot add).
+ *   ep_staging_alloc    the send/receive buffers (HBM, or HBM plus pinned host bounce
+ *                       buffers) with their flags and DMA streams.
+ *
+ * Conventions for every call:
+ *   - Pointers named *_dev (and every array argument not marked "host") are device
+ *     pointers on the current HIP device; the caller owns them.  bf16 data is passed as
+ *     raw 16-bit patterns.  Byte offsets are 64-bit; rows are never assumed < 2^31 bytes.
+ *   - Every call only enqueues work on `stream` (0 = the null stream) and returns; the
+ *     outputs are valid once `stream` has reached that point.  Only ep_layout_status,
+ *     ep_staging_status, ep_staging_alloc/free and ep_trace_read block.
+ *   - Argument errors a host can see are reported synchronously and nothing is enqueued.
+ *     Errors that depend on device data (an expert id out of range, a token row naming
+ *     an expert twice, a flag wait that expired) are recorded in a status word and read
+ *     by ep_layout_status / ep_staging_status.  No call throws.
+ *   - ep_last_error() returns this thread's text for the last non-OK status.
+ *   - Calls on one ep_staging must not overlap from several host threads.
+ */
+#ifndef EP_H
+#define EP_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define EP_ABI_VERSION 1
+#define EP_MAX_EXPERTS 2048 /* largest E the layout kernels accept */
+
+typedef enum {
+    EP_OK = 0,
+    EP_ERR_INVALID_ARG = 1, /* a size, pointer or mode the call cannot accept */
+    EP_ERR_BAD_ROUTING = 2, /* an expert id outside [0,E) or repeated within a token row */
+    EP_ERR_HIP = 3,         /* the HIP runtime reported an error (text in ep_last_error) */
+    EP_ERR_OOM = 4,         /* device or pinned host allocation failed */
+    EP_ERR_TIMEOUT = 5,     /* a bounded completion-flag wait expired */
+} ep_status;
+
+typedef enum {
+    EP_STAGING_HBM = 0,         /* send/recv buffers in HBM only; no host leg */
+    EP_STAGING_PINNED_HOST = 1, /* plus pinned host bounce buffers, SDMA legs, host flags */
+} ep_staging_kind;
+
+typedef enum {
+    EP_OUT_BF16 = 0, /* combine output rounded to nearest-even bf16 */
+    EP_OUT_F32 = 1,  /* combine output as the fp32 accumulator itself (exactness tests) */
+} ep_out_dtype;
+
+typedef struct ep_staging ep_staging; /* opaque, owned by the library */
+
+int32_t ep_abi_version(void);
+const char *ep_status_name(int32_t status);
+const char *ep_last_error(void);
+
+/* ------------------------------------------------------------------------- layout */
+
+/* Bytes of device workspace ep_dispatch_layout needs for T tokens, top-k, E experts. */
+ep_status ep_layout_workspace_bytes(int64_t num_tokens, int32_t topk, int32_t num_experts,
+                                    size_t *bytes /* host out */);
+
+/* Dispatch layout (Sec. 4.3 grouping; Sec. 4.5 routing-aware rows): a stable counting
+ * sort of the T*k routing entries by expert id.
+ *   topk_idx        int32 [T][k] row-major: slot j of token t selects expert topk_idx[t*k+j].
+ *   expert_counts   int32 [E]: rows for expert e (one per (token, slot) selecting it).
+ *   expert_offsets  int32 [E+1]: exclusive prefix sum of expert_counts; [E] = T*k.
+ *   rank_counts     int32 [R]: rows for rank r = sum of its experts' counts.
+ *   rank_offsets    int32 [R+1]: rank_offsets[r] = expert_offsets[r*E/R]; [R] = T*k.
+ *   slot_pos        int32 [T*k]: packed row of slot t*k+j = expert_offsets[e] + number of
+ *                   earlier slots (smaller flat index) with the same expert.
+ *   row_src         int32 [T*k] or NULL: inverse of slot_pos (row p came from slot row_src[p]).
+ *   workspace       device scratch of ep_layout_workspace_bytes() bytes; it also holds
+ *                   the routing status word read by ep_layout_status.
+ * Requires T >= 0, T*k < 2^31, 1 <= k <= E <= EP_MAX_EXPERTS, R >= 1, E % R == 0.
+ * T == 0 is valid: counts and offsets are written as zeros.  With an invalid expert id
+ * the outputs are unspecified but every write stays inside the arrays above, and the
+ * slot of that id gets slot_pos = -1. */
+ep_status ep_dispatch_layout(const int32_t *topk_idx, int64_t num_tokens, int32_t topk,
+                             int32_t num_experts, int32_t num_ranks,
+                             int32_t *expert_counts, int32_t *expert_offsets,
+                             int32_t *rank_counts, int32_t *rank_offsets,
+                             int32_t *slot_pos, int32_t *row_src,
+                             void *workspace, size_t workspace_bytes, hipStream_t stream);
+
+/* Synchronizes `stream`, then reads the status word the last layout on `workspace` left:
+ * EP_OK, or EP_ERR_BAD_ROUTING (an id outside [0,E) or an expert repeated in a row). */
+ep_status ep_layout_status(const void *workspace, hipStream_t stream);
+
+/* ------------------------------------------------------------------------ staging */
+
+/* Allocates the staging of one rank.
+ *   kind         EP_STAGING_HBM or EP_STAGING_PINNED_HOST.
+ *   max_rows     rows per buffer (>= T*k of every later call), hidden = H (multiple of 8).
+ *   num_ranks    R: number of senders whose completion flags ep_combine waits for.
+ *   num_buffers  1..8 independent buffer sets (alternate them between rounds).
+ *   chunk_bytes  size of one host-leg DMA chunk (0 = 8 MiB); rounded up to 4 KiB.
+ * Per buffer: HBM send (packed) and recv (returned rows) buffers of max_rows*H*2 bytes;
+ * with PINNED_HOST also pinned host send/recv bounce buffers of the same size, one
+ * uint32 send flag per chunk and one uint32 recv flag per sender in coherent pinned host
+ * memory, all zero-initialised.  Creates two non-blocking DMA streams (up = D2H,
+ * down = H2D) and one signalling stream, all at default priority. */
+ep_status ep_staging_alloc(ep_staging_kind kind, int64_t max_rows, int32_t hidden,
+                           int32_t num_ranks, int32_t num_buffers, int64_t chunk_bytes,
+                           ep_staging **out);
+ep_status ep_staging_free(ep_staging *s);
+
+typedef struct {
+    int32_t kind, num_ranks, num_buffers, hidden;
+    int64_t max_rows, row_bytes, buffer_bytes, chunk_bytes;
+    int32_t max_chunks;           /* send flags per buffer */
+    void *dev_send, *dev_recv;    /* device, buffer_bytes each */
+    void *host_send, *host_recv;  /* pinned host, or NULL in HBM mode */
+    uint32_t *send_flags;         /* host [max_chunks], or NULL: flag c = epoch when chunk c landed */
+    uint32_t *recv_flags;         /* host [num_ranks], or NULL: set to epoch by sender r */
+} ep_staging_view;
+
+/* Pointers and sizes of buffer set `buf` (host pointers are usable from the host). */
+ep_status ep_staging_get(ep_staging *s, int32_t buf, ep_staging_view *view);
+
+/* Bounded flag wait used by ep_combine with host staging: give up after timeout_us
+ * microseconds (default 10 s), pausing sleep_units*64 cycles between polls (default 2). */
+ep_status ep_staging_set_wait(ep_staging *s, int64_t timeout_us, int32_t sleep_units);
+
+/* Synchronizes the staging's streams and `stream`, then returns and clears its status
+ * word: EP_OK, or EP_ERR_TIMEOUT if a flag wait expired since the last call. */
+ep_status ep_staging_status(ep_staging *s, hipStream_t stream);
+
+/* --------------------------------------------------------------- dispatch / combine */
+
+/* Dispatch of one round (epoch) into buffer set `buf`:
+ *   packed[slot_pos[t*k+j]][:] = x[t][:] for every token t and slot j   (bf16 byte copy)
+ * into the staging's HBM send buffer.  x_dev: bf16 [T][H]; slot_pos: int32 [T*k] from
+ * ep_dispatch_layout; rows with slot_pos outside [0, max_rows) are skipped.
+ * With PINNED_HOST, the first T*k rows then go device->host on the up stream in
+ * chunk_bytes pieces, and after chunk c has landed send_flags[c] is set to `epoch`.
+ * `stream` waits for the whole leg before later work.  Epochs should increase per
+ * round (flags compare as signed 32-bit differences). */
+ep_status ep_dispatch(const void *x_dev, int64_t num_tokens, int32_t hidden, int32_t topk,
+                      const int32_t *slot_pos, ep_staging *s, int32_t buf, uint32_t epoch,
+                      hipStream_t stream);
+
+/* Combine of one round from buffer set `buf`:
+ *   out[t][:] = sum_{j<k} topk_w[t*k+j] * recv[slot_pos[t*k+j]][:]
+ * accumulated in fp32 with fused multiply-adds in slot order j = 0..k-1, then rounded
+ * to nearest-even bf16 (EP_OUT_BF16) or stored as fp32 (EP_OUT_F32).  recv holds the
+ * returned rows in the packed layout.  With PINNED_HOST, first waits (bounded, see
+ * ep_staging_set_wait) until recv_flags[r] has reached `epoch` for every sender r, then
+ * moves the first T*k rows host->device on the down stream in chunk_bytes pieces.
+ * topk_w: float [T][k]; out: [T][H] of out_dtype.  Slots whose slot_pos is outside
+ * [0, max_rows) contribute nothing. */
+ep_status ep_combine(ep_staging *s, int32_t buf, uint32_t epoch, const int32_t *slot_pos,
+                     const float *topk_w, int64_t num_tokens, int32_t hidden, int32_t topk,
+                     void *out_dev, ep_out_dtype out_dtype, hipStream_t stream);
+
+/* ------------------------------------------------------------------ measurement */
+
+typedef struct {
+    char name[48];
+    int64_t count;
+    double total_ms, min_ms, max_ms;
+} ep_trace_stat;
+
+/* While enabled, every kernel launch and every host-leg DMA run of the library is
+ * bracketed by HIP timing events on the stream it runs on. */
+ep_status ep_trace_enable(int32_t on);
+/* Synchronizes the pending events and returns per-name totals (up to `capacity`). */
+ep_status ep_trace_read(ep_trace_stat *stats, int32_t capacity, int32_t *count);
+ep_status ep_trace_reset(void);
+
+/* A plain streaming copy kernel (16-byte vectors): the attainable-bandwidth probe and
+ * the calibration for hardware byte counters.  bytes must be a multiple of 16. */
+ep_status ep_copy_probe(void *dst_dev, const void *src_dev, size_t bytes, hipStream_t stream);
+
+/* hipMemcpyAsync(kind = default) passthrough for bindings that hold raw pointers. */
+ep_status ep_memcpy(void *dst, const void *src, size_t bytes, hipStream_t stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* EP_H */

@@ -1,0 +1,44 @@
+/*
+ * ep_sim.h -- simulated peer ranks for one-GPU runs of host-staged dispatch/combine.
+ *
+ * HARNESS, not part of dispatch or combine.  With one GPU there are no peer ranks; a
+ * host thread stands in for them on the host side of the staging, where the paper's
+ * peers meet (Sec. 4.2: pinned host memory as the shared medium; Sec. 4.4: completion
+ * flags in host memory).  For every posted round it
+ *   1. waits until the send flag of the round's last DMA chunk holds the round's epoch
+ *      (chunks land in order, so every packed row is then in the host send buffer),
+ *   2. in ECHO mode copies the host send buffer to the host recv buffer (every expert
+ *      is the identity), otherwise leaves the recv buffer as the harness filled it,
+ *   3. optionally sleeps delay_us (emulating the peers' expert computation), then
+ *   4. sets every sender's recv flag to the epoch, releasing this rank's combine.
+ * The thread polls with a pause instruction and gives up on a round after 60 s, which
+ * ep_sim_peers_drain then reports as EP_ERR_TIMEOUT.
+ */
+#ifndef EP_SIM_H
+#define EP_SIM_H
+
+#include "ep.h"
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum { EP_SIM_FLAGS_ONLY = 0, EP_SIM_ECHO = 1 } ep_sim_mode;
+
+typedef struct ep_sim_peers ep_sim_peers;
+
+/* Starts the peer thread for a PINNED_HOST staging (EP_ERR_INVALID_ARG otherwise). */
+ep_status ep_sim_peers_start(ep_staging *s, ep_sim_mode mode, ep_sim_peers **out);
+/* Queues one round: `rows` packed rows were dispatched into buffer `buf` with `epoch`. */
+ep_status ep_sim_peers_post(ep_sim_peers *p, int32_t buf, uint32_t epoch, int64_t rows,
+                            int64_t delay_us);
+/* Blocks until every posted round was answered (or timeout_ms passed). */
+ep_status ep_sim_peers_drain(ep_sim_peers *p, int64_t timeout_ms);
+/* Stops and joins the thread (pending rounds are dropped). */
+ep_status ep_sim_peers_stop(ep_sim_peers *p);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* EP_SIM_H */

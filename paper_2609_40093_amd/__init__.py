@@ -1,0 +1,19 @@
+"""MI355X-native expert-parallel MoE token dispatch and combine (one rank's share).
+
+The work happens in libep.so (HIP kernels for gfx950 plus SDMA host legs; C ABI in
+include/ep.h).  ``paper_2609_40093_amd.api`` is its Python binding; the names below are
+re-exported lazily so that ``paper_2609_40093_amd.synth`` (input generation only) can be
+imported without torch or a GPU.
+"""
+
+_API = ("EPError", "Layout", "Staging", "SimPeers", "dispatch_layout", "layout_status", "dispatch", "combine",
+        "trace_enable", "trace_read", "trace_reset", "copy_probe", "workspace_bytes")
+
+__all__ = list(_API)
+
+
+def __getattr__(name):
+    if name in _API:
+        from . import api
+        return getattr(api, name)
+    raise AttributeError(name)

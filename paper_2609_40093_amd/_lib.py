@@ -1,0 +1,82 @@
+"""ctypes declarations of libep.so (include/ep.h and include/ep_sim.h).
+
+Loading fails loudly when the library has not been built: there is no fallback path.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(PKG, "libep.so")
+
+EP_OK, EP_ERR_INVALID_ARG, EP_ERR_BAD_ROUTING, EP_ERR_HIP, EP_ERR_OOM, EP_ERR_TIMEOUT = range(6)
+EP_STAGING_HBM, EP_STAGING_PINNED_HOST = 0, 1
+EP_OUT_BF16, EP_OUT_F32 = 0, 1
+EP_SIM_FLAGS_ONLY, EP_SIM_ECHO = 0, 1
+EP_MAX_EXPERTS = 2048
+
+c_i32, c_i64, c_u32, c_size, c_vp = ctypes.c_int32, ctypes.c_int64, ctypes.c_uint32, ctypes.c_size_t, ctypes.c_void_p
+c_i32p = ctypes.POINTER(ctypes.c_int32)
+
+
+class StagingView(ctypes.Structure):
+    _fields_ = [("kind", c_i32), ("num_ranks", c_i32), ("num_buffers", c_i32), ("hidden", c_i32),
+                ("max_rows", c_i64), ("row_bytes", c_i64), ("buffer_bytes", c_i64), ("chunk_bytes", c_i64),
+                ("max_chunks", c_i32),
+                ("dev_send", c_vp), ("dev_recv", c_vp), ("host_send", c_vp), ("host_recv", c_vp),
+                ("send_flags", c_vp), ("recv_flags", c_vp)]
+
+
+class TraceStat(ctypes.Structure):
+    _fields_ = [("name", ctypes.c_char * 48), ("count", c_i64), ("total_ms", ctypes.c_double),
+                ("min_ms", ctypes.c_double), ("max_ms", ctypes.c_double)]
+
+
+# name -> (restype, argtypes)
+SIGNATURES = {
+    "ep_abi_version": (c_i32, []),
+    "ep_status_name": (ctypes.c_char_p, [c_i32]),
+    "ep_last_error": (ctypes.c_char_p, []),
+    "ep_layout_workspace_bytes": (c_i32, [c_i64, c_i32, c_i32, ctypes.POINTER(c_size)]),
+    "ep_dispatch_layout": (c_i32, [c_vp, c_i64, c_i32, c_i32, c_i32, c_vp, c_vp, c_vp, c_vp, c_vp, c_vp,
+                                   c_vp, c_size, c_vp]),
+    "ep_layout_status": (c_i32, [c_vp, c_vp]),
+    "ep_staging_alloc": (c_i32, [c_i32, c_i64, c_i32, c_i32, c_i32, c_i64, ctypes.POINTER(c_vp)]),
+    "ep_staging_free": (c_i32, [c_vp]),
+    "ep_staging_get": (c_i32, [c_vp, c_i32, ctypes.POINTER(StagingView)]),
+    "ep_staging_set_wait": (c_i32, [c_vp, c_i64, c_i32]),
+    "ep_staging_status": (c_i32, [c_vp, c_vp]),
+    "ep_dispatch": (c_i32, [c_vp, c_i64, c_i32, c_i32, c_vp, c_vp, c_i32, c_u32, c_vp]),
+    "ep_combine": (c_i32, [c_vp, c_i32, c_u32, c_vp, c_vp, c_i64, c_i32, c_i32, c_vp, c_i32, c_vp]),
+    "ep_trace_enable": (c_i32, [c_i32]),
+    "ep_trace_read": (c_i32, [ctypes.POINTER(TraceStat), c_i32, ctypes.POINTER(c_i32)]),
+    "ep_trace_reset": (c_i32, []),
+    "ep_copy_probe": (c_i32, [c_vp, c_vp, c_size, c_vp]),
+    "ep_memcpy": (c_i32, [c_vp, c_vp, c_size, c_vp]),
+    "ep_sim_peers_start": (c_i32, [c_vp, c_i32, ctypes.POINTER(c_vp)]),
+    "ep_sim_peers_post": (c_i32, [c_vp, c_i32, c_u32, c_i64, c_i64]),
+    "ep_sim_peers_drain": (c_i32, [c_vp, c_i64]),
+    "ep_sim_peers_stop": (c_i32, [c_vp]),
+}
+
+_lib = None
+
+
+def load(path: str = LIB_PATH):
+    """Load libep.so; raises if it is missing (build it with __graft_entry__.build())."""
+    global _lib
+    if _lib is not None and path == LIB_PATH:
+        return _lib
+    if not os.path.exists(path):
+        raise RuntimeError(f"{path} is not built: run `python -c 'import __graft_entry__ as g; g.build()'`")
+    lib = ctypes.CDLL(path)
+    for name, (res, args) in SIGNATURES.items():
+        fn = getattr(lib, name)
+        fn.restype = res
+        fn.argtypes = args
+    if lib.ep_abi_version() != 1:
+        raise RuntimeError("libep.so ABI version mismatch")
+    if path == LIB_PATH:
+        _lib = lib
+    return lib

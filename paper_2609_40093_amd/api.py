@@ -1,0 +1,284 @@
+"""Python binding of libep: the same calls as include/ep.h, marshalling only.
+
+Every step of dispatch and combine runs in the library's HIP kernels or its DMA legs;
+PyTorch provides device memory and streams.  Tensors must live on the current CUDA/HIP
+device.  bf16 payload may be given as torch.bfloat16 or as raw 16-bit patterns
+(torch.int16 / torch.uint16); only the bytes are used.
+"""
+from __future__ import annotations
+
+import ctypes
+from dataclasses import dataclass
+from typing import Optional
+
+import numpy as np
+import torch
+
+from . import _lib
+from ._lib import (EP_OK, EP_ERR_BAD_ROUTING, EP_ERR_TIMEOUT, EP_STAGING_HBM, EP_STAGING_PINNED_HOST,
+                   EP_OUT_BF16, EP_OUT_F32, EP_SIM_ECHO, EP_SIM_FLAGS_ONLY)
+
+__all__ = ["EPError", "Layout", "Staging", "SimPeers", "dispatch_layout", "layout_status", "dispatch",
+           "combine", "trace_enable", "trace_read", "trace_reset", "copy_probe", "workspace_bytes"]
+
+_PAYLOAD_DTYPES = (torch.bfloat16, torch.int16, torch.uint16)
+
+
+class EPError(RuntimeError):
+    def __init__(self, status: int, message: str):
+        super().__init__(message)
+        self.status = status
+
+
+def _lib_handle():
+    return _lib.load()
+
+
+def _check(status: int, what: str):
+    if status != EP_OK:
+        lib = _lib_handle()
+        name = lib.ep_status_name(status).decode()
+        raise EPError(status, f"{what}: {name}: {lib.ep_last_error().decode()}")
+
+
+def _stream_ptr(stream: Optional[torch.cuda.Stream]) -> ctypes.c_void_p:
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+def _ptr(t: Optional[torch.Tensor]) -> ctypes.c_void_p:
+    return ctypes.c_void_p(t.data_ptr() if t is not None and t.numel() else None)
+
+
+def _need(t: torch.Tensor, name: str, dtypes, ndim=None):
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be a device tensor")
+    if t.dtype not in dtypes:
+        raise ValueError(f"{name} has dtype {t.dtype}, expected one of {dtypes}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if ndim is not None and t.dim() != ndim:
+        raise ValueError(f"{name} must have {ndim} dimensions")
+
+
+def workspace_bytes(num_tokens: int, topk: int, num_experts: int) -> int:
+    n = ctypes.c_size_t()
+    _check(_lib_handle().ep_layout_workspace_bytes(num_tokens, topk, num_experts, ctypes.byref(n)),
+           "ep_layout_workspace_bytes")
+    return n.value
+
+
+@dataclass
+class Layout:
+    num_tokens: int
+    topk: int
+    num_experts: int
+    num_ranks: int
+    expert_counts: torch.Tensor
+    expert_offsets: torch.Tensor
+    rank_counts: torch.Tensor
+    rank_offsets: torch.Tensor
+    slot_pos: torch.Tensor
+    row_src: Optional[torch.Tensor]
+    workspace: torch.Tensor
+
+
+def dispatch_layout(topk_idx: torch.Tensor, num_experts: int, num_ranks: int, *, with_row_src: bool = True,
+                    out: Optional[Layout] = None, stream=None) -> Layout:
+    """ep_dispatch_layout on a [T, k] int32 routing tensor; outputs are device tensors."""
+    _need(topk_idx, "topk_idx", (torch.int32,), 2)
+    T, k = topk_idx.shape
+    dev = topk_idx.device
+    if out is None or out.num_tokens != T or out.topk != k or out.num_experts != num_experts \
+            or out.num_ranks != num_ranks:
+        i32 = dict(dtype=torch.int32, device=dev)
+        out = Layout(T, k, num_experts, num_ranks,
+                     torch.empty(num_experts, **i32), torch.empty(num_experts + 1, **i32),
+                     torch.empty(num_ranks, **i32), torch.empty(num_ranks + 1, **i32),
+                     torch.empty(T * k, **i32), torch.empty(T * k, **i32) if with_row_src else None,
+                     torch.empty(workspace_bytes(T, k, num_experts) if 1 <= k <= num_experts
+                                 and 1 <= num_experts <= _lib.EP_MAX_EXPERTS else 256,
+                                 dtype=torch.uint8, device=dev))
+    st = _lib_handle().ep_dispatch_layout(
+        _ptr(topk_idx), T, k, num_experts, num_ranks, _ptr(out.expert_counts), _ptr(out.expert_offsets),
+        _ptr(out.rank_counts), _ptr(out.rank_offsets), _ptr(out.slot_pos), _ptr(out.row_src),
+        _ptr(out.workspace), out.workspace.numel(), _stream_ptr(stream))
+    _check(st, "ep_dispatch_layout")
+    return out
+
+
+def layout_status(layout: Layout, stream=None) -> None:
+    """Synchronizes and raises EPError(EP_ERR_BAD_ROUTING) if the routing was rejected."""
+    _check(_lib_handle().ep_layout_status(_ptr(layout.workspace), _stream_ptr(stream)), "ep_layout_status")
+
+
+class Staging:
+    """Library-owned send/recv buffers of one rank (ep_staging_alloc)."""
+
+    def __init__(self, kind: str, max_rows: int, hidden: int, num_ranks: int, num_buffers: int = 2,
+                 chunk_bytes: int = 0):
+        kinds = {"hbm": EP_STAGING_HBM, "pinned": EP_STAGING_PINNED_HOST}
+        if kind not in kinds:
+            raise ValueError(f"kind must be one of {list(kinds)}")
+        self.kind = kind
+        handle = ctypes.c_void_p()
+        _check(_lib_handle().ep_staging_alloc(kinds[kind], max_rows, hidden, num_ranks, num_buffers,
+                                              chunk_bytes, ctypes.byref(handle)), "ep_staging_alloc")
+        self.handle = handle
+        self.views = [self._view(b) for b in range(num_buffers)]
+        v = self.views[0]
+        self.max_rows, self.hidden, self.num_ranks = v.max_rows, v.hidden, v.num_ranks
+        self.num_buffers, self.row_bytes, self.chunk_bytes = v.num_buffers, v.row_bytes, v.chunk_bytes
+        self.max_chunks = v.max_chunks
+
+    def _view(self, buf: int) -> _lib.StagingView:
+        v = _lib.StagingView()
+        _check(_lib_handle().ep_staging_get(self.handle, buf, ctypes.byref(v)), "ep_staging_get")
+        return v
+
+    def close(self):
+        if self.handle:
+            _check(_lib_handle().ep_staging_free(self.handle), "ep_staging_free")
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    # host views (pinned staging only): zero-copy numpy arrays over pinned memory
+    def host_array(self, which: str, buf: int = 0) -> np.ndarray:
+        v = self.views[buf]
+        if which in ("send", "recv"):
+            ptr = v.host_send if which == "send" else v.host_recv
+            if not ptr:
+                raise ValueError("host buffers exist only with pinned staging")
+            return np.ctypeslib.as_array(ctypes.cast(ptr, ctypes.POINTER(ctypes.c_uint16)),
+                                         shape=(self.max_rows, self.hidden))
+        if which in ("send_flags", "recv_flags"):
+            ptr = v.send_flags if which == "send_flags" else v.recv_flags
+            if not ptr:
+                raise ValueError("flags exist only with pinned staging")
+            n = self.max_chunks if which == "send_flags" else self.num_ranks
+            return np.ctypeslib.as_array(ctypes.cast(ptr, ctypes.POINTER(ctypes.c_uint32)), shape=(n,))
+        raise ValueError(which)
+
+    def read_device(self, which: str, rows: int, buf: int = 0, stream=None) -> torch.Tensor:
+        """Copy of the first `rows` rows of the device send or recv buffer (int16 bits)."""
+        v = self.views[buf]
+        ptr = v.dev_send if which == "send" else v.dev_recv
+        out = torch.empty((rows, self.hidden), dtype=torch.int16, device="cuda")
+        _check(_lib_handle().ep_memcpy(_ptr(out), ctypes.c_void_p(ptr), rows * self.row_bytes,
+                                       _stream_ptr(stream)), "ep_memcpy")
+        return out
+
+    def write_device(self, which: str, rows: torch.Tensor, buf: int = 0, stream=None) -> None:
+        """Copies a [rows, hidden] 16-bit device tensor into the device send or recv buffer."""
+        _need(rows, "rows", _PAYLOAD_DTYPES, 2)
+        if rows.shape[1] != self.hidden or rows.shape[0] > self.max_rows:
+            raise ValueError("rows do not fit the staging buffer")
+        v = self.views[buf]
+        ptr = v.dev_send if which == "send" else v.dev_recv
+        _check(_lib_handle().ep_memcpy(ctypes.c_void_p(ptr), _ptr(rows), rows.numel() * 2, _stream_ptr(stream)),
+               "ep_memcpy")
+
+    def set_wait(self, timeout_us: int, sleep_units: int = 2) -> None:
+        _check(_lib_handle().ep_staging_set_wait(self.handle, timeout_us, sleep_units), "ep_staging_set_wait")
+
+    def status(self, stream=None) -> None:
+        """Synchronizes; raises EPError(EP_ERR_TIMEOUT) if a flag wait expired."""
+        _check(_lib_handle().ep_staging_status(self.handle, _stream_ptr(stream)), "ep_staging_status")
+
+
+def dispatch(x: torch.Tensor, slot_pos: torch.Tensor, staging: Staging, *, topk: int, buf: int = 0,
+             epoch: int = 1, stream=None) -> None:
+    """ep_dispatch: pack x [T, H] (bf16 bits) into staging buffer `buf` (and its host leg)."""
+    _need(x, "x", _PAYLOAD_DTYPES, 2)
+    _need(slot_pos, "slot_pos", (torch.int32,), 1)
+    T, H = x.shape
+    if slot_pos.numel() != T * topk:
+        raise ValueError("slot_pos must hold T*topk entries")
+    _check(_lib_handle().ep_dispatch(_ptr(x), T, H, topk, _ptr(slot_pos), staging.handle, buf, epoch & 0xFFFFFFFF,
+                                     _stream_ptr(stream)), "ep_dispatch")
+
+
+def combine(staging: Staging, slot_pos: torch.Tensor, topk_w: torch.Tensor, *, out: Optional[torch.Tensor] = None,
+            out_dtype: torch.dtype = torch.bfloat16, buf: int = 0, epoch: int = 1, stream=None) -> torch.Tensor:
+    """ep_combine: out [T, H] = sum_j w[t, j] * recv[slot_pos[t*k + j]] (fp32 accumulate)."""
+    _need(topk_w, "topk_w", (torch.float32,), 2)
+    _need(slot_pos, "slot_pos", (torch.int32,), 1)
+    T, k = topk_w.shape
+    H = staging.hidden
+    if out is None:
+        out = torch.empty((T, H), dtype=out_dtype, device=topk_w.device)
+    if out.dtype == torch.float32:
+        code = EP_OUT_F32
+    elif out.dtype in _PAYLOAD_DTYPES:
+        code = EP_OUT_BF16
+    else:
+        raise ValueError("out must be bf16 (or 16-bit bits) or float32")
+    _need(out, "out", (out.dtype,), 2)
+    if tuple(out.shape) != (T, H) or slot_pos.numel() != T * k:
+        raise ValueError("shape mismatch between out, topk_w and slot_pos")
+    _check(_lib_handle().ep_combine(staging.handle, buf, epoch & 0xFFFFFFFF, _ptr(slot_pos), _ptr(topk_w), T, H, k,
+                                    _ptr(out), code, _stream_ptr(stream)), "ep_combine")
+    return out
+
+
+class SimPeers:
+    """Host thread standing in for the peer ranks of a pinned staging (include/ep_sim.h)."""
+
+    def __init__(self, staging: Staging, echo: bool = False):
+        handle = ctypes.c_void_p()
+        _check(_lib_handle().ep_sim_peers_start(staging.handle, EP_SIM_ECHO if echo else EP_SIM_FLAGS_ONLY,
+                                                ctypes.byref(handle)), "ep_sim_peers_start")
+        self.handle = handle
+        self.staging = staging  # keep the staging alive while the thread reads it
+
+    def post(self, buf: int, epoch: int, rows: int, delay_us: int = 0) -> None:
+        _check(_lib_handle().ep_sim_peers_post(self.handle, buf, epoch & 0xFFFFFFFF, rows, delay_us),
+               "ep_sim_peers_post")
+
+    def drain(self, timeout_ms: int = 60000) -> None:
+        _check(_lib_handle().ep_sim_peers_drain(self.handle, timeout_ms), "ep_sim_peers_drain")
+
+    def close(self) -> None:
+        if self.handle:
+            _lib_handle().ep_sim_peers_stop(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+def trace_enable(on: bool = True) -> None:
+    _check(_lib_handle().ep_trace_enable(1 if on else 0), "ep_trace_enable")
+
+
+def trace_reset() -> None:
+    _check(_lib_handle().ep_trace_reset(), "ep_trace_reset")
+
+
+def trace_read() -> dict:
+    """{name: {count, total_ms, mean_ms, min_ms, max_ms}} of the traced launches so far."""
+    cap = 64
+    arr = (_lib.TraceStat * cap)()
+    n = ctypes.c_int32()
+    _check(_lib_handle().ep_trace_read(arr, cap, ctypes.byref(n)), "ep_trace_read")
+    out = {}
+    for i in range(n.value):
+        s = arr[i]
+        out[s.name.decode()] = dict(count=s.count, total_ms=s.total_ms, mean_ms=s.total_ms / max(1, s.count),
+                                    min_ms=s.min_ms, max_ms=s.max_ms)
+    return out
+
+
+def copy_probe(dst: torch.Tensor, src: torch.Tensor, stream=None) -> None:
+    nbytes = src.numel() * src.element_size()
+    if dst.numel() * dst.element_size() < nbytes:
+        raise ValueError("dst smaller than src")
+    _check(_lib_handle().ep_copy_probe(_ptr(dst), _ptr(src), nbytes, _stream_ptr(stream)), "ep_copy_probe")

@@ -1,0 +1,571 @@
+// ep_api.cpp -- host side of libep: the C ABI declared in include/ep.h.
+//
+// Argument checks, staging buffers and their DMA streams, the chunked host legs, flag
+// writes and waits, and the timing-event tracer.  Every call enqueues on the caller's
+// stream; the library's side streams (up = D2H, down = H2D, sig = flag writes) join the
+// caller's stream through events, so the caller sees one ordered stream.
+#include "ep.h"
+#include "ep_internal.h"
+
+#include <algorithm>
+#include <atomic>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <map>
+#include <mutex>
+#include <string>
+#include <vector>
+
+namespace {
+
+thread_local std::string g_last_error;
+
+ep_status fail(ep_status st, const char *fmt, ...) {
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof buf, fmt, ap);
+    va_end(ap);
+    g_last_error = buf;
+    return st;
+}
+
+ep_status hip_fail(hipError_t e, const char *what) {
+    (void)hipGetLastError();  // reported here; do not let a later launch check see it again
+    return fail(e == hipErrorOutOfMemory ? EP_ERR_OOM : EP_ERR_HIP, "%s: %s (%d)", what,
+                hipGetErrorString(e), (int)e);
+}
+
+#define EP_HIP(call)                                                                                \
+    do {                                                                                            \
+        hipError_t e_ = (call);                                                                     \
+        if (e_ != hipSuccess)                                                                       \
+            return hip_fail(e_, #call);                                                             \
+    } while (0)
+
+bool aligned16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+constexpr int kMaxBuffers = 8;
+constexpr int64_t kDefaultChunk = 8ll << 20;
+
+}  // namespace
+
+struct ep_staging {
+    int device = -1;
+    ep_staging_kind kind = EP_STAGING_HBM;
+    int64_t max_rows = 0;
+    int32_t hidden = 0, num_ranks = 0, num_buffers = 0, max_chunks = 0;
+    int64_t row_bytes = 0, buffer_bytes = 0, chunk_bytes = 0;
+    void *dev_send[kMaxBuffers] = {}, *dev_recv[kMaxBuffers] = {};
+    void *host_send[kMaxBuffers] = {}, *host_recv[kMaxBuffers] = {};
+    uint32_t *flags = nullptr;  // coherent pinned: send [nbuf][max_chunks], recv [nbuf][R], status
+    size_t flag_words = 0;
+    hipStream_t up = nullptr, down = nullptr, sig = nullptr;
+    hipEvent_t ev_up_in[kMaxBuffers] = {}, ev_up_done[kMaxBuffers] = {};
+    hipEvent_t ev_down_in[kMaxBuffers] = {}, ev_down_done[kMaxBuffers] = {};
+    std::vector<hipEvent_t> ev_chunk;  // [nbuf][max_chunks]
+    int64_t timeout_us = 10ll * 1000 * 1000;
+    int32_t sleep_units = 2;
+    int64_t wall_clock_khz = 100000;
+
+    uint32_t *send_flags(int b) const { return flags + (size_t)b * max_chunks; }
+    uint32_t *recv_flags(int b) const {
+        return flags + (size_t)num_buffers * max_chunks + (size_t)b * num_ranks;
+    }
+    uint32_t *status() const { return flags + (size_t)num_buffers * (max_chunks + num_ranks); }
+};
+
+// ------------------------------------------------------------------------- tracing
+
+namespace ep {
+namespace {
+std::atomic<bool> g_trace_on{false};
+std::mutex g_trace_mu;
+struct Pending {
+    std::string name;
+    hipEvent_t start, stop;
+};
+std::vector<Pending> g_pending;
+std::vector<hipEvent_t> g_event_pool;
+struct Stat {
+    int64_t count = 0;
+    double total = 0, mn = 1e300, mx = 0;
+};
+std::map<std::string, Stat> g_stats;
+
+hipEvent_t pool_get() {
+    if (!g_event_pool.empty()) {
+        hipEvent_t e = g_event_pool.back();
+        g_event_pool.pop_back();
+        return e;
+    }
+    hipEvent_t e = nullptr;
+    if (hipEventCreate(&e) != hipSuccess)
+        return nullptr;
+    return e;
+}
+}  // namespace
+
+TraceSlot trace_acquire() {
+    TraceSlot s;
+    if (!g_trace_on.load(std::memory_order_relaxed))
+        return s;
+    std::lock_guard<std::mutex> lk(g_trace_mu);
+    s.start = pool_get();
+    s.stop = pool_get();
+    if (!s.start || !s.stop) {
+        if (s.start)
+            g_event_pool.push_back(s.start);
+        if (s.stop)
+            g_event_pool.push_back(s.stop);
+        s = TraceSlot{};
+    }
+    return s;
+}
+
+void trace_submit(const char *name, TraceSlot slot) {
+    if (!slot.start)
+        return;
+    std::lock_guard<std::mutex> lk(g_trace_mu);
+    g_pending.push_back({name, slot.start, slot.stop});
+}
+
+}  // namespace ep
+
+// ---------------------------------------------------------------------------- misc
+
+extern "C" int32_t ep_abi_version(void) { return EP_ABI_VERSION; }
+
+extern "C" const char *ep_status_name(int32_t status) {
+    switch (status) {
+    case EP_OK: return "EP_OK";
+    case EP_ERR_INVALID_ARG: return "EP_ERR_INVALID_ARG";
+    case EP_ERR_BAD_ROUTING: return "EP_ERR_BAD_ROUTING";
+    case EP_ERR_HIP: return "EP_ERR_HIP";
+    case EP_ERR_OOM: return "EP_ERR_OOM";
+    case EP_ERR_TIMEOUT: return "EP_ERR_TIMEOUT";
+    default: return "EP_ERR_UNKNOWN";
+    }
+}
+
+extern "C" const char *ep_last_error(void) { return g_last_error.c_str(); }
+
+// -------------------------------------------------------------------------- layout
+
+extern "C" ep_status ep_layout_workspace_bytes(int64_t num_tokens, int32_t topk, int32_t num_experts,
+                                               size_t *bytes) {
+    if (!bytes)
+        return fail(EP_ERR_INVALID_ARG, "ep_layout_workspace_bytes: bytes is NULL");
+    if (num_tokens < 0 || topk < 1 || num_experts < 1 || num_experts > EP_MAX_EXPERTS)
+        return fail(EP_ERR_INVALID_ARG, "ep_layout_workspace_bytes: bad sizes T=%lld k=%d E=%d",
+                    (long long)num_tokens, topk, num_experts);
+    *bytes = ep::layout_workspace_bytes(num_tokens * topk, num_experts);
+    return EP_OK;
+}
+
+extern "C" ep_status ep_dispatch_layout(const int32_t *topk_idx, int64_t num_tokens, int32_t topk,
+                                        int32_t num_experts, int32_t num_ranks, int32_t *expert_counts,
+                                        int32_t *expert_offsets, int32_t *rank_counts,
+                                        int32_t *rank_offsets, int32_t *slot_pos, int32_t *row_src,
+                                        void *workspace, size_t workspace_bytes, hipStream_t stream) {
+    const int64_t T = num_tokens;
+    const int32_t k = topk, E = num_experts, R = num_ranks;
+    if (T < 0 || E < 1 || E > EP_MAX_EXPERTS || k < 1 || k > E || R < 1 || E % R != 0)
+        return fail(EP_ERR_INVALID_ARG,
+                    "ep_dispatch_layout: need T >= 0, 1 <= k <= E <= %d, R >= 1, E %% R == 0 "
+                    "(T=%lld k=%d E=%d R=%d)",
+                    EP_MAX_EXPERTS, (long long)T, k, E, R);
+    if (T * (int64_t)k > INT32_MAX)
+        return fail(EP_ERR_INVALID_ARG, "ep_dispatch_layout: T*k = %lld does not fit int32",
+                    (long long)(T * k));
+    if (!expert_counts || !expert_offsets || !rank_counts || !rank_offsets || !workspace)
+        return fail(EP_ERR_INVALID_ARG, "ep_dispatch_layout: NULL output or workspace");
+    if (T > 0 && (!topk_idx || !slot_pos))
+        return fail(EP_ERR_INVALID_ARG, "ep_dispatch_layout: NULL topk_idx or slot_pos");
+    const size_t need = ep::layout_workspace_bytes(T * k, E);
+    if (workspace_bytes < need)
+        return fail(EP_ERR_INVALID_ARG, "ep_dispatch_layout: workspace of %zu bytes, need %zu",
+                    workspace_bytes, need);
+    ep::LayoutArgs a{};
+    a.topk_idx = topk_idx;
+    a.slots = T * k;
+    a.k = k;
+    a.E = E;
+    a.R = R;
+    a.nbits = E > 1 ? 32 - __builtin_clz((unsigned)(E - 1)) : 0;
+    a.expert_counts = expert_counts;
+    a.expert_offsets = expert_offsets;
+    a.rank_counts = rank_counts;
+    a.rank_offsets = rank_offsets;
+    a.slot_pos = slot_pos;
+    a.row_src = row_src;
+    a.status = reinterpret_cast<uint32_t *>(workspace);
+    a.tile_hist = ep::layout_tiles(a.slots) > 1
+                      ? reinterpret_cast<int32_t *>(static_cast<char *>(workspace) + ep::kWorkspaceHeader)
+                      : nullptr;
+    EP_HIP(ep::launch_layout(a, stream));
+    return EP_OK;
+}
+
+extern "C" ep_status ep_layout_status(const void *workspace, hipStream_t stream) {
+    if (!workspace)
+        return fail(EP_ERR_INVALID_ARG, "ep_layout_status: workspace is NULL");
+    EP_HIP(hipStreamSynchronize(stream));
+    uint32_t word = 0;
+    EP_HIP(hipMemcpy(&word, workspace, sizeof word, hipMemcpyDeviceToHost));
+    if (word == 0)
+        return EP_OK;
+    return fail(EP_ERR_BAD_ROUTING, "routing rejected:%s%s",
+                (word & ep::kRoutingIdOutOfRange) ? " expert id outside [0,E)" : "",
+                (word & ep::kRoutingDuplicate) ? " expert repeated within a token row" : "");
+}
+
+// ------------------------------------------------------------------------- staging
+
+namespace {
+
+void staging_release(ep_staging *s) {
+    for (int b = 0; b < kMaxBuffers; ++b) {
+        if (s->dev_send[b]) (void)hipFree(s->dev_send[b]);
+        if (s->dev_recv[b]) (void)hipFree(s->dev_recv[b]);
+        if (s->host_send[b]) (void)hipHostFree(s->host_send[b]);
+        if (s->host_recv[b]) (void)hipHostFree(s->host_recv[b]);
+        for (hipEvent_t e : {s->ev_up_in[b], s->ev_up_done[b], s->ev_down_in[b], s->ev_down_done[b]})
+            if (e) (void)hipEventDestroy(e);
+    }
+    for (hipEvent_t e : s->ev_chunk)
+        if (e) (void)hipEventDestroy(e);
+    if (s->flags) (void)hipHostFree(s->flags);
+    for (hipStream_t st : {s->up, s->down, s->sig})
+        if (st) (void)hipStreamDestroy(st);
+    delete s;
+}
+
+ep_status check_device(const ep_staging *s, const char *who) {
+    int dev = -1;
+    EP_HIP(hipGetDevice(&dev));
+    if (dev != s->device)
+        return fail(EP_ERR_INVALID_ARG, "%s: staging lives on device %d, current device is %d", who,
+                    s->device, dev);
+    return EP_OK;
+}
+
+}  // namespace
+
+extern "C" ep_status ep_staging_alloc(ep_staging_kind kind, int64_t max_rows, int32_t hidden,
+                                      int32_t num_ranks, int32_t num_buffers, int64_t chunk_bytes,
+                                      ep_staging **out) {
+    if (!out)
+        return fail(EP_ERR_INVALID_ARG, "ep_staging_alloc: out is NULL");
+    *out = nullptr;
+    if (kind != EP_STAGING_HBM && kind != EP_STAGING_PINNED_HOST)
+        return fail(EP_ERR_INVALID_ARG, "ep_staging_alloc: unknown kind %d", (int)kind);
+    if (max_rows < 1 || hidden < 8 || hidden % 8 != 0 || num_ranks < 1 || num_buffers < 1 ||
+        num_buffers > kMaxBuffers || chunk_bytes < 0)
+        return fail(EP_ERR_INVALID_ARG,
+                    "ep_staging_alloc: need max_rows >= 1, hidden a positive multiple of 8, "
+                    "num_ranks >= 1, 1 <= num_buffers <= %d, chunk_bytes >= 0",
+                    kMaxBuffers);
+    ep_staging *s = new ep_staging();
+    s->kind = kind;
+    s->max_rows = max_rows;
+    s->hidden = hidden;
+    s->num_ranks = num_ranks;
+    s->num_buffers = num_buffers;
+    s->row_bytes = (int64_t)hidden * 2;
+    s->buffer_bytes = max_rows * s->row_bytes;
+    int64_t chunk = chunk_bytes == 0 ? kDefaultChunk : chunk_bytes;
+    chunk = (chunk + 4095) / 4096 * 4096;
+    s->chunk_bytes = chunk;
+    s->max_chunks = (int32_t)std::max<int64_t>(1, (s->buffer_bytes + chunk - 1) / chunk);
+
+#define EP_ALLOC_HIP(call)                                                                          \
+    do {                                                                                            \
+        hipError_t e_ = (call);                                                                     \
+        if (e_ != hipSuccess) {                                                                     \
+            ep_status st_ = hip_fail(e_, #call);                                                    \
+            staging_release(s);                                                                     \
+            return st_;                                                                             \
+        }                                                                                           \
+    } while (0)
+
+    EP_ALLOC_HIP(hipGetDevice(&s->device));
+    int khz = 0;
+    EP_ALLOC_HIP(hipDeviceGetAttribute(&khz, hipDeviceAttributeWallClockRate, s->device));
+    if (khz > 0)
+        s->wall_clock_khz = khz;
+    for (int b = 0; b < num_buffers; ++b) {
+        EP_ALLOC_HIP(hipMalloc(&s->dev_send[b], (size_t)s->buffer_bytes));
+        EP_ALLOC_HIP(hipMalloc(&s->dev_recv[b], (size_t)s->buffer_bytes));
+    }
+    if (kind == EP_STAGING_PINNED_HOST) {
+        for (int b = 0; b < num_buffers; ++b) {
+            EP_ALLOC_HIP(hipHostMalloc(&s->host_send[b], (size_t)s->buffer_bytes, hipHostMallocDefault));
+            EP_ALLOC_HIP(hipHostMalloc(&s->host_recv[b], (size_t)s->buffer_bytes, hipHostMallocDefault));
+        }
+        s->flag_words = (size_t)num_buffers * (s->max_chunks + num_ranks) + 1;
+        EP_ALLOC_HIP(hipHostMalloc((void **)&s->flags, s->flag_words * sizeof(uint32_t),
+                                   hipHostMallocCoherent));
+        std::memset(s->flags, 0, s->flag_words * sizeof(uint32_t));
+        EP_ALLOC_HIP(hipStreamCreateWithFlags(&s->up, hipStreamNonBlocking));
+        EP_ALLOC_HIP(hipStreamCreateWithFlags(&s->down, hipStreamNonBlocking));
+        EP_ALLOC_HIP(hipStreamCreateWithFlags(&s->sig, hipStreamNonBlocking));
+        for (int b = 0; b < num_buffers; ++b) {
+            EP_ALLOC_HIP(hipEventCreateWithFlags(&s->ev_up_in[b], hipEventDisableTiming));
+            EP_ALLOC_HIP(hipEventCreateWithFlags(&s->ev_up_done[b], hipEventDisableTiming));
+            EP_ALLOC_HIP(hipEventCreateWithFlags(&s->ev_down_in[b], hipEventDisableTiming));
+            EP_ALLOC_HIP(hipEventCreateWithFlags(&s->ev_down_done[b], hipEventDisableTiming));
+        }
+        s->ev_chunk.assign((size_t)num_buffers * s->max_chunks, nullptr);
+        for (auto &e : s->ev_chunk)
+            EP_ALLOC_HIP(hipEventCreateWithFlags(&e, hipEventDisableTiming));
+    }
+#undef EP_ALLOC_HIP
+    *out = s;
+    return EP_OK;
+}
+
+extern "C" ep_status ep_staging_free(ep_staging *s) {
+    if (!s)
+        return EP_OK;
+    int prev = -1;
+    if (hipGetDevice(&prev) == hipSuccess && prev != s->device)
+        (void)hipSetDevice(s->device);
+    for (hipStream_t st : {s->up, s->down, s->sig})
+        if (st) (void)hipStreamSynchronize(st);
+    staging_release(s);
+    if (prev >= 0)
+        (void)hipSetDevice(prev);
+    return EP_OK;
+}
+
+extern "C" ep_status ep_staging_get(ep_staging *s, int32_t buf, ep_staging_view *v) {
+    if (!s || !v)
+        return fail(EP_ERR_INVALID_ARG, "ep_staging_get: NULL argument");
+    if (buf < 0 || buf >= s->num_buffers)
+        return fail(EP_ERR_INVALID_ARG, "ep_staging_get: buffer %d of %d", buf, s->num_buffers);
+    const bool pinned = s->kind == EP_STAGING_PINNED_HOST;
+    v->kind = s->kind;
+    v->num_ranks = s->num_ranks;
+    v->num_buffers = s->num_buffers;
+    v->hidden = s->hidden;
+    v->max_rows = s->max_rows;
+    v->row_bytes = s->row_bytes;
+    v->buffer_bytes = s->buffer_bytes;
+    v->chunk_bytes = s->chunk_bytes;
+    v->max_chunks = s->max_chunks;
+    v->dev_send = s->dev_send[buf];
+    v->dev_recv = s->dev_recv[buf];
+    v->host_send = pinned ? s->host_send[buf] : nullptr;
+    v->host_recv = pinned ? s->host_recv[buf] : nullptr;
+    v->send_flags = pinned ? s->send_flags(buf) : nullptr;
+    v->recv_flags = pinned ? s->recv_flags(buf) : nullptr;
+    return EP_OK;
+}
+
+extern "C" ep_status ep_staging_set_wait(ep_staging *s, int64_t timeout_us, int32_t sleep_units) {
+    if (!s || timeout_us < 0 || sleep_units < 0 || sleep_units > 1000)
+        return fail(EP_ERR_INVALID_ARG, "ep_staging_set_wait: need timeout_us >= 0, 0 <= sleep_units <= 1000");
+    s->timeout_us = timeout_us;
+    s->sleep_units = sleep_units;
+    return EP_OK;
+}
+
+extern "C" ep_status ep_staging_status(ep_staging *s, hipStream_t stream) {
+    if (!s)
+        return fail(EP_ERR_INVALID_ARG, "ep_staging_status: staging is NULL");
+    ep_status st = check_device(s, "ep_staging_status");
+    if (st != EP_OK)
+        return st;
+    EP_HIP(hipStreamSynchronize(stream));
+    for (hipStream_t side : {s->up, s->down, s->sig})
+        if (side) EP_HIP(hipStreamSynchronize(side));
+    if (!s->flags)
+        return EP_OK;
+    const uint32_t word = __atomic_exchange_n(s->status(), 0u, __ATOMIC_ACQ_REL);
+    if (word == EP_ERR_TIMEOUT)
+        return fail(EP_ERR_TIMEOUT, "a completion-flag wait expired after %lld us",
+                    (long long)s->timeout_us);
+    if (word != 0)
+        return fail(EP_ERR_HIP, "unexpected staging status word %u", word);
+    return EP_OK;
+}
+
+// --------------------------------------------------------------- dispatch / combine
+
+namespace {
+
+ep_status check_round(const ep_staging *s, const char *who, int64_t T, int32_t H, int32_t k,
+                      int32_t buf, const int32_t *slot_pos) {
+    if (!s)
+        return fail(EP_ERR_INVALID_ARG, "%s: staging is NULL", who);
+    if (T < 0 || k < 1 || H != s->hidden)
+        return fail(EP_ERR_INVALID_ARG, "%s: need T >= 0, k >= 1 and H == staging hidden (%d), got T=%lld k=%d H=%d",
+                    who, s->hidden, (long long)T, k, H);
+    if (T * (int64_t)k > s->max_rows)
+        return fail(EP_ERR_INVALID_ARG, "%s: T*k = %lld rows exceed the staging's %lld", who,
+                    (long long)(T * k), (long long)s->max_rows);
+    if (buf < 0 || buf >= s->num_buffers)
+        return fail(EP_ERR_INVALID_ARG, "%s: buffer %d of %d", who, buf, s->num_buffers);
+    if (T > 0 && !slot_pos)
+        return fail(EP_ERR_INVALID_ARG, "%s: slot_pos is NULL", who);
+    return check_device(s, who);
+}
+
+}  // namespace
+
+extern "C" ep_status ep_dispatch(const void *x_dev, int64_t num_tokens, int32_t hidden, int32_t topk,
+                                 const int32_t *slot_pos, ep_staging *s, int32_t buf, uint32_t epoch,
+                                 hipStream_t stream) {
+    ep_status st = check_round(s, "ep_dispatch", num_tokens, hidden, topk, buf, slot_pos);
+    if (st != EP_OK)
+        return st;
+    if (num_tokens > 0 && (!x_dev || !aligned16(x_dev)))
+        return fail(EP_ERR_INVALID_ARG, "ep_dispatch: x must be a non-NULL 16-byte aligned pointer");
+    const int64_t rows = num_tokens * topk;
+    EP_HIP(ep::launch_pack(x_dev, num_tokens, hidden, topk, slot_pos, s->dev_send[buf], s->max_rows, stream));
+    if (s->kind != EP_STAGING_PINNED_HOST || rows == 0)
+        return EP_OK;
+
+    // Host leg on the up stream, fixed-size chunks of the contiguous packed rows; after
+    // each chunk has landed, the sig stream raises that chunk's flag.  The copies never
+    // wait for a flag write.
+    const int64_t bytes = rows * s->row_bytes;
+    const int64_t chunks = (bytes + s->chunk_bytes - 1) / s->chunk_bytes;
+    char *dsrc = static_cast<char *>(s->dev_send[buf]);
+    char *hdst = static_cast<char *>(s->host_send[buf]);
+    EP_HIP(hipEventRecord(s->ev_up_in[buf], stream));
+    EP_HIP(hipStreamWaitEvent(s->up, s->ev_up_in[buf], 0));
+    ep::TraceSlot ts = ep::trace_acquire();
+    if (ts.start)
+        EP_HIP(hipEventRecord(ts.start, s->up));
+    for (int64_t c = 0; c < chunks; ++c) {
+        const int64_t off = c * s->chunk_bytes;
+        const int64_t len = std::min<int64_t>(s->chunk_bytes, bytes - off);
+        EP_HIP(hipMemcpyAsync(hdst + off, dsrc + off, (size_t)len, hipMemcpyDeviceToHost, s->up));
+        hipEvent_t ev = s->ev_chunk[(size_t)buf * s->max_chunks + c];
+        EP_HIP(hipEventRecord(ev, s->up));
+        EP_HIP(hipStreamWaitEvent(s->sig, ev, 0));
+        EP_HIP(ep::launch_write_flag(s->send_flags(buf) + c, epoch, s->sig));
+    }
+    if (ts.stop) {
+        EP_HIP(hipEventRecord(ts.stop, s->up));
+        ep::trace_submit("d2h", ts);
+    }
+    EP_HIP(hipEventRecord(s->ev_up_done[buf], s->sig));
+    EP_HIP(hipStreamWaitEvent(stream, s->ev_up_done[buf], 0));
+    return EP_OK;
+}
+
+extern "C" ep_status ep_combine(ep_staging *s, int32_t buf, uint32_t epoch, const int32_t *slot_pos,
+                                const float *topk_w, int64_t num_tokens, int32_t hidden, int32_t topk,
+                                void *out_dev, ep_out_dtype out_dtype, hipStream_t stream) {
+    ep_status st = check_round(s, "ep_combine", num_tokens, hidden, topk, buf, slot_pos);
+    if (st != EP_OK)
+        return st;
+    if (out_dtype != EP_OUT_BF16 && out_dtype != EP_OUT_F32)
+        return fail(EP_ERR_INVALID_ARG, "ep_combine: unknown out_dtype %d", (int)out_dtype);
+    if (num_tokens > 0 && (!topk_w || !out_dev || !aligned16(out_dev)))
+        return fail(EP_ERR_INVALID_ARG, "ep_combine: topk_w and a 16-byte aligned out are required");
+    const int64_t rows = num_tokens * topk;
+    if (rows == 0)
+        return EP_OK;
+    if (s->kind == EP_STAGING_PINNED_HOST) {
+        // Wait (bounded) for every sender's flag, then the host leg on the down stream.
+        const int64_t bytes = rows * s->row_bytes;
+        const int64_t chunks = (bytes + s->chunk_bytes - 1) / s->chunk_bytes;
+        char *hsrc = static_cast<char *>(s->host_recv[buf]);
+        char *ddst = static_cast<char *>(s->dev_recv[buf]);
+        const int64_t ticks = s->timeout_us * s->wall_clock_khz / 1000;
+        EP_HIP(hipEventRecord(s->ev_down_in[buf], stream));
+        EP_HIP(hipStreamWaitEvent(s->down, s->ev_down_in[buf], 0));
+        EP_HIP(ep::launch_wait_flags(s->recv_flags(buf), s->num_ranks, epoch, ticks, s->sleep_units,
+                                     s->status(), s->down));
+        ep::TraceSlot ts = ep::trace_acquire();
+        if (ts.start)
+            EP_HIP(hipEventRecord(ts.start, s->down));
+        for (int64_t c = 0; c < chunks; ++c) {
+            const int64_t off = c * s->chunk_bytes;
+            const int64_t len = std::min<int64_t>(s->chunk_bytes, bytes - off);
+            EP_HIP(hipMemcpyAsync(ddst + off, hsrc + off, (size_t)len, hipMemcpyHostToDevice, s->down));
+        }
+        if (ts.stop) {
+            EP_HIP(hipEventRecord(ts.stop, s->down));
+            ep::trace_submit("h2d", ts);
+        }
+        EP_HIP(hipEventRecord(s->ev_down_done[buf], s->down));
+        EP_HIP(hipStreamWaitEvent(stream, s->ev_down_done[buf], 0));
+    }
+    EP_HIP(ep::launch_combine(s->dev_recv[buf], slot_pos, topk_w, num_tokens, hidden, topk, out_dev,
+                              out_dtype == EP_OUT_F32, s->max_rows, stream));
+    return EP_OK;
+}
+
+// ---------------------------------------------------------------------- measurement
+
+extern "C" ep_status ep_trace_enable(int32_t on) {
+    ep::g_trace_on.store(on != 0);
+    return EP_OK;
+}
+
+extern "C" ep_status ep_trace_read(ep_trace_stat *stats, int32_t capacity, int32_t *count) {
+    if (!count || capacity < 0 || (capacity > 0 && !stats))
+        return fail(EP_ERR_INVALID_ARG, "ep_trace_read: bad arguments");
+    std::lock_guard<std::mutex> lk(ep::g_trace_mu);
+    for (auto &p : ep::g_pending) {
+        float ms = 0.f;
+        EP_HIP(hipEventSynchronize(p.stop));
+        EP_HIP(hipEventElapsedTime(&ms, p.start, p.stop));
+        ep::Stat &s = ep::g_stats[p.name];
+        s.count += 1;
+        s.total += ms;
+        s.mn = std::min<double>(s.mn, ms);
+        s.mx = std::max<double>(s.mx, ms);
+        ep::g_event_pool.push_back(p.start);
+        ep::g_event_pool.push_back(p.stop);
+    }
+    ep::g_pending.clear();
+    int32_t n = 0;
+    for (auto &kv : ep::g_stats) {
+        if (n < capacity) {
+            ep_trace_stat &o = stats[n];
+            std::memset(&o, 0, sizeof o);
+            std::snprintf(o.name, sizeof o.name, "%s", kv.first.c_str());
+            o.count = kv.second.count;
+            o.total_ms = kv.second.total;
+            o.min_ms = kv.second.count ? kv.second.mn : 0.0;
+            o.max_ms = kv.second.mx;
+        }
+        ++n;
+    }
+    *count = std::min(n, capacity);
+    return EP_OK;
+}
+
+extern "C" ep_status ep_trace_reset(void) {
+    std::lock_guard<std::mutex> lk(ep::g_trace_mu);
+    for (auto &p : ep::g_pending) {
+        (void)hipEventSynchronize(p.stop);
+        ep::g_event_pool.push_back(p.start);
+        ep::g_event_pool.push_back(p.stop);
+    }
+    ep::g_pending.clear();
+    ep::g_stats.clear();
+    return EP_OK;
+}
+
+extern "C" ep_status ep_copy_probe(void *dst_dev, const void *src_dev, size_t bytes, hipStream_t stream) {
+    if (bytes % 16 != 0 || (bytes && (!dst_dev || !src_dev || !aligned16(dst_dev) || !aligned16(src_dev))))
+        return fail(EP_ERR_INVALID_ARG, "ep_copy_probe: 16-byte aligned pointers and a multiple of 16 bytes");
+    EP_HIP(ep::launch_copy(dst_dev, src_dev, bytes, stream));
+    return EP_OK;
+}
+
+extern "C" ep_status ep_memcpy(void *dst, const void *src, size_t bytes, hipStream_t stream) {
+    if (bytes && (!dst || !src))
+        return fail(EP_ERR_INVALID_ARG, "ep_memcpy: NULL pointer");
+    if (bytes)
+        EP_HIP(hipMemcpyAsync(dst, src, bytes, hipMemcpyDefault, stream));
+    return EP_OK;
+}

@@ -1,0 +1,69 @@
+// signal.hip -- completion flags in pinned host memory (Sec. 4.4 of the paper).
+//
+// The payload stays contiguous and the flags live apart from it, one 32-bit word per
+// sender (receive side) or per DMA chunk (send side), each with a single writer, so no
+// atomic read-modify-write is needed.  A flag holds the epoch of the round that filled
+// its data; a reader accepts it when (int32)(flag - epoch) >= 0, so a flag left over from
+// an earlier round is never taken for the current one.
+//
+// wait_flags_kernel: one lane per remote sender polls its flag with system-scope loads
+// (they bypass the GPU caches and cross PCIe) and sleeps between polls, instead of a
+// large thread block spinning.  The wait is bounded by the constant-rate wall clock; on
+// expiry the kernel records a timeout in the host status word and exits, so the stream
+// never hangs on a flag that does not come.
+#include "ep_internal.h"
+
+namespace ep {
+namespace {
+
+constexpr uint32_t kStatusTimeout = 5u;  // EP_ERR_TIMEOUT
+
+__global__ __launch_bounds__(64) void wait_flags_kernel(const uint32_t *flags, int32_t n,
+                                                        uint32_t epoch, int64_t timeout_ticks,
+                                                        int32_t sleep_units, uint32_t *status) {
+    const int32_t i = blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= n)
+        return;
+    const int64_t t0 = wall_clock64();
+    for (;;) {
+        const uint32_t f = __hip_atomic_load(flags + i, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_SYSTEM);
+        if ((int32_t)(f - epoch) >= 0)
+            break;
+        if (wall_clock64() - t0 > timeout_ticks) {
+            __hip_atomic_store(status, kStatusTimeout, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+            break;
+        }
+        for (int32_t s = 0; s < sleep_units; ++s)
+            __builtin_amdgcn_s_sleep(1);
+    }
+}
+
+__global__ __launch_bounds__(64) void write_flag_kernel(uint32_t *flag, uint32_t epoch) {
+    if (threadIdx.x == 0)
+        __hip_atomic_store(flag, epoch, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_SYSTEM);
+}
+
+}  // namespace
+
+hipError_t launch_wait_flags(const uint32_t *flags, int32_t n, uint32_t epoch,
+                             int64_t timeout_ticks, int32_t sleep_units, uint32_t *status,
+                             hipStream_t stream) {
+    if (n <= 0)
+        return hipSuccess;
+    (void)hipGetLastError();  // drop an error left by an earlier, already reported call
+    TraceSlot ts = trace_acquire();
+    hipExtLaunchKernelGGL(wait_flags_kernel, dim3((unsigned)((n + 63) / 64)), dim3(64), 0, stream,
+                          ts.start, ts.stop, 0, flags, n, epoch, timeout_ticks, sleep_units, status);
+    hipError_t err = hipGetLastError();
+    if (err == hipSuccess)
+        trace_submit("wait_flags", ts);
+    return err;
+}
+
+hipError_t launch_write_flag(uint32_t *flag, uint32_t epoch, hipStream_t stream) {
+    (void)hipGetLastError();
+    hipLaunchKernelGGL(write_flag_kernel, dim3(1), dim3(64), 0, stream, flag, epoch);
+    return hipGetLastError();
+}
+
+}  // namespace ep

@@ -1,0 +1,161 @@
+"""HIP path vs. CPU oracle, element by element, on the same seeded inputs.
+
+Layout (counts, offsets, slot positions, inverse) and packed rows must match bit for
+bit.  The bf16 combine must be within max abs 2e-2 and mean abs 2e-3 of the oracle's
+exact (fp64) sums; element by element, the fp32 output must lie within k fp32
+roundings of the exact sum and the bf16 output within that plus one bf16 rounding, and
+at least 99% of bf16 outputs must equal the oracle's own rounding of the exact sum.
+Cases span several layout tiles (4096 routing entries each) with ragged tails, ragged
+column chunks, the four smaller workloads at full size, and degenerate routings.
+"""
+import numpy as np
+import pytest
+import torch
+
+import paper_2609_40093_amd as ep
+from paper_2609_40093_amd.synth import bf16_bits_to_f32
+from gpu_cases import (TOL_MAX_ABS, TOL_MEAN_ABS, bf16_ulp_distance, combine_errors, from_config,
+                       make_case, oracle_reference, say)
+
+pytestmark = pytest.mark.gpu
+
+DEV = "cuda"
+
+
+def synth_f32(bits: np.ndarray) -> np.ndarray:
+    return bf16_bits_to_f32(bits).astype(np.float64)
+
+
+def dev_bits(a: np.ndarray) -> torch.Tensor:
+    return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).to(DEV)
+
+
+def host_bits(t: torch.Tensor) -> np.ndarray:
+    return t.cpu().numpy().view(np.uint16)
+
+
+def run_hip(case, out_f32=False):
+    """layout -> dispatch -> combine through libep with HBM staging."""
+    idx = torch.from_numpy(case.topk_idx).to(DEV)
+    lay = ep.dispatch_layout(idx, case.E, case.R)
+    ep.layout_status(lay)
+    st = ep.Staging("hbm", max(1, case.slots), case.H, case.R, num_buffers=1)
+    ep.dispatch(dev_bits(case.x), lay.slot_pos, st, topk=case.k)
+    packed = host_bits(st.read_device("send", case.slots))
+    st.write_device("recv", dev_bits(case.y))
+    w = torch.from_numpy(case.topk_w).to(DEV)
+    out = ep.combine(st, lay.slot_pos, w, out_dtype=torch.float32 if out_f32 else torch.bfloat16)
+    torch.cuda.synchronize()
+    res = dict(expert_counts=lay.expert_counts.cpu().numpy(), expert_offsets=lay.expert_offsets.cpu().numpy(),
+               rank_counts=lay.rank_counts.cpu().numpy(), rank_offsets=lay.rank_offsets.cpu().numpy(),
+               slot_pos=lay.slot_pos.cpu().numpy(), row_src=lay.row_src.cpu().numpy(), packed=packed,
+               out=out.cpu().numpy() if out_f32 else host_bits(out.view(torch.int16)))
+    st.close()
+    return res
+
+
+def check_case(case):
+    say(f"{case.name}: T={case.T} H={case.H} E={case.E} k={case.k} R={case.R}")
+    lay, packed, exact, b16, f32 = oracle_reference(case)
+    got = run_hip(case)
+    for key in ("expert_counts", "expert_offsets", "rank_counts", "rank_offsets", "slot_pos", "row_src"):
+        want = getattr(lay, key)
+        assert np.array_equal(got[key], want), f"{key} differs at {np.nonzero(got[key] != want)[0][:8]}"
+    assert got["packed"].tobytes() == packed.tobytes(), "packed rows differ"
+    mx, mean = combine_errors(got["out"], exact)
+    assert mx <= TOL_MAX_ABS and mean <= TOL_MEAN_ABS, f"combine error max {mx} mean {mean}"
+    got32 = run_hip(case, out_f32=True)["out"].astype(np.float64)
+    if case.T:
+        # error bound of k fused multiply-adds in fp32 (each rounding <= 2^-24 of a partial
+        # sum, itself <= sum_j |w_j y_j|) followed by one round to nearest bf16 (<= 2^-8 relative)
+        absum = np.zeros_like(exact)
+        yv = (case.y.astype(np.uint32) << 16).view(np.float32).astype(np.float64)
+        for j in range(case.k):
+            absum += np.abs(case.topk_w[:, j:j + 1].astype(np.float64) * yv[lay.slot_pos[j::case.k]])
+        f32_err = case.k * 2.0 ** -24 * absum
+        assert np.all(np.abs(got32 - exact) <= f32_err + 1e-38), "fp32 combine outside k roundings"
+        got16 = synth_f32(got["out"])
+        bound16 = f32_err * (1 + 2.0 ** -8) + 2.0 ** -8 * np.abs(exact) + 1e-38
+        assert np.all(np.abs(got16 - exact) <= bound16), "bf16 combine outside fp32-then-round bound"
+        same = float((bf16_ulp_distance(got["out"], b16) == 0).mean())
+        assert same >= 0.99, f"only {same:.4f} of outputs equal the oracle's rounding"
+
+
+CASES = [
+    # name, T, H, E, k, R, routing
+    ("tiles3_ragged", 1500, 2056, 64, 8, 8, "random"),      # 12000 entries: 2 full tiles + tail; ragged chunk
+    ("tile_exact", 2048, 256, 32, 2, 4, "random"),          # exactly one tile
+    ("tile_plus_one", 4097, 64, 16, 1, 2, "random"),        # one tile + one entry
+    ("many_tiles_small_rows", 20000, 8, 256, 8, 8, "skewed"),  # 40 tiles, H = 8 (one vector)
+    ("max_experts", 3000, 128, 2048, 4, 8, "random"),       # E at the kernel limit
+    ("one_expert", 333, 512, 1, 1, 1, "random"),
+    ("k_equals_E", 100, 1024, 6, 6, 3, "random"),
+    ("odd_E", 999, 136, 96, 5, 8, "random"),
+    ("firstk_empty_experts", 5000, 256, 128, 8, 8, "firstk"),
+    ("lastk_reversed", 700, 256, 64, 4, 4, "lastk"),
+    ("roundrobin", 4096, 128, 256, 8, 8, "roundrobin"),
+    ("single_token", 1, 7168, 256, 8, 8, "random"),
+]
+
+
+@pytest.mark.parametrize("spec", CASES, ids=[c[0] for c in CASES])
+def test_parity_shapes(spec):
+    name, T, H, E, k, R, kind = spec
+    check_case(make_case(name, T, H, E, k, R, kind, seed=len(name)))
+
+
+@pytest.mark.parametrize("name", ["tiny", "coarse", "fine", "decode"])
+def test_parity_workloads(name):
+    check_case(from_config(name))
+
+
+def test_empty_batch():
+    case = make_case("empty", 0, 64, 8, 2, 4, "random")
+    say("empty batch")
+    idx = torch.zeros((0, 2), dtype=torch.int32, device=DEV)
+    lay = ep.dispatch_layout(idx, 8, 4)
+    ep.layout_status(lay)
+    assert lay.expert_counts.cpu().tolist() == [0] * 8
+    assert lay.expert_offsets.cpu().tolist() == [0] * 9
+    assert lay.rank_offsets.cpu().tolist() == [0] * 5
+    st = ep.Staging("hbm", 1, 64, 4, num_buffers=1)
+    ep.dispatch(torch.zeros((0, 64), dtype=torch.int16, device=DEV), lay.slot_pos, st, topk=2)
+    out = ep.combine(st, lay.slot_pos, torch.zeros((0, 2), dtype=torch.float32, device=DEV))
+    torch.cuda.synchronize()
+    assert out.shape == (0, 64)
+    st.close()
+    del case
+
+
+def test_layout_deterministic():
+    """Positions never depend on scheduling: 20 runs give identical bytes."""
+    case = make_case("det", 30000, 8, 256, 8, 8, "skewed", seed=3)
+    say("determinism x20")
+    idx = torch.from_numpy(case.topk_idx).to(DEV)
+    first = None
+    for _ in range(20):
+        lay = ep.dispatch_layout(idx, case.E, case.R)
+        cur = torch.cat([lay.slot_pos, lay.row_src, lay.expert_offsets]).cpu().numpy()
+        if first is None:
+            first = cur
+        assert np.array_equal(cur, first)
+
+
+def test_identity_roundtrip_exact():
+    """combine(dispatch(x)) with identity experts and dyadic gates returns x exactly
+    (fp32 and bf16 outputs); with the workload's softmax gates within 1e-2 relative."""
+    case = make_case("identity", 3000, 1024, 64, 4, 8, "random", seed=5, gates="uniform")
+    say("identity round trip")
+    idx = torch.from_numpy(case.topk_idx).to(DEV)
+    lay = ep.dispatch_layout(idx, case.E, case.R)
+    st = ep.Staging("hbm", case.slots, case.H, case.R, num_buffers=1)
+    x = dev_bits(case.x)
+    ep.dispatch(x, lay.slot_pos, st, topk=case.k)
+    st.write_device("recv", st.read_device("send", case.slots))   # every expert is the identity
+    w = torch.from_numpy(case.topk_w).to(DEV)
+    out32 = ep.combine(st, lay.slot_pos, w, out_dtype=torch.float32)
+    out16 = ep.combine(st, lay.slot_pos, w)
+    xf = torch.from_numpy(case.x.view(np.int16)).view(torch.bfloat16).float()
+    assert torch.equal(out32.cpu(), xf)
+    assert torch.equal(out16.view(torch.int16).cpu(), torch.from_numpy(case.x.view(np.int16)))
+    st.close()
