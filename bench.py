@@ -1,0 +1,365 @@
+"""Benchmark of one rank's MoE dispatch + combine on one MI355X.
+
+A step is one MoE layer's communication share: dispatch layout, pack, and the
+gate-weighted combine of the returned rows (the peers' expert outputs are seeded data
+already in the receive buffer).  `value` is token payload throughput with HBM staging:
+(dispatch payload + combine payload) / layer time, each payload T*k*2H bytes.  The same
+layer with pinned host staging (SDMA legs, host flags, simulated peers) is timed after
+it and reported under "pinned_staging"; that rate includes PCIe and is never `value`.
+
+Inputs and staging are rotated over enough buffer sets that each step's working set
+has left the 256 MB Infinity Cache before it is used again.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "dispatch & combine GB/s token payload (μs/MoE layer) + % HBM/PCIe roofline, 1 GPU"
+HBM_PEAK_GBPS = 8000.0      # MI355X HBM3E
+PCIE_PEAK_GBPS = 64.0       # PCIe Gen5 x16, per direction
+MALL_BYTES = 256 << 20
+
+
+def parse():
+    p = argparse.ArgumentParser()
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=50)
+    p.add_argument("--warmup", type=int, default=10)
+    p.add_argument("--workload", default="coarse", help="synth config name (default: the coarse-expert layer)")
+    p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--no-pinned", action="store_true")
+    p.add_argument("--cpu-seconds", type=float, default=10.0)
+    return p.parse_args()
+
+
+def algorithmic_bytes(cfg) -> dict:
+    """Bytes each kernel must move per launch (reads + writes), per the path's definition."""
+    T, H, k = cfg.T, cfg.H, cfg.k
+    n = T * k
+    row = 2 * H
+    return {
+        "pack": T * row + n * row + 4 * n,                  # read x once, write k copies, read slot_pos
+        "combine": n * row + 8 * n + T * row,               # read k rows, gates and slot_pos, write out
+        "layout_rank": 4 * n + 4 * n + 4 * n,               # read ids, write slot_pos and row_src
+        "layout_histogram": 4 * n,
+    }
+
+
+def source_hash(name: str) -> str:
+    path = os.path.join(ROOT, "paper_2609_40093_amd", "csrc", name)
+    return hashlib.sha256(open(path, "rb").read()).hexdigest()[:16]
+
+
+def committed_traffic(workload: str, kernel: str):
+    """HBM bytes per launch from the committed rocprofv3 counter summary, if it was taken
+    on the kernel source as it is now (else None)."""
+    path = os.path.join(ROOT, "profiles", f"traffic_{kernel}_{workload}.json")
+    if not os.path.exists(path):
+        return None
+    d = json.load(open(path))
+    if d.get("source_sha256") != source_hash(f"{kernel}.hip"):
+        return None
+    return d.get("traffic_bytes_per_launch")
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(json.dumps({"error": "this benchmark runs on exactly one GPU: the path is one rank's share "
+                                   "of an expert-parallel group, simulated on a single MI355X; "
+                                   f"--gpus {args.gpus} is not supported"}))
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    import paper_2609_40093_amd as ep
+    from paper_2609_40093_amd import _lib, synth
+
+    _lib.load()                                        # fails loudly if libep.so is missing
+    torch.cuda.set_device(0)
+    dev = torch.device("cuda", 0)
+    cfg = synth.config(args.workload)
+    inp = synth.make_inputs(cfg)
+    y = inp.expert_outputs()
+    T, H, E, k, R = cfg.T, cfg.H, cfg.E, cfg.k, cfg.R
+    n = cfg.slots
+    payload = cfg.payload_bytes
+    step_bytes = 2 * payload + T * 2 * H * 2   # x, packed, recv, out per set (for rotation sizing)
+    nsets = max(2, min(8, -(-3 * MALL_BYTES // step_bytes) + 1))
+    stream = torch.cuda.current_stream()
+
+    x_d = torch.from_numpy(inp.x.view(np.int16)).to(dev)
+    idx_d = torch.from_numpy(inp.topk_idx).to(dev)
+    w_d = torch.from_numpy(inp.topk_w).to(dev)
+    y_d = torch.from_numpy(y.view(np.int16)).to(dev)
+    sets = []
+    for s in range(nsets):
+        sets.append(dict(x=x_d.clone(), idx=idx_d.clone(), w=w_d.clone(),
+                         out=torch.empty((T, H), dtype=torch.bfloat16, device=dev), lay=None))
+    staging = ep.Staging("hbm", n, H, R, num_buffers=nsets)
+    for s in range(nsets):
+        staging.write_device("recv", y_d, buf=s)
+    torch.cuda.synchronize()
+
+    def step(i, trace=None):
+        """One layer; `trace` names the one kernel ("pack" or "combine") whose launch is
+        bracketed by timing events, so that measuring costs the host almost nothing."""
+        st = sets[i % nsets]
+        st["lay"] = ep.dispatch_layout(st["idx"], E, R, out=st["lay"])
+        if trace == "pack":
+            ep.trace_enable(True)
+        ep.dispatch(st["x"], st["lay"].slot_pos, staging, topk=k, buf=i % nsets, epoch=i + 1)
+        if trace == "pack":
+            ep.trace_enable(False)
+        elif trace == "combine":
+            ep.trace_enable(True)
+        ep.combine(staging, st["lay"].slot_pos, st["w"], out=st["out"], buf=i % nsets, epoch=i + 1)
+        if trace == "combine":
+            ep.trace_enable(False)
+
+    # ---- HBM staging: warmup, then exactly K timed steps; pack and combine are timed
+    #      live on alternate steps with HIP events on the stream they run on
+    for i in range(args.warmup):
+        step(i)
+    ep.layout_status(sets[0]["lay"])
+    torch.cuda.synchronize()
+    ep.trace_reset()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        step(args.warmup + i, trace="pack" if i % 2 == 0 else "combine")
+    t_issue = time.perf_counter()
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    kstats = ep.trace_read()
+    ms_per_step = (t1 - t0) * 1e3 / args.steps
+    value = 2 * payload / (ms_per_step * 1e-3) / 1e9
+    issue_us = (t_issue - t0) * 1e6 / args.steps
+    # breakdown pass (not timed): every kernel of every step bracketed by events
+    ep.trace_reset()
+    ep.trace_enable(True)
+    for i in range(args.steps):
+        step(args.warmup + args.steps + i)
+    torch.cuda.synchronize()
+    ep.trace_enable(False)
+    breakdown = ep.trace_read()
+    for name, st_ in breakdown.items():
+        if name not in kstats:
+            kstats[name] = st_
+
+    abytes = algorithmic_bytes(cfg)
+    kernels = {}
+    for name, st in kstats.items():
+        us = st["mean_ms"] * 1e3
+        entry = {"launches": st["count"], "avg_us": round(us, 3),
+                 "measured": "timed region" if name in ("pack", "combine") else "breakdown pass"}
+        if name in abytes and us > 0:
+            entry["algorithmic_bytes"] = abytes[name]
+            entry["GBps"] = round(abytes[name] / (us * 1e-6) / 1e9, 1)
+            entry["hbm_frac"] = round(entry["GBps"] / HBM_PEAK_GBPS, 4)
+        kernels[name] = entry
+    dominant = max(("pack", "combine"), key=lambda nm: kernels.get(nm, {}).get("avg_us", 0.0))
+    dk = kernels[dominant]
+    traffic = committed_traffic(args.workload, dominant)
+
+    # ---- attainable HBM bandwidth: plain streaming copy of 1 GiB
+    a = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
+    b = torch.empty_like(a)
+    for _ in range(2):
+        ep.copy_probe(b, a)
+    torch.cuda.synchronize()
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    ev0.record()
+    for _ in range(5):
+        ep.copy_probe(b, a)
+    ev1.record()
+    torch.cuda.synchronize()
+    copy_gbps = 2 * (1 << 30) * 5 / (ev0.elapsed_time(ev1) * 1e-3) / 1e9
+    del a, b
+
+    result = {
+        "metric": METRIC,
+        "value": round(value, 2),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {
+            "workload": f"{cfg.name} MoE layer: T={T} tokens, H={H}, E={E} experts, top-{k}, "
+                        f"R={R}-rank EP group (rank 0 on one GPU), HBM staging",
+            "T": T, "H": H, "E": E, "k": k, "R": R, "staging": "hbm",
+            "payload_bytes_per_op": payload, "us_per_layer": round(ms_per_step * 1e3, 2),
+            "buffer_sets_rotated": nsets, "parallelism": "1 GPU (one EP rank)",
+            "host_issue_us_per_step": round(issue_us, 1),
+        },
+        "roofline": {
+            "bound": "hbm",
+            "kernel": dominant,
+            "achieved": dk.get("GBps"),
+            "peak": HBM_PEAK_GBPS,
+            "unit": "GB/s",
+            "frac": dk.get("hbm_frac"),
+            "traffic": traffic,
+            "algorithmic_bytes_per_launch": dk.get("algorithmic_bytes"),
+            "avg_launch_us": dk.get("avg_us"),
+        },
+        "kernels": kernels,
+        "hbm_copy_probe_GBps": round(copy_gbps, 1),
+    }
+
+    # ---- pinned host staging: the same layer with SDMA legs, host flags, simulated peers
+    if not args.no_pinned:
+        result["pinned_staging"] = bench_pinned(cfg, inp, y, args, dev)
+
+    # ---- CPU baseline: the oracle, single-threaded, on whole layers of the same workload
+    if not args.no_cpu_baseline:
+        result["cpu_baseline"] = cpu_baseline(cfg, inp, y, args.cpu_seconds)
+
+    print(json.dumps(result))
+
+
+def bench_pinned(cfg, inp, y, args, dev) -> dict:
+    import numpy as np
+    import torch
+
+    import paper_2609_40093_amd as ep
+
+    T, H, E, k, R = cfg.T, cfg.H, cfg.E, cfg.k, cfg.R
+    n = cfg.slots
+    nbuf = 2
+    st = ep.Staging("pinned", n, H, R, num_buffers=nbuf)
+    for b in range(nbuf):
+        st.host_array("recv", b)[:n] = y
+    peers = ep.SimPeers(st, echo=False)
+    x = torch.from_numpy(inp.x.view(np.int16)).to(dev)
+    idx = torch.from_numpy(inp.topk_idx).to(dev)
+    w = torch.from_numpy(inp.topk_w).to(dev)
+    out = torch.empty((T, H), dtype=torch.bfloat16, device=dev)
+    lay = ep.dispatch_layout(idx, E, R)
+
+    def step(i):
+        buf, epoch = i % nbuf, i + 1
+        ep.dispatch_layout(idx, E, R, out=lay)
+        ep.dispatch(x, lay.slot_pos, st, topk=k, buf=buf, epoch=epoch)
+        peers.post(buf, epoch, n)
+        ep.combine(st, lay.slot_pos, w, out=out, buf=buf, epoch=epoch)
+
+    steps = max(5, args.steps // 2)
+    for i in range(args.warmup):
+        step(i)
+    st.status()
+    peers.drain()
+    ep.trace_reset()
+    ep.trace_enable(True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(steps):
+        step(args.warmup + i)
+    st.status()
+    t1 = time.perf_counter()
+    peers.drain()
+    ep.trace_enable(False)
+    ks = ep.trace_read()
+    ms = (t1 - t0) * 1e3 / steps
+    legs = {}
+    for name in ("d2h_leg", "h2d_leg", "wait_d2h", "wait_recv", "release_signal", "pack", "combine",
+                 "layout_rank", "layout_histogram"):
+        if name in ks:
+            legs[name] = {"avg_us": round(ks[name]["mean_ms"] * 1e3, 2)}
+    pcie_bytes = n * 2 * H
+    for name in ("d2h_leg", "h2d_leg"):
+        if name in legs and legs[name]["avg_us"] > 0:
+            legs[name]["GBps"] = round(pcie_bytes / (legs[name]["avg_us"] * 1e-6) / 1e9, 2)
+    peers.close()
+    st.close()
+    peaks = pcie_peaks(dev)
+    res = {
+        "us_per_layer": round(ms * 1e3, 1),
+        "payload_GBps": round(2 * cfg.payload_bytes / (ms * 1e-3) / 1e9, 2),
+        "steps": steps,
+        "legs": legs,
+        "pcie_bytes_per_leg": pcie_bytes,
+        "pcie_measured_peak_GBps": peaks,
+        "pcie_published_peak_GBps": PCIE_PEAK_GBPS,
+    }
+    for name, key in (("d2h_leg", "d2h_alone"), ("h2d_leg", "h2d_alone")):
+        if "GBps" in legs.get(name, {}) and peaks.get(key):
+            legs[name]["frac_of_measured_peak"] = round(legs[name]["GBps"] / peaks[key], 3)
+    return res
+
+
+def pcie_peaks(dev) -> dict:
+    """hipMemcpyAsync of 1 GiB between pinned host memory and HBM: each direction alone
+    and both together on two streams."""
+    import torch
+    nbytes = 1 << 30
+    h1 = torch.empty(nbytes, dtype=torch.uint8, pin_memory=True)
+    h2 = torch.empty(nbytes, dtype=torch.uint8, pin_memory=True)
+    d1 = torch.empty(nbytes, dtype=torch.uint8, device=dev)
+    d2 = torch.empty(nbytes, dtype=torch.uint8, device=dev)
+    s1, s2 = torch.cuda.Stream(), torch.cuda.Stream()
+
+    def timed(fn, reps=3):
+        fn()
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(reps):
+            fn()
+        torch.cuda.synchronize()
+        return (time.perf_counter() - t0) / reps
+
+    def d2h():
+        with torch.cuda.stream(s1):
+            h1.copy_(d1, non_blocking=True)
+
+    def h2d():
+        with torch.cuda.stream(s2):
+            d2.copy_(h2, non_blocking=True)
+
+    def both():
+        d2h()
+        h2d()
+
+    t_d2h, t_h2d, t_both = timed(d2h), timed(h2d), timed(both)
+    return {"d2h_alone": round(nbytes / t_d2h / 1e9, 2), "h2d_alone": round(nbytes / t_h2d / 1e9, 2),
+            "bidirectional_total": round(2 * nbytes / t_both / 1e9, 2)}
+
+
+def cpu_baseline(cfg, inp, y, seconds: float) -> dict:
+    """The oracle as it stands (plain C, one thread) over whole layers of the workload."""
+    import oracle
+    oracle.load()
+    passes, t0 = 0, time.perf_counter()
+    while True:
+        lay = oracle.layout(inp.topk_idx, cfg.E, cfg.R)
+        oracle.pack(inp.x, lay.slot_pos, cfg.k)
+        oracle.combine(y, lay.slot_pos, inp.topk_w)
+        passes += 1
+        el = time.perf_counter() - t0
+        if el >= seconds:
+            break
+    return {"value": round(2 * cfg.payload_bytes * passes / el / 1e9, 4), "unit": "GB/s", "cores": 1,
+            "kind": "oracle",
+            "sample": f"{passes} whole {cfg.name} layers (layout + pack + combine with fp64 sums), "
+                      f"{el:.1f} s on one host thread",
+            "us_per_layer": round(el / passes * 1e6, 1)}
+
+
+if __name__ == "__main__":
+    main()

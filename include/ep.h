@@ -122,12 +122,12 @@ ep_status ep_layout_status(const void *workspace, hipStream_t stream);
  *   max_rows     rows per buffer (>= T*k of every later call), hidden = H (multiple of 8).
  *   num_ranks    R: number of senders whose completion flags ep_combine waits for.
  *   num_buffers  1..8 independent buffer sets (alternate them between rounds).
- *   chunk_bytes  size of one host-leg DMA chunk (0 = 8 MiB); rounded up to 4 KiB.
+ *   chunk_bytes  size of one device->host DMA chunk (0 = 64 MiB); rounded up to 4 KiB.
  * Per buffer: HBM send (packed) and recv (returned rows) buffers of max_rows*H*2 bytes;
  * with PINNED_HOST also pinned host send/recv bounce buffers of the same size, one
  * uint32 send flag per chunk and one uint32 recv flag per sender in coherent pinned host
- * memory, all zero-initialised.  Creates two non-blocking DMA streams (up = D2H,
- * down = H2D) and one signalling stream, all at default priority. */
+ * memory, all zero-initialised.  Creates two non-blocking DMA streams at default
+ * priority: up (device->host) and down (host->device). */
 ep_status ep_staging_alloc(ep_staging_kind kind, int64_t max_rows, int32_t hidden,
                            int32_t num_ranks, int32_t num_buffers, int64_t chunk_bytes,
                            ep_staging **out);
@@ -160,9 +160,10 @@ ep_status ep_staging_status(ep_staging *s, hipStream_t stream);
  *   packed[slot_pos[t*k+j]][:] = x[t][:] for every token t and slot j   (bf16 byte copy)
  * into the staging's HBM send buffer.  x_dev: bf16 [T][H]; slot_pos: int32 [T*k] from
  * ep_dispatch_layout; rows with slot_pos outside [0, max_rows) are skipped.
- * With PINNED_HOST, the first T*k rows then go device->host on the up stream in
- * chunk_bytes pieces, and after chunk c has landed send_flags[c] is set to `epoch`.
- * `stream` waits for the whole leg before later work.  Epochs should increase per
+ * With PINNED_HOST, the first T*k rows then go device->host on an SDMA engine in
+ * chunk_bytes pieces, and after chunk c has landed send_flags[c] is set to `epoch`
+ * (a 4-byte DMA copy queued behind the chunk).  `stream` waits (bounded) for the last
+ * flag before later work.  Epochs should increase per
  * round (flags compare as signed 32-bit differences). */
 ep_status ep_dispatch(const void *x_dev, int64_t num_tokens, int32_t hidden, int32_t topk,
                       const int32_t *slot_pos, ep_staging *s, int32_t buf, uint32_t epoch,
@@ -174,7 +175,7 @@ ep_status ep_dispatch(const void *x_dev, int64_t num_tokens, int32_t hidden, int
  * to nearest-even bf16 (EP_OUT_BF16) or stored as fp32 (EP_OUT_F32).  recv holds the
  * returned rows in the packed layout.  With PINNED_HOST, first waits (bounded, see
  * ep_staging_set_wait) until recv_flags[r] has reached `epoch` for every sender r, then
- * moves the first T*k rows host->device on the down stream in chunk_bytes pieces.
+ * moves the first T*k rows host->device (one DMA copy, ordered on `stream`).
  * topk_w: float [T][k]; out: [T][H] of out_dtype.  Slots whose slot_pos is outside
  * [0, max_rows) contribute nothing. */
 ep_status ep_combine(ep_staging *s, int32_t buf, uint32_t epoch, const int32_t *slot_pos,

@@ -30,8 +30,14 @@ class EPError(RuntimeError):
         self.status = status
 
 
+_handle = None
+
+
 def _lib_handle():
-    return _lib.load()
+    global _handle
+    if _handle is None:
+        _handle = _lib.load()
+    return _handle
 
 
 def _check(status: int, what: str):
@@ -41,13 +47,20 @@ def _check(status: int, what: str):
         raise EPError(status, f"{what}: {name}: {lib.ep_last_error().decode()}")
 
 
-def _stream_ptr(stream: Optional[torch.cuda.Stream]) -> ctypes.c_void_p:
-    s = stream if stream is not None else torch.cuda.current_stream()
-    return ctypes.c_void_p(s.cuda_stream)
+_raw_stream = getattr(torch._C, "_cuda_getCurrentRawStream", None)
 
 
-def _ptr(t: Optional[torch.Tensor]) -> ctypes.c_void_p:
-    return ctypes.c_void_p(t.data_ptr() if t is not None and t.numel() else None)
+def _stream_ptr(stream=None) -> int:
+    """Raw HIP stream handle: `stream` (torch stream or int handle), else the current stream."""
+    if stream is None:
+        if _raw_stream is not None:
+            return _raw_stream(torch.cuda.current_device())
+        return torch.cuda.current_stream().cuda_stream
+    return stream if isinstance(stream, int) else stream.cuda_stream
+
+
+def _ptr(t: Optional[torch.Tensor]):
+    return t.data_ptr() if t is not None and t.numel() else None
 
 
 def _need(t: torch.Tensor, name: str, dtypes, ndim=None):

@@ -11,7 +11,7 @@
 // Mapping: one wave per (token, column chunk of 64*U 16-byte vectors); the k slot
 // positions and gates are wave-uniform scalar loads.  Slots are taken KC at a time and
 // all KC*U row loads of a batch are issued before their FMAs, keeping KC*U KiB in flight
-// per wave.
+// per wave.  Rows are read once: loads and stores are non-temporal.
 #include "ep_internal.h"
 
 namespace ep {
@@ -65,7 +65,7 @@ __global__ __launch_bounds__(256) void combine_kernel(const u32x4 *__restrict__ 
 #pragma unroll
             for (int u = 0; u < U; ++u) {
                 const int32_t v = v0 + u * kWave + lane;
-                d[jj][u] = ok[jj] && v < V ? src[v] : u32x4{0u, 0u, 0u, 0u};
+                d[jj][u] = ok[jj] && v < V ? __builtin_nontemporal_load(src + v) : u32x4{0u, 0u, 0u, 0u};
             }
         }
 #pragma unroll

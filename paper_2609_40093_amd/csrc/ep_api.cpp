@@ -2,15 +2,23 @@
 //
 // Argument checks, staging buffers and their DMA streams, the chunked host legs, flag
 // writes and waits, and the timing-event tracer.  Every call enqueues on the caller's
-// stream; the library's side streams (up = D2H, down = H2D, sig = flag writes) join the
-// caller's stream through events, so the caller sees one ordered stream.
+// stream; the library's side streams (up = D2H, down = H2D) join the caller's stream
+// through events, so the caller sees one ordered stream.
+//
+// Device->host legs run on an SDMA engine driven through ROCr (sdma.h), because the HIP
+// runtime may turn a device->host hipMemcpyAsync into a copy kernel on the compute
+// units.  Host->device legs are hipMemcpyAsync copies, which the runtime places on SDMA.
+// EP_HOSTLEG_COPY=hip sends the device->host leg through hipMemcpyAsync too (the
+// runtime's own choice of engine, kept as a measured comparison).
 #include "ep.h"
 #include "ep_internal.h"
+#include "sdma.h"
 
 #include <algorithm>
 #include <atomic>
 #include <cstdarg>
 #include <cstdio>
+#include <cstdlib>
 #include <cstring>
 #include <map>
 #include <mutex>
@@ -47,7 +55,19 @@ ep_status hip_fail(hipError_t e, const char *what) {
 bool aligned16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
 constexpr int kMaxBuffers = 8;
-constexpr int64_t kDefaultChunk = 8ll << 20;
+constexpr int64_t kDefaultChunk = 64ll << 20;
+constexpr size_t kEpochStride = 64;  // one device epoch word per buffer set, 64 B apart
+
+constexpr int kSdmaSlots = 4;        // device->host rounds in flight per staging
+
+// true: the device->host leg goes through hipMemcpyAsync instead of the SDMA lane.
+bool d2h_through_hip() {
+    static const bool v = [] {
+        const char *e = std::getenv("EP_HOSTLEG_COPY");
+        return e && std::strcmp(e, "hip") == 0;
+    }();
+    return v;
+}
 
 }  // namespace
 
@@ -61,10 +81,12 @@ struct ep_staging {
     void *host_send[kMaxBuffers] = {}, *host_recv[kMaxBuffers] = {};
     uint32_t *flags = nullptr;  // coherent pinned: send [nbuf][max_chunks], recv [nbuf][R], status
     size_t flag_words = 0;
-    hipStream_t up = nullptr, down = nullptr, sig = nullptr;
+    char *dev_epoch = nullptr;  // device: the epoch of each buffer set's current round
+    ep::SdmaLane *lane = nullptr;  // device->host leg on one SDMA engine
+    hipEvent_t ev_sysrel = nullptr;  // records a system-scope release before the lane reads
+    hipStream_t up = nullptr, down = nullptr;
     hipEvent_t ev_up_in[kMaxBuffers] = {}, ev_up_done[kMaxBuffers] = {};
     hipEvent_t ev_down_in[kMaxBuffers] = {}, ev_down_done[kMaxBuffers] = {};
-    std::vector<hipEvent_t> ev_chunk;  // [nbuf][max_chunks]
     int64_t timeout_us = 10ll * 1000 * 1000;
     int32_t sleep_units = 2;
     int64_t wall_clock_khz = 100000;
@@ -74,6 +96,7 @@ struct ep_staging {
         return flags + (size_t)num_buffers * max_chunks + (size_t)b * num_ranks;
     }
     uint32_t *status() const { return flags + (size_t)num_buffers * (max_chunks + num_ranks); }
+    uint32_t *epoch_word(int b) const { return reinterpret_cast<uint32_t *>(dev_epoch + b * kEpochStride); }
 };
 
 // ------------------------------------------------------------------------- tracing
@@ -100,8 +123,9 @@ hipEvent_t pool_get() {
         g_event_pool.pop_back();
         return e;
     }
+    // timing-only events: no system-scope cache writeback folded into the measured span
     hipEvent_t e = nullptr;
-    if (hipEventCreate(&e) != hipSuccess)
+    if (hipEventCreateWithFlags(&e, hipEventDisableSystemFence) != hipSuccess)
         return nullptr;
     return e;
 }
@@ -201,7 +225,7 @@ extern "C" ep_status ep_dispatch_layout(const int32_t *topk_idx, int64_t num_tok
     a.slot_pos = slot_pos;
     a.row_src = row_src;
     a.status = reinterpret_cast<uint32_t *>(workspace);
-    a.tile_hist = ep::layout_tiles(a.slots) > 1
+    a.tile_hist = ep::layout_tiles(a.slots, E) > 1
                       ? reinterpret_cast<int32_t *>(static_cast<char *>(workspace) + ep::kWorkspaceHeader)
                       : nullptr;
     EP_HIP(ep::launch_layout(a, stream));
@@ -234,10 +258,14 @@ void staging_release(ep_staging *s) {
         for (hipEvent_t e : {s->ev_up_in[b], s->ev_up_done[b], s->ev_down_in[b], s->ev_down_done[b]})
             if (e) (void)hipEventDestroy(e);
     }
-    for (hipEvent_t e : s->ev_chunk)
-        if (e) (void)hipEventDestroy(e);
+    if (s->lane) {
+        s->lane->release();
+        delete s->lane;
+    }
+    if (s->ev_sysrel) (void)hipEventDestroy(s->ev_sysrel);
     if (s->flags) (void)hipHostFree(s->flags);
-    for (hipStream_t st : {s->up, s->down, s->sig})
+    if (s->dev_epoch) (void)hipFree(s->dev_epoch);
+    for (hipStream_t st : {s->up, s->down})
         if (st) (void)hipStreamDestroy(st);
     delete s;
 }
@@ -310,16 +338,22 @@ extern "C" ep_status ep_staging_alloc(ep_staging_kind kind, int64_t max_rows, in
         std::memset(s->flags, 0, s->flag_words * sizeof(uint32_t));
         EP_ALLOC_HIP(hipStreamCreateWithFlags(&s->up, hipStreamNonBlocking));
         EP_ALLOC_HIP(hipStreamCreateWithFlags(&s->down, hipStreamNonBlocking));
-        EP_ALLOC_HIP(hipStreamCreateWithFlags(&s->sig, hipStreamNonBlocking));
+        EP_ALLOC_HIP(hipMalloc((void **)&s->dev_epoch, kMaxBuffers * kEpochStride));
+        EP_ALLOC_HIP(hipEventCreateWithFlags(&s->ev_sysrel, hipEventDisableTiming | hipEventReleaseToSystem));
+        if (!d2h_through_hip()) {
+            std::string err;
+            s->lane = new ep::SdmaLane();
+            if (!s->lane->init(s->device, kSdmaSlots, err)) {
+                staging_release(s);
+                return fail(EP_ERR_HIP, "ep_staging_alloc: SDMA lane: %s", err.c_str());
+            }
+        }
         for (int b = 0; b < num_buffers; ++b) {
             EP_ALLOC_HIP(hipEventCreateWithFlags(&s->ev_up_in[b], hipEventDisableTiming));
             EP_ALLOC_HIP(hipEventCreateWithFlags(&s->ev_up_done[b], hipEventDisableTiming));
             EP_ALLOC_HIP(hipEventCreateWithFlags(&s->ev_down_in[b], hipEventDisableTiming));
             EP_ALLOC_HIP(hipEventCreateWithFlags(&s->ev_down_done[b], hipEventDisableTiming));
         }
-        s->ev_chunk.assign((size_t)num_buffers * s->max_chunks, nullptr);
-        for (auto &e : s->ev_chunk)
-            EP_ALLOC_HIP(hipEventCreateWithFlags(&e, hipEventDisableTiming));
     }
 #undef EP_ALLOC_HIP
     *out = s;
@@ -332,7 +366,7 @@ extern "C" ep_status ep_staging_free(ep_staging *s) {
     int prev = -1;
     if (hipGetDevice(&prev) == hipSuccess && prev != s->device)
         (void)hipSetDevice(s->device);
-    for (hipStream_t st : {s->up, s->down, s->sig})
+    for (hipStream_t st : {s->up, s->down})
         if (st) (void)hipStreamSynchronize(st);
     staging_release(s);
     if (prev >= 0)
@@ -379,7 +413,7 @@ extern "C" ep_status ep_staging_status(ep_staging *s, hipStream_t stream) {
     if (st != EP_OK)
         return st;
     EP_HIP(hipStreamSynchronize(stream));
-    for (hipStream_t side : {s->up, s->down, s->sig})
+    for (hipStream_t side : {s->up, s->down})
         if (side) EP_HIP(hipStreamSynchronize(side));
     if (!s->flags)
         return EP_OK;
@@ -424,36 +458,60 @@ extern "C" ep_status ep_dispatch(const void *x_dev, int64_t num_tokens, int32_t 
     if (num_tokens > 0 && (!x_dev || !aligned16(x_dev)))
         return fail(EP_ERR_INVALID_ARG, "ep_dispatch: x must be a non-NULL 16-byte aligned pointer");
     const int64_t rows = num_tokens * topk;
-    EP_HIP(ep::launch_pack(x_dev, num_tokens, hidden, topk, slot_pos, s->dev_send[buf], s->max_rows, stream));
-    if (s->kind != EP_STAGING_PINNED_HOST || rows == 0)
+    const bool pinned = s->kind == EP_STAGING_PINNED_HOST;
+    EP_HIP(ep::launch_pack(x_dev, num_tokens, hidden, topk, slot_pos, s->dev_send[buf], s->max_rows,
+                           pinned ? s->epoch_word(buf) : nullptr, epoch, stream));
+    if (!pinned || rows == 0)
         return EP_OK;
 
-    // Host leg on the up stream, fixed-size chunks of the contiguous packed rows; after
-    // each chunk has landed, the sig stream raises that chunk's flag.  The copies never
-    // wait for a flag write.
     const int64_t bytes = rows * s->row_bytes;
     const int64_t chunks = (bytes + s->chunk_bytes - 1) / s->chunk_bytes;
     char *dsrc = static_cast<char *>(s->dev_send[buf]);
     char *hdst = static_cast<char *>(s->host_send[buf]);
+    ep::TraceSlot ts = ep::trace_acquire();
+    if (s->lane) {
+        // SDMA lane: make the packed rows visible at system scope (every XCD's L2), release
+        // the lane's start signal from the stream, submit chunk + flag copies to the engine,
+        // and let the stream wait (bounded) for the last flag.
+        std::string err;
+        ep::SdmaLane::Round round;
+        if (!s->lane->begin(round, s->timeout_us, err))
+            return fail(EP_ERR_TIMEOUT, "ep_dispatch: %s", err.c_str());
+        if (ts.start)
+            EP_HIP(hipEventRecord(ts.start, stream));
+        EP_HIP(hipEventRecord(s->ev_sysrel, stream));
+        EP_HIP(ep::launch_release_signal(round.start_value, stream));
+        if (!s->lane->submit(round, hdst, dsrc, bytes, s->chunk_bytes, s->send_flags(buf), s->epoch_word(buf),
+                             epoch, err))
+            return fail(EP_ERR_HIP, "ep_dispatch: %s", err.c_str());
+        const int64_t ticks = s->timeout_us * s->wall_clock_khz / 1000;
+        EP_HIP(ep::launch_wait_flags("wait_d2h", s->send_flags(buf) + (chunks - 1), 1, epoch, ticks,
+                                     s->sleep_units, s->status(), stream));
+        if (ts.stop) {
+            EP_HIP(hipEventRecord(ts.stop, stream));
+            ep::trace_submit("d2h_leg", ts);
+        }
+        return EP_OK;
+    }
+
+    // hipMemcpyAsync path on the up stream: each chunk followed by a 4-byte copy of this
+    // round's epoch (written by the pack kernel) into the chunk's flag.
     EP_HIP(hipEventRecord(s->ev_up_in[buf], stream));
     EP_HIP(hipStreamWaitEvent(s->up, s->ev_up_in[buf], 0));
-    ep::TraceSlot ts = ep::trace_acquire();
     if (ts.start)
         EP_HIP(hipEventRecord(ts.start, s->up));
     for (int64_t c = 0; c < chunks; ++c) {
         const int64_t off = c * s->chunk_bytes;
         const int64_t len = std::min<int64_t>(s->chunk_bytes, bytes - off);
         EP_HIP(hipMemcpyAsync(hdst + off, dsrc + off, (size_t)len, hipMemcpyDeviceToHost, s->up));
-        hipEvent_t ev = s->ev_chunk[(size_t)buf * s->max_chunks + c];
-        EP_HIP(hipEventRecord(ev, s->up));
-        EP_HIP(hipStreamWaitEvent(s->sig, ev, 0));
-        EP_HIP(ep::launch_write_flag(s->send_flags(buf) + c, epoch, s->sig));
+        EP_HIP(hipMemcpyAsync(s->send_flags(buf) + c, s->epoch_word(buf), sizeof(uint32_t),
+                              hipMemcpyDeviceToHost, s->up));
     }
     if (ts.stop) {
         EP_HIP(hipEventRecord(ts.stop, s->up));
-        ep::trace_submit("d2h", ts);
+        ep::trace_submit("d2h_leg", ts);
     }
-    EP_HIP(hipEventRecord(s->ev_up_done[buf], s->sig));
+    EP_HIP(hipEventRecord(s->ev_up_done[buf], s->up));
     EP_HIP(hipStreamWaitEvent(stream, s->ev_up_done[buf], 0));
     return EP_OK;
 }
@@ -472,30 +530,21 @@ extern "C" ep_status ep_combine(ep_staging *s, int32_t buf, uint32_t epoch, cons
     if (rows == 0)
         return EP_OK;
     if (s->kind == EP_STAGING_PINNED_HOST) {
-        // Wait (bounded) for every sender's flag, then the host leg on the down stream.
+        // Wait (bounded) for every sender's flag, then the host leg as one copy on the
+        // caller's stream: the reduction needs every row, and a copy the runtime orders
+        // inside one stream reaches the next kernel sooner than one joined from another.
         const int64_t bytes = rows * s->row_bytes;
-        const int64_t chunks = (bytes + s->chunk_bytes - 1) / s->chunk_bytes;
-        char *hsrc = static_cast<char *>(s->host_recv[buf]);
-        char *ddst = static_cast<char *>(s->dev_recv[buf]);
         const int64_t ticks = s->timeout_us * s->wall_clock_khz / 1000;
-        EP_HIP(hipEventRecord(s->ev_down_in[buf], stream));
-        EP_HIP(hipStreamWaitEvent(s->down, s->ev_down_in[buf], 0));
-        EP_HIP(ep::launch_wait_flags(s->recv_flags(buf), s->num_ranks, epoch, ticks, s->sleep_units,
-                                     s->status(), s->down));
+        EP_HIP(ep::launch_wait_flags("wait_recv", s->recv_flags(buf), s->num_ranks, epoch, ticks, s->sleep_units,
+                                     s->status(), stream));
         ep::TraceSlot ts = ep::trace_acquire();
         if (ts.start)
-            EP_HIP(hipEventRecord(ts.start, s->down));
-        for (int64_t c = 0; c < chunks; ++c) {
-            const int64_t off = c * s->chunk_bytes;
-            const int64_t len = std::min<int64_t>(s->chunk_bytes, bytes - off);
-            EP_HIP(hipMemcpyAsync(ddst + off, hsrc + off, (size_t)len, hipMemcpyHostToDevice, s->down));
-        }
+            EP_HIP(hipEventRecord(ts.start, stream));
+        EP_HIP(hipMemcpyAsync(s->dev_recv[buf], s->host_recv[buf], (size_t)bytes, hipMemcpyHostToDevice, stream));
         if (ts.stop) {
-            EP_HIP(hipEventRecord(ts.stop, s->down));
-            ep::trace_submit("h2d", ts);
+            EP_HIP(hipEventRecord(ts.stop, stream));
+            ep::trace_submit("h2d_leg", ts);
         }
-        EP_HIP(hipEventRecord(s->ev_down_done[buf], s->down));
-        EP_HIP(hipStreamWaitEvent(stream, s->ev_down_done[buf], 0));
     }
     EP_HIP(ep::launch_combine(s->dev_recv[buf], slot_pos, topk_w, num_tokens, hidden, topk, out_dev,
                               out_dtype == EP_OUT_F32, s->max_rows, stream));

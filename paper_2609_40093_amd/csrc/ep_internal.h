@@ -15,24 +15,30 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 constexpr int kWave = 64;
 
 // ---- layout geometry -----------------------------------------------------------
-constexpr int kLayoutThreads = 256;                       // 4 waves per workgroup
-constexpr int kLayoutWaves = kLayoutThreads / kWave;
-constexpr int kTileSlots = 4096;                          // routing entries per tile
-constexpr int kSlotsPerWave = kTileSlots / kLayoutWaves;  // contiguous run per wave
-constexpr int kRoundsPerWave = kSlotsPerWave / kWave;     // 64 entries per round
+// A workgroup of W waves ranks one tile; each wave walks kLayoutRounds rounds of 64
+// routing entries.  W = 16 while W per-wave counter rows of E experts (plus the scan
+// arrays) fit in 64 KiB of LDS, else 4.
+constexpr int kLayoutRounds = 8;
 constexpr int kMaxExperts = 2048;
+constexpr int layout_waves(int32_t experts) { return experts <= 512 ? 16 : 4; }
+constexpr int64_t layout_tile_slots(int waves) { return (int64_t)waves * kWave * kLayoutRounds; }
 
 // Routing status bits left in the layout workspace's status word.
 constexpr uint32_t kRoutingIdOutOfRange = 1u;
 constexpr uint32_t kRoutingDuplicate = 2u;
 
-// Layout workspace: [0,256) status word (+ padding), then int32 tile histogram
-// [num_tiles][E] when more than one tile is needed.
+// Layout workspace: [0,256) status word (+ padding); when more than one tile is needed,
+// then int32 tile totals [num_tiles][E] and per-wave counts [num_tiles][W][E].
 constexpr size_t kWorkspaceHeader = 256;
-inline int64_t layout_tiles(int64_t slots) { return (slots + kTileSlots - 1) / kTileSlots; }
+inline int64_t layout_tiles(int64_t slots, int32_t experts) {
+    const int64_t tile = layout_tile_slots(layout_waves(experts));
+    return (slots + tile - 1) / tile;
+}
 inline size_t layout_workspace_bytes(int64_t slots, int32_t experts) {
-    int64_t tiles = layout_tiles(slots);
-    return kWorkspaceHeader + (tiles > 1 ? (size_t)tiles * (size_t)experts * sizeof(int32_t) : 0);
+    const int64_t tiles = layout_tiles(slots, experts);
+    return kWorkspaceHeader + (tiles > 1 ? (size_t)tiles * (1 + layout_waves(experts)) * (size_t)experts *
+                                               sizeof(int32_t)
+                                         : 0);
 }
 
 // ---- timing events (tracing) -----------------------------------------------------
@@ -53,22 +59,27 @@ struct LayoutArgs {
     int32_t *expert_counts, *expert_offsets, *rank_counts, *rank_offsets;
     int32_t *slot_pos, *row_src;
     uint32_t *status;
-    int32_t *tile_hist;  // [tiles][E] or null for one tile
+    int32_t *tile_hist;  // [tiles][E] tile totals, then [tiles][waves][E] wave counts; null for one tile
 };
 hipError_t launch_layout(const LayoutArgs &a, hipStream_t stream);
 
+// Also stores `epoch` into *epoch_word (when non-null) for the host leg's flag copies.
 hipError_t launch_pack(const void *x, int64_t T, int32_t H, int32_t k, const int32_t *slot_pos,
-                       void *packed, int64_t max_rows, hipStream_t stream);
+                       void *packed, int64_t max_rows, uint32_t *epoch_word, uint32_t epoch,
+                       hipStream_t stream);
 
 hipError_t launch_combine(const void *recv, const int32_t *slot_pos, const float *topk_w,
                           int64_t T, int32_t H, int32_t k, void *out, bool out_f32,
                           int64_t max_rows, hipStream_t stream);
 
-hipError_t launch_wait_flags(const uint32_t *flags, int32_t n, uint32_t epoch,
+// One lane per flag polls flags[i] until (int32)(flags[i] - epoch) >= 0, at most
+// timeout_ticks of the constant-rate wall clock; on expiry stores EP_ERR_TIMEOUT to *status.
+hipError_t launch_wait_flags(const char *name, const uint32_t *flags, int32_t n, uint32_t epoch,
                              int64_t timeout_ticks, int32_t sleep_units, uint32_t *status,
                              hipStream_t stream);
 
-hipError_t launch_write_flag(uint32_t *flag, uint32_t epoch, hipStream_t stream);
+// Stores 0 into *value (a DMA dependency signal) with a system-scope release.
+hipError_t launch_release_signal(int64_t *value, hipStream_t stream);
 
 hipError_t launch_copy(void *dst, const void *src, size_t bytes, hipStream_t stream);
 

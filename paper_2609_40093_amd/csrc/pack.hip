@@ -22,8 +22,11 @@ template <int U>
 __global__ __launch_bounds__(256) void pack_kernel(const u32x4 *__restrict__ x, int64_t T, int32_t V,
                                                    int32_t chunks, int32_t k,
                                                    const int32_t *__restrict__ slot_pos,
-                                                   u32x4 *__restrict__ packed, int64_t max_rows) {
+                                                   u32x4 *__restrict__ packed, int64_t max_rows,
+                                                   uint32_t *epoch_word, uint32_t epoch) {
     const int lane = threadIdx.x & (kWave - 1);
+    if (epoch_word && blockIdx.x == 0 && threadIdx.x == 0)
+        *epoch_word = epoch;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
     const int64_t item = (int64_t)blockIdx.x * (blockDim.x / kWave) + wave;
     const int64_t t = item / chunks;
@@ -55,7 +58,8 @@ __global__ __launch_bounds__(256) void pack_kernel(const u32x4 *__restrict__ x, 
 }  // namespace
 
 hipError_t launch_pack(const void *x, int64_t T, int32_t H, int32_t k, const int32_t *slot_pos,
-                       void *packed, int64_t max_rows, hipStream_t stream) {
+                       void *packed, int64_t max_rows, uint32_t *epoch_word, uint32_t epoch,
+                       hipStream_t stream) {
     if (T == 0)
         return hipSuccess;
     const int32_t V = H / 8;
@@ -67,7 +71,7 @@ hipError_t launch_pack(const void *x, int64_t T, int32_t H, int32_t k, const int
     TraceSlot ts = trace_acquire();
     hipExtLaunchKernelGGL(pack_kernel<kPackU>, dim3((unsigned)blocks), dim3(waves_per_block * kWave), 0,
                           stream, ts.start, ts.stop, 0, (const u32x4 *)x, T, V, chunks, k, slot_pos,
-                          (u32x4 *)packed, max_rows);
+                          (u32x4 *)packed, max_rows, epoch_word, epoch);
     hipError_t err = hipGetLastError();
     if (err == hipSuccess)
         trace_submit("pack", ts);

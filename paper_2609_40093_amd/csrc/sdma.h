@@ -1,0 +1,64 @@
+// sdma.h -- device->host leg on one SDMA engine, driven through the ROCr runtime.
+//
+// The HIP runtime may run a device->host hipMemcpyAsync as a copy kernel on the compute
+// units; this lane submits the leg to a chosen SDMA engine instead (Sec. 4.3 of the
+// paper: bulk data moves on DMA engines so that no compute unit is spent on it).
+//
+// Ordering, per round:
+//   stream:  pack kernel -> event with system-scope release (every XCD's L2 written
+//            back) -> 1-wave kernel storing 0 into the round's start signal
+//   SDMA:    [poll start signal == 0] copy chunk 0 -> [poll chunk 0 done] copy epoch word
+//            -> send flag 0 -> copy chunk 1 -> ... (one engine, in order)
+//   stream:  bounded wait until the last chunk's flag holds the epoch
+// Signals of a round are reused only once that round's last flag is seen on the host.
+#pragma once
+
+#include <hsa/hsa.h>
+#include <hsa/hsa_ext_amd.h>
+
+#include <cstdint>
+#include <string>
+#include <vector>
+
+namespace ep {
+
+class SdmaLane {
+public:
+    // Finds the GPU agent of HIP device `device`, its nearest CPU agent and a free SDMA
+    // engine for device->host copies.  Returns false with `err` set on failure.
+    bool init(int device, int slots, std::string &err);
+    void release();
+
+    struct Round {
+        int64_t *start_value = nullptr;  // device-writable value of the start signal
+        int slot = -1;
+    };
+    // Reserves a slot whose previous round has finished (its last flag reached its epoch),
+    // waiting on the host for at most timeout_us.  Resets the slot's start signal.
+    bool begin(Round &r, int64_t timeout_us, std::string &err);
+    // Submits the chunk copies and the flag copies of a round (after the stream work that
+    // releases the start signal has been enqueued).
+    bool submit(const Round &r, void *host_dst, const void *dev_src, int64_t bytes, int64_t chunk_bytes,
+                uint32_t *flags, const uint32_t *epoch_word, uint32_t epoch, std::string &err);
+
+    const char *engine_name() const { return engine_name_.c_str(); }
+
+private:
+    struct Slot {
+        hsa_signal_t start{};
+        std::vector<hsa_signal_t> done;  // one per chunk, grown on demand
+        volatile uint32_t *last_flag = nullptr;
+        uint32_t epoch = 0;
+        bool busy = false;
+    };
+    bool ensure_done_signals(Slot &s, int64_t n, std::string &err);
+
+    hsa_agent_t gpu_{}, cpu_{};
+    uint32_t engine_ = 0;  // hsa_amd_sdma_engine_id_t bit, 0 = let the runtime choose
+    std::string engine_name_;
+    std::vector<Slot> slots_;
+    int next_ = 0;
+    bool ready_ = false;
+};
+
+}  // namespace ep

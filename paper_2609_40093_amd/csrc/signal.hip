@@ -1,8 +1,8 @@
 // signal.hip -- completion flags in pinned host memory (Sec. 4.4 of the paper).
 //
 // The payload stays contiguous and the flags live apart from it, one 32-bit word per
-// sender (receive side) or per DMA chunk (send side), each with a single writer, so no
-// atomic read-modify-write is needed.  A flag holds the epoch of the round that filled
+// sender (receive side) or per DMA chunk (send side, written by a 4-byte DMA copy queued
+// behind the chunk), each with a single writer, so no atomic read-modify-write is needed.  A flag holds the epoch of the round that filled
 // its data; a reader accepts it when (int32)(flag - epoch) >= 0, so a flag left over from
 // an earlier round is never taken for the current one.
 //
@@ -38,14 +38,25 @@ __global__ __launch_bounds__(64) void wait_flags_kernel(const uint32_t *flags, i
     }
 }
 
-__global__ __launch_bounds__(64) void write_flag_kernel(uint32_t *flag, uint32_t epoch) {
+// Releases a DMA-engine dependency: stores 0 into a signal value the engine polls.
+__global__ __launch_bounds__(64) void release_signal_kernel(int64_t *value) {
     if (threadIdx.x == 0)
-        __hip_atomic_store(flag, epoch, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_SYSTEM);
+        __hip_atomic_store(value, (int64_t)0, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_SYSTEM);
 }
 
 }  // namespace
 
-hipError_t launch_wait_flags(const uint32_t *flags, int32_t n, uint32_t epoch,
+hipError_t launch_release_signal(int64_t *value, hipStream_t stream) {
+    (void)hipGetLastError();
+    TraceSlot ts = trace_acquire();
+    hipExtLaunchKernelGGL(release_signal_kernel, dim3(1), dim3(64), 0, stream, ts.start, ts.stop, 0, value);
+    hipError_t err = hipGetLastError();
+    if (err == hipSuccess)
+        trace_submit("release_signal", ts);
+    return err;
+}
+
+hipError_t launch_wait_flags(const char *name, const uint32_t *flags, int32_t n, uint32_t epoch,
                              int64_t timeout_ticks, int32_t sleep_units, uint32_t *status,
                              hipStream_t stream) {
     if (n <= 0)
@@ -56,14 +67,8 @@ hipError_t launch_wait_flags(const uint32_t *flags, int32_t n, uint32_t epoch,
                           ts.start, ts.stop, 0, flags, n, epoch, timeout_ticks, sleep_units, status);
     hipError_t err = hipGetLastError();
     if (err == hipSuccess)
-        trace_submit("wait_flags", ts);
+        trace_submit(name, ts);
     return err;
-}
-
-hipError_t launch_write_flag(uint32_t *flag, uint32_t epoch, hipStream_t stream) {
-    (void)hipGetLastError();
-    hipLaunchKernelGGL(write_flag_kernel, dim3(1), dim3(64), 0, stream, flag, epoch);
-    return hipGetLastError();
 }
 
 }  // namespace ep

@@ -58,7 +58,7 @@ def test_workspace_bytes(lib):
     assert lib.ep_layout_workspace_bytes(128, 2, 16, ctypes.byref(n)) == 0
     assert n.value == 256                           # one tile: status word only
     assert lib.ep_layout_workspace_bytes(32768, 8, 256, ctypes.byref(n)) == 0
-    assert n.value == 256 + 64 * 256 * 4            # 64 tiles of 4096 entries x 256 experts
+    assert n.value == 256 + 32 * 17 * 256 * 4       # 32 tiles of 8192 entries: totals + 16 waves' counts
     assert lib.ep_layout_workspace_bytes(-1, 2, 16, ctypes.byref(n)) == _lib.EP_ERR_INVALID_ARG
     assert lib.ep_layout_workspace_bytes(4, 2, 4096, ctypes.byref(n)) == _lib.EP_ERR_INVALID_ARG
     assert b"bad sizes" in lib.ep_last_error()

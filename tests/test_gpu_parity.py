@@ -83,11 +83,13 @@ def check_case(case):
 
 CASES = [
     # name, T, H, E, k, R, routing
-    ("tiles3_ragged", 1500, 2056, 64, 8, 8, "random"),      # 12000 entries: 2 full tiles + tail; ragged chunk
-    ("tile_exact", 2048, 256, 32, 2, 4, "random"),          # exactly one tile
-    ("tile_plus_one", 4097, 64, 16, 1, 2, "random"),        # one tile + one entry
-    ("many_tiles_small_rows", 20000, 8, 256, 8, 8, "skewed"),  # 40 tiles, H = 8 (one vector)
-    ("max_experts", 3000, 128, 2048, 4, 8, "random"),       # E at the kernel limit
+    ("tiles3_ragged", 2500, 2056, 64, 8, 8, "random"),      # 20000 entries: 2 full tiles + tail; ragged chunk
+    ("tile_exact", 4096, 256, 32, 2, 4, "random"),          # exactly one tile (8192 entries)
+    ("tile_plus_one", 8193, 64, 16, 1, 2, "random"),        # one tile + one entry
+    ("many_tiles_small_rows", 40000, 8, 256, 8, 8, "skewed"),  # 40 tiles, H = 8 (one vector)
+    ("max_experts", 3000, 128, 2048, 4, 8, "random"),       # E at the kernel limit (4-wave tiles)
+    ("wide_experts_one_tile", 100, 64, 1024, 4, 8, "random"),  # 4-wave tile, single kernel
+    ("e512_two_tiles", 2000, 64, 512, 8, 8, "skewed"),      # largest E of the 16-wave tiles
     ("one_expert", 333, 512, 1, 1, 1, "random"),
     ("k_equals_E", 100, 1024, 6, 6, 3, "random"),
     ("odd_E", 999, 136, 96, 5, 8, "random"),
@@ -129,7 +131,7 @@ def test_empty_batch():
 
 def test_layout_deterministic():
     """Positions never depend on scheduling: 20 runs give identical bytes."""
-    case = make_case("det", 30000, 8, 256, 8, 8, "skewed", seed=3)
+    case = make_case("det", 60000, 8, 256, 8, 8, "skewed", seed=3)
     say("determinism x20")
     idx = torch.from_numpy(case.topk_idx).to(DEV)
     first = None
