@@ -265,8 +265,7 @@ def bench_pinned(cfg, inp, y, args, dev) -> dict:
         step(i)
     st.status()
     peers.drain()
-    ep.trace_reset()
-    ep.trace_enable(True)
+    # timed region: untraced (events around DMA legs add markers that slow the hand-offs)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for i in range(steps):
@@ -274,9 +273,16 @@ def bench_pinned(cfg, inp, y, args, dev) -> dict:
     st.status()
     t1 = time.perf_counter()
     peers.drain()
+    ms = (t1 - t0) * 1e3 / steps
+    # breakdown pass (not timed): every kernel and leg bracketed by events
+    ep.trace_reset()
+    ep.trace_enable(True)
+    for i in range(steps):
+        step(args.warmup + steps + i)
+    st.status()
+    peers.drain()
     ep.trace_enable(False)
     ks = ep.trace_read()
-    ms = (t1 - t0) * 1e3 / steps
     legs = {}
     for name in ("d2h_leg", "h2d_leg", "wait_d2h", "wait_recv", "release_signal", "pack", "combine",
                  "layout_rank", "layout_histogram"):
@@ -294,6 +300,7 @@ def bench_pinned(cfg, inp, y, args, dev) -> dict:
         "payload_GBps": round(2 * cfg.payload_bytes / (ms * 1e-3) / 1e9, 2),
         "steps": steps,
         "legs": legs,
+        "legs_note": "legs from a separate traced pass; events around DMA legs inflate their span",
         "pcie_bytes_per_leg": pcie_bytes,
         "pcie_measured_peak_GBps": peaks,
         "pcie_published_peak_GBps": PCIE_PEAK_GBPS,

@@ -113,6 +113,19 @@ def pack(x: np.ndarray, slot_pos: np.ndarray, k: int, rows: int = None, lib=None
     return out[:rows]
 
 
+def pack_rows(x: np.ndarray, row_src: np.ndarray, k: int, rows: np.ndarray) -> np.ndarray:
+    """The pack definition evaluated at selected packed rows only: row p holds the token
+    row x[row_src[p] // k] (for full-size checks where the whole packed buffer is large)."""
+    return np.ascontiguousarray(x[np.asarray(row_src)[np.asarray(rows)] // k])
+
+
+def combine_tokens(y_rows: np.ndarray, topk_w: np.ndarray):
+    """combine() for selected tokens: y_rows[i*k + j] is the returned row of slot j of the
+    i-th selected token, topk_w [n, k] their gates."""
+    n, k = topk_w.shape
+    return combine(y_rows, np.arange(n * k, dtype=np.int32), topk_w)
+
+
 def combine(y: np.ndarray, slot_pos: np.ndarray, topk_w: np.ndarray, lib=None):
     """Returns (exact float64 [T,H], bf16 bits uint16 [T,H], float32 [T,H])."""
     lib = lib or load()

@@ -239,6 +239,8 @@ def pin_pack(lib):
         packed = oracle.pack(x, np.array(b["slot_pos"], np.int32), k, lib=lib)
         want = x[np.array(b["row_src"]) // k]
         assert packed.tobytes() == want.tobytes(), "packed rows differ"
+        rows = np.arange(T * k)[::3]
+        assert oracle.pack_rows(x, np.array(b["row_src"]), k, rows).tobytes() == packed[rows].tobytes()
 
 
 # --------------------------------------------------------------------------- combine pins
@@ -283,6 +285,9 @@ def pin_combine_inverse_permutation(lib):
     y[(y & 0x7F80) == 0x7F80] &= 0xBFFF
     _, b16, _ = oracle.combine(y, slot_pos, np.ones((T, 1), np.float32), lib=lib)
     assert b16.tobytes() == y[slot_pos].tobytes()
+    # the per-token form gives the same rows
+    _, b16_tok, _ = oracle.combine_tokens(y[slot_pos[::2]], np.ones((len(slot_pos[::2]), 1), np.float32))
+    assert b16_tok.tobytes() == b16[::2].tobytes()
 
 
 def pin_combine_identity(lib):
