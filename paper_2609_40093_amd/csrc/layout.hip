@@ -232,6 +232,9 @@ __global__ __launch_bounds__(W * 64) void layout_rank_kernel(LayoutArgs a, int32
     //    previous round / the 64 entries before the run for lanes near the front).
     int *wave_base = wave_cnt + w * E;
     bool bad_id = false, dup = false;
+    // slot index within the token row, advanced by 64 mod k per round (no division per round)
+    const int32_t step = kWave % a.k;
+    int32_t jslot = (int32_t)((run_begin + lane) % a.k);
 #pragma unroll
     for (int r = 0; r < kLayoutRounds; ++r) {
         const int64_t round_begin = run_begin + r * kWave;
@@ -243,7 +246,10 @@ __global__ __launch_bounds__(W * 64) void layout_rank_kernel(LayoutArgs a, int32
         const bool valid = in_range && (unsigned)e < (unsigned)E;
         const uint64_t m = match_expert(e, valid, a.nbits);
         const int32_t ii = (int32_t)i;
-        const int32_t jslot = in_range ? ii - (ii / a.k) * a.k : 0;
+        if (r > 0) {
+            jslot += step;
+            jslot -= jslot >= a.k ? a.k : 0;
+        }
         if (a.k <= kWave) {
             const int earlier_round = r == 0 ? halo : ids[r == 0 ? 0 : r - 1];
             for (int d = 1; d < a.k; ++d) {
