@@ -49,8 +49,7 @@ def algorithmic_bytes(cfg) -> dict:
     return {
         "pack": T * row + n * row + 4 * n,                  # read x once, write k copies, read slot_pos
         "combine": n * row + 8 * n + T * row,               # read k rows, gates and slot_pos, write out
-        "layout_rank": 4 * n + 4 * n + 4 * n,               # read ids, write slot_pos and row_src
-        "layout_histogram": 4 * n,
+        "layout": 4 * n + 4 * n + 4 * n,                    # read ids, write slot_pos and row_src
     }
 
 
@@ -285,7 +284,7 @@ def bench_pinned(cfg, inp, y, args, dev) -> dict:
     ks = ep.trace_read()
     legs = {}
     for name in ("d2h_leg", "h2d_leg", "wait_d2h", "wait_recv", "release_signal", "pack", "combine",
-                 "layout_rank", "layout_histogram"):
+                 "layout"):
         if name in ks:
             legs[name] = {"avg_us": round(ks[name]["mean_ms"] * 1e3, 2)}
     pcie_bytes = n * 2 * H

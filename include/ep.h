@@ -98,8 +98,11 @@ ep_status ep_layout_workspace_bytes(int64_t num_tokens, int32_t topk, int32_t nu
  *   slot_pos        int32 [T*k]: packed row of slot t*k+j = expert_offsets[e] + number of
  *                   earlier slots (smaller flat index) with the same expert.
  *   row_src         int32 [T*k] or NULL: inverse of slot_pos (row p came from slot row_src[p]).
- *   workspace       device scratch of ep_layout_workspace_bytes() bytes; it also holds
- *                   the routing status word read by ep_layout_status.
+ *   workspace       device scratch of ep_layout_workspace_bytes() bytes, zero-filled
+ *                   before its first use (e.g. hipMemset) and otherwise left alone between
+ *                   calls: it carries a call counter from one call to the next, the
+ *                   tiles' exchanged totals, and the status read by ep_layout_status.
+ *                   Calls that share a workspace must be ordered (same stream or events).
  * Requires T >= 0, T*k < 2^31, 1 <= k <= E <= EP_MAX_EXPERTS, R >= 1, E % R == 0.
  * T == 0 is valid: counts and offsets are written as zeros.  With an invalid expert id
  * the outputs are unspecified but every write stays inside the arrays above, and the
@@ -112,7 +115,11 @@ ep_status ep_dispatch_layout(const int32_t *topk_idx, int64_t num_tokens, int32_
                              void *workspace, size_t workspace_bytes, hipStream_t stream);
 
 /* Synchronizes `stream`, then reads the status word the last layout on `workspace` left:
- * EP_OK, or EP_ERR_BAD_ROUTING (an id outside [0,E) or an expert repeated in a row). */
+ * EP_OK, or EP_ERR_BAD_ROUTING (an id outside [0,E) or an expert repeated in a row), or
+ * EP_ERR_TIMEOUT if a layout's workgroups could not all run at once within a second (the
+ * device was held by other work); that state sticks until the workspace is zero-filled
+ * again, and the outputs of the call that timed out are unspecified (stores stay inside
+ * the arrays). */
 ep_status ep_layout_status(const void *workspace, hipStream_t stream);
 
 /* ------------------------------------------------------------------------ staging */

@@ -109,7 +109,7 @@ def dispatch_layout(topk_idx: torch.Tensor, num_experts: int, num_ranks: int, *,
                      torch.empty(num_experts, **i32), torch.empty(num_experts + 1, **i32),
                      torch.empty(num_ranks, **i32), torch.empty(num_ranks + 1, **i32),
                      torch.empty(T * k, **i32), torch.empty(T * k, **i32) if with_row_src else None,
-                     torch.empty(workspace_bytes(T, k, num_experts) if 1 <= k <= num_experts
+                     torch.zeros(workspace_bytes(T, k, num_experts) if 1 <= k <= num_experts
                                  and 1 <= num_experts <= _lib.EP_MAX_EXPERTS else 256,
                                  dtype=torch.uint8, device=dev))
     st = _lib_handle().ep_dispatch_layout(

@@ -224,10 +224,11 @@ extern "C" ep_status ep_dispatch_layout(const int32_t *topk_idx, int64_t num_tok
     a.rank_offsets = rank_offsets;
     a.slot_pos = slot_pos;
     a.row_src = row_src;
-    a.status = reinterpret_cast<uint32_t *>(workspace);
-    a.tile_hist = ep::layout_tiles(a.slots, E) > 1
-                      ? reinterpret_cast<int32_t *>(static_cast<char *>(workspace) + ep::kWorkspaceHeader)
-                      : nullptr;
+    char *ws = static_cast<char *>(workspace);
+    a.status = reinterpret_cast<uint32_t *>(ws);
+    a.epoch = reinterpret_cast<uint32_t *>(ws + ep::kWorkspaceEpoch);
+    a.timed_out = reinterpret_cast<uint32_t *>(ws + ep::kWorkspaceTimeout);
+    a.tile_words = reinterpret_cast<uint64_t *>(ws + ep::kWorkspaceHeader);
     EP_HIP(ep::launch_layout(a, stream));
     return EP_OK;
 }
@@ -236,8 +237,13 @@ extern "C" ep_status ep_layout_status(const void *workspace, hipStream_t stream)
     if (!workspace)
         return fail(EP_ERR_INVALID_ARG, "ep_layout_status: workspace is NULL");
     EP_HIP(hipStreamSynchronize(stream));
-    uint32_t word = 0;
+    uint32_t word = 0, timed_out = 0;
     EP_HIP(hipMemcpy(&word, workspace, sizeof word, hipMemcpyDeviceToHost));
+    EP_HIP(hipMemcpy(&timed_out, static_cast<const char *>(workspace) + ep::kWorkspaceTimeout, sizeof timed_out,
+                     hipMemcpyDeviceToHost));
+    if (timed_out)
+        return fail(EP_ERR_TIMEOUT, "a layout on this workspace gave up waiting for the totals of other "
+                                    "workgroups; zero-fill the workspace before using it again");
     if (word == 0)
         return EP_OK;
     return fail(EP_ERR_BAD_ROUTING, "routing rejected:%s%s",

@@ -4,6 +4,7 @@
 #include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cstddef>
 #include <cstdint>
 
@@ -15,30 +16,61 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 constexpr int kWave = 64;
 
 // ---- layout geometry -----------------------------------------------------------
-// A workgroup of W waves ranks one tile; each wave walks kLayoutRounds rounds of 64
-// routing entries.  W = 16 while W per-wave counter rows of E experts (plus the scan
-// arrays) fit in 64 KiB of LDS, else 4.
-constexpr int kLayoutRounds = 8;
+// The routing array is cut into tiles, one workgroup each; a workgroup has W waves and
+// each wave walks `rounds` rounds of 64 entries.  All tiles' workgroups are resident at
+// once (at most kLayoutMaxTiles of them, never more than the device's compute units):
+// each publishes its per-expert totals and reads everyone else's before ranking.
 constexpr int kMaxExperts = 2048;
-constexpr int layout_waves(int32_t experts) { return experts <= 512 ? 16 : 4; }
-constexpr int64_t layout_tile_slots(int waves) { return (int64_t)waves * kWave * kLayoutRounds; }
+constexpr int kLayoutMaxTiles = 256;
+constexpr int kLayoutRankCache = 8;  // rounds whose ids and in-wave ranks stay in registers
+struct LayoutGeom {
+    int waves;
+    int rounds;
+    int64_t tiles;
+};
+// Smallest tiles (most workgroups) such that the tile count stays within max_tiles and
+// the cross-tile gather reads at most 16 words per thread; W = 16 only while 16 rows of
+// per-wave counters fit in LDS (E <= 512).
+inline LayoutGeom layout_geometry(int64_t slots, int32_t experts, int64_t max_tiles) {
+    struct Cand {
+        int waves, rounds;
+    };
+    static constexpr Cand kCands[] = {{4, 1}, {4, 2}, {4, 4}, {4, 8}, {16, 1}, {16, 2}, {16, 4}, {16, 8}};
+    const bool wide = experts <= 512;
+    const int64_t cols = (int64_t)experts + 1;
+    for (const Cand &c : kCands) {
+        if (wide ? (c.waves == 4 && c.rounds > 2) : c.waves == 16)
+            continue;
+        const int64_t tile = (int64_t)kWave * c.waves * c.rounds;
+        const int64_t tiles = slots > tile ? (slots + tile - 1) / tile : 1;
+        if (tiles <= max_tiles && tiles * cols <= 16 * kWave * c.waves)
+            return {c.waves, c.rounds, tiles};
+    }
+    const int waves = wide ? 16 : 4;
+    const int64_t per_round = (int64_t)kWave * waves;
+    int64_t cap = 64 * per_round / cols;
+    cap = cap < 1 ? 1 : (cap > max_tiles ? max_tiles : cap);
+    const int64_t rounds = (slots + per_round * cap - 1) / (per_round * cap);
+    const int64_t tiles = (slots + per_round * rounds - 1) / (per_round * rounds);
+    return {waves, (int)(rounds < 1 ? 1 : rounds), tiles < 1 ? 1 : tiles};
+}
 
 // Routing status bits left in the layout workspace's status word.
 constexpr uint32_t kRoutingIdOutOfRange = 1u;
 constexpr uint32_t kRoutingDuplicate = 2u;
 
-// Layout workspace: [0,256) status word (+ padding); when more than one tile is needed,
-// then int32 tile totals [num_tiles][E] and per-wave counts [num_tiles][W][E].
+// Layout workspace (zero-filled before its first use):
+//   byte   0  uint32 routing status of the last call
+//   byte  64  uint32 epoch: calls on this workspace so far that used several tiles
+//   byte 128  uint32 nonzero once a workgroup gave up waiting for another's totals
+//   byte 256  uint64 [tiles][E+1] words (epoch+1) << 32 | value: a tile's per-expert
+//             totals, then its routing error bits
 constexpr size_t kWorkspaceHeader = 256;
-inline int64_t layout_tiles(int64_t slots, int32_t experts) {
-    const int64_t tile = layout_tile_slots(layout_waves(experts));
-    return (slots + tile - 1) / tile;
-}
+constexpr size_t kWorkspaceEpoch = 64;
+constexpr size_t kWorkspaceTimeout = 128;
 inline size_t layout_workspace_bytes(int64_t slots, int32_t experts) {
-    const int64_t tiles = layout_tiles(slots, experts);
-    return kWorkspaceHeader + (tiles > 1 ? (size_t)tiles * (1 + layout_waves(experts)) * (size_t)experts *
-                                               sizeof(int32_t)
-                                         : 0);
+    const LayoutGeom g = layout_geometry(slots, experts, kLayoutMaxTiles);
+    return kWorkspaceHeader + (g.tiles > 1 ? (size_t)g.tiles * ((size_t)experts + 1) * sizeof(uint64_t) : 0);
 }
 
 // ---- timing events (tracing) -----------------------------------------------------
@@ -58,10 +90,13 @@ struct LayoutArgs {
     int32_t k, E, R, nbits;
     int32_t *expert_counts, *expert_offsets, *rank_counts, *rank_offsets;
     int32_t *slot_pos, *row_src;
-    uint32_t *status;
-    int32_t *tile_hist;  // [tiles][E] tile totals, then [tiles][waves][E] wave counts; null for one tile
+    uint32_t *status;        // workspace byte 0
+    uint32_t *epoch;         // workspace byte 64
+    uint32_t *timed_out;     // workspace byte 128
+    uint64_t *tile_words;    // workspace byte 256
+    int64_t timeout_ticks;   // wall-clock ticks a workgroup waits for the others' totals
 };
-hipError_t launch_layout(const LayoutArgs &a, hipStream_t stream);
+hipError_t launch_layout(LayoutArgs a, hipStream_t stream);
 
 // Also stores `epoch` into *epoch_word (when non-null) for the host leg's flag copies.
 hipError_t launch_pack(const void *x, int64_t T, int32_t H, int32_t k, const int32_t *slot_pos,

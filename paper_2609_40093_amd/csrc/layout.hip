@@ -3,22 +3,29 @@
 // in expert order, hence contiguous per destination rank).  Sec. 4.3 of the paper groups
 // tokens by the experts that consume them; Sec. 4.5 sends each destination only its rows.
 //
-// Work split: the routing array is cut into tiles, one workgroup per tile, W waves per
-// workgroup, each wave owning a contiguous run of kLayoutRounds x 64 entries.  W is 16
-// (1024 lanes) when the per-wave counters of E experts fit in LDS next to each other,
-// else 4, so that a tile's entries are ranked by many waves at once while each wave
-// walks only a few rounds.
-//  * Inside a wave, the lanes holding the same expert are found with ceil(log2 E) 64-lane
-//    ballots ("match any"); a lane's rank among them is a masked popcount (mbcnt), and
-//    one leader lane per distinct expert updates the wave's counter in LDS.  No atomics
-//    decide any position, so the result is deterministic.
-//  * Across waves and tiles, positions come from exclusive prefix sums: per-wave counts
-//    in LDS (within the tile) and a per-tile histogram in the workspace (across tiles).
-//  * Expert offsets are a workgroup-wide exclusive scan built on a DPP wave scan.
-// One tile: a single kernel does everything.  Several tiles: a histogram kernel (tile
-// totals and per-wave counts), then the ranking kernel (each workgroup re-reads the small
-// [tiles][E] totals and its own per-wave counts instead of counting again).
+// One kernel, one workgroup per tile of the routing array, all workgroups resident at
+// once.  A workgroup has W waves; each wave owns a contiguous run of `rounds` x 64 entries.
+//  1. Count.  Inside a wave, the lanes holding the same expert are found with ceil(log2 E)
+//     64-lane ballots ("match any"); a lane's rank among them is a masked popcount
+//     (mbcnt).  One leader lane per distinct expert adds the group's size to the wave's
+//     counter row in LDS; every lane of the group reads the counter's old value first, so
+//     it learns its rank among the wave's earlier entries of that expert at the same
+//     time.  Routing errors (ids outside [0,E), an expert twice in one token row) are
+//     found here too.  No atomic decides any position: the result is deterministic.
+//  2. Exchange (several tiles).  Each workgroup publishes its per-expert totals and error
+//     bits as 64-bit words tagged with the call's epoch, then reads every tile's words,
+//     waiting (bounded by the wall clock) until all carry this call's tag: the sum over
+//     all tiles gives the expert totals, the sum over earlier tiles the rows of each
+//     expert that precede this tile.  A tag travels with each value, so neither a reset
+//     of the words nor an atomic counter is needed; the first workgroup advances the
+//     epoch once it has seen every tile's words, i.e. once every workgroup has read it.
+//  3. Expert offsets: a workgroup-wide exclusive scan built on a DPP wave scan.
+//  4. Positions: expert offset + rows in earlier tiles + rows in earlier waves + the rank
+//     kept from step 1 (read-only LDS lookups, no dependency between rounds).  Runs of
+//     more than kLayoutRankCache rounds (very large inputs) rank a second time instead.
 #include "ep_internal.h"
+
+#include <mutex>
 
 namespace ep {
 namespace {
@@ -51,123 +58,242 @@ __device__ __forceinline__ int wave_inclusive_scan(int v) {
     return v;
 }
 
-// The routing ids of this wave's run, one register per round of 64 entries.
-__device__ __forceinline__ void load_ids(const int32_t *__restrict__ idx, int64_t slots,
-                                         int64_t run_begin, int lane, int (&ids)[kLayoutRounds]) {
-#pragma unroll
-    for (int r = 0; r < kLayoutRounds; ++r) {
-        const int64_t i = run_begin + r * kWave + lane;
-        ids[r] = i < slots ? idx[i] : -1;
-    }
+__device__ __forceinline__ uint64_t load_word(const uint64_t *p) {
+    return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void store_word(uint64_t *p, uint64_t v) {
+    __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
-// Adds this wave's per-expert counts of its run to cnt[0..E) (LDS row owned by the wave).
-__device__ __forceinline__ void wave_count(const int (&ids)[kLayoutRounds], int64_t slots,
-                                           int64_t run_begin, int lane, int E, int nbits,
-                                           int *cnt) {
-#pragma unroll
-    for (int r = 0; r < kLayoutRounds; ++r) {
-        const int64_t round_begin = run_begin + r * kWave;
-        if (round_begin >= slots)
-            break;
-        const int e = ids[r];
-        const bool valid = round_begin + lane < slots && (unsigned)e < (unsigned)E;
-        const uint64_t m = match_expert(e, valid, nbits);
-        if (valid && lanes_below(m) == 0)
-            cnt[e] += __popcll(m);
+// Does entry i (expert e, slot jslot of its token row) repeat an expert named by an
+// earlier slot of the same row?  m: lanes of this round with the same valid expert;
+// earlier: the ids of the 64 entries before this round (rows that straddle rounds).
+// Every lane must call it (the shuffles read other lanes).
+__device__ __forceinline__ bool repeats_in_row(const LayoutArgs &a, int e, bool valid, uint64_t m,
+                                               int earlier, int64_t i, int lane, int jslot) {
+    const int k = a.k;
+    if (kWave % k == 0) {
+        // rounds start at multiples of 64, so a row's k entries are k neighbouring lanes
+        const uint64_t row = (k == kWave ? ~0ull : ((1ull << k) - 1)) << (lane - jslot);
+        return valid && __popcll(m & row) > 1;
     }
-}
-
-template <int W>
-__global__ __launch_bounds__(W * 64) void layout_histogram_kernel(LayoutArgs a) {
-    constexpr int kThreads = W * kWave;
-    extern __shared__ int lds[];  // [W][E]
-    const int tid = threadIdx.x, lane = tid & (kWave - 1), w = tid / kWave;
-    const int E = a.E;
-    const int64_t run_begin = (int64_t)blockIdx.x * layout_tile_slots(W) + (int64_t)w * kLayoutRounds * kWave;
-    int ids[kLayoutRounds];
-    load_ids(a.topk_idx, a.slots, run_begin, lane, ids);
-    for (int i = tid; i < W * E; i += kThreads)
-        lds[i] = 0;
-    if (blockIdx.x == 0 && tid == 0)
-        *a.status = 0u;  // the ranking kernel (next on the stream) records routing errors
-    __syncthreads();
-    wave_count(ids, a.slots, run_begin, lane, E, a.nbits, lds + w * E);
-    __syncthreads();
-    const int64_t tiles = gridDim.x;
-    int32_t *tot = a.tile_hist + (int64_t)blockIdx.x * E;
-    int32_t *per_wave = a.tile_hist + tiles * E + (int64_t)blockIdx.x * W * E;
-    for (int e = tid; e < E; e += kThreads) {
-        int s = 0;
-#pragma unroll
-        for (int v = 0; v < W; ++v) {
-            const int c = lds[v * E + e];
-            per_wave[v * E + e] = c;
-            s += c;
+    bool dup = false;
+    if (k <= kWave) {
+        for (int d = 1; d < k; ++d) {
+            const int src = (lane - d) & (kWave - 1);
+            const int same = __shfl(e, src);
+            const int prev = __shfl(earlier, src);
+            dup |= valid && d <= jslot && (lane >= d ? same : prev) == e;
         }
-        tot[e] = s;
+    } else if (valid) {
+        const int32_t *row = a.topk_idx + (i - jslot);
+        for (int jj = 0; jj < jslot; ++jj)
+            dup |= row[jj] == e;
     }
+    return dup;
+}
+
+// Step 1 for one round: returns the entry's rank among this wave's entries of its expert
+// so far (-1 when it is not a valid entry) and bumps the wave's counter row.
+__device__ __forceinline__ int count_entry(const LayoutArgs &a, int e, int earlier, int64_t i, int lane,
+                                           int jslot, int *cnt, uint32_t &err) {
+    const bool in_range = i < a.slots;
+    const bool valid = in_range && (unsigned)e < (unsigned)a.E;
+    const uint64_t m = match_expert(e, valid, a.nbits);
+    if (in_range && !valid)
+        err |= kRoutingIdOutOfRange;
+    if (repeats_in_row(a, e, valid, m, earlier, i, lane, jslot))
+        err |= kRoutingDuplicate;
+    int rank = -1;
+    if (valid) {
+        const int below = lanes_below(m);
+        const int old = cnt[e];
+        rank = old + below;
+        if (below == 0)
+            cnt[e] = old + (int)__popcll(m);
+    }
+    return rank;
+}
+
+__device__ __forceinline__ void write_position(const LayoutArgs &a, int64_t i, int pos) {
+    // positions are < T*k by construction; the check keeps every store inside the arrays
+    // even if a timed-out exchange left inconsistent totals
+    if ((uint64_t)(uint32_t)pos >= (uint64_t)a.slots)
+        pos = -1;
+    a.slot_pos[i] = pos;
+    if (pos >= 0 && a.row_src)
+        a.row_src[pos] = (int32_t)i;
+}
+
+// Step 2: sums the words every tile published -- over all tiles into tot[e], over the
+// tiles before `tile` into pre[e] -- and ORs their error bits into *err.  Each thread
+// takes one column (expert, or the error column) and a strided share of the tiles, with
+// 8 loads in flight.  Returns false if some word still lacked this call's tag after
+// timeout_ticks of the wall clock.
+template <int kThreads>
+__device__ bool gather_tiles(const LayoutArgs &a, int tiles, int tile, uint32_t want, int *tot, int *pre,
+                             int *err, int tid) {
+    const int cols = a.E + 1;
+    const int groups = kThreads / cols > 0 ? kThreads / cols : 1;
+    const int64_t t_start = wall_clock64();
+    bool ok = true;
+    for (int q = tid; q < cols * groups; q += kThreads) {
+        const int g = q / cols, c = q - g * cols;
+        int all = 0, before = 0;
+        for (int t0 = g; t0 < tiles; t0 += 8 * groups) {
+            uint64_t v[8];
+#pragma unroll
+            for (int u = 0; u < 8; ++u) {
+                const int t = t0 + u * groups;
+                v[u] = t < tiles ? load_word(a.tile_words + (int64_t)t * cols + c) : (uint64_t)want << 32;
+            }
+#pragma unroll
+            for (int u = 0; u < 8; ++u) {
+                const int t = t0 + u * groups;
+                while (ok && (uint32_t)(v[u] >> 32) != want) {
+                    if (wall_clock64() - t_start > a.timeout_ticks) {
+                        ok = false;
+                    } else {
+                        __builtin_amdgcn_s_sleep(2);
+                        v[u] = load_word(a.tile_words + (int64_t)t * cols + c);
+                    }
+                }
+                const int n = (int)(uint32_t)v[u];
+                if (t < tiles) {
+                    if (c < cols - 1) {
+                        all += n;
+                        before += t < tile ? n : 0;
+                    } else {
+                        all |= n;
+                    }
+                }
+            }
+        }
+        if (c < cols - 1) {
+            atomicAdd(&tot[c], all);
+            atomicAdd(&pre[c], before);
+        } else {
+            atomicOr(err, all);
+        }
+    }
+    return ok;
 }
 
 template <int W>
-__global__ __launch_bounds__(W * 64) void layout_rank_kernel(LayoutArgs a, int32_t tiles) {
+__global__ __launch_bounds__(W * 64) void layout_kernel(LayoutArgs a, int32_t rounds, int32_t tiles) {
     constexpr int kThreads = W * kWave;
     extern __shared__ int lds[];
     const int E = a.E;
-    int *wave_cnt = lds;            // [W][E]: counts, then running bases
+    int *wave_cnt = lds;            // [W][E]: per-wave counts, then per-wave first rows
     int *offs = wave_cnt + W * E;   // [E+1] exclusive expert offsets
     int *tot = offs + E + 1;        // [E] rows per expert over all tiles
     int *pre = tot + E;             // [E] rows per expert in earlier tiles
     int *wave_sum = pre + E;        // [W] scan carries
+    int *flags = wave_sum + W;      // [0] this tile's error bits [1] all tiles' [2] timed out
     const int tid = threadIdx.x, lane = tid & (kWave - 1), w = tid / kWave;
-    const int64_t tile = blockIdx.x;
+    const int tile = blockIdx.x;
+    const int64_t run_begin = ((int64_t)tile * W + w) * rounds * kWave;
+    const bool cached = rounds <= kLayoutRankCache;
 
-    // every global read is issued up front: this wave's ids, the 64 ids before its run
-    // (for the duplicate check), and with several tiles the histogram of the first pass
-    const int64_t run_begin = tile * layout_tile_slots(W) + (int64_t)w * kLayoutRounds * kWave;
-    int ids[kLayoutRounds];
-    load_ids(a.topk_idx, a.slots, run_begin, lane, ids);
-    const int64_t halo_i = run_begin - kWave + lane;
-    const int halo = halo_i >= 0 && halo_i < a.slots ? a.topk_idx[halo_i] : -1;
-
-    // 1-2. this wave's counts, per-expert totals and rows in earlier tiles
-    if (tiles == 1) {
-        for (int i = tid; i < W * E; i += kThreads)
-            wave_cnt[i] = 0;
-        if (tid == 0)
-            *a.status = 0u;
-        __syncthreads();
-        wave_count(ids, a.slots, run_begin, lane, E, a.nbits, wave_cnt + w * E);
-        __syncthreads();
-        for (int e = tid; e < E; e += kThreads) {
-            int t = 0;
+    // every global read is issued up front: this wave's ids (cached runs), the 64 ids
+    // before its run (rows that straddle rounds), the epoch of the workspace
+    int ids[kLayoutRankCache];
+    if (cached) {
 #pragma unroll
-            for (int v = 0; v < W; ++v)
-                t += wave_cnt[v * E + e];
-            tot[e] = t;
-            pre[e] = 0;
+        for (int r = 0; r < kLayoutRankCache; ++r) {
+            const int64_t i = run_begin + r * kWave + lane;
+            ids[r] = r < rounds && i < a.slots ? a.topk_idx[i] : -1;
+        }
+    }
+    const bool aligned = kWave % a.k == 0;
+    int halo = -1;
+    if (!aligned) {
+        const int64_t h = run_begin - kWave + lane;
+        halo = h >= 0 && h < a.slots ? a.topk_idx[h] : -1;
+    }
+    const uint32_t want = tiles > 1 ? __hip_atomic_load(a.epoch, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) + 1u : 0u;
+
+    for (int i = tid; i < W * E; i += kThreads)
+        wave_cnt[i] = 0;
+    for (int i = tid; i < 2 * E; i += kThreads)
+        tot[i] = 0;  // tot and pre
+    if (tid < 3)
+        flags[tid] = 0;
+    __syncthreads();
+
+    // 1. count, rank within the wave, routing errors
+    int *cnt = wave_cnt + w * E;
+    uint32_t err = 0;
+    const int32_t step = kWave % a.k;
+    int32_t jslot = aligned ? lane % a.k : (int32_t)((run_begin + lane) % a.k);
+    int rank[kLayoutRankCache];
+    if (cached) {
+#pragma unroll
+        for (int r = 0; r < kLayoutRankCache; ++r) {
+            const int64_t round_begin = run_begin + r * kWave;
+            if (r >= rounds || round_begin >= a.slots)
+                break;
+            if (r > 0 && step) {
+                jslot += step;
+                jslot -= jslot >= a.k ? a.k : 0;
+            }
+            rank[r] = count_entry(a, ids[r], r == 0 ? halo : ids[r == 0 ? 0 : r - 1], round_begin + lane, lane,
+                                  jslot, cnt, err);
         }
     } else {
-        const int32_t *own = a.tile_hist + (int64_t)tiles * E + tile * W * E;
-        for (int i = tid; i < W * E; i += kThreads)
-            wave_cnt[i] = own[i];
-        for (int e = tid; e < E; e += kThreads) {
-            int t = 0, p = 0;
-            // batches of 16 independent loads keep the histogram reads in flight together
-            for (int64_t b0 = 0; b0 < tiles; b0 += 16) {
-                int c[16];
-#pragma unroll
-                for (int q = 0; q < 16; ++q)
-                    c[q] = b0 + q < tiles ? a.tile_hist[(b0 + q) * E + e] : 0;
-#pragma unroll
-                for (int q = 0; q < 16; ++q) {
-                    t += c[q];
-                    p += b0 + q < tile ? c[q] : 0;
-                }
+        int earlier = halo;
+        int next = run_begin + lane < a.slots ? a.topk_idx[run_begin + lane] : -1;
+        for (int r = 0; r < rounds; ++r) {
+            const int64_t round_begin = run_begin + (int64_t)r * kWave;
+            if (round_begin >= a.slots)
+                break;
+            const int e = next;
+            const int64_t ni = round_begin + kWave + lane;
+            next = r + 1 < rounds && ni < a.slots ? a.topk_idx[ni] : -1;
+            if (r > 0 && step) {
+                jslot += step;
+                jslot -= jslot >= a.k ? a.k : 0;
             }
-            tot[e] = t;
-            pre[e] = p;
+            (void)count_entry(a, e, earlier, round_begin + lane, lane, jslot, cnt, err);
+            earlier = e;
         }
+    }
+    const uint32_t wave_err = (__ballot(err & kRoutingIdOutOfRange) ? kRoutingIdOutOfRange : 0u) |
+                              (__ballot(err & kRoutingDuplicate) ? kRoutingDuplicate : 0u);
+    if (wave_err && lane == 0)
+        atomicOr(&flags[0], (int)wave_err);
+    __syncthreads();
+
+    // 2. tile totals; with several tiles, publish them and read everyone's
+    for (int e = tid; e < E; e += kThreads) {
+        int s = 0;
+#pragma unroll
+        for (int v = 0; v < W; ++v)
+            s += wave_cnt[v * E + e];
+        if (tiles > 1)
+            store_word(a.tile_words + (int64_t)tile * (E + 1) + e, (uint64_t)want << 32 | (uint32_t)s);
+        else
+            tot[e] = s;
+    }
+    bool timed_out = false;
+    if (tiles > 1) {
+        if (tid == 0)
+            store_word(a.tile_words + (int64_t)tile * (E + 1) + E, (uint64_t)want << 32 | (uint32_t)flags[0]);
+        if (!gather_tiles<kThreads>(a, tiles, tile, want, tot, pre, &flags[1], tid))
+            flags[2] = 1;
+        __syncthreads();
+        timed_out = flags[2] != 0;
+    } else if (tid == 0) {
+        flags[1] = flags[0];
+    }
+    if (timed_out) {
+        // the totals are incomplete: report it, and give this tile's entries no row
+        if (tid == 0)
+            __hip_atomic_fetch_or(a.timed_out, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        for (int64_t i = run_begin + lane, end = run_begin + (int64_t)rounds * kWave; i < end && i < a.slots;
+             i += kWave)
+            a.slot_pos[i] = -1;
+        return;
     }
     __syncthreads();
 
@@ -199,8 +325,8 @@ __global__ __launch_bounds__(W * 64) void layout_rank_kernel(LayoutArgs a, int32
         offs[E] = total;
     __syncthreads();
 
-    // 4. counts and offsets (first workgroup), and each wave's first row per expert
-    if (blockIdx.x == 0) {
+    // counts, offsets and status (first workgroup), and each wave's first row per expert
+    if (tile == 0) {
         for (int e = tid; e < E; e += kThreads) {
             a.expert_counts[e] = tot[e];
             a.expert_offsets[e] = offs[e];
@@ -213,6 +339,9 @@ __global__ __launch_bounds__(W * 64) void layout_rank_kernel(LayoutArgs a, int32
         if (tid == 0) {
             a.expert_offsets[E] = offs[E];
             a.rank_offsets[a.R] = offs[E];
+            *a.status = (uint32_t)flags[1];
+            if (tiles > 1)  // every workgroup has read the epoch: it published this call's tag
+                __hip_atomic_store(a.epoch, want, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         }
     }
     for (int e = tid; e < E; e += kThreads) {
@@ -226,92 +355,92 @@ __global__ __launch_bounds__(W * 64) void layout_rank_kernel(LayoutArgs a, int32
     }
     __syncthreads();
 
-    // 5. positions: running base of the expert in this wave + rank among equal lanes.
-    //    A token must name k different experts: each slot compares its id with the j
-    //    earlier slots of its row, read from neighbouring lanes (this round, or the
-    //    previous round / the 64 entries before the run for lanes near the front).
-    int *wave_base = wave_cnt + w * E;
-    bool bad_id = false, dup = false;
-    // slot index within the token row, advanced by 64 mod k per round (no division per round)
-    const int32_t step = kWave % a.k;
-    int32_t jslot = (int32_t)((run_begin + lane) % a.k);
+    // 4. positions
+    int *base = wave_cnt + w * E;
+    if (cached) {
 #pragma unroll
-    for (int r = 0; r < kLayoutRounds; ++r) {
-        const int64_t round_begin = run_begin + r * kWave;
-        if (round_begin >= a.slots)
-            break;
-        const int64_t i = round_begin + lane;
-        const bool in_range = i < a.slots;
-        const int e = ids[r];
-        const bool valid = in_range && (unsigned)e < (unsigned)E;
-        const uint64_t m = match_expert(e, valid, a.nbits);
-        const int32_t ii = (int32_t)i;
-        if (r > 0) {
-            jslot += step;
-            jslot -= jslot >= a.k ? a.k : 0;
+        for (int r = 0; r < kLayoutRankCache; ++r) {
+            const int64_t round_begin = run_begin + r * kWave;
+            if (r >= rounds || round_begin >= a.slots)
+                break;
+            const int64_t i = round_begin + lane;
+            if (i < a.slots)
+                write_position(a, i, rank[r] >= 0 ? base[ids[r]] + rank[r] : -1);
         }
-        if (a.k <= kWave) {
-            const int earlier_round = r == 0 ? halo : ids[r == 0 ? 0 : r - 1];
-            for (int d = 1; d < a.k; ++d) {
-                const int src = (lane - d) & (kWave - 1);
-                const int same = __shfl(e, src);
-                const int prev = __shfl(earlier_round, src);
-                dup |= valid && d <= jslot && (lane >= d ? same : prev) == e;
+    } else {
+        for (int r = 0; r < rounds; ++r) {
+            const int64_t round_begin = run_begin + (int64_t)r * kWave;
+            if (round_begin >= a.slots)
+                break;
+            const int64_t i = round_begin + lane;
+            const bool in_range = i < a.slots;
+            const int e = in_range ? a.topk_idx[i] : -1;
+            const bool valid = in_range && (unsigned)e < (unsigned)E;
+            const uint64_t m = match_expert(e, valid, a.nbits);
+            int pos = -1;
+            if (valid) {
+                const int below = lanes_below(m);
+                const int b = base[e];
+                pos = b + below;
+                if (below == 0)
+                    base[e] = b + (int)__popcll(m);
             }
-        } else if (valid) {
-            const int32_t *row = a.topk_idx + (ii - jslot);
-            for (int32_t jj = 0; jj < jslot; ++jj)
-                dup |= row[jj] == e;
-        }
-        int pos = -1;
-        if (valid) {
-            const int below = lanes_below(m);
-            const int b = wave_base[e];
-            pos = b + below;
-            if (below == 0)
-                wave_base[e] = b + __popcll(m);
-        }
-        bad_id |= in_range && !valid;
-        if (in_range) {
-            a.slot_pos[i] = pos;
-            if (valid && a.row_src)
-                a.row_src[pos] = (int32_t)i;
+            if (in_range)
+                write_position(a, i, pos);
         }
     }
-    const uint32_t err = (__ballot(bad_id) ? kRoutingIdOutOfRange : 0u) |
-                         (__ballot(dup) ? kRoutingDuplicate : 0u);
-    if (err && lane == 0)
-        atomicOr(a.status, err);
+}
+
+// Compute units and wall-clock rate of a device, read once.
+struct DeviceInfo {
+    int cus = 0;
+    int64_t wall_khz = 0;
+};
+DeviceInfo device_info(int dev) {
+    static std::mutex mu;
+    static DeviceInfo cache[64];
+    std::lock_guard<std::mutex> lock(mu);
+    if (dev < 0 || dev >= 64)
+        return {};
+    DeviceInfo &d = cache[dev];
+    if (d.cus == 0) {
+        int cus = 0, khz = 0;
+        if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+            hipDeviceGetAttribute(&khz, hipDeviceAttributeWallClockRate, dev) != hipSuccess)
+            return {};
+        d.cus = cus;
+        d.wall_khz = khz > 0 ? khz : 100000;
+    }
+    return d;
 }
 
 template <int W>
-hipError_t launch_layout_w(const LayoutArgs &a, hipStream_t stream) {
-    const int64_t tiles = std::max<int64_t>(1, layout_tiles(a.slots, a.E));
-    const size_t rank_lds = sizeof(int) * ((size_t)W * a.E + (a.E + 1) + 2 * (size_t)a.E + W);
-    if (tiles > 1) {
-        (void)hipGetLastError();  // drop an error left by an earlier, already reported call
-        TraceSlot ts = trace_acquire();
-        hipExtLaunchKernelGGL(layout_histogram_kernel<W>, dim3((unsigned)tiles), dim3(W * kWave),
-                              (uint32_t)(sizeof(int) * W * a.E), stream, ts.start, ts.stop, 0, a);
-        hipError_t err = hipGetLastError();
-        if (err != hipSuccess)
-            return err;
-        trace_submit("layout_histogram", ts);
-    }
-    (void)hipGetLastError();
+hipError_t launch_layout_w(LayoutArgs a, const LayoutGeom &g, hipStream_t stream) {
+    const size_t lds = sizeof(int) * ((size_t)W * a.E + (a.E + 1) + 2 * (size_t)a.E + W + 3);
+    (void)hipGetLastError();  // drop an error left by an earlier, already reported call
     TraceSlot ts = trace_acquire();
-    hipExtLaunchKernelGGL(layout_rank_kernel<W>, dim3((unsigned)tiles), dim3(W * kWave), (uint32_t)rank_lds,
-                          stream, ts.start, ts.stop, 0, a, (int32_t)tiles);
+    hipExtLaunchKernelGGL(layout_kernel<W>, dim3((unsigned)g.tiles), dim3(W * kWave), (uint32_t)lds, stream,
+                          ts.start, ts.stop, 0, a, (int32_t)g.rounds, (int32_t)g.tiles);
     hipError_t err = hipGetLastError();
     if (err == hipSuccess)
-        trace_submit("layout_rank", ts);
+        trace_submit("layout", ts);
     return err;
 }
 
 }  // namespace
 
-hipError_t launch_layout(const LayoutArgs &a, hipStream_t stream) {
-    return layout_waves(a.E) == 16 ? launch_layout_w<16>(a, stream) : launch_layout_w<4>(a, stream);
+hipError_t launch_layout(LayoutArgs a, hipStream_t stream) {
+    int dev = 0;
+    hipError_t err = hipGetDevice(&dev);
+    if (err != hipSuccess)
+        return err;
+    const DeviceInfo info = device_info(dev);
+    if (info.cus <= 0)
+        return hipErrorInvalidDevice;
+    // one workgroup per compute unit at most: all of them fit on the device at once
+    const LayoutGeom g = layout_geometry(a.slots, a.E, std::min<int64_t>(kLayoutMaxTiles, info.cus));
+    a.timeout_ticks = info.wall_khz * 1000;  // one second
+    return g.waves == 16 ? launch_layout_w<16>(a, g, stream) : launch_layout_w<4>(a, g, stream);
 }
 
 }  // namespace ep

@@ -56,9 +56,11 @@ def test_status_names(lib):
 def test_workspace_bytes(lib):
     n = ctypes.c_size_t()
     assert lib.ep_layout_workspace_bytes(128, 2, 16, ctypes.byref(n)) == 0
-    assert n.value == 256                           # one tile: status word only
+    assert n.value == 256                           # one tile: header only
+    assert lib.ep_layout_workspace_bytes(4096, 2, 8, ctypes.byref(n)) == 0
+    assert n.value == 256 + 32 * 9 * 8              # 32 tiles of 4 x 64 entries: 8 totals + error word
     assert lib.ep_layout_workspace_bytes(32768, 8, 256, ctypes.byref(n)) == 0
-    assert n.value == 256 + 32 * 17 * 256 * 4       # 32 tiles of 8192 entries: totals + 16 waves' counts
+    assert n.value == 256 + 32 * 257 * 8            # 32 tiles of 16 x 8 x 64 entries
     assert lib.ep_layout_workspace_bytes(-1, 2, 16, ctypes.byref(n)) == _lib.EP_ERR_INVALID_ARG
     assert lib.ep_layout_workspace_bytes(4, 2, 4096, ctypes.byref(n)) == _lib.EP_ERR_INVALID_ARG
     assert b"bad sizes" in lib.ep_last_error()

@@ -5,13 +5,14 @@ bit.  The bf16 combine must be within max abs 2e-2 and mean abs 2e-3 of the orac
 exact (fp64) sums; element by element, the fp32 output must lie within k fp32
 roundings of the exact sum and the bf16 output within that plus one bf16 rounding, and
 at least 99% of bf16 outputs must equal the oracle's own rounding of the exact sum.
-Cases span several layout tiles (4096 routing entries each) with ragged tails, ragged
-column chunks, the four smaller workloads at full size, and degenerate routings.
+Cases span one to tens of layout tiles with ragged tails, ragged column chunks, the
+four smaller workloads at full size, and degenerate routings.
 """
 import numpy as np
 import pytest
 import torch
 
+import oracle
 import paper_2609_40093_amd as ep
 from paper_2609_40093_amd.synth import bf16_bits_to_f32
 from gpu_cases import (TOL_MAX_ABS, TOL_MEAN_ABS, bf16_ulp_distance, combine_errors, from_config,
@@ -82,17 +83,21 @@ def check_case(case):
 
 
 CASES = [
-    # name, T, H, E, k, R, routing
-    ("tiles3_ragged", 2500, 2056, 64, 8, 8, "random"),      # 20000 entries: 2 full tiles + tail; ragged chunk
-    ("tile_exact", 4096, 256, 32, 2, 4, "random"),          # exactly one tile (8192 entries)
-    ("tile_plus_one", 8193, 64, 16, 1, 2, "random"),        # one tile + one entry
-    ("many_tiles_small_rows", 40000, 8, 256, 8, 8, "skewed"),  # 40 tiles, H = 8 (one vector)
-    ("max_experts", 3000, 128, 2048, 4, 8, "random"),       # E at the kernel limit (4-wave tiles)
-    ("wide_experts_one_tile", 100, 64, 1024, 4, 8, "random"),  # 4-wave tile, single kernel
-    ("e512_two_tiles", 2000, 64, 512, 8, 8, "skewed"),      # largest E of the 16-wave tiles
+    # name, T, H, E, k, R, routing.  Layout tiles (waves x rounds x 64 entries) noted as
+    # tiles x W x rounds; several tiles exchange their totals through the workspace.
+    ("tiles3_ragged", 2500, 2056, 64, 8, 8, "random"),      # 40 x 4 x 2, ragged last tile; ragged chunk
+    ("tile_exact", 4096, 256, 32, 2, 4, "random"),          # 32 x 4 x 1, every tile full
+    ("tile_plus_one", 8193, 64, 16, 1, 2, "random"),        # 33 x 4 x 1, last tile holds one entry
+    ("many_tiles_small_rows", 40000, 8, 256, 8, 8, "skewed"),  # 40 x 16 x 8; H = 8 (one vector)
+    ("max_experts", 3000, 128, 2048, 4, 8, "random"),       # E at the kernel limit: 7 x 4 x 7
+    ("max_experts_rerank", 4096, 16, 2048, 8, 8, "skewed"),  # 7 x 4 x 19: runs too long to keep ranks
+    ("wide_experts_one_tile", 100, 64, 1024, 4, 8, "random"),  # 2 x 4 x 1
+    ("e512_sixteen_tiles", 2000, 64, 512, 8, 8, "skewed"),  # 16 x 16 x 1, largest E of 16-wave tiles
     ("one_expert", 333, 512, 1, 1, 1, "random"),
-    ("k_equals_E", 100, 1024, 6, 6, 3, "random"),
+    ("k_equals_E", 100, 1024, 6, 6, 3, "random"),           # rows straddle rounds (64 % 6 != 0)
     ("odd_E", 999, 136, 96, 5, 8, "random"),
+    ("k3_rows_straddle_tiles", 20000, 8, 40, 3, 4, "random"),  # 59 x 16 x 1, rows cross waves and tiles
+    ("k96_rows_longer_than_a_round", 300, 8, 128, 96, 8, "random"),
     ("firstk_empty_experts", 5000, 256, 128, 8, 8, "firstk"),
     ("lastk_reversed", 700, 256, 64, 4, 4, "lastk"),
     ("roundrobin", 4096, 128, 256, 8, 8, "roundrobin"),
@@ -134,13 +139,38 @@ def test_layout_deterministic():
     case = make_case("det", 60000, 8, 256, 8, 8, "skewed", seed=3)
     say("determinism x20")
     idx = torch.from_numpy(case.topk_idx).to(DEV)
-    first = None
-    for _ in range(20):
-        lay = ep.dispatch_layout(idx, case.E, case.R)
+    first, lay = None, None
+    for _ in range(20):   # one workspace: its epoch advances on every call
+        lay = ep.dispatch_layout(idx, case.E, case.R, out=lay)
         cur = torch.cat([lay.slot_pos, lay.row_src, lay.expert_offsets]).cpu().numpy()
         if first is None:
             first = cur
         assert np.array_equal(cur, first)
+    ep.layout_status(lay)
+
+
+def test_workspace_reused_across_sizes():
+    """One workspace serves calls of different tile counts in turn (the words of a
+    larger earlier call stay behind, tagged with an older epoch)."""
+    from paper_2609_40093_amd import api
+    E, R, k = 64, 8, 4
+    ws = torch.zeros(ep.workspace_bytes(20000, k, E), dtype=torch.uint8, device=DEV)
+    lib = api._lib_handle()
+    for step, T in enumerate([20000, 300, 20000, 5, 7000, 20000, 1]):
+        say(f"shared workspace step {step}: T={T}")
+        case = make_case(f"reuse{step}", T, 8, E, k, R, "skewed" if step % 2 else "random", seed=10 + step)
+        want = oracle.layout(case.topk_idx, E, R)
+        idx = torch.from_numpy(case.topk_idx).to(DEV)
+        i32 = dict(dtype=torch.int32, device=DEV)
+        outs = [torch.empty(E, **i32), torch.empty(E + 1, **i32), torch.empty(R, **i32),
+                torch.empty(R + 1, **i32), torch.empty(T * k, **i32), torch.empty(T * k, **i32)]
+        st = lib.ep_dispatch_layout(api._ptr(idx), T, k, E, R, *[api._ptr(t) for t in outs],
+                                    api._ptr(ws), ws.numel(), api._stream_ptr(None))
+        assert st == 0, lib.ep_last_error()
+        assert lib.ep_layout_status(api._ptr(ws), api._stream_ptr(None)) == 0, lib.ep_last_error()
+        for got, key in zip(outs, ("expert_counts", "expert_offsets", "rank_counts", "rank_offsets",
+                                   "slot_pos", "row_src")):
+            assert np.array_equal(got.cpu().numpy(), getattr(want, key)), f"step {step}: {key} differs"
 
 
 def test_identity_roundtrip_exact():
