@@ -54,7 +54,7 @@
 extern "C" {
 #endif
 
-#define EP_ABI_VERSION 1
+#define EP_ABI_VERSION 2
 #define EP_MAX_EXPERTS 2048 /* largest E the layout kernels accept */
 
 typedef enum {
@@ -148,6 +148,16 @@ typedef struct {
     void *host_send, *host_recv;  /* pinned host, or NULL in HBM mode */
     uint32_t *send_flags;         /* host [max_chunks], or NULL: flag c = epoch when chunk c landed */
     uint32_t *recv_flags;         /* host [num_ranks], or NULL: set to epoch by sender r */
+    /* exchange modes (ep_staging_set_mode); NULL until EP_MODE_DUPLEX allocated them */
+    uint32_t mode;
+    int32_t self_rank;
+    void *dev_in;                 /* device, buffer_bytes: rows every sender dispatched to this rank */
+    void *host_in, *host_ret;     /* pinned host, buffer_bytes: inbound rows; this rank's outbound results */
+    uint32_t *in_flags;           /* host [num_ranks]: sender r sets epoch when its inbound rows are in host_in */
+    uint32_t *ret_flags;          /* host [num_ranks]: set to epoch once the results for rank r are in host_ret */
+    uint32_t *in_landed;          /* host [num_ranks]: set to epoch once sender r's inbound rows are in dev_in */
+    uint32_t *recv_landed;        /* host [num_ranks]: set to epoch once sender r's returned rows are in dev_recv */
+    const int64_t *in_offsets;    /* host [num_ranks+1]: first dev_in/host_in row of each sender (last dispatch) */
 } ep_staging_view;
 
 /* Pointers and sizes of buffer set `buf` (host pointers are usable from the host). */
@@ -161,6 +171,38 @@ ep_status ep_staging_set_wait(ep_staging *s, int64_t timeout_us, int32_t sleep_u
  * word: EP_OK, or EP_ERR_TIMEOUT if a flag wait expired since the last call. */
 ep_status ep_staging_status(ep_staging *s, hipStream_t stream);
 
+/* Exchange modes of a PINNED_HOST staging (bit flags; 0 = the default legs above).
+ * Every mode reads the layout's rank_offsets on the host (a small device->host copy of
+ * R+1 words, the mirror) before it queues the DMA copies, since segment boundaries come
+ * from routing computed on the device (Sec. 4.5: routing-aware transfers need the
+ * routing metadata on the host); the calls then wait on the host for that mirror.
+ *   EP_MODE_PER_SENDER   combine downloads each sender's segment of returned rows as
+ *                        soon as that sender's flag arrives, on an SDMA engine of its
+ *                        own, instead of waiting for the last sender (Sec. 4.4,
+ *                        per-sender waiting policy).
+ *   EP_MODE_DUPLEX       each phase moves both PCIe directions at once (Sec. 4.3,
+ *                        full-duplex transfers on two DMA contexts): dispatch also
+ *                        downloads the rows every sender dispatched to this rank
+ *                        (host_in -> dev_in, rows per sender from ep_staging_set_inbound),
+ *                        and combine also uploads this rank's expert results for every
+ *                        sender (dev_in -> host_ret, one ret flag per destination raised
+ *                        as soon as its part is written).  The rank's own segment makes
+ *                        the round trip through host memory like any other.
+ *   EP_MODE_REMOTE_ONLY  (with DUPLEX) the rank's own segment never crosses PCIe: it is
+ *                        copied inside HBM (packed -> dev_in, dev_in -> recv).
+ * self_rank: the rank this GPU plays (0..R-1).  Requires R <= 63.  Allocates host_in,
+ * dev_in and host_ret on first use of DUPLEX. */
+#define EP_MODE_PER_SENDER 1u
+#define EP_MODE_DUPLEX 2u
+#define EP_MODE_REMOTE_ONLY 4u
+ep_status ep_staging_set_mode(ep_staging *s, uint32_t mode, int32_t self_rank);
+
+/* Rows each sender r != self_rank dispatches to this rank in buffer set `buf` (host
+ * array of num_ranks; the self entry is ignored: it is this rank's own segment).  Used by
+ * EP_MODE_DUPLEX dispatches; the inbound rows of sender r occupy host_in/dev_in rows
+ * [in_offsets[r], in_offsets[r+1]) in rank order. */
+ep_status ep_staging_set_inbound(ep_staging *s, int32_t buf, const int64_t *rows_per_sender);
+
 /* --------------------------------------------------------------- dispatch / combine */
 
 /* Dispatch of one round (epoch) into buffer set `buf`:
@@ -171,10 +213,13 @@ ep_status ep_staging_status(ep_staging *s, hipStream_t stream);
  * chunk_bytes pieces, and after chunk c has landed send_flags[c] is set to `epoch`
  * (a 4-byte DMA copy queued behind the chunk).  `stream` waits (bounded) for the last
  * flag before later work.  Epochs should increase per
- * round (flags compare as signed 32-bit differences). */
+ * round (flags compare as signed 32-bit differences).
+ * rank_offsets: int32 [R+1] from ep_dispatch_layout; required by the exchange modes
+ * (ep_staging_set_mode), else may be NULL.  With EP_MODE_REMOTE_ONLY the chunks' flags
+ * are still all raised, but no byte of the own segment is copied. */
 ep_status ep_dispatch(const void *x_dev, int64_t num_tokens, int32_t hidden, int32_t topk,
-                      const int32_t *slot_pos, ep_staging *s, int32_t buf, uint32_t epoch,
-                      hipStream_t stream);
+                      const int32_t *slot_pos, const int32_t *rank_offsets, ep_staging *s,
+                      int32_t buf, uint32_t epoch, hipStream_t stream);
 
 /* Combine of one round from buffer set `buf`:
  *   out[t][:] = sum_{j<k} topk_w[t*k+j] * recv[slot_pos[t*k+j]][:]
@@ -184,10 +229,12 @@ ep_status ep_dispatch(const void *x_dev, int64_t num_tokens, int32_t hidden, int
  * ep_staging_set_wait) until recv_flags[r] has reached `epoch` for every sender r, then
  * moves the first T*k rows host->device (one DMA copy, ordered on `stream`).
  * topk_w: float [T][k]; out: [T][H] of out_dtype.  Slots whose slot_pos is outside
- * [0, max_rows) contribute nothing. */
+ * [0, max_rows) contribute nothing.  rank_offsets as for ep_dispatch (the exchange modes
+ * reuse the offsets read by the dispatch of the same buffer set and epoch). */
 ep_status ep_combine(ep_staging *s, int32_t buf, uint32_t epoch, const int32_t *slot_pos,
-                     const float *topk_w, int64_t num_tokens, int32_t hidden, int32_t topk,
-                     void *out_dev, ep_out_dtype out_dtype, hipStream_t stream);
+                     const int32_t *rank_offsets, const float *topk_w, int64_t num_tokens,
+                     int32_t hidden, int32_t topk, void *out_dev, ep_out_dtype out_dtype,
+                     hipStream_t stream);
 
 /* ------------------------------------------------------------------ measurement */
 
@@ -207,6 +254,12 @@ ep_status ep_trace_reset(void);
 /* A plain streaming copy kernel (16-byte vectors): the attainable-bandwidth probe and
  * the calibration for hardware byte counters.  bytes must be a multiple of 16. */
 ep_status ep_copy_probe(void *dst_dev, const void *src_dev, size_t bytes, hipStream_t stream);
+
+/* PCIe probe on the SDMA engines the exchange uses: `dirs` bit 0 moves `bytes`
+ * device->host (dev -> host), bit 1 host->device (host + bytes -> dev + bytes), both
+ * bits at once on two engines.  host: pinned, dev: device, 2*bytes each.  Blocks; writes
+ * the host-timed aggregate rate in GB/s (1e9 B/s) to *gbps. */
+ep_status ep_pcie_probe(void *host, void *dev, size_t bytes, int32_t dirs, double *gbps);
 
 /* hipMemcpyAsync(kind = default) passthrough for bindings that hold raw pointers. */
 ep_status ep_memcpy(void *dst, const void *src, size_t bytes, hipStream_t stream);

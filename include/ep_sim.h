@@ -5,12 +5,16 @@
  * host thread stands in for them on the host side of the staging, where the paper's
  * peers meet (Sec. 4.2: pinned host memory as the shared medium; Sec. 4.4: completion
  * flags in host memory).  For every posted round it
+ *   0. with EP_MODE_DUPLEX, announces every other sender's inbound rows (which the
+ *      harness wrote into host_in beforehand): in_flags[r] = epoch, inbound_us[r] after
+ *      the post, in order of those delays,
  *   1. waits until the send flag of the round's last DMA chunk holds the round's epoch
  *      (chunks land in order, so every packed row is then in the host send buffer),
  *   2. in ECHO mode copies the host send buffer to the host recv buffer (every expert
  *      is the identity), otherwise leaves the recv buffer as the harness filled it,
- *   3. optionally sleeps delay_us (emulating the peers' expert computation), then
- *   4. sets every sender's recv flag to the epoch, releasing this rank's combine.
+ *   3. waits delay_us (emulating the peers' expert computation), then
+ *   4. sets each sender's recv flag to the epoch, sender r return_us[r] later than that
+ *      (skewed senders), releasing this rank's combine.
  * The thread polls with a pause instruction and gives up on a round after 60 s, which
  * ep_sim_peers_drain then reports as EP_ERR_TIMEOUT.
  */
@@ -32,6 +36,9 @@ ep_status ep_sim_peers_start(ep_staging *s, ep_sim_mode mode, ep_sim_peers **out
 /* Queues one round: `rows` packed rows were dispatched into buffer `buf` with `epoch`. */
 ep_status ep_sim_peers_post(ep_sim_peers *p, int32_t buf, uint32_t epoch, int64_t rows,
                             int64_t delay_us);
+/* Per-sender delays in microseconds, arrays of num_ranks (NULL = all zero), used by the
+ * rounds posted after this call (steps 0 and 4 above). */
+ep_status ep_sim_peers_set_delays(ep_sim_peers *p, const int64_t *inbound_us, const int64_t *return_us);
 /* Blocks until every posted round was answered (or timeout_ms passed). */
 ep_status ep_sim_peers_drain(ep_sim_peers *p, int64_t timeout_ms);
 /* Stops and joins the thread (pending rounds are dropped). */

@@ -14,6 +14,8 @@ EP_OK, EP_ERR_INVALID_ARG, EP_ERR_BAD_ROUTING, EP_ERR_HIP, EP_ERR_OOM, EP_ERR_TI
 EP_STAGING_HBM, EP_STAGING_PINNED_HOST = 0, 1
 EP_OUT_BF16, EP_OUT_F32 = 0, 1
 EP_SIM_FLAGS_ONLY, EP_SIM_ECHO = 0, 1
+EP_MODE_PER_SENDER, EP_MODE_DUPLEX, EP_MODE_REMOTE_ONLY = 1, 2, 4
+ABI_VERSION = 2
 EP_MAX_EXPERTS = 2048
 
 c_i32, c_i64, c_u32, c_size, c_vp = ctypes.c_int32, ctypes.c_int64, ctypes.c_uint32, ctypes.c_size_t, ctypes.c_void_p
@@ -25,7 +27,10 @@ class StagingView(ctypes.Structure):
                 ("max_rows", c_i64), ("row_bytes", c_i64), ("buffer_bytes", c_i64), ("chunk_bytes", c_i64),
                 ("max_chunks", c_i32),
                 ("dev_send", c_vp), ("dev_recv", c_vp), ("host_send", c_vp), ("host_recv", c_vp),
-                ("send_flags", c_vp), ("recv_flags", c_vp)]
+                ("send_flags", c_vp), ("recv_flags", c_vp),
+                ("mode", c_u32), ("self_rank", c_i32), ("dev_in", c_vp), ("host_in", c_vp), ("host_ret", c_vp),
+                ("in_flags", c_vp), ("ret_flags", c_vp), ("in_landed", c_vp), ("recv_landed", c_vp),
+                ("in_offsets", c_vp)]
 
 
 class TraceStat(ctypes.Structure):
@@ -47,15 +52,19 @@ SIGNATURES = {
     "ep_staging_get": (c_i32, [c_vp, c_i32, ctypes.POINTER(StagingView)]),
     "ep_staging_set_wait": (c_i32, [c_vp, c_i64, c_i32]),
     "ep_staging_status": (c_i32, [c_vp, c_vp]),
-    "ep_dispatch": (c_i32, [c_vp, c_i64, c_i32, c_i32, c_vp, c_vp, c_i32, c_u32, c_vp]),
-    "ep_combine": (c_i32, [c_vp, c_i32, c_u32, c_vp, c_vp, c_i64, c_i32, c_i32, c_vp, c_i32, c_vp]),
+    "ep_staging_set_mode": (c_i32, [c_vp, c_u32, c_i32]),
+    "ep_staging_set_inbound": (c_i32, [c_vp, c_i32, ctypes.POINTER(c_i64)]),
+    "ep_dispatch": (c_i32, [c_vp, c_i64, c_i32, c_i32, c_vp, c_vp, c_vp, c_i32, c_u32, c_vp]),
+    "ep_combine": (c_i32, [c_vp, c_i32, c_u32, c_vp, c_vp, c_vp, c_i64, c_i32, c_i32, c_vp, c_i32, c_vp]),
     "ep_trace_enable": (c_i32, [c_i32]),
     "ep_trace_read": (c_i32, [ctypes.POINTER(TraceStat), c_i32, ctypes.POINTER(c_i32)]),
     "ep_trace_reset": (c_i32, []),
     "ep_copy_probe": (c_i32, [c_vp, c_vp, c_size, c_vp]),
     "ep_memcpy": (c_i32, [c_vp, c_vp, c_size, c_vp]),
+    "ep_pcie_probe": (c_i32, [c_vp, c_vp, c_size, c_i32, ctypes.POINTER(ctypes.c_double)]),
     "ep_sim_peers_start": (c_i32, [c_vp, c_i32, ctypes.POINTER(c_vp)]),
     "ep_sim_peers_post": (c_i32, [c_vp, c_i32, c_u32, c_i64, c_i64]),
+    "ep_sim_peers_set_delays": (c_i32, [c_vp, ctypes.POINTER(c_i64), ctypes.POINTER(c_i64)]),
     "ep_sim_peers_drain": (c_i32, [c_vp, c_i64]),
     "ep_sim_peers_stop": (c_i32, [c_vp]),
 }
@@ -75,7 +84,7 @@ def load(path: str = LIB_PATH):
         fn = getattr(lib, name)
         fn.restype = res
         fn.argtypes = args
-    if lib.ep_abi_version() != 1:
+    if lib.ep_abi_version() != ABI_VERSION:
         raise RuntimeError("libep.so ABI version mismatch")
     if path == LIB_PATH:
         _lib = lib

@@ -18,8 +18,11 @@ from . import _lib
 from ._lib import (EP_OK, EP_ERR_BAD_ROUTING, EP_ERR_TIMEOUT, EP_STAGING_HBM, EP_STAGING_PINNED_HOST,
                    EP_OUT_BF16, EP_OUT_F32, EP_SIM_ECHO, EP_SIM_FLAGS_ONLY)
 
+MODE_PER_SENDER, MODE_DUPLEX, MODE_REMOTE_ONLY = _lib.EP_MODE_PER_SENDER, _lib.EP_MODE_DUPLEX, _lib.EP_MODE_REMOTE_ONLY
+
 __all__ = ["EPError", "Layout", "Staging", "SimPeers", "dispatch_layout", "layout_status", "dispatch",
-           "combine", "trace_enable", "trace_read", "trace_reset", "copy_probe", "workspace_bytes"]
+           "combine", "trace_enable", "trace_read", "trace_reset", "copy_probe", "workspace_bytes",
+           "pcie_probe", "MODE_PER_SENDER", "MODE_DUPLEX", "MODE_REMOTE_ONLY"]
 
 _PAYLOAD_DTYPES = (torch.bfloat16, torch.int16, torch.uint16)
 
@@ -160,39 +163,61 @@ class Staging:
         except Exception:
             pass
 
+    def set_mode(self, mode: int, self_rank: int = 0) -> None:
+        """ep_staging_set_mode: EP_MODE_* bits (per-sender, duplex, remote-only)."""
+        _check(_lib_handle().ep_staging_set_mode(self.handle, mode, self_rank), "ep_staging_set_mode")
+        self.views = [self._view(b) for b in range(self.num_buffers)]
+
+    def set_inbound(self, buf: int, rows_per_sender) -> None:
+        """ep_staging_set_inbound: rows each other sender dispatches to this rank."""
+        arr = (ctypes.c_int64 * self.num_ranks)(*[int(r) for r in rows_per_sender])
+        _check(_lib_handle().ep_staging_set_inbound(self.handle, buf, arr), "ep_staging_set_inbound")
+
     # host views (pinned staging only): zero-copy numpy arrays over pinned memory
+    _HOST_BUFFERS = {"send": "host_send", "recv": "host_recv", "in": "host_in", "ret": "host_ret"}
+    _HOST_FLAGS = {"send_flags": "send_flags", "recv_flags": "recv_flags", "in_flags": "in_flags",
+                   "ret_flags": "ret_flags", "in_landed": "in_landed", "recv_landed": "recv_landed"}
+
     def host_array(self, which: str, buf: int = 0) -> np.ndarray:
         v = self.views[buf]
-        if which in ("send", "recv"):
-            ptr = v.host_send if which == "send" else v.host_recv
+        if which in self._HOST_BUFFERS:
+            ptr = getattr(v, self._HOST_BUFFERS[which])
             if not ptr:
-                raise ValueError("host buffers exist only with pinned staging")
+                raise ValueError(f"host buffer {which!r} does not exist in this staging mode")
             return np.ctypeslib.as_array(ctypes.cast(ptr, ctypes.POINTER(ctypes.c_uint16)),
                                          shape=(self.max_rows, self.hidden))
-        if which in ("send_flags", "recv_flags"):
-            ptr = v.send_flags if which == "send_flags" else v.recv_flags
+        if which in self._HOST_FLAGS:
+            ptr = getattr(v, self._HOST_FLAGS[which])
             if not ptr:
                 raise ValueError("flags exist only with pinned staging")
             n = self.max_chunks if which == "send_flags" else self.num_ranks
             return np.ctypeslib.as_array(ctypes.cast(ptr, ctypes.POINTER(ctypes.c_uint32)), shape=(n,))
+        if which == "in_offsets":
+            return np.ctypeslib.as_array(ctypes.cast(v.in_offsets, ctypes.POINTER(ctypes.c_int64)),
+                                         shape=(self.num_ranks + 1,))
         raise ValueError(which)
 
-    def read_device(self, which: str, rows: int, buf: int = 0, stream=None) -> torch.Tensor:
-        """Copy of the first `rows` rows of the device send or recv buffer (int16 bits)."""
+    def _dev_ptr(self, which: str, buf: int):
         v = self.views[buf]
-        ptr = v.dev_send if which == "send" else v.dev_recv
+        ptr = {"send": v.dev_send, "recv": v.dev_recv, "in": v.dev_in}.get(which)
+        if not ptr:
+            raise ValueError(f"device buffer {which!r} does not exist in this staging mode")
+        return ptr
+
+    def read_device(self, which: str, rows: int, buf: int = 0, stream=None) -> torch.Tensor:
+        """Copy of the first `rows` rows of the device send, recv or in buffer (int16 bits)."""
+        ptr = self._dev_ptr(which, buf)
         out = torch.empty((rows, self.hidden), dtype=torch.int16, device="cuda")
         _check(_lib_handle().ep_memcpy(_ptr(out), ctypes.c_void_p(ptr), rows * self.row_bytes,
                                        _stream_ptr(stream)), "ep_memcpy")
         return out
 
     def write_device(self, which: str, rows: torch.Tensor, buf: int = 0, stream=None) -> None:
-        """Copies a [rows, hidden] 16-bit device tensor into the device send or recv buffer."""
+        """Copies a [rows, hidden] 16-bit device tensor into the device send, recv or in buffer."""
         _need(rows, "rows", _PAYLOAD_DTYPES, 2)
         if rows.shape[1] != self.hidden or rows.shape[0] > self.max_rows:
             raise ValueError("rows do not fit the staging buffer")
-        v = self.views[buf]
-        ptr = v.dev_send if which == "send" else v.dev_recv
+        ptr = self._dev_ptr(which, buf)
         _check(_lib_handle().ep_memcpy(ctypes.c_void_p(ptr), _ptr(rows), rows.numel() * 2, _stream_ptr(stream)),
                "ep_memcpy")
 
@@ -204,20 +229,31 @@ class Staging:
         _check(_lib_handle().ep_staging_status(self.handle, _stream_ptr(stream)), "ep_staging_status")
 
 
+def _offsets_ptr(rank_offsets: Optional[torch.Tensor], staging: "Staging"):
+    if rank_offsets is None:
+        return None
+    _need(rank_offsets, "rank_offsets", (torch.int32,), 1)
+    if rank_offsets.numel() != staging.num_ranks + 1:
+        raise ValueError("rank_offsets must hold num_ranks + 1 entries")
+    return _ptr(rank_offsets)
+
+
 def dispatch(x: torch.Tensor, slot_pos: torch.Tensor, staging: Staging, *, topk: int, buf: int = 0,
-             epoch: int = 1, stream=None) -> None:
-    """ep_dispatch: pack x [T, H] (bf16 bits) into staging buffer `buf` (and its host leg)."""
+             epoch: int = 1, rank_offsets: Optional[torch.Tensor] = None, stream=None) -> None:
+    """ep_dispatch: pack x [T, H] (bf16 bits) into staging buffer `buf` (and its host leg).
+    rank_offsets (the layout's, int32 [R+1]) is required by the exchange modes."""
     _need(x, "x", _PAYLOAD_DTYPES, 2)
     _need(slot_pos, "slot_pos", (torch.int32,), 1)
     T, H = x.shape
     if slot_pos.numel() != T * topk:
         raise ValueError("slot_pos must hold T*topk entries")
-    _check(_lib_handle().ep_dispatch(_ptr(x), T, H, topk, _ptr(slot_pos), staging.handle, buf, epoch & 0xFFFFFFFF,
-                                     _stream_ptr(stream)), "ep_dispatch")
+    _check(_lib_handle().ep_dispatch(_ptr(x), T, H, topk, _ptr(slot_pos), _offsets_ptr(rank_offsets, staging),
+                                     staging.handle, buf, epoch & 0xFFFFFFFF, _stream_ptr(stream)), "ep_dispatch")
 
 
 def combine(staging: Staging, slot_pos: torch.Tensor, topk_w: torch.Tensor, *, out: Optional[torch.Tensor] = None,
-            out_dtype: torch.dtype = torch.bfloat16, buf: int = 0, epoch: int = 1, stream=None) -> torch.Tensor:
+            out_dtype: torch.dtype = torch.bfloat16, buf: int = 0, epoch: int = 1,
+            rank_offsets: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
     """ep_combine: out [T, H] = sum_j w[t, j] * recv[slot_pos[t*k + j]] (fp32 accumulate)."""
     _need(topk_w, "topk_w", (torch.float32,), 2)
     _need(slot_pos, "slot_pos", (torch.int32,), 1)
@@ -234,7 +270,8 @@ def combine(staging: Staging, slot_pos: torch.Tensor, topk_w: torch.Tensor, *, o
     _need(out, "out", (out.dtype,), 2)
     if tuple(out.shape) != (T, H) or slot_pos.numel() != T * k:
         raise ValueError("shape mismatch between out, topk_w and slot_pos")
-    _check(_lib_handle().ep_combine(staging.handle, buf, epoch & 0xFFFFFFFF, _ptr(slot_pos), _ptr(topk_w), T, H, k,
+    _check(_lib_handle().ep_combine(staging.handle, buf, epoch & 0xFFFFFFFF, _ptr(slot_pos),
+                                    _offsets_ptr(rank_offsets, staging), _ptr(topk_w), T, H, k,
                                     _ptr(out), code, _stream_ptr(stream)), "ep_combine")
     return out
 
@@ -252,6 +289,15 @@ class SimPeers:
     def post(self, buf: int, epoch: int, rows: int, delay_us: int = 0) -> None:
         _check(_lib_handle().ep_sim_peers_post(self.handle, buf, epoch & 0xFFFFFFFF, rows, delay_us),
                "ep_sim_peers_post")
+
+    def set_delays(self, inbound_us=None, return_us=None) -> None:
+        """Per-sender delays (microseconds) for rounds posted from now on."""
+        R = self.staging.num_ranks
+
+        def arr(v):
+            return None if v is None else (ctypes.c_int64 * R)(*[int(t) for t in v])
+        _check(_lib_handle().ep_sim_peers_set_delays(self.handle, arr(inbound_us), arr(return_us)),
+               "ep_sim_peers_set_delays")
 
     def drain(self, timeout_ms: int = 60000) -> None:
         _check(_lib_handle().ep_sim_peers_drain(self.handle, timeout_ms), "ep_sim_peers_drain")
@@ -295,3 +341,13 @@ def copy_probe(dst: torch.Tensor, src: torch.Tensor, stream=None) -> None:
     if dst.numel() * dst.element_size() < nbytes:
         raise ValueError("dst smaller than src")
     _check(_lib_handle().ep_copy_probe(_ptr(dst), _ptr(src), nbytes, _stream_ptr(stream)), "ep_copy_probe")
+
+
+def pcie_probe(host: torch.Tensor, dev: torch.Tensor, nbytes: int, dirs: int) -> float:
+    """ep_pcie_probe: GB/s over PCIe on the exchange's SDMA engines (dirs: 1 = device->host,
+    2 = host->device, 3 = both at once).  host (pinned) and dev hold 2*nbytes each."""
+    if host.numel() * host.element_size() < 2 * nbytes or dev.numel() * dev.element_size() < 2 * nbytes:
+        raise ValueError("host and dev must hold 2*nbytes")
+    g = ctypes.c_double()
+    _check(_lib_handle().ep_pcie_probe(_ptr(host), _ptr(dev), nbytes, dirs, ctypes.byref(g)), "ep_pcie_probe")
+    return g.value

@@ -12,7 +12,7 @@
 // runtime's own choice of engine, kept as a measured comparison).
 #include "ep.h"
 #include "ep_internal.h"
-#include "sdma.h"
+#include "staging.h"
 
 #include <algorithm>
 #include <atomic>
@@ -26,8 +26,10 @@
 #include <vector>
 
 namespace {
-
 thread_local std::string g_last_error;
+}  // namespace
+
+namespace ep {
 
 ep_status fail(ep_status st, const char *fmt, ...) {
     char buf[512];
@@ -45,22 +47,6 @@ ep_status hip_fail(hipError_t e, const char *what) {
                 hipGetErrorString(e), (int)e);
 }
 
-#define EP_HIP(call)                                                                                \
-    do {                                                                                            \
-        hipError_t e_ = (call);                                                                     \
-        if (e_ != hipSuccess)                                                                       \
-            return hip_fail(e_, #call);                                                             \
-    } while (0)
-
-bool aligned16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
-
-constexpr int kMaxBuffers = 8;
-constexpr int64_t kDefaultChunk = 64ll << 20;
-constexpr size_t kEpochStride = 64;  // one device epoch word per buffer set, 64 B apart
-
-constexpr int kSdmaSlots = 4;        // device->host rounds in flight per staging
-
-// true: the device->host leg goes through hipMemcpyAsync instead of the SDMA lane.
 bool d2h_through_hip() {
     static const bool v = [] {
         const char *e = std::getenv("EP_HOSTLEG_COPY");
@@ -69,35 +55,16 @@ bool d2h_through_hip() {
     return v;
 }
 
-}  // namespace
+}  // namespace ep
 
-struct ep_staging {
-    int device = -1;
-    ep_staging_kind kind = EP_STAGING_HBM;
-    int64_t max_rows = 0;
-    int32_t hidden = 0, num_ranks = 0, num_buffers = 0, max_chunks = 0;
-    int64_t row_bytes = 0, buffer_bytes = 0, chunk_bytes = 0;
-    void *dev_send[kMaxBuffers] = {}, *dev_recv[kMaxBuffers] = {};
-    void *host_send[kMaxBuffers] = {}, *host_recv[kMaxBuffers] = {};
-    uint32_t *flags = nullptr;  // coherent pinned: send [nbuf][max_chunks], recv [nbuf][R], status
-    size_t flag_words = 0;
-    char *dev_epoch = nullptr;  // device: the epoch of each buffer set's current round
-    ep::SdmaLane *lane = nullptr;  // device->host leg on one SDMA engine
-    hipEvent_t ev_sysrel = nullptr;  // records a system-scope release before the lane reads
-    hipStream_t up = nullptr, down = nullptr;
-    hipEvent_t ev_up_in[kMaxBuffers] = {}, ev_up_done[kMaxBuffers] = {};
-    hipEvent_t ev_down_in[kMaxBuffers] = {}, ev_down_done[kMaxBuffers] = {};
-    int64_t timeout_us = 10ll * 1000 * 1000;
-    int32_t sleep_units = 2;
-    int64_t wall_clock_khz = 100000;
-
-    uint32_t *send_flags(int b) const { return flags + (size_t)b * max_chunks; }
-    uint32_t *recv_flags(int b) const {
-        return flags + (size_t)num_buffers * max_chunks + (size_t)b * num_ranks;
-    }
-    uint32_t *status() const { return flags + (size_t)num_buffers * (max_chunks + num_ranks); }
-    uint32_t *epoch_word(int b) const { return reinterpret_cast<uint32_t *>(dev_epoch + b * kEpochStride); }
-};
+using ep::aligned16;
+using ep::d2h_through_hip;
+using ep::fail;
+using ep::hip_fail;
+using ep::kDefaultChunk;
+using ep::kEpochStride;
+using ep::kMaxBuffers;
+using ep::kSdmaSlots;
 
 // ------------------------------------------------------------------------- tracing
 
@@ -261,6 +228,9 @@ void staging_release(ep_staging *s) {
         if (s->dev_recv[b]) (void)hipFree(s->dev_recv[b]);
         if (s->host_send[b]) (void)hipHostFree(s->host_send[b]);
         if (s->host_recv[b]) (void)hipHostFree(s->host_recv[b]);
+        if (s->dev_in[b]) (void)hipFree(s->dev_in[b]);
+        if (s->host_in[b]) (void)hipHostFree(s->host_in[b]);
+        if (s->host_ret[b]) (void)hipHostFree(s->host_ret[b]);
         for (hipEvent_t e : {s->ev_up_in[b], s->ev_up_done[b], s->ev_down_in[b], s->ev_down_done[b]})
             if (e) (void)hipEventDestroy(e);
     }
@@ -268,6 +238,7 @@ void staging_release(ep_staging *s) {
         s->lane->release();
         delete s->lane;
     }
+    ep::exchange_destroy(s->xchg);
     if (s->ev_sysrel) (void)hipEventDestroy(s->ev_sysrel);
     if (s->flags) (void)hipHostFree(s->flags);
     if (s->dev_epoch) (void)hipFree(s->dev_epoch);
@@ -313,6 +284,12 @@ extern "C" ep_status ep_staging_alloc(ep_staging_kind kind, int64_t max_rows, in
     chunk = (chunk + 4095) / 4096 * 4096;
     s->chunk_bytes = chunk;
     s->max_chunks = (int32_t)std::max<int64_t>(1, (s->buffer_bytes + chunk - 1) / chunk);
+    s->rows_in.assign((size_t)num_buffers * num_ranks, 0);
+    s->off_in.assign((size_t)num_buffers * (num_ranks + 1), 0);
+    s->offs_cache.assign((size_t)num_buffers * (num_ranks + 1), 0);
+    s->offs_epoch.assign((size_t)num_buffers, 0);
+    s->offs_valid.assign((size_t)num_buffers, 0);
+    s->in_epoch.assign((size_t)num_buffers, 0);
 
 #define EP_ALLOC_HIP(call)                                                                          \
     do {                                                                                            \
@@ -338,7 +315,7 @@ extern "C" ep_status ep_staging_alloc(ep_staging_kind kind, int64_t max_rows, in
             EP_ALLOC_HIP(hipHostMalloc(&s->host_send[b], (size_t)s->buffer_bytes, hipHostMallocDefault));
             EP_ALLOC_HIP(hipHostMalloc(&s->host_recv[b], (size_t)s->buffer_bytes, hipHostMallocDefault));
         }
-        s->flag_words = (size_t)num_buffers * (s->max_chunks + num_ranks) + 1;
+        s->flag_words = ep_staging::flag_words_for(num_buffers, s->max_chunks, num_ranks);
         EP_ALLOC_HIP(hipHostMalloc((void **)&s->flags, s->flag_words * sizeof(uint32_t),
                                    hipHostMallocCoherent));
         std::memset(s->flags, 0, s->flag_words * sizeof(uint32_t));
@@ -401,6 +378,81 @@ extern "C" ep_status ep_staging_get(ep_staging *s, int32_t buf, ep_staging_view 
     v->host_recv = pinned ? s->host_recv[buf] : nullptr;
     v->send_flags = pinned ? s->send_flags(buf) : nullptr;
     v->recv_flags = pinned ? s->recv_flags(buf) : nullptr;
+    v->mode = s->mode;
+    v->self_rank = s->self_rank;
+    v->dev_in = s->dev_in[buf];
+    v->host_in = s->host_in[buf];
+    v->host_ret = s->host_ret[buf];
+    v->in_flags = pinned ? s->in_flags(buf) : nullptr;
+    v->ret_flags = pinned ? s->ret_flags(buf) : nullptr;
+    v->in_landed = pinned ? s->in_landed(buf) : nullptr;
+    v->recv_landed = pinned ? s->recv_landed(buf) : nullptr;
+    v->in_offsets = &s->off_in[(size_t)buf * (s->num_ranks + 1)];
+    return EP_OK;
+}
+
+extern "C" ep_status ep_staging_set_mode(ep_staging *s, uint32_t mode, int32_t self_rank) {
+    if (!s)
+        return fail(EP_ERR_INVALID_ARG, "ep_staging_set_mode: staging is NULL");
+    const uint32_t known = EP_MODE_PER_SENDER | EP_MODE_DUPLEX | EP_MODE_REMOTE_ONLY;
+    if (mode & ~known)
+        return fail(EP_ERR_INVALID_ARG, "ep_staging_set_mode: unknown mode bits 0x%x", mode & ~known);
+    if (mode && s->kind != EP_STAGING_PINNED_HOST)
+        return fail(EP_ERR_INVALID_ARG, "ep_staging_set_mode: exchange modes need a PINNED_HOST staging");
+    if ((mode & EP_MODE_REMOTE_ONLY) && !(mode & EP_MODE_DUPLEX))
+        return fail(EP_ERR_INVALID_ARG, "ep_staging_set_mode: EP_MODE_REMOTE_ONLY needs EP_MODE_DUPLEX");
+    if (mode && s->num_ranks > ep::kMaxExchangeRanks)
+        return fail(EP_ERR_INVALID_ARG, "ep_staging_set_mode: at most %d ranks in the exchange modes, have %d",
+                    ep::kMaxExchangeRanks, s->num_ranks);
+    if (self_rank < 0 || self_rank >= s->num_ranks)
+        return fail(EP_ERR_INVALID_ARG, "ep_staging_set_mode: self_rank %d outside [0, %d)", self_rank,
+                    s->num_ranks);
+    ep_status st = check_device(s, "ep_staging_set_mode");
+    if (st != EP_OK)
+        return st;
+    for (hipStream_t side : {s->up, s->down})  // no leg of the previous mode may still run
+        if (side) EP_HIP(hipStreamSynchronize(side));
+    if ((mode & EP_MODE_DUPLEX) && !s->dev_in[0]) {
+        for (int b = 0; b < s->num_buffers; ++b) {
+            hipError_t e = hipMalloc(&s->dev_in[b], (size_t)s->buffer_bytes);
+            if (e == hipSuccess)
+                e = hipHostMalloc(&s->host_in[b], (size_t)s->buffer_bytes, hipHostMallocDefault);
+            if (e == hipSuccess)
+                e = hipHostMalloc(&s->host_ret[b], (size_t)s->buffer_bytes, hipHostMallocDefault);
+            if (e != hipSuccess)
+                return hip_fail(e, "ep_staging_set_mode: duplex buffers");
+        }
+    }
+    if (mode && !s->xchg) {
+        std::string err;
+        s->xchg = ep::exchange_create(s->device, kSdmaSlots, err);
+        if (!s->xchg)
+            return fail(EP_ERR_HIP, "ep_staging_set_mode: SDMA engines: %s", err.c_str());
+    }
+    s->mode = mode;
+    s->self_rank = self_rank;
+    std::fill(s->offs_valid.begin(), s->offs_valid.end(), 0);
+    std::fill(s->in_epoch.begin(), s->in_epoch.end(), 0);
+    return EP_OK;
+}
+
+extern "C" ep_status ep_staging_set_inbound(ep_staging *s, int32_t buf, const int64_t *rows_per_sender) {
+    if (!s || !rows_per_sender)
+        return fail(EP_ERR_INVALID_ARG, "ep_staging_set_inbound: NULL argument");
+    if (buf < 0 || buf >= s->num_buffers)
+        return fail(EP_ERR_INVALID_ARG, "ep_staging_set_inbound: buffer %d of %d", buf, s->num_buffers);
+    int64_t total = 0;
+    for (int r = 0; r < s->num_ranks; ++r) {
+        if (rows_per_sender[r] < 0)
+            return fail(EP_ERR_INVALID_ARG, "ep_staging_set_inbound: negative row count for sender %d", r);
+        if (r != s->self_rank)
+            total += rows_per_sender[r];
+    }
+    if (total > s->max_rows)
+        return fail(EP_ERR_INVALID_ARG, "ep_staging_set_inbound: %lld rows from other senders exceed %lld",
+                    (long long)total, (long long)s->max_rows);
+    for (int r = 0; r < s->num_ranks; ++r)
+        s->rows_in[(size_t)buf * s->num_ranks + r] = r == s->self_rank ? 0 : rows_per_sender[r];
     return EP_OK;
 }
 
@@ -456,8 +508,8 @@ ep_status check_round(const ep_staging *s, const char *who, int64_t T, int32_t H
 }  // namespace
 
 extern "C" ep_status ep_dispatch(const void *x_dev, int64_t num_tokens, int32_t hidden, int32_t topk,
-                                 const int32_t *slot_pos, ep_staging *s, int32_t buf, uint32_t epoch,
-                                 hipStream_t stream) {
+                                 const int32_t *slot_pos, const int32_t *rank_offsets, ep_staging *s,
+                                 int32_t buf, uint32_t epoch, hipStream_t stream) {
     ep_status st = check_round(s, "ep_dispatch", num_tokens, hidden, topk, buf, slot_pos);
     if (st != EP_OK)
         return st;
@@ -465,10 +517,18 @@ extern "C" ep_status ep_dispatch(const void *x_dev, int64_t num_tokens, int32_t 
         return fail(EP_ERR_INVALID_ARG, "ep_dispatch: x must be a non-NULL 16-byte aligned pointer");
     const int64_t rows = num_tokens * topk;
     const bool pinned = s->kind == EP_STAGING_PINNED_HOST;
+    const bool exchange = pinned && s->mode != 0 && rows > 0;
+    if (exchange) {  // the offsets travel to the host while the pack runs
+        st = ep::exchange_enqueue_mirror(s, buf, epoch, rank_offsets, stream, "ep_dispatch");
+        if (st != EP_OK)
+            return st;
+    }
     EP_HIP(ep::launch_pack(x_dev, num_tokens, hidden, topk, slot_pos, s->dev_send[buf], s->max_rows,
                            pinned ? s->epoch_word(buf) : nullptr, epoch, stream));
     if (!pinned || rows == 0)
         return EP_OK;
+    if (exchange)
+        return ep::exchange_dispatch(s, buf, epoch, rows, stream);
 
     const int64_t bytes = rows * s->row_bytes;
     const int64_t chunks = (bytes + s->chunk_bytes - 1) / s->chunk_bytes;
@@ -523,8 +583,9 @@ extern "C" ep_status ep_dispatch(const void *x_dev, int64_t num_tokens, int32_t 
 }
 
 extern "C" ep_status ep_combine(ep_staging *s, int32_t buf, uint32_t epoch, const int32_t *slot_pos,
-                                const float *topk_w, int64_t num_tokens, int32_t hidden, int32_t topk,
-                                void *out_dev, ep_out_dtype out_dtype, hipStream_t stream) {
+                                const int32_t *rank_offsets, const float *topk_w, int64_t num_tokens,
+                                int32_t hidden, int32_t topk, void *out_dev, ep_out_dtype out_dtype,
+                                hipStream_t stream) {
     ep_status st = check_round(s, "ep_combine", num_tokens, hidden, topk, buf, slot_pos);
     if (st != EP_OK)
         return st;
@@ -535,7 +596,11 @@ extern "C" ep_status ep_combine(ep_staging *s, int32_t buf, uint32_t epoch, cons
     const int64_t rows = num_tokens * topk;
     if (rows == 0)
         return EP_OK;
-    if (s->kind == EP_STAGING_PINNED_HOST) {
+    if (s->kind == EP_STAGING_PINNED_HOST && s->mode != 0) {
+        st = ep::exchange_combine(s, buf, epoch, rows, rank_offsets, stream);
+        if (st != EP_OK)
+            return st;
+    } else if (s->kind == EP_STAGING_PINNED_HOST) {
         // Wait (bounded) for every sender's flag, then the host leg as one copy on the
         // caller's stream: the reduction needs every row, and a copy the runtime orders
         // inside one stream reaches the next kernel sooner than one joined from another.

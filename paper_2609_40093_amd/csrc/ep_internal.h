@@ -116,6 +116,25 @@ hipError_t launch_wait_flags(const char *name, const uint32_t *flags, int32_t n,
 // Stores 0 into *value (a DMA dependency signal) with a system-scope release.
 hipError_t launch_release_signal(int64_t *value, hipStream_t stream);
 
+// Gate over up to kMaxGate flags (see signal.hip): waits for flag[i] to hold the epoch and
+// stores 0 into release[i] (per flag) or release[0] (all = 1, after every flag).
+constexpr int kMaxGate = 64;
+struct GateArgs {
+    const uint32_t *flag[kMaxGate];
+    int64_t *release[kMaxGate];
+    int32_t n = 0;
+    int32_t all = 0;
+    uint32_t epoch = 0;
+    int32_t sleep_units = 2;
+    int64_t timeout_ticks = 0;
+    uint32_t *status = nullptr;
+};
+hipError_t launch_gate(const char *name, const GateArgs &g, hipStream_t stream);
+// Stores `epoch` into *epoch_word, then 0 into *value (a DMA start signal).
+hipError_t launch_stamp_release(uint32_t *epoch_word, uint32_t epoch, int64_t *value, hipStream_t stream);
+// Copies n int32 from device memory to host words host[0..n), then stores `epoch` in host[n].
+hipError_t launch_mirror(const int32_t *src, int32_t n, uint32_t *host, uint32_t epoch, hipStream_t stream);
+
 hipError_t launch_copy(void *dst, const void *src, size_t bytes, hipStream_t stream);
 
 }  // namespace ep

@@ -47,9 +47,9 @@ hsa_status_t visit_agent(hsa_agent_t a, void *data) {
     return HSA_STATUS_SUCCESS;
 }
 
-}  // namespace
-
-bool SdmaLane::init(int device, int slots, std::string &err) {
+// The ROCr GPU agent of HIP device `device` (matched by PCI location) and its nearest CPU
+// agent.  Takes a ROCr reference (hsa_init) that the caller drops with hsa_shut_down.
+bool find_agents(int device, hsa_agent_t &gpu, hsa_agent_t &cpu, std::string &err) {
     hsa_status_t st = hsa_init();  // the HIP runtime initialised ROCr already; adds a reference
     if (st != HSA_STATUS_SUCCESS) {
         err = hsa_text("hsa_init", st);
@@ -60,6 +60,7 @@ bool SdmaLane::init(int device, int slots, std::string &err) {
         hipDeviceGetAttribute(&dev, hipDeviceAttributePciDeviceId, device) != hipSuccess ||
         hipDeviceGetAttribute(&domain, hipDeviceAttributePciDomainId, device) != hipSuccess) {
         err = "cannot read the PCI location of the HIP device";
+        hsa_shut_down();
         return false;
     }
     AgentSearch search;
@@ -68,19 +69,37 @@ bool SdmaLane::init(int device, int slots, std::string &err) {
     hsa_iterate_agents(visit_agent, &search);
     if (!search.found) {
         err = "no ROCr GPU agent at the HIP device's PCI location";
+        hsa_shut_down();
         return false;
     }
-    gpu_ = search.gpu;
+    gpu = search.gpu;
     hsa_agent_t near{};
-    if (hsa_agent_get_info(gpu_, static_cast<hsa_agent_info_t>(HSA_AMD_AGENT_INFO_NEAREST_CPU), &near) ==
+    if (hsa_agent_get_info(gpu, static_cast<hsa_agent_info_t>(HSA_AMD_AGENT_INFO_NEAREST_CPU), &near) ==
             HSA_STATUS_SUCCESS && near.handle)
-        cpu_ = near;
+        cpu = near;
     else if (search.have_cpu)
-        cpu_ = search.first_cpu;
+        cpu = search.first_cpu;
     else {
         err = "no ROCr CPU agent";
+        hsa_shut_down();
         return false;
     }
+    return true;
+}
+
+int engine_index(uint32_t bit) {
+    int id = 0;
+    while (bit && !((bit >> id) & 1u))
+        ++id;
+    return id;
+}
+
+}  // namespace
+
+bool SdmaLane::init(int device, int slots, std::string &err) {
+    if (!find_agents(device, gpu_, cpu_, err))
+        return false;
+    hsa_status_t st;
     uint32_t avail = 0, pref = 0;
     if (hsa_amd_memory_copy_engine_status(cpu_, gpu_, &avail) != HSA_STATUS_SUCCESS)
         avail = 0;
@@ -207,6 +226,68 @@ bool SdmaLane::submit(const Round &r, void *host_dst, const void *dev_src, int64
     s.busy = true;
     s.last_flag = flags + (chunks - 1);
     s.epoch = epoch;
+    return true;
+}
+
+// ---------------------------------------------------------------------- DmaEngines
+
+bool DmaEngines::init(int device, std::string &err) {
+    if (!find_agents(device, gpu_, cpu_, err))
+        return false;
+    ready_ = true;
+    uint32_t out_avail = 0, out_pref = 0, in_avail = 0;
+    if (hsa_amd_memory_copy_engine_status(cpu_, gpu_, &out_avail) != HSA_STATUS_SUCCESS)
+        out_avail = 0;
+    if (hsa_amd_memory_get_preferred_copy_engine(cpu_, gpu_, &out_pref) != HSA_STATUS_SUCCESS)
+        out_pref = 0;
+    if (hsa_amd_memory_copy_engine_status(gpu_, cpu_, &in_avail) != HSA_STATUS_SUCCESS)
+        in_avail = 0;
+    const uint32_t pick = (out_pref & out_avail) ? (out_pref & out_avail) : out_avail;
+    out_ = pick & (~pick + 1u);
+    if (!out_) {
+        err = "no SDMA engine available for device->host copies";
+        return false;
+    }
+    for (uint32_t m = in_avail & ~out_; m; m &= m - 1)
+        in_.push_back(m & (~m + 1u));
+    char buf[96];
+    std::snprintf(buf, sizeof buf, "out sdma%d, in %d engines (masks out 0x%x in 0x%x)", engine_index(out_),
+                  (int)in_.size(), out_avail, in_avail);
+    desc_ = buf;
+    return true;
+}
+
+void DmaEngines::release() {
+    if (ready_)
+        hsa_shut_down();
+    ready_ = false;
+}
+
+bool DmaEngines::make_signal(hsa_signal_t &sig, std::string &err) {
+    hsa_status_t st = hsa_amd_signal_create(1, 0, nullptr, HSA_AMD_SIGNAL_AMD_GPU_ONLY, &sig);
+    if (st != HSA_STATUS_SUCCESS) {
+        err = hsa_text("hsa_amd_signal_create", st);
+        return false;
+    }
+    return true;
+}
+
+int64_t *DmaEngines::value_pointer(hsa_signal_t sig) {
+    volatile hsa_signal_value_t *value = nullptr;
+    if (hsa_amd_signal_value_pointer(sig, &value) != HSA_STATUS_SUCCESS)
+        return nullptr;
+    return const_cast<int64_t *>(reinterpret_cast<volatile int64_t *>(value));
+}
+
+bool DmaEngines::copy(uint32_t engine, void *dst, bool dst_host, const void *src, bool src_host, size_t len,
+                      const hsa_signal_t *deps, int ndeps, hsa_signal_t done, std::string &err) {
+    hsa_status_t st = hsa_amd_memory_async_copy_on_engine(
+        dst, dst_host ? cpu_ : gpu_, src, src_host ? cpu_ : gpu_, len, (uint32_t)ndeps, deps, done,
+        (hsa_amd_sdma_engine_id_t)engine, false);
+    if (st != HSA_STATUS_SUCCESS) {
+        err = hsa_text("SDMA copy submission", st);
+        return false;
+    }
     return true;
 }
 

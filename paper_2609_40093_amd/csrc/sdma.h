@@ -61,4 +61,36 @@ private:
     bool ready_ = false;
 };
 
+// SDMA engines of one GPU for the exchange legs (device->host and host->device), driven
+// through ROCr.  Copies run on an engine named by its id bit, after dependency signals
+// reach 0, and decrement a completion signal when they land.  One engine carries the
+// device->host direction; the host->device copies of different senders go to different
+// engines, so a late sender never holds up a ready one (an engine runs its queue in order).
+class DmaEngines {
+public:
+    bool init(int device, std::string &err);
+    void release();
+
+    uint32_t out_engine() const { return out_; }
+    // Engine for the i-th host->device stream of copies.
+    uint32_t in_engine(int i) const { return in_.empty() ? out_ : in_[(size_t)i % in_.size()]; }
+    int in_engines() const { return (int)in_.size(); }
+    const std::string &describe() const { return desc_; }
+
+    // A GPU-only signal with value 1 (the device stores 0 into it to start a copy, or a
+    // copy decrements it when it lands).
+    bool make_signal(hsa_signal_t &sig, std::string &err);
+    static int64_t *value_pointer(hsa_signal_t sig);
+    // One copy of len bytes; dst_host / src_host say which side is pinned host memory.
+    bool copy(uint32_t engine, void *dst, bool dst_host, const void *src, bool src_host, size_t len,
+              const hsa_signal_t *deps, int ndeps, hsa_signal_t done, std::string &err);
+
+private:
+    hsa_agent_t gpu_{}, cpu_{};
+    uint32_t out_ = 0;
+    std::vector<uint32_t> in_;
+    std::string desc_;
+    bool ready_ = false;
+};
+
 }  // namespace ep

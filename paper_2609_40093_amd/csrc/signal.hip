@@ -44,7 +44,97 @@ __global__ __launch_bounds__(64) void release_signal_kernel(int64_t *value) {
         __hip_atomic_store(value, (int64_t)0, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_SYSTEM);
 }
 
+// Waits for a list of flags (any memory) and releases DMA copies as they arrive: lane i
+// polls flag[i] until it holds the epoch; per-flag mode then stores 0 into release[i] at
+// once (that sender's copy starts while other senders are still working), all-flags mode
+// stores 0 into release[0] when the last flag is in.  A null release only waits.  On
+// timeout every remaining release is still stored, so no queued copy waits forever; the
+// status word records the timeout.
+__global__ __launch_bounds__(64) void gate_kernel(GateArgs g) {
+    const int i = threadIdx.x;
+    bool done = i >= g.n;
+    bool released = done || g.all || !g.release[i];
+    const int64_t t0 = wall_clock64();
+    bool late = false;
+    while (!__all(done)) {
+        if (!done) {
+            const uint32_t f = __hip_atomic_load(g.flag[i], __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_SYSTEM);
+            if ((int32_t)(f - g.epoch) >= 0) {
+                done = true;
+                if (!released) {
+                    __hip_atomic_store(g.release[i], (int64_t)0, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_SYSTEM);
+                    released = true;
+                }
+            }
+        }
+        if (wall_clock64() - t0 > g.timeout_ticks) {
+            late = true;
+            break;
+        }
+        for (int32_t s = 0; s < g.sleep_units; ++s)
+            __builtin_amdgcn_s_sleep(1);
+    }
+    if (late) {
+        if (i == 0)
+            __hip_atomic_store(g.status, kStatusTimeout, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+        if (!released)
+            __hip_atomic_store(g.release[i], (int64_t)0, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_SYSTEM);
+    }
+    if (g.all && i == 0 && g.release[0])
+        __hip_atomic_store(g.release[0], (int64_t)0, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_SYSTEM);
+}
+
+// Stores the round's epoch into the word the DMA flag copies read, then releases a copy.
+__global__ __launch_bounds__(64) void stamp_release_kernel(uint32_t *epoch_word, uint32_t epoch, int64_t *value) {
+    if (threadIdx.x == 0) {
+        __hip_atomic_store(epoch_word, epoch, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+        __hip_atomic_store(value, (int64_t)0, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_SYSTEM);
+    }
+}
+
+// Copies n int32 values (rank offsets) to host memory, then the epoch as a tag after them.
+__global__ __launch_bounds__(64) void mirror_kernel(const int32_t *src, int32_t n, uint32_t *host, uint32_t epoch) {
+    if (threadIdx.x != 0)
+        return;
+    for (int i = 0; i < n; ++i)  // one thread: its release below orders every store before it
+        __hip_atomic_store(host + i, (uint32_t)src[i], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+    __hip_atomic_store(host + n, epoch, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_SYSTEM);
+}
+
 }  // namespace
+
+hipError_t launch_gate(const char *name, const GateArgs &g, hipStream_t stream) {
+    if (g.n <= 0 || g.n > kMaxGate)
+        return g.n == 0 ? hipSuccess : hipErrorInvalidValue;
+    (void)hipGetLastError();
+    TraceSlot ts = trace_acquire();
+    hipExtLaunchKernelGGL(gate_kernel, dim3(1), dim3(64), 0, stream, ts.start, ts.stop, 0, g);
+    hipError_t err = hipGetLastError();
+    if (err == hipSuccess)
+        trace_submit(name, ts);
+    return err;
+}
+
+hipError_t launch_stamp_release(uint32_t *epoch_word, uint32_t epoch, int64_t *value, hipStream_t stream) {
+    (void)hipGetLastError();
+    TraceSlot ts = trace_acquire();
+    hipExtLaunchKernelGGL(stamp_release_kernel, dim3(1), dim3(64), 0, stream, ts.start, ts.stop, 0, epoch_word,
+                          epoch, value);
+    hipError_t err = hipGetLastError();
+    if (err == hipSuccess)
+        trace_submit("release_signal", ts);
+    return err;
+}
+
+hipError_t launch_mirror(const int32_t *src, int32_t n, uint32_t *host, uint32_t epoch, hipStream_t stream) {
+    (void)hipGetLastError();
+    TraceSlot ts = trace_acquire();
+    hipExtLaunchKernelGGL(mirror_kernel, dim3(1), dim3(64), 0, stream, ts.start, ts.stop, 0, src, n, host, epoch);
+    hipError_t err = hipGetLastError();
+    if (err == hipSuccess)
+        trace_submit("mirror_offsets", ts);
+    return err;
+}
 
 hipError_t launch_release_signal(int64_t *value, hipStream_t stream) {
     (void)hipGetLastError();

@@ -11,15 +11,40 @@
 #include <deque>
 #include <mutex>
 #include <thread>
+#include <utility>
+#include <vector>
 
 namespace {
+
+using Clock = std::chrono::steady_clock;
 
 struct Round {
     int32_t buf;
     uint32_t epoch;
     int64_t rows;
     int64_t delay_us;
+    Clock::time_point posted;
+    std::vector<int64_t> inbound_us, return_us;  // per sender
 };
+
+// Sleeps until `t` (or returns false once `stop` is set).
+bool sleep_until(Clock::time_point t, const std::atomic<bool> &stop) {
+    while (Clock::now() < t) {
+        if (stop)
+            return false;
+        std::this_thread::sleep_for(std::min<Clock::duration>(t - Clock::now(), std::chrono::milliseconds(5)));
+    }
+    return true;
+}
+
+// Sender indices ordered by their delay.
+std::vector<int> by_delay(const std::vector<int64_t> &d) {
+    std::vector<int> o(d.size());
+    for (size_t i = 0; i < o.size(); ++i)
+        o[i] = (int)i;
+    std::stable_sort(o.begin(), o.end(), [&](int a, int b) { return d[(size_t)a] < d[(size_t)b]; });
+    return o;
+}
 
 constexpr int64_t kGiveUpMs = 60 * 1000;
 
@@ -32,9 +57,10 @@ struct ep_sim_peers {
     std::mutex mu;
     std::condition_variable cv, done_cv;
     std::deque<Round> q;
-    bool stop = false;
+    std::atomic<bool> stop{false};
     int64_t posted = 0, answered = 0;
     std::atomic<int> timed_out{0};
+    std::vector<int64_t> inbound_us, return_us;  // delays for rounds posted from now on
 
     void run() {
         for (;;) {
@@ -60,18 +86,27 @@ struct ep_sim_peers {
         ep_staging_view v;
         if (ep_staging_get(s, r.buf, &v) != EP_OK)
             return;
+        if ((v.mode & EP_MODE_DUPLEX) && v.in_flags) {
+            for (int i : by_delay(r.inbound_us)) {
+                if (i == v.self_rank)
+                    continue;
+                if (!sleep_until(r.posted + std::chrono::microseconds(r.inbound_us[(size_t)i]), stop))
+                    return;
+                __atomic_store_n(v.in_flags + i, r.epoch, __ATOMIC_RELEASE);
+            }
+        }
         const int64_t bytes = r.rows * v.row_bytes;
         if (bytes > 0) {
             const int64_t last = (bytes + v.chunk_bytes - 1) / v.chunk_bytes - 1;
             const uint32_t *flag = v.send_flags + last;
-            const auto t0 = std::chrono::steady_clock::now();
+            const auto t0 = Clock::now();
             uint32_t spins = 0;
             while ((int32_t)(__atomic_load_n(flag, __ATOMIC_ACQUIRE) - r.epoch) < 0) {
                 _mm_pause();
                 if (++spins % 4096 == 0) {
                     if (stop)
                         return;
-                    if (std::chrono::steady_clock::now() - t0 > std::chrono::milliseconds(kGiveUpMs)) {
+                    if (Clock::now() - t0 > std::chrono::milliseconds(kGiveUpMs)) {
                         timed_out.store(1);
                         return;
                     }
@@ -80,10 +115,12 @@ struct ep_sim_peers {
             if (mode == EP_SIM_ECHO)
                 std::memcpy(v.host_recv, v.host_send, (size_t)bytes);
         }
-        if (r.delay_us > 0)
-            std::this_thread::sleep_for(std::chrono::microseconds(r.delay_us));
-        for (int32_t i = 0; i < v.num_ranks; ++i)
+        const auto landed = Clock::now() + std::chrono::microseconds(r.delay_us);
+        for (int i : by_delay(r.return_us)) {
+            if (!sleep_until(landed + std::chrono::microseconds(r.return_us[(size_t)i]), stop))
+                return;
             __atomic_store_n(v.recv_flags + i, r.epoch, __ATOMIC_RELEASE);
+        }
     }
 };
 
@@ -110,10 +147,32 @@ extern "C" ep_status ep_sim_peers_post(ep_sim_peers *p, int32_t buf, uint32_t ep
         return EP_ERR_INVALID_ARG;
     {
         std::lock_guard<std::mutex> lk(p->mu);
-        p->q.push_back({buf, epoch, rows, delay_us});
+        Round r{buf, epoch, rows, delay_us, Clock::now(), p->inbound_us, p->return_us};
+        r.inbound_us.resize((size_t)v.num_ranks, 0);
+        r.return_us.resize((size_t)v.num_ranks, 0);
+        p->q.push_back(std::move(r));
         ++p->posted;
     }
     p->cv.notify_one();
+    return EP_OK;
+}
+
+extern "C" ep_status ep_sim_peers_set_delays(ep_sim_peers *p, const int64_t *inbound_us, const int64_t *return_us) {
+    if (!p)
+        return EP_ERR_INVALID_ARG;
+    ep_staging_view v;
+    if (ep_staging_get(p->s, 0, &v) != EP_OK)
+        return EP_ERR_INVALID_ARG;
+    std::vector<int64_t> in((size_t)v.num_ranks, 0), ret((size_t)v.num_ranks, 0);
+    for (int i = 0; i < v.num_ranks; ++i) {
+        in[(size_t)i] = inbound_us ? inbound_us[i] : 0;
+        ret[(size_t)i] = return_us ? return_us[i] : 0;
+        if (in[(size_t)i] < 0 || ret[(size_t)i] < 0)
+            return EP_ERR_INVALID_ARG;
+    }
+    std::lock_guard<std::mutex> lk(p->mu);
+    p->inbound_us = std::move(in);
+    p->return_us = std::move(ret);
     return EP_OK;
 }
 

@@ -47,7 +47,7 @@ def test_binding_covers_every_symbol():
 
 
 def test_status_names(lib):
-    assert lib.ep_abi_version() == 1
+    assert lib.ep_abi_version() == _lib.ABI_VERSION == 2
     assert lib.ep_status_name(0) == b"EP_OK"
     assert lib.ep_status_name(5) == b"EP_ERR_TIMEOUT"
     assert lib.ep_status_name(99) == b"EP_ERR_UNKNOWN"
@@ -97,8 +97,15 @@ def test_null_staging_calls(lib):
     assert lib.ep_staging_set_wait(None, 10, 1) == _lib.EP_ERR_INVALID_ARG
     assert lib.ep_staging_status(None, None) == _lib.EP_ERR_INVALID_ARG
     assert lib.ep_staging_free(None) == 0
-    assert lib.ep_dispatch(None, 4, 64, 2, None, None, 0, 1, None) == _lib.EP_ERR_INVALID_ARG
-    assert lib.ep_combine(None, 0, 1, None, None, 4, 64, 2, None, 0, None) == _lib.EP_ERR_INVALID_ARG
+    assert lib.ep_dispatch(None, 4, 64, 2, None, None, None, 0, 1, None) == _lib.EP_ERR_INVALID_ARG
+    assert lib.ep_combine(None, 0, 1, None, None, None, 4, 64, 2, None, 0, None) == _lib.EP_ERR_INVALID_ARG
+    assert lib.ep_staging_set_mode(None, 0, 0) == _lib.EP_ERR_INVALID_ARG
+    assert lib.ep_staging_set_inbound(None, 0, None) == _lib.EP_ERR_INVALID_ARG
+    g = ctypes.c_double()
+    assert lib.ep_pcie_probe(None, None, 16, 1, ctypes.byref(g)) == _lib.EP_ERR_INVALID_ARG
+    assert lib.ep_pcie_probe(ctypes.c_void_p(16), ctypes.c_void_p(16), 16, 4, ctypes.byref(g)) == \
+        _lib.EP_ERR_INVALID_ARG
+    assert lib.ep_sim_peers_set_delays(None, None, None) == _lib.EP_ERR_INVALID_ARG
     assert lib.ep_sim_peers_start(None, 0, ctypes.byref(ctypes.c_void_p())) == _lib.EP_ERR_INVALID_ARG
     assert lib.ep_sim_peers_stop(None) == 0
     assert lib.ep_copy_probe(ctypes.c_void_p(16), ctypes.c_void_p(16), 15, None) == _lib.EP_ERR_INVALID_ARG
