@@ -233,7 +233,21 @@ def main():
     print(json.dumps(result))
 
 
+PINNED_MODES = (
+    # name, mode bits (EP_MODE_*: 1 per-sender, 2 duplex, 4 remote-only)
+    ("default", 0),
+    ("per_sender", 1),
+    ("duplex", 2),
+    ("duplex_per_sender", 3),
+    ("duplex_remote_only_per_sender", 7),
+)
+
+
 def bench_pinned(cfg, inp, y, args, dev) -> dict:
+    """The same layer with pinned host staging, in each exchange mode.  Simulated peers
+    announce their rows at once (no skew).  In the duplex modes every sender r sends this
+    rank as many rows as it sends r (a symmetric traffic matrix), so each phase moves the
+    same bytes both ways; PCIe bytes per layer count both directions."""
     import numpy as np
     import torch
 
@@ -241,110 +255,118 @@ def bench_pinned(cfg, inp, y, args, dev) -> dict:
 
     T, H, E, k, R = cfg.T, cfg.H, cfg.E, cfg.k, cfg.R
     n = cfg.slots
+    rb = 2 * H
     nbuf = 2
-    st = ep.Staging("pinned", n, H, R, num_buffers=nbuf)
-    for b in range(nbuf):
-        st.host_array("recv", b)[:n] = y
-    peers = ep.SimPeers(st, echo=False)
     x = torch.from_numpy(inp.x.view(np.int16)).to(dev)
     idx = torch.from_numpy(inp.topk_idx).to(dev)
     w = torch.from_numpy(inp.topk_w).to(dev)
     out = torch.empty((T, H), dtype=torch.bfloat16, device=dev)
     lay = ep.dispatch_layout(idx, E, R)
-
-    def step(i):
-        buf, epoch = i % nbuf, i + 1
-        ep.dispatch_layout(idx, E, R, out=lay)
-        ep.dispatch(x, lay.slot_pos, st, topk=k, buf=buf, epoch=epoch)
-        peers.post(buf, epoch, n)
-        ep.combine(st, lay.slot_pos, w, out=out, buf=buf, epoch=epoch)
-
+    counts = lay.rank_counts.cpu().numpy().astype(np.int64)
+    me = 0
     steps = max(5, args.steps // 2)
-    for i in range(args.warmup):
-        step(i)
-    st.status()
-    peers.drain()
-    # timed region: untraced (events around DMA legs add markers that slow the hand-offs)
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for i in range(steps):
-        step(args.warmup + i)
-    st.status()
-    t1 = time.perf_counter()
-    peers.drain()
-    ms = (t1 - t0) * 1e3 / steps
-    # breakdown pass (not timed): every kernel and leg bracketed by events
-    ep.trace_reset()
-    ep.trace_enable(True)
-    for i in range(steps):
-        step(args.warmup + steps + i)
-    st.status()
-    peers.drain()
-    ep.trace_enable(False)
-    ks = ep.trace_read()
-    legs = {}
-    for name in ("d2h_leg", "h2d_leg", "wait_d2h", "wait_recv", "release_signal", "pack", "combine",
-                 "layout"):
-        if name in ks:
-            legs[name] = {"avg_us": round(ks[name]["mean_ms"] * 1e3, 2)}
-    pcie_bytes = n * 2 * H
-    for name in ("d2h_leg", "h2d_leg"):
-        if name in legs and legs[name]["avg_us"] > 0:
-            legs[name]["GBps"] = round(pcie_bytes / (legs[name]["avg_us"] * 1e-6) / 1e9, 2)
-    peers.close()
-    st.close()
     peaks = pcie_peaks(dev)
-    res = {
-        "us_per_layer": round(ms * 1e3, 1),
-        "payload_GBps": round(2 * cfg.payload_bytes / (ms * 1e-3) / 1e9, 2),
+    modes = {}
+    for name, mode in PINNED_MODES:
+        st = ep.Staging("pinned", n, H, R, num_buffers=nbuf)
+        if mode:
+            st.set_mode(mode, self_rank=me)
+        inbound_rows = 0
+        for b in range(nbuf):
+            st.host_array("recv", b)[:n] = y
+            if mode & ep.MODE_DUPLEX:
+                rin = counts.copy()
+                rin[me] = 0
+                st.set_inbound(b, rin)
+                inbound_rows = int(rin.sum()) + int(counts[me])
+                st.host_array("in", b)[:inbound_rows] = y[:inbound_rows]
+        peers = ep.SimPeers(st, echo=False)
+
+        def step(i):
+            buf, epoch = i % nbuf, i + 1
+            ep.dispatch_layout(idx, E, R, out=lay)
+            peers.post(buf, epoch, n)
+            ep.dispatch(x, lay.slot_pos, st, topk=k, buf=buf, epoch=epoch, rank_offsets=lay.rank_offsets)
+            ep.combine(st, lay.slot_pos, w, out=out, buf=buf, epoch=epoch, rank_offsets=lay.rank_offsets)
+
+        for i in range(args.warmup):
+            step(i)
+        st.status()
+        peers.drain()
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for i in range(steps):
+            step(args.warmup + i)
+        st.status()
+        t1 = time.perf_counter()
+        peers.drain()
+        ms = (t1 - t0) * 1e3 / steps
+        legs = {}
+        if mode == 0:
+            # breakdown pass (not timed): every kernel and leg bracketed by events
+            ep.trace_reset()
+            ep.trace_enable(True)
+            for i in range(steps):
+                step(args.warmup + steps + i)
+            st.status()
+            peers.drain()
+            ep.trace_enable(False)
+            ks = ep.trace_read()
+            for kn in ("d2h_leg", "h2d_leg", "wait_d2h", "wait_recv", "release_signal", "pack", "combine", "layout"):
+                if kn in ks:
+                    legs[kn] = {"avg_us": round(ks[kn]["mean_ms"] * 1e3, 2)}
+            for kn, key in (("d2h_leg", "d2h_alone"), ("h2d_leg", "h2d_alone")):
+                if kn in legs and legs[kn]["avg_us"] > 0:
+                    legs[kn]["GBps"] = round(n * rb / (legs[kn]["avg_us"] * 1e-6) / 1e9, 2)
+                    legs[kn]["frac_of_measured_peak"] = round(legs[kn]["GBps"] / peaks[key], 3)
+        peers.close()
+        st.close()
+        self_rows = int(counts[me]) if mode & ep.MODE_REMOTE_ONLY else 0
+        if mode & ep.MODE_DUPLEX:
+            pcie = 2 * (n - self_rows) * rb + 2 * (inbound_rows - self_rows) * rb
+            peak = peaks["both"]
+        else:
+            pcie = 2 * n * rb
+            peak = peaks["d2h_alone"]
+        gbps = pcie / (ms * 1e-3) / 1e9
+        modes[name] = {
+            "mode_bits": mode,
+            "us_per_layer": round(ms * 1e3, 1),
+            "payload_GBps": round(2 * cfg.payload_bytes / (ms * 1e-3) / 1e9, 2),
+            "pcie_bytes_per_layer": pcie,
+            "pcie_GBps": round(gbps, 2),
+            "pcie_peak_used_GBps": peak,
+            "frac_of_measured_pcie_peak": round(gbps / peak, 3),
+        }
+        if legs:
+            modes[name]["legs"] = legs
+            modes[name]["legs_note"] = "from a separate traced pass; events around DMA legs inflate their span"
+    return {
         "steps": steps,
-        "legs": legs,
-        "legs_note": "legs from a separate traced pass; events around DMA legs inflate their span",
-        "pcie_bytes_per_leg": pcie_bytes,
+        "modes": modes,
         "pcie_measured_peak_GBps": peaks,
         "pcie_published_peak_GBps": PCIE_PEAK_GBPS,
+        "note": "default and per_sender move T*k rows each way per layer (one direction per phase); "
+                "the duplex modes also move the rows other senders dispatch to this rank and this rank's "
+                "results for them (symmetric traffic), so each phase uses both PCIe directions; the "
+                "duplex peak is the two-engine bidirectional probe",
     }
-    for name, key in (("d2h_leg", "d2h_alone"), ("h2d_leg", "h2d_alone")):
-        if "GBps" in legs.get(name, {}) and peaks.get(key):
-            legs[name]["frac_of_measured_peak"] = round(legs[name]["GBps"] / peaks[key], 3)
-    return res
 
 
 def pcie_peaks(dev) -> dict:
-    """hipMemcpyAsync of 1 GiB between pinned host memory and HBM: each direction alone
-    and both together on two streams."""
+    """SDMA copies of 1 GiB between pinned host memory and HBM on the exchange's engines
+    (ep_pcie_probe): each direction alone and both at once on two engines."""
     import torch
+
+    import paper_2609_40093_amd as ep
     nbytes = 1 << 30
-    h1 = torch.empty(nbytes, dtype=torch.uint8, pin_memory=True)
-    h2 = torch.empty(nbytes, dtype=torch.uint8, pin_memory=True)
-    d1 = torch.empty(nbytes, dtype=torch.uint8, device=dev)
-    d2 = torch.empty(nbytes, dtype=torch.uint8, device=dev)
-    s1, s2 = torch.cuda.Stream(), torch.cuda.Stream()
-
-    def timed(fn, reps=3):
-        fn()
-        torch.cuda.synchronize()
-        t0 = time.perf_counter()
-        for _ in range(reps):
-            fn()
-        torch.cuda.synchronize()
-        return (time.perf_counter() - t0) / reps
-
-    def d2h():
-        with torch.cuda.stream(s1):
-            h1.copy_(d1, non_blocking=True)
-
-    def h2d():
-        with torch.cuda.stream(s2):
-            d2.copy_(h2, non_blocking=True)
-
-    def both():
-        d2h()
-        h2d()
-
-    t_d2h, t_h2d, t_both = timed(d2h), timed(h2d), timed(both)
-    return {"d2h_alone": round(nbytes / t_d2h / 1e9, 2), "h2d_alone": round(nbytes / t_h2d / 1e9, 2),
-            "bidirectional_total": round(2 * nbytes / t_both / 1e9, 2)}
+    host = torch.empty(2 * nbytes, dtype=torch.uint8, pin_memory=True)
+    devb = torch.empty(2 * nbytes, dtype=torch.uint8, device=dev)
+    res = {"d2h_alone": round(ep.pcie_probe(host, devb, nbytes, 1), 2),
+           "h2d_alone": round(ep.pcie_probe(host, devb, nbytes, 2), 2),
+           "both": round(ep.pcie_probe(host, devb, nbytes, 3), 2)}
+    del host, devb
+    return res
 
 
 def cpu_baseline(cfg, inp, y, seconds: float) -> dict:

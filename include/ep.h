@@ -176,10 +176,11 @@ ep_status ep_staging_status(ep_staging *s, hipStream_t stream);
  * R+1 words, the mirror) before it queues the DMA copies, since segment boundaries come
  * from routing computed on the device (Sec. 4.5: routing-aware transfers need the
  * routing metadata on the host); the calls then wait on the host for that mirror.
- *   EP_MODE_PER_SENDER   combine downloads each sender's segment of returned rows as
- *                        soon as that sender's flag arrives, on an SDMA engine of its
- *                        own, instead of waiting for the last sender (Sec. 4.4,
- *                        per-sender waiting policy).
+ *   EP_MODE_PER_SENDER   each sender's rows are downloaded as soon as that sender's
+ *                        flag arrives instead of after the last sender's (Sec. 4.4,
+ *                        per-sender waiting policy): a library thread watches the flags
+ *                        in host memory and queues the copies on the one host->device
+ *                        SDMA engine in arrival order.
  *   EP_MODE_DUPLEX       each phase moves both PCIe directions at once (Sec. 4.3,
  *                        full-duplex transfers on two DMA contexts): dispatch also
  *                        downloads the rows every sender dispatched to this rank

@@ -289,6 +289,7 @@ extern "C" ep_status ep_staging_alloc(ep_staging_kind kind, int64_t max_rows, in
     s->offs_cache.assign((size_t)num_buffers * (num_ranks + 1), 0);
     s->offs_epoch.assign((size_t)num_buffers, 0);
     s->offs_valid.assign((size_t)num_buffers, 0);
+    s->offs_sent.assign((size_t)num_buffers, 0);
     s->in_epoch.assign((size_t)num_buffers, 0);
 
 #define EP_ALLOC_HIP(call)                                                                          \

@@ -1,29 +1,34 @@
 // exchange.cpp -- host legs of a PINNED_HOST staging in the exchange modes
 // (EP_MODE_PER_SENDER, EP_MODE_DUPLEX, EP_MODE_REMOTE_ONLY; include/ep.h).
 //
-// Every byte crosses PCIe on an SDMA engine (Sec. 4.3: DMA offload), queued by the host
-// through ROCr with its dependencies expressed as signals, so nothing waits on the host:
+// Every byte crosses PCIe on an SDMA engine (Sec. 4.3: DMA offload), queued through ROCr
+// with its dependencies expressed as signals:
 //   - device->host copies (this rank's packed rows; in duplex mode also its results for
 //     the other ranks) run on one engine, started by a one-lane kernel on the caller's
 //     stream that stores 0 into the copies' start signal after a system-scope release;
-//   - host->device copies (rows from each sender) run one sender per engine, each gated
-//     by a one-wave kernel in which lane r polls sender r's completion flag in host
-//     memory, pausing between polls, and starts that sender's copy the moment it holds
-//     the epoch (Sec. 4.4: flags apart from the payload, one polling lane per sender,
-//     per-sender waiting policy).  In the default all-senders policy the lane that sees
-//     the last flag starts every copy at once;
+//   - host->device copies (rows from each sender) run on one other engine, so that the
+//     two PCIe directions overlap (Sec. 4.3: full-duplex transfers on two DMA contexts).
+//     A host thread (the courier) queues each sender's copy the moment that sender's
+//     completion flag in host memory holds the epoch (Sec. 4.4: flags apart from the
+//     payload, per-sender waiting policy), or all of a call's copies once the last flag
+//     is in (all-senders policy); the copies also wait for the caller's stream to release
+//     the target buffer;
 //   - each copy is followed on its engine by a 4-byte copy of the round's epoch into a
 //     flag (send chunk, landed, or returned-out), and the caller's stream waits for
-//     those flags before the reduction or the next round.
+//     those flags (one polling lane per flag, pausing between polls) before the
+//     reduction or the next round.
 // Segment boundaries are routing-dependent and computed on the device; the host reads
-// them once per round through a small mirror of rank_offsets (Sec. 4.5), which makes the
-// dispatch wait on the host until the layout of that round has run.
+// them once per round through a small mirror of rank_offsets (Sec. 4.5), which makes a
+// duplex or remote-only dispatch wait on the host until the layout of that round has run.
 #include "staging.h"
 
 #include <immintrin.h>
 
 #include <algorithm>
 #include <chrono>
+#include <condition_variable>
+#include <deque>
+#include <mutex>
 #include <thread>
 #include <utility>
 
@@ -38,18 +43,143 @@ struct XSlot {
     std::vector<std::pair<const uint32_t *, uint32_t>> finish;
 };
 
+// One host->device copy of a sender's rows: queued once *ready holds the epoch, then a
+// 4-byte copy of the epoch into *landed.
+struct InCopy {
+    const uint32_t *ready;
+    char *dst;
+    const char *src;
+    int64_t len;
+    hsa_signal_t done;
+    uint32_t *landed;
+};
+
+// The host->device copies of one call.  They all go to the one inbound engine and all
+// depend on `start`, which the caller's stream releases once the target buffer is free.
+struct InJob {
+    std::vector<InCopy> copies;
+    uint32_t epoch = 0;
+    bool per_sender = false;
+    hsa_signal_t start{};
+    const uint32_t *epoch_word = nullptr;
+    hsa_signal_t landed_done{};
+    uint32_t *status = nullptr;
+    std::chrono::steady_clock::time_point deadline;
+};
+
+// Host thread that queues inbound copies in the order their senders' flags arrive.
+// Measured on MI355X: one device->host engine next to one host->device engine fills both
+// PCIe directions (about 96 GB/s together), but host->device copies on two or more engines
+// at once pull the total down to about 61 GB/s.  So every inbound copy shares one engine,
+// and to keep a late sender from holding up ready ones queued behind it on that in-order
+// engine, a copy is queued only once its sender's flag (host memory, read without a PCIe
+// round trip) holds the epoch.  With the all-senders policy a call's copies are queued
+// together when the last flag is in.
+class Courier {
+public:
+    void start(DmaEngines *dma) {
+        dma_ = dma;
+        th_ = std::thread([this] { run(); });
+    }
+    void stop() {
+        {
+            std::lock_guard<std::mutex> lk(mu_);
+            stop_ = true;
+        }
+        cv_.notify_all();
+        if (th_.joinable())
+            th_.join();
+    }
+    void post(InJob &&j) {
+        {
+            std::lock_guard<std::mutex> lk(mu_);
+            incoming_.push_back(std::move(j));
+        }
+        cv_.notify_one();
+    }
+
+private:
+    static bool ready(const InJob &j, const InCopy &c) {
+        return (int32_t)(__atomic_load_n(c.ready, __ATOMIC_ACQUIRE) - j.epoch) >= 0;
+    }
+    bool submit(InJob &j, const InCopy &c) {
+        std::string err;
+        const uint32_t eng = dma_->in_engine(0);
+        if (dma_->copy(eng, c.dst, false, c.src, true, (size_t)c.len, &j.start, 1, c.done, err) &&
+            dma_->copy(eng, c.landed, true, j.epoch_word, false, sizeof(uint32_t), &c.done, 1, j.landed_done, err))
+            return true;
+        __atomic_store_n(j.status, (uint32_t)EP_ERR_HIP, __ATOMIC_RELEASE);
+        return false;
+    }
+    // Queues what is ready; returns true once every copy of the job is queued.
+    bool progress(InJob &j) {
+        const bool late = std::chrono::steady_clock::now() > j.deadline;
+        bool all = true;
+        if (!j.per_sender && !late)
+            for (const InCopy &c : j.copies)
+                all = all && ready(j, c);
+        for (size_t i = 0; i < j.copies.size();) {
+            if (late || (j.per_sender ? ready(j, j.copies[i]) : all)) {
+                if (late && !ready(j, j.copies[i]))
+                    __atomic_store_n(j.status, (uint32_t)EP_ERR_TIMEOUT, __ATOMIC_RELEASE);
+                submit(j, j.copies[i]);  // queued even when late, so no wait on the device hangs
+                j.copies.erase(j.copies.begin() + (std::ptrdiff_t)i);
+            } else {
+                ++i;
+            }
+        }
+        return j.copies.empty();
+    }
+    void run() {
+        std::unique_lock<std::mutex> lk(mu_);
+        for (;;) {
+            if (stop_)
+                return;
+            while (!incoming_.empty()) {
+                active_.push_back(std::move(incoming_.front()));
+                incoming_.pop_front();
+            }
+            if (active_.empty()) {
+                cv_.wait(lk, [&] { return stop_ || !incoming_.empty(); });
+                continue;
+            }
+            lk.unlock();
+            for (size_t i = 0; i < active_.size();) {
+                if (progress(active_[i]))
+                    active_.erase(active_.begin() + (std::ptrdiff_t)i);
+                else
+                    ++i;
+            }
+            for (int p = 0; p < 64; ++p)
+                _mm_pause();
+            lk.lock();
+        }
+    }
+
+    DmaEngines *dma_ = nullptr;
+    std::thread th_;
+    std::mutex mu_;
+    std::condition_variable cv_;
+    std::deque<InJob> incoming_;
+    std::vector<InJob> active_;
+    bool stop_ = false;
+};
+
 class Exchange {
 public:
     DmaEngines dma;
+    Courier courier;
 
     bool init(int device, int nslots, std::string &err) {
         if (!dma.init(device, err))
             return false;
         slots_.resize((size_t)nslots);
+        courier.start(&dma);
         return true;
     }
 
     void release() {
+        courier.stop();
         for (XSlot &s : slots_)
             for (hsa_signal_t g : s.sigs)
                 hsa_signal_destroy(g);
@@ -147,37 +277,25 @@ ep_status wait_offsets(ep_staging *s, int b, uint32_t epoch, int64_t rows, const
     return EP_OK;
 }
 
-// One host->device copy of a sender's rows, gated by `go`, then its landed flag.
-struct InCopy {
-    char *dst;
-    const char *src;
-    int64_t len;
-    hsa_signal_t go, done;
-    uint32_t engine;
-    uint32_t *landed;
-};
-
-// Launches the gate first (so no copy is ever queued behind a start signal that nothing
-// will release), then queues the copies and their landed flags.
-ep_status submit_inbound(Exchange &x, GateArgs &gate, bool per_sender, hsa_signal_t start_all,
-                         const std::vector<InCopy> &plan, const uint32_t *epoch_word, hsa_signal_t landed_done,
-                         const char *gate_name, const char *who, hipStream_t stream) {
-    if (!per_sender && gate.n > 0) {
-        gate.all = 1;
-        gate.release[0] = DmaEngines::value_pointer(start_all);
-    }
-    EP_HIP(launch_gate(gate_name, gate, stream));
-    std::string err;
-    for (const InCopy &c : plan)
-        if (!x.dma.copy(c.engine, c.dst, false, c.src, true, (size_t)c.len, &c.go, 1, c.done, err) ||
-            !x.dma.copy(c.engine, c.landed, true, epoch_word, false, sizeof(uint32_t), &c.done, 1, landed_done, err))
-            return fail(EP_ERR_HIP, "%s: %s", who, err.c_str());
-    return EP_OK;
+// Hands a call's inbound copies to the courier.
+void post_inbound(Exchange &x, const ep_staging *s, std::vector<InCopy> &&plan, uint32_t epoch, bool per_sender,
+                  hsa_signal_t start, const uint32_t *epoch_word, hsa_signal_t landed_done) {
+    if (plan.empty())
+        return;
+    InJob j;
+    j.copies = std::move(plan);
+    j.epoch = epoch;
+    j.per_sender = per_sender;
+    j.start = start;
+    j.epoch_word = epoch_word;
+    j.landed_done = landed_done;
+    j.status = s->status();
+    j.deadline = std::chrono::steady_clock::now() + std::chrono::microseconds(s->timeout_us);
+    x.courier.post(std::move(j));
 }
 
 struct Batch {
-    GateArgs gate;     // start copies on flags
-    GateArgs waits;    // flags the stream waits for afterwards
+    GateArgs waits;    // flags the stream waits for after the copies
     void add_wait(const uint32_t *flag) {
         waits.flag[waits.n] = flag;
         waits.release[waits.n] = nullptr;
@@ -206,21 +324,28 @@ ep_status exchange_enqueue_mirror(ep_staging *s, int b, uint32_t epoch, const in
                                   hipStream_t stream, const char *who) {
     if (!rank_offsets)
         return fail(EP_ERR_INVALID_ARG, "%s: the exchange modes need rank_offsets", who);
+    // a stale tag equal to this epoch would be taken for this round's offsets
+    __atomic_store_n(s->mirror(b) + s->R() + 1, epoch - 1, __ATOMIC_RELEASE);
     EP_HIP(launch_mirror(rank_offsets, s->num_ranks + 1, s->mirror(b), epoch, stream));
     s->offs_valid[(size_t)b] = 0;
+    s->offs_sent[(size_t)b] = epoch;
     return EP_OK;
 }
 
 ep_status exchange_dispatch(ep_staging *s, int b, uint32_t epoch, int64_t rows, hipStream_t stream) {
     const char *who = "ep_dispatch";
-    ep_status st = wait_offsets(s, b, epoch, rows, who);
-    if (st != EP_OK)
-        return st;
     const int R = s->num_ranks, me = s->self_rank;
     const int64_t rb = s->row_bytes;
-    const int32_t *ro = &s->offs_cache[(size_t)b * (R + 1)];
     const bool duplex = s->mode & EP_MODE_DUPLEX, remote_only = s->mode & EP_MODE_REMOTE_ONLY,
                per_sender = s->mode & EP_MODE_PER_SENDER;
+    // only the own segment's place depends on the offsets here: with neither duplex nor
+    // remote-only legs the dispatch does not wait for them (the combine will)
+    if (duplex || remote_only) {
+        ep_status st = wait_offsets(s, b, epoch, rows, who);
+        if (st != EP_OK)
+            return st;
+    }
+    const int32_t *ro = &s->offs_cache[(size_t)b * (R + 1)];
     Exchange &x = *s->xchg;
     std::string err;
 
@@ -261,7 +386,6 @@ ep_status exchange_dispatch(ep_staging *s, int b, uint32_t epoch, int64_t rows, 
         ranges.push_back({0, bytes});
     }
     Batch bt;
-    init_gate(bt.gate, s, epoch);
     init_gate(bt.waits, s, epoch);
     if (chunks > 0) {
         hsa_signal_t flags_done{};
@@ -289,18 +413,17 @@ ep_status exchange_dispatch(ep_staging *s, int b, uint32_t epoch, int64_t rows, 
         slot->finish.push_back({s->send_flags(b) + (chunks - 1), epoch});
     }
 
-    // ---- inbound (duplex): every sender's rows -> dev_in, one engine per sender
+    // ---- inbound (duplex): every sender's rows -> dev_in on the inbound engine, each
+    //      sender's copy queued when its flag arrives (the courier)
     if (duplex) {
         char *din = static_cast<char *>(s->dev_in[b]);
         char *hin = static_cast<char *>(s->host_in[b]);
         int copies = 0;
         for (int r = 0; r < R; ++r)
             copies += rin[r] > 0 && !(r == me && remote_only);
-        hsa_signal_t landed_done{}, start_all{};
-        if (copies > 0 && (!x.signal(*slot, copies, landed_done, err) ||
-                           (!per_sender && !x.signal(*slot, 1, start_all, err))))
+        hsa_signal_t landed_done{};
+        if (copies > 0 && !x.signal(*slot, copies, landed_done, err))
             return fail(EP_ERR_HIP, "%s: %s", who, err.c_str());
-        int lane = 0;
         std::vector<InCopy> plan;
         for (int r = 0; r < R; ++r) {
             if (rin[r] == 0)
@@ -314,20 +437,14 @@ ep_status exchange_dispatch(ep_staging *s, int b, uint32_t epoch, int64_t rows, 
             // own segment: back from the host send buffer once its last chunk's flag is up
             const uint32_t *ready = r == me ? s->send_flags(b) + ((ro[me + 1] * rb - 1) / chunk) : s->in_flags(b) + r;
             const char *src = r == me ? hsend + ro[me] * rb : hin + off[r] * rb;
-            hsa_signal_t go = start_all, d{};
-            if ((per_sender && !x.signal(*slot, 1, go, err)) || !x.signal(*slot, 1, d, err))
+            hsa_signal_t d{};
+            if (!x.signal(*slot, 1, d, err))
                 return fail(EP_ERR_HIP, "%s: %s", who, err.c_str());
-            bt.gate.flag[bt.gate.n] = ready;
-            bt.gate.release[bt.gate.n] = per_sender ? DmaEngines::value_pointer(go) : nullptr;
-            ++bt.gate.n;
-            plan.push_back({dst, src, len, go, d, x.dma.in_engine(lane++), s->in_landed(b) + r});
+            plan.push_back({ready, dst, src, len, d, s->in_landed(b) + r});
             bt.add_wait(s->in_landed(b) + r);
             slot->finish.push_back({s->in_landed(b) + r, epoch});
         }
-        st = submit_inbound(x, bt.gate, per_sender, start_all, plan, ew, landed_done, "gate_inbound", who,
-                            stream);
-        if (st != EP_OK)
-            return st;
+        post_inbound(x, s, std::move(plan), epoch, per_sender, start, ew, landed_done);
         s->in_epoch[(size_t)b] = epoch;
     }
     EP_HIP(launch_gate("wait_dispatch", bt.waits, stream));
@@ -339,7 +456,10 @@ ep_status exchange_combine(ep_staging *s, int b, uint32_t epoch, int64_t rows, c
     const char *who = "ep_combine";
     const int R = s->num_ranks, me = s->self_rank;
     if (!(s->offs_valid[(size_t)b] && s->offs_epoch[(size_t)b] == epoch)) {
-        ep_status st = exchange_enqueue_mirror(s, b, epoch, rank_offsets, stream, who);
+        // the dispatch of this round queued the mirror already (it ran right after the
+        // layout); otherwise queue one now
+        ep_status st = s->offs_sent[(size_t)b] == epoch ? EP_OK
+                                                         : exchange_enqueue_mirror(s, b, epoch, rank_offsets, stream, who);
         if (st == EP_OK)
             st = wait_offsets(s, b, epoch, rows, who);
         if (st != EP_OK)
@@ -376,7 +496,6 @@ ep_status exchange_combine(ep_staging *s, int b, uint32_t epoch, int64_t rows, c
     EP_HIP(hipEventRecord(s->ev_sysrel, stream));
     EP_HIP(launch_stamp_release(ew, epoch, DmaEngines::value_pointer(start), stream));
     Batch bt;
-    init_gate(bt.gate, s, epoch);
     init_gate(bt.waits, s, epoch);
 
     // ---- outbound (duplex): this rank's results for sender r's rows -> host_ret
@@ -402,15 +521,14 @@ ep_status exchange_combine(ep_staging *s, int b, uint32_t epoch, int64_t rows, c
         }
     }
 
-    // ---- inbound: sender r's returned rows for this rank's segment r -> dev_recv
+    // ---- inbound: sender r's returned rows for this rank's segment r -> dev_recv, on the
+    //      inbound engine as each sender's flag arrives (the courier)
     int copies = 0;
     for (int r = 0; r < R; ++r)
         copies += ro[r + 1] > ro[r] && !(r == me && remote_only);
-    hsa_signal_t landed_done{}, start_all{};
-    if (copies > 0 &&
-        (!x.signal(*slot, copies, landed_done, err) || (!per_sender && !x.signal(*slot, 1, start_all, err))))
+    hsa_signal_t landed_done{};
+    if (copies > 0 && !x.signal(*slot, copies, landed_done, err))
         return fail(EP_ERR_HIP, "%s: %s", who, err.c_str());
-    int lane = 0;
     std::vector<InCopy> plan;
     for (int r = 0; r < R; ++r) {
         const int64_t n = ro[r + 1] - ro[r];
@@ -424,20 +542,14 @@ ep_status exchange_combine(ep_staging *s, int b, uint32_t epoch, int64_t rows, c
         const bool own_dup = r == me && duplex;  // own results come back from host_ret
         const uint32_t *ready = own_dup ? s->ret_flags(b) + me : s->recv_flags(b) + r;
         const char *src = own_dup ? hret + off[me] * rb : hrecv + ro[r] * rb;
-        hsa_signal_t go = start_all, d{};
-        if ((per_sender && !x.signal(*slot, 1, go, err)) || !x.signal(*slot, 1, d, err))
+        hsa_signal_t d{};
+        if (!x.signal(*slot, 1, d, err))
             return fail(EP_ERR_HIP, "%s: %s", who, err.c_str());
-        bt.gate.flag[bt.gate.n] = ready;
-        bt.gate.release[bt.gate.n] = per_sender ? DmaEngines::value_pointer(go) : nullptr;
-        ++bt.gate.n;
-        plan.push_back({dst, src, n * rb, go, d, x.dma.in_engine(lane++), s->recv_landed(b) + r});
+        plan.push_back({ready, dst, src, n * rb, d, s->recv_landed(b) + r});
         bt.add_wait(s->recv_landed(b) + r);
         slot->finish.push_back({s->recv_landed(b) + r, epoch});
     }
-    ep_status st = submit_inbound(x, bt.gate, per_sender, start_all, plan, ew, landed_done, "gate_returned",
-                                  who, stream);
-    if (st != EP_OK)
-        return st;
+    post_inbound(x, s, std::move(plan), epoch, per_sender, start, ew, landed_done);
     EP_HIP(launch_gate("wait_combine", bt.waits, stream));
     return EP_OK;
 }

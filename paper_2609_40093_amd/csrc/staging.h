@@ -90,6 +90,7 @@ struct ep_staging {
     std::vector<int32_t> offs_cache;  // [nbuf][R+1] rank offsets read through the mirror
     std::vector<uint32_t> offs_epoch; // [nbuf] epoch of offs_cache (valid when offs_valid)
     std::vector<uint8_t> offs_valid;  // [nbuf]
+    std::vector<uint32_t> offs_sent;  // [nbuf] epoch of the last mirror queued (may still be in flight)
     std::vector<uint32_t> in_epoch;   // [nbuf] epoch of the last duplex dispatch (off_in valid)
     ep::Exchange *xchg = nullptr;
 
