@@ -38,6 +38,7 @@ def parse():
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--no-pinned", action="store_true")
     p.add_argument("--cpu-seconds", type=float, default=10.0)
+    p.add_argument("--chunk-mib", type=int, default=16, help="device->host DMA chunk of the pinned legs")
     return p.parse_args()
 
 
@@ -127,7 +128,7 @@ def main():
             ep.trace_enable(False)
 
     # ---- HBM staging: warmup, then exactly K timed steps; pack and combine are timed
-    #      live on alternate steps with HIP events on the stream they run on
+    #      live with HIP events on the stream they run on
     for i in range(args.warmup):
         step(i)
     ep.layout_status(sets[0]["lay"])
@@ -135,8 +136,10 @@ def main():
     ep.trace_reset()
     torch.cuda.synchronize()
     t0 = time.perf_counter()
+    # one step in four carries timing events (they cost the stream ~2 us per traced
+    # launch), alternating between pack and combine
     for i in range(args.steps):
-        step(args.warmup + i, trace="pack" if i % 2 == 0 else "combine")
+        step(args.warmup + i, trace=("pack", None, "combine", None)[i % 4])
     t_issue = time.perf_counter()
     torch.cuda.synchronize()
     t1 = time.perf_counter()
@@ -268,7 +271,7 @@ def bench_pinned(cfg, inp, y, args, dev) -> dict:
     peaks = pcie_peaks(dev)
     modes = {}
     for name, mode in PINNED_MODES:
-        st = ep.Staging("pinned", n, H, R, num_buffers=nbuf)
+        st = ep.Staging("pinned", n, H, R, num_buffers=nbuf, chunk_bytes=args.chunk_mib << 20)
         if mode:
             st.set_mode(mode, self_rank=me)
         inbound_rows = 0
@@ -343,6 +346,7 @@ def bench_pinned(cfg, inp, y, args, dev) -> dict:
             modes[name]["legs_note"] = "from a separate traced pass; events around DMA legs inflate their span"
     return {
         "steps": steps,
+        "chunk_bytes": args.chunk_mib << 20,
         "modes": modes,
         "pcie_measured_peak_GBps": peaks,
         "pcie_published_peak_GBps": PCIE_PEAK_GBPS,

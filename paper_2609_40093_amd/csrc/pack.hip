@@ -8,9 +8,10 @@
 // is wave-uniform, so the k slot positions are scalar loads; each lane loads U 16-byte
 // vectors of the row (all in flight together) and stores them to the k destination rows.
 // Consecutive lanes touch consecutive 16-byte pieces of one row: every load and store is
-// a fully coalesced 1 KiB wave access.  Which store and mapping variant is used follows
-// bandwidth measured on MI355X: plain stores for the k-row fan-out, and for rows of at
-// most 4 KiB with k >= 4 one wave per (token, chunk, slot).  Rows carry no reuse across
+// a fully coalesced 1 KiB wave access.  Loads and stores are non-temporal (the rows are
+// touched once; streaming stores leave no dirty lines for the end-of-kernel writeback).
+// Which mapping is used follows bandwidth measured on MI355X: for rows of at most 4 KiB
+// with k >= 4, one wave per (token, chunk, slot).  Rows carry no reuse across
 // workgroups, so the workgroup-to-XCD placement needs no remapping.
 #include "ep_internal.h"
 
@@ -52,7 +53,7 @@ __global__ __launch_bounds__(256) void pack_kernel(const u32x4 *__restrict__ x, 
         for (int u = 0; u < U; ++u) {
             const int32_t v = v0 + u * kWave + lane;
             if (v < V)
-                dst[v] = d[u];
+                __builtin_nontemporal_store(d[u], dst + v);
         }
     }
 }
