@@ -10,6 +10,9 @@ marshals numpy arrays.  Every function follows a passage of the paper (Lee et al
   layout  -- Sec. 4.3 grouping of tokens by expert; Sec. 4.5 routing-aware rows
   pack    -- Sec. 2.2 packing of routing-dependent rows into a contiguous region
   combine -- Sec. 4.3 reduction of a token's returned contributions on its owner
+  local_layout, block_reduce, pcie_volume -- Sec. 4.2 dense All-Gather / Reduce-Scatter:
+             receive-side grouping by local expert, the destination's sum of blocks, and
+             the per-GPU PCIe volume of each collective
 Pins (tests/test_oracle_*.py): brute force, closed forms, library routines, exact
 rational arithmetic; see the module docstrings there.
 """
@@ -57,6 +60,11 @@ def _bind(lib):
                                       ctypes.c_int32, vp, vp, vp]
     lib.ep_oracle_double_to_bf16_n.restype = None
     lib.ep_oracle_double_to_bf16_n.argtypes = [f64p, ctypes.c_int64, u16p]
+    lib.ep_oracle_local_layout.restype = ctypes.c_int
+    lib.ep_oracle_local_layout.argtypes = [i32p, ctypes.c_int64, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32,
+                                           ctypes.c_int32, i32p, i32p, i32p, vp]
+    lib.ep_oracle_block_reduce.restype = None
+    lib.ep_oracle_block_reduce.argtypes = [f64p, ctypes.c_int32, ctypes.c_int64, vp, vp, vp]
     return lib
 
 
@@ -154,3 +162,68 @@ def double_to_bf16(v: np.ndarray, lib=None) -> np.ndarray:
 def bf16_to_double(b: np.ndarray) -> np.ndarray:
     """Widen bf16 bits to float64 (exact; appends 16 zero bits)."""
     return (np.asarray(b, dtype=np.uint16).astype(np.uint32) << 16).view(np.float32).astype(np.float64)
+
+
+@dataclass
+class LocalLayout:
+    status: int
+    local_counts: np.ndarray
+    local_offsets: np.ndarray
+    slot_pos: np.ndarray
+    row_src: np.ndarray
+
+
+def local_layout(topk_idx: np.ndarray, E: int, e_lo: int, e_hi: int, lib=None) -> LocalLayout:
+    """Grouping of N gathered tokens by the local experts [e_lo, e_hi) (slot_pos -1 elsewhere)."""
+    lib = lib or load()
+    idx = np.ascontiguousarray(topk_idx, dtype=np.int32)
+    N, k = idx.shape
+    L = max(e_hi - e_lo, 1)
+    lc = np.zeros(L, np.int32)
+    lo = np.zeros(L + 1, np.int32)
+    sp = np.full(max(N * k, 1), -1, np.int32)
+    rs = np.full(max(N * k, 1), -1, np.int32)
+    st = lib.ep_oracle_local_layout(idx.reshape(-1) if N else np.zeros(1, np.int32), N, k, E, e_lo, e_hi,
+                                    lc, lo, sp, rs.ctypes.data)
+    n_local = int(lo[-1]) if st == OK else 0
+    return LocalLayout(st, lc, lo, sp[:N * k], rs[:n_local])
+
+
+def block_reduce(blocks: np.ndarray, lib=None):
+    """Sum of R blocks (float64 [R, ...] holding bf16 or float values) in rank order.
+    Returns (exact float64, bf16 bits uint16, float32), each shaped like one block."""
+    lib = lib or load()
+    b = np.ascontiguousarray(blocks, dtype=np.float64)
+    R = b.shape[0]
+    shape = b.shape[1:]
+    n = int(np.prod(shape)) if shape else 1
+    exact = np.zeros(n, np.float64)
+    b16 = np.zeros(n, np.uint16)
+    f32 = np.zeros(n, np.float32)
+    if n and R:
+        lib.ep_oracle_block_reduce(b.reshape(-1), R, n, exact.ctypes.data, b16.ctypes.data, f32.ctypes.data)
+    return exact.reshape(shape), b16.reshape(shape), f32.reshape(shape)
+
+
+def pcie_volume(collective: str, algorithm: str, N: int, S: float) -> dict:
+    """Per-GPU PCIe bytes of the collectives of Sec. 4.2, for N GPUs with shards of S bytes
+    (host memory as the only shared medium, every byte crossing PCIe once per hop):
+      all_gather ring           each of the N-1 relay steps writes one shard to host memory
+                                and reads one back: up (N-1)S, down (N-1)S
+      all_gather single_step    upload the own shard once, download the N-1 others:
+                                up S, down (N-1)S
+      reduce_scatter ring       (N-1)S each way, as the ring All-Gather
+      reduce_scatter gpu        upload the N-1 blocks for the other GPUs, download the N-1
+                                blocks for this GPU's shard: up (N-1)S, down (N-1)S
+      reduce_scatter cpu        upload the N-1 blocks, download one block already summed
+                                in host memory: up (N-1)S, down S
+    """
+    table = {
+        ("all_gather", "ring"): ((N - 1) * S, (N - 1) * S),
+        ("all_gather", "single_step"): (S, (N - 1) * S),
+        ("reduce_scatter", "ring"): ((N - 1) * S, (N - 1) * S),
+        ("reduce_scatter", "gpu"): ((N - 1) * S, (N - 1) * S),
+        ("reduce_scatter", "cpu"): ((N - 1) * S, S),
+    }
+    up, down = table[(collective, algorithm)]
+    return {"up": up, "down": down, "total": up + down}

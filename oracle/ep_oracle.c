@@ -144,6 +144,8 @@ void ep_oracle_combine(const uint16_t *y, const int32_t *slot_pos, const float *
         /* contributions in slot order j = 0..k-1; each product of a binary32 gate and a
          * bf16 value is exact in double */
         for (int32_t j = 0; j < k; ++j) {
+            if (slot_pos[t * k + j] < 0)
+                continue;   /* routed to another rank: no contribution here */
             double w = (double)topk_w[t * k + j];
             const uint16_t *row = y + (int64_t)slot_pos[t * k + j] * H;
             for (int32_t h = 0; h < H; ++h)
@@ -160,4 +162,68 @@ void ep_oracle_combine(const uint16_t *y, const int32_t *slot_pos, const float *
         }
     }
     free(acc);
+}
+
+int ep_oracle_local_layout(const int32_t *topk_idx, int64_t N, int32_t k, int32_t E, int32_t e_lo,
+                           int32_t e_hi, int32_t *local_counts, int32_t *local_offsets,
+                           int32_t *slot_pos, int32_t *row_src) {
+    if (N < 0 || k < 1 || E < 1 || k > E || e_lo < 0 || e_lo >= e_hi || e_hi > E)
+        return EP_ORACLE_INVALID_ARG;
+    /* 1. validate every row: ids in [0,E), no expert twice */
+    for (int64_t t = 0; t < N; ++t)
+        for (int32_t j = 0; j < k; ++j) {
+            int32_t e = topk_idx[t * k + j];
+            if (e < 0 || e >= E)
+                return EP_ORACLE_BAD_ROUTING;
+            for (int32_t jj = 0; jj < j; ++jj)
+                if (topk_idx[t * k + jj] == e)
+                    return EP_ORACLE_BAD_ROUTING;
+        }
+    const int32_t L = e_hi - e_lo;
+    /* 2. count the slots that name a local expert */
+    for (int32_t l = 0; l < L; ++l)
+        local_counts[l] = 0;
+    for (int64_t i = 0; i < N * k; ++i) {
+        int32_t e = topk_idx[i];
+        if (e >= e_lo && e < e_hi)
+            local_counts[e - e_lo] += 1;
+    }
+    /* 3. exclusive prefix sum */
+    local_offsets[0] = 0;
+    for (int32_t l = 0; l < L; ++l)
+        local_offsets[l + 1] = local_offsets[l] + local_counts[l];
+    /* 4. place local slots in increasing flat index; others get -1 */
+    int32_t *cursor = (int32_t *)malloc(sizeof(int32_t) * (size_t)L);
+    if (!cursor)
+        abort();
+    for (int32_t l = 0; l < L; ++l)
+        cursor[l] = local_offsets[l];
+    for (int64_t i = 0; i < N * k; ++i) {
+        int32_t e = topk_idx[i];
+        if (e < e_lo || e >= e_hi) {
+            slot_pos[i] = -1;
+            continue;
+        }
+        int32_t p = cursor[e - e_lo]++;
+        slot_pos[i] = p;
+        if (row_src)
+            row_src[p] = (int32_t)i;
+    }
+    free(cursor);
+    return EP_ORACLE_OK;
+}
+
+void ep_oracle_block_reduce(const double *blocks, int32_t R, int64_t n, double *out_exact,
+                            uint16_t *out_bf16, float *out_f32) {
+    for (int64_t i = 0; i < n; ++i) {
+        double acc = 0.0;
+        for (int32_t d = 0; d < R; ++d)   /* blocks summed in rank order */
+            acc = acc + blocks[(int64_t)d * n + i];
+        if (out_exact)
+            out_exact[i] = acc;
+        if (out_bf16)
+            out_bf16[i] = ep_oracle_double_to_bf16(acc);
+        if (out_f32)
+            out_f32[i] = (float)acc;
+    }
 }

@@ -58,12 +58,32 @@ void ep_oracle_pack(const uint16_t *x, int64_t T, int32_t H, int32_t k,
 
 /* Combine (Sec. 4.3 GPU-side reduction of the returned contributions):
  *   exact[t][h] = sum_{j<k} w[t][j] * y[slot_pos[t*k+j]][h]   (double)
- * y: bf16 [*][H] in packed order; w: float [T][k].  Any output pointer may be NULL:
+ * y: bf16 [*][H] in packed order; w: float [T][k].  A slot with slot_pos < 0 (not routed
+ * to this rank, see ep_oracle_local_layout) contributes nothing, so over the gathered
+ * tokens of the dense design this gives each shard's partial block (Sec. 4.2: a GPU's
+ * contribution to an output shard).  Any output pointer may be NULL:
  *   out_exact: double [T][H]; out_bf16: bf16 [T][H] (exact rounded to nearest-even);
  *   out_f32: float [T][H] (exact rounded to nearest-even). */
 void ep_oracle_combine(const uint16_t *y, const int32_t *slot_pos, const float *topk_w,
                        int64_t T, int32_t H, int32_t k,
                        double *out_exact, uint16_t *out_bf16, float *out_f32);
+
+/* Receive-side grouping of the dense design (Sec. 4.3: each GPU groups the tokens it
+ * gathered by the experts it owns): the stable counting sort of ep_oracle_layout over N
+ * gathered tokens, restricted to the local experts [e_lo, e_hi).  Slots naming another
+ * expert get slot_pos = -1 and are not counted.  Outputs: local_counts[L],
+ * local_offsets[L+1] (L = e_hi - e_lo), slot_pos[N*k], row_src[local rows] (may be NULL).
+ * Returns EP_ORACLE_INVALID_ARG unless 0 <= e_lo < e_hi <= E, EP_ORACLE_BAD_ROUTING for
+ * an id outside [0,E) or repeated within a token row. */
+int ep_oracle_local_layout(const int32_t *topk_idx, int64_t N, int32_t k, int32_t E, int32_t e_lo,
+                           int32_t e_hi, int32_t *local_counts, int32_t *local_offsets,
+                           int32_t *slot_pos, int32_t *row_src);
+
+/* Block reduction of the Reduce-Scatter (Sec. 4.2: the destination sums the blocks of the
+ * other GPUs with its own):  exact[i] = sum_{d<R} blocks[d*n + i]  (double), i < n.
+ * Any output pointer may be NULL; rounding as in ep_oracle_combine. */
+void ep_oracle_block_reduce(const double *blocks, int32_t R, int64_t n, double *out_exact,
+                            uint16_t *out_bf16, float *out_f32);
 
 /* bf16 <-> double.  bf16 = sign, 8 exponent bits, 7 fraction bits (the upper half of an
  * IEEE-754 binary32).  The narrowing rounds to nearest, ties to even; NaN stays NaN. */

@@ -360,7 +360,115 @@ def pin_bf16_torch(lib):
     assert all((int(g) & 0x7F80) == 0x7F80 and (int(g) & 0x7F) for g in got_nan)
 
 
+# ------------------------------------------------------------ dense All-Gather / Reduce-Scatter
+
+def brute_local_layout(idx: np.ndarray, e_lo: int, e_hi: int):
+    """Grouping by definition: the slots naming a local expert, ordered by (expert, slot)."""
+    flat = [int(v) for v in idx.reshape(-1)]
+    local = [i for i in range(len(flat)) if e_lo <= flat[i] < e_hi]
+    order = sorted(local, key=lambda i: (flat[i], i))
+    slot_pos = [-1] * len(flat)
+    for p, i in enumerate(order):
+        slot_pos[i] = p
+    counts = [flat.count(e) for e in range(e_lo, e_hi)]
+    offsets = [sum(counts[:l]) for l in range(e_hi - e_lo + 1)]
+    return dict(local_counts=counts, local_offsets=offsets, slot_pos=slot_pos, row_src=order)
+
+
+def pin_local_layout_bruteforce(lib):
+    rng = np.random.default_rng(41)
+    for N, E, k in [(1, 4, 2), (9, 6, 3), (40, 16, 4), (64, 8, 8), (0, 4, 1)]:
+        idx = random_routing(rng, N, E, k)
+        for e_lo, e_hi in [(0, E), (0, 1), (E - 1, E), (E // 4, E // 2 + 1)]:
+            if e_lo >= e_hi:
+                continue
+            got = oracle.local_layout(idx, E, e_lo, e_hi, lib=lib)
+            assert got.status == oracle.OK
+            want = brute_local_layout(idx, e_lo, e_hi)
+            for key, val in want.items():
+                _eq(f"local {key} N={N} window=[{e_lo},{e_hi})", getattr(got, key), val)
+
+
+def pin_local_layout_window_of_global(lib):
+    """Inside its window, the local grouping is the global one shifted by the window's first
+    offset (the global layout is pinned on its own)."""
+    cfg = synth.config("fine")
+    idx = synth.make_inputs(cfg).topk_idx[:2000]
+    g = oracle.layout(idx, cfg.E, cfg.R, lib=lib)
+    L = cfg.E // cfg.R
+    flat = idx.reshape(-1)
+    for r in range(cfg.R):
+        loc = oracle.local_layout(idx, cfg.E, r * L, (r + 1) * L, lib=lib)
+        inside = (flat >= r * L) & (flat < (r + 1) * L)
+        _eq("local slot_pos", loc.slot_pos[inside], g.slot_pos[inside] - g.expert_offsets[r * L])
+        assert np.all(loc.slot_pos[~inside] == -1)
+        _eq("local counts", loc.local_counts, g.expert_counts[r * L:(r + 1) * L])
+
+
+def pin_local_layout_validation(lib):
+    idx = np.array([[0, 1], [2, 3]], np.int32)
+    for e_lo, e_hi in [(2, 2), (3, 1), (-1, 2), (0, 5)]:
+        assert oracle.local_layout(idx, 4, e_lo, e_hi, lib=lib).status == oracle.INVALID_ARG
+    assert oracle.local_layout(np.array([[0, 4]], np.int32), 4, 0, 2, lib=lib).status == oracle.BAD_ROUTING
+    assert oracle.local_layout(np.array([[3, 3]], np.int32), 4, 0, 2, lib=lib).status == oracle.BAD_ROUTING
+
+
+def pin_partials_sum_to_combine(lib):
+    """Every rank's partial block over its own experts, summed over ranks, is the combine of
+    the routing-aware path (exact: dyadic gates and small-integer rows)."""
+    rng = np.random.default_rng(43)
+    N, H, E, k, R = 50, 12, 16, 4, 4
+    idx = random_routing(rng, N, E, k)
+    w = (rng.integers(1, 8, size=(N, k)) / 8.0).astype(np.float32)
+    g = oracle.layout(idx, E, R, lib=lib)
+    vals = rng.integers(-64, 64, size=(N * k, H)).astype(np.float32)
+    y = (vals.view(np.uint32) >> 16).astype(np.uint16)        # exact bf16 of small integers
+    full, _, _ = oracle.combine(y, g.slot_pos, w, lib=lib)
+    L = E // R
+    total = np.zeros_like(full)
+    for r in range(R):
+        loc = oracle.local_layout(idx, E, r * L, (r + 1) * L, lib=lib)
+        y_loc = y[g.slot_pos[loc.row_src]] if loc.row_src.size else np.zeros((0, H), np.uint16)
+        part, _, _ = oracle.combine(np.ascontiguousarray(y_loc) if y_loc.size else np.zeros((1, H), np.uint16),
+                                    loc.slot_pos, w, lib=lib)
+        total += part
+    _eq("sum of partial blocks", total, full)
+
+
+def pin_block_reduce_fraction(lib):
+    """Exact rational sums of bf16 blocks, rounded by the independent ties-to-even helper."""
+    rng = np.random.default_rng(44)
+    R, n = 5, 300
+    # sign and fraction random, exponents within 2^-20..2^20: five 8-bit significands
+    # spanning 40 binades sum exactly in double, so one rounding to bf16 is compared
+    sign = rng.integers(0, 2, size=(R, n), dtype=np.uint32) << 15
+    expo = rng.integers(127 - 20, 127 + 21, size=(R, n), dtype=np.uint32) << 7
+    frac = rng.integers(0, 128, size=(R, n), dtype=np.uint32)
+    bits = (sign | expo | frac).astype(np.uint16)
+    vals = oracle.bf16_to_double(bits)
+    exact, b16, _ = oracle.block_reduce(vals, lib=lib)
+    for i in range(n):
+        q = sum((bf16_fraction(int(bits[d, i])) for d in range(R)), Fraction(0))
+        assert exact[i] == float(q) or abs(Fraction(exact[i]) - q) <= abs(q) * Fraction(1, 1 << 50), i
+        assert int(b16[i]) == bf16_from_fraction(q), f"block_reduce bf16 at {i}"
+    ones = np.ones((7, 3), np.float64) * 0.75
+    _eq("seven equal blocks", oracle.block_reduce(ones, lib=lib)[0], np.full(3, 5.25))
+
+
+def pin_pcie_volume_golden(lib):
+    del lib
+    for line in open(os.path.join(GOLDEN, "pcie_volume.txt")):
+        line = line.split("#")[0].split()
+        if not line:
+            continue
+        coll, alg, N, total = line[0], line[1], int(line[2]), int(line[3])
+        got = oracle.pcie_volume(coll, alg, N, 1.0)["total"]
+        assert got == total, f"{coll} {alg} N={N}: model {got} != paper {total}"
+
+
 ALL_PINS = [pin_layout_golden, pin_layout_bruteforce, pin_layout_closed_forms, pin_layout_argsort,
             pin_layout_invariants, pin_layout_validation, pin_pack, pin_combine_fraction,
             pin_combine_inverse_permutation, pin_combine_identity, pin_combine_scaled_identity,
-            pin_bf16_golden, pin_bf16_torch]
+            pin_bf16_golden, pin_bf16_torch,
+            pin_local_layout_bruteforce, pin_local_layout_window_of_global, pin_local_layout_validation,
+            pin_partials_sum_to_combine, pin_block_reduce_fraction, pin_pcie_volume_golden]
