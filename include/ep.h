@@ -237,6 +237,100 @@ ep_status ep_combine(ep_staging *s, int32_t buf, uint32_t epoch, const int32_t *
                      int32_t hidden, int32_t topk, void *out_dev, ep_out_dtype out_dtype,
                      hipStream_t stream);
 
+/* ------------------------------------------------------- dense collectives (Sec. 4.2)
+ *
+ * The paper's adopted design: dispatch is a single-step All-Gather of every rank's token
+ * rows, combine a Reduce-Scatter of partial blocks, both through pinned host memory as
+ * the one medium all ranks share.  For this rank (self_rank of R, T tokens per rank):
+ *   ep_allgather          uploads its shard once and downloads the R-1 others as their
+ *                         ranks' flags arrive: S up, (R-1)S down (S = T*H*2 bytes);
+ *   ep_dispatch_layout_local, ep_pack
+ *                         group the R*T gathered tokens by the experts this rank owns
+ *                         (Sec. 4.3) and pack them for the expert computation;
+ *   ep_combine_rows       turns the experts' outputs into R partial blocks, block d =
+ *                         this rank's contribution to rank d's shard (gate-weighted sum over
+ *                         its local experts, fp32 accumulation);
+ *   ep_reducescatter      uploads the R-1 blocks for the other ranks and sums the blocks for
+ *                         its own shard: on the GPU after downloading R-1 blocks ((R-1)S up,
+ *                         (R-1)S down), or with the partial host reduction (Sec. 4.5: host
+ *                         threads sum the R-1 remote blocks in pinned memory, one block goes
+ *                         down, (R-1)S up, S down).
+ * Every transfer runs on SDMA engines as in the exchange modes (one device->host engine,
+ * one host->device engine whose copies are queued in flag-arrival order). */
+typedef struct ep_dense ep_dense; /* opaque, owned by the library */
+
+/* Buffers of `num_buffers` independent rounds for up to max_tokens tokens per rank:
+ * pinned host [R][max_tokens][H] shard slots, device [R][max_tokens][H] gathered rows,
+ * pinned host and device [R][max_tokens][H] blocks in block_dtype (bf16 rounded to
+ * nearest-even, or fp32), coherent host flags.  R <= 32. */
+ep_status ep_dense_alloc(int64_t max_tokens, int32_t hidden, int32_t num_ranks, int32_t self_rank,
+                         int32_t num_buffers, ep_out_dtype block_dtype, ep_dense **out);
+ep_status ep_dense_free(ep_dense *d);
+
+typedef struct {
+    int32_t num_ranks, self_rank, num_buffers, hidden, block_dtype;
+    int64_t max_tokens, row_bytes, block_row_bytes;
+    void *host_ag;          /* pinned: rank r's shard at rows [r*T, (r+1)*T) of a T-token call */
+    void *dev_gathered;     /* device, same layout: the All-Gather's result */
+    void *host_rs_out;      /* pinned: this rank's block for rank r at rows [r*T, (r+1)*T) */
+    void *host_rs_in;       /* pinned: rank r's block for this rank (own slot: the host-side sum) */
+    void *dev_rs_in;        /* device, same layout as host_rs_in */
+    uint32_t *ag_flags;     /* host [R]: rank r sets epoch once its shard is in host_ag */
+    uint32_t *ag_landed;    /* host [R]: epoch once rank r's shard is in dev_gathered */
+    uint32_t *rs_out_flags; /* host [R]: epoch once this rank's block for r is in host_rs_out */
+    uint32_t *rs_in_flags;  /* host [R]: rank r sets epoch once its block for this rank is in host_rs_in */
+    uint32_t *rs_landed;    /* host [R]: epoch once that block (or the host sum, own slot) is on the GPU */
+} ep_dense_view;
+ep_status ep_dense_get(ep_dense *d, int32_t buf, ep_dense_view *view);
+
+/* mode: 0 (download after the last rank's flag) or EP_MODE_PER_SENDER; timeout_us bounds
+ * every flag wait (default 10 s); host_threads: threads of the partial host reduction
+ * (0 keeps the current count). */
+ep_status ep_dense_set_policy(ep_dense *d, uint32_t mode, int64_t timeout_us, int32_t host_threads);
+/* Synchronizes `stream`; returns and clears the status word (EP_ERR_TIMEOUT after an expired
+ * wait). */
+ep_status ep_dense_status(ep_dense *d, hipStream_t stream);
+/* PCIe payload bytes queued so far by this staging's collectives, each direction (flag
+ * words not counted): the measured side of the volume model of Sec. 4.2. */
+ep_status ep_dense_bytes(ep_dense *d, int64_t *up, int64_t *down);
+
+/* All-Gather of round `epoch` into buffer set `buf`: x_dev bf16 [T][H] is this rank's
+ * shard; afterwards the gathered rows are dev_gathered [R*T][H] (rank order). */
+ep_status ep_allgather(ep_dense *d, int32_t buf, uint32_t epoch, const void *x_dev, int64_t num_tokens,
+                       hipStream_t stream);
+
+/* Reduce-Scatter of round `epoch`: blocks_dev [R][T][H] in the block dtype (block r: this
+ * rank's contribution to rank r's shard); out_dev [T][H] = sum over r of the blocks for
+ * this rank's shard, fp32 accumulation in rank order, stored as out_dtype.  With
+ * reduce_on_host the R-1 remote blocks are first summed by host threads (fp32, rank order,
+ * stored in the block dtype) and the GPU adds its own block to that sum. */
+ep_status ep_reducescatter(ep_dense *d, int32_t buf, uint32_t epoch, const void *blocks_dev, int64_t num_tokens,
+                           int32_t reduce_on_host, void *out_dev, ep_out_dtype out_dtype, hipStream_t stream);
+
+/* Grouping of N (gathered) tokens by the experts [e_lo, e_hi) of E: ep_dispatch_layout
+ * restricted to a window (Sec. 4.3: each rank groups the tokens it received by the
+ * experts it owns).  Outputs local_counts[L], local_offsets[L+1] (L = e_hi - e_lo),
+ * slot_pos[N*k] (-1 for slots naming other experts), row_src[local rows] or NULL.
+ * Routing errors (ids outside [0,E), an expert twice in a row) are checked over every
+ * id, as in ep_dispatch_layout.  workspace: ep_layout_workspace_bytes(N, k, L) bytes,
+ * zero-filled before first use. */
+ep_status ep_dispatch_layout_local(const int32_t *topk_idx, int64_t num_tokens, int32_t topk, int32_t num_experts,
+                                   int32_t e_lo, int32_t e_hi, int32_t *local_counts, int32_t *local_offsets,
+                                   int32_t *slot_pos, int32_t *row_src, void *workspace, size_t workspace_bytes,
+                                   hipStream_t stream);
+
+/* out[slot_pos[t*k+j]][:] = x[t][:] for slots with slot_pos in [0, max_rows) (the pack of
+ * ep_dispatch on caller-owned buffers). */
+ep_status ep_pack(const void *x_dev, int64_t num_tokens, int32_t hidden, int32_t topk, const int32_t *slot_pos,
+                  void *out_dev, int64_t max_rows, hipStream_t stream);
+
+/* out[t][:] = sum_j topk_w[t*k+j] * y[slot_pos[t*k+j]][:] over slots with slot_pos in
+ * [0, max_rows) (the reduction of ep_combine on caller-owned buffers; over the gathered
+ * tokens with a window layout it yields the partial blocks of ep_reducescatter). */
+ep_status ep_combine_rows(const void *y_dev, int64_t max_rows, const int32_t *slot_pos, const float *topk_w,
+                          int64_t num_tokens, int32_t hidden, int32_t topk, void *out_dev, ep_out_dtype out_dtype,
+                          hipStream_t stream);
+
 /* ------------------------------------------------------------------ measurement */
 
 typedef struct {

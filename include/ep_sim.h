@@ -39,6 +39,12 @@ ep_status ep_sim_peers_post(ep_sim_peers *p, int32_t buf, uint32_t epoch, int64_
 /* Per-sender delays in microseconds, arrays of num_ranks (NULL = all zero), used by the
  * rounds posted after this call (steps 0 and 4 above). */
 ep_status ep_sim_peers_set_delays(ep_sim_peers *p, const int64_t *inbound_us, const int64_t *return_us);
+/* Simulated peers of a dense staging (ep_dense).  For each posted round the thread sets
+ * the other ranks' flags, in order of their delays: phase 0 (All-Gather) ag_flags[r] =
+ * epoch inbound_us[r] after the post; phase 1 (Reduce-Scatter) rs_in_flags[r] = epoch
+ * return_us[r] after the post.  The harness writes the peers' shards and blocks first. */
+ep_status ep_sim_dense_start(ep_dense *d, ep_sim_peers **out);
+ep_status ep_sim_dense_post(ep_sim_peers *p, int32_t buf, uint32_t epoch, int32_t phase);
 /* Blocks until every posted round was answered (or timeout_ms passed). */
 ep_status ep_sim_peers_drain(ep_sim_peers *p, int64_t timeout_ms);
 /* Stops and joins the thread (pending rounds are dropped). */

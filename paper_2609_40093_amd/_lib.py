@@ -33,6 +33,14 @@ class StagingView(ctypes.Structure):
                 ("in_offsets", c_vp)]
 
 
+class DenseView(ctypes.Structure):
+    _fields_ = [("num_ranks", c_i32), ("self_rank", c_i32), ("num_buffers", c_i32), ("hidden", c_i32),
+                ("block_dtype", c_i32), ("max_tokens", c_i64), ("row_bytes", c_i64), ("block_row_bytes", c_i64),
+                ("host_ag", c_vp), ("dev_gathered", c_vp), ("host_rs_out", c_vp), ("host_rs_in", c_vp),
+                ("dev_rs_in", c_vp), ("ag_flags", c_vp), ("ag_landed", c_vp), ("rs_out_flags", c_vp),
+                ("rs_in_flags", c_vp), ("rs_landed", c_vp)]
+
+
 class TraceStat(ctypes.Structure):
     _fields_ = [("name", ctypes.c_char * 48), ("count", c_i64), ("total_ms", ctypes.c_double),
                 ("min_ms", ctypes.c_double), ("max_ms", ctypes.c_double)]
@@ -56,6 +64,18 @@ SIGNATURES = {
     "ep_staging_set_inbound": (c_i32, [c_vp, c_i32, ctypes.POINTER(c_i64)]),
     "ep_dispatch": (c_i32, [c_vp, c_i64, c_i32, c_i32, c_vp, c_vp, c_vp, c_i32, c_u32, c_vp]),
     "ep_combine": (c_i32, [c_vp, c_i32, c_u32, c_vp, c_vp, c_vp, c_i64, c_i32, c_i32, c_vp, c_i32, c_vp]),
+    "ep_dense_alloc": (c_i32, [c_i64, c_i32, c_i32, c_i32, c_i32, c_i32, ctypes.POINTER(c_vp)]),
+    "ep_dense_free": (c_i32, [c_vp]),
+    "ep_dense_get": (c_i32, [c_vp, c_i32, ctypes.POINTER(DenseView)]),
+    "ep_dense_set_policy": (c_i32, [c_vp, c_u32, c_i64, c_i32]),
+    "ep_dense_status": (c_i32, [c_vp, c_vp]),
+    "ep_dense_bytes": (c_i32, [c_vp, ctypes.POINTER(c_i64), ctypes.POINTER(c_i64)]),
+    "ep_allgather": (c_i32, [c_vp, c_i32, c_u32, c_vp, c_i64, c_vp]),
+    "ep_reducescatter": (c_i32, [c_vp, c_i32, c_u32, c_vp, c_i64, c_i32, c_vp, c_i32, c_vp]),
+    "ep_dispatch_layout_local": (c_i32, [c_vp, c_i64, c_i32, c_i32, c_i32, c_i32, c_vp, c_vp, c_vp, c_vp, c_vp,
+                                         c_size, c_vp]),
+    "ep_pack": (c_i32, [c_vp, c_i64, c_i32, c_i32, c_vp, c_vp, c_i64, c_vp]),
+    "ep_combine_rows": (c_i32, [c_vp, c_i64, c_vp, c_vp, c_i64, c_i32, c_i32, c_vp, c_i32, c_vp]),
     "ep_trace_enable": (c_i32, [c_i32]),
     "ep_trace_read": (c_i32, [ctypes.POINTER(TraceStat), c_i32, ctypes.POINTER(c_i32)]),
     "ep_trace_reset": (c_i32, []),
@@ -65,6 +85,8 @@ SIGNATURES = {
     "ep_sim_peers_start": (c_i32, [c_vp, c_i32, ctypes.POINTER(c_vp)]),
     "ep_sim_peers_post": (c_i32, [c_vp, c_i32, c_u32, c_i64, c_i64]),
     "ep_sim_peers_set_delays": (c_i32, [c_vp, ctypes.POINTER(c_i64), ctypes.POINTER(c_i64)]),
+    "ep_sim_dense_start": (c_i32, [c_vp, ctypes.POINTER(c_vp)]),
+    "ep_sim_dense_post": (c_i32, [c_vp, c_i32, c_u32, c_i32]),
     "ep_sim_peers_drain": (c_i32, [c_vp, c_i64]),
     "ep_sim_peers_stop": (c_i32, [c_vp]),
 }

@@ -22,7 +22,8 @@ MODE_PER_SENDER, MODE_DUPLEX, MODE_REMOTE_ONLY = _lib.EP_MODE_PER_SENDER, _lib.E
 
 __all__ = ["EPError", "Layout", "Staging", "SimPeers", "dispatch_layout", "layout_status", "dispatch",
            "combine", "trace_enable", "trace_read", "trace_reset", "copy_probe", "workspace_bytes",
-           "pcie_probe", "MODE_PER_SENDER", "MODE_DUPLEX", "MODE_REMOTE_ONLY"]
+           "pcie_probe", "MODE_PER_SENDER", "MODE_DUPLEX", "MODE_REMOTE_ONLY", "LocalLayout",
+           "dispatch_layout_local", "pack", "combine_rows", "Dense", "allgather", "reducescatter"]
 
 _PAYLOAD_DTYPES = (torch.bfloat16, torch.int16, torch.uint16)
 
@@ -120,6 +121,71 @@ def dispatch_layout(topk_idx: torch.Tensor, num_experts: int, num_ranks: int, *,
         _ptr(out.rank_counts), _ptr(out.rank_offsets), _ptr(out.slot_pos), _ptr(out.row_src),
         _ptr(out.workspace), out.workspace.numel(), _stream_ptr(stream))
     _check(st, "ep_dispatch_layout")
+    return out
+
+
+@dataclass
+class LocalLayout:
+    num_tokens: int
+    topk: int
+    num_experts: int
+    e_lo: int
+    e_hi: int
+    local_counts: torch.Tensor
+    local_offsets: torch.Tensor
+    slot_pos: torch.Tensor
+    row_src: Optional[torch.Tensor]
+    workspace: torch.Tensor
+
+
+def dispatch_layout_local(topk_idx: torch.Tensor, num_experts: int, e_lo: int, e_hi: int, *,
+                          with_row_src: bool = True, out: Optional[LocalLayout] = None,
+                          stream=None) -> LocalLayout:
+    """ep_dispatch_layout_local: group N (gathered) tokens by the experts [e_lo, e_hi)."""
+    _need(topk_idx, "topk_idx", (torch.int32,), 2)
+    N, k = topk_idx.shape
+    dev = topk_idx.device
+    L = e_hi - e_lo
+    if out is None or (out.num_tokens, out.topk, out.num_experts, out.e_lo, out.e_hi) != (N, k, num_experts, e_lo,
+                                                                                          e_hi):
+        i32 = dict(dtype=torch.int32, device=dev)
+        ws = workspace_bytes(N, k, L) if 1 <= k <= L <= _lib.EP_MAX_EXPERTS else 256
+        out = LocalLayout(N, k, num_experts, e_lo, e_hi, torch.empty(max(L, 1), **i32),
+                          torch.empty(max(L, 0) + 1, **i32), torch.empty(N * k, **i32),
+                          torch.empty(N * k, **i32) if with_row_src else None,
+                          torch.zeros(max(ws, 256), dtype=torch.uint8, device=dev))
+    _check(_lib_handle().ep_dispatch_layout_local(
+        _ptr(topk_idx), N, k, num_experts, e_lo, e_hi, _ptr(out.local_counts), _ptr(out.local_offsets),
+        _ptr(out.slot_pos), _ptr(out.row_src), _ptr(out.workspace), out.workspace.numel(), _stream_ptr(stream)),
+        "ep_dispatch_layout_local")
+    return out
+
+
+def pack(x: torch.Tensor, slot_pos: torch.Tensor, out: torch.Tensor, *, topk: int, stream=None) -> torch.Tensor:
+    """ep_pack: out[slot_pos[t*k+j]] = x[t] (slots outside [0, len(out)) skipped)."""
+    _need(x, "x", _PAYLOAD_DTYPES, 2)
+    _need(out, "out", _PAYLOAD_DTYPES, 2)
+    _need(slot_pos, "slot_pos", (torch.int32,), 1)
+    N, H = x.shape
+    if out.shape[1] != H or slot_pos.numel() != N * topk:
+        raise ValueError("shape mismatch between x, out and slot_pos")
+    _check(_lib_handle().ep_pack(_ptr(x), N, H, topk, _ptr(slot_pos), _ptr(out), out.shape[0], _stream_ptr(stream)),
+           "ep_pack")
+    return out
+
+
+def combine_rows(y: torch.Tensor, slot_pos: torch.Tensor, topk_w: torch.Tensor, out: torch.Tensor,
+                 stream=None) -> torch.Tensor:
+    """ep_combine_rows: out[t] = sum_j w[t, j] * y[slot_pos[t*k + j]] (fp32 accumulation)."""
+    _need(topk_w, "topk_w", (torch.float32,), 2)
+    _need(slot_pos, "slot_pos", (torch.int32,), 1)
+    N, k = topk_w.shape
+    H = out.shape[1]
+    code = EP_OUT_F32 if out.dtype == torch.float32 else EP_OUT_BF16
+    if y.numel() and y.shape[1] != H or slot_pos.numel() != N * k or out.shape[0] != N:
+        raise ValueError("shape mismatch between y, out, topk_w and slot_pos")
+    _check(_lib_handle().ep_combine_rows(_ptr(y), y.shape[0] if y.numel() else 0, _ptr(slot_pos), _ptr(topk_w), N, H,
+                                         k, _ptr(out), code, _stream_ptr(stream)), "ep_combine_rows")
     return out
 
 
@@ -276,15 +342,118 @@ def combine(staging: Staging, slot_pos: torch.Tensor, topk_w: torch.Tensor, *, o
     return out
 
 
+class Dense:
+    """Dense collectives of one rank (ep_dense_alloc): All-Gather / Reduce-Scatter staging."""
+
+    def __init__(self, max_tokens: int, hidden: int, num_ranks: int, self_rank: int = 0, num_buffers: int = 2,
+                 block_dtype: torch.dtype = torch.bfloat16):
+        handle = ctypes.c_void_p()
+        code = EP_OUT_F32 if block_dtype == torch.float32 else EP_OUT_BF16
+        _check(_lib_handle().ep_dense_alloc(max_tokens, hidden, num_ranks, self_rank, num_buffers, code,
+                                            ctypes.byref(handle)), "ep_dense_alloc")
+        self.handle = handle
+        self.views = []
+        for b in range(num_buffers):
+            v = _lib.DenseView()
+            _check(_lib_handle().ep_dense_get(handle, b, ctypes.byref(v)), "ep_dense_get")
+            self.views.append(v)
+        self.max_tokens, self.hidden, self.num_ranks, self.self_rank = max_tokens, hidden, num_ranks, self_rank
+        self.num_buffers = num_buffers
+        self.block_dtype = torch.float32 if code == EP_OUT_F32 else torch.bfloat16
+
+    def close(self):
+        if self.handle:
+            _check(_lib_handle().ep_dense_free(self.handle), "ep_dense_free")
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def set_policy(self, per_sender: bool = False, timeout_us: int = 10_000_000, host_threads: int = 0) -> None:
+        _check(_lib_handle().ep_dense_set_policy(self.handle, MODE_PER_SENDER if per_sender else 0, timeout_us,
+                                                 host_threads), "ep_dense_set_policy")
+
+    def status(self, stream=None) -> None:
+        _check(_lib_handle().ep_dense_status(self.handle, _stream_ptr(stream)), "ep_dense_status")
+
+    def bytes_moved(self):
+        up, down = ctypes.c_int64(), ctypes.c_int64()
+        _check(_lib_handle().ep_dense_bytes(self.handle, ctypes.byref(up), ctypes.byref(down)), "ep_dense_bytes")
+        return up.value, down.value
+
+    _HOST = {"ag": ("host_ag", False), "rs_out": ("host_rs_out", True), "rs_in": ("host_rs_in", True)}
+    _FLAGS = ("ag_flags", "ag_landed", "rs_out_flags", "rs_in_flags", "rs_landed")
+
+    def host_array(self, which: str, buf: int = 0) -> np.ndarray:
+        """[R * max_tokens, H] view of a pinned host buffer (uint16 bits, or float32 blocks)."""
+        v = self.views[buf]
+        if which in self._FLAGS:
+            return np.ctypeslib.as_array(ctypes.cast(getattr(v, which), ctypes.POINTER(ctypes.c_uint32)),
+                                         shape=(self.num_ranks,))
+        field, is_block = self._HOST[which]
+        ctype = ctypes.c_float if is_block and self.block_dtype == torch.float32 else ctypes.c_uint16
+        return np.ctypeslib.as_array(ctypes.cast(getattr(v, field), ctypes.POINTER(ctype)),
+                                     shape=(self.num_ranks * self.max_tokens, self.hidden))
+
+    def device_rows(self, which: str, rows: int, buf: int = 0, stream=None) -> torch.Tensor:
+        """Copy of the first `rows` rows of dev_gathered ("gathered") or dev_rs_in ("rs_in")."""
+        v = self.views[buf]
+        if which == "gathered":
+            ptr, dt, rb = v.dev_gathered, torch.int16, v.row_bytes
+        else:
+            ptr, dt, rb = v.dev_rs_in, (torch.float32 if self.block_dtype == torch.float32 else torch.int16), \
+                v.block_row_bytes
+        out = torch.empty((rows, self.hidden), dtype=dt, device="cuda")
+        _check(_lib_handle().ep_memcpy(_ptr(out), ctypes.c_void_p(ptr), rows * rb, _stream_ptr(stream)), "ep_memcpy")
+        return out
+
+
+def allgather(dense: Dense, x: torch.Tensor, *, buf: int = 0, epoch: int = 1, stream=None) -> None:
+    """ep_allgather: this rank's shard x [T, H] -> gathered rows of every rank."""
+    _need(x, "x", _PAYLOAD_DTYPES, 2)
+    T, H = x.shape
+    if H != dense.hidden:
+        raise ValueError("hidden size differs from the staging's")
+    _check(_lib_handle().ep_allgather(dense.handle, buf, epoch & 0xFFFFFFFF, _ptr(x), T, _stream_ptr(stream)),
+           "ep_allgather")
+
+
+def reducescatter(dense: Dense, blocks: torch.Tensor, *, num_tokens: int, out: Optional[torch.Tensor] = None,
+                  out_dtype: torch.dtype = torch.bfloat16, reduce_on_host: bool = False, buf: int = 0,
+                  epoch: int = 1, stream=None) -> torch.Tensor:
+    """ep_reducescatter: blocks [R*T, H] (block dtype) -> out [T, H], the sum for this rank's shard."""
+    T, H = num_tokens, dense.hidden
+    if tuple(blocks.shape) != (dense.num_ranks * T, H):
+        raise ValueError("blocks must be [R*T, H]")
+    if out is None:
+        out = torch.empty((T, H), dtype=out_dtype, device=blocks.device)
+    code = EP_OUT_F32 if out.dtype == torch.float32 else EP_OUT_BF16
+    _check(_lib_handle().ep_reducescatter(dense.handle, buf, epoch & 0xFFFFFFFF, _ptr(blocks), T,
+                                          1 if reduce_on_host else 0, _ptr(out), code, _stream_ptr(stream)),
+           "ep_reducescatter")
+    return out
+
+
 class SimPeers:
     """Host thread standing in for the peer ranks of a pinned staging (include/ep_sim.h)."""
 
-    def __init__(self, staging: Staging, echo: bool = False):
+    def __init__(self, staging, echo: bool = False):
         handle = ctypes.c_void_p()
-        _check(_lib_handle().ep_sim_peers_start(staging.handle, EP_SIM_ECHO if echo else EP_SIM_FLAGS_ONLY,
-                                                ctypes.byref(handle)), "ep_sim_peers_start")
+        if isinstance(staging, Dense):
+            _check(_lib_handle().ep_sim_dense_start(staging.handle, ctypes.byref(handle)), "ep_sim_dense_start")
+        else:
+            _check(_lib_handle().ep_sim_peers_start(staging.handle, EP_SIM_ECHO if echo else EP_SIM_FLAGS_ONLY,
+                                                    ctypes.byref(handle)), "ep_sim_peers_start")
         self.handle = handle
         self.staging = staging  # keep the staging alive while the thread reads it
+
+    def post_dense(self, buf: int, epoch: int, phase: str) -> None:
+        """Dense staging: announce the other ranks' shards ("ag") or blocks ("rs")."""
+        _check(_lib_handle().ep_sim_dense_post(self.handle, buf, epoch & 0xFFFFFFFF, 0 if phase == "ag" else 1),
+               "ep_sim_dense_post")
 
     def post(self, buf: int, epoch: int, rows: int, delay_us: int = 0) -> None:
         _check(_lib_handle().ep_sim_peers_post(self.handle, buf, epoch & 0xFFFFFFFF, rows, delay_us),

@@ -185,6 +185,9 @@ extern "C" ep_status ep_dispatch_layout(const int32_t *topk_idx, int64_t num_tok
     a.E = E;
     a.R = R;
     a.nbits = E > 1 ? 32 - __builtin_clz((unsigned)(E - 1)) : 0;
+    a.e_lo = 0;
+    a.all_E = E;
+    a.all_nbits = a.nbits;
     a.expert_counts = expert_counts;
     a.expert_offsets = expert_offsets;
     a.rank_counts = rank_counts;
@@ -197,6 +200,80 @@ extern "C" ep_status ep_dispatch_layout(const int32_t *topk_idx, int64_t num_tok
     a.timed_out = reinterpret_cast<uint32_t *>(ws + ep::kWorkspaceTimeout);
     a.tile_words = reinterpret_cast<uint64_t *>(ws + ep::kWorkspaceHeader);
     EP_HIP(ep::launch_layout(a, stream));
+    return EP_OK;
+}
+
+extern "C" ep_status ep_dispatch_layout_local(const int32_t *topk_idx, int64_t num_tokens, int32_t topk,
+                                              int32_t num_experts, int32_t e_lo, int32_t e_hi,
+                                              int32_t *local_counts, int32_t *local_offsets, int32_t *slot_pos,
+                                              int32_t *row_src, void *workspace, size_t workspace_bytes,
+                                              hipStream_t stream) {
+    const int64_t N = num_tokens;
+    const int32_t k = topk, E = num_experts;
+    if (N < 0 || E < 1 || E > EP_MAX_EXPERTS || k < 1 || k > E || e_lo < 0 || e_lo >= e_hi || e_hi > E)
+        return fail(EP_ERR_INVALID_ARG,
+                    "ep_dispatch_layout_local: need N >= 0, 1 <= k <= E <= %d, 0 <= e_lo < e_hi <= E "
+                    "(N=%lld k=%d E=%d window [%d,%d))",
+                    EP_MAX_EXPERTS, (long long)N, k, E, e_lo, e_hi);
+    if (N * (int64_t)k > INT32_MAX)
+        return fail(EP_ERR_INVALID_ARG, "ep_dispatch_layout_local: N*k = %lld does not fit int32", (long long)(N * k));
+    if (!local_counts || !local_offsets || !workspace)
+        return fail(EP_ERR_INVALID_ARG, "ep_dispatch_layout_local: NULL output or workspace");
+    if (N > 0 && (!topk_idx || !slot_pos))
+        return fail(EP_ERR_INVALID_ARG, "ep_dispatch_layout_local: NULL topk_idx or slot_pos");
+    const int32_t L = e_hi - e_lo;
+    const size_t need = ep::layout_workspace_bytes(N * k, L);
+    if (workspace_bytes < need)
+        return fail(EP_ERR_INVALID_ARG, "ep_dispatch_layout_local: workspace of %zu bytes, need %zu",
+                    workspace_bytes, need);
+    char *ws = static_cast<char *>(workspace);
+    ep::LayoutArgs a{};
+    a.topk_idx = topk_idx;
+    a.slots = N * k;
+    a.k = k;
+    a.E = L;
+    a.R = 1;  // one segment: the rows of the whole window
+    a.nbits = L > 1 ? 32 - __builtin_clz((unsigned)(L - 1)) : 0;
+    a.e_lo = e_lo;
+    a.all_E = E;
+    a.all_nbits = E > 1 ? 32 - __builtin_clz((unsigned)(E - 1)) : 0;
+    a.expert_counts = local_counts;
+    a.expert_offsets = local_offsets;
+    a.rank_counts = reinterpret_cast<int32_t *>(ws + ep::kWorkspaceScratch);      // [1], unused by callers
+    a.rank_offsets = reinterpret_cast<int32_t *>(ws + ep::kWorkspaceScratch + 4); // [2]
+    a.slot_pos = slot_pos;
+    a.row_src = row_src;
+    a.status = reinterpret_cast<uint32_t *>(ws);
+    a.epoch = reinterpret_cast<uint32_t *>(ws + ep::kWorkspaceEpoch);
+    a.timed_out = reinterpret_cast<uint32_t *>(ws + ep::kWorkspaceTimeout);
+    a.tile_words = reinterpret_cast<uint64_t *>(ws + ep::kWorkspaceHeader);
+    EP_HIP(ep::launch_layout(a, stream));
+    return EP_OK;
+}
+
+extern "C" ep_status ep_pack(const void *x_dev, int64_t num_tokens, int32_t hidden, int32_t topk,
+                             const int32_t *slot_pos, void *out_dev, int64_t max_rows, hipStream_t stream) {
+    if (num_tokens < 0 || topk < 1 || hidden < 8 || hidden % 8 != 0 || max_rows < 0)
+        return fail(EP_ERR_INVALID_ARG, "ep_pack: need N >= 0, k >= 1, H a positive multiple of 8, max_rows >= 0");
+    if (num_tokens > 0 && (!x_dev || !slot_pos || !out_dev || !aligned16(x_dev) || !aligned16(out_dev)))
+        return fail(EP_ERR_INVALID_ARG, "ep_pack: x, slot_pos and a 16-byte aligned out are required");
+    EP_HIP(ep::launch_pack(x_dev, num_tokens, hidden, topk, slot_pos, out_dev, max_rows, nullptr, 0, stream));
+    return EP_OK;
+}
+
+extern "C" ep_status ep_combine_rows(const void *y_dev, int64_t max_rows, const int32_t *slot_pos,
+                                     const float *topk_w, int64_t num_tokens, int32_t hidden, int32_t topk,
+                                     void *out_dev, ep_out_dtype out_dtype, hipStream_t stream) {
+    if (num_tokens < 0 || topk < 1 || hidden < 8 || hidden % 8 != 0 || max_rows < 0)
+        return fail(EP_ERR_INVALID_ARG,
+                    "ep_combine_rows: need N >= 0, k >= 1, H a positive multiple of 8, max_rows >= 0");
+    if (out_dtype != EP_OUT_BF16 && out_dtype != EP_OUT_F32)
+        return fail(EP_ERR_INVALID_ARG, "ep_combine_rows: unknown out_dtype %d", (int)out_dtype);
+    if (num_tokens > 0 && (!slot_pos || !topk_w || !out_dev || !aligned16(out_dev) ||
+                           (max_rows > 0 && (!y_dev || !aligned16(y_dev)))))
+        return fail(EP_ERR_INVALID_ARG, "ep_combine_rows: slot_pos, topk_w and 16-byte aligned y/out are required");
+    EP_HIP(ep::launch_combine(y_dev, slot_pos, topk_w, num_tokens, hidden, topk, out_dev, out_dtype == EP_OUT_F32,
+                              max_rows, stream));
     return EP_OK;
 }
 

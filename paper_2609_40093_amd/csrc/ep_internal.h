@@ -63,11 +63,13 @@ constexpr uint32_t kRoutingDuplicate = 2u;
 //   byte   0  uint32 routing status of the last call
 //   byte  64  uint32 epoch: calls on this workspace so far that used several tiles
 //   byte 128  uint32 nonzero once a workgroup gave up waiting for another's totals
+//   byte 192  int32 [3] rank count/offsets of a window layout (one segment)
 //   byte 256  uint64 [tiles][E+1] words (epoch+1) << 32 | value: a tile's per-expert
 //             totals, then its routing error bits
 constexpr size_t kWorkspaceHeader = 256;
 constexpr size_t kWorkspaceEpoch = 64;
 constexpr size_t kWorkspaceTimeout = 128;
+constexpr size_t kWorkspaceScratch = 192;  // 3 words the one-segment local layout writes
 inline size_t layout_workspace_bytes(int64_t slots, int32_t experts) {
     const LayoutGeom g = layout_geometry(slots, experts, kLayoutMaxTiles);
     return kWorkspaceHeader + (g.tiles > 1 ? (size_t)g.tiles * ((size_t)experts + 1) * sizeof(uint64_t) : 0);
@@ -87,7 +89,10 @@ void trace_submit(const char *name, TraceSlot slot);
 struct LayoutArgs {
     const int32_t *topk_idx;
     int64_t slots;  // T*k
+    // E: experts grouped (the window [e_lo, e_lo + E) of all_E experts); nbits covers E,
+    // all_nbits covers all_E (duplicate check over the raw ids when the window is narrower)
     int32_t k, E, R, nbits;
+    int32_t e_lo = 0, all_E = 0, all_nbits = 0;
     int32_t *expert_counts, *expert_offsets, *rank_counts, *rank_offsets;
     int32_t *slot_pos, *row_src;
     uint32_t *status;        // workspace byte 0
@@ -134,6 +139,17 @@ hipError_t launch_gate(const char *name, const GateArgs &g, hipStream_t stream);
 hipError_t launch_stamp_release(uint32_t *epoch_word, uint32_t epoch, int64_t *value, hipStream_t stream);
 // Copies n int32 from device memory to host words host[0..n), then stores `epoch` in host[n].
 hipError_t launch_mirror(const int32_t *src, int32_t n, uint32_t *host, uint32_t epoch, hipStream_t stream);
+
+// Up to kMaxBlocks equally shaped blocks summed element-wise by launch_block_reduce.
+constexpr int kMaxBlocks = 32;
+struct BlockList {
+    const void *ptr[kMaxBlocks];
+    int32_t n = 0;
+};
+// out[i] = sum_b block_b[i] over n elements (n % 8 == 0, 16-byte aligned blocks), fp32
+// accumulation in list order; blocks bf16 or fp32 (f32_in), out bf16 (nearest-even) or fp32.
+hipError_t launch_block_reduce(const BlockList &bl, bool f32_in, int64_t n, void *out, bool f32_out,
+                               hipStream_t stream);
 
 hipError_t launch_copy(void *dst, const void *src, size_t bytes, hipStream_t stream);
 

@@ -2,6 +2,9 @@
 // entries by expert id (rows grouped by expert, token order kept inside a group, groups
 // in expert order, hence contiguous per destination rank).  Sec. 4.3 of the paper groups
 // tokens by the experts that consume them; Sec. 4.5 sends each destination only its rows.
+// The same kernel groups only a window of experts (the receive side of the dense design,
+// Sec. 4.2-4.3: a rank groups the tokens it gathered by the experts it owns); entries
+// naming other experts get no row and are not errors.
 //
 // One kernel, one workgroup per tile of the routing array, all workgroups resident at
 // once.  A workgroup has W waves; each wave owns a contiguous run of `rounds` x 64 entries.
@@ -93,16 +96,26 @@ __device__ __forceinline__ bool repeats_in_row(const LayoutArgs &a, int e, bool 
     return dup;
 }
 
+// An id names one of the grouped experts when it falls in the window [e_lo, e_lo + E).
+__device__ __forceinline__ bool in_window(const LayoutArgs &a, int id) {
+    return (unsigned)(id - a.e_lo) < (unsigned)a.E;
+}
+
 // Step 1 for one round: returns the entry's rank among this wave's entries of its expert
-// so far (-1 when it is not a valid entry) and bumps the wave's counter row.
-__device__ __forceinline__ int count_entry(const LayoutArgs &a, int e, int earlier, int64_t i, int lane,
+// so far (-1 when it does not name a grouped expert) and bumps the wave's counter row.
+
+__device__ __forceinline__ int count_entry(const LayoutArgs &a, int id, int earlier, int64_t i, int lane,
                                            int jslot, int *cnt, uint32_t &err) {
     const bool in_range = i < a.slots;
-    const bool valid = in_range && (unsigned)e < (unsigned)a.E;
+    const bool id_ok = in_range && (unsigned)id < (unsigned)a.all_E;
+    const bool valid = id_ok && in_window(a, id);
+    const int e = id - a.e_lo;
     const uint64_t m = match_expert(e, valid, a.nbits);
-    if (in_range && !valid)
+    if (in_range && !id_ok)
         err |= kRoutingIdOutOfRange;
-    if (repeats_in_row(a, e, valid, m, earlier, i, lane, jslot))
+    // duplicates are judged on the raw ids, also outside the window
+    const uint64_t m_all = a.E == a.all_E ? m : match_expert(id, id_ok, a.all_nbits);
+    if (repeats_in_row(a, id, id_ok, m_all, earlier, i, lane, jslot))
         err |= kRoutingDuplicate;
     int rank = -1;
     if (valid) {
@@ -365,7 +378,7 @@ __global__ __launch_bounds__(W * 64) void layout_kernel(LayoutArgs a, int32_t ro
                 break;
             const int64_t i = round_begin + lane;
             if (i < a.slots)
-                write_position(a, i, rank[r] >= 0 ? base[ids[r]] + rank[r] : -1);
+                write_position(a, i, rank[r] >= 0 ? base[ids[r] - a.e_lo] + rank[r] : -1);
         }
     } else {
         for (int r = 0; r < rounds; ++r) {
@@ -374,8 +387,9 @@ __global__ __launch_bounds__(W * 64) void layout_kernel(LayoutArgs a, int32_t ro
                 break;
             const int64_t i = round_begin + lane;
             const bool in_range = i < a.slots;
-            const int e = in_range ? a.topk_idx[i] : -1;
-            const bool valid = in_range && (unsigned)e < (unsigned)E;
+            const int id = in_range ? a.topk_idx[i] : -1;
+            const bool valid = in_range && (unsigned)id < (unsigned)a.all_E && in_window(a, id);
+            const int e = id - a.e_lo;
             const uint64_t m = match_expert(e, valid, a.nbits);
             int pos = -1;
             if (valid) {

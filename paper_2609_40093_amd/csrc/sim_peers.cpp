@@ -21,7 +21,7 @@ using Clock = std::chrono::steady_clock;
 struct Round {
     int32_t buf;
     uint32_t epoch;
-    int64_t rows;
+    int64_t rows;   // exchange staging: packed rows; dense staging: the phase (0 AG, 1 RS)
     int64_t delay_us;
     Clock::time_point posted;
     std::vector<int64_t> inbound_us, return_us;  // per sender
@@ -52,6 +52,7 @@ constexpr int64_t kGiveUpMs = 60 * 1000;
 
 struct ep_sim_peers {
     ep_staging *s = nullptr;
+    ep_dense *dense = nullptr;
     ep_sim_mode mode = EP_SIM_FLAGS_ONLY;
     std::thread th;
     std::mutex mu;
@@ -82,7 +83,28 @@ struct ep_sim_peers {
         }
     }
 
+    // dense staging: the other ranks' flags of one phase, in order of their delays
+    void serve_dense(const Round &r) {
+        ep_dense_view v;
+        if (ep_dense_get(dense, r.buf, &v) != EP_OK)
+            return;
+        const bool ag = r.rows == 0;
+        const std::vector<int64_t> &delay = ag ? r.inbound_us : r.return_us;
+        uint32_t *flags = ag ? v.ag_flags : v.rs_in_flags;
+        for (int i : by_delay(delay)) {
+            if (i == v.self_rank)
+                continue;
+            if (!sleep_until(r.posted + std::chrono::microseconds(delay[(size_t)i]), stop))
+                return;
+            __atomic_store_n(flags + i, r.epoch, __ATOMIC_RELEASE);
+        }
+    }
+
     void serve(const Round &r) {
+        if (dense) {
+            serve_dense(r);
+            return;
+        }
         ep_staging_view v;
         if (ep_staging_get(s, r.buf, &v) != EP_OK)
             return;
@@ -140,7 +162,7 @@ extern "C" ep_status ep_sim_peers_start(ep_staging *s, ep_sim_mode mode, ep_sim_
 
 extern "C" ep_status ep_sim_peers_post(ep_sim_peers *p, int32_t buf, uint32_t epoch, int64_t rows,
                                        int64_t delay_us) {
-    if (!p || rows < 0 || delay_us < 0)
+    if (!p || p->dense || rows < 0 || delay_us < 0)
         return EP_ERR_INVALID_ARG;
     ep_staging_view v;
     if (ep_staging_get(p->s, buf, &v) != EP_OK || rows > v.max_rows)
@@ -157,14 +179,56 @@ extern "C" ep_status ep_sim_peers_post(ep_sim_peers *p, int32_t buf, uint32_t ep
     return EP_OK;
 }
 
+namespace {
+int sim_ranks(ep_sim_peers *p) {
+    if (p->dense) {
+        ep_dense_view v;
+        return ep_dense_get(p->dense, 0, &v) == EP_OK ? v.num_ranks : -1;
+    }
+    ep_staging_view v;
+    return ep_staging_get(p->s, 0, &v) == EP_OK ? v.num_ranks : -1;
+}
+}  // namespace
+
+extern "C" ep_status ep_sim_dense_start(ep_dense *d, ep_sim_peers **out) {
+    if (!d || !out)
+        return EP_ERR_INVALID_ARG;
+    ep_dense_view v;
+    if (ep_dense_get(d, 0, &v) != EP_OK)
+        return EP_ERR_INVALID_ARG;
+    ep_sim_peers *p = new ep_sim_peers();
+    p->dense = d;
+    p->th = std::thread([p] { p->run(); });
+    *out = p;
+    return EP_OK;
+}
+
+extern "C" ep_status ep_sim_dense_post(ep_sim_peers *p, int32_t buf, uint32_t epoch, int32_t phase) {
+    if (!p || !p->dense || (phase != 0 && phase != 1))
+        return EP_ERR_INVALID_ARG;
+    ep_dense_view v;
+    if (ep_dense_get(p->dense, buf, &v) != EP_OK)
+        return EP_ERR_INVALID_ARG;
+    {
+        std::lock_guard<std::mutex> lk(p->mu);
+        Round r{buf, epoch, phase, 0, Clock::now(), p->inbound_us, p->return_us};
+        r.inbound_us.resize((size_t)v.num_ranks, 0);
+        r.return_us.resize((size_t)v.num_ranks, 0);
+        p->q.push_back(std::move(r));
+        ++p->posted;
+    }
+    p->cv.notify_one();
+    return EP_OK;
+}
+
 extern "C" ep_status ep_sim_peers_set_delays(ep_sim_peers *p, const int64_t *inbound_us, const int64_t *return_us) {
     if (!p)
         return EP_ERR_INVALID_ARG;
-    ep_staging_view v;
-    if (ep_staging_get(p->s, 0, &v) != EP_OK)
+    const int R = sim_ranks(p);
+    if (R < 1)
         return EP_ERR_INVALID_ARG;
-    std::vector<int64_t> in((size_t)v.num_ranks, 0), ret((size_t)v.num_ranks, 0);
-    for (int i = 0; i < v.num_ranks; ++i) {
+    std::vector<int64_t> in((size_t)R, 0), ret((size_t)R, 0);
+    for (int i = 0; i < R; ++i) {
         in[(size_t)i] = inbound_us ? inbound_us[i] : 0;
         ret[(size_t)i] = return_us ? return_us[i] : 0;
         if (in[(size_t)i] < 0 || ret[(size_t)i] < 0)
