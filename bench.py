@@ -13,6 +13,7 @@ has left the 256 MB Infinity Cache before it is used again.
 from __future__ import annotations
 
 import argparse
+import ctypes
 import hashlib
 import json
 import os
@@ -344,10 +345,12 @@ def bench_pinned(cfg, inp, y, args, dev) -> dict:
         if legs:
             modes[name]["legs"] = legs
             modes[name]["legs_note"] = "from a separate traced pass; events around DMA legs inflate their span"
+    dense = bench_dense(cfg, inp, args, dev, peaks)
     return {
         "steps": steps,
         "chunk_bytes": args.chunk_mib << 20,
         "modes": modes,
+        "dense_allgather_reducescatter": dense,
         "pcie_measured_peak_GBps": peaks,
         "pcie_published_peak_GBps": PCIE_PEAK_GBPS,
         "note": "default and per_sender move T*k rows each way per layer (one direction per phase); "
@@ -355,6 +358,93 @@ def bench_pinned(cfg, inp, y, args, dev) -> dict:
                 "results for them (symmetric traffic), so each phase uses both PCIe directions; the "
                 "duplex peak is the two-engine bidirectional probe",
     }
+
+
+def bench_dense(cfg, inp, args, dev, peaks) -> dict:
+    """The paper's adopted design for the same layer (Sec. 4.2): single-step All-Gather of
+    every rank's T tokens, grouping of the R*T gathered tokens by this rank's experts,
+    identity experts, partial blocks (bf16), Reduce-Scatter with GPU or partial host
+    reduction.  The other ranks' shards and blocks are seeded data their simulated peers
+    announce at once; their routing is this rank's routing rotated over the tokens (the
+    same distribution)."""
+    import numpy as np
+    import torch
+
+    import paper_2609_40093_amd as ep
+    from paper_2609_40093_amd import synth
+
+    T, H, E, k, R = cfg.T, cfg.H, cfg.E, cfg.k, cfg.R
+    me, L, nbuf = 0, cfg.E // cfg.R, 2
+    idx_all = np.concatenate([np.roll(inp.topk_idx, r * T // R, axis=0) for r in range(R)])
+    w_all = np.concatenate([np.roll(inp.topk_w, r * T // R, axis=0) for r in range(R)])
+    idx_d = torch.from_numpy(idx_all).to(dev)
+    w_d = torch.from_numpy(w_all).to(dev)
+    x = torch.from_numpy(inp.x.view(np.int16)).to(dev)
+    res = {}
+    for name, on_host in (("gpu_reduction", False), ("partial_host_reduction", True)):
+        d = ep.Dense(T, H, R, self_rank=me, num_buffers=nbuf)
+        d.set_policy(per_sender=True)
+        for b in range(nbuf):
+            hag, hin = d.host_array("ag", b), d.host_array("rs_in", b)
+            for r in range(R):
+                if r != me:
+                    rows = synth.normal_bf16_rows(np.random.SeedSequence([cfg.seed, 7, r]), T, H)
+                    hag[r * T:(r + 1) * T] = rows
+                    hin[r * T:(r + 1) * T] = rows
+        peers = ep.SimPeers(d)
+        lay = ep.dispatch_layout_local(idx_d, E, me * L, (me + 1) * L)
+        y_local = torch.empty((R * T * k, H), dtype=torch.int16, device=dev)   # every local row fits
+        blocks = torch.empty((R * T, H), dtype=torch.bfloat16, device=dev)
+        out = torch.empty((T, H), dtype=torch.bfloat16, device=dev)
+
+        def step(i):
+            buf, epoch = i % nbuf, i + 1
+            peers.post_dense(buf, epoch, "ag")
+            ep.allgather(d, x, buf=buf, epoch=epoch)
+            ep.dispatch_layout_local(idx_d, E, me * L, (me + 1) * L, out=lay)
+            g = d.views[buf].dev_gathered
+            # pack straight from the gathered device buffer (raw pointer of the staging)
+            ep.api._check(ep.api._lib_handle().ep_pack(ctypes.c_void_p(g), R * T, H, k, ep.api._ptr(lay.slot_pos),
+                                                       ep.api._ptr(y_local), y_local.shape[0],
+                                                       ep.api._stream_ptr(None)), "ep_pack")
+            ep.combine_rows(y_local, lay.slot_pos, w_d, blocks)
+            peers.post_dense(buf, epoch, "rs")
+            ep.reducescatter(d, blocks, num_tokens=T, out=out, reduce_on_host=on_host, buf=buf, epoch=epoch)
+
+        steps = max(5, args.steps // 4)
+        for i in range(args.warmup):
+            step(i)
+        d.status()
+        peers.drain()
+        up0, down0 = d.bytes_moved()
+        t0 = time.perf_counter()
+        for i in range(steps):
+            step(args.warmup + i)
+        d.status()
+        t1 = time.perf_counter()
+        up1, down1 = d.bytes_moved()
+        peers.drain()
+        # breakdown pass (not timed): kernels, gates and the host reduction
+        ep.trace_reset()
+        ep.trace_enable(True)
+        for i in range(steps):
+            step(args.warmup + steps + i)
+        d.status()
+        peers.drain()
+        ep.trace_enable(False)
+        ks = ep.trace_read()
+        peers.close()
+        d.close()
+        ms = (t1 - t0) * 1e3 / steps
+        pcie = ((up1 - up0) + (down1 - down0)) / steps
+        gbps = pcie / (ms * 1e-3) / 1e9
+        res[name] = {"us_per_layer": round(ms * 1e3, 1), "pcie_bytes_per_layer": int(pcie),
+                     "pcie_up_down_per_layer": [int((up1 - up0) / steps), int((down1 - down0) / steps)],
+                     "pcie_GBps": round(gbps, 2), "frac_of_measured_pcie_peak": round(gbps / peaks["both"], 3),
+                     "breakdown_avg_us": {kn: round(v["mean_ms"] * 1e3, 1) for kn, v in ks.items()}}
+    res["note"] = ("per-sender policy; payload per layer: All-Gather S up + (R-1)S down, Reduce-Scatter (R-1)S up "
+                   "and (R-1)S down (GPU reduction) or S down (host reduction), S = T*H*2 bytes")
+    return res
 
 
 def pcie_peaks(dev) -> dict:

@@ -510,7 +510,10 @@ extern "C" ep_status ep_reducescatter(ep_dense *d, int32_t buf, uint32_t epoch, 
                     }
                 }
             };
+            const auto t0 = std::chrono::steady_clock::now();
             pool->run(n, sum);
+            ep::trace_host("host_reduce",
+                           std::chrono::duration<double, std::milli>(std::chrono::steady_clock::now() - t0).count());
         };
         j.copies.push_back({nullptr, din + me * block, hin + me * block, block, dn, d->rs_landed(buf) + me});
         add_wait(waits, d->rs_landed(buf) + me);

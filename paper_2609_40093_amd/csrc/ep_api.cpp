@@ -122,6 +122,17 @@ void trace_submit(const char *name, TraceSlot slot) {
     g_pending.push_back({name, slot.start, slot.stop});
 }
 
+void trace_host(const char *name, double ms) {
+    if (!g_trace_on.load(std::memory_order_relaxed))
+        return;
+    std::lock_guard<std::mutex> lk(g_trace_mu);
+    Stat &s = g_stats[name];
+    s.count += 1;
+    s.total += ms;
+    s.mn = std::min(s.mn, ms);
+    s.mx = std::max(s.mx, ms);
+}
+
 }  // namespace ep
 
 // ---------------------------------------------------------------------------- misc

@@ -84,6 +84,8 @@ struct TraceSlot {
 TraceSlot trace_acquire();
 // Registers a launched pair under `name` (no-op for null events).
 void trace_submit(const char *name, TraceSlot slot);
+// Adds a host-timed span (milliseconds) under `name` while tracing is enabled.
+void trace_host(const char *name, double ms);
 
 // ---- kernel launchers (return the launch's hipError_t) ----------------------------
 struct LayoutArgs {
