@@ -158,6 +158,8 @@ typedef struct {
     uint32_t *in_landed;          /* host [num_ranks]: set to epoch once sender r's inbound rows are in dev_in */
     uint32_t *recv_landed;        /* host [num_ranks]: set to epoch once sender r's returned rows are in dev_recv */
     const int64_t *in_offsets;    /* host [num_ranks+1]: first dev_in/host_in row of each sender (last dispatch) */
+    uint32_t *send_credits;       /* host [num_ranks]: receiver r sets the round once it consumed this send buffer */
+    uint32_t *recv_credit;        /* host word: this rank sets the round once it consumed this recv buffer */
 } ep_staging_view;
 
 /* Pointers and sizes of buffer set `buf` (host pointers are usable from the host). */
@@ -236,6 +238,36 @@ ep_status ep_combine(ep_staging *s, int32_t buf, uint32_t epoch, const int32_t *
                      const int32_t *rank_offsets, const float *topk_w, int64_t num_tokens,
                      int32_t hidden, int32_t topk, void *out_dev, ep_out_dtype out_dtype,
                      hipStream_t stream);
+
+/* -------------------------------------------------- graph-replayed rounds (Sec. 4.5)
+ *
+ * For decode, where a captured HIP graph replays every layer.  The round number lives in
+ * device memory and every kernel of these calls reads it there, so the captured launches
+ * stay valid from one replay to the next; nothing is passed per round from the host.
+ * Buffer set b = round % 2 alternates (a PINNED_HOST staging with num_buffers == 2): a
+ * sender writes buffer set b only after every receiver has credited its contents of two
+ * rounds ago, and credits its own receive buffer once the reduction has read it (Sec. 4.4:
+ * receivers send credits by writes; the double buffer lets the next round start without
+ * a global synchronization).  The rows move on the compute units (stores to and loads from
+ * pinned host memory) because a captured DMA copy keeps the addresses recorded at capture
+ * (Sec. 4.5); at decode sizes the compute units are not the contended resource.
+ *   ep_round_advance   round += 1; the first call of each round (capture it too).
+ *   ep_dispatch_graph  waits for send_credits of buffer set b to reach round - 2, packs the
+ *                      rows straight into host_send of set b, then sets that set's
+ *                      send_flags[0] = round.
+ *   ep_combine_graph   waits for recv_flags of set b to reach round (every sender), reduces
+ *                      the rows straight from host_recv of set b, then sets recv_credit of
+ *                      set b = round.
+ * Arguments and results as for ep_dispatch / ep_combine (slot_pos from a layout whose
+ * workspace was zero-filled once: the layout is replay-safe too).  Graph rounds and the
+ * other legs must not be mixed on one staging. */
+ep_status ep_round_advance(ep_staging *s, hipStream_t stream);
+/* Synchronizes the device and reads the round counter. */
+ep_status ep_round_read(ep_staging *s, uint32_t *round);
+ep_status ep_dispatch_graph(const void *x_dev, int64_t num_tokens, int32_t hidden, int32_t topk,
+                            const int32_t *slot_pos, ep_staging *s, hipStream_t stream);
+ep_status ep_combine_graph(ep_staging *s, const int32_t *slot_pos, const float *topk_w, int64_t num_tokens,
+                           int32_t hidden, int32_t topk, void *out_dev, ep_out_dtype out_dtype, hipStream_t stream);
 
 /* ------------------------------------------------------- dense collectives (Sec. 4.2)
  *

@@ -30,7 +30,7 @@ class StagingView(ctypes.Structure):
                 ("send_flags", c_vp), ("recv_flags", c_vp),
                 ("mode", c_u32), ("self_rank", c_i32), ("dev_in", c_vp), ("host_in", c_vp), ("host_ret", c_vp),
                 ("in_flags", c_vp), ("ret_flags", c_vp), ("in_landed", c_vp), ("recv_landed", c_vp),
-                ("in_offsets", c_vp)]
+                ("in_offsets", c_vp), ("send_credits", c_vp), ("recv_credit", c_vp)]
 
 
 class DenseView(ctypes.Structure):
@@ -64,6 +64,12 @@ SIGNATURES = {
     "ep_staging_set_inbound": (c_i32, [c_vp, c_i32, ctypes.POINTER(c_i64)]),
     "ep_dispatch": (c_i32, [c_vp, c_i64, c_i32, c_i32, c_vp, c_vp, c_vp, c_i32, c_u32, c_vp]),
     "ep_combine": (c_i32, [c_vp, c_i32, c_u32, c_vp, c_vp, c_vp, c_i64, c_i32, c_i32, c_vp, c_i32, c_vp]),
+    "ep_round_advance": (c_i32, [c_vp, c_vp]),
+    "ep_round_read": (c_i32, [c_vp, ctypes.POINTER(c_u32)]),
+    "ep_dispatch_graph": (c_i32, [c_vp, c_i64, c_i32, c_i32, c_vp, c_vp, c_vp]),
+    "ep_combine_graph": (c_i32, [c_vp, c_vp, c_vp, c_i64, c_i32, c_i32, c_vp, c_i32, c_vp]),
+    "ep_sim_graph_start": (c_i32, [c_vp, c_i64, c_i64, ctypes.POINTER(c_vp)]),
+    "ep_sim_graph_wait": (c_i32, [c_vp, c_u32, c_i64]),
     "ep_dense_alloc": (c_i32, [c_i64, c_i32, c_i32, c_i32, c_i32, c_i32, ctypes.POINTER(c_vp)]),
     "ep_dense_free": (c_i32, [c_vp]),
     "ep_dense_get": (c_i32, [c_vp, c_i32, ctypes.POINTER(DenseView)]),

@@ -23,7 +23,8 @@ MODE_PER_SENDER, MODE_DUPLEX, MODE_REMOTE_ONLY = _lib.EP_MODE_PER_SENDER, _lib.E
 __all__ = ["EPError", "Layout", "Staging", "SimPeers", "dispatch_layout", "layout_status", "dispatch",
            "combine", "trace_enable", "trace_read", "trace_reset", "copy_probe", "workspace_bytes",
            "pcie_probe", "MODE_PER_SENDER", "MODE_DUPLEX", "MODE_REMOTE_ONLY", "LocalLayout",
-           "dispatch_layout_local", "pack", "combine_rows", "Dense", "allgather", "reducescatter"]
+           "dispatch_layout_local", "pack", "combine_rows", "Dense", "allgather", "reducescatter",
+           "round_advance", "round_read", "dispatch_graph", "combine_graph"]
 
 _PAYLOAD_DTYPES = (torch.bfloat16, torch.int16, torch.uint16)
 
@@ -242,7 +243,8 @@ class Staging:
     # host views (pinned staging only): zero-copy numpy arrays over pinned memory
     _HOST_BUFFERS = {"send": "host_send", "recv": "host_recv", "in": "host_in", "ret": "host_ret"}
     _HOST_FLAGS = {"send_flags": "send_flags", "recv_flags": "recv_flags", "in_flags": "in_flags",
-                   "ret_flags": "ret_flags", "in_landed": "in_landed", "recv_landed": "recv_landed"}
+                   "ret_flags": "ret_flags", "in_landed": "in_landed", "recv_landed": "recv_landed",
+                   "send_credits": "send_credits", "recv_credit": "recv_credit"}
 
     def host_array(self, which: str, buf: int = 0) -> np.ndarray:
         v = self.views[buf]
@@ -256,7 +258,7 @@ class Staging:
             ptr = getattr(v, self._HOST_FLAGS[which])
             if not ptr:
                 raise ValueError("flags exist only with pinned staging")
-            n = self.max_chunks if which == "send_flags" else self.num_ranks
+            n = {"send_flags": self.max_chunks, "recv_credit": 1}.get(which, self.num_ranks)
             return np.ctypeslib.as_array(ctypes.cast(ptr, ctypes.POINTER(ctypes.c_uint32)), shape=(n,))
         if which == "in_offsets":
             return np.ctypeslib.as_array(ctypes.cast(v.in_offsets, ctypes.POINTER(ctypes.c_int64)),
@@ -437,18 +439,61 @@ def reducescatter(dense: Dense, blocks: torch.Tensor, *, num_tokens: int, out: O
     return out
 
 
+def round_advance(staging: Staging, stream=None) -> None:
+    """ep_round_advance: next graph-replayed round (device-side counter)."""
+    _check(_lib_handle().ep_round_advance(staging.handle, _stream_ptr(stream)), "ep_round_advance")
+
+
+def round_read(staging: Staging) -> int:
+    r = ctypes.c_uint32()
+    _check(_lib_handle().ep_round_read(staging.handle, ctypes.byref(r)), "ep_round_read")
+    return r.value
+
+
+def dispatch_graph(x: torch.Tensor, slot_pos: torch.Tensor, staging: Staging, *, topk: int, stream=None) -> None:
+    """ep_dispatch_graph: pack x into the pinned send buffer of set round % 2 (replay-safe)."""
+    _need(x, "x", _PAYLOAD_DTYPES, 2)
+    _need(slot_pos, "slot_pos", (torch.int32,), 1)
+    T, H = x.shape
+    if slot_pos.numel() != T * topk:
+        raise ValueError("slot_pos must hold T*topk entries")
+    _check(_lib_handle().ep_dispatch_graph(_ptr(x), T, H, topk, _ptr(slot_pos), staging.handle, _stream_ptr(stream)),
+           "ep_dispatch_graph")
+
+
+def combine_graph(staging: Staging, slot_pos: torch.Tensor, topk_w: torch.Tensor, out: torch.Tensor,
+                  stream=None) -> torch.Tensor:
+    """ep_combine_graph: reduce the returned rows of set round % 2 straight from pinned memory."""
+    _need(topk_w, "topk_w", (torch.float32,), 2)
+    _need(slot_pos, "slot_pos", (torch.int32,), 1)
+    T, k = topk_w.shape
+    code = EP_OUT_F32 if out.dtype == torch.float32 else EP_OUT_BF16
+    if tuple(out.shape) != (T, staging.hidden) or slot_pos.numel() != T * k:
+        raise ValueError("shape mismatch between out, topk_w and slot_pos")
+    _check(_lib_handle().ep_combine_graph(staging.handle, _ptr(slot_pos), _ptr(topk_w), T, staging.hidden, k,
+                                          _ptr(out), code, _stream_ptr(stream)), "ep_combine_graph")
+    return out
+
+
 class SimPeers:
     """Host thread standing in for the peer ranks of a pinned staging (include/ep_sim.h)."""
 
-    def __init__(self, staging, echo: bool = False):
+    def __init__(self, staging, echo: bool = False, graph_rows: Optional[int] = None, graph_delay_us: int = 0):
         handle = ctypes.c_void_p()
-        if isinstance(staging, Dense):
+        if graph_rows is not None:
+            _check(_lib_handle().ep_sim_graph_start(staging.handle, graph_rows, graph_delay_us, ctypes.byref(handle)),
+                   "ep_sim_graph_start")
+        elif isinstance(staging, Dense):
             _check(_lib_handle().ep_sim_dense_start(staging.handle, ctypes.byref(handle)), "ep_sim_dense_start")
         else:
             _check(_lib_handle().ep_sim_peers_start(staging.handle, EP_SIM_ECHO if echo else EP_SIM_FLAGS_ONLY,
                                                     ctypes.byref(handle)), "ep_sim_peers_start")
         self.handle = handle
         self.staging = staging  # keep the staging alive while the thread reads it
+
+    def wait_round(self, round_: int, timeout_ms: int = 60000) -> None:
+        """Graph rounds: block until the peers finished round `round_`."""
+        _check(_lib_handle().ep_sim_graph_wait(self.handle, round_ & 0xFFFFFFFF, timeout_ms), "ep_sim_graph_wait")
 
     def post_dense(self, buf: int, epoch: int, phase: str) -> None:
         """Dense staging: announce the other ranks' shards ("ag") or blocks ("rs")."""

@@ -33,8 +33,11 @@ __global__ __launch_bounds__(256) void combine_kernel(const u32x4 *__restrict__ 
                                                       const int32_t *__restrict__ slot_pos,
                                                       const float *__restrict__ topk_w, int64_t T,
                                                       int32_t V, int32_t chunks, int32_t k,
-                                                      void *__restrict__ out, int64_t max_rows) {
+                                                      void *__restrict__ out, int64_t max_rows,
+                                                      RoundSel sel) {
     const int lane = threadIdx.x & (kWave - 1);
+    if (sel.round && (__hip_atomic_load(sel.round, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) & 1u))
+        recv = static_cast<const u32x4 *>(sel.alt);
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
     const int64_t item = (int64_t)blockIdx.x * (blockDim.x / kWave) + wave;
     const int64_t t = item / chunks;
@@ -107,7 +110,7 @@ __global__ __launch_bounds__(256) void combine_kernel(const u32x4 *__restrict__ 
 template <int U, int KC>
 hipError_t launch_uk(const void *recv, const int32_t *slot_pos, const float *topk_w, int64_t T,
                      int32_t V, int32_t k, void *out, bool out_f32, int64_t max_rows,
-                     hipStream_t stream) {
+                     hipStream_t stream, RoundSel sel) {
     const int32_t chunks = (V + U * kWave - 1) / (U * kWave);
     const int64_t items = T * chunks;
     const int waves_per_block = 4;
@@ -117,11 +120,11 @@ hipError_t launch_uk(const void *recv, const int32_t *slot_pos, const float *top
     if (out_f32)
         hipExtLaunchKernelGGL(combine_kernel<U, KC, true>, dim3((unsigned)blocks),
                               dim3(waves_per_block * kWave), 0, stream, ts.start, ts.stop, 0,
-                              (const u32x4 *)recv, slot_pos, topk_w, T, V, chunks, k, out, max_rows);
+                              (const u32x4 *)recv, slot_pos, topk_w, T, V, chunks, k, out, max_rows, sel);
     else
         hipExtLaunchKernelGGL(combine_kernel<U, KC, false>, dim3((unsigned)blocks),
                               dim3(waves_per_block * kWave), 0, stream, ts.start, ts.stop, 0,
-                              (const u32x4 *)recv, slot_pos, topk_w, T, V, chunks, k, out, max_rows);
+                              (const u32x4 *)recv, slot_pos, topk_w, T, V, chunks, k, out, max_rows, sel);
     hipError_t err = hipGetLastError();
     if (err == hipSuccess)
         trace_submit("combine", ts);
@@ -132,18 +135,18 @@ hipError_t launch_uk(const void *recv, const int32_t *slot_pos, const float *top
 
 hipError_t launch_combine(const void *recv, const int32_t *slot_pos, const float *topk_w,
                           int64_t T, int32_t H, int32_t k, void *out, bool out_f32,
-                          int64_t max_rows, hipStream_t stream) {
+                          int64_t max_rows, hipStream_t stream, RoundSel sel) {
     if (T == 0)
         return hipSuccess;
     const int32_t V = H / 8;
     // KC*U 16-byte loads per lane in flight: 16 for k >= 8, fewer accumulators for small k
     if (k >= 8)
-        return launch_uk<2, 8>(recv, slot_pos, topk_w, T, V, k, out, out_f32, max_rows, stream);
+        return launch_uk<2, 8>(recv, slot_pos, topk_w, T, V, k, out, out_f32, max_rows, stream, sel);
     if (k >= 4)
-        return launch_uk<4, 4>(recv, slot_pos, topk_w, T, V, k, out, out_f32, max_rows, stream);
+        return launch_uk<4, 4>(recv, slot_pos, topk_w, T, V, k, out, out_f32, max_rows, stream, sel);
     if (k >= 2)
-        return launch_uk<4, 2>(recv, slot_pos, topk_w, T, V, k, out, out_f32, max_rows, stream);
-    return launch_uk<4, 1>(recv, slot_pos, topk_w, T, V, k, out, out_f32, max_rows, stream);
+        return launch_uk<4, 2>(recv, slot_pos, topk_w, T, V, k, out, out_f32, max_rows, stream, sel);
+    return launch_uk<4, 1>(recv, slot_pos, topk_w, T, V, k, out, out_f32, max_rows, stream, sel);
 }
 
 }  // namespace ep

@@ -330,6 +330,7 @@ void staging_release(ep_staging *s) {
     if (s->ev_sysrel) (void)hipEventDestroy(s->ev_sysrel);
     if (s->flags) (void)hipHostFree(s->flags);
     if (s->dev_epoch) (void)hipFree(s->dev_epoch);
+    if (s->dev_round) (void)hipFree(s->dev_round);
     for (hipStream_t st : {s->up, s->down})
         if (st) (void)hipStreamDestroy(st);
     delete s;
@@ -411,6 +412,8 @@ extern "C" ep_status ep_staging_alloc(ep_staging_kind kind, int64_t max_rows, in
         EP_ALLOC_HIP(hipStreamCreateWithFlags(&s->up, hipStreamNonBlocking));
         EP_ALLOC_HIP(hipStreamCreateWithFlags(&s->down, hipStreamNonBlocking));
         EP_ALLOC_HIP(hipMalloc((void **)&s->dev_epoch, kMaxBuffers * kEpochStride));
+        EP_ALLOC_HIP(hipMalloc((void **)&s->dev_round, 256));
+        EP_ALLOC_HIP(hipMemset(s->dev_round, 0, 256));
         EP_ALLOC_HIP(hipEventCreateWithFlags(&s->ev_sysrel, hipEventDisableTiming | hipEventReleaseToSystem));
         if (!d2h_through_hip()) {
             std::string err;
@@ -477,6 +480,8 @@ extern "C" ep_status ep_staging_get(ep_staging *s, int32_t buf, ep_staging_view 
     v->in_landed = pinned ? s->in_landed(buf) : nullptr;
     v->recv_landed = pinned ? s->recv_landed(buf) : nullptr;
     v->in_offsets = &s->off_in[(size_t)buf * (s->num_ranks + 1)];
+    v->send_credits = pinned ? s->send_credit(buf) : nullptr;
+    v->recv_credit = pinned ? s->recv_credit(buf) : nullptr;
     return EP_OK;
 }
 
@@ -708,6 +713,88 @@ extern "C" ep_status ep_combine(ep_staging *s, int32_t buf, uint32_t epoch, cons
     }
     EP_HIP(ep::launch_combine(s->dev_recv[buf], slot_pos, topk_w, num_tokens, hidden, topk, out_dev,
                               out_dtype == EP_OUT_F32, s->max_rows, stream));
+    return EP_OK;
+}
+
+// ----------------------------------------------------------- graph-replayed rounds
+
+namespace {
+
+ep_status check_graph(const ep_staging *s, const char *who) {
+    if (!s)
+        return fail(EP_ERR_INVALID_ARG, "%s: staging is NULL", who);
+    if (s->kind != EP_STAGING_PINNED_HOST || s->num_buffers != 2)
+        return fail(EP_ERR_INVALID_ARG, "%s: graph rounds need a PINNED_HOST staging with 2 buffer sets", who);
+    if (s->num_ranks > 64)
+        return fail(EP_ERR_INVALID_ARG, "%s: at most 64 ranks, have %d", who, s->num_ranks);
+    return check_device(s, who);
+}
+
+}  // namespace
+
+extern "C" ep_status ep_round_advance(ep_staging *s, hipStream_t stream) {
+    ep_status st = check_graph(s, "ep_round_advance");
+    if (st != EP_OK)
+        return st;
+    EP_HIP(ep::launch_round_advance(s->dev_round, stream));
+    return EP_OK;
+}
+
+extern "C" ep_status ep_round_read(ep_staging *s, uint32_t *round) {
+    ep_status st = check_graph(s, "ep_round_read");
+    if (st != EP_OK)
+        return st;
+    if (!round)
+        return fail(EP_ERR_INVALID_ARG, "ep_round_read: round is NULL");
+    EP_HIP(hipDeviceSynchronize());
+    EP_HIP(hipMemcpy(round, s->dev_round, sizeof(uint32_t), hipMemcpyDeviceToHost));
+    return EP_OK;
+}
+
+extern "C" ep_status ep_dispatch_graph(const void *x_dev, int64_t num_tokens, int32_t hidden, int32_t topk,
+                                       const int32_t *slot_pos, ep_staging *s, hipStream_t stream) {
+    ep_status st = check_graph(s, "ep_dispatch_graph");
+    if (st == EP_OK)
+        st = check_round(s, "ep_dispatch_graph", num_tokens, hidden, topk, 0, slot_pos);
+    if (st != EP_OK)
+        return st;
+    if (num_tokens > 0 && (!x_dev || !aligned16(x_dev)))
+        return fail(EP_ERR_INVALID_ARG, "ep_dispatch_graph: x must be a non-NULL 16-byte aligned pointer");
+    const int64_t ticks = s->timeout_us * s->wall_clock_khz / 1000;
+    // buffer set round % 2 is free once every receiver credited its contents of two rounds ago
+    EP_HIP(ep::launch_round_gate("wait_credits", s->dev_round, s->send_credit(0), s->num_ranks, s->num_ranks, -2,
+                                 ticks, s->sleep_units, s->status(), stream));
+    ep::RoundSel sel;
+    sel.alt = s->host_send[1];
+    sel.round = s->dev_round;
+    EP_HIP(ep::launch_pack(x_dev, num_tokens, hidden, topk, slot_pos, s->host_send[0], s->max_rows, nullptr, 0, stream,
+                           sel, true));
+    EP_HIP(ep::launch_round_stamp(s->dev_round, s->send_flags(0), s->max_chunks, 1, stream));
+    return EP_OK;
+}
+
+extern "C" ep_status ep_combine_graph(ep_staging *s, const int32_t *slot_pos, const float *topk_w,
+                                      int64_t num_tokens, int32_t hidden, int32_t topk, void *out_dev,
+                                      ep_out_dtype out_dtype, hipStream_t stream) {
+    ep_status st = check_graph(s, "ep_combine_graph");
+    if (st == EP_OK)
+        st = check_round(s, "ep_combine_graph", num_tokens, hidden, topk, 0, slot_pos);
+    if (st != EP_OK)
+        return st;
+    if (out_dtype != EP_OUT_BF16 && out_dtype != EP_OUT_F32)
+        return fail(EP_ERR_INVALID_ARG, "ep_combine_graph: unknown out_dtype %d", (int)out_dtype);
+    if (num_tokens > 0 && (!topk_w || !out_dev || !aligned16(out_dev)))
+        return fail(EP_ERR_INVALID_ARG, "ep_combine_graph: topk_w and a 16-byte aligned out are required");
+    const int64_t ticks = s->timeout_us * s->wall_clock_khz / 1000;
+    EP_HIP(ep::launch_round_gate("wait_returned", s->dev_round, s->recv_flags(0), s->num_ranks, s->num_ranks, 0,
+                                 ticks, s->sleep_units, s->status(), stream));
+    ep::RoundSel sel;
+    sel.alt = s->host_recv[1];
+    sel.round = s->dev_round;
+    EP_HIP(ep::launch_combine(s->host_recv[0], slot_pos, topk_w, num_tokens, hidden, topk, out_dev,
+                              out_dtype == EP_OUT_F32, s->max_rows, stream, sel));
+    // the returned rows of this round are consumed: credit the buffer set to the senders
+    EP_HIP(ep::launch_round_stamp(s->dev_round, s->recv_credit(0), 1, 1, stream));
     return EP_OK;
 }
 

@@ -105,14 +105,24 @@ struct LayoutArgs {
 };
 hipError_t launch_layout(LayoutArgs a, hipStream_t stream);
 
+// Buffer chosen at run time by the parity of a round counter in device memory (graph-
+// replayed rounds): `alt` replaces the kernel's buffer argument on odd rounds.  No choice
+// when `round` is null.
+struct RoundSel {
+    const void *alt = nullptr;
+    const uint32_t *round = nullptr;
+};
+
 // Also stores `epoch` into *epoch_word (when non-null) for the host leg's flag copies.
+// fence_system: every wave ends with a system-scope release (rows stored to host memory
+// are visible to the host before any later kernel runs).
 hipError_t launch_pack(const void *x, int64_t T, int32_t H, int32_t k, const int32_t *slot_pos,
                        void *packed, int64_t max_rows, uint32_t *epoch_word, uint32_t epoch,
-                       hipStream_t stream);
+                       hipStream_t stream, RoundSel sel = {}, bool fence_system = false);
 
 hipError_t launch_combine(const void *recv, const int32_t *slot_pos, const float *topk_w,
                           int64_t T, int32_t H, int32_t k, void *out, bool out_f32,
-                          int64_t max_rows, hipStream_t stream);
+                          int64_t max_rows, hipStream_t stream, RoundSel sel = {});
 
 // One lane per flag polls flags[i] until (int32)(flags[i] - epoch) >= 0, at most
 // timeout_ticks of the constant-rate wall clock; on expiry stores EP_ERR_TIMEOUT to *status.
@@ -152,6 +162,18 @@ struct BlockList {
 // accumulation in list order; blocks bf16 or fp32 (f32_in), out bf16 (nearest-even) or fp32.
 hipError_t launch_block_reduce(const BlockList &bl, bool f32_in, int64_t n, void *out, bool f32_out,
                                hipStream_t stream);
+
+// Round-counter kernels of graph-replayed rounds (signal.hip):
+//   launch_round_advance: *round += 1;
+//   launch_round_gate: waits until flags[(round % 2) * stride + i] - (round + delta) >= 0
+//     (signed) for i < n, bounded like the other flag waits;
+//   launch_round_stamp: after a system-scope release, words[(round % 2) * stride + i] =
+//     round for i < n.
+hipError_t launch_round_advance(uint32_t *round, hipStream_t stream);
+hipError_t launch_round_gate(const char *name, const uint32_t *round, const uint32_t *flags, int32_t stride,
+                             int32_t n, int32_t delta, int64_t timeout_ticks, int32_t sleep_units, uint32_t *status,
+                             hipStream_t stream);
+hipError_t launch_round_stamp(const uint32_t *round, uint32_t *words, int32_t stride, int32_t n, hipStream_t stream);
 
 hipError_t launch_copy(void *dst, const void *src, size_t bytes, hipStream_t stream);
 

@@ -26,10 +26,13 @@ __global__ __launch_bounds__(256) void pack_kernel(const u32x4 *__restrict__ x, 
                                                    int32_t chunks, int32_t k,
                                                    const int32_t *__restrict__ slot_pos,
                                                    u32x4 *__restrict__ packed, int64_t max_rows,
-                                                   uint32_t *epoch_word, uint32_t epoch) {
+                                                   uint32_t *epoch_word, uint32_t epoch, RoundSel sel,
+                                                   bool fence_system) {
     const int lane = threadIdx.x & (kWave - 1);
     if (epoch_word && blockIdx.x == 0 && threadIdx.x == 0)
         *epoch_word = epoch;
+    if (sel.round && (__hip_atomic_load(sel.round, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) & 1u))
+        packed = static_cast<u32x4 *>(const_cast<void *>(sel.alt));
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
     const int64_t item = (int64_t)blockIdx.x * (blockDim.x / kWave) + wave;
     const int64_t t = item / chunks;
@@ -56,6 +59,8 @@ __global__ __launch_bounds__(256) void pack_kernel(const u32x4 *__restrict__ x, 
                 __builtin_nontemporal_store(d[u], dst + v);
         }
     }
+    if (fence_system)
+        __threadfence_system();
 }
 
 // One wave per (token, chunk, slot), the k waves of a chunk adjacent: each wave writes a
@@ -66,10 +71,13 @@ __global__ __launch_bounds__(256) void pack_slot_kernel(const u32x4 *__restrict_
                                                         int32_t chunks, int32_t k,
                                                         const int32_t *__restrict__ slot_pos,
                                                         u32x4 *__restrict__ packed, int64_t max_rows,
-                                                        uint32_t *epoch_word, uint32_t epoch) {
+                                                        uint32_t *epoch_word, uint32_t epoch, RoundSel sel,
+                                                        bool fence_system) {
     const int lane = threadIdx.x & (kWave - 1);
     if (epoch_word && blockIdx.x == 0 && threadIdx.x == 0)
         *epoch_word = epoch;
+    if (sel.round && (__hip_atomic_load(sel.round, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) & 1u))
+        packed = static_cast<u32x4 *>(const_cast<void *>(sel.alt));
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
     const int64_t item = (int64_t)blockIdx.x * (blockDim.x / kWave) + wave;
     const int64_t tc = item / k;
@@ -95,13 +103,15 @@ __global__ __launch_bounds__(256) void pack_slot_kernel(const u32x4 *__restrict_
         if (v < V)
             __builtin_nontemporal_store(d[u], dst + v);
     }
+    if (fence_system)
+        __threadfence_system();
 }
 
 }  // namespace
 
 hipError_t launch_pack(const void *x, int64_t T, int32_t H, int32_t k, const int32_t *slot_pos,
                        void *packed, int64_t max_rows, uint32_t *epoch_word, uint32_t epoch,
-                       hipStream_t stream) {
+                       hipStream_t stream, RoundSel sel, bool fence_system) {
     if (T == 0)
         return hipSuccess;
     const int32_t V = H / 8;
@@ -115,11 +125,11 @@ hipError_t launch_pack(const void *x, int64_t T, int32_t H, int32_t k, const int
     if (per_slot)
         hipExtLaunchKernelGGL(pack_slot_kernel<kPackU>, dim3((unsigned)blocks), dim3(waves_per_block * kWave), 0,
                               stream, ts.start, ts.stop, 0, (const u32x4 *)x, T, V, chunks, k, slot_pos,
-                              (u32x4 *)packed, max_rows, epoch_word, epoch);
+                              (u32x4 *)packed, max_rows, epoch_word, epoch, sel, fence_system);
     else
         hipExtLaunchKernelGGL(pack_kernel<kPackU>, dim3((unsigned)blocks), dim3(waves_per_block * kWave), 0,
                               stream, ts.start, ts.stop, 0, (const u32x4 *)x, T, V, chunks, k, slot_pos,
-                              (u32x4 *)packed, max_rows, epoch_word, epoch);
+                              (u32x4 *)packed, max_rows, epoch_word, epoch, sel, fence_system);
     hipError_t err = hipGetLastError();
     if (err == hipSuccess)
         trace_submit("pack", ts);

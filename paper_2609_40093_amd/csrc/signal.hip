@@ -101,7 +101,92 @@ __global__ __launch_bounds__(64) void mirror_kernel(const int32_t *src, int32_t 
     __hip_atomic_store(host + n, epoch, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_SYSTEM);
 }
 
+// Graph-replayed rounds read their round number from device memory, so the captured
+// launches stay valid from one replay to the next.
+__global__ __launch_bounds__(64) void round_advance_kernel(uint32_t *round) {
+    if (threadIdx.x == 0)  // agent scope: every XCD's later kernels read the new value
+        __hip_atomic_fetch_add(round, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// Waits until flags[(round % 2) * stride + i] has reached round + delta, i < n (one lane
+// per flag, pausing between polls, bounded by the wall clock).
+__global__ __launch_bounds__(64) void round_gate_kernel(const uint32_t *round_ptr, const uint32_t *flags,
+                                                        int32_t stride, int32_t n, int32_t delta, int64_t timeout_ticks,
+                                                        int32_t sleep_units, uint32_t *status) {
+    const int32_t i = threadIdx.x;
+    if (i >= n)
+        return;
+    const uint32_t round = __hip_atomic_load(round_ptr, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    const uint32_t want = round + (uint32_t)delta;
+    const uint32_t *f = flags + (round & 1u) * (uint32_t)stride + i;
+    const int64_t t0 = wall_clock64();
+    for (;;) {
+        if ((int32_t)(__hip_atomic_load(f, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_SYSTEM) - want) >= 0)
+            break;
+        if (wall_clock64() - t0 > timeout_ticks) {
+            __hip_atomic_store(status, kStatusTimeout, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+            break;
+        }
+        for (int32_t s = 0; s < sleep_units; ++s)
+            __builtin_amdgcn_s_sleep(1);
+    }
+}
+
+// Publishes the round: after a system-scope release, words[(round % 2) * stride + i] =
+// round for i < n (a send flag, or a credit for a consumed buffer).
+__global__ __launch_bounds__(64) void round_stamp_kernel(const uint32_t *round_ptr, uint32_t *words, int32_t stride,
+                                                         int32_t n) {
+    const int32_t i = threadIdx.x;
+    if (i >= n)
+        return;
+    const uint32_t round = __hip_atomic_load(round_ptr, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    __hip_atomic_store(words + (round & 1u) * (uint32_t)stride + i, round, __ATOMIC_RELEASE,
+                       __HIP_MEMORY_SCOPE_SYSTEM);
+}
+
 }  // namespace
+
+hipError_t launch_round_advance(uint32_t *round, hipStream_t stream) {
+    (void)hipGetLastError();
+    TraceSlot ts = trace_acquire();
+    hipExtLaunchKernelGGL(round_advance_kernel, dim3(1), dim3(64), 0, stream, ts.start, ts.stop, 0, round);
+    hipError_t err = hipGetLastError();
+    if (err == hipSuccess)
+        trace_submit("round_advance", ts);
+    return err;
+}
+
+hipError_t launch_round_gate(const char *name, const uint32_t *round, const uint32_t *flags, int32_t stride,
+                             int32_t n, int32_t delta, int64_t timeout_ticks, int32_t sleep_units, uint32_t *status,
+                             hipStream_t stream) {
+    if (n <= 0)
+        return hipSuccess;
+    if (n > 64)
+        return hipErrorInvalidValue;
+    (void)hipGetLastError();
+    TraceSlot ts = trace_acquire();
+    hipExtLaunchKernelGGL(round_gate_kernel, dim3(1), dim3(64), 0, stream, ts.start, ts.stop, 0, round, flags, stride,
+                          n, delta, timeout_ticks, sleep_units, status);
+    hipError_t err = hipGetLastError();
+    if (err == hipSuccess)
+        trace_submit(name, ts);
+    return err;
+}
+
+hipError_t launch_round_stamp(const uint32_t *round, uint32_t *words, int32_t stride, int32_t n, hipStream_t stream) {
+    if (n <= 0)
+        return hipSuccess;
+    if (n > 64)
+        return hipErrorInvalidValue;
+    (void)hipGetLastError();
+    TraceSlot ts = trace_acquire();
+    hipExtLaunchKernelGGL(round_stamp_kernel, dim3(1), dim3(64), 0, stream, ts.start, ts.stop, 0, round, words,
+                          stride, n);
+    hipError_t err = hipGetLastError();
+    if (err == hipSuccess)
+        trace_submit("round_stamp", ts);
+    return err;
+}
 
 hipError_t launch_gate(const char *name, const GateArgs &g, hipStream_t stream) {
     if (g.n <= 0 || g.n > kMaxGate)

@@ -62,6 +62,50 @@ struct ep_sim_peers {
     int64_t posted = 0, answered = 0;
     std::atomic<int> timed_out{0};
     std::vector<int64_t> inbound_us, return_us;  // delays for rounds posted from now on
+    // graph-replayed rounds: the thread follows the rounds by itself (no posts)
+    bool graph = false;
+    int64_t graph_rows = 0, graph_delay_us = 0;
+    std::atomic<uint32_t> graph_done{0};
+
+    // Waits until (int32)(*w - want) >= 0; false on stop or after the give-up time.
+    bool wait_word(const uint32_t *w, uint32_t want) {
+        const auto t0 = Clock::now();
+        uint32_t spins = 0;
+        while ((int32_t)(__atomic_load_n(w, __ATOMIC_ACQUIRE) - want) < 0) {
+            _mm_pause();
+            if (++spins % 4096 == 0) {
+                if (stop)
+                    return false;
+                if (Clock::now() - t0 > std::chrono::milliseconds(kGiveUpMs)) {
+                    timed_out.store(1);
+                    return false;
+                }
+            }
+        }
+        return true;
+    }
+
+    // Round r uses buffer set r % 2: wait for this rank's send flag, wait until this rank
+    // credited the receive buffer of round r - 2, echo the rows (identity experts), credit
+    // the send buffer, then raise every sender's recv flag.
+    void run_graph() {
+        for (uint32_t r = 1;; ++r) {
+            ep_staging_view v;
+            if (ep_staging_get(s, (int32_t)(r & 1u), &v) != EP_OK)
+                return;
+            if (!wait_word(v.send_flags, r) || !wait_word(v.recv_credit, r - 2u))
+                return;
+            std::memcpy(v.host_recv, v.host_send, (size_t)(graph_rows * v.row_bytes));
+            for (int i = 0; i < v.num_ranks; ++i)
+                __atomic_store_n(v.send_credits + i, r, __ATOMIC_RELEASE);
+            if (graph_delay_us > 0 && !sleep_until(Clock::now() + std::chrono::microseconds(graph_delay_us), stop))
+                return;
+            for (int i = 0; i < v.num_ranks; ++i)
+                __atomic_store_n(v.recv_flags + i, r, __ATOMIC_RELEASE);
+            graph_done.store(r, std::memory_order_release);
+            done_cv.notify_all();
+        }
+    }
 
     void run() {
         for (;;) {
@@ -238,6 +282,33 @@ extern "C" ep_status ep_sim_peers_set_delays(ep_sim_peers *p, const int64_t *inb
     p->inbound_us = std::move(in);
     p->return_us = std::move(ret);
     return EP_OK;
+}
+
+extern "C" ep_status ep_sim_graph_start(ep_staging *s, int64_t rows, int64_t delay_us, ep_sim_peers **out) {
+    if (!s || !out || rows < 0 || delay_us < 0)
+        return EP_ERR_INVALID_ARG;
+    ep_staging_view v;
+    if (ep_staging_get(s, 0, &v) != EP_OK || v.kind != EP_STAGING_PINNED_HOST || v.num_buffers != 2 ||
+        rows > v.max_rows)
+        return EP_ERR_INVALID_ARG;
+    ep_sim_peers *p = new ep_sim_peers();
+    p->s = s;
+    p->graph = true;
+    p->graph_rows = rows;
+    p->graph_delay_us = delay_us;
+    p->th = std::thread([p] { p->run_graph(); });
+    *out = p;
+    return EP_OK;
+}
+
+extern "C" ep_status ep_sim_graph_wait(ep_sim_peers *p, uint32_t round, int64_t timeout_ms) {
+    if (!p || !p->graph)
+        return EP_ERR_INVALID_ARG;
+    std::unique_lock<std::mutex> lk(p->mu);
+    const bool ok = p->done_cv.wait_for(lk, std::chrono::milliseconds(timeout_ms), [&] {
+        return (int32_t)(p->graph_done.load(std::memory_order_acquire) - round) >= 0 || p->timed_out.load();
+    });
+    return ok && !p->timed_out.load() ? EP_OK : EP_ERR_TIMEOUT;
 }
 
 extern "C" ep_status ep_sim_peers_drain(ep_sim_peers *p, int64_t timeout_ms) {

@@ -68,10 +68,12 @@ struct ep_staging {
     void *host_send[ep::kMaxBuffers] = {}, *host_recv[ep::kMaxBuffers] = {};
     // coherent pinned words: send [nbuf][max_chunks], recv [nbuf][R], status, then
     // inbound [nbuf][R], returned-out [nbuf][R], inbound-landed [nbuf][R],
-    // recv-landed [nbuf][R], offsets mirror [nbuf][R+2]
+    // recv-landed [nbuf][R], offsets mirror [nbuf][R+2], send credits [nbuf][R],
+    // recv credits [nbuf]
     uint32_t *flags = nullptr;
     size_t flag_words = 0;
     char *dev_epoch = nullptr;       // device: the epoch of each buffer set's current round
+    uint32_t *dev_round = nullptr;   // device: round counter of graph-replayed rounds
     ep::SdmaLane *lane = nullptr;    // default device->host leg on one SDMA engine
     hipEvent_t ev_sysrel = nullptr;  // records a system-scope release before a DMA engine reads
     hipStream_t up = nullptr, down = nullptr;
@@ -105,8 +107,11 @@ struct ep_staging {
     uint32_t *in_landed(int b) const { return ext_base() + 2 * nb() * R() + (size_t)b * R(); }
     uint32_t *recv_landed(int b) const { return ext_base() + 3 * nb() * R() + (size_t)b * R(); }
     uint32_t *mirror(int b) const { return ext_base() + 4 * nb() * R() + (size_t)b * (R() + 2); }
+    uint32_t *send_credit(int b) const { return mirror(0) + nb() * (R() + 2) + (size_t)b * R(); }
+    uint32_t *recv_credit(int b) const { return send_credit(0) + nb() * R() + (size_t)b; }
     static size_t flag_words_for(int nbuf, int max_chunks, int R) {
-        return (size_t)nbuf * (max_chunks + R) + 1 + 4 * (size_t)nbuf * R + (size_t)nbuf * (R + 2);
+        return (size_t)nbuf * (max_chunks + R) + 1 + 4 * (size_t)nbuf * R + (size_t)nbuf * (R + 2) +
+               (size_t)nbuf * R + (size_t)nbuf;
     }
     uint32_t *epoch_word(int b) const { return reinterpret_cast<uint32_t *>(dev_epoch + b * ep::kEpochStride); }
 };
