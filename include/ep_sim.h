@@ -48,10 +48,11 @@ ep_status ep_sim_dense_post(ep_sim_peers *p, int32_t buf, uint32_t epoch, int32_
 /* Simulated peers of graph-replayed rounds (ep_round_advance, ep_dispatch_graph,
  * ep_combine_graph) on a PINNED_HOST staging with 2 buffer sets.  The thread follows the
  * rounds r = 1, 2, ... by itself: it waits for send_flags[0] of set r % 2 to reach r and
- * for this rank's recv_credit of that set to reach r - 2, echoes the first `rows` rows of
- * the send buffer into the recv buffer (identity experts), credits the send buffer
- * (send_credits = r), waits delay_us, and sets every sender's recv flag to r. */
-ep_status ep_sim_graph_start(ep_staging *s, int64_t rows, int64_t delay_us, ep_sim_peers **out);
+ * for this rank's recv_credit of that set to reach r - 2, with `echo` copies the first
+ * `rows` rows of the send buffer into the recv buffer (identity experts; otherwise the
+ * recv buffer keeps what the harness wrote), credits the send buffer (send_credits = r),
+ * waits delay_us, and sets every sender's recv flag to r. */
+ep_status ep_sim_graph_start(ep_staging *s, int64_t rows, int64_t delay_us, int32_t echo, ep_sim_peers **out);
 /* Blocks until the thread finished round `round` (or timeout_ms passed). */
 ep_status ep_sim_graph_wait(ep_sim_peers *p, uint32_t round, int64_t timeout_ms);
 /* Blocks until every posted round was answered (or timeout_ms passed). */

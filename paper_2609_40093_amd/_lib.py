@@ -68,7 +68,7 @@ SIGNATURES = {
     "ep_round_read": (c_i32, [c_vp, ctypes.POINTER(c_u32)]),
     "ep_dispatch_graph": (c_i32, [c_vp, c_i64, c_i32, c_i32, c_vp, c_vp, c_vp]),
     "ep_combine_graph": (c_i32, [c_vp, c_vp, c_vp, c_i64, c_i32, c_i32, c_vp, c_i32, c_vp]),
-    "ep_sim_graph_start": (c_i32, [c_vp, c_i64, c_i64, ctypes.POINTER(c_vp)]),
+    "ep_sim_graph_start": (c_i32, [c_vp, c_i64, c_i64, c_i32, ctypes.POINTER(c_vp)]),
     "ep_sim_graph_wait": (c_i32, [c_vp, c_u32, c_i64]),
     "ep_dense_alloc": (c_i32, [c_i64, c_i32, c_i32, c_i32, c_i32, c_i32, ctypes.POINTER(c_vp)]),
     "ep_dense_free": (c_i32, [c_vp]),

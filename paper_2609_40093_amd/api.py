@@ -481,8 +481,8 @@ class SimPeers:
     def __init__(self, staging, echo: bool = False, graph_rows: Optional[int] = None, graph_delay_us: int = 0):
         handle = ctypes.c_void_p()
         if graph_rows is not None:
-            _check(_lib_handle().ep_sim_graph_start(staging.handle, graph_rows, graph_delay_us, ctypes.byref(handle)),
-                   "ep_sim_graph_start")
+            _check(_lib_handle().ep_sim_graph_start(staging.handle, graph_rows, graph_delay_us, 1 if echo else 0,
+                                                    ctypes.byref(handle)), "ep_sim_graph_start")
         elif isinstance(staging, Dense):
             _check(_lib_handle().ep_sim_dense_start(staging.handle, ctypes.byref(handle)), "ep_sim_dense_start")
         else:

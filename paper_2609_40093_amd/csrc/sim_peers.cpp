@@ -65,6 +65,7 @@ struct ep_sim_peers {
     // graph-replayed rounds: the thread follows the rounds by itself (no posts)
     bool graph = false;
     int64_t graph_rows = 0, graph_delay_us = 0;
+    bool graph_echo = true;
     std::atomic<uint32_t> graph_done{0};
 
     // Waits until (int32)(*w - want) >= 0; false on stop or after the give-up time.
@@ -95,7 +96,8 @@ struct ep_sim_peers {
                 return;
             if (!wait_word(v.send_flags, r) || !wait_word(v.recv_credit, r - 2u))
                 return;
-            std::memcpy(v.host_recv, v.host_send, (size_t)(graph_rows * v.row_bytes));
+            if (graph_echo)
+                std::memcpy(v.host_recv, v.host_send, (size_t)(graph_rows * v.row_bytes));
             for (int i = 0; i < v.num_ranks; ++i)
                 __atomic_store_n(v.send_credits + i, r, __ATOMIC_RELEASE);
             if (graph_delay_us > 0 && !sleep_until(Clock::now() + std::chrono::microseconds(graph_delay_us), stop))
@@ -284,7 +286,8 @@ extern "C" ep_status ep_sim_peers_set_delays(ep_sim_peers *p, const int64_t *inb
     return EP_OK;
 }
 
-extern "C" ep_status ep_sim_graph_start(ep_staging *s, int64_t rows, int64_t delay_us, ep_sim_peers **out) {
+extern "C" ep_status ep_sim_graph_start(ep_staging *s, int64_t rows, int64_t delay_us, int32_t echo,
+                                        ep_sim_peers **out) {
     if (!s || !out || rows < 0 || delay_us < 0)
         return EP_ERR_INVALID_ARG;
     ep_staging_view v;
@@ -296,6 +299,7 @@ extern "C" ep_status ep_sim_graph_start(ep_staging *s, int64_t rows, int64_t del
     p->graph = true;
     p->graph_rows = rows;
     p->graph_delay_us = delay_us;
+    p->graph_echo = echo != 0;
     p->th = std::thread([p] { p->run_graph(); });
     *out = p;
     return EP_OK;

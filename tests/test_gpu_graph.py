@@ -25,7 +25,7 @@ def setup(T=256, H=1024, E=64, k=8, R=8, delay_us=0, seed=31):
     case = make_case("graph", T, H, E, k, R, "random", seed=seed, gates="uniform")
     rows = T * k
     st = ep.Staging("pinned", rows, H, R, num_buffers=2)
-    peers = ep.SimPeers(st, graph_rows=rows, graph_delay_us=delay_us)
+    peers = ep.SimPeers(st, echo=True, graph_rows=rows, graph_delay_us=delay_us)
     idx = torch.from_numpy(case.topk_idx).to(DEV)
     w = torch.from_numpy(case.topk_w).to(DEV)
     x = torch.zeros((T, H), dtype=torch.int16, device=DEV)
