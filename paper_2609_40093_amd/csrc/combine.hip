@@ -139,13 +139,14 @@ hipError_t launch_combine(const void *recv, const int32_t *slot_pos, const float
     if (T == 0)
         return hipSuccess;
     const int32_t V = H / 8;
-    // KC*U 16-byte loads per lane in flight: 16 for k >= 8, fewer accumulators for small k
+    // KC*U 16-byte loads per lane in flight: 16 for k >= 4, 4 for k = 2 and 3 (two-group
+    // chunks: more waves, which measured faster on MI355X than four-group chunks there)
     if (k >= 8)
         return launch_uk<2, 8>(recv, slot_pos, topk_w, T, V, k, out, out_f32, max_rows, stream, sel);
     if (k >= 4)
         return launch_uk<4, 4>(recv, slot_pos, topk_w, T, V, k, out, out_f32, max_rows, stream, sel);
     if (k >= 2)
-        return launch_uk<4, 2>(recv, slot_pos, topk_w, T, V, k, out, out_f32, max_rows, stream, sel);
+        return launch_uk<2, 2>(recv, slot_pos, topk_w, T, V, k, out, out_f32, max_rows, stream, sel);
     return launch_uk<4, 1>(recv, slot_pos, topk_w, T, V, k, out, out_f32, max_rows, stream, sel);
 }
 

@@ -4,26 +4,57 @@
 // gathered into one contiguous segment per destination (Sec. 2.2 of the paper).  The
 // kernel is HBM-bound: it reads each token row once and writes it k times.
 //
-// Mapping: one wave per (token, column chunk of 64*U 16-byte vectors).  The token index
-// is wave-uniform, so the k slot positions are scalar loads; each lane loads U 16-byte
-// vectors of the row (all in flight together) and stores them to the k destination rows.
-// Consecutive lanes touch consecutive 16-byte pieces of one row: every load and store is
-// a fully coalesced 1 KiB wave access.  Loads and stores are non-temporal (the rows are
-// touched once; streaming stores leave no dirty lines for the end-of-kernel writeback).
-// Which mapping is used follows bandwidth measured on MI355X: for rows of at most 4 KiB
-// with k >= 4, one wave per (token, chunk, slot).  Rows carry no reuse across
-// workgroups, so the workgroup-to-XCD placement needs no remapping.
+// Mapping: a row of V 16-byte vectors is G = ceil(V/64) groups of 64 (one vector per
+// lane); a wave moves one chunk of `gpc` groups (all its loads in flight together) of one
+// row.  Consecutive lanes touch consecutive 16-byte pieces of the row: every load and
+// store is a fully coalesced 1 KiB wave access.
+//   EXACT instances: V is a multiple of 64 and the chunk length U divides G, so every
+//     load and store is unconditional, at a compile-time offset;
+//   generic instances (rows whose length is not a multiple of 64 vectors, or G with no
+//     usable divisor): chunks of up to U groups; loads stay unconditional (a group past
+//     the chunk's end reloads the chunk's last group, a lane past the row's end reloads
+//     the row's last vector: L2 hits, no HBM traffic); stores are guarded.
+//
+// Which mapping is used follows bandwidth measured on MI355X with inputs outside the
+// memory-side cache:
+//   k < 4:  one wave per (token, chunk): the chunk is loaded once (non-temporal) and
+//           stored to the k rows;
+//   k >= 4: one wave per (token, chunk, slot), the k waves of a chunk adjacent: each wave
+//           writes a single destination row; the chunk's loads after the first come from
+//           L2 (cached loads), and each wave feeds one write stream instead of k;
+//   chunk:  the largest divisor of G of at most 16 groups (16 KiB): a whole row for rows
+//           up to 16 KiB; long exact chunks measured faster than 4-group chunks and than
+//           16-group chunks with guarded tails.  Rows with no divisor of at least 4 groups
+//           (G a prime above 16) use the generic 16-group instance.
+// Stores are non-temporal (rows are written once; streaming stores leave no dirty lines
+// for the end-of-kernel writeback).  Rows carry no reuse across workgroups, so the
+// workgroup-to-XCD placement needs no remapping.
 #include "ep_internal.h"
 
 namespace ep {
 namespace {
 
-constexpr int kPackU = 4;  // 16-byte vectors per lane per chunk
+struct PackGeom {
+    int32_t V;       // 16-byte vectors per row
+    int32_t G;       // groups of 64 vectors per row
+    int32_t gpc;     // groups per chunk (<= the kernel's U)
+    int32_t chunks;  // chunks per row
+};
+
+// Vector of the row that lane `lane` loads for group u of a generic chunk starting at
+// group g0 with ng groups: always inside the row.
+__device__ __forceinline__ int32_t load_index(int32_t g0, int u, int32_t ng, int lane, int32_t V) {
+    return min((g0 + min(u, ng - 1)) * kWave + lane, V - 1);
+}
+
+// Whether the store of group u of a generic chunk is inside the chunk and the row.
+__device__ __forceinline__ bool store_ok(int32_t g0, int u, int32_t ng, int lane, int32_t V) {
+    return u < ng && (g0 + u) * kWave + lane < V;
+}
 
 // One wave per (token, chunk): the chunk is loaded once and stored to the k rows.
-template <int U>
-__global__ __launch_bounds__(256) void pack_kernel(const u32x4 *__restrict__ x, int64_t T, int32_t V,
-                                                   int32_t chunks, int32_t k,
+template <int U, bool EXACT>
+__global__ __launch_bounds__(256) void pack_kernel(const u32x4 *__restrict__ x, int64_t T, PackGeom pg, int32_t k,
                                                    const int32_t *__restrict__ slot_pos,
                                                    u32x4 *__restrict__ packed, int64_t max_rows,
                                                    uint32_t *epoch_word, uint32_t epoch, RoundSel sel,
@@ -35,40 +66,35 @@ __global__ __launch_bounds__(256) void pack_kernel(const u32x4 *__restrict__ x, 
         packed = static_cast<u32x4 *>(const_cast<void *>(sel.alt));
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
     const int64_t item = (int64_t)blockIdx.x * (blockDim.x / kWave) + wave;
-    const int64_t t = item / chunks;
+    const int64_t t = item / pg.chunks;
     if (t >= T)
         return;
-    const int32_t v0 = (int32_t)(item - t * chunks) * (U * kWave);
-    const u32x4 *src = x + t * V;
+    const int32_t g0 = (int32_t)(item - t * pg.chunks) * pg.gpc;
+    const int32_t ng = EXACT ? U : min(pg.gpc, pg.G - g0);  // wave-uniform, >= 1
+    const u32x4 *src = x + t * pg.V;
     u32x4 d[U];
 #pragma unroll
-    for (int u = 0; u < U; ++u) {
-        const int32_t v = v0 + u * kWave + lane;
-        d[u] = v < V ? __builtin_nontemporal_load(src + v) : u32x4{0u, 0u, 0u, 0u};
-    }
+    for (int u = 0; u < U; ++u)
+        d[u] = __builtin_nontemporal_load(src + (EXACT ? (g0 + u) * kWave + lane : load_index(g0, u, ng, lane, pg.V)));
     const int32_t *sp = slot_pos + t * k;
     for (int32_t j = 0; j < k; ++j) {
         const int64_t p = sp[j];
         if (p < 0 || p >= max_rows)
             continue;
-        u32x4 *dst = packed + p * V;
+        u32x4 *dst = packed + p * pg.V + g0 * kWave + lane;
 #pragma unroll
-        for (int u = 0; u < U; ++u) {
-            const int32_t v = v0 + u * kWave + lane;
-            if (v < V)
-                __builtin_nontemporal_store(d[u], dst + v);
-        }
+        for (int u = 0; u < U; ++u)
+            if (EXACT || store_ok(g0, u, ng, lane, pg.V))
+                __builtin_nontemporal_store(d[u], dst + u * kWave);
     }
     if (fence_system)
         __threadfence_system();
 }
 
 // One wave per (token, chunk, slot), the k waves of a chunk adjacent: each wave writes a
-// single destination row; the chunk's k reads after the first come from L2.  Faster for
-// narrow rows with many slots, where each wave otherwise feeds k write streams.
-template <int U>
-__global__ __launch_bounds__(256) void pack_slot_kernel(const u32x4 *__restrict__ x, int64_t T, int32_t V,
-                                                        int32_t chunks, int32_t k,
+// single destination row.
+template <int U, bool EXACT>
+__global__ __launch_bounds__(256) void pack_slot_kernel(const u32x4 *__restrict__ x, int64_t T, PackGeom pg, int32_t k,
                                                         const int32_t *__restrict__ slot_pos,
                                                         u32x4 *__restrict__ packed, int64_t max_rows,
                                                         uint32_t *epoch_word, uint32_t epoch, RoundSel sel,
@@ -82,30 +108,42 @@ __global__ __launch_bounds__(256) void pack_slot_kernel(const u32x4 *__restrict_
     const int64_t item = (int64_t)blockIdx.x * (blockDim.x / kWave) + wave;
     const int64_t tc = item / k;
     const int32_t j = (int32_t)(item - tc * k);
-    const int64_t t = tc / chunks;
+    const int64_t t = tc / pg.chunks;
     if (t >= T)
         return;
-    const int32_t v0 = (int32_t)(tc - t * chunks) * (U * kWave);
+    const int32_t g0 = (int32_t)(tc - t * pg.chunks) * pg.gpc;
+    const int32_t ng = EXACT ? U : min(pg.gpc, pg.G - g0);  // wave-uniform, >= 1
     const int64_t p = slot_pos[t * k + j];
     if (p < 0 || p >= max_rows)
         return;
-    const u32x4 *src = x + t * V;
-    u32x4 *dst = packed + p * V;
+    const u32x4 *src = x + t * pg.V;
+    u32x4 *dst = packed + p * pg.V + g0 * kWave + lane;
     u32x4 d[U];
 #pragma unroll
-    for (int u = 0; u < U; ++u) {
-        const int32_t v = v0 + u * kWave + lane;
-        d[u] = v < V ? src[v] : u32x4{0u, 0u, 0u, 0u};
-    }
+    for (int u = 0; u < U; ++u)
+        d[u] = src[EXACT ? (g0 + u) * kWave + lane : load_index(g0, u, ng, lane, pg.V)];
 #pragma unroll
-    for (int u = 0; u < U; ++u) {
-        const int32_t v = v0 + u * kWave + lane;
-        if (v < V)
-            __builtin_nontemporal_store(d[u], dst + v);
-    }
+    for (int u = 0; u < U; ++u)
+        if (EXACT || store_ok(g0, u, ng, lane, pg.V))
+            __builtin_nontemporal_store(d[u], dst + u * kWave);
     if (fence_system)
         __threadfence_system();
 }
+
+template <int U, bool EXACT>
+void launch_pack_u(bool per_slot, dim3 grid, hipStream_t stream, TraceSlot ts, const u32x4 *x, int64_t T,
+                   const PackGeom &pg, int32_t k, const int32_t *slot_pos, u32x4 *packed, int64_t max_rows,
+                   uint32_t *epoch_word, uint32_t epoch, RoundSel sel, bool fence_system) {
+    if (per_slot)
+        hipExtLaunchKernelGGL(pack_slot_kernel<U, EXACT>, grid, dim3(256), 0, stream, ts.start, ts.stop, 0, x, T, pg,
+                              k, slot_pos, packed, max_rows, epoch_word, epoch, sel, fence_system);
+    else
+        hipExtLaunchKernelGGL(pack_kernel<U, EXACT>, grid, dim3(256), 0, stream, ts.start, ts.stop, 0, x, T, pg, k,
+                              slot_pos, packed, max_rows, epoch_word, epoch, sel, fence_system);
+}
+
+// Chunk lengths with an EXACT instance (groups of 64 vectors), longest first.
+constexpr int kExactU[] = {16, 15, 14, 13, 12, 11, 10, 9, 8, 7, 6, 5, 4, 3, 2, 1};
 
 }  // namespace
 
@@ -114,22 +152,53 @@ hipError_t launch_pack(const void *x, int64_t T, int32_t H, int32_t k, const int
                        hipStream_t stream, RoundSel sel, bool fence_system) {
     if (T == 0)
         return hipSuccess;
-    const int32_t V = H / 8;
-    const int32_t chunks = (V + kPackU * kWave - 1) / (kPackU * kWave);
-    const bool per_slot = V <= 256 && k >= 4;   // rows of at most 4 KiB, many slots
-    const int64_t items = T * chunks * (per_slot ? k : 1);
-    const int waves_per_block = 4;
-    const int64_t blocks = (items + waves_per_block - 1) / waves_per_block;
+    PackGeom pg;
+    pg.V = H / 8;
+    pg.G = (pg.V + kWave - 1) / kWave;
+    const bool per_slot = k >= 4;
+    int exact = 0;  // chunk length of the EXACT instance, 0: generic
+    if (pg.V % kWave == 0)
+        for (int u : kExactU)
+            if (pg.G % u == 0) {
+                exact = u >= (pg.G < 4 ? pg.G : 4) ? u : 0;  // no short chunks for long rows
+                break;
+            }
+    pg.gpc = exact ? exact : (pg.G < 16 ? pg.G : 16);
+    pg.chunks = (pg.G + pg.gpc - 1) / pg.gpc;
+    const int64_t items = (per_slot ? T * k : T) * pg.chunks;
+    const int64_t blocks = (items + 3) / 4;  // 4 waves per workgroup
+    if (blocks > INT32_MAX)
+        return hipErrorInvalidValue;
+    const dim3 grid((unsigned)blocks);
+    const u32x4 *xv = static_cast<const u32x4 *>(x);
+    u32x4 *pv = static_cast<u32x4 *>(packed);
     (void)hipGetLastError();  // drop an error left by an earlier, already reported call
     TraceSlot ts = trace_acquire();
-    if (per_slot)
-        hipExtLaunchKernelGGL(pack_slot_kernel<kPackU>, dim3((unsigned)blocks), dim3(waves_per_block * kWave), 0,
-                              stream, ts.start, ts.stop, 0, (const u32x4 *)x, T, V, chunks, k, slot_pos,
-                              (u32x4 *)packed, max_rows, epoch_word, epoch, sel, fence_system);
-    else
-        hipExtLaunchKernelGGL(pack_kernel<kPackU>, dim3((unsigned)blocks), dim3(waves_per_block * kWave), 0,
-                              stream, ts.start, ts.stop, 0, (const u32x4 *)x, T, V, chunks, k, slot_pos,
-                              (u32x4 *)packed, max_rows, epoch_word, epoch, sel, fence_system);
+#define EP_PACK_ARGS per_slot, grid, stream, ts, xv, T, pg, k, slot_pos, pv, max_rows, epoch_word, epoch, sel, fence_system
+    switch (exact) {
+    case 16: launch_pack_u<16, true>(EP_PACK_ARGS); break;
+    case 15: launch_pack_u<15, true>(EP_PACK_ARGS); break;
+    case 14: launch_pack_u<14, true>(EP_PACK_ARGS); break;
+    case 13: launch_pack_u<13, true>(EP_PACK_ARGS); break;
+    case 12: launch_pack_u<12, true>(EP_PACK_ARGS); break;
+    case 11: launch_pack_u<11, true>(EP_PACK_ARGS); break;
+    case 10: launch_pack_u<10, true>(EP_PACK_ARGS); break;
+    case 9: launch_pack_u<9, true>(EP_PACK_ARGS); break;
+    case 8: launch_pack_u<8, true>(EP_PACK_ARGS); break;
+    case 7: launch_pack_u<7, true>(EP_PACK_ARGS); break;
+    case 6: launch_pack_u<6, true>(EP_PACK_ARGS); break;
+    case 5: launch_pack_u<5, true>(EP_PACK_ARGS); break;
+    case 4: launch_pack_u<4, true>(EP_PACK_ARGS); break;
+    case 3: launch_pack_u<3, true>(EP_PACK_ARGS); break;
+    case 2: launch_pack_u<2, true>(EP_PACK_ARGS); break;
+    case 1: launch_pack_u<1, true>(EP_PACK_ARGS); break;
+    default:
+        if (pg.gpc > 4)
+            launch_pack_u<16, false>(EP_PACK_ARGS);
+        else
+            launch_pack_u<4, false>(EP_PACK_ARGS);
+    }
+#undef EP_PACK_ARGS
     hipError_t err = hipGetLastError();
     if (err == hipSuccess)
         trace_submit("pack", ts);

@@ -102,6 +102,17 @@ CASES = [
     ("lastk_reversed", 700, 256, 64, 4, 4, "lastk"),
     ("roundrobin", 4096, 128, 256, 8, 8, "roundrobin"),
     ("single_token", 1, 7168, 256, 8, 8, "random"),
+    # row lengths (groups of 64 16-byte vectors) picking each pack chunk instance:
+    # exact chunks of 3, 6, 10, 11, 15, 16 and 9 (two chunks) groups; 17 groups (prime)
+    # takes the generic instance with a one-group tail chunk
+    ("rows_3_groups", 300, 1536, 16, 2, 4, "random"),
+    ("rows_6_groups_per_slot", 200, 3072, 32, 8, 8, "random"),
+    ("rows_10_groups", 300, 5120, 16, 4, 4, "random"),
+    ("rows_11_groups", 150, 5632, 16, 2, 4, "random"),
+    ("rows_15_groups", 100, 7680, 16, 2, 4, "random"),
+    ("rows_16_groups", 200, 8192, 8, 2, 4, "random"),
+    ("rows_18_groups_two_chunks", 100, 9216, 16, 2, 4, "random"),
+    ("rows_17_groups_generic", 120, 8704, 16, 4, 4, "random"),
 ]
 
 
