@@ -2,7 +2,9 @@
 
 A step is one MoE layer's communication share: dispatch layout, pack, and the
 gate-weighted combine of the returned rows (the peers' expert outputs are seeded data
-already in the receive buffer).  `value` is token payload throughput with HBM staging:
+already in the receive buffer).  Layout and pack are one call (ep_dispatch_fused), which
+runs them as one kernel when the layer has few experts (as the headline layer does) and
+as two kernels otherwise; the two-kernel path is also timed, for comparison.  `value` is token payload throughput with HBM staging:
 (dispatch payload + combine payload) / layer time, each payload T*k*2H bytes.  The same
 layer with pinned host staging (SDMA legs, host flags, simulated peers) is timed after
 it and reported under "pinned_staging"; that rate includes PCIe and is never `value`.
@@ -48,11 +50,18 @@ def algorithmic_bytes(cfg) -> dict:
     T, H, k = cfg.T, cfg.H, cfg.k
     n = T * k
     row = 2 * H
-    return {
+    out = {
         "pack": T * row + n * row + 4 * n,                  # read x once, write k copies, read slot_pos
         "combine": n * row + 8 * n + T * row,               # read k rows, gates and slot_pos, write out
         "layout": 4 * n + 4 * n + 4 * n,                    # read ids, write slot_pos and row_src
     }
+    # one kernel: read ids and x once, write k copies, slot_pos and row_src
+    out["layout_pack"] = T * row + n * row + 4 * n + 4 * n + 4 * n
+    return out
+
+
+KERNEL_SOURCES = {"pack": "pack.hip", "combine": "combine.hip", "layout": "layout.hip", "layout_pack": "fused.hip"}
+TIMED_KERNELS = ("layout_pack", "pack", "combine")
 
 
 def source_hash(name: str) -> str:
@@ -67,7 +76,7 @@ def committed_traffic(workload: str, kernel: str):
     if not os.path.exists(path):
         return None
     d = json.load(open(path))
-    if d.get("source_sha256") != source_hash(f"{kernel}.hip"):
+    if d.get("source_sha256") != source_hash(KERNEL_SOURCES.get(kernel, f"{kernel}.hip")):
         return None
     return d.get("traffic_bytes_per_launch")
 
@@ -112,15 +121,20 @@ def main():
         staging.write_device("recv", y_d, buf=s)
     torch.cuda.synchronize()
 
-    def step(i, trace=None):
-        """One layer; `trace` names the one kernel ("pack" or "combine") whose launch is
-        bracketed by timing events, so that measuring costs the host almost nothing."""
+    def step(i, trace=None, fused=True):
+        """One layer; `trace` names the call ("dispatch" or "combine") whose kernels are
+        bracketed by timing events, so that measuring costs the host almost nothing.
+        fused=False: layout and dispatch as two calls (two kernels)."""
         st = sets[i % nsets]
-        st["lay"] = ep.dispatch_layout(st["idx"], E, R, out=st["lay"])
-        if trace == "pack":
+        if trace == "dispatch":
             ep.trace_enable(True)
-        ep.dispatch(st["x"], st["lay"].slot_pos, staging, topk=k, buf=i % nsets, epoch=i + 1)
-        if trace == "pack":
+        if fused:
+            st["lay"] = ep.dispatch_fused(st["x"], st["idx"], E, R, staging, buf=i % nsets, epoch=i + 1,
+                                          out=st["lay"])
+        else:
+            st["lay"] = ep.dispatch_layout(st["idx"], E, R, out=st["lay"])
+            ep.dispatch(st["x"], st["lay"].slot_pos, staging, topk=k, buf=i % nsets, epoch=i + 1)
+        if trace == "dispatch":
             ep.trace_enable(False)
         elif trace == "combine":
             ep.trace_enable(True)
@@ -128,8 +142,8 @@ def main():
         if trace == "combine":
             ep.trace_enable(False)
 
-    # ---- HBM staging: warmup, then exactly K timed steps; pack and combine are timed
-    #      live with HIP events on the stream they run on
+    # ---- HBM staging: warmup, then exactly K timed steps; the dispatch and combine
+    #      kernels are timed live with HIP events on the stream they run on
     for i in range(args.warmup):
         step(i)
     ep.layout_status(sets[0]["lay"])
@@ -138,9 +152,9 @@ def main():
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     # one step in four carries timing events (they cost the stream ~2 us per traced
-    # launch), alternating between pack and combine
+    # launch), alternating between the dispatch and the combine
     for i in range(args.steps):
-        step(args.warmup + i, trace=("pack", None, "combine", None)[i % 4])
+        step(args.warmup + i, trace=("dispatch", None, "combine", None)[i % 4])
     t_issue = time.perf_counter()
     torch.cuda.synchronize()
     t1 = time.perf_counter()
@@ -159,19 +173,35 @@ def main():
     for name, st_ in breakdown.items():
         if name not in kstats:
             kstats[name] = st_
+    # the two-kernel path (layout, then pack) on the same steps, for comparison
+    for i in range(args.warmup):
+        step(i, fused=False)
+    torch.cuda.synchronize()
+    u0 = time.perf_counter()
+    for i in range(args.steps):
+        step(args.warmup + i, fused=False)
+    torch.cuda.synchronize()
+    two_ms = (time.perf_counter() - u0) * 1e3 / args.steps
+    ep.trace_reset()
+    ep.trace_enable(True)
+    for i in range(args.steps):
+        step(args.warmup + args.steps + i, fused=False)
+    torch.cuda.synchronize()
+    ep.trace_enable(False)
+    two_kernels = {name: round(st_["mean_ms"] * 1e3, 3) for name, st_ in ep.trace_read().items()}
 
     abytes = algorithmic_bytes(cfg)
     kernels = {}
     for name, st in kstats.items():
         us = st["mean_ms"] * 1e3
         entry = {"launches": st["count"], "avg_us": round(us, 3),
-                 "measured": "timed region" if name in ("pack", "combine") else "breakdown pass"}
+                 "measured": "timed region" if name in TIMED_KERNELS else "breakdown pass"}
         if name in abytes and us > 0:
             entry["algorithmic_bytes"] = abytes[name]
             entry["GBps"] = round(abytes[name] / (us * 1e-6) / 1e9, 1)
             entry["hbm_frac"] = round(entry["GBps"] / HBM_PEAK_GBPS, 4)
         kernels[name] = entry
-    dominant = max(("pack", "combine"), key=lambda nm: kernels.get(nm, {}).get("avg_us", 0.0))
+    dominant = max(TIMED_KERNELS, key=lambda nm: kernels.get(nm, {}).get("avg_us", 0.0))
     dk = kernels[dominant]
     traffic = committed_traffic(args.workload, dominant)
 
@@ -223,6 +253,12 @@ def main():
             "avg_launch_us": dk.get("avg_us"),
         },
         "kernels": kernels,
+        "two_kernel_dispatch": {
+            "note": "the same layer with layout and pack as two calls (two kernels); event-bracketed kernel averages",
+            "us_per_layer": round(two_ms * 1e3, 2),
+            "payload_GBps": round(2 * payload / (two_ms * 1e-3) / 1e9, 1),
+            "kernel_avg_us": two_kernels,
+        },
         "hbm_copy_probe_GBps": round(copy_gbps, 1),
     }
 

@@ -54,7 +54,7 @@
 extern "C" {
 #endif
 
-#define EP_ABI_VERSION 2
+#define EP_ABI_VERSION 3
 #define EP_MAX_EXPERTS 2048 /* largest E the layout kernels accept */
 
 typedef enum {
@@ -223,6 +223,25 @@ ep_status ep_staging_set_inbound(ep_staging *s, int32_t buf, const int64_t *rows
 ep_status ep_dispatch(const void *x_dev, int64_t num_tokens, int32_t hidden, int32_t topk,
                       const int32_t *slot_pos, const int32_t *rank_offsets, ep_staging *s,
                       int32_t buf, uint32_t epoch, hipStream_t stream);
+
+/* Layout and dispatch in one call: the same results as ep_dispatch_layout(topk_idx, ...)
+ * followed by ep_dispatch(x_dev, T, hidden, topk, slot_pos, rank_offsets, s, buf, epoch),
+ * bit for bit, and the same arguments, ownership and errors (the layout arguments as in
+ * ep_dispatch_layout, the rest as in ep_dispatch; every argument is checked before
+ * anything is enqueued).  Sec. 4.3 (tokens grouped by the experts that consume them)
+ * and Sec. 2.2 (rows packed into contiguous segments for the DMA engine).
+ * For few experts one kernel does both steps, each workgroup counting every routing
+ * entry itself (no exchange between workgroups, no second kernel): with HBM staging or
+ * the default pinned mode, E <= 32, topk in {1, 2, 4}, T*topk <= 65536, hidden a
+ * multiple of 512 with hidden/512 in {1, 2, 4, 8, 16}, and topk_idx 16-byte aligned.
+ * Otherwise the two steps run as their own kernels.  The fused kernel writes only the
+ * status word of the workspace. */
+ep_status ep_dispatch_fused(const int32_t *topk_idx, int64_t num_tokens, int32_t topk,
+                            int32_t num_experts, int32_t num_ranks, int32_t *expert_counts,
+                            int32_t *expert_offsets, int32_t *rank_counts, int32_t *rank_offsets,
+                            int32_t *slot_pos, int32_t *row_src, void *workspace, size_t workspace_bytes,
+                            const void *x_dev, int32_t hidden, ep_staging *s, int32_t buf, uint32_t epoch,
+                            hipStream_t stream);
 
 /* Combine of one round from buffer set `buf`:
  *   out[t][:] = sum_{j<k} topk_w[t*k+j] * recv[slot_pos[t*k+j]][:]

@@ -15,7 +15,7 @@ EP_STAGING_HBM, EP_STAGING_PINNED_HOST = 0, 1
 EP_OUT_BF16, EP_OUT_F32 = 0, 1
 EP_SIM_FLAGS_ONLY, EP_SIM_ECHO = 0, 1
 EP_MODE_PER_SENDER, EP_MODE_DUPLEX, EP_MODE_REMOTE_ONLY = 1, 2, 4
-ABI_VERSION = 2
+ABI_VERSION = 3
 EP_MAX_EXPERTS = 2048
 
 c_i32, c_i64, c_u32, c_size, c_vp = ctypes.c_int32, ctypes.c_int64, ctypes.c_uint32, ctypes.c_size_t, ctypes.c_void_p
@@ -63,6 +63,8 @@ SIGNATURES = {
     "ep_staging_set_mode": (c_i32, [c_vp, c_u32, c_i32]),
     "ep_staging_set_inbound": (c_i32, [c_vp, c_i32, ctypes.POINTER(c_i64)]),
     "ep_dispatch": (c_i32, [c_vp, c_i64, c_i32, c_i32, c_vp, c_vp, c_vp, c_i32, c_u32, c_vp]),
+    "ep_dispatch_fused": (c_i32, [c_vp, c_i64, c_i32, c_i32, c_i32, c_vp, c_vp, c_vp, c_vp, c_vp, c_vp,
+                                  c_vp, c_size, c_vp, c_i32, c_vp, c_i32, c_u32, c_vp]),
     "ep_combine": (c_i32, [c_vp, c_i32, c_u32, c_vp, c_vp, c_vp, c_i64, c_i32, c_i32, c_vp, c_i32, c_vp]),
     "ep_round_advance": (c_i32, [c_vp, c_vp]),
     "ep_round_read": (c_i32, [c_vp, ctypes.POINTER(c_u32)]),

@@ -101,22 +101,28 @@ class Layout:
     workspace: torch.Tensor
 
 
+def _layout_buffers(T: int, k: int, num_experts: int, num_ranks: int, dev, with_row_src: bool,
+                    out: Optional[Layout]) -> Layout:
+    """The layout's output tensors and zero-filled workspace (reused when `out` fits)."""
+    if out is not None and (out.num_tokens, out.topk, out.num_experts, out.num_ranks) == (T, k, num_experts,
+                                                                                          num_ranks):
+        return out
+    i32 = dict(dtype=torch.int32, device=dev)
+    return Layout(T, k, num_experts, num_ranks,
+                  torch.empty(num_experts, **i32), torch.empty(num_experts + 1, **i32),
+                  torch.empty(num_ranks, **i32), torch.empty(num_ranks + 1, **i32),
+                  torch.empty(T * k, **i32), torch.empty(T * k, **i32) if with_row_src else None,
+                  torch.zeros(workspace_bytes(T, k, num_experts) if 1 <= k <= num_experts
+                              and 1 <= num_experts <= _lib.EP_MAX_EXPERTS else 256,
+                              dtype=torch.uint8, device=dev))
+
+
 def dispatch_layout(topk_idx: torch.Tensor, num_experts: int, num_ranks: int, *, with_row_src: bool = True,
                     out: Optional[Layout] = None, stream=None) -> Layout:
     """ep_dispatch_layout on a [T, k] int32 routing tensor; outputs are device tensors."""
     _need(topk_idx, "topk_idx", (torch.int32,), 2)
     T, k = topk_idx.shape
-    dev = topk_idx.device
-    if out is None or out.num_tokens != T or out.topk != k or out.num_experts != num_experts \
-            or out.num_ranks != num_ranks:
-        i32 = dict(dtype=torch.int32, device=dev)
-        out = Layout(T, k, num_experts, num_ranks,
-                     torch.empty(num_experts, **i32), torch.empty(num_experts + 1, **i32),
-                     torch.empty(num_ranks, **i32), torch.empty(num_ranks + 1, **i32),
-                     torch.empty(T * k, **i32), torch.empty(T * k, **i32) if with_row_src else None,
-                     torch.zeros(workspace_bytes(T, k, num_experts) if 1 <= k <= num_experts
-                                 and 1 <= num_experts <= _lib.EP_MAX_EXPERTS else 256,
-                                 dtype=torch.uint8, device=dev))
+    out = _layout_buffers(T, k, num_experts, num_ranks, topk_idx.device, with_row_src, out)
     st = _lib_handle().ep_dispatch_layout(
         _ptr(topk_idx), T, k, num_experts, num_ranks, _ptr(out.expert_counts), _ptr(out.expert_offsets),
         _ptr(out.rank_counts), _ptr(out.rank_offsets), _ptr(out.slot_pos), _ptr(out.row_src),
@@ -317,6 +323,25 @@ def dispatch(x: torch.Tensor, slot_pos: torch.Tensor, staging: Staging, *, topk:
         raise ValueError("slot_pos must hold T*topk entries")
     _check(_lib_handle().ep_dispatch(_ptr(x), T, H, topk, _ptr(slot_pos), _offsets_ptr(rank_offsets, staging),
                                      staging.handle, buf, epoch & 0xFFFFFFFF, _stream_ptr(stream)), "ep_dispatch")
+
+
+def dispatch_fused(x: torch.Tensor, topk_idx: torch.Tensor, num_experts: int, num_ranks: int, staging: Staging, *,
+                   buf: int = 0, epoch: int = 1, with_row_src: bool = True, out: Optional[Layout] = None,
+                   stream=None) -> Layout:
+    """ep_dispatch_fused: dispatch_layout then dispatch in one call (one kernel for few
+    experts); returns the layout, as dispatch_layout does."""
+    _need(topk_idx, "topk_idx", (torch.int32,), 2)
+    _need(x, "x", _PAYLOAD_DTYPES, 2)
+    T, k = topk_idx.shape
+    if x.shape[0] != T:
+        raise ValueError("x and topk_idx must have the same number of tokens")
+    out = _layout_buffers(T, k, num_experts, num_ranks, topk_idx.device, with_row_src, out)
+    _check(_lib_handle().ep_dispatch_fused(
+        _ptr(topk_idx), T, k, num_experts, num_ranks, _ptr(out.expert_counts), _ptr(out.expert_offsets),
+        _ptr(out.rank_counts), _ptr(out.rank_offsets), _ptr(out.slot_pos), _ptr(out.row_src),
+        _ptr(out.workspace), out.workspace.numel(), _ptr(x), x.shape[1], staging.handle, buf, epoch & 0xFFFFFFFF,
+        _stream_ptr(stream)), "ep_dispatch_fused")
+    return out
 
 
 def combine(staging: Staging, slot_pos: torch.Tensor, topk_w: torch.Tensor, *, out: Optional[torch.Tensor] = None,

@@ -166,6 +166,30 @@ extern "C" ep_status ep_layout_workspace_bytes(int64_t num_tokens, int32_t topk,
     return EP_OK;
 }
 
+namespace {
+
+// Host-visible argument checks of a dispatch layout call.
+ep_status check_layout_args(const char *who, int64_t T, int32_t k, int32_t E, int32_t R, const int32_t *topk_idx,
+                            const int32_t *expert_counts, const int32_t *expert_offsets, const int32_t *rank_counts,
+                            const int32_t *rank_offsets, const int32_t *slot_pos, const void *workspace,
+                            size_t workspace_bytes) {
+    if (T < 0 || E < 1 || E > EP_MAX_EXPERTS || k < 1 || k > E || R < 1 || E % R != 0)
+        return fail(EP_ERR_INVALID_ARG, "%s: need T >= 0, 1 <= k <= E <= %d, R >= 1, E %% R == 0 (T=%lld k=%d E=%d R=%d)",
+                    who, EP_MAX_EXPERTS, (long long)T, k, E, R);
+    if (T * (int64_t)k > INT32_MAX)
+        return fail(EP_ERR_INVALID_ARG, "%s: T*k = %lld does not fit int32", who, (long long)(T * k));
+    if (!expert_counts || !expert_offsets || !rank_counts || !rank_offsets || !workspace)
+        return fail(EP_ERR_INVALID_ARG, "%s: NULL output or workspace", who);
+    if (T > 0 && (!topk_idx || !slot_pos))
+        return fail(EP_ERR_INVALID_ARG, "%s: NULL topk_idx or slot_pos", who);
+    const size_t need = ep::layout_workspace_bytes(T * k, E);
+    if (workspace_bytes < need)
+        return fail(EP_ERR_INVALID_ARG, "%s: workspace of %zu bytes, need %zu", who, workspace_bytes, need);
+    return EP_OK;
+}
+
+}  // namespace
+
 extern "C" ep_status ep_dispatch_layout(const int32_t *topk_idx, int64_t num_tokens, int32_t topk,
                                         int32_t num_experts, int32_t num_ranks, int32_t *expert_counts,
                                         int32_t *expert_offsets, int32_t *rank_counts,
@@ -173,22 +197,10 @@ extern "C" ep_status ep_dispatch_layout(const int32_t *topk_idx, int64_t num_tok
                                         void *workspace, size_t workspace_bytes, hipStream_t stream) {
     const int64_t T = num_tokens;
     const int32_t k = topk, E = num_experts, R = num_ranks;
-    if (T < 0 || E < 1 || E > EP_MAX_EXPERTS || k < 1 || k > E || R < 1 || E % R != 0)
-        return fail(EP_ERR_INVALID_ARG,
-                    "ep_dispatch_layout: need T >= 0, 1 <= k <= E <= %d, R >= 1, E %% R == 0 "
-                    "(T=%lld k=%d E=%d R=%d)",
-                    EP_MAX_EXPERTS, (long long)T, k, E, R);
-    if (T * (int64_t)k > INT32_MAX)
-        return fail(EP_ERR_INVALID_ARG, "ep_dispatch_layout: T*k = %lld does not fit int32",
-                    (long long)(T * k));
-    if (!expert_counts || !expert_offsets || !rank_counts || !rank_offsets || !workspace)
-        return fail(EP_ERR_INVALID_ARG, "ep_dispatch_layout: NULL output or workspace");
-    if (T > 0 && (!topk_idx || !slot_pos))
-        return fail(EP_ERR_INVALID_ARG, "ep_dispatch_layout: NULL topk_idx or slot_pos");
-    const size_t need = ep::layout_workspace_bytes(T * k, E);
-    if (workspace_bytes < need)
-        return fail(EP_ERR_INVALID_ARG, "ep_dispatch_layout: workspace of %zu bytes, need %zu",
-                    workspace_bytes, need);
+    const ep_status st = check_layout_args("ep_dispatch_layout", T, k, E, R, topk_idx, expert_counts, expert_offsets,
+                                           rank_counts, rank_offsets, slot_pos, workspace, workspace_bytes);
+    if (st != EP_OK)
+        return st;
     ep::LayoutArgs a{};
     a.topk_idx = topk_idx;
     a.slots = T * k;
@@ -599,31 +611,9 @@ ep_status check_round(const ep_staging *s, const char *who, int64_t T, int32_t H
     return check_device(s, who);
 }
 
-}  // namespace
-
-extern "C" ep_status ep_dispatch(const void *x_dev, int64_t num_tokens, int32_t hidden, int32_t topk,
-                                 const int32_t *slot_pos, const int32_t *rank_offsets, ep_staging *s,
-                                 int32_t buf, uint32_t epoch, hipStream_t stream) {
-    ep_status st = check_round(s, "ep_dispatch", num_tokens, hidden, topk, buf, slot_pos);
-    if (st != EP_OK)
-        return st;
-    if (num_tokens > 0 && (!x_dev || !aligned16(x_dev)))
-        return fail(EP_ERR_INVALID_ARG, "ep_dispatch: x must be a non-NULL 16-byte aligned pointer");
-    const int64_t rows = num_tokens * topk;
-    const bool pinned = s->kind == EP_STAGING_PINNED_HOST;
-    const bool exchange = pinned && s->mode != 0 && rows > 0;
-    if (exchange) {  // the offsets travel to the host while the pack runs
-        st = ep::exchange_enqueue_mirror(s, buf, epoch, rank_offsets, stream, "ep_dispatch");
-        if (st != EP_OK)
-            return st;
-    }
-    EP_HIP(ep::launch_pack(x_dev, num_tokens, hidden, topk, slot_pos, s->dev_send[buf], s->max_rows,
-                           pinned ? s->epoch_word(buf) : nullptr, epoch, stream));
-    if (!pinned || rows == 0)
-        return EP_OK;
-    if (exchange)
-        return ep::exchange_dispatch(s, buf, epoch, rows, stream);
-
+// Host leg of a dispatch in the default pinned mode: the packed rows of s->dev_send[buf]
+// go to the host bounce buffer in chunks, one flag per chunk.
+ep_status dispatch_default_legs(ep_staging *s, int32_t buf, uint32_t epoch, int64_t rows, hipStream_t stream) {
     const int64_t bytes = rows * s->row_bytes;
     const int64_t chunks = (bytes + s->chunk_bytes - 1) / s->chunk_bytes;
     char *dsrc = static_cast<char *>(s->dev_send[buf]);
@@ -674,6 +664,88 @@ extern "C" ep_status ep_dispatch(const void *x_dev, int64_t num_tokens, int32_t 
     EP_HIP(hipEventRecord(s->ev_up_done[buf], s->up));
     EP_HIP(hipStreamWaitEvent(stream, s->ev_up_done[buf], 0));
     return EP_OK;
+}
+
+}  // namespace
+
+extern "C" ep_status ep_dispatch(const void *x_dev, int64_t num_tokens, int32_t hidden, int32_t topk,
+                                 const int32_t *slot_pos, const int32_t *rank_offsets, ep_staging *s,
+                                 int32_t buf, uint32_t epoch, hipStream_t stream) {
+    ep_status st = check_round(s, "ep_dispatch", num_tokens, hidden, topk, buf, slot_pos);
+    if (st != EP_OK)
+        return st;
+    if (num_tokens > 0 && (!x_dev || !aligned16(x_dev)))
+        return fail(EP_ERR_INVALID_ARG, "ep_dispatch: x must be a non-NULL 16-byte aligned pointer");
+    const int64_t rows = num_tokens * topk;
+    const bool pinned = s->kind == EP_STAGING_PINNED_HOST;
+    const bool exchange = pinned && s->mode != 0 && rows > 0;
+    if (exchange) {  // the offsets travel to the host while the pack runs
+        st = ep::exchange_enqueue_mirror(s, buf, epoch, rank_offsets, stream, "ep_dispatch");
+        if (st != EP_OK)
+            return st;
+    }
+    EP_HIP(ep::launch_pack(x_dev, num_tokens, hidden, topk, slot_pos, s->dev_send[buf], s->max_rows,
+                           pinned ? s->epoch_word(buf) : nullptr, epoch, stream));
+    if (!pinned || rows == 0)
+        return EP_OK;
+    if (exchange)
+        return ep::exchange_dispatch(s, buf, epoch, rows, stream);
+
+    return dispatch_default_legs(s, buf, epoch, rows, stream);
+}
+
+extern "C" ep_status ep_dispatch_fused(const int32_t *topk_idx, int64_t num_tokens, int32_t topk,
+                                       int32_t num_experts, int32_t num_ranks, int32_t *expert_counts,
+                                       int32_t *expert_offsets, int32_t *rank_counts, int32_t *rank_offsets,
+                                       int32_t *slot_pos, int32_t *row_src, void *workspace, size_t workspace_bytes,
+                                       const void *x_dev, int32_t hidden, ep_staging *s, int32_t buf, uint32_t epoch,
+                                       hipStream_t stream) {
+    const int64_t T = num_tokens;
+    const int32_t k = topk, E = num_experts, R = num_ranks;
+    // every argument of both steps is checked before anything is enqueued
+    ep_status st = check_layout_args("ep_dispatch_fused", T, k, E, R, topk_idx, expert_counts, expert_offsets,
+                                     rank_counts, rank_offsets, slot_pos, workspace, workspace_bytes);
+    if (st != EP_OK)
+        return st;
+    st = check_round(s, "ep_dispatch_fused", T, hidden, k, buf, slot_pos);
+    if (st != EP_OK)
+        return st;
+    if (T > 0 && (!x_dev || !aligned16(x_dev)))
+        return fail(EP_ERR_INVALID_ARG, "ep_dispatch_fused: x must be a non-NULL 16-byte aligned pointer");
+    const bool pinned = s->kind == EP_STAGING_PINNED_HOST;
+    if ((pinned && s->mode != 0) || !ep::fused_layout_pack_fits(T, k, E, hidden, topk_idx)) {
+        // the two steps as separate kernels (the exchange modes also send the offsets to
+        // the host between them)
+        st = ep_dispatch_layout(topk_idx, T, k, E, R, expert_counts, expert_offsets, rank_counts, rank_offsets,
+                                slot_pos, row_src, workspace, workspace_bytes, stream);
+        if (st != EP_OK)
+            return st;
+        return ep_dispatch(x_dev, T, hidden, k, slot_pos, rank_offsets, s, buf, epoch, stream);
+    }
+    ep::FusedArgs a{};
+    a.topk_idx = topk_idx;
+    a.T = T;
+    a.k = k;
+    a.E = E;
+    a.R = R;
+    a.nbits = E > 1 ? 32 - __builtin_clz((unsigned)(E - 1)) : 0;
+    a.expert_counts = expert_counts;
+    a.expert_offsets = expert_offsets;
+    a.rank_counts = rank_counts;
+    a.rank_offsets = rank_offsets;
+    a.slot_pos = slot_pos;
+    a.row_src = row_src;
+    a.status = static_cast<uint32_t *>(workspace);
+    a.x = x_dev;
+    a.H = hidden;
+    a.packed = s->dev_send[buf];
+    a.max_rows = s->max_rows;
+    a.epoch_word = pinned ? s->epoch_word(buf) : nullptr;
+    a.epoch = epoch;
+    EP_HIP(ep::launch_layout_pack(a, stream));
+    if (!pinned)
+        return EP_OK;
+    return dispatch_default_legs(s, buf, epoch, T * k, stream);
 }
 
 extern "C" ep_status ep_combine(ep_staging *s, int32_t buf, uint32_t epoch, const int32_t *slot_pos,

@@ -105,6 +105,26 @@ struct LayoutArgs {
 };
 hipError_t launch_layout(LayoutArgs a, hipStream_t stream);
 
+// Layout and pack in one kernel for small expert counts (see fused.hip).  Same outputs
+// as launch_layout followed by launch_pack; no workspace besides the status word.
+struct FusedArgs {
+    const int32_t *topk_idx;  // 16-byte aligned
+    int64_t T;
+    int32_t k, E, R, nbits;
+    int32_t *expert_counts, *expert_offsets, *rank_counts, *rank_offsets;
+    int32_t *slot_pos, *row_src;
+    uint32_t *status;         // layout workspace byte 0
+    const void *x;            // [T][H] 16-bit rows, 16-byte aligned
+    int32_t H;
+    void *packed;             // [max_rows][H]
+    int64_t max_rows;
+    uint32_t *epoch_word;     // stores `epoch` when non-null (host leg flag copies)
+    uint32_t epoch;
+};
+// Whether the fused kernel covers these sizes (otherwise: layout, then pack).
+bool fused_layout_pack_fits(int64_t T, int32_t k, int32_t E, int32_t H, const void *topk_idx);
+hipError_t launch_layout_pack(const FusedArgs &a, hipStream_t stream);
+
 // Buffer chosen at run time by the parity of a round counter in device memory (graph-
 // replayed rounds): `alt` replaces the kernel's buffer argument on odd rounds.  No choice
 // when `round` is null.

@@ -1,0 +1,302 @@
+// fused.hip -- dispatch layout and pack in one kernel, for small expert counts.
+//
+// The layout (a stable counting sort of the T*k routing entries by expert, Sec. 4.3 of
+// the paper) and the pack (each destination's rows gathered into one contiguous segment,
+// Sec. 2.2) otherwise run as two kernels, and the layout's workgroups exchange their
+// per-expert totals through memory.  With few experts every workgroup can afford to count
+// all entries itself; that removes the exchange and the kernel boundary between layout
+// and pack.  A workgroup owns 16*tpw consecutive tokens (one run of tpw per wave):
+//   A. each wave issues the loads of its first ids, then those of its first token row
+//      (they do not depend on the layout; vector loads complete in order, so the ids
+//      come first);
+//   B. the workgroup counts all T*k entries (16-byte loads of 4 ids) with LDS atomic
+//      adds into 16 copies of the per-expert counters, chosen by lane, so that lanes of
+//      one instruction naming the same expert rarely hit the same word (vector and LDS
+//      work only: a ballot per id would queue every wave of the compute unit on its one
+//      scalar unit), both over all entries and over the entries before its own range;
+//      routing errors (an id outside [0,E), an expert twice in one token row) are found
+//      in the same pass;
+//   C. the totals' exclusive scan (DPP) gives the expert offsets; workgroup 0 stores the
+//      counts, offsets, rank counts/offsets and the status word;
+//   D. wave 0 ranks the workgroup's own entries in flat order (ballot match-any and a
+//      masked popcount, as the layout kernel does: stable), stores slot_pos / row_src and
+//      keeps the rows in LDS;
+//   E. each wave stores its tokens' rows to their k packed rows (non-temporal; a row is
+//      U groups of 64 16-byte vectors, one per lane, all loads in flight together).
+// The outputs equal those of the layout kernel followed by the pack kernel, bit for bit.
+// Workgroups never wait on each other, so nothing needs them resident together.
+//
+// Limits (the host falls back to the two kernels outside them): E <= 32 (a lane per
+// expert in step B), k in {1, 2, 4} (a token row lies inside one 4-id load), T*k <= 65536
+// (every workgroup reads every id), rows of 1, 2, 4, 8 or 16 groups (H a multiple of 512
+// up to 8192), a 16-byte aligned routing array.
+#include "ep_internal.h"
+#include "wave.h"
+
+namespace ep {
+namespace {
+
+constexpr int kFWaves = 16;                  // waves per workgroup
+constexpr int kFThreads = kFWaves * kWave;   // 1024
+constexpr int kFMaxE = 32;                   // experts: one lane each in step B
+constexpr int64_t kFMaxSlots = 65536;        // T*k: every workgroup reads every id
+constexpr int kFMaxOwn = 256;                // entries one workgroup owns (LDS rows)
+constexpr int kFOwnRounds = kFMaxOwn / kWave;
+constexpr int kFBatch = 4;                   // 16-byte id loads in flight per lane
+constexpr int kFMaxBlocks = 256;             // workgroups: each reads all ids once
+
+typedef int32_t i32x4 __attribute__((ext_vector_type(4)));
+
+// Does a token row inside a 4-id group name an expert twice?  Ids outside [0,E) are not
+// compared (they are errors of their own).
+template <int K>
+__device__ __forceinline__ bool row_repeats(i32x4 v, int E) {
+    auto ok = [E](int id) { return (unsigned)id < (unsigned)E; };
+    if constexpr (K == 2)
+        return (ok(v[0]) && v[0] == v[1]) || (ok(v[2]) && v[2] == v[3]);
+    else if constexpr (K == 4)
+        return (ok(v[0]) && (v[0] == v[1] || v[0] == v[2] || v[0] == v[3])) ||
+               (ok(v[1]) && (v[1] == v[2] || v[1] == v[3])) || (ok(v[2]) && v[2] == v[3]);
+    else
+        return false;
+}
+
+// Loads the 4-id groups qw + b*kFThreads + lane of a batch: every load is issued (an
+// index past the last whole group rereads that group; the caller masks it by index), so
+// the compiler can count the loads in flight and wait for the ids alone.
+__device__ __forceinline__ void load_ids(const i32x4 *q, int64_t full, int64_t qw, int lane, i32x4 *v) {
+#pragma unroll
+    for (int b = 0; b < kFBatch; ++b)
+        v[b] = q[min(qw + (int64_t)b * kFThreads + lane, full - 1)];
+}
+
+constexpr int kFCopies = 16;  // copies of the LDS counters (lane % 16 picks one)
+
+// Counts one id into the LDS counters (all entries, and those before this workgroup's).
+__device__ __forceinline__ void count_id(int id, bool in, bool before, int E, int *s_all, int *s_pre, int copy,
+                                         bool &bad_id) {
+    const bool valid = in && (unsigned)id < (unsigned)E;
+    bad_id |= in && !valid;
+    if (valid) {
+        atomicAdd(&s_all[copy * kFMaxE + id], 1);
+        if (before)
+            atomicAdd(&s_pre[copy * kFMaxE + id], 1);
+    }
+}
+
+template <int U, int K>
+__global__ __launch_bounds__(kFThreads) void layout_pack_kernel(FusedArgs a, int32_t tpw) {
+    __shared__ int s_all[kFCopies * kFMaxE];
+    __shared__ int s_pre[kFCopies * kFMaxE];
+    __shared__ int s_base[kFMaxE];
+    __shared__ int s_pos[kFMaxOwn];
+    __shared__ int s_err;
+    const int tid = threadIdx.x, lane = tid & (kWave - 1), w = tid / kWave;
+    const int64_t slots = a.T * K;
+    const int64_t tok0 = (int64_t)blockIdx.x * kFWaves * tpw;
+    const int64_t tok1 = min(a.T, tok0 + (int64_t)kFWaves * tpw);
+    const int64_t ent0 = tok0 * K, ent1 = tok1 * K;
+    const int32_t V = a.H / 8;
+    const u32x4 *x = static_cast<const u32x4 *>(a.x);
+    const i32x4 *q = reinterpret_cast<const i32x4 *>(a.topk_idx);
+    const int64_t full = slots / 4;  // whole 4-id groups; the 0..3 ids after them are the tail
+    constexpr int64_t kStride = (int64_t)kFThreads * kFBatch;
+
+    // A. first ids, the own entries' ids (step D), then this wave's first token row (a
+    //    wave past the workgroup's last token loads that token instead, storing nothing)
+    i32x4 v[kFBatch];
+    int64_t qw = (int64_t)w * kWave;
+    if (full > 0)
+        load_ids(q, full, qw, lane, v);
+    int own_id[kFOwnRounds];
+#pragma unroll
+    for (int r = 0; r < kFOwnRounds; ++r)
+        own_id[r] = a.topk_idx[min(ent0 + r * kWave + lane, ent1 - 1)];  // masked by index in step D
+    const int64_t wtok = tok0 + (int64_t)w * tpw;
+    u32x4 d[U];
+    {
+        const u32x4 *src = x + min(wtok, tok1 - 1) * V + lane;
+#pragma unroll
+        for (int u = 0; u < U; ++u)
+            d[u] = __builtin_nontemporal_load(src + u * kWave);
+    }
+    if (tid < kFCopies * kFMaxE) {
+        s_all[tid] = 0;
+        s_pre[tid] = 0;
+    }
+    if (tid == 0)
+        s_err = 0;
+    __syncthreads();
+
+    // B. count all entries into the LDS counters
+    bool bad_id = false, dup = false;
+    auto count_batch = [&](int64_t qb) {
+#pragma unroll
+        for (int b = 0; b < kFBatch; ++b) {
+            const int64_t g = qb + (int64_t)b * kFThreads;  // this round's first group
+            if (g >= full)
+                break;
+            const int64_t qi = g + lane;
+            const bool in = qi < full;
+            // entries before this workgroup's: whole 4-id groups (ent0 is a multiple of 16)
+            const bool before = qi * 4 < ent0;
+            dup |= in && row_repeats<K>(v[b], a.E);
+#pragma unroll
+            for (int c = 0; c < 4; ++c)
+                count_id(v[b][c], in, before, a.E, s_all, s_pre, lane % kFCopies, bad_id);
+        }
+    };
+    // the first batch outside the loop: its wait leaves the token row's loads in flight
+    if (qw < full)
+        count_batch(qw);
+    for (qw += kStride; qw < full; qw += kStride) {  // wave-uniform; T*k > 16384 only
+        load_ids(q, full, qw, lane, v);
+        count_batch(qw);
+    }
+    if (w == 0 && full * 4 < slots) {  // the tail: 1..3 ids (a whole token row for k <= 2)
+        const int64_t i = full * 4 + lane;
+        const bool in = i < slots;
+        const int id = in ? a.topk_idx[i] : -1;
+        if (K == 2 && lane == 0)
+            dup |= (unsigned)id < (unsigned)a.E && id == a.topk_idx[i + 1];  // the tail is one row
+        count_id(id, in, i < ent0, a.E, s_all, s_pre, lane % kFCopies, bad_id);
+    }
+    const uint32_t wave_err = (__ballot(bad_id) ? kRoutingIdOutOfRange : 0u) | (__ballot(dup) ? kRoutingDuplicate : 0u);
+    if (lane == 0 && wave_err)
+        atomicOr(&s_err, (int)wave_err);
+    __syncthreads();
+
+    if (w == 0) {
+        // C. totals, offsets; workgroup 0 stores the layout's counts and the status
+        int tot = 0, pre = 0;
+        if (lane < a.E) {
+#pragma unroll
+            for (int c = 0; c < kFCopies; ++c) {
+                tot += s_all[c * kFMaxE + lane];
+                pre += s_pre[c * kFMaxE + lane];
+            }
+        }
+        const int excl = wave_inclusive_scan(tot) - tot;  // lane E: the total
+        if (lane < a.E)
+            s_base[lane] = excl + pre;
+        if (blockIdx.x == 0) {
+            if (lane < a.E)
+                a.expert_counts[lane] = tot;
+            if (lane <= a.E)
+                a.expert_offsets[lane] = excl;
+            const int L = a.E / a.R;
+            const int lo = __shfl(excl, min(lane, a.R) * L);
+            const int hi = __shfl(excl, min(lane + 1, a.R) * L);
+            if (lane < a.R)
+                a.rank_counts[lane] = hi - lo;
+            if (lane <= a.R)
+                a.rank_offsets[lane] = lo;
+            if (lane == 0) {
+                *a.status = (uint32_t)s_err;
+                if (a.epoch_word)
+                    *a.epoch_word = a.epoch;
+            }
+        }
+        // D. rank the own entries in flat order
+#pragma unroll
+        for (int r = 0; r < kFOwnRounds; ++r) {
+            const int64_t i = ent0 + r * kWave + lane;
+            if (ent0 + r * kWave >= ent1)
+                break;
+            const int id = i < ent1 ? own_id[r] : -1;
+            const bool valid = i < ent1 && (unsigned)id < (unsigned)a.E;
+            const uint64_t m = match_expert(id, valid, a.nbits);
+            int pos = -1;
+            if (valid) {
+                const int below = lanes_below(m);
+                const int b = s_base[id];
+                pos = b + below;
+                if (below == 0)
+                    s_base[id] = b + (int)__popcll(m);
+            }
+            if (i < ent1) {
+                if ((uint64_t)(uint32_t)pos >= (uint64_t)slots)
+                    pos = -1;  // cannot happen with consistent counts; keeps every store in bounds
+                a.slot_pos[i] = pos;
+                if (pos >= 0 && a.row_src)
+                    a.row_src[pos] = (int32_t)i;
+                s_pos[i - ent0] = pos;
+            }
+        }
+    }
+    __syncthreads();
+
+    // E. store each token row to its k packed rows
+    u32x4 *packed = static_cast<u32x4 *>(a.packed);
+    for (int j0 = 0; j0 < tpw; ++j0) {
+        const int64_t t = wtok + j0;
+        if (t >= tok1)
+            break;
+        if (j0 > 0) {
+            const u32x4 *src = x + t * V + lane;
+#pragma unroll
+            for (int u = 0; u < U; ++u)
+                d[u] = __builtin_nontemporal_load(src + u * kWave);
+        }
+#pragma unroll
+        for (int j = 0; j < K; ++j) {
+            const int64_t p = s_pos[(t - tok0) * K + j];
+            if (p < 0 || p >= a.max_rows)
+                continue;
+            u32x4 *dst = packed + p * V + lane;
+#pragma unroll
+            for (int u = 0; u < U; ++u)
+                __builtin_nontemporal_store(d[u], dst + u * kWave);
+        }
+    }
+}
+
+template <int U>
+void launch_k(const FusedArgs &a, int32_t tpw, unsigned blocks, hipStream_t stream, TraceSlot ts) {
+    if (a.k == 1)
+        hipExtLaunchKernelGGL(layout_pack_kernel<U, 1>, dim3(blocks), dim3(kFThreads), 0, stream, ts.start, ts.stop, 0,
+                              a, tpw);
+    else if (a.k == 2)
+        hipExtLaunchKernelGGL(layout_pack_kernel<U, 2>, dim3(blocks), dim3(kFThreads), 0, stream, ts.start, ts.stop, 0,
+                              a, tpw);
+    else
+        hipExtLaunchKernelGGL(layout_pack_kernel<U, 4>, dim3(blocks), dim3(kFThreads), 0, stream, ts.start, ts.stop, 0,
+                              a, tpw);
+}
+
+}  // namespace
+
+bool fused_layout_pack_fits(int64_t T, int32_t k, int32_t E, int32_t H, const void *topk_idx) {
+    if (T < 1 || E < 1 || E > kFMaxE || !(k == 1 || k == 2 || k == 4) || T * k > kFMaxSlots)
+        return false;
+    if (H % 512 != 0)
+        return false;
+    const int G = H / 512;
+    return (G == 1 || G == 2 || G == 4 || G == 8 || G == 16) && reinterpret_cast<uintptr_t>(topk_idx) % 16 == 0;
+}
+
+hipError_t launch_layout_pack(const FusedArgs &a, hipStream_t stream) {
+    if (!fused_layout_pack_fits(a.T, a.k, a.E, a.H, a.topk_idx) || a.R < 1 || a.E % a.R != 0)
+        return hipErrorInvalidValue;
+    // tokens per wave: enough that at most kFMaxBlocks workgroups cover T
+    const int64_t per_block_min = (a.T + kFMaxBlocks - 1) / kFMaxBlocks;
+    const int32_t tpw = (int32_t)((per_block_min + kFWaves - 1) / kFWaves);
+    const int64_t blocks = (a.T + (int64_t)kFWaves * tpw - 1) / ((int64_t)kFWaves * tpw);
+    if ((int64_t)kFWaves * tpw * a.k > kFMaxOwn)
+        return hipErrorInvalidValue;  // excluded by the limits above
+    (void)hipGetLastError();  // drop an error left by an earlier, already reported call
+    TraceSlot ts = trace_acquire();
+    switch (a.H / 512) {
+    case 1: launch_k<1>(a, tpw, (unsigned)blocks, stream, ts); break;
+    case 2: launch_k<2>(a, tpw, (unsigned)blocks, stream, ts); break;
+    case 4: launch_k<4>(a, tpw, (unsigned)blocks, stream, ts); break;
+    case 8: launch_k<8>(a, tpw, (unsigned)blocks, stream, ts); break;
+    default: launch_k<16>(a, tpw, (unsigned)blocks, stream, ts); break;
+    }
+    hipError_t err = hipGetLastError();
+    if (err == hipSuccess)
+        trace_submit("layout_pack", ts);
+    return err;
+}
+
+}  // namespace ep

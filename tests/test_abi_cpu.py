@@ -47,7 +47,7 @@ def test_binding_covers_every_symbol():
 
 
 def test_status_names(lib):
-    assert lib.ep_abi_version() == _lib.ABI_VERSION == 2
+    assert lib.ep_abi_version() == _lib.ABI_VERSION == 3
     assert lib.ep_status_name(0) == b"EP_OK"
     assert lib.ep_status_name(5) == b"EP_ERR_TIMEOUT"
     assert lib.ep_status_name(99) == b"EP_ERR_UNKNOWN"
@@ -81,6 +81,18 @@ def test_layout_rejects_null_and_small_workspace(lib):
     assert lib.ep_dispatch_layout(None, 4, 2, 8, 4, d, d, d, d, d, None, d, 1 << 20, None) == _lib.EP_ERR_INVALID_ARG
     assert lib.ep_dispatch_layout(d, 40000, 2, 8, 4, d, d, d, d, d, None, d, 256, None) == _lib.EP_ERR_INVALID_ARG
     assert b"workspace" in lib.ep_last_error()
+
+
+@pytest.mark.parametrize("T,k,E,R", [(-1, 2, 8, 4), (4, 0, 8, 4), (4, 9, 8, 4), (4, 2, 8, 3), (4, 2, 4096, 8)])
+def test_fused_dispatch_rejects_bad_arguments(lib, T, k, E, R):
+    """ep_dispatch_fused checks the layout's arguments, then the dispatch's (a NULL
+    staging), before it touches a device."""
+    d = ctypes.c_void_p(16)   # never dereferenced: the call must fail first
+    st = lib.ep_dispatch_fused(d, T, k, E, R, d, d, d, d, d, None, d, 1 << 20, d, 512, None, 0, 1, None)
+    assert st == _lib.EP_ERR_INVALID_ARG
+    assert b"ep_dispatch_fused" in lib.ep_last_error()
+    good = lib.ep_dispatch_fused(d, 4, 2, 8, 4, d, d, d, d, d, None, d, 1 << 20, d, 512, None, 0, 1, None)
+    assert good == _lib.EP_ERR_INVALID_ARG and b"staging is NULL" in lib.ep_last_error()
 
 
 @pytest.mark.parametrize("args", [(7, 10, 64, 4, 1, 0), (0, 0, 64, 4, 1, 0), (0, 10, 12, 4, 1, 0),

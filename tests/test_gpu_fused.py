@@ -1,0 +1,268 @@
+"""ep_dispatch_fused: layout and pack in one call (one kernel for few experts).
+
+Its outputs must equal the oracle's layout and pack, and the two-call path's
+(ep_dispatch_layout then ep_dispatch) bit for bit: counts, offsets, rank counts and
+offsets, slot_pos, row_src and the packed rows, also with routing errors.  The trace
+shows which kernel ran, so the fused kernel's cases are known to have used it and the
+fallback cases to have used the two kernels.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2609_40093_amd as ep
+from gpu_cases import from_config, make_case, say
+
+pytestmark = pytest.mark.gpu
+
+DEV = "cuda"
+LAYOUT_KEYS = ("expert_counts", "expert_offsets", "rank_counts", "rank_offsets", "slot_pos", "row_src")
+
+
+def to_dev(a):
+    return torch.from_numpy(np.ascontiguousarray(a)).to(DEV)
+
+
+def run_fused(idx_d, x_d, E, R, staging, buf=0, epoch=1):
+    ep.trace_reset()
+    ep.trace_enable(True)
+    lay = ep.dispatch_fused(x_d, idx_d, E, R, staging, buf=buf, epoch=epoch)
+    ep.trace_enable(False)
+    torch.cuda.synchronize()
+    kernels = set(ep.trace_read())
+    return lay, kernels
+
+
+def run_two_calls(idx_d, x_d, E, R, staging, k, buf=0, epoch=1):
+    lay = ep.dispatch_layout(idx_d, E, R)
+    ep.dispatch(x_d, lay.slot_pos, staging, topk=k, buf=buf, epoch=epoch, rank_offsets=lay.rank_offsets)
+    torch.cuda.synchronize()
+    return lay
+
+
+def layout_np(lay):
+    return {key: getattr(lay, key).cpu().numpy() for key in LAYOUT_KEYS}
+
+
+FUSED_CASES = [
+    # name, T, H, E, k, R, routing; every case fits the fused kernel
+    ("k2_e8_rows8", 4096, 4096, 8, 2, 4, "skewed"),
+    ("k2_e16_rows2", 128, 1024, 16, 2, 4, "random"),
+    ("k1_e4_rows1_ragged_tokens", 1001, 512, 4, 1, 2, "random"),
+    ("k4_e32_rows4", 3000, 2048, 32, 4, 8, "skewed"),
+    ("k2_e3_odd_experts", 17, 512, 3, 2, 3, "random"),
+    ("k2_rows16", 300, 8192, 8, 2, 2, "random"),
+    ("single_token", 1, 1024, 8, 2, 4, "random"),
+    ("k4_empty_experts", 999, 512, 16, 4, 4, "firstk"),
+    ("k2_limit_65536_slots", 32768, 512, 32, 2, 8, "random"),   # 8 tokens per wave
+    ("k4_limit_65536_slots", 16384, 512, 16, 4, 4, "skewed"),
+    ("k1_limit_65536_slots", 65536, 512, 2, 1, 1, "random"),    # 16 tokens per wave
+]
+
+
+@pytest.mark.parametrize("spec", FUSED_CASES, ids=[c[0] for c in FUSED_CASES])
+def test_fused_matches_oracle_and_two_calls(spec):
+    name, T, H, E, k, R, kind = spec
+    case = make_case(name, T, H, E, k, R, kind, seed=len(name))
+    say(f"fused {name}: T={T} H={H} E={E} k={k} R={R}")
+    ref = oracle.layout(case.topk_idx, E, R)
+    assert ref.status == oracle.OK
+    packed_ref = oracle.pack(case.x, ref.slot_pos, k)
+    idx_d, x_d = to_dev(case.topk_idx), to_dev(case.x.view(np.int16))
+    st = ep.Staging("hbm", T * k, H, R, num_buffers=2)
+    lay, kernels = run_fused(idx_d, x_d, E, R, st, buf=1)
+    assert "layout_pack" in kernels and "layout" not in kernels and "pack" not in kernels, kernels
+    ep.layout_status(lay)
+    got = layout_np(lay)
+    for key in LAYOUT_KEYS:
+        assert np.array_equal(got[key], getattr(ref, key)), f"{key} differs from the oracle"
+    packed = st.read_device("send", T * k, buf=1).cpu().numpy().view(np.uint16)
+    assert packed.tobytes() == packed_ref.tobytes(), "packed rows differ from the oracle"
+    # the two-call path on the other buffer set gives the same bytes
+    lay2 = run_two_calls(idx_d, x_d, E, R, st, k, buf=0)
+    for key in LAYOUT_KEYS:
+        assert np.array_equal(getattr(lay2, key).cpu().numpy(), got[key]), f"{key}: fused != two calls"
+    assert st.read_device("send", T * k, buf=0).cpu().numpy().tobytes() == packed.tobytes()
+    st.close()
+
+
+def test_fused_workloads_tiny_and_coarse():
+    for name in ("tiny", "coarse"):
+        case = from_config(name)
+        say(f"fused workload {name}")
+        ref = oracle.layout(case.topk_idx, case.E, case.R)
+        st = ep.Staging("hbm", case.slots, case.H, case.R, num_buffers=1)
+        lay, kernels = run_fused(to_dev(case.topk_idx), to_dev(case.x.view(np.int16)), case.E, case.R, st)
+        assert "layout_pack" in kernels
+        ep.layout_status(lay)
+        assert np.array_equal(lay.slot_pos.cpu().numpy(), ref.slot_pos)
+        assert np.array_equal(lay.rank_offsets.cpu().numpy(), ref.rank_offsets)
+        packed = st.read_device("send", case.slots).cpu().numpy().view(np.uint16)
+        assert packed.tobytes() == oracle.pack(case.x, ref.slot_pos, case.k).tobytes()
+        st.close()
+
+
+def test_fused_repeated_calls_reuse_buffers():
+    """Rounds on one layout object and staging: each round's routing and rows are new."""
+    T, H, E, k, R = 2048, 1024, 8, 2, 4
+    st = ep.Staging("hbm", T * k, H, R, num_buffers=2)
+    lay = None
+    for r in range(4):
+        case = make_case(f"round{r}", T, H, E, k, R, "skewed" if r % 2 else "random", seed=100 + r)
+        say(f"fused round {r}")
+        lay = ep.dispatch_fused(to_dev(case.x.view(np.int16)), to_dev(case.topk_idx), E, R, st, buf=r % 2,
+                                epoch=r + 1, out=lay)
+        ep.layout_status(lay)
+        ref = oracle.layout(case.topk_idx, E, R)
+        assert np.array_equal(lay.slot_pos.cpu().numpy(), ref.slot_pos), f"round {r}"
+        assert np.array_equal(lay.expert_counts.cpu().numpy(), ref.expert_counts), f"round {r}"
+        packed = st.read_device("send", T * k, buf=r % 2).cpu().numpy().view(np.uint16)
+        assert packed.tobytes() == oracle.pack(case.x, ref.slot_pos, k).tobytes(), f"round {r}"
+    st.close()
+
+
+FALLBACK_CASES = [
+    # outside the fused kernel's limits: the two kernels run
+    ("e64_too_many_experts", 500, 512, 64, 2, 4),
+    ("k8", 300, 512, 16, 8, 4),
+    ("k3", 300, 512, 16, 3, 4),
+    ("rows14", 200, 7168, 16, 2, 4),
+    ("h520_not_whole_groups", 100, 520, 8, 2, 2),
+    ("slots_over_limit", 40000, 512, 8, 2, 4),
+]
+
+
+@pytest.mark.parametrize("spec", FALLBACK_CASES, ids=[c[0] for c in FALLBACK_CASES])
+def test_fallback_runs_two_kernels(spec):
+    name, T, H, E, k, R = spec
+    case = make_case(name, T, H, E, k, R, "random", seed=7)
+    say(f"fused fallback {name}")
+    ref = oracle.layout(case.topk_idx, E, R)
+    st = ep.Staging("hbm", T * k, H, R, num_buffers=1)
+    lay, kernels = run_fused(to_dev(case.topk_idx), to_dev(case.x.view(np.int16)), E, R, st)
+    assert "layout_pack" not in kernels and {"layout", "pack"} <= kernels, kernels
+    ep.layout_status(lay)
+    assert np.array_equal(lay.slot_pos.cpu().numpy(), ref.slot_pos)
+    packed = st.read_device("send", T * k).cpu().numpy().view(np.uint16)
+    assert packed.tobytes() == oracle.pack(case.x, ref.slot_pos, k).tobytes()
+    st.close()
+
+
+def test_misaligned_routing_falls_back():
+    T, H, E, k, R = 512, 512, 8, 2, 4
+    case = make_case("misaligned_idx", T, H, E, k, R, "random", seed=8)
+    big = np.zeros((T + 1, k), np.int32)
+    big[1:] = case.topk_idx
+    idx_d = to_dev(big)[1:]                     # 8 bytes past a 16-byte boundary
+    assert idx_d.data_ptr() % 16 != 0
+    say("fused with a misaligned routing array")
+    st = ep.Staging("hbm", T * k, H, R, num_buffers=1)
+    lay, kernels = run_fused(idx_d, to_dev(case.x.view(np.int16)), E, R, st)
+    assert "layout_pack" not in kernels
+    ep.layout_status(lay)
+    ref = oracle.layout(case.topk_idx, E, R)
+    assert np.array_equal(lay.slot_pos.cpu().numpy(), ref.slot_pos)
+    st.close()
+
+
+@pytest.mark.parametrize("k", [1, 2, 4])
+def test_fused_routing_errors_match_two_calls(k):
+    """Ids outside [0,E) get no row and are reported; a repeated expert is reported and
+    still ranked; the fused kernel and the layout kernel agree on every output."""
+    T, H, E, R = 700, 512, 16, 4
+    case = make_case(f"errors_k{k}", T, H, E, k, R, "random", seed=9)
+    idx = case.topk_idx.copy()
+    idx[5, 0] = E
+    idx[321, k - 1] = -7
+    if k > 1:
+        idx[600, 1] = idx[600, 0]
+    say(f"fused routing errors k={k}")
+    idx_d, x_d = to_dev(idx), to_dev(case.x.view(np.int16))
+    st = ep.Staging("hbm", T * k, H, R, num_buffers=2)
+    lay, kernels = run_fused(idx_d, x_d, E, R, st, buf=0)
+    assert "layout_pack" in kernels
+    with pytest.raises(ep.EPError) as ei:
+        ep.layout_status(lay)
+    assert ei.value.status == 2
+    msg = str(ei.value)
+    assert "outside" in msg and (k == 1 or "repeated" in msg), msg
+    got = layout_np(lay)
+    assert got["slot_pos"][5 * k] == -1 and got["slot_pos"][321 * k + k - 1] == -1
+    lay2 = run_two_calls(idx_d, x_d, E, R, st, k, buf=1)
+    with pytest.raises(ep.EPError):
+        ep.layout_status(lay2)
+    for key in LAYOUT_KEYS:
+        if key == "row_src":   # rows no slot maps to are left unwritten by both paths
+            continue
+        assert np.array_equal(getattr(lay2, key).cpu().numpy(), got[key]), f"{key}: fused != two calls"
+    valid = got["slot_pos"] >= 0
+    rows = got["slot_pos"][valid]
+    a = st.read_device("send", T * k, buf=0).cpu().numpy()[rows]
+    b = st.read_device("send", T * k, buf=1).cpu().numpy()[rows]
+    assert a.tobytes() == b.tobytes()
+    # the next good routing on the same workspace clears the status
+    lay = ep.dispatch_fused(x_d, to_dev(case.topk_idx), E, R, st, out=lay)
+    ep.layout_status(lay)
+    st.close()
+
+
+def test_fused_pinned_default_mode_host_leg():
+    """Pinned staging, default mode: the fused kernel, then the SDMA leg and its flags."""
+    case = make_case("pinned_fused", 1024, 2048, 8, 2, 4, "random", seed=10)
+    say("fused dispatch with pinned staging")
+    st = ep.Staging("pinned", case.slots, case.H, case.R, num_buffers=2)
+    lay, kernels = run_fused(to_dev(case.topk_idx), to_dev(case.x.view(np.int16)), case.E, case.R, st,
+                             buf=1, epoch=5)
+    assert "layout_pack" in kernels
+    st.status()
+    ref = oracle.layout(case.topk_idx, case.E, case.R)
+    assert np.array_equal(lay.slot_pos.cpu().numpy(), ref.slot_pos)
+    sent = st.host_array("send", 1)[:case.slots]
+    assert sent.tobytes() == oracle.pack(case.x, ref.slot_pos, case.k).tobytes()
+    flags = st.host_array("send_flags", 1)
+    assert flags[0] == 5
+    st.close()
+
+
+def test_fused_exchange_mode_falls_back():
+    case = make_case("pinned_exchange", 512, 1024, 8, 2, 4, "random", seed=11, gates="uniform")
+    say("fused dispatch with an exchange mode")
+    st = ep.Staging("pinned", case.slots, case.H, case.R, num_buffers=1)
+    st.set_mode(ep.MODE_PER_SENDER, 0)
+    peers = ep.SimPeers(st, echo=True)
+    peers.post(0, 3, case.slots)
+    lay, kernels = run_fused(to_dev(case.topk_idx), to_dev(case.x.view(np.int16)), case.E, case.R, st, epoch=3)
+    assert "layout_pack" not in kernels and "pack" in kernels
+    w = to_dev(case.topk_w)
+    out32 = ep.combine(st, lay.slot_pos, w, out_dtype=torch.float32, epoch=3, rank_offsets=lay.rank_offsets)
+    st.status()
+    peers.drain()
+    ref = oracle.layout(case.topk_idx, case.E, case.R)
+    assert np.array_equal(lay.slot_pos.cpu().numpy(), ref.slot_pos)
+    sent = st.host_array("send", 0)[:case.slots]
+    assert sent.tobytes() == oracle.pack(case.x, ref.slot_pos, case.k).tobytes()
+    # identity experts (the peers echo the rows) and gates of 1/2: combine returns x exactly
+    xf = torch.from_numpy(case.x.view(np.int16)).view(torch.bfloat16).float()
+    assert torch.equal(out32.cpu(), xf)
+    peers.close()
+    st.close()
+
+
+def test_fused_argument_errors_enqueue_nothing():
+    case = make_case("fused_args", 64, 512, 8, 2, 4, "random", seed=12)
+    idx_d, x_d = to_dev(case.topk_idx), to_dev(case.x.view(np.int16))
+    say("fused argument checks")
+    small = ep.Staging("hbm", case.slots - 1, 512, 4, num_buffers=1)
+    with pytest.raises(ep.EPError, match="exceed"):
+        ep.dispatch_fused(x_d, idx_d, 8, 4, small)
+    st = ep.Staging("hbm", case.slots, 512, 4, num_buffers=1)
+    with pytest.raises(ep.EPError, match="E % R"):
+        ep.dispatch_fused(x_d, idx_d, 8, 3, st)
+    with pytest.raises(ep.EPError, match="buffer"):
+        ep.dispatch_fused(x_d, idx_d, 8, 4, st, buf=1)
+    flat = torch.zeros(64 * 512 + 8, dtype=torch.int16, device=DEV)
+    with pytest.raises(ep.EPError, match="aligned"):
+        ep.dispatch_fused(flat[1:1 + 64 * 512].view(64, 512), idx_d, 8, 4, st)
+    small.close()
+    st.close()
