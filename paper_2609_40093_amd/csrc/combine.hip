@@ -11,7 +11,12 @@
 // Mapping: one wave per (token, column chunk of 64*U 16-byte vectors); the k slot
 // positions and gates are wave-uniform scalar loads.  Slots are taken KC at a time and
 // all KC*U row loads of a batch are issued before their FMAs, keeping KC*U KiB in flight
-// per wave.  Rows are read once: loads and stores are non-temporal.
+// per wave.  Nothing is conditional: a slot without a row reads row 0 with its bits
+// masked to +0 and its gate set to -0, so it adds exactly -0, which leaves every sum
+// unchanged (signs of zero included) -- a branch around it would let the compiler sink
+// the slot's loads into the branch and serialize them behind the previous slot's.  In
+// EXACT instances (rows a whole number of chunks) no lane carries a bounds mask either.
+// Rows are read once: loads and stores are non-temporal.
 #include "ep_internal.h"
 
 namespace ep {
@@ -28,7 +33,8 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
     return __builtin_bit_cast(uint32_t, b);
 }
 
-template <int U, int KC, bool F32_OUT>
+// FIXED_K: k == KC (one batch of slots, its bounds known at compile time).
+template <int U, int KC, bool F32_OUT, bool EXACT, bool FIXED_K>
 __global__ __launch_bounds__(256) void combine_kernel(const u32x4 *__restrict__ recv,
                                                       const int32_t *__restrict__ slot_pos,
                                                       const float *__restrict__ topk_w, int64_t T,
@@ -44,8 +50,9 @@ __global__ __launch_bounds__(256) void combine_kernel(const u32x4 *__restrict__ 
     if (t >= T)
         return;
     const int32_t v0 = (int32_t)(item - t * chunks) * (U * kWave);
-    const int32_t *sp = slot_pos + t * k;
-    const float *wt = topk_w + t * k;
+    const int32_t kk = FIXED_K ? KC : k;
+    const int32_t *sp = slot_pos + t * kk;
+    const float *wt = topk_w + t * kk;
 
     float acc[U][8];
 #pragma unroll
@@ -54,41 +61,43 @@ __global__ __launch_bounds__(256) void combine_kernel(const u32x4 *__restrict__ 
         for (int q = 0; q < 8; ++q)
             acc[u][q] = 0.0f;
 
-    for (int32_t j0 = 0; j0 < k; j0 += KC) {
+    for (int32_t j0 = 0; j0 < kk; j0 += KC) {
         u32x4 d[KC][U];
         float g[KC];
-        bool ok[KC];
+        uint32_t keep[KC];  // all ones for a slot with a row, else 0
 #pragma unroll
         for (int jj = 0; jj < KC; ++jj) {
             const int32_t j = j0 + jj;
-            const int64_t p = j < k ? (int64_t)sp[j] : -1;
-            ok[jj] = p >= 0 && p < max_rows;
-            g[jj] = ok[jj] ? wt[j] : 0.0f;
-            const u32x4 *src = recv + (ok[jj] ? p : 0) * V;
+            const int32_t jc = min(j, kk - 1);  // loads issued for every jj; a slot past k has no row
+            const int64_t p = j < kk ? (int64_t)sp[jc] : -1;  // wave-uniform
+            const float gj = wt[jc];
+            const bool ok = p >= 0 && p < max_rows;
+            keep[jj] = ok ? ~0u : 0u;
+            g[jj] = ok ? gj : -0.0f;
+            const u32x4 *src = recv + (ok ? p : 0) * V;
 #pragma unroll
             for (int u = 0; u < U; ++u) {
                 const int32_t v = v0 + u * kWave + lane;
-                d[jj][u] = ok[jj] && v < V ? __builtin_nontemporal_load(src + v) : u32x4{0u, 0u, 0u, 0u};
+                d[jj][u] = EXACT ? __builtin_nontemporal_load(src + v)
+                                 : __builtin_nontemporal_load(src + min(v, V - 1));
             }
         }
 #pragma unroll
-        for (int jj = 0; jj < KC; ++jj) {
-            if (!ok[jj])
-                continue;
+        for (int jj = 0; jj < KC; ++jj)
 #pragma unroll
             for (int u = 0; u < U; ++u)
 #pragma unroll
                 for (int q = 0; q < 4; ++q) {
-                    acc[u][2 * q] = __builtin_fmaf(g[jj], bf16_lo(d[jj][u][q]), acc[u][2 * q]);
-                    acc[u][2 * q + 1] = __builtin_fmaf(g[jj], bf16_hi(d[jj][u][q]), acc[u][2 * q + 1]);
+                    const uint32_t bits = d[jj][u][q] & keep[jj];
+                    acc[u][2 * q] = __builtin_fmaf(g[jj], bf16_lo(bits), acc[u][2 * q]);
+                    acc[u][2 * q + 1] = __builtin_fmaf(g[jj], bf16_hi(bits), acc[u][2 * q + 1]);
                 }
-        }
     }
 
 #pragma unroll
     for (int u = 0; u < U; ++u) {
         const int32_t v = v0 + u * kWave + lane;
-        if (v >= V)
+        if (!EXACT && v >= V)
             continue;
         const int64_t o = t * V + v;
         if constexpr (F32_OUT) {
@@ -107,6 +116,12 @@ __global__ __launch_bounds__(256) void combine_kernel(const u32x4 *__restrict__ 
     }
 }
 
+// With no rows to read every output is zero (each sum is empty).
+__global__ __launch_bounds__(256) void zero_fill_kernel(u32x4 *__restrict__ out, int64_t n) {
+    for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n; i += (int64_t)gridDim.x * 256)
+        out[i] = u32x4{0u, 0u, 0u, 0u};
+}
+
 template <int U, int KC>
 hipError_t launch_uk(const void *recv, const int32_t *slot_pos, const float *topk_w, int64_t T,
                      int32_t V, int32_t k, void *out, bool out_f32, int64_t max_rows,
@@ -115,16 +130,27 @@ hipError_t launch_uk(const void *recv, const int32_t *slot_pos, const float *top
     const int64_t items = T * chunks;
     const int waves_per_block = 4;
     const int64_t blocks = (items + waves_per_block - 1) / waves_per_block;
+    if (blocks > INT32_MAX)
+        return hipErrorInvalidValue;
+    const bool exact = V % (U * kWave) == 0;
+    const dim3 grid((unsigned)blocks), block(waves_per_block * kWave);
+    const u32x4 *rv = static_cast<const u32x4 *>(recv);
     (void)hipGetLastError();  // drop an error left by an earlier, already reported call
     TraceSlot ts = trace_acquire();
-    if (out_f32)
-        hipExtLaunchKernelGGL(combine_kernel<U, KC, true>, dim3((unsigned)blocks),
-                              dim3(waves_per_block * kWave), 0, stream, ts.start, ts.stop, 0,
-                              (const u32x4 *)recv, slot_pos, topk_w, T, V, chunks, k, out, max_rows, sel);
+#define EP_COMBINE_ARGS grid, block, 0, stream, ts.start, ts.stop, 0, rv, slot_pos, topk_w, T, V, chunks, k, out, max_rows, sel
+#define EP_COMBINE_LAUNCH(F32, EX)                                                      \
+    (k == KC ? hipExtLaunchKernelGGL((combine_kernel<U, KC, F32, EX, true>), EP_COMBINE_ARGS) \
+             : hipExtLaunchKernelGGL((combine_kernel<U, KC, F32, EX, false>), EP_COMBINE_ARGS))
+    if (out_f32 && exact)
+        EP_COMBINE_LAUNCH(true, true);
+    else if (out_f32)
+        EP_COMBINE_LAUNCH(true, false);
+    else if (exact)
+        EP_COMBINE_LAUNCH(false, true);
     else
-        hipExtLaunchKernelGGL(combine_kernel<U, KC, false>, dim3((unsigned)blocks),
-                              dim3(waves_per_block * kWave), 0, stream, ts.start, ts.stop, 0,
-                              (const u32x4 *)recv, slot_pos, topk_w, T, V, chunks, k, out, max_rows, sel);
+        EP_COMBINE_LAUNCH(false, false);
+#undef EP_COMBINE_LAUNCH
+#undef EP_COMBINE_ARGS
     hipError_t err = hipGetLastError();
     if (err == hipSuccess)
         trace_submit("combine", ts);
@@ -139,6 +165,13 @@ hipError_t launch_combine(const void *recv, const int32_t *slot_pos, const float
     if (T == 0)
         return hipSuccess;
     const int32_t V = H / 8;
+    if (max_rows <= 0) {  // the kernels below read row 0 for slots without a row
+        const int64_t n = T * V * (out_f32 ? 2 : 1);
+        const int64_t blocks = std::min<int64_t>((n + 255) / 256, 4096);
+        (void)hipGetLastError();
+        hipLaunchKernelGGL(zero_fill_kernel, dim3((unsigned)blocks), dim3(256), 0, stream, static_cast<u32x4 *>(out), n);
+        return hipGetLastError();
+    }
     // KC*U 16-byte loads per lane in flight: 16 for k >= 4, 4 for k = 2 and 3 (two-group
     // chunks: more waves, which measured faster on MI355X than four-group chunks there)
     if (k >= 8)

@@ -72,6 +72,19 @@ def test_window_layout_pack_partials(N, E, k, window):
     assert np.array_equal(out16.view(torch.int16).cpu().numpy().view(np.uint16), b16)
 
 
+@pytest.mark.parametrize("out_dtype", [torch.float32, torch.bfloat16])
+def test_combine_rows_without_rows_is_zero(out_dtype):
+    """A window no token routes to: no rows, every slot -1, every sum empty."""
+    say(f"combine_rows with no rows ({out_dtype})")
+    N, H, k = 37, 72, 2
+    slot_pos = torch.full((N * k,), -1, dtype=torch.int32, device=DEV)
+    w = torch.full((N, k), 0.5, dtype=torch.float32, device=DEV)
+    y = torch.empty((0, H), dtype=torch.int16, device=DEV)
+    out = torch.full((N, H), 7.0, dtype=out_dtype, device=DEV)
+    ep.combine_rows(y, slot_pos, w, out)
+    assert torch.count_nonzero(out.float()).item() == 0
+
+
 def test_window_layout_routing_errors():
     say("window layout routing errors")
     idx = np.array([[0, 1], [2, 2], [3, 0]], np.int32)       # a duplicate outside the window
