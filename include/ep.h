@@ -232,7 +232,7 @@ ep_status ep_dispatch(const void *x_dev, int64_t num_tokens, int32_t hidden, int
  * and Sec. 2.2 (rows packed into contiguous segments for the DMA engine).
  * For few experts one kernel does both steps, each workgroup counting every routing
  * entry itself (no exchange between workgroups, no second kernel): with HBM staging or
- * the default pinned mode, E <= 32, topk in {1, 2, 4}, T*topk <= 65536, hidden a
+ * the default pinned mode, E <= 64, topk in {1, 2, 4}, T*topk <= 65536, hidden a
  * multiple of 512 with hidden/512 in {1, 2, 4, 8, 16}, and topk_idx 16-byte aligned.
  * Otherwise the two steps run as their own kernels.  The fused kernel writes only the
  * status word of the workspace. */

@@ -26,8 +26,8 @@
 // The outputs equal those of the layout kernel followed by the pack kernel, bit for bit.
 // Workgroups never wait on each other, so nothing needs them resident together.
 //
-// Limits (the host falls back to the two kernels outside them): E <= 32 (a lane per
-// expert in step B), k in {1, 2, 4} (a token row lies inside one 4-id load), T*k <= 65536
+// Limits (the host falls back to the two kernels outside them): E <= 64 (a lane per
+// expert in step C), k in {1, 2, 4} (a token row lies inside one 4-id load), T*k <= 65536
 // (every workgroup reads every id), rows of 1, 2, 4, 8 or 16 groups (H a multiple of 512
 // up to 8192), a 16-byte aligned routing array.
 #include "ep_internal.h"
@@ -38,7 +38,7 @@ namespace {
 
 constexpr int kFWaves = 16;                  // waves per workgroup
 constexpr int kFThreads = kFWaves * kWave;   // 1024
-constexpr int kFMaxE = 32;                   // experts: one lane each in step B
+constexpr int kFMaxE = 64;                   // experts: one lane each in step C
 constexpr int64_t kFMaxSlots = 65536;        // T*k: every workgroup reads every id
 constexpr int kFMaxOwn = 256;                // entries one workgroup owns (LDS rows)
 constexpr int kFOwnRounds = kFMaxOwn / kWave;
@@ -176,22 +176,33 @@ __global__ __launch_bounds__(kFThreads) void layout_pack_kernel(FusedArgs a, int
                 pre += s_pre[c * kFMaxE + lane];
             }
         }
-        const int excl = wave_inclusive_scan(tot) - tot;  // lane E: the total
+        const int incl = wave_inclusive_scan(tot);
+        const int excl = incl - tot;
+        const int total = __shfl(incl, kWave - 1);
         if (lane < a.E)
             s_base[lane] = excl + pre;
         if (blockIdx.x == 0) {
             if (lane < a.E)
                 a.expert_counts[lane] = tot;
-            if (lane <= a.E)
+            if (lane <= a.E)  // lane E (< 64) holds the total too; E == 64 is stored below
                 a.expert_offsets[lane] = excl;
+            // rank r's first row: the exclusive offset of expert r*L (the total for r = R)
             const int L = a.E / a.R;
-            const int lo = __shfl(excl, min(lane, a.R) * L);
-            const int hi = __shfl(excl, min(lane + 1, a.R) * L);
+            auto offset_of = [&](int e) {
+                const int v = __shfl(excl, min(e, kWave - 1));
+                return e >= a.E ? total : v;
+            };
+            const int lo = offset_of(min(lane, a.R) * L);
+            const int hi = offset_of(min(lane + 1, a.R) * L);
             if (lane < a.R)
                 a.rank_counts[lane] = hi - lo;
             if (lane <= a.R)
                 a.rank_offsets[lane] = lo;
             if (lane == 0) {
+                if (a.E == kWave)
+                    a.expert_offsets[kWave] = total;
+                if (a.R == kWave)
+                    a.rank_offsets[kWave] = total;
                 *a.status = (uint32_t)s_err;
                 if (a.epoch_word)
                     *a.epoch_word = a.epoch;

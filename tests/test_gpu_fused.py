@@ -58,6 +58,9 @@ FUSED_CASES = [
     ("k2_limit_65536_slots", 32768, 512, 32, 2, 8, "random"),   # 8 tokens per wave
     ("k4_limit_65536_slots", 16384, 512, 16, 4, 4, "skewed"),
     ("k1_limit_65536_slots", 65536, 512, 2, 1, 1, "random"),    # 16 tokens per wave
+    ("e33", 2000, 1024, 33, 2, 3, "random"),
+    ("e64_r64_one_expert_per_rank", 5000, 2048, 64, 2, 64, "skewed"),
+    ("e64_k4", 7000, 512, 64, 4, 8, "random"),
 ]
 
 
@@ -124,7 +127,8 @@ def test_fused_repeated_calls_reuse_buffers():
 
 FALLBACK_CASES = [
     # outside the fused kernel's limits: the two kernels run
-    ("e64_too_many_experts", 500, 512, 64, 2, 4),
+    ("e65_too_many_experts", 500, 512, 65, 2, 5),
+    ("e128", 500, 512, 128, 2, 4),
     ("k8", 300, 512, 16, 8, 4),
     ("k3", 300, 512, 16, 3, 4),
     ("rows14", 200, 7168, 16, 2, 4),
