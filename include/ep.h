@@ -388,6 +388,9 @@ typedef struct {
     char name[48];
     int64_t count;
     double total_ms, min_ms, max_ms;
+    /* percentiles of the traced durations (the sample of rank round(q*(count-1)) in
+     * sorted order; computed over the first 65536 durations of each name) */
+    double p10_ms, p50_ms, p90_ms;
 } ep_trace_stat;
 
 /* While enabled, every kernel launch and every host-leg DMA run of the library is

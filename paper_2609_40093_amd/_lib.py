@@ -43,7 +43,8 @@ class DenseView(ctypes.Structure):
 
 class TraceStat(ctypes.Structure):
     _fields_ = [("name", ctypes.c_char * 48), ("count", c_i64), ("total_ms", ctypes.c_double),
-                ("min_ms", ctypes.c_double), ("max_ms", ctypes.c_double)]
+                ("min_ms", ctypes.c_double), ("max_ms", ctypes.c_double), ("p10_ms", ctypes.c_double),
+                ("p50_ms", ctypes.c_double), ("p90_ms", ctypes.c_double)]
 
 
 # name -> (restype, argtypes)

@@ -562,7 +562,8 @@ def trace_reset() -> None:
 
 
 def trace_read() -> dict:
-    """{name: {count, total_ms, mean_ms, min_ms, max_ms}} of the traced launches so far."""
+    """{name: {count, total_ms, mean_ms, min_ms, max_ms, p10_ms, p50_ms, p90_ms}} of the traced
+    launches so far."""
     cap = 64
     arr = (_lib.TraceStat * cap)()
     n = ctypes.c_int32()
@@ -571,7 +572,8 @@ def trace_read() -> dict:
     for i in range(n.value):
         s = arr[i]
         out[s.name.decode()] = dict(count=s.count, total_ms=s.total_ms, mean_ms=s.total_ms / max(1, s.count),
-                                    min_ms=s.min_ms, max_ms=s.max_ms)
+                                    min_ms=s.min_ms, max_ms=s.max_ms, p10_ms=s.p10_ms, p50_ms=s.p50_ms,
+                                    p90_ms=s.p90_ms)
     return out
 
 

@@ -78,10 +78,26 @@ struct Pending {
 };
 std::vector<Pending> g_pending;
 std::vector<hipEvent_t> g_event_pool;
+constexpr size_t kTraceSamples = 65536;  // durations kept per name for the percentiles
 struct Stat {
     int64_t count = 0;
     double total = 0, mn = 1e300, mx = 0;
+    std::vector<float> samples;
+    void add(double ms) {
+        count += 1;
+        total += ms;
+        mn = std::min(mn, ms);
+        mx = std::max(mx, ms);
+        if (samples.size() < kTraceSamples)
+            samples.push_back((float)ms);
+    }
 };
+double percentile(std::vector<float> v, double q) {  // by copy: sorted here
+    if (v.empty())
+        return 0.0;
+    std::sort(v.begin(), v.end());
+    return v[(size_t)(q * (double)(v.size() - 1) + 0.5)];
+}
 std::map<std::string, Stat> g_stats;
 
 hipEvent_t pool_get() {
@@ -126,11 +142,7 @@ void trace_host(const char *name, double ms) {
     if (!g_trace_on.load(std::memory_order_relaxed))
         return;
     std::lock_guard<std::mutex> lk(g_trace_mu);
-    Stat &s = g_stats[name];
-    s.count += 1;
-    s.total += ms;
-    s.mn = std::min(s.mn, ms);
-    s.mx = std::max(s.mx, ms);
+    g_stats[name].add(ms);
 }
 
 }  // namespace ep
@@ -885,11 +897,7 @@ extern "C" ep_status ep_trace_read(ep_trace_stat *stats, int32_t capacity, int32
         float ms = 0.f;
         EP_HIP(hipEventSynchronize(p.stop));
         EP_HIP(hipEventElapsedTime(&ms, p.start, p.stop));
-        ep::Stat &s = ep::g_stats[p.name];
-        s.count += 1;
-        s.total += ms;
-        s.mn = std::min<double>(s.mn, ms);
-        s.mx = std::max<double>(s.mx, ms);
+        ep::g_stats[p.name].add(ms);
         ep::g_event_pool.push_back(p.start);
         ep::g_event_pool.push_back(p.stop);
     }
@@ -904,6 +912,9 @@ extern "C" ep_status ep_trace_read(ep_trace_stat *stats, int32_t capacity, int32
             o.total_ms = kv.second.total;
             o.min_ms = kv.second.count ? kv.second.mn : 0.0;
             o.max_ms = kv.second.mx;
+            o.p10_ms = ep::percentile(kv.second.samples, 0.1);
+            o.p50_ms = ep::percentile(kv.second.samples, 0.5);
+            o.p90_ms = ep::percentile(kv.second.samples, 0.9);
         }
         ++n;
     }

@@ -124,6 +124,7 @@ def test_null_staging_calls(lib):
 
 
 def test_trace_without_launches(lib):
+    assert ctypes.sizeof(_lib.TraceStat) == 48 + 8 + 6 * 8    # ep_trace_stat in include/ep.h
     assert lib.ep_trace_reset() == 0
     arr = (_lib.TraceStat * 4)()
     n = ctypes.c_int32(-1)

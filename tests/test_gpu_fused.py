@@ -270,3 +270,21 @@ def test_fused_argument_errors_enqueue_nothing():
         ep.dispatch_fused(flat[1:1 + 64 * 512].view(64, 512), idx_d, 8, 4, st)
     small.close()
     st.close()
+
+
+def test_trace_percentiles():
+    """The trace's percentiles lie between the minimum and the maximum, in order."""
+    case = make_case("trace", 2048, 1024, 8, 2, 4, "random", seed=13)
+    idx_d, x_d = to_dev(case.topk_idx), to_dev(case.x.view(np.int16))
+    st = ep.Staging("hbm", case.slots, case.H, case.R, num_buffers=1)
+    say("trace percentiles")
+    ep.trace_reset()
+    ep.trace_enable(True)
+    lay = None
+    for _ in range(25):
+        lay = ep.dispatch_fused(x_d, idx_d, case.E, case.R, st, out=lay)
+    ep.trace_enable(False)
+    s = ep.trace_read()["layout_pack"]
+    assert s["count"] == 25
+    assert 0 < s["min_ms"] <= s["p10_ms"] <= s["p50_ms"] <= s["p90_ms"] <= s["max_ms"]
+    st.close()
