@@ -5,7 +5,10 @@
 // Sec. 2.2) otherwise run as two kernels, and the layout's workgroups exchange their
 // per-expert totals through memory.  With few experts every workgroup can afford to count
 // all entries itself; that removes the exchange and the kernel boundary between layout
-// and pack.  A workgroup owns 16*tpw consecutive tokens (one run of tpw per wave):
+// and pack.  A workgroup of W waves owns W*tpw consecutive tokens (a run of tpw per
+// wave); W is 4, 8 or 16 by the number of routing entries (each workgroup counts all of
+// them, so fewer, larger workgroups for more entries; more, smaller ones for few -- less
+// of the kernel waits on its last workgroups):
 //   A. each wave issues the loads of its first ids, then those of its first token row
 //      (they do not depend on the layout; vector loads complete in order, so the ids
 //      come first);
@@ -36,14 +39,13 @@
 namespace ep {
 namespace {
 
-constexpr int kFWaves = 16;                  // waves per workgroup
-constexpr int kFThreads = kFWaves * kWave;   // 1024
+constexpr int kFMaxThreads = 16 * kWave;    // largest workgroup (16 waves)
 constexpr int kFMaxE = 64;                   // experts: one lane each in step C
 constexpr int64_t kFMaxSlots = 65536;        // T*k: every workgroup reads every id
 constexpr int kFMaxOwn = 256;                // entries one workgroup owns (LDS rows)
 constexpr int kFOwnRounds = kFMaxOwn / kWave;
 constexpr int kFBatch = 4;                   // 16-byte id loads in flight per lane
-constexpr int kFMaxBlocks = 256;             // workgroups: each reads all ids once
+constexpr int kFMaxWaves = 4096;             // waves in flight over the device (16 per CU)
 
 typedef int32_t i32x4 __attribute__((ext_vector_type(4)));
 
@@ -61,13 +63,14 @@ __device__ __forceinline__ bool row_repeats(i32x4 v, int E) {
         return false;
 }
 
-// Loads the 4-id groups qw + b*kFThreads + lane of a batch: every load is issued (an
-// index past the last whole group rereads that group; the caller masks it by index), so
-// the compiler can count the loads in flight and wait for the ids alone.
-__device__ __forceinline__ void load_ids(const i32x4 *q, int64_t full, int64_t qw, int lane, i32x4 *v) {
+// Loads the 4-id groups qw + b*threads + lane of a batch: every load is issued (an index
+// past the last whole group rereads that group; the caller masks it by index), so the
+// compiler can count the loads in flight and wait for the ids alone.
+__device__ __forceinline__ void load_ids(const i32x4 *q, int64_t full, int64_t qw, int lane, int threads,
+                                         i32x4 *v) {
 #pragma unroll
     for (int b = 0; b < kFBatch; ++b)
-        v[b] = q[min(qw + (int64_t)b * kFThreads + lane, full - 1)];
+        v[b] = q[min(qw + (int64_t)b * threads + lane, full - 1)];
 }
 
 constexpr int kFCopies = 16;  // copies of the LDS counters (lane % 16 picks one)
@@ -85,29 +88,30 @@ __device__ __forceinline__ void count_id(int id, bool in, bool before, int E, in
 }
 
 template <int U, int K>
-__global__ __launch_bounds__(kFThreads) void layout_pack_kernel(FusedArgs a, int32_t tpw) {
+__global__ __launch_bounds__(kFMaxThreads) void layout_pack_kernel(FusedArgs a, int32_t tpw) {
     __shared__ int s_all[kFCopies * kFMaxE];
     __shared__ int s_pre[kFCopies * kFMaxE];
     __shared__ int s_base[kFMaxE];
     __shared__ int s_pos[kFMaxOwn];
     __shared__ int s_err;
     const int tid = threadIdx.x, lane = tid & (kWave - 1), w = tid / kWave;
+    const int threads = blockDim.x, waves = threads / kWave;
     const int64_t slots = a.T * K;
-    const int64_t tok0 = (int64_t)blockIdx.x * kFWaves * tpw;
-    const int64_t tok1 = min(a.T, tok0 + (int64_t)kFWaves * tpw);
+    const int64_t tok0 = (int64_t)blockIdx.x * waves * tpw;
+    const int64_t tok1 = min(a.T, tok0 + (int64_t)waves * tpw);
     const int64_t ent0 = tok0 * K, ent1 = tok1 * K;
     const int32_t V = a.H / 8;
     const u32x4 *x = static_cast<const u32x4 *>(a.x);
     const i32x4 *q = reinterpret_cast<const i32x4 *>(a.topk_idx);
     const int64_t full = slots / 4;  // whole 4-id groups; the 0..3 ids after them are the tail
-    constexpr int64_t kStride = (int64_t)kFThreads * kFBatch;
+    const int64_t stride = (int64_t)threads * kFBatch;
 
     // A. first ids, the own entries' ids (step D), then this wave's first token row (a
     //    wave past the workgroup's last token loads that token instead, storing nothing)
     i32x4 v[kFBatch];
     int64_t qw = (int64_t)w * kWave;
     if (full > 0)
-        load_ids(q, full, qw, lane, v);
+        load_ids(q, full, qw, lane, threads, v);
     int own_id[kFOwnRounds];
 #pragma unroll
     for (int r = 0; r < kFOwnRounds; ++r)
@@ -120,9 +124,9 @@ __global__ __launch_bounds__(kFThreads) void layout_pack_kernel(FusedArgs a, int
         for (int u = 0; u < U; ++u)
             d[u] = __builtin_nontemporal_load(src + u * kWave);
     }
-    if (tid < kFCopies * kFMaxE) {
-        s_all[tid] = 0;
-        s_pre[tid] = 0;
+    for (int i = tid; i < kFCopies * kFMaxE; i += threads) {
+        s_all[i] = 0;
+        s_pre[i] = 0;
     }
     if (tid == 0)
         s_err = 0;
@@ -133,12 +137,12 @@ __global__ __launch_bounds__(kFThreads) void layout_pack_kernel(FusedArgs a, int
     auto count_batch = [&](int64_t qb) {
 #pragma unroll
         for (int b = 0; b < kFBatch; ++b) {
-            const int64_t g = qb + (int64_t)b * kFThreads;  // this round's first group
+            const int64_t g = qb + (int64_t)b * threads;  // this round's first group
             if (g >= full)
                 break;
             const int64_t qi = g + lane;
             const bool in = qi < full;
-            // entries before this workgroup's: whole 4-id groups (ent0 is a multiple of 16)
+            // entries before this workgroup's: whole 4-id groups (ent0 is a multiple of 4)
             const bool before = qi * 4 < ent0;
             dup |= in && row_repeats<K>(v[b], a.E);
 #pragma unroll
@@ -149,8 +153,8 @@ __global__ __launch_bounds__(kFThreads) void layout_pack_kernel(FusedArgs a, int
     // the first batch outside the loop: its wait leaves the token row's loads in flight
     if (qw < full)
         count_batch(qw);
-    for (qw += kStride; qw < full; qw += kStride) {  // wave-uniform; T*k > 16384 only
-        load_ids(q, full, qw, lane, v);
+    for (qw += stride; qw < full; qw += stride) {  // wave-uniform; many entries only
+        load_ids(q, full, qw, lane, threads, v);
         count_batch(qw);
     }
     if (w == 0 && full * 4 < slots) {  // the tail: 1..3 ids (a whole token row for k <= 2)
@@ -263,15 +267,15 @@ __global__ __launch_bounds__(kFThreads) void layout_pack_kernel(FusedArgs a, int
 }
 
 template <int U>
-void launch_k(const FusedArgs &a, int32_t tpw, unsigned blocks, hipStream_t stream, TraceSlot ts) {
+void launch_k(const FusedArgs &a, int32_t tpw, unsigned blocks, int threads, hipStream_t stream, TraceSlot ts) {
     if (a.k == 1)
-        hipExtLaunchKernelGGL(layout_pack_kernel<U, 1>, dim3(blocks), dim3(kFThreads), 0, stream, ts.start, ts.stop, 0,
+        hipExtLaunchKernelGGL(layout_pack_kernel<U, 1>, dim3(blocks), dim3(threads), 0, stream, ts.start, ts.stop, 0,
                               a, tpw);
     else if (a.k == 2)
-        hipExtLaunchKernelGGL(layout_pack_kernel<U, 2>, dim3(blocks), dim3(kFThreads), 0, stream, ts.start, ts.stop, 0,
+        hipExtLaunchKernelGGL(layout_pack_kernel<U, 2>, dim3(blocks), dim3(threads), 0, stream, ts.start, ts.stop, 0,
                               a, tpw);
     else
-        hipExtLaunchKernelGGL(layout_pack_kernel<U, 4>, dim3(blocks), dim3(kFThreads), 0, stream, ts.start, ts.stop, 0,
+        hipExtLaunchKernelGGL(layout_pack_kernel<U, 4>, dim3(blocks), dim3(threads), 0, stream, ts.start, ts.stop, 0,
                               a, tpw);
 }
 
@@ -289,20 +293,25 @@ bool fused_layout_pack_fits(int64_t T, int32_t k, int32_t E, int32_t H, const vo
 hipError_t launch_layout_pack(const FusedArgs &a, hipStream_t stream) {
     if (!fused_layout_pack_fits(a.T, a.k, a.E, a.H, a.topk_idx) || a.R < 1 || a.E % a.R != 0)
         return hipErrorInvalidValue;
-    // tokens per wave: enough that at most kFMaxBlocks workgroups cover T
-    const int64_t per_block_min = (a.T + kFMaxBlocks - 1) / kFMaxBlocks;
-    const int32_t tpw = (int32_t)((per_block_min + kFWaves - 1) / kFWaves);
-    const int64_t blocks = (a.T + (int64_t)kFWaves * tpw - 1) / ((int64_t)kFWaves * tpw);
-    if ((int64_t)kFWaves * tpw * a.k > kFMaxOwn)
+    // workgroup size by the entries every workgroup counts (measured on MI355X: 4 or 8
+    // waves win up to 8192 entries, 16 above); tokens per wave: enough that the workgroups
+    // hold at most kFMaxWaves waves
+    const int64_t slots = a.T * a.k;
+    const int waves = slots <= 4096 ? 4 : (slots <= 8192 ? 8 : 16);
+    const int64_t max_blocks = kFMaxWaves / waves;
+    const int64_t per_block_min = (a.T + max_blocks - 1) / max_blocks;
+    const int32_t tpw = (int32_t)((per_block_min + waves - 1) / waves);
+    const int64_t blocks = (a.T + (int64_t)waves * tpw - 1) / ((int64_t)waves * tpw);
+    if ((int64_t)waves * tpw * a.k > kFMaxOwn)
         return hipErrorInvalidValue;  // excluded by the limits above
     (void)hipGetLastError();  // drop an error left by an earlier, already reported call
     TraceSlot ts = trace_acquire();
     switch (a.H / 512) {
-    case 1: launch_k<1>(a, tpw, (unsigned)blocks, stream, ts); break;
-    case 2: launch_k<2>(a, tpw, (unsigned)blocks, stream, ts); break;
-    case 4: launch_k<4>(a, tpw, (unsigned)blocks, stream, ts); break;
-    case 8: launch_k<8>(a, tpw, (unsigned)blocks, stream, ts); break;
-    default: launch_k<16>(a, tpw, (unsigned)blocks, stream, ts); break;
+    case 1: launch_k<1>(a, tpw, (unsigned)blocks, waves * kWave, stream, ts); break;
+    case 2: launch_k<2>(a, tpw, (unsigned)blocks, waves * kWave, stream, ts); break;
+    case 4: launch_k<4>(a, tpw, (unsigned)blocks, waves * kWave, stream, ts); break;
+    case 8: launch_k<8>(a, tpw, (unsigned)blocks, waves * kWave, stream, ts); break;
+    default: launch_k<16>(a, tpw, (unsigned)blocks, waves * kWave, stream, ts); break;
     }
     hipError_t err = hipGetLastError();
     if (err == hipSuccess)

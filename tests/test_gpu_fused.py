@@ -46,7 +46,8 @@ def layout_np(lay):
 
 
 FUSED_CASES = [
-    # name, T, H, E, k, R, routing; every case fits the fused kernel
+    # name, T, H, E, k, R, routing; every case fits the fused kernel (workgroups of 4 waves
+    # up to 4096 entries, 8 up to 8192, 16 above: all three sizes appear)
     ("k2_e8_rows8", 4096, 4096, 8, 2, 4, "skewed"),
     ("k2_e16_rows2", 128, 1024, 16, 2, 4, "random"),
     ("k1_e4_rows1_ragged_tokens", 1001, 512, 4, 1, 2, "random"),
@@ -59,6 +60,8 @@ FUSED_CASES = [
     ("k4_limit_65536_slots", 16384, 512, 16, 4, 4, "skewed"),
     ("k1_limit_65536_slots", 65536, 512, 2, 1, 1, "random"),    # 16 tokens per wave
     ("e33", 2000, 1024, 33, 2, 3, "random"),
+    ("eight_wave_groups_ragged", 3001, 2048, 16, 2, 4, "skewed"),   # 6002 entries: 8-wave workgroups
+    ("eight_wave_groups_k1", 5000, 1024, 8, 1, 2, "random"),
     ("e64_r64_one_expert_per_rank", 5000, 2048, 64, 2, 64, "skewed"),
     ("e64_k4", 7000, 512, 64, 4, 8, "random"),
 ]
