@@ -35,7 +35,7 @@ MALL_BYTES = 256 << 20
 def parse():
     p = argparse.ArgumentParser()
     p.add_argument("--gpus", type=int, default=1)
-    p.add_argument("--steps", type=int, default=50)
+    p.add_argument("--steps", type=int, default=200)
     p.add_argument("--warmup", type=int, default=10)
     p.add_argument("--workload", default="coarse", help="synth config name (default: the coarse-expert layer)")
     p.add_argument("--no-cpu-baseline", action="store_true")
@@ -151,10 +151,10 @@ def main():
     ep.trace_reset()
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    # one step in four carries timing events (they cost the stream ~2 us per traced
+    # one step in eight carries timing events (they cost the stream ~2 us per traced
     # launch), alternating between the dispatch and the combine
     for i in range(args.steps):
-        step(args.warmup + i, trace=("dispatch", None, "combine", None)[i % 4])
+        step(args.warmup + i, trace=("dispatch", None, None, None, "combine", None, None, None)[i % 8])
     t_issue = time.perf_counter()
     torch.cuda.synchronize()
     t1 = time.perf_counter()
@@ -322,7 +322,7 @@ def bench_pinned(cfg, inp, y, args, dev) -> dict:
     lay = ep.dispatch_layout(idx, E, R)
     counts = lay.rank_counts.cpu().numpy().astype(np.int64)
     me = 0
-    steps = max(5, args.steps // 2)
+    steps = max(5, min(args.steps // 2, 50))
     peaks = pcie_peaks(dev)
     modes = {}
     for name, mode in PINNED_MODES:
@@ -518,7 +518,7 @@ def bench_dense(cfg, inp, args, dev, peaks) -> dict:
             peers.post_dense(buf, epoch, "rs")
             ep.reducescatter(d, blocks, num_tokens=T, out=out, reduce_on_host=on_host, buf=buf, epoch=epoch)
 
-        steps = max(5, args.steps // 4)
+        steps = max(5, min(args.steps // 4, 25))
         for i in range(args.warmup):
             step(i)
         d.status()
@@ -599,7 +599,7 @@ def bench_graph(names, args, dev, peaks) -> dict:
         for _ in range(args.warmup):
             g.replay()
         torch.cuda.synchronize()
-        steps = max(10, args.steps)
+        steps = max(10, min(args.steps, 100))
         t0 = time.perf_counter()
         for _ in range(steps):
             g.replay()
