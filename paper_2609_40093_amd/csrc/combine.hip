@@ -33,8 +33,10 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
     return __builtin_bit_cast(uint32_t, b);
 }
 
-// FIXED_K: k == KC (one batch of slots, its bounds known at compile time).
-template <int U, int KC, bool F32_OUT, bool EXACT, bool FIXED_K>
+// FIXED_K: k == KC (one batch of slots, its bounds known at compile time).  SEL: the
+// receive buffer is chosen by a round counter in device memory (graph-replayed rounds);
+// without it the kernel loads nothing before the slot positions.
+template <int U, int KC, bool F32_OUT, bool EXACT, bool FIXED_K, bool SEL>
 __global__ __launch_bounds__(256) void combine_kernel(const u32x4 *__restrict__ recv,
                                                       const int32_t *__restrict__ slot_pos,
                                                       const float *__restrict__ topk_w, int64_t T,
@@ -42,7 +44,7 @@ __global__ __launch_bounds__(256) void combine_kernel(const u32x4 *__restrict__ 
                                                       void *__restrict__ out, int64_t max_rows,
                                                       RoundSel sel) {
     const int lane = threadIdx.x & (kWave - 1);
-    if (sel.round && (__hip_atomic_load(sel.round, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) & 1u))
+    if (SEL && (__hip_atomic_load(sel.round, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) & 1u))
         recv = static_cast<const u32x4 *>(sel.alt);
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
     const int64_t item = (int64_t)blockIdx.x * (blockDim.x / kWave) + wave;
@@ -65,22 +67,27 @@ __global__ __launch_bounds__(256) void combine_kernel(const u32x4 *__restrict__ 
         u32x4 d[KC][U];
         float g[KC];
         uint32_t keep[KC];  // all ones for a slot with a row, else 0
+        bool ok[KC];
+        // positions first, then every row load, then the gates (needed only by the FMAs);
+        // every load is issued for every jj (a slot past k has no row)
 #pragma unroll
         for (int jj = 0; jj < KC; ++jj) {
             const int32_t j = j0 + jj;
-            const int32_t jc = min(j, kk - 1);  // loads issued for every jj; a slot past k has no row
-            const int64_t p = j < kk ? (int64_t)sp[jc] : -1;  // wave-uniform
-            const float gj = wt[jc];
-            const bool ok = p >= 0 && p < max_rows;
-            keep[jj] = ok ? ~0u : 0u;
-            g[jj] = ok ? gj : -0.0f;
-            const u32x4 *src = recv + (ok ? p : 0) * V;
+            const int64_t p = j < kk ? (int64_t)sp[min(j, kk - 1)] : -1;  // wave-uniform
+            ok[jj] = p >= 0 && p < max_rows;
+            keep[jj] = ok[jj] ? ~0u : 0u;
+            const u32x4 *src = recv + (ok[jj] ? p : 0) * V;
 #pragma unroll
             for (int u = 0; u < U; ++u) {
                 const int32_t v = v0 + u * kWave + lane;
                 d[jj][u] = EXACT ? __builtin_nontemporal_load(src + v)
                                  : __builtin_nontemporal_load(src + min(v, V - 1));
             }
+        }
+#pragma unroll
+        for (int jj = 0; jj < KC; ++jj) {
+            const float gj = wt[min(j0 + jj, kk - 1)];
+            g[jj] = ok[jj] ? gj : -0.0f;
         }
 #pragma unroll
         for (int jj = 0; jj < KC; ++jj)
@@ -138,10 +145,14 @@ hipError_t launch_uk(const void *recv, const int32_t *slot_pos, const float *top
     (void)hipGetLastError();  // drop an error left by an earlier, already reported call
     TraceSlot ts = trace_acquire();
 #define EP_COMBINE_ARGS grid, block, 0, stream, ts.start, ts.stop, 0, rv, slot_pos, topk_w, T, V, chunks, k, out, max_rows, sel
-#define EP_COMBINE_LAUNCH(F32, EX)                                                      \
-    (k == KC ? hipExtLaunchKernelGGL((combine_kernel<U, KC, F32, EX, true>), EP_COMBINE_ARGS) \
-             : hipExtLaunchKernelGGL((combine_kernel<U, KC, F32, EX, false>), EP_COMBINE_ARGS))
-    if (out_f32 && exact)
+#define EP_COMBINE_LAUNCH(F32, EX)                                                             \
+    (k == KC ? hipExtLaunchKernelGGL((combine_kernel<U, KC, F32, EX, true, false>), EP_COMBINE_ARGS) \
+             : hipExtLaunchKernelGGL((combine_kernel<U, KC, F32, EX, false, false>), EP_COMBINE_ARGS))
+    if (sel.round && out_f32)  // graph-replayed rounds: the general instance reading the round
+        hipExtLaunchKernelGGL((combine_kernel<U, KC, true, false, false, true>), EP_COMBINE_ARGS);
+    else if (sel.round)
+        hipExtLaunchKernelGGL((combine_kernel<U, KC, false, false, false, true>), EP_COMBINE_ARGS);
+    else if (out_f32 && exact)
         EP_COMBINE_LAUNCH(true, true);
     else if (out_f32)
         EP_COMBINE_LAUNCH(true, false);
