@@ -87,7 +87,10 @@ __device__ __forceinline__ void count_id(int id, bool in, bool before, int E, in
     }
 }
 
-template <int U, int K>
+// MULTI: more ids than one batch of the workgroup's loads (the count loops).  Instances
+// without the loop have only straight-line loads, so the compiler's waits stay exact and
+// no wave waits for its token row before the count's barrier.
+template <int U, int K, bool MULTI>
 __global__ __launch_bounds__(kFMaxThreads) void layout_pack_kernel(FusedArgs a, int32_t tpw) {
     __shared__ int s_all[kFCopies * kFMaxE];
     __shared__ int s_pre[kFCopies * kFMaxE];
@@ -116,6 +119,12 @@ __global__ __launch_bounds__(kFMaxThreads) void layout_pack_kernel(FusedArgs a, 
 #pragma unroll
     for (int r = 0; r < kFOwnRounds; ++r)
         own_id[r] = a.topk_idx[min(ent0 + r * kWave + lane, ent1 - 1)];  // masked by index in step D
+    // the 0..3 ids after the whole 4-id groups (wave 0 counts them): loaded here, with the
+    // rest, so that no load is left after the count (a load there would make every wave
+    // wait for its token row before the count's barrier)
+    const int64_t ti = full * 4 + lane;
+    const int tail_id = a.topk_idx[min(ti, slots - 1)];
+    const int tail_next = a.topk_idx[min(ti + 1, slots - 1)];
     const int64_t wtok = tok0 + (int64_t)w * tpw;
     u32x4 d[U];
     {
@@ -153,17 +162,18 @@ __global__ __launch_bounds__(kFMaxThreads) void layout_pack_kernel(FusedArgs a, 
     // the first batch outside the loop: its wait leaves the token row's loads in flight
     if (qw < full)
         count_batch(qw);
-    for (qw += stride; qw < full; qw += stride) {  // wave-uniform; many entries only
-        load_ids(q, full, qw, lane, threads, v);
-        count_batch(qw);
+    if (MULTI) {
+        for (qw += stride; qw < full; qw += stride) {  // wave-uniform
+            load_ids(q, full, qw, lane, threads, v);
+            count_batch(qw);
+        }
     }
     if (w == 0 && full * 4 < slots) {  // the tail: 1..3 ids (a whole token row for k <= 2)
-        const int64_t i = full * 4 + lane;
-        const bool in = i < slots;
-        const int id = in ? a.topk_idx[i] : -1;
+        const bool in = ti < slots;
+        const int id = in ? tail_id : -1;
         if (K == 2 && lane == 0)
-            dup |= (unsigned)id < (unsigned)a.E && id == a.topk_idx[i + 1];  // the tail is one row
-        count_id(id, in, i < ent0, a.E, s_all, s_pre, lane % kFCopies, bad_id);
+            dup |= (unsigned)id < (unsigned)a.E && id == tail_next;  // the tail is one row
+        count_id(id, in, ti < ent0, a.E, s_all, s_pre, lane % kFCopies, bad_id);
     }
     const uint32_t wave_err = (__ballot(bad_id) ? kRoutingIdOutOfRange : 0u) | (__ballot(dup) ? kRoutingDuplicate : 0u);
     if (lane == 0 && wave_err)
@@ -266,17 +276,26 @@ __global__ __launch_bounds__(kFMaxThreads) void layout_pack_kernel(FusedArgs a, 
     }
 }
 
+template <int U, bool MULTI>
+void launch_km(const FusedArgs &a, int32_t tpw, unsigned blocks, int threads, hipStream_t stream, TraceSlot ts) {
+    if (a.k == 1)
+        hipExtLaunchKernelGGL((layout_pack_kernel<U, 1, MULTI>), dim3(blocks), dim3(threads), 0, stream, ts.start,
+                              ts.stop, 0, a, tpw);
+    else if (a.k == 2)
+        hipExtLaunchKernelGGL((layout_pack_kernel<U, 2, MULTI>), dim3(blocks), dim3(threads), 0, stream, ts.start,
+                              ts.stop, 0, a, tpw);
+    else
+        hipExtLaunchKernelGGL((layout_pack_kernel<U, 4, MULTI>), dim3(blocks), dim3(threads), 0, stream, ts.start,
+                              ts.stop, 0, a, tpw);
+}
+
 template <int U>
 void launch_k(const FusedArgs &a, int32_t tpw, unsigned blocks, int threads, hipStream_t stream, TraceSlot ts) {
-    if (a.k == 1)
-        hipExtLaunchKernelGGL(layout_pack_kernel<U, 1>, dim3(blocks), dim3(threads), 0, stream, ts.start, ts.stop, 0,
-                              a, tpw);
-    else if (a.k == 2)
-        hipExtLaunchKernelGGL(layout_pack_kernel<U, 2>, dim3(blocks), dim3(threads), 0, stream, ts.start, ts.stop, 0,
-                              a, tpw);
+    // one batch is kFBatch 4-id groups per thread
+    if (a.T * a.k > (int64_t)threads * kFBatch * 4)
+        launch_km<U, true>(a, tpw, blocks, threads, stream, ts);
     else
-        hipExtLaunchKernelGGL(layout_pack_kernel<U, 4>, dim3(blocks), dim3(threads), 0, stream, ts.start, ts.stop, 0,
-                              a, tpw);
+        launch_km<U, false>(a, tpw, blocks, threads, stream, ts);
 }
 
 }  // namespace
