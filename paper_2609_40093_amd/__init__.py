@@ -18,5 +18,7 @@ __all__ = list(_API)
 def __getattr__(name):
     if name in _API:
         from . import api
-        return getattr(api, name)
+        value = getattr(api, name)
+        globals()[name] = value  # later lookups skip this function
+        return value
     raise AttributeError(name)
