@@ -62,6 +62,14 @@ FUSED_CASES = [
     ("e33", 2000, 1024, 33, 2, 3, "random"),
     ("eight_wave_groups_ragged", 3001, 2048, 16, 2, 4, "skewed"),   # 6002 entries: 8-wave workgroups
     ("eight_wave_groups_k1", 5000, 1024, 8, 1, 2, "random"),
+    ("one_expert", 100, 512, 1, 1, 1, "random"),
+    ("ids_shorter_than_one_group", 3, 512, 4, 1, 2, "random"),      # no whole 4-id group
+    # each side of the workgroup-size and count-loop switches (4096, 8192, 16384 entries)
+    ("entries_4096", 2048, 512, 8, 2, 4, "random"),
+    ("entries_4098", 2049, 512, 8, 2, 4, "random"),
+    ("entries_8194", 4097, 512, 8, 2, 4, "random"),
+    ("entries_16384", 8192, 512, 16, 2, 4, "skewed"),
+    ("entries_16386", 8193, 512, 16, 2, 4, "skewed"),
     ("e64_r64_one_expert_per_rank", 5000, 2048, 64, 2, 64, "skewed"),
     ("e64_k4", 7000, 512, 64, 4, 8, "random"),
 ]
