@@ -231,6 +231,7 @@ def main():
     torch.cuda.synchronize()
     copy_gbps = 2 * (1 << 30) * 5 / (ev0.elapsed_time(ev1) * 1e-3) / 1e9
     del a, b
+    same_copy = same_bytes_copy(dev, abytes[dominant], nsets)
 
     result = {
         "metric": METRIC,
@@ -278,6 +279,8 @@ def main():
             "kernel_avg_us": two_kernels,
         },
         "hbm_copy_probe_GBps": round(copy_gbps, 1),
+        "same_bytes_copy": dict(same_copy, kernel=dominant,
+                                kernel_speed_vs_copy=round(same_copy["avg_us"] / dk["avg_us"], 3)),
     }
 
     # ---- pinned host staging: the same layer with SDMA legs, host flags, simulated peers
@@ -634,6 +637,32 @@ def pcie_peaks(dev) -> dict:
            "both": round(ep.pcie_probe(host, devb, nbytes, 3), 2)}
     del host, devb
     return res
+
+
+def same_bytes_copy(dev, nbytes: int, nsets: int, launches: int = 40) -> dict:
+    """The library's plain streaming copy moving `nbytes` per launch (half read, half
+    written), over `nsets` rotated buffer pairs and timed by the same launch events as the
+    path's kernels: what simple streaming code reaches on this chip at this size."""
+    import torch
+
+    import paper_2609_40093_amd as ep
+    half = nbytes // 2 // 4096 * 4096
+    pairs = [(torch.empty(half, dtype=torch.uint8, device=dev), torch.empty(half, dtype=torch.uint8, device=dev))
+             for _ in range(nsets)]
+    for j in range(2 * nsets):
+        ep.copy_probe(pairs[j % nsets][1], pairs[j % nsets][0])
+    torch.cuda.synchronize()
+    ep.trace_reset()
+    ep.trace_enable(True)
+    for j in range(launches):
+        ep.copy_probe(pairs[j % nsets][1], pairs[j % nsets][0])
+    torch.cuda.synchronize()
+    ep.trace_enable(False)
+    st = ep.trace_read()["copy_probe"]
+    ep.trace_reset()
+    us = st["mean_ms"] * 1e3
+    return {"bytes_per_launch": 2 * half, "launches": st["count"], "avg_us": round(us, 3),
+            "p50_us": round(st["p50_ms"] * 1e3, 3), "GBps": round(2 * half / (us * 1e-6) / 1e9, 1)}
 
 
 def cpu_baseline(cfg, inp, y, seconds: float) -> dict:
