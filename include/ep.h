@@ -138,6 +138,10 @@ ep_status ep_layout_status(const void *workspace, hipStream_t stream);
 ep_status ep_staging_alloc(ep_staging_kind kind, int64_t max_rows, int32_t hidden,
                            int32_t num_ranks, int32_t num_buffers, int64_t chunk_bytes,
                            ep_staging **out);
+/* Frees a staging (NULL is a no-op).  Blocks: synchronises the staging's device, waits
+ * for every SDMA copy still in flight (queued copies whose flags never came are started
+ * first, so that none writes freed memory; at most 5 s in all), then frees the buffers.
+ * Stop simulated peers of the staging (ep_sim_peers_stop) before. */
 ep_status ep_staging_free(ep_staging *s);
 
 typedef struct {
@@ -316,6 +320,7 @@ typedef struct ep_dense ep_dense; /* opaque, owned by the library */
  * nearest-even, or fp32), coherent host flags.  R <= 32. */
 ep_status ep_dense_alloc(int64_t max_tokens, int32_t hidden, int32_t num_ranks, int32_t self_rank,
                          int32_t num_buffers, ep_out_dtype block_dtype, ep_dense **out);
+/* Frees a dense staging, after the device and every SDMA copy in flight as ep_staging_free. */
 ep_status ep_dense_free(ep_dense *d);
 
 typedef struct {
@@ -336,7 +341,7 @@ ep_status ep_dense_get(ep_dense *d, int32_t buf, ep_dense_view *view);
 
 /* mode: 0 (download after the last rank's flag) or EP_MODE_PER_SENDER; timeout_us bounds
  * every flag wait (default 10 s); host_threads: threads of the partial host reduction
- * (0 keeps the current count). */
+ * (0 keeps the current count).  Waits for a partial host reduction in progress. */
 ep_status ep_dense_set_policy(ep_dense *d, uint32_t mode, int64_t timeout_us, int32_t host_threads);
 /* Synchronizes `stream`; returns and clears the status word (EP_ERR_TIMEOUT after an expired
  * wait). */

@@ -26,35 +26,35 @@ namespace {
 constexpr int kDenseMaxBuffers = 8;
 
 // Fixed set of host threads for the partial host reduction; run() splits [0, n) into
-// `workers + 1` parts (the calling thread takes one).
+// `workers + 1` parts (the calling thread takes one).  run() is called by the courier
+// thread; start() and stop() wait for a run() in progress before touching the workers.
 class HostPool {
 public:
     void start(int threads) {
-        stop();
+        std::lock_guard<std::mutex> busy(run_mu_);
+        join_all();
         stop_ = false;
+        // a new worker takes only work posted after it was made (no run() can post while
+        // run_mu_ is held)
+        const uint64_t gen = gen_;
         for (int i = 0; i < threads; ++i)
-            th_.emplace_back([this, i] { loop(i); });
+            th_.emplace_back([this, i, gen] { loop(i, gen); });
+        nworkers_.store(threads, std::memory_order_relaxed);
     }
     void stop() {
-        {
-            std::lock_guard<std::mutex> lk(mu_);
-            stop_ = true;
-        }
-        cv_.notify_all();
-        for (std::thread &t : th_)
-            if (t.joinable())
-                t.join();
-        th_.clear();
+        std::lock_guard<std::mutex> busy(run_mu_);
+        join_all();
     }
-    int workers() const { return (int)th_.size(); }
+    int workers() const { return nworkers_.load(std::memory_order_relaxed); }
     void run(int64_t n, const std::function<void(int64_t, int64_t)> &fn) {
-        const int parts = workers() + 1;
+        std::lock_guard<std::mutex> busy(run_mu_);
+        const int parts = (int)th_.size() + 1;
         {
             std::lock_guard<std::mutex> lk(mu_);
             fn_ = &fn;
             n_ = n;
             parts_ = parts;
-            pending_ = workers();
+            pending_ = parts - 1;
             ++gen_;
         }
         cv_.notify_all();
@@ -65,8 +65,19 @@ public:
     }
 
 private:
-    void loop(int i) {
-        uint64_t seen = 0;
+    void join_all() {
+        {
+            std::lock_guard<std::mutex> lk(mu_);
+            stop_ = true;
+        }
+        cv_.notify_all();
+        for (std::thread &t : th_)
+            if (t.joinable())
+                t.join();
+        th_.clear();
+        nworkers_.store(0, std::memory_order_relaxed);
+    }
+    void loop(int i, uint64_t seen) {
         std::unique_lock<std::mutex> lk(mu_);
         for (;;) {
             cv_.wait(lk, [&] { return stop_ || gen_ != seen; });
@@ -84,6 +95,8 @@ private:
     }
 
     std::vector<std::thread> th_;
+    std::atomic<int> nworkers_{0};
+    std::mutex run_mu_;  // held by run(), start() and stop()
     std::mutex mu_;
     std::condition_variable cv_, done_cv_;
     const std::function<void(int64_t, int64_t)> *fn_ = nullptr;

@@ -335,6 +335,14 @@ extern "C" ep_status ep_layout_status(const void *workspace, hipStream_t stream)
 namespace {
 
 void staging_release(ep_staging *s) {
+    // first the SDMA copies (each waits until its copies have landed), then their buffers
+    if (s->lane) {
+        s->lane->release();
+        delete s->lane;
+        s->lane = nullptr;
+    }
+    ep::exchange_destroy(s->xchg);
+    s->xchg = nullptr;
     for (int b = 0; b < kMaxBuffers; ++b) {
         if (s->dev_send[b]) (void)hipFree(s->dev_send[b]);
         if (s->dev_recv[b]) (void)hipFree(s->dev_recv[b]);
@@ -346,11 +354,6 @@ void staging_release(ep_staging *s) {
         for (hipEvent_t e : {s->ev_up_in[b], s->ev_up_done[b], s->ev_down_in[b], s->ev_down_done[b]})
             if (e) (void)hipEventDestroy(e);
     }
-    if (s->lane) {
-        s->lane->release();
-        delete s->lane;
-    }
-    ep::exchange_destroy(s->xchg);
     if (s->ev_sysrel) (void)hipEventDestroy(s->ev_sysrel);
     if (s->flags) (void)hipHostFree(s->flags);
     if (s->dev_epoch) (void)hipFree(s->dev_epoch);
@@ -465,8 +468,8 @@ extern "C" ep_status ep_staging_free(ep_staging *s) {
     int prev = -1;
     if (hipGetDevice(&prev) == hipSuccess && prev != s->device)
         (void)hipSetDevice(s->device);
-    for (hipStream_t st : {s->up, s->down})
-        if (st) (void)hipStreamSynchronize(st);
+    // every stream that used the staging has run (so each SDMA copy has been started)
+    (void)hipDeviceSynchronize();
     staging_release(s);
     if (prev >= 0)
         (void)hipSetDevice(prev);

@@ -391,6 +391,9 @@ extern "C" ep_status ep_pcie_probe(void *host, void *dev, size_t bytes, int32_t 
     hsa_signal_t sig[2] = {};
     for (hsa_signal_t &g : sig)
         if (hsa_signal_create(1, 0, nullptr, &g) != HSA_STATUS_SUCCESS) {
+            for (hsa_signal_t made : sig)
+                if (made.handle)
+                    hsa_signal_destroy(made);
             dma.release();
             return fail(EP_ERR_HIP, "ep_pcie_probe: hsa_signal_create failed");
         }

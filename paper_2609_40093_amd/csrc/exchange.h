@@ -69,6 +69,9 @@ public:
         dma_ = dma;
         th_ = std::thread([this] { run(); });
     }
+    // Ends the thread, then queues every copy it still held (ready or not, without the
+    // host work of all-senders jobs), so that each of them lands and raises its flag: a
+    // release can then wait for all flags before freeing what the copies touch.
     void stop() {
         {
             std::lock_guard<std::mutex> lk(mu_);
@@ -77,6 +80,15 @@ public:
         cv_.notify_all();
         if (th_.joinable())
             th_.join();
+        while (!incoming_.empty()) {
+            active_.push_back(std::move(incoming_.front()));
+            incoming_.pop_front();
+        }
+        for (InJob &j : active_)
+            for (const InCopy &c : j.copies)
+                if (dma_)
+                    submit(j, c);
+        active_.clear();
     }
     void post(InJob &&j) {
         {
@@ -179,11 +191,25 @@ public:
         return true;
     }
 
+    // Waits (bounded) for every copy of every slot to land, then frees the signals.  Call
+    // it after the streams that start the copies have run and before freeing the buffers
+    // the copies touch.
     void release() {
         courier.stop();
+        const auto t0 = std::chrono::steady_clock::now();
+        bool drained = true;
+        uint32_t spins = 0;
         for (XSlot &s : slots_)
-            for (hsa_signal_t g : s.sigs)
-                hsa_signal_destroy(g);
+            for (const auto &f : s.finish)
+                while (drained && (int32_t)(__atomic_load_n(f.first, __ATOMIC_ACQUIRE) - f.second) < 0)
+                    if (++spins % 1024 == 0) {
+                        std::this_thread::yield();
+                        drained = std::chrono::steady_clock::now() - t0 < std::chrono::microseconds(kReleaseDrainUs);
+                    }
+        if (drained)  // otherwise a copy may still wait on these signals: keep them alive
+            for (XSlot &s : slots_)
+                for (hsa_signal_t g : s.sigs)
+                    hsa_signal_destroy(g);
         slots_.clear();
         dma.release();
     }

@@ -130,6 +130,8 @@ bool SdmaLane::init(int device, int slots, std::string &err) {
 }
 
 void SdmaLane::release() {
+    if (!drain(kReleaseDrainUs))
+        slots_.clear();  // a copy may still wait on these signals: keep them alive
     for (Slot &s : slots_) {
         if (s.start.handle)
             hsa_signal_destroy(s.start);
@@ -226,6 +228,24 @@ bool SdmaLane::submit(const Round &r, void *host_dst, const void *dev_src, int64
     s.busy = true;
     s.last_flag = flags + (chunks - 1);
     s.epoch = epoch;
+    return true;
+}
+
+bool SdmaLane::drain(int64_t timeout_us) {
+    const auto t0 = std::chrono::steady_clock::now();
+    uint32_t spins = 0;
+    for (Slot &s : slots_) {
+        if (!s.busy)
+            continue;
+        while ((int32_t)(__atomic_load_n(s.last_flag, __ATOMIC_ACQUIRE) - s.epoch) < 0) {
+            if (++spins % 64 == 0) {
+                std::this_thread::yield();
+                if (std::chrono::steady_clock::now() - t0 > std::chrono::microseconds(timeout_us))
+                    return false;
+            }
+        }
+        s.busy = false;
+    }
     return true;
 }
 

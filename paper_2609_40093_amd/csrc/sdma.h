@@ -22,6 +22,9 @@
 
 namespace ep {
 
+// Longest a release waits for copies still in flight before it frees their signals.
+constexpr int64_t kReleaseDrainUs = 5ll * 1000 * 1000;
+
 class SdmaLane {
 public:
     // Finds the GPU agent of HIP device `device`, its nearest CPU agent and a free SDMA
@@ -40,6 +43,11 @@ public:
     // releases the start signal has been enqueued).
     bool submit(const Round &r, void *host_dst, const void *dev_src, int64_t bytes, int64_t chunk_bytes,
                 uint32_t *flags, const uint32_t *epoch_word, uint32_t epoch, std::string &err);
+    // Waits on the host (at most timeout_us in all) until every submitted round's last flag
+    // holds its epoch, i.e. until no copy of this lane is still in flight.  Call it after
+    // the streams that release the rounds' start signals have run, before freeing the
+    // buffers the copies touch.  Returns false if a round did not finish in time.
+    bool drain(int64_t timeout_us);
 
     const char *engine_name() const { return engine_name_.c_str(); }
 
@@ -64,8 +72,8 @@ private:
 // SDMA engines of one GPU for the exchange legs (device->host and host->device), driven
 // through ROCr.  Copies run on an engine named by its id bit, after dependency signals
 // reach 0, and decrement a completion signal when they land.  One engine carries the
-// device->host direction; the host->device copies of different senders go to different
-// engines, so a late sender never holds up a ready one (an engine runs its queue in order).
+// device->host direction and the first other engine the host->device direction (the
+// callers queue every inbound copy on that one engine).
 class DmaEngines {
 public:
     bool init(int device, std::string &err);

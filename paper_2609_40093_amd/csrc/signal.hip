@@ -201,6 +201,8 @@ hipError_t launch_gate(const char *name, const GateArgs &g, hipStream_t stream) 
 }
 
 hipError_t launch_stamp_release(uint32_t *epoch_word, uint32_t epoch, int64_t *value, hipStream_t stream) {
+    if (!epoch_word || !value)  // e.g. a signal whose value pointer could not be read
+        return hipErrorInvalidValue;
     (void)hipGetLastError();
     TraceSlot ts = trace_acquire();
     hipExtLaunchKernelGGL(stamp_release_kernel, dim3(1), dim3(64), 0, stream, ts.start, ts.stop, 0, epoch_word,
@@ -222,6 +224,8 @@ hipError_t launch_mirror(const int32_t *src, int32_t n, uint32_t *host, uint32_t
 }
 
 hipError_t launch_release_signal(int64_t *value, hipStream_t stream) {
+    if (!value)
+        return hipErrorInvalidValue;
     (void)hipGetLastError();
     TraceSlot ts = trace_acquire();
     hipExtLaunchKernelGGL(release_signal_kernel, dim3(1), dim3(64), 0, stream, ts.start, ts.stop, 0, value);

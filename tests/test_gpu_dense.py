@@ -226,3 +226,39 @@ def test_dense_per_sender_ready_ranks_land_first():
     peers.drain()
     peers.close()
     d.close()
+
+
+def test_set_policy_while_a_host_reduction_is_pending():
+    """ep_dense_set_policy called over and over while a Reduce-Scatter with partial host
+    reduction is pending (its ranks' blocks arrive 0.2 s late, then the host sums them):
+    each call waits for a reduction in progress instead of stopping its threads, and the
+    round's result is exact (dyadic blocks, fp32)."""
+    R, me, T, H = 4, 1, 1024, 512
+    say("dense set_policy during a pending host reduction")
+    d = ep.Dense(T, H, R, self_rank=me, num_buffers=1, block_dtype=torch.float32)
+    d.set_policy(per_sender=False, host_threads=4)
+    peers = ep.SimPeers(d)
+    peers.set_delays(inbound_us=[0] * R, return_us=[200_000] * R)
+    rng = np.random.default_rng(12)
+    blocks_h = (rng.integers(-64, 64, size=(R * T, H)) / 8).astype(np.float32)
+    rs_in = d.host_array("rs_in")
+    want = blocks_h[me * T:(me + 1) * T].copy()
+    for r in range(R):
+        if r != me:
+            blk = (rng.integers(-64, 64, size=(T, H)) / 8).astype(np.float32)
+            rs_in[r * T:(r + 1) * T] = blk
+            want += blk                                  # multiples of 1/8 below 64: exact
+    blocks = torch.from_numpy(blocks_h).to(DEV)
+    peers.post_dense(0, 7, "rs")
+    out = ep.reducescatter(d, blocks, num_tokens=T, out_dtype=torch.float32, reduce_on_host=True, epoch=7)
+    t_end = time.monotonic() + 0.5
+    n = 0
+    while time.monotonic() < t_end:
+        d.set_policy(per_sender=False, host_threads=2 + n % 4)
+        n += 1
+        time.sleep(0.001)
+    d.status()
+    assert np.array_equal(out.cpu().numpy(), want)
+    peers.drain()
+    peers.close()
+    d.close()

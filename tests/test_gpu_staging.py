@@ -169,3 +169,55 @@ def test_coarse_layer_pinned_with_peers():
     assert mx <= TOL_MAX_ABS and mean <= TOL_MEAN_ABS
     peers.close()
     st.close()
+
+
+def test_free_waits_for_the_host_leg_in_flight():
+    """ep_staging_free right after a dispatch whose SDMA upload (128 MiB, several ms over
+    PCIe) is still running: the free waits for the copies to land before it frees their
+    buffers, so pinned memory allocated right after keeps what is written into it, and a
+    new staging runs a correct round."""
+    T, H, E, k, R = 8192, 4096, 8, 2, 4
+    case = make_case("free_in_flight", T, H, E, k, R, "random", seed=6)
+    say("free a pinned staging while its host leg is in flight")
+    _, packed, _, _, _ = oracle_reference(case)
+    lay = layout_of(case)
+    x = dev_bits(case.x)
+    st = ep.Staging("pinned", case.slots, H, R, num_buffers=1, chunk_bytes=1 << 20)
+    ep.dispatch(x, lay.slot_pos, st, topk=k, buf=0, epoch=9)
+    t0 = time.monotonic()
+    st.close()
+    assert time.monotonic() - t0 < 6.0
+    fresh = torch.full((case.slots * H,), 0x5A5A, dtype=torch.int16, pin_memory=True)
+    time.sleep(0.02)
+    assert bool((fresh == 0x5A5A).all()), "pinned memory changed after the staging was freed"
+    del fresh
+    st2 = ep.Staging("pinned", case.slots, H, R, num_buffers=1, chunk_bytes=1 << 20)
+    ep.dispatch(x, lay.slot_pos, st2, topk=k, buf=0, epoch=1)
+    st2.status()
+    assert st2.host_array("send", 0)[:case.slots].tobytes() == packed.tobytes()
+    st2.close()
+
+
+def test_free_after_an_unanswered_exchange_round():
+    """A duplex dispatch whose senders never raise their flags (no peers, a 0.3 s wait):
+    the wait expires normally, and freeing the staging then queues the inbound copies the
+    library still holds and waits for them to land; a new staging runs a correct round."""
+    T, H, E, k, R, me = 512, 1024, 16, 2, 4, 1
+    case = make_case("unanswered", T, H, E, k, R, "random", seed=8)
+    say("free after an exchange round nobody answered")
+    _, packed, _, _, _ = oracle_reference(case)
+    lay = layout_of(case)
+    x = dev_bits(case.x)
+    st = ep.Staging("pinned", case.slots, H, R, num_buffers=1, chunk_bytes=1 << 20)
+    st.set_mode(ep.MODE_DUPLEX | ep.MODE_PER_SENDER, self_rank=me)
+    st.set_wait(timeout_us=300_000, sleep_units=1)
+    st.set_inbound(0, [0 if r == me else 64 for r in range(R)])
+    ep.dispatch(x, lay.slot_pos, st, topk=k, buf=0, epoch=3, rank_offsets=lay.rank_offsets)
+    t0 = time.monotonic()
+    st.close()
+    assert time.monotonic() - t0 < 8.0
+    st2 = ep.Staging("pinned", case.slots, H, R, num_buffers=1, chunk_bytes=1 << 20)
+    ep.dispatch(x, lay.slot_pos, st2, topk=k, buf=0, epoch=1)
+    st2.status()
+    assert st2.host_array("send", 0)[:case.slots].tobytes() == packed.tobytes()
+    st2.close()
