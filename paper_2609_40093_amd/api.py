@@ -71,6 +71,8 @@ def _ptr(t: Optional[torch.Tensor]):
 def _need(t: torch.Tensor, name: str, dtypes, ndim=None):
     if not t.is_cuda:
         raise ValueError(f"{name} must be a device tensor")
+    if t.device.index != torch.cuda.current_device():
+        raise ValueError(f"{name} lives on {t.device}, not on the current device")
     if t.dtype not in dtypes:
         raise ValueError(f"{name} has dtype {t.dtype}, expected one of {dtypes}")
     if not t.is_contiguous():
@@ -186,6 +188,9 @@ def combine_rows(y: torch.Tensor, slot_pos: torch.Tensor, topk_w: torch.Tensor, 
     """ep_combine_rows: out[t] = sum_j w[t, j] * y[slot_pos[t*k + j]] (fp32 accumulation)."""
     _need(topk_w, "topk_w", (torch.float32,), 2)
     _need(slot_pos, "slot_pos", (torch.int32,), 1)
+    _need(out, "out", _PAYLOAD_DTYPES + (torch.float32,), 2)
+    if y.numel():
+        _need(y, "y", _PAYLOAD_DTYPES, 2)
     N, k = topk_w.shape
     H = out.shape[1]
     code = EP_OUT_F32 if out.dtype == torch.float32 else EP_OUT_BF16
@@ -280,6 +285,8 @@ class Staging:
 
     def read_device(self, which: str, rows: int, buf: int = 0, stream=None) -> torch.Tensor:
         """Copy of the first `rows` rows of the device send, recv or in buffer (int16 bits)."""
+        if not 0 <= rows <= self.max_rows:
+            raise ValueError(f"rows must be in [0, {self.max_rows}]")
         ptr = self._dev_ptr(which, buf)
         out = torch.empty((rows, self.hidden), dtype=torch.int16, device="cuda")
         _check(_lib_handle().ep_memcpy(_ptr(out), ctypes.c_void_p(ptr), rows * self.row_bytes,
@@ -427,6 +434,8 @@ class Dense:
 
     def device_rows(self, which: str, rows: int, buf: int = 0, stream=None) -> torch.Tensor:
         """Copy of the first `rows` rows of dev_gathered ("gathered") or dev_rs_in ("rs_in")."""
+        if not 0 <= rows <= self.num_ranks * self.max_tokens:
+            raise ValueError(f"rows must be in [0, {self.num_ranks * self.max_tokens}]")
         v = self.views[buf]
         if which == "gathered":
             ptr, dt, rb = v.dev_gathered, torch.int16, v.row_bytes
@@ -453,10 +462,15 @@ def reducescatter(dense: Dense, blocks: torch.Tensor, *, num_tokens: int, out: O
                   epoch: int = 1, stream=None) -> torch.Tensor:
     """ep_reducescatter: blocks [R*T, H] (block dtype) -> out [T, H], the sum for this rank's shard."""
     T, H = num_tokens, dense.hidden
+    block_dtypes = (torch.float32,) if dense.block_dtype == torch.float32 else _PAYLOAD_DTYPES
+    _need(blocks, "blocks", block_dtypes, 2)
     if tuple(blocks.shape) != (dense.num_ranks * T, H):
         raise ValueError("blocks must be [R*T, H]")
     if out is None:
         out = torch.empty((T, H), dtype=out_dtype, device=blocks.device)
+    _need(out, "out", _PAYLOAD_DTYPES + (torch.float32,), 2)
+    if tuple(out.shape) != (T, H):
+        raise ValueError("out must be [T, H]")
     code = EP_OUT_F32 if out.dtype == torch.float32 else EP_OUT_BF16
     _check(_lib_handle().ep_reducescatter(dense.handle, buf, epoch & 0xFFFFFFFF, _ptr(blocks), T,
                                           1 if reduce_on_host else 0, _ptr(out), code, _stream_ptr(stream)),
@@ -491,6 +505,7 @@ def combine_graph(staging: Staging, slot_pos: torch.Tensor, topk_w: torch.Tensor
     """ep_combine_graph: reduce the returned rows of set round % 2 straight from pinned memory."""
     _need(topk_w, "topk_w", (torch.float32,), 2)
     _need(slot_pos, "slot_pos", (torch.int32,), 1)
+    _need(out, "out", _PAYLOAD_DTYPES + (torch.float32,), 2)
     T, k = topk_w.shape
     code = EP_OUT_F32 if out.dtype == torch.float32 else EP_OUT_BF16
     if tuple(out.shape) != (T, staging.hidden) or slot_pos.numel() != T * k:
@@ -578,6 +593,8 @@ def trace_read() -> dict:
 
 
 def copy_probe(dst: torch.Tensor, src: torch.Tensor, stream=None) -> None:
+    for t, name in ((dst, "dst"), (src, "src")):
+        _need(t, name, (t.dtype,))
     nbytes = src.numel() * src.element_size()
     if dst.numel() * dst.element_size() < nbytes:
         raise ValueError("dst smaller than src")
@@ -587,6 +604,9 @@ def copy_probe(dst: torch.Tensor, src: torch.Tensor, stream=None) -> None:
 def pcie_probe(host: torch.Tensor, dev: torch.Tensor, nbytes: int, dirs: int) -> float:
     """ep_pcie_probe: GB/s over PCIe on the exchange's SDMA engines (dirs: 1 = device->host,
     2 = host->device, 3 = both at once).  host (pinned) and dev hold 2*nbytes each."""
+    if host.is_cuda or not host.is_pinned() or not host.is_contiguous():
+        raise ValueError("host must be a contiguous pinned host tensor")
+    _need(dev, "dev", (dev.dtype,))
     if host.numel() * host.element_size() < 2 * nbytes or dev.numel() * dev.element_size() < 2 * nbytes:
         raise ValueError("host and dev must hold 2*nbytes")
     g = ctypes.c_double()

@@ -533,13 +533,20 @@ extern "C" ep_status ep_staging_set_mode(ep_staging *s, uint32_t mode, int32_t s
         return st;
     for (hipStream_t side : {s->up, s->down})  // no leg of the previous mode may still run
         if (side) EP_HIP(hipStreamSynchronize(side));
-    if ((mode & EP_MODE_DUPLEX) && !s->dev_in[0]) {
+    if (mode & EP_MODE_DUPLEX) {
+        // each missing buffer on its own, so a call that failed half-way leaves none NULL
+        // behind a later success
         for (int b = 0; b < s->num_buffers; ++b) {
-            hipError_t e = hipMalloc(&s->dev_in[b], (size_t)s->buffer_bytes);
-            if (e == hipSuccess)
-                e = hipHostMalloc(&s->host_in[b], (size_t)s->buffer_bytes, hipHostMallocDefault);
-            if (e == hipSuccess)
-                e = hipHostMalloc(&s->host_ret[b], (size_t)s->buffer_bytes, hipHostMallocDefault);
+            hipError_t e = hipSuccess;
+            void *p = nullptr;
+            if (!s->dev_in[b] && (e = hipMalloc(&p, (size_t)s->buffer_bytes)) == hipSuccess)
+                s->dev_in[b] = p;
+            if (e == hipSuccess && !s->host_in[b] &&
+                (e = hipHostMalloc(&p, (size_t)s->buffer_bytes, hipHostMallocDefault)) == hipSuccess)
+                s->host_in[b] = p;
+            if (e == hipSuccess && !s->host_ret[b] &&
+                (e = hipHostMalloc(&p, (size_t)s->buffer_bytes, hipHostMallocDefault)) == hipSuccess)
+                s->host_ret[b] = p;
             if (e != hipSuccess)
                 return hip_fail(e, "ep_staging_set_mode: duplex buffers");
         }
@@ -633,7 +640,6 @@ ep_status dispatch_default_legs(ep_staging *s, int32_t buf, uint32_t epoch, int6
     const int64_t chunks = (bytes + s->chunk_bytes - 1) / s->chunk_bytes;
     char *dsrc = static_cast<char *>(s->dev_send[buf]);
     char *hdst = static_cast<char *>(s->host_send[buf]);
-    ep::TraceSlot ts = ep::trace_acquire();
     if (s->lane) {
         // SDMA lane: make the packed rows visible at system scope (every XCD's L2), release
         // the lane's start signal from the stream, submit chunk + flag copies to the engine,
@@ -642,6 +648,7 @@ ep_status dispatch_default_legs(ep_staging *s, int32_t buf, uint32_t epoch, int6
         ep::SdmaLane::Round round;
         if (!s->lane->begin(round, s->timeout_us, err))
             return fail(EP_ERR_TIMEOUT, "ep_dispatch: %s", err.c_str());
+        ep::TraceSlot ts = ep::trace_acquire();
         if (ts.start)
             EP_HIP(hipEventRecord(ts.start, stream));
         EP_HIP(hipEventRecord(s->ev_sysrel, stream));
@@ -661,6 +668,7 @@ ep_status dispatch_default_legs(ep_staging *s, int32_t buf, uint32_t epoch, int6
 
     // hipMemcpyAsync path on the up stream: each chunk followed by a 4-byte copy of this
     // round's epoch (written by the pack kernel) into the chunk's flag.
+    ep::TraceSlot ts = ep::trace_acquire();
     EP_HIP(hipEventRecord(s->ev_up_in[buf], stream));
     EP_HIP(hipStreamWaitEvent(s->up, s->ev_up_in[buf], 0));
     if (ts.start)
@@ -896,15 +904,23 @@ extern "C" ep_status ep_trace_read(ep_trace_stat *stats, int32_t capacity, int32
     if (!count || capacity < 0 || (capacity > 0 && !stats))
         return fail(EP_ERR_INVALID_ARG, "ep_trace_read: bad arguments");
     std::lock_guard<std::mutex> lk(ep::g_trace_mu);
+    // every pending pair goes back to the pool exactly once, also after a failed query
+    hipError_t first = hipSuccess;
     for (auto &p : ep::g_pending) {
         float ms = 0.f;
-        EP_HIP(hipEventSynchronize(p.stop));
-        EP_HIP(hipEventElapsedTime(&ms, p.start, p.stop));
-        ep::g_stats[p.name].add(ms);
+        hipError_t e = hipEventSynchronize(p.stop);
+        if (e == hipSuccess)
+            e = hipEventElapsedTime(&ms, p.start, p.stop);
+        if (e == hipSuccess)
+            ep::g_stats[p.name].add(ms);
+        else if (first == hipSuccess)
+            first = e;
         ep::g_event_pool.push_back(p.start);
         ep::g_event_pool.push_back(p.stop);
     }
     ep::g_pending.clear();
+    if (first != hipSuccess)
+        return hip_fail(first, "ep_trace_read: timing events");
     int32_t n = 0;
     for (auto &kv : ep::g_stats) {
         if (n < capacity) {

@@ -135,3 +135,11 @@ def test_trace_without_launches(lib):
 def test_binding_fails_loudly_without_library(tmp_path):
     with pytest.raises(RuntimeError, match="not built"):
         _lib.load(str(tmp_path / "libep.so"))
+
+
+def test_binding_rejects_host_tensors_before_the_library():
+    """A host tensor where the library expects device memory is refused in Python."""
+    torch = pytest.importorskip("torch")
+    import paper_2609_40093_amd as ep
+    with pytest.raises(ValueError, match="must be a device tensor"):
+        ep.copy_probe(torch.empty(64, dtype=torch.uint8), torch.empty(64, dtype=torch.uint8))

@@ -78,3 +78,39 @@ def test_impossible_device_staging_is_oom():
     with pytest.raises(ep.EPError) as ei:
         ep.Staging("hbm", 1 << 36, 8192, 8, num_buffers=1)     # 1 PiB per buffer
     assert ei.value.status == 4
+
+
+def test_binding_rejects_host_and_misshaped_tensors():
+    """The binding refuses, before any library call, tensors the kernels or engines would
+    read as device (or pinned) memory but are not: host tensors, strided views, the wrong
+    block dtype, and row counts beyond a staging buffer."""
+    say("binding argument checks")
+    N, H, k, R = 16, 64, 2, 4
+    slot_pos = torch.zeros(N * k, dtype=torch.int32, device=DEV)
+    w = torch.full((N, k), 0.5, dtype=torch.float32, device=DEV)
+    y = torch.zeros((N * k, H), dtype=torch.int16, device=DEV)
+    out = torch.zeros((N, H), dtype=torch.float32, device=DEV)
+    with pytest.raises(ValueError, match="y must be a device tensor"):
+        ep.combine_rows(y.cpu(), slot_pos, w, out)
+    with pytest.raises(ValueError, match="out must be a device tensor"):
+        ep.combine_rows(y, slot_pos, w, out.cpu())
+    with pytest.raises(ValueError, match="out must be contiguous"):
+        ep.combine_rows(y, slot_pos, w, torch.zeros((H, N), dtype=torch.float32, device=DEV).t())
+    with pytest.raises(ValueError, match="dst must be a device tensor"):
+        ep.copy_probe(torch.empty(64, dtype=torch.uint8), torch.empty(64, dtype=torch.uint8, device=DEV))
+    with pytest.raises(ValueError, match="pinned"):
+        ep.pcie_probe(torch.empty(128, dtype=torch.uint8), torch.empty(128, dtype=torch.uint8, device=DEV), 64, 1)
+    st = ep.Staging("pinned", N * k, H, R, num_buffers=1)
+    with pytest.raises(ValueError, match="rows must be in"):
+        st.read_device("send", N * k + 1)
+    with pytest.raises(ValueError, match="out must be a device tensor"):
+        ep.combine_graph(st, slot_pos, w, out.cpu())
+    st.close()
+    d = ep.Dense(N, H, R, self_rank=0, num_buffers=1, block_dtype=torch.float32)
+    with pytest.raises(ValueError, match="blocks must be a device tensor"):
+        ep.reducescatter(d, torch.zeros((R * N, H), dtype=torch.float32), num_tokens=N)
+    with pytest.raises(ValueError, match="blocks has dtype"):
+        ep.reducescatter(d, torch.zeros((R * N, H), dtype=torch.int16, device=DEV), num_tokens=N)
+    with pytest.raises(ValueError, match="rows must be in"):
+        d.device_rows("gathered", R * N + 1)
+    d.close()
