@@ -398,8 +398,11 @@ typedef struct {
     double p10_ms, p50_ms, p90_ms;
 } ep_trace_stat;
 
-/* While enabled, every kernel launch and every host-leg DMA run of the library is
- * bracketed by HIP timing events on the stream it runs on. */
+/* While enabled, every kernel launch of the library is bracketed by HIP timing events on
+ * the stream it runs on (the launch's own start and stop events), and the host's partial
+ * reductions are timed on the host.  DMA copies are not bracketed: timing events around
+ * an SDMA copy misreport its span (it can exceed the span of the call that holds it); the
+ * flag-wait kernels after a leg (wait_d2h, ...) span the copies they wait for. */
 ep_status ep_trace_enable(int32_t on);
 /* Synchronizes the pending events and returns per-name totals (up to `capacity`). */
 ep_status ep_trace_read(ep_trace_stat *stats, int32_t capacity, int32_t *count);

@@ -648,9 +648,6 @@ ep_status dispatch_default_legs(ep_staging *s, int32_t buf, uint32_t epoch, int6
         ep::SdmaLane::Round round;
         if (!s->lane->begin(round, s->timeout_us, err))
             return fail(EP_ERR_TIMEOUT, "ep_dispatch: %s", err.c_str());
-        ep::TraceSlot ts = ep::trace_acquire();
-        if (ts.start)
-            EP_HIP(hipEventRecord(ts.start, stream));
         EP_HIP(hipEventRecord(s->ev_sysrel, stream));
         EP_HIP(ep::launch_release_signal(round.start_value, stream));
         if (!s->lane->submit(round, hdst, dsrc, bytes, s->chunk_bytes, s->send_flags(buf), s->epoch_word(buf),
@@ -659,30 +656,19 @@ ep_status dispatch_default_legs(ep_staging *s, int32_t buf, uint32_t epoch, int6
         const int64_t ticks = s->timeout_us * s->wall_clock_khz / 1000;
         EP_HIP(ep::launch_wait_flags("wait_d2h", s->send_flags(buf) + (chunks - 1), 1, epoch, ticks,
                                      s->sleep_units, s->status(), stream));
-        if (ts.stop) {
-            EP_HIP(hipEventRecord(ts.stop, stream));
-            ep::trace_submit("d2h_leg", ts);
-        }
         return EP_OK;
     }
 
     // hipMemcpyAsync path on the up stream: each chunk followed by a 4-byte copy of this
     // round's epoch (written by the pack kernel) into the chunk's flag.
-    ep::TraceSlot ts = ep::trace_acquire();
     EP_HIP(hipEventRecord(s->ev_up_in[buf], stream));
     EP_HIP(hipStreamWaitEvent(s->up, s->ev_up_in[buf], 0));
-    if (ts.start)
-        EP_HIP(hipEventRecord(ts.start, s->up));
     for (int64_t c = 0; c < chunks; ++c) {
         const int64_t off = c * s->chunk_bytes;
         const int64_t len = std::min<int64_t>(s->chunk_bytes, bytes - off);
         EP_HIP(hipMemcpyAsync(hdst + off, dsrc + off, (size_t)len, hipMemcpyDeviceToHost, s->up));
         EP_HIP(hipMemcpyAsync(s->send_flags(buf) + c, s->epoch_word(buf), sizeof(uint32_t),
                               hipMemcpyDeviceToHost, s->up));
-    }
-    if (ts.stop) {
-        EP_HIP(hipEventRecord(ts.stop, s->up));
-        ep::trace_submit("d2h_leg", ts);
     }
     EP_HIP(hipEventRecord(s->ev_up_done[buf], s->up));
     EP_HIP(hipStreamWaitEvent(stream, s->ev_up_done[buf], 0));
@@ -797,14 +783,9 @@ extern "C" ep_status ep_combine(ep_staging *s, int32_t buf, uint32_t epoch, cons
         const int64_t ticks = s->timeout_us * s->wall_clock_khz / 1000;
         EP_HIP(ep::launch_wait_flags("wait_recv", s->recv_flags(buf), s->num_ranks, epoch, ticks, s->sleep_units,
                                      s->status(), stream));
-        ep::TraceSlot ts = ep::trace_acquire();
-        if (ts.start)
-            EP_HIP(hipEventRecord(ts.start, stream));
+        // no timing events around this copy: on this runtime their span can exceed the
+        // call that holds them, and they delay the copy
         EP_HIP(hipMemcpyAsync(s->dev_recv[buf], s->host_recv[buf], (size_t)bytes, hipMemcpyHostToDevice, stream));
-        if (ts.stop) {
-            EP_HIP(hipEventRecord(ts.stop, stream));
-            ep::trace_submit("h2d_leg", ts);
-        }
     }
     EP_HIP(ep::launch_combine(s->dev_recv[buf], slot_pos, topk_w, num_tokens, hidden, topk, out_dev,
                               out_dtype == EP_OUT_F32, s->max_rows, stream));
