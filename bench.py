@@ -264,6 +264,7 @@ def main():
             "traffic": traffic,
             "algorithmic_bytes_per_launch": dk.get("algorithmic_bytes"),
             "avg_launch_us": dk.get("avg_us"),
+            "dispatch_and_combine": pair_roofline(kernels),
         },
         "kernels": kernels,
         "warm_cache": {
@@ -671,6 +672,18 @@ def pcie_peaks(dev) -> dict:
            "both": round(ep.pcie_probe(host, devb, nbytes, 3), 2)}
     del host, devb
     return res
+
+
+def pair_roofline(kernels: dict) -> dict:
+    """The dispatch kernel and combine of one layer together: their algorithmic bytes over
+    their summed average durations, against the HBM peak."""
+    disp = "layout_pack" if "layout_pack" in kernels else "pack"
+    pair = [kernels[disp], kernels["combine"]]
+    nbytes = sum(k["algorithmic_bytes"] for k in pair)
+    us = sum(k["avg_us"] for k in pair)
+    gbps = nbytes / (us * 1e-6) / 1e9
+    return {"kernels": [disp, "combine"], "algorithmic_bytes": nbytes, "avg_us": round(us, 3),
+            "achieved": round(gbps, 1), "frac": round(gbps / HBM_PEAK_GBPS, 4)}
 
 
 def same_bytes_copy(dev, nbytes: int, nsets: int, launches: int = 40) -> dict:
