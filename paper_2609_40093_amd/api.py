@@ -53,6 +53,7 @@ def _check(status: int, what: str):
 
 
 _raw_stream = getattr(torch._C, "_cuda_getCurrentRawStream", None)
+_get_device = getattr(torch._C, "_cuda_getDevice", None) or torch.cuda.current_device
 
 
 def _stream_ptr(stream=None) -> int:
@@ -71,7 +72,7 @@ def _ptr(t: Optional[torch.Tensor]):
 def _need(t: torch.Tensor, name: str, dtypes, ndim=None):
     if not t.is_cuda:
         raise ValueError(f"{name} must be a device tensor")
-    if t.device.index != torch.cuda.current_device():
+    if t.device.index != _get_device():
         raise ValueError(f"{name} lives on {t.device}, not on the current device")
     if t.dtype not in dtypes:
         raise ValueError(f"{name} has dtype {t.dtype}, expected one of {dtypes}")
