@@ -234,12 +234,12 @@ ep_status ep_dispatch(const void *x_dev, int64_t num_tokens, int32_t hidden, int
  * ep_dispatch_layout, the rest as in ep_dispatch; every argument is checked before
  * anything is enqueued).  Sec. 4.3 (tokens grouped by the experts that consume them)
  * and Sec. 2.2 (rows packed into contiguous segments for the DMA engine).
- * For few experts one kernel does both steps, each workgroup counting every routing
- * entry itself (no exchange between workgroups, no second kernel): with HBM staging or
- * the default pinned mode, E <= 64, topk in {1, 2, 4}, T*topk <= 65536, hidden a
- * multiple of 512 with hidden/512 in {1, 2, 4, 8, 16}, and topk_idx 16-byte aligned.
- * Otherwise the two steps run as their own kernels.  The fused kernel writes only the
- * status word of the workspace. */
+ * For few routing entries one kernel does both steps, each workgroup counting every
+ * routing entry itself (no exchange between workgroups, no second kernel): with HBM
+ * staging or the default pinned mode, E <= 256, topk in {1, 2, 4, 8}, T*topk <= 65536
+ * when E <= 64 and topk <= 4, otherwise T*topk <= 16384 (8192 when hidden > 4096),
+ * hidden = 512 * g with g in {1, 2, 4, 8, 14, 16}, and topk_idx 16-byte aligned.  Otherwise the two steps run
+ * as their own kernels.  The fused kernel writes only the status word of the workspace. */
 ep_status ep_dispatch_fused(const int32_t *topk_idx, int64_t num_tokens, int32_t topk,
                             int32_t num_experts, int32_t num_ranks, int32_t *expert_counts,
                             int32_t *expert_offsets, int32_t *rank_counts, int32_t *rank_offsets,

@@ -18,8 +18,9 @@
 //      work only: a ballot per id would queue every wave of the compute unit on its one
 //      scalar unit), both over all entries and over the entries before its own range;
 //      routing errors (an id outside [0,E), an expert twice in one token row) are found
-//      in the same pass;
-//   C. the totals' exclusive scan (DPP) gives the expert offsets; workgroup 0 stores the
+//      in the same pass (a top-8 row spans the 4-id groups of two neighbouring lanes);
+//   C. the totals' exclusive scan (DPP; a lane per expert, or four consecutive experts
+//      per lane above 64 experts) gives the expert offsets; workgroup 0 stores the
 //      counts, offsets, rank counts/offsets and the status word;
 //   D. wave 0 ranks the workgroup's own entries in flat order (ballot match-any and a
 //      masked popcount, as the layout kernel does: stable), stores slot_pos / row_src and
@@ -29,10 +30,12 @@
 // The outputs equal those of the layout kernel followed by the pack kernel, bit for bit.
 // Workgroups never wait on each other, so nothing needs them resident together.
 //
-// Limits (the host falls back to the two kernels outside them): E <= 64 (a lane per
-// expert in step C), k in {1, 2, 4} (a token row lies inside one 4-id load), T*k <= 65536
-// (every workgroup reads every id), rows of 1, 2, 4, 8 or 16 groups (H a multiple of 512
-// up to 8192), a 16-byte aligned routing array.
+// Limits (the host falls back to the two kernels outside them): E <= 256 (four experts
+// per lane in step C), k in {1, 2, 4, 8} (a token row inside one 4-id load, or two for
+// top-8), T*k <= 65536 for E <= 64 and k <= 4, else T*k <= 16384 for rows up to 8 KiB and
+// 8192 for longer ones (every workgroup reads and counts every id before its stores:
+// beyond that the layout kernel's exchange of totals costs less), rows of 1, 2, 4, 8, 14
+// or 16 groups (H = 512 * groups), a 16-byte aligned routing array.
 #include "ep_internal.h"
 #include "wave.h"
 
@@ -40,8 +43,13 @@ namespace ep {
 namespace {
 
 constexpr int kFMaxThreads = 16 * kWave;    // largest workgroup (16 waves)
-constexpr int kFMaxE = 64;                   // experts: one lane each in step C
+constexpr int kFNarrowE = 64;                // experts with one lane each in step C
+constexpr int kFMaxE = 4 * kWave;            // experts with four per lane (wide instances)
 constexpr int64_t kFMaxSlots = 65536;        // T*k: every workgroup reads every id
+// T*k for E > 64 or k = 8 (measured on MI355X: at 16384 ids the one kernel still wins
+// with 4 KiB rows, 20-24 against 23-29 us, and loses with 14 KiB rows, 56 against 55 us)
+constexpr int64_t kFMaxSlotsWide = 16384;    // rows of at most 8 KiB
+constexpr int64_t kFMaxSlotsWideLong = 8192; // longer rows
 constexpr int kFMaxOwn = 256;                // entries one workgroup owns (LDS rows)
 constexpr int kFOwnRounds = kFMaxOwn / kWave;
 constexpr int kFBatch = 4;                   // 16-byte id loads in flight per lane
@@ -75,26 +83,40 @@ __device__ __forceinline__ void load_ids(const i32x4 *q, int64_t full, int64_t q
 
 constexpr int kFCopies = 16;  // copies of the LDS counters (lane % 16 picks one)
 
-// Counts one id into the LDS counters (all entries, and those before this workgroup's).
+// Counts one id into the LDS counters (all entries, and those before this workgroup's);
+// ME counters per copy.
+template <int ME>
 __device__ __forceinline__ void count_id(int id, bool in, bool before, int E, int *s_all, int *s_pre, int copy,
                                          bool &bad_id) {
     const bool valid = in && (unsigned)id < (unsigned)E;
     bad_id |= in && !valid;
     if (valid) {
-        atomicAdd(&s_all[copy * kFMaxE + id], 1);
+        atomicAdd(&s_all[copy * ME + id], 1);
         if (before)
-            atomicAdd(&s_pre[copy * kFMaxE + id], 1);
+            atomicAdd(&s_pre[copy * ME + id], 1);
     }
+}
+
+// Does any id of `a` (in [0,E)) equal one of `b`?  (The two halves of a top-8 row.)
+__device__ __forceinline__ bool halves_repeat(i32x4 a, i32x4 b, int E) {
+    bool r = false;
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+        r |= (unsigned)a[i] < (unsigned)E && (a[i] == b[0] || a[i] == b[1] || a[i] == b[2] || a[i] == b[3]);
+    return r;
 }
 
 // MULTI: more ids than one batch of the workgroup's loads (the count loops).  Instances
 // without the loop have only straight-line loads, so the compiler's waits stay exact and
-// no wave waits for its token row before the count's barrier.
-template <int U, int K, bool MULTI>
+// no wave waits for its token row before the count's barrier.  WIDE: more than 64
+// experts (four per lane in step C).
+template <int U, int K, bool MULTI, bool WIDE>
 __global__ __launch_bounds__(kFMaxThreads) void layout_pack_kernel(FusedArgs a, int32_t tpw) {
-    __shared__ int s_all[kFCopies * kFMaxE];
-    __shared__ int s_pre[kFCopies * kFMaxE];
-    __shared__ int s_base[kFMaxE];
+    constexpr int ME = WIDE ? kFMaxE : kFNarrowE;  // counters per copy
+    __shared__ int s_all[kFCopies * ME];
+    __shared__ int s_pre[kFCopies * ME];
+    __shared__ int s_base[ME];
+    __shared__ int s_off[WIDE ? ME + 1 : 1];
     __shared__ int s_pos[kFMaxOwn];
     __shared__ int s_err;
     const int tid = threadIdx.x, lane = tid & (kWave - 1), w = tid / kWave;
@@ -133,7 +155,7 @@ __global__ __launch_bounds__(kFMaxThreads) void layout_pack_kernel(FusedArgs a, 
         for (int u = 0; u < U; ++u)
             d[u] = __builtin_nontemporal_load(src + u * kWave);
     }
-    for (int i = tid; i < kFCopies * kFMaxE; i += threads) {
+    for (int i = tid; i < kFCopies * ME; i += threads) {
         s_all[i] = 0;
         s_pre[i] = 0;
     }
@@ -153,10 +175,20 @@ __global__ __launch_bounds__(kFMaxThreads) void layout_pack_kernel(FusedArgs a, 
             const bool in = qi < full;
             // entries before this workgroup's: whole 4-id groups (ent0 is a multiple of 4)
             const bool before = qi * 4 < ent0;
-            dup |= in && row_repeats<K>(v[b], a.E);
+            if constexpr (K == 8) {
+                // a row is the groups of lanes 2m and 2m+1 (qi and lane have the same
+                // parity; full = 2T is even, so both halves are in or out together)
+                i32x4 o;
+#pragma unroll
+                for (int c = 0; c < 4; ++c)
+                    o[c] = __shfl_xor(v[b][c], 1);
+                dup |= in && (row_repeats<4>(v[b], a.E) || ((lane & 1) == 0 && halves_repeat(v[b], o, a.E)));
+            } else {
+                dup |= in && row_repeats<K>(v[b], a.E);
+            }
 #pragma unroll
             for (int c = 0; c < 4; ++c)
-                count_id(v[b][c], in, before, a.E, s_all, s_pre, lane % kFCopies, bad_id);
+                count_id<ME>(v[b][c], in, before, a.E, s_all, s_pre, lane % kFCopies, bad_id);
         }
     };
     // the first batch outside the loop: its wait leaves the token row's loads in flight
@@ -173,21 +205,73 @@ __global__ __launch_bounds__(kFMaxThreads) void layout_pack_kernel(FusedArgs a, 
         const int id = in ? tail_id : -1;
         if (K == 2 && lane == 0)
             dup |= (unsigned)id < (unsigned)a.E && id == tail_next;  // the tail is one row
-        count_id(id, in, ti < ent0, a.E, s_all, s_pre, lane % kFCopies, bad_id);
+        count_id<ME>(id, in, ti < ent0, a.E, s_all, s_pre, lane % kFCopies, bad_id);
     }
     const uint32_t wave_err = (__ballot(bad_id) ? kRoutingIdOutOfRange : 0u) | (__ballot(dup) ? kRoutingDuplicate : 0u);
     if (lane == 0 && wave_err)
         atomicOr(&s_err, (int)wave_err);
     __syncthreads();
 
-    if (w == 0) {
+    if (w == 0 && WIDE) {
+        // C (wide). Lane l holds experts 4l..4l+3: their totals, one scan of the lanes'
+        // sums, the offsets of each expert kept in LDS (read back by other lanes of this
+        // wave only, in program order)
+        int tot[4], pre[4], sum = 0;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            const int e = 4 * lane + q;
+            tot[q] = pre[q] = 0;
+            if (e < a.E) {
+#pragma unroll
+                for (int c = 0; c < kFCopies; ++c) {
+                    tot[q] += s_all[c * ME + e];
+                    pre[q] += s_pre[c * ME + e];
+                }
+            }
+            sum += tot[q];
+        }
+        const int incl = wave_inclusive_scan(sum);
+        const int total = __shfl(incl, kWave - 1);
+        int run = incl - sum;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            const int e = 4 * lane + q;
+            if (e < a.E) {
+                s_off[e] = run;
+                s_base[e] = run + pre[q];
+            }
+            run += tot[q];
+        }
+        if (lane == 0)
+            s_off[a.E] = total;
+        __builtin_amdgcn_wave_barrier();  // the reads below follow every lane's writes
+        if (blockIdx.x == 0) {
+#pragma unroll
+            for (int q = 0; q < 4; ++q)
+                if (4 * lane + q < a.E)
+                    a.expert_counts[4 * lane + q] = tot[q];
+            const int L = a.E / a.R;
+            for (int e = lane; e <= a.E; e += kWave)
+                a.expert_offsets[e] = s_off[e];
+            for (int r = lane; r <= a.R; r += kWave) {
+                a.rank_offsets[r] = s_off[r * L];
+                if (r < a.R)
+                    a.rank_counts[r] = s_off[(r + 1) * L] - s_off[r * L];
+            }
+            if (lane == 0) {
+                *a.status = (uint32_t)s_err;
+                if (a.epoch_word)
+                    *a.epoch_word = a.epoch;
+            }
+        }
+    } else if (w == 0) {
         // C. totals, offsets; workgroup 0 stores the layout's counts and the status
         int tot = 0, pre = 0;
         if (lane < a.E) {
 #pragma unroll
             for (int c = 0; c < kFCopies; ++c) {
-                tot += s_all[c * kFMaxE + lane];
-                pre += s_pre[c * kFMaxE + lane];
+                tot += s_all[c * ME + lane];
+                pre += s_pre[c * ME + lane];
             }
         }
         const int incl = wave_inclusive_scan(tot);
@@ -222,7 +306,10 @@ __global__ __launch_bounds__(kFMaxThreads) void layout_pack_kernel(FusedArgs a, 
                     *a.epoch_word = a.epoch;
             }
         }
-        // D. rank the own entries in flat order
+    }
+    if (w == 0) {
+        // D. rank the own entries in flat order (s_base as step C left it, written by this
+        //    wave)
 #pragma unroll
         for (int r = 0; r < kFOwnRounds; ++r) {
             const int64_t i = ent0 + r * kWave + lane;
@@ -276,37 +363,59 @@ __global__ __launch_bounds__(kFMaxThreads) void layout_pack_kernel(FusedArgs a, 
     }
 }
 
-template <int U, bool MULTI>
-void launch_km(const FusedArgs &a, int32_t tpw, unsigned blocks, int threads, hipStream_t stream, TraceSlot ts) {
-    if (a.k == 1)
-        hipExtLaunchKernelGGL((layout_pack_kernel<U, 1, MULTI>), dim3(blocks), dim3(threads), 0, stream, ts.start,
-                              ts.stop, 0, a, tpw);
-    else if (a.k == 2)
-        hipExtLaunchKernelGGL((layout_pack_kernel<U, 2, MULTI>), dim3(blocks), dim3(threads), 0, stream, ts.start,
-                              ts.stop, 0, a, tpw);
-    else
-        hipExtLaunchKernelGGL((layout_pack_kernel<U, 4, MULTI>), dim3(blocks), dim3(threads), 0, stream, ts.start,
-                              ts.stop, 0, a, tpw);
+template <int U, int K, bool MULTI, bool WIDE>
+void launch_one(const FusedArgs &a, int32_t tpw, unsigned blocks, int threads, hipStream_t stream, TraceSlot ts) {
+    hipExtLaunchKernelGGL((layout_pack_kernel<U, K, MULTI, WIDE>), dim3(blocks), dim3(threads), 0, stream, ts.start,
+                          ts.stop, 0, a, tpw);
 }
 
+// Picks the instance: the count loop only where one batch of loads does not cover every
+// id (never within the wide limits: at most 16384 ids, 1024 threads x 16), four experts
+// per lane above 64 experts.
 template <int U>
-void launch_k(const FusedArgs &a, int32_t tpw, unsigned blocks, int threads, hipStream_t stream, TraceSlot ts) {
-    // one batch is kFBatch 4-id groups per thread
-    if (a.T * a.k > (int64_t)threads * kFBatch * 4)
-        launch_km<U, true>(a, tpw, blocks, threads, stream, ts);
-    else
-        launch_km<U, false>(a, tpw, blocks, threads, stream, ts);
+hipError_t launch_k(const FusedArgs &a, int32_t tpw, unsigned blocks, int threads, hipStream_t stream,
+                    TraceSlot ts) {
+    const bool multi = a.T * a.k > (int64_t)threads * kFBatch * 4;  // one batch: kFBatch 4-id groups per thread
+    const bool wide = a.E > kFNarrowE;
+    if ((wide || a.k == 8) && multi)
+        return hipErrorInvalidValue;  // excluded by the limits
+    switch (a.k) {
+    case 1:
+        wide ? launch_one<U, 1, false, true>(a, tpw, blocks, threads, stream, ts)
+             : (multi ? launch_one<U, 1, true, false>(a, tpw, blocks, threads, stream, ts)
+                      : launch_one<U, 1, false, false>(a, tpw, blocks, threads, stream, ts));
+        break;
+    case 2:
+        wide ? launch_one<U, 2, false, true>(a, tpw, blocks, threads, stream, ts)
+             : (multi ? launch_one<U, 2, true, false>(a, tpw, blocks, threads, stream, ts)
+                      : launch_one<U, 2, false, false>(a, tpw, blocks, threads, stream, ts));
+        break;
+    case 4:
+        wide ? launch_one<U, 4, false, true>(a, tpw, blocks, threads, stream, ts)
+             : (multi ? launch_one<U, 4, true, false>(a, tpw, blocks, threads, stream, ts)
+                      : launch_one<U, 4, false, false>(a, tpw, blocks, threads, stream, ts));
+        break;
+    default:
+        wide ? launch_one<U, 8, false, true>(a, tpw, blocks, threads, stream, ts)
+             : launch_one<U, 8, false, false>(a, tpw, blocks, threads, stream, ts);
+        break;
+    }
+    return hipSuccess;
 }
 
 }  // namespace
 
 bool fused_layout_pack_fits(int64_t T, int32_t k, int32_t E, int32_t H, const void *topk_idx) {
-    if (T < 1 || E < 1 || E > kFMaxE || !(k == 1 || k == 2 || k == 4) || T * k > kFMaxSlots)
+    if (T < 1 || E < 1 || E > kFMaxE || k > E || !(k == 1 || k == 2 || k == 4 || k == 8))
+        return false;
+    const int64_t wide_limit = H <= 4096 ? kFMaxSlotsWide : kFMaxSlotsWideLong;
+    if (T * k > (E > kFNarrowE || k == 8 ? wide_limit : kFMaxSlots))
         return false;
     if (H % 512 != 0)
         return false;
     const int G = H / 512;
-    return (G == 1 || G == 2 || G == 4 || G == 8 || G == 16) && reinterpret_cast<uintptr_t>(topk_idx) % 16 == 0;
+    return (G == 1 || G == 2 || G == 4 || G == 8 || G == 14 || G == 16) &&
+           reinterpret_cast<uintptr_t>(topk_idx) % 16 == 0;
 }
 
 hipError_t launch_layout_pack(const FusedArgs &a, hipStream_t stream) {
@@ -325,14 +434,20 @@ hipError_t launch_layout_pack(const FusedArgs &a, hipStream_t stream) {
         return hipErrorInvalidValue;  // excluded by the limits above
     (void)hipGetLastError();  // drop an error left by an earlier, already reported call
     TraceSlot ts = trace_acquire();
+    const unsigned nb = (unsigned)blocks;
+    const int threads = waves * kWave;
+    hipError_t err;
     switch (a.H / 512) {
-    case 1: launch_k<1>(a, tpw, (unsigned)blocks, waves * kWave, stream, ts); break;
-    case 2: launch_k<2>(a, tpw, (unsigned)blocks, waves * kWave, stream, ts); break;
-    case 4: launch_k<4>(a, tpw, (unsigned)blocks, waves * kWave, stream, ts); break;
-    case 8: launch_k<8>(a, tpw, (unsigned)blocks, waves * kWave, stream, ts); break;
-    default: launch_k<16>(a, tpw, (unsigned)blocks, waves * kWave, stream, ts); break;
+    case 1: err = launch_k<1>(a, tpw, nb, threads, stream, ts); break;
+    case 2: err = launch_k<2>(a, tpw, nb, threads, stream, ts); break;
+    case 4: err = launch_k<4>(a, tpw, nb, threads, stream, ts); break;
+    case 8: err = launch_k<8>(a, tpw, nb, threads, stream, ts); break;
+    case 14: err = launch_k<14>(a, tpw, nb, threads, stream, ts); break;
+    default: err = launch_k<16>(a, tpw, nb, threads, stream, ts); break;
     }
-    hipError_t err = hipGetLastError();
+    if (err != hipSuccess)
+        return err;  // nothing was launched (unreachable within the limits)
+    err = hipGetLastError();
     if (err == hipSuccess)
         trace_submit("layout_pack", ts);
     return err;

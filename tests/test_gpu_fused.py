@@ -1,4 +1,4 @@
-"""ep_dispatch_fused: layout and pack in one call (one kernel for few experts).
+"""ep_dispatch_fused: layout and pack in one call (one kernel up to 256 experts and top-8).
 
 Its outputs must equal the oracle's layout and pack, and the two-call path's
 (ep_dispatch_layout then ep_dispatch) bit for bit: counts, offsets, rank counts and
@@ -72,6 +72,24 @@ FUSED_CASES = [
     ("entries_16386", 8193, 512, 16, 2, 4, "skewed"),
     ("e64_r64_one_expert_per_rank", 5000, 2048, 64, 2, 64, "skewed"),
     ("e64_k4", 7000, 512, 64, 4, 8, "random"),
+    # above 64 experts (four per lane in the scan) and top-8 (a row spans two 4-id
+    # groups), up to 16384 entries (8192 for rows over 8 KiB); rows of 14 groups (H = 7168)
+    ("decode_shape_k8_e256_rows14", 256, 7168, 256, 8, 8, "skewed"),
+    ("k8_e16", 300, 512, 16, 8, 4, "random"),
+    ("k8_e64_r64", 500, 1024, 64, 8, 64, "skewed"),
+    ("k8_e128_8192", 1024, 512, 128, 8, 8, "random"),           # 8-wave workgroups
+    ("k8_e128_limit_16384", 2048, 2048, 128, 8, 8, "random"),   # 16-wave workgroups
+    ("e256_k2_limit_16384", 8192, 512, 256, 2, 8, "skewed"),    # 2 tokens per wave
+    ("k8_rows14_limit_8192", 1024, 7168, 256, 8, 8, "random"),
+    ("k8_ragged_tokens", 333, 512, 32, 8, 4, "random"),
+    ("e65", 500, 512, 65, 2, 5, "random"),
+    ("e128_k4", 2000, 1024, 128, 4, 8, "skewed"),
+    ("e256_k1_limit_8192", 8192, 512, 256, 1, 8, "random"),     # 2 tokens per wave
+    ("e256_r256_one_expert_per_rank", 300, 512, 256, 2, 256, "random"),
+    ("e255_odd_wide", 200, 512, 255, 4, 5, "random"),
+    ("e200_empty_experts", 999, 512, 200, 4, 4, "firstk"),
+    ("rows14_k2", 200, 7168, 16, 2, 4, "random"),
+    ("rows14_e128_k1", 600, 7168, 128, 1, 4, "random"),
 ]
 
 
@@ -138,11 +156,12 @@ def test_fused_repeated_calls_reuse_buffers():
 
 FALLBACK_CASES = [
     # outside the fused kernel's limits: the two kernels run
-    ("e65_too_many_experts", 500, 512, 65, 2, 5),
-    ("e128", 500, 512, 128, 2, 4),
-    ("k8", 300, 512, 16, 8, 4),
+    ("e257_too_many_experts", 300, 512, 257, 2, 1),
+    ("k8_over_16384_entries", 2049, 512, 16, 8, 4),
+    ("e65_over_16384_entries", 8193, 512, 65, 2, 5),
+    ("k8_rows14_over_8192_entries", 1025, 7168, 16, 8, 4),
     ("k3", 300, 512, 16, 3, 4),
-    ("rows14", 200, 7168, 16, 2, 4),
+    ("rows12", 200, 6144, 16, 2, 4),
     ("h520_not_whole_groups", 100, 520, 8, 2, 2),
     ("slots_over_limit", 40000, 512, 8, 2, 4),
 ]
@@ -181,18 +200,18 @@ def test_misaligned_routing_falls_back():
     st.close()
 
 
-@pytest.mark.parametrize("k", [1, 2, 4])
-def test_fused_routing_errors_match_two_calls(k):
+@pytest.mark.parametrize("k,E", [(1, 16), (2, 16), (4, 16), (8, 16), (2, 128), (8, 128)])
+def test_fused_routing_errors_match_two_calls(k, E):
     """Ids outside [0,E) get no row and are reported; a repeated expert is reported and
     still ranked; the fused kernel and the layout kernel agree on every output."""
-    T, H, E, R = 700, 512, 16, 4
-    case = make_case(f"errors_k{k}", T, H, E, k, R, "random", seed=9)
+    T, H, R = 700, 512, 4   # at most 5600 entries: every case fits the fused kernel
+    case = make_case(f"errors_k{k}_e{E}", T, H, E, k, R, "random", seed=9)
     idx = case.topk_idx.copy()
     idx[5, 0] = E
     idx[321, k - 1] = -7
     if k > 1:
         idx[600, 1] = idx[600, 0]
-    say(f"fused routing errors k={k}")
+    say(f"fused routing errors k={k} E={E}")
     idx_d, x_d = to_dev(idx), to_dev(case.x.view(np.int16))
     st = ep.Staging("hbm", T * k, H, R, num_buffers=2)
     lay, kernels = run_fused(idx_d, x_d, E, R, st, buf=0)
@@ -219,6 +238,30 @@ def test_fused_routing_errors_match_two_calls(k):
     # the next good routing on the same workspace clears the status
     lay = ep.dispatch_fused(x_d, to_dev(case.topk_idx), E, R, st, out=lay)
     ep.layout_status(lay)
+    st.close()
+
+
+@pytest.mark.parametrize("first,second", [(1, 2), (1, 6), (3, 4), (7, 0)],
+                         ids=["same_half", "across_halves", "halves_edge", "last_and_first"])
+def test_fused_k8_repeated_expert(first, second):
+    """A top-8 row naming one expert twice, within one of its 4-id halves or across them
+    (the halves sit in neighbouring lanes): reported, and equal to the two-call path."""
+    T, H, E, R = 300, 512, 32, 4
+    case = make_case("k8_repeat", T, H, E, 8, R, "random", seed=12)
+    idx = case.topk_idx.copy()
+    idx[123, second] = idx[123, first]
+    say(f"fused top-8 repeated expert at slots {first} and {second}")
+    idx_d, x_d = to_dev(idx), to_dev(case.x.view(np.int16))
+    st = ep.Staging("hbm", T * 8, H, R, num_buffers=2)
+    lay, kernels = run_fused(idx_d, x_d, E, R, st, buf=0)
+    assert "layout_pack" in kernels
+    with pytest.raises(ep.EPError, match="repeated"):
+        ep.layout_status(lay)
+    lay2 = run_two_calls(idx_d, x_d, E, R, st, 8, buf=1)
+    with pytest.raises(ep.EPError, match="repeated"):
+        ep.layout_status(lay2)
+    for key in LAYOUT_KEYS:
+        assert np.array_equal(getattr(lay2, key).cpu().numpy(), getattr(lay, key).cpu().numpy()), key
     st.close()
 
 
