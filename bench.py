@@ -60,13 +60,20 @@ def algorithmic_bytes(cfg) -> dict:
     return out
 
 
-KERNEL_SOURCES = {"pack": "pack.hip", "combine": "combine.hip", "layout": "layout.hip", "layout_pack": "fused.hip"}
+# the files each kernel is compiled from: its source and the package headers it includes
+KERNEL_SOURCES = {"pack": ("pack.hip", "ep_internal.h"), "combine": ("combine.hip", "ep_internal.h"),
+                  "layout": ("layout.hip", "wave.h", "ep_internal.h"),
+                  "layout_pack": ("fused.hip", "wave.h", "ep_internal.h")}
 TIMED_KERNELS = ("layout_pack", "pack", "combine")
 
 
-def source_hash(name: str) -> str:
-    path = os.path.join(ROOT, "paper_2609_40093_amd", "csrc", name)
-    return hashlib.sha256(open(path, "rb").read()).hexdigest()[:16]
+def source_hash(kernel: str) -> str:
+    """Hash of the files the kernel is compiled from (a change to any of them makes the
+    committed counter figures stale)."""
+    h = hashlib.sha256()
+    for name in KERNEL_SOURCES[kernel]:
+        h.update(open(os.path.join(ROOT, "paper_2609_40093_amd", "csrc", name), "rb").read())
+    return h.hexdigest()[:16]
 
 
 def committed_traffic(workload: str, kernel: str):
@@ -76,7 +83,7 @@ def committed_traffic(workload: str, kernel: str):
     if not os.path.exists(path):
         return None
     d = json.load(open(path))
-    if d.get("source_sha256") != source_hash(KERNEL_SOURCES.get(kernel, f"{kernel}.hip")):
+    if kernel not in KERNEL_SOURCES or d.get("source_sha256") != source_hash(kernel):
         return None
     return d.get("traffic_bytes_per_launch")
 

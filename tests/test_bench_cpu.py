@@ -1,0 +1,86 @@
+"""bench.py's host logic on the CPU: the algorithmic bytes behind every roofline figure,
+the pair roofline, the committed counter figures' freshness check, and the one-GPU rule."""
+import json
+import os
+import subprocess
+import sys
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+sys.path.insert(0, ROOT)
+
+import bench  # noqa: E402
+from paper_2609_40093_amd import synth  # noqa: E402
+
+# Bytes each kernel must move per layer, in MB (1e6), for the five workloads: the figures
+# of the hot-path scope table, worked out from the definitions (pack reads each token row
+# once and writes its k copies plus the slot positions; combine reads the k rows, gates
+# and slot positions and writes one row per token).
+EXPECTED_MB = {
+    "tiny": (0.787, 0.788),
+    "coarse": (100.7, 100.7),
+    "fine": (302.3, 302.5),
+    "decode": (33.0, 33.0),
+    "prefill": (4229.0, 4230.0),
+}
+
+
+@pytest.mark.parametrize("name", sorted(EXPECTED_MB))
+def test_algorithmic_bytes_match_the_scope_table(name):
+    cfg = synth.config(name)
+    b = bench.algorithmic_bytes(cfg)
+    pack_mb, combine_mb = EXPECTED_MB[name]
+    digits = 3 if pack_mb < 1 else (1 if pack_mb < 1000 else 0)
+    assert round(b["pack"] / 1e6, digits) == pack_mb
+    assert round(b["combine"] / 1e6, digits) == combine_mb
+    n = cfg.T * cfg.k
+    assert b["layout_pack"] == b["pack"] + 8 * n        # plus reading the ids and writing row_src
+    assert b["layout"] == 12 * n
+
+
+def test_pair_roofline_sums_bytes_and_time():
+    kernels = {"layout_pack": {"algorithmic_bytes": 100, "avg_us": 1e-3},
+               "combine": {"algorithmic_bytes": 300, "avg_us": 3e-3}}
+    r = bench.pair_roofline(kernels)
+    assert r["kernels"] == ["layout_pack", "combine"]
+    assert r["algorithmic_bytes"] == 400 and r["avg_us"] == pytest.approx(4e-3)
+    assert r["achieved"] == pytest.approx(100.0) and r["frac"] == pytest.approx(100.0 / bench.HBM_PEAK_GBPS)
+    two = {"pack": kernels["layout_pack"], "combine": kernels["combine"]}
+    assert bench.pair_roofline(two)["kernels"] == ["pack", "combine"]
+
+
+@pytest.mark.parametrize("kernel", ["layout_pack", "pack", "combine"])
+def test_committed_traffic_is_fresh_and_close_to_the_definition(kernel, monkeypatch):
+    """A committed counter figure is used only while the kernel's sources hash as when it
+    was taken; when used, it is within 2% of the algorithmic bytes (no wasted re-reads)."""
+    path = os.path.join(ROOT, "profiles", f"traffic_{kernel}_coarse.json")
+    if not os.path.exists(path):
+        pytest.skip("no committed counter summary for this kernel")
+    traffic = bench.committed_traffic("coarse", kernel)
+    if traffic is None:
+        pytest.skip("the kernel changed since its counters were taken (the bench reports null)")
+    want = bench.algorithmic_bytes(synth.config("coarse"))[kernel]
+    assert abs(traffic - want) <= 0.02 * want
+    assert json.load(open(path))["source_sha256"] == bench.source_hash(kernel)
+    monkeypatch.setattr(bench, "source_hash", lambda k: "0" * 16)
+    assert bench.committed_traffic("coarse", kernel) is None
+
+
+def test_kernel_hash_covers_its_headers(tmp_path, monkeypatch):
+    """The hash changes with any file the kernel is compiled from, headers included."""
+    csrc = tmp_path / "paper_2609_40093_amd" / "csrc"
+    csrc.mkdir(parents=True)
+    for name in bench.KERNEL_SOURCES["layout_pack"]:
+        (csrc / name).write_text(name)
+    monkeypatch.setattr(bench, "ROOT", str(tmp_path))
+    h0 = bench.source_hash("layout_pack")
+    (csrc / "wave.h").write_text("changed")
+    assert bench.source_hash("layout_pack") != h0
+
+
+def test_refuses_more_than_one_gpu():
+    r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--gpus", "2"], capture_output=True,
+                       text=True, timeout=120)
+    assert r.returncode == 2
+    assert "exactly one GPU" in json.loads(r.stdout.strip().splitlines()[-1])["error"]
