@@ -4,8 +4,9 @@ guard its reuse, and the rows move on the compute units to and from pinned memor
 A round = ep_round_advance, layout, ep_dispatch_graph, ep_combine_graph.  Simulated peers
 echo the rows (identity experts), so with dyadic gates every round returns x exactly.
 The same round is run eagerly and captured once in a HIP graph and replayed; between
-replays new rows are written into the captured input buffer, so a replay that reused
-stale rows, a stale buffer set or a stale round number fails.
+replays new rows and a new routing are written into the captured input buffers, so a
+replay that reused stale rows, a stale layout, a stale buffer set or a stale round number
+fails.
 """
 import numpy as np
 import pytest
@@ -94,12 +95,19 @@ def test_graph_capture_replay():
         say(f"graph replay {rep}")
         xr = payload(case, 100 + rep)
         x.copy_(torch.from_numpy(xr.view(np.int16)))
+        # a new routing in the captured routing buffer: the captured layout must recompute
+        route = make_case("graph_route", case.T, case.H, case.E, case.k, case.R, "random", seed=200 + rep)
+        idx.copy_(torch.from_numpy(route.topk_idx))
         g.replay()
         torch.cuda.synchronize()
         peers.wait_round(2 + rep)
         st.status()
         assert np.array_equal(out.cpu().numpy(), as_f32(xr)), f"replay {rep}"
         assert st.host_array("send_flags", (2 + rep) % 2)[0] == 2 + rep
+        ref = oracle.layout(route.topk_idx, case.E, case.R)
+        assert np.array_equal(lay.slot_pos.cpu().numpy(), ref.slot_pos), f"replay {rep}: stale layout"
+        sent = st.host_array("send", (2 + rep) % 2)[:case.slots]
+        assert np.array_equal(sent, oracle.pack(xr, ref.slot_pos, case.k)), f"replay {rep}: pinned send rows"
     assert ep.round_read(st) == 7
     peers.close()
     st.close()
