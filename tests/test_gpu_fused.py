@@ -12,7 +12,7 @@ import torch
 
 import oracle
 import paper_2609_40093_amd as ep
-from gpu_cases import from_config, make_case, say
+from gpu_cases import TOL_MAX_ABS, TOL_MEAN_ABS, combine_errors, from_config, make_case, say
 
 pytestmark = pytest.mark.gpu
 
@@ -341,4 +341,51 @@ def test_trace_percentiles():
     s = ep.trace_read()["layout_pack"]
     assert s["count"] == 25
     assert 0 < s["min_ms"] <= s["p10_ms"] <= s["p50_ms"] <= s["p90_ms"] <= s["max_ms"]
+    st.close()
+
+
+def test_fused_dispatch_and_combine_replay_in_a_graph():
+    """The benchmark's step (one-kernel dispatch, then combine; HBM staging) captured once
+    in a HIP graph and replayed with new rows, a new routing and new gates written into the
+    captured inputs each time: every replay's layout, packed rows and combine match the
+    oracle's for its inputs."""
+    T, H, E, k, R = 1024, 2048, 8, 2, 4
+    base = make_case("fused_graph", T, H, E, k, R, "random", seed=40)
+    st = ep.Staging("hbm", T * k, H, R, num_buffers=1)
+    x = to_dev(base.x.view(np.int16))
+    idx = to_dev(base.topk_idx)
+    w = to_dev(base.topk_w)
+    y = to_dev(base.y.view(np.int16))
+    st.write_device("recv", y)
+    out = torch.empty((T, H), dtype=torch.bfloat16, device=DEV)
+    lay = ep.dispatch_fused(x, idx, E, R, st)
+    ep.combine(st, lay.slot_pos, w, out=out)
+    torch.cuda.synchronize()
+    say("fused step: graph capture")
+    g = torch.cuda.CUDAGraph()
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        with torch.cuda.graph(g, stream=s):
+            ep.dispatch_fused(x, idx, E, R, st, out=lay)
+            ep.combine(st, lay.slot_pos, w, out=out)
+    torch.cuda.current_stream().wait_stream(s)
+    torch.cuda.synchronize()
+    for rep in range(4):
+        say(f"fused step: graph replay {rep}")
+        case = make_case("fused_graph_rep", T, H, E, k, R, "skewed" if rep % 2 else "random", seed=50 + rep)
+        x.copy_(to_dev(case.x.view(np.int16)))
+        idx.copy_(to_dev(case.topk_idx))
+        w.copy_(to_dev(case.topk_w))
+        g.replay()
+        torch.cuda.synchronize()
+        ep.layout_status(lay)
+        ref = oracle.layout(case.topk_idx, E, R)
+        for key in LAYOUT_KEYS:
+            assert np.array_equal(getattr(lay, key).cpu().numpy(), getattr(ref, key)), f"replay {rep}: {key}"
+        packed = st.read_device("send", T * k).cpu().numpy().view(np.uint16)
+        assert packed.tobytes() == oracle.pack(case.x, ref.slot_pos, k).tobytes(), f"replay {rep}: packed"
+        exact, _, _ = oracle.combine(base.y, ref.slot_pos, case.topk_w)
+        mx, mean = combine_errors(out.view(torch.int16).cpu().numpy().view(np.uint16), exact)
+        assert mx <= TOL_MAX_ABS and mean <= TOL_MEAN_ABS, f"replay {rep}: combine {mx} {mean}"
     st.close()
