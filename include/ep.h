@@ -197,11 +197,22 @@ ep_status ep_staging_status(ep_staging *s, hipStream_t stream);
  *                        the round trip through host memory like any other.
  *   EP_MODE_REMOTE_ONLY  (with DUPLEX) the rank's own segment never crosses PCIe: it is
  *                        copied inside HBM (packed -> dev_in, dev_in -> recv).
- * self_rank: the rank this GPU plays (0..R-1).  Requires R <= 63.  Allocates host_in,
- * dev_in and host_ret on first use of DUPLEX. */
+ *   EP_MODE_ACCUMULATE   (with PER_SENDER) ep_combine reduces each sender's returned rows
+ *                        as they land (Sec. 4.4 per-sender policy; Sec. 4.5: computation
+ *                        begins upon each sender's completion): one pass per growth of
+ *                        the set of landed senders adds, for every token, the slots of the
+ *                        longest prefix whose senders have all landed, to an fp32 partial
+ *                        sum in device memory.  Every token's k rows still go in slot
+ *                        order from +0, so `out` equals that of the single reduction bit
+ *                        for bit, whatever order the senders arrive in.  Adds T*H*4 bytes
+ *                        of device memory per buffer set (allocated by the first combine,
+ *                        regrown when T*H grows).
+ * self_rank: the rank this GPU plays (0..R-1).  The exchange modes require R <= 32.
+ * Allocates host_in, dev_in and host_ret on first use of DUPLEX. */
 #define EP_MODE_PER_SENDER 1u
 #define EP_MODE_DUPLEX 2u
 #define EP_MODE_REMOTE_ONLY 4u
+#define EP_MODE_ACCUMULATE 8u
 ep_status ep_staging_set_mode(ep_staging *s, uint32_t mode, int32_t self_rank);
 
 /* Rows each sender r != self_rank dispatches to this rank in buffer set `buf` (host

@@ -14,7 +14,7 @@ EP_OK, EP_ERR_INVALID_ARG, EP_ERR_BAD_ROUTING, EP_ERR_HIP, EP_ERR_OOM, EP_ERR_TI
 EP_STAGING_HBM, EP_STAGING_PINNED_HOST = 0, 1
 EP_OUT_BF16, EP_OUT_F32 = 0, 1
 EP_SIM_FLAGS_ONLY, EP_SIM_ECHO = 0, 1
-EP_MODE_PER_SENDER, EP_MODE_DUPLEX, EP_MODE_REMOTE_ONLY = 1, 2, 4
+EP_MODE_PER_SENDER, EP_MODE_DUPLEX, EP_MODE_REMOTE_ONLY, EP_MODE_ACCUMULATE = 1, 2, 4, 8
 ABI_VERSION = 3
 EP_MAX_EXPERTS = 2048
 

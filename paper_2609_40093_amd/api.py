@@ -19,10 +19,11 @@ from ._lib import (EP_OK, EP_ERR_BAD_ROUTING, EP_ERR_TIMEOUT, EP_STAGING_HBM, EP
                    EP_OUT_BF16, EP_OUT_F32, EP_SIM_ECHO, EP_SIM_FLAGS_ONLY)
 
 MODE_PER_SENDER, MODE_DUPLEX, MODE_REMOTE_ONLY = _lib.EP_MODE_PER_SENDER, _lib.EP_MODE_DUPLEX, _lib.EP_MODE_REMOTE_ONLY
+MODE_ACCUMULATE = _lib.EP_MODE_ACCUMULATE
 
 __all__ = ["EPError", "Layout", "Staging", "SimPeers", "dispatch_layout", "layout_status", "dispatch",
            "combine", "trace_enable", "trace_read", "trace_reset", "copy_probe", "workspace_bytes",
-           "pcie_probe", "MODE_PER_SENDER", "MODE_DUPLEX", "MODE_REMOTE_ONLY", "LocalLayout",
+           "pcie_probe", "MODE_PER_SENDER", "MODE_DUPLEX", "MODE_REMOTE_ONLY", "MODE_ACCUMULATE", "LocalLayout",
            "dispatch_layout_local", "pack", "combine_rows", "Dense", "allgather", "reducescatter",
            "round_advance", "round_read", "dispatch_graph", "combine_graph"]
 

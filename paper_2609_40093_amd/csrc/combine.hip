@@ -168,6 +168,114 @@ hipError_t launch_uk(const void *recv, const int32_t *slot_pos, const float *top
     return err;
 }
 
+// One pass of the per-sender accumulation (a combine that reduces each sender's returned
+// rows as they land).  For a token and a set M of senders, p_M is the length of the
+// longest prefix of its k slots whose rows all come from senders in M (a slot without a
+// row belongs to every prefix; a row's sender is the rank segment holding it, rows past
+// the last segment count as the last sender's).  Pass i adds the slots [p_prev, p_cur)
+// for M = masks[i], masks[i + 1] -- in slot order, to the fp32 partial kept in `acc` (from
+// +0 unless an earlier pass added a row of this token), by the very FMAs of
+// combine_kernel -- and writes a token whose prefix is complete to `out`.  Sets only
+// grow, so every slot is added once and in slot order: the result equals combine_kernel's
+// bit for bit whatever order the senders arrive in.  A slot without a row is skipped:
+// combine_kernel adds exactly -0 for it, which changes nothing.  One wave per (token,
+// 64-vector chunk).
+template <bool F32_OUT>
+__global__ __launch_bounds__(256) void accumulate_kernel(const u32x4 *__restrict__ recv,
+                                                         const int32_t *__restrict__ slot_pos,
+                                                         const float *__restrict__ topk_w, int64_t T, int32_t V,
+                                                         int32_t chunks, int32_t k,
+                                                         const int32_t *__restrict__ rank_offsets, int32_t R,
+                                                         const uint32_t *__restrict__ masks, int32_t i,
+                                                         float *__restrict__ acc, void *__restrict__ out,
+                                                         int64_t max_rows) {
+    const int lane = threadIdx.x & (kWave - 1);
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
+    const int64_t item = (int64_t)blockIdx.x * (blockDim.x / kWave) + wave;
+    const int64_t t = item / chunks;
+    if (t >= T)
+        return;
+    const int32_t v = (int32_t)(item - t * chunks) * kWave + lane;
+    const bool vin = v < V;
+    const int32_t ro = lane <= R ? rank_offsets[lane] : INT32_MAX;  // lane r: first row of rank r
+    const uint32_t prev = masks[i], cur = masks[i + 1];
+    const int32_t *sp = slot_pos + t * k;
+    auto sender = [&](int64_t p) {  // the segment holding row p (wave-uniform p)
+        return min((int)__popcll(__ballot(ro <= p)) - 1, R - 1);
+    };
+    int32_t pp = -1, pc = k;
+    bool added_before = false;  // a row of this token went into acc in an earlier pass
+    for (int32_t j = 0; j < k; ++j) {  // wave-uniform
+        const int64_t p = sp[j];
+        if (p < 0 || p >= max_rows)
+            continue;
+        const int r = sender(p);
+        if (pp < 0) {
+            if ((prev >> r) & 1u)
+                added_before = true;
+            else
+                pp = j;
+        }
+        if (!((cur >> r) & 1u)) {
+            pc = j;
+            break;
+        }
+    }
+    if (pp < 0) {  // every row of the token was in before this pass
+        if (i != 0)
+            return;    // written by an earlier pass
+        pp = k;        // a token without rows: written by pass 0, as +0 (combine_kernel's sum)
+    } else if (pc == pp) {
+        return;
+    }
+    const int64_t o = t * V + (vin ? v : 0);
+    float a[8];
+    if (added_before && vin) {
+        const u32x4 lo = reinterpret_cast<const u32x4 *>(acc)[2 * o];
+        const u32x4 hi = reinterpret_cast<const u32x4 *>(acc)[2 * o + 1];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            a[q] = __uint_as_float(lo[q]);
+            a[4 + q] = __uint_as_float(hi[q]);
+        }
+    } else {
+#pragma unroll
+        for (int q = 0; q < 8; ++q)
+            a[q] = 0.0f;
+    }
+    for (int32_t j = pp; j < pc; ++j) {
+        const int64_t p = sp[j];
+        if (p < 0 || p >= max_rows)
+            continue;
+        const float g = topk_w[t * k + j];
+        const u32x4 d = __builtin_nontemporal_load(recv + p * V + (vin ? v : 0));
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            a[2 * q] = __builtin_fmaf(g, bf16_lo(d[q]), a[2 * q]);
+            a[2 * q + 1] = __builtin_fmaf(g, bf16_hi(d[q]), a[2 * q + 1]);
+        }
+    }
+    if (!vin)
+        return;
+    if (pc == k) {
+        if constexpr (F32_OUT) {
+            u32x4 *dst = (u32x4 *)out + 2 * o;
+            __builtin_nontemporal_store(u32x4{__float_as_uint(a[0]), __float_as_uint(a[1]), __float_as_uint(a[2]),
+                                              __float_as_uint(a[3])}, dst);
+            __builtin_nontemporal_store(u32x4{__float_as_uint(a[4]), __float_as_uint(a[5]), __float_as_uint(a[6]),
+                                              __float_as_uint(a[7])}, dst + 1);
+        } else {
+            const u32x4 r = {pack_bf16x2(a[0], a[1]), pack_bf16x2(a[2], a[3]), pack_bf16x2(a[4], a[5]),
+                             pack_bf16x2(a[6], a[7])};
+            __builtin_nontemporal_store(r, (u32x4 *)out + o);
+        }
+    } else {
+        u32x4 *dst = reinterpret_cast<u32x4 *>(acc) + 2 * o;
+        dst[0] = u32x4{__float_as_uint(a[0]), __float_as_uint(a[1]), __float_as_uint(a[2]), __float_as_uint(a[3])};
+        dst[1] = u32x4{__float_as_uint(a[4]), __float_as_uint(a[5]), __float_as_uint(a[6]), __float_as_uint(a[7])};
+    }
+}
+
 }  // namespace
 
 hipError_t launch_combine(const void *recv, const int32_t *slot_pos, const float *topk_w,
@@ -192,6 +300,35 @@ hipError_t launch_combine(const void *recv, const int32_t *slot_pos, const float
     if (k >= 2)
         return launch_uk<2, 2>(recv, slot_pos, topk_w, T, V, k, out, out_f32, max_rows, stream, sel);
     return launch_uk<4, 1>(recv, slot_pos, topk_w, T, V, k, out, out_f32, max_rows, stream, sel);
+}
+
+hipError_t launch_accumulate(const void *recv, const int32_t *slot_pos, const float *topk_w, int64_t T, int32_t H,
+                             int32_t k, const int32_t *rank_offsets, int32_t R, const uint32_t *masks, int32_t i,
+                             float *acc, void *out, bool out_f32, int64_t max_rows, hipStream_t stream) {
+    if (T <= 0)
+        return hipSuccess;
+    if (!recv || !slot_pos || !topk_w || !rank_offsets || !masks || !acc || !out || H % 8 != 0 || R < 1 ||
+        R > 32 || i < 0)
+        return hipErrorInvalidValue;
+    const int32_t V = H / 8;
+    const int32_t chunks = (V + kWave - 1) / kWave;
+    const int64_t blocks = (T * chunks + 3) / 4;
+    if (blocks > INT32_MAX)
+        return hipErrorInvalidValue;
+    (void)hipGetLastError();
+    TraceSlot ts = trace_acquire();
+    if (out_f32)
+        hipExtLaunchKernelGGL(accumulate_kernel<true>, dim3((unsigned)blocks), dim3(256), 0, stream, ts.start,
+                              ts.stop, 0, (const u32x4 *)recv, slot_pos, topk_w, T, V, chunks, k, rank_offsets, R,
+                              masks, i, acc, out, max_rows);
+    else
+        hipExtLaunchKernelGGL(accumulate_kernel<false>, dim3((unsigned)blocks), dim3(256), 0, stream, ts.start,
+                              ts.stop, 0, (const u32x4 *)recv, slot_pos, topk_w, T, V, chunks, k, rank_offsets, R,
+                              masks, i, acc, out, max_rows);
+    hipError_t err = hipGetLastError();
+    if (err == hipSuccess)
+        trace_submit("accumulate", ts);
+    return err;
 }
 
 }  // namespace ep

@@ -351,6 +351,7 @@ void staging_release(ep_staging *s) {
         if (s->dev_in[b]) (void)hipFree(s->dev_in[b]);
         if (s->host_in[b]) (void)hipHostFree(s->host_in[b]);
         if (s->host_ret[b]) (void)hipHostFree(s->host_ret[b]);
+        if (s->dev_acc[b]) (void)hipFree(s->dev_acc[b]);
         for (hipEvent_t e : {s->ev_up_in[b], s->ev_up_done[b], s->ev_down_in[b], s->ev_down_done[b]})
             if (e) (void)hipEventDestroy(e);
     }
@@ -358,6 +359,7 @@ void staging_release(ep_staging *s) {
     if (s->flags) (void)hipHostFree(s->flags);
     if (s->dev_epoch) (void)hipFree(s->dev_epoch);
     if (s->dev_round) (void)hipFree(s->dev_round);
+    if (s->dev_masks) (void)hipFree(s->dev_masks);
     for (hipStream_t st : {s->up, s->down})
         if (st) (void)hipStreamDestroy(st);
     delete s;
@@ -515,13 +517,15 @@ extern "C" ep_status ep_staging_get(ep_staging *s, int32_t buf, ep_staging_view 
 extern "C" ep_status ep_staging_set_mode(ep_staging *s, uint32_t mode, int32_t self_rank) {
     if (!s)
         return fail(EP_ERR_INVALID_ARG, "ep_staging_set_mode: staging is NULL");
-    const uint32_t known = EP_MODE_PER_SENDER | EP_MODE_DUPLEX | EP_MODE_REMOTE_ONLY;
+    const uint32_t known = EP_MODE_PER_SENDER | EP_MODE_DUPLEX | EP_MODE_REMOTE_ONLY | EP_MODE_ACCUMULATE;
     if (mode & ~known)
         return fail(EP_ERR_INVALID_ARG, "ep_staging_set_mode: unknown mode bits 0x%x", mode & ~known);
     if (mode && s->kind != EP_STAGING_PINNED_HOST)
         return fail(EP_ERR_INVALID_ARG, "ep_staging_set_mode: exchange modes need a PINNED_HOST staging");
     if ((mode & EP_MODE_REMOTE_ONLY) && !(mode & EP_MODE_DUPLEX))
         return fail(EP_ERR_INVALID_ARG, "ep_staging_set_mode: EP_MODE_REMOTE_ONLY needs EP_MODE_DUPLEX");
+    if ((mode & EP_MODE_ACCUMULATE) && !(mode & EP_MODE_PER_SENDER))
+        return fail(EP_ERR_INVALID_ARG, "ep_staging_set_mode: EP_MODE_ACCUMULATE needs EP_MODE_PER_SENDER");
     if (mode && s->num_ranks > ep::kMaxExchangeRanks)
         return fail(EP_ERR_INVALID_ARG, "ep_staging_set_mode: at most %d ranks in the exchange modes, have %d",
                     ep::kMaxExchangeRanks, s->num_ranks);
@@ -550,6 +554,13 @@ extern "C" ep_status ep_staging_set_mode(ep_staging *s, uint32_t mode, int32_t s
             if (e != hipSuccess)
                 return hip_fail(e, "ep_staging_set_mode: duplex buffers");
         }
+    }
+    if ((mode & EP_MODE_ACCUMULATE) && !s->dev_masks) {
+        void *p = nullptr;
+        hipError_t e = hipMalloc(&p, (size_t)ep::kMaxBuffers * ep::kMaskWords * sizeof(uint32_t));
+        if (e != hipSuccess)
+            return hip_fail(e, "ep_staging_set_mode: landed-set words");
+        s->dev_masks = static_cast<uint32_t *>(p);
     }
     if (mode && !s->xchg) {
         std::string err;
@@ -771,6 +782,27 @@ extern "C" ep_status ep_combine(ep_staging *s, int32_t buf, uint32_t epoch, cons
     const int64_t rows = num_tokens * topk;
     if (rows == 0)
         return EP_OK;
+    if (s->kind == EP_STAGING_PINNED_HOST && (s->mode & EP_MODE_ACCUMULATE)) {
+        if (!rank_offsets)  // the passes find each row's sender from the device offsets
+            return fail(EP_ERR_INVALID_ARG, "ep_combine: EP_MODE_ACCUMULATE needs rank_offsets");
+        // fp32 partial sums of this buffer set, grown on demand (after the device has
+        // finished the rounds that used the smaller buffer)
+        const size_t need = (size_t)num_tokens * (size_t)hidden * sizeof(float);
+        if (s->acc_bytes[buf] < need) {
+            if (s->dev_acc[buf]) {
+                EP_HIP(hipDeviceSynchronize());
+                EP_HIP(hipFree(s->dev_acc[buf]));
+                s->dev_acc[buf] = nullptr;
+                s->acc_bytes[buf] = 0;
+            }
+            void *p = nullptr;
+            EP_HIP(hipMalloc(&p, need));
+            s->dev_acc[buf] = static_cast<float *>(p);
+            s->acc_bytes[buf] = need;
+        }
+        const ep::AccumulateCall call{slot_pos, topk_w, num_tokens, topk, out_dev, out_dtype == EP_OUT_F32};
+        return ep::exchange_combine(s, buf, epoch, rows, rank_offsets, stream, &call);
+    }
     if (s->kind == EP_STAGING_PINNED_HOST && s->mode != 0) {
         st = ep::exchange_combine(s, buf, epoch, rows, rank_offsets, stream);
         if (st != EP_OK)

@@ -144,6 +144,18 @@ hipError_t launch_combine(const void *recv, const int32_t *slot_pos, const float
                           int64_t T, int32_t H, int32_t k, void *out, bool out_f32,
                           int64_t max_rows, hipStream_t stream, RoundSel sel = {});
 
+// Per-sender accumulation (combine.hip, signal.hip).  masks: device words, masks[0] the
+// senders whose rows need no wait, masks[i + 1] the senders landed before pass i.
+// launch_landed_set waits (bounded) until the landed set (landed[r] holds the epoch)
+// grows past masks[i] (base for i = 0) and records it; launch_accumulate runs pass i
+// into the fp32 partial acc [T][H], writing each token to out once its k slots are in.
+hipError_t launch_landed_set(const uint32_t *landed, int32_t R, uint32_t epoch, uint32_t base, uint32_t *masks,
+                             int32_t i, int64_t timeout_ticks, int32_t sleep_units, uint32_t *status,
+                             hipStream_t stream);
+hipError_t launch_accumulate(const void *recv, const int32_t *slot_pos, const float *topk_w, int64_t T, int32_t H,
+                             int32_t k, const int32_t *rank_offsets, int32_t R, const uint32_t *masks, int32_t i,
+                             float *acc, void *out, bool out_f32, int64_t max_rows, hipStream_t stream);
+
 // One lane per flag polls flags[i] until (int32)(flags[i] - epoch) >= 0, at most
 // timeout_ticks of the constant-rate wall clock; on expiry stores EP_ERR_TIMEOUT to *status.
 hipError_t launch_wait_flags(const char *name, const uint32_t *flags, int32_t n, uint32_t epoch,

@@ -254,7 +254,7 @@ ep_status exchange_dispatch(ep_staging *s, int b, uint32_t epoch, int64_t rows, 
 }
 
 ep_status exchange_combine(ep_staging *s, int b, uint32_t epoch, int64_t rows, const int32_t *rank_offsets,
-                           hipStream_t stream) {
+                           hipStream_t stream, const AccumulateCall *acc) {
     const char *who = "ep_combine";
     const int R = s->num_ranks, me = s->self_rank;
     if (!(s->offs_valid[(size_t)b] && s->offs_epoch[(size_t)b] == epoch)) {
@@ -325,6 +325,7 @@ ep_status exchange_combine(ep_staging *s, int b, uint32_t epoch, int64_t rows, c
 
     // ---- inbound: sender r's returned rows for this rank's segment r -> dev_recv, on the
     //      inbound engine as each sender's flag arrives (the courier)
+    uint32_t base = 0;  // senders whose rows need no wait: none, or copied inside HBM
     int copies = 0;
     for (int r = 0; r < R; ++r)
         copies += ro[r + 1] > ro[r] && !(r == me && remote_only);
@@ -334,11 +335,14 @@ ep_status exchange_combine(ep_staging *s, int b, uint32_t epoch, int64_t rows, c
     std::vector<InCopy> plan;
     for (int r = 0; r < R; ++r) {
         const int64_t n = ro[r + 1] - ro[r];
-        if (n == 0)
+        if (n == 0) {
+            base |= 1u << r;
             continue;
+        }
         char *dst = drecv + ro[r] * rb;
         if (r == me && remote_only) {
             EP_HIP(hipMemcpyAsync(dst, din + off[me] * rb, (size_t)(n * rb), hipMemcpyDeviceToDevice, stream));
+            base |= 1u << r;
             continue;
         }
         const bool own_dup = r == me && duplex;  // own results come back from host_ret
@@ -348,11 +352,29 @@ ep_status exchange_combine(ep_staging *s, int b, uint32_t epoch, int64_t rows, c
         if (!x.signal(*slot, 1, d, err))
             return fail(EP_ERR_HIP, "%s: %s", who, err.c_str());
         plan.push_back({ready, dst, src, n * rb, d, s->recv_landed(b) + r});
-        bt.add_wait(s->recv_landed(b) + r);
+        if (!acc)
+            bt.add_wait(s->recv_landed(b) + r);
         slot->finish.push_back({s->recv_landed(b) + r, epoch});
     }
     post_inbound(x, s, std::move(plan), epoch, per_sender, start, ew, landed_done);
-    EP_HIP(launch_gate("wait_combine", bt.waits, stream));
+    if (!acc) {
+        EP_HIP(launch_gate("wait_combine", bt.waits, stream));
+        return EP_OK;
+    }
+
+    // ---- the reduction, one pass per growth of the set of landed senders (at most one
+    //      pass per sender that needs a wait; later passes find nothing left to add)
+    const int passes = std::max(1, R - __builtin_popcount(base));
+    uint32_t *masks = s->dev_masks + (size_t)b * kMaskWords;
+    const int64_t ticks = s->timeout_us * s->wall_clock_khz / 1000;
+    for (int i = 0; i < passes; ++i) {
+        EP_HIP(launch_landed_set(s->recv_landed(b), R, epoch, base, masks, i, ticks, s->sleep_units, s->status(),
+                                 stream));
+        EP_HIP(launch_accumulate(drecv, acc->slot_pos, acc->topk_w, acc->T, s->hidden, acc->k, rank_offsets, R,
+                                 masks, i, s->dev_acc[b], acc->out, acc->out_f32, s->max_rows, stream));
+    }
+    if (bt.waits.n > 0)  // duplex: the results this rank returned are out of dev_in
+        EP_HIP(launch_gate("wait_returned_out", bt.waits, stream));
     return EP_OK;
 }
 

@@ -144,7 +144,63 @@ __global__ __launch_bounds__(64) void round_stamp_kernel(const uint32_t *round_p
                        __HIP_MEMORY_SCOPE_SYSTEM);
 }
 
+// The set of senders whose rows pass i of the per-sender accumulation may add: the set of
+// pass i - 1 (masks[i]; empty before pass 0) with the senders of `base` (rows that need no
+// wait) and those whose landed[r] holds the epoch.  Waits (one lane per sender, pausing
+// between polls, bounded by the wall clock) until it holds a sender outside pass i - 1's
+// set and `base`, or every sender, so that every pass adds a sender that was waited for
+// and one pass per such sender suffices.  Records the set in masks[i + 1] (and the empty
+// set in masks[0]).  On expiry it records every sender (the rows still missing are
+// reduced as they are) and leaves a timeout in the status word.
+__global__ __launch_bounds__(64) void landed_set_kernel(const uint32_t *landed, int32_t R, uint32_t epoch,
+                                                        uint32_t base, uint32_t *masks, int32_t i,
+                                                        int64_t timeout_ticks, int32_t sleep_units,
+                                                        uint32_t *status) {
+    const int lane = threadIdx.x;
+    const uint32_t full = R >= 32 ? ~0u : ((1u << R) - 1u);
+    const uint32_t prev = i == 0 ? 0u : __hip_atomic_load(masks + i, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    const uint32_t start = prev | base;
+    uint32_t m = start;
+    const int64_t t0 = wall_clock64();
+    for (;;) {
+        bool in = false;
+        if (lane < R && !((start >> lane) & 1u))
+            in = (int32_t)(__hip_atomic_load(landed + lane, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_SYSTEM) - epoch) >= 0;
+        m = start | (uint32_t)__ballot(in);
+        if (m != start || m == full)
+            break;
+        if (wall_clock64() - t0 > timeout_ticks) {
+            if (lane == 0)
+                __hip_atomic_store(status, kStatusTimeout, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+            m = full;
+            break;
+        }
+        for (int32_t s = 0; s < sleep_units; ++s)
+            __builtin_amdgcn_s_sleep(1);
+    }
+    if (lane == 0) {
+        if (i == 0)
+            __hip_atomic_store(masks, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        __hip_atomic_store(masks + i + 1, m, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+}
+
 }  // namespace
+
+hipError_t launch_landed_set(const uint32_t *landed, int32_t R, uint32_t epoch, uint32_t base, uint32_t *masks,
+                             int32_t i, int64_t timeout_ticks, int32_t sleep_units, uint32_t *status,
+                             hipStream_t stream) {
+    if (!landed || !masks || R < 1 || R > 32 || i < 0)
+        return hipErrorInvalidValue;
+    (void)hipGetLastError();
+    TraceSlot ts = trace_acquire();
+    hipExtLaunchKernelGGL(landed_set_kernel, dim3(1), dim3(64), 0, stream, ts.start, ts.stop, 0, landed, R, epoch,
+                          base, masks, i, timeout_ticks, sleep_units, status);
+    hipError_t err = hipGetLastError();
+    if (err == hipSuccess)
+        trace_submit("landed_set", ts);
+    return err;
+}
 
 hipError_t launch_round_advance(uint32_t *round, hipStream_t stream) {
     (void)hipGetLastError();

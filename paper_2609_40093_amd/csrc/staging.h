@@ -38,7 +38,8 @@ bool d2h_through_hip();
 
 // ---- exchange modes (exchange.cpp)
 class Exchange;
-constexpr int kMaxExchangeRanks = 32;  // 2R flags fit one polling wave
+constexpr int kMaxExchangeRanks = 32;  // 2R flags fit one polling wave; a sender set fits 32 bits
+constexpr int kMaskWords = 64;         // landed-set words per buffer set (EP_MODE_ACCUMULATE)
 Exchange *exchange_create(int device, int nslots, std::string &err);
 void exchange_destroy(Exchange *x);
 const char *exchange_engines(const Exchange *x);
@@ -51,11 +52,22 @@ namespace ep {
 // Queues the copy of rank_offsets to the host mirror of buffer set b (before the pack).
 ep_status exchange_enqueue_mirror(ep_staging *s, int b, uint32_t epoch, const int32_t *rank_offsets,
                                   hipStream_t stream, const char *who);
+// The reduction of a combine in EP_MODE_ACCUMULATE: run by exchange_combine itself, one
+// pass per arrival of senders.
+struct AccumulateCall {
+    const int32_t *slot_pos;
+    const float *topk_w;
+    int64_t T;
+    int32_t k;
+    void *out;
+    bool out_f32;
+};
 // Host legs of a dispatch (after the pack was queued) and of a combine (before the
-// reduction is queued), in the staging's exchange mode.
+// reduction is queued, or with the reduction when `acc` is given), in the staging's
+// exchange mode.
 ep_status exchange_dispatch(ep_staging *s, int b, uint32_t epoch, int64_t rows, hipStream_t stream);
 ep_status exchange_combine(ep_staging *s, int b, uint32_t epoch, int64_t rows, const int32_t *rank_offsets,
-                           hipStream_t stream);
+                           hipStream_t stream, const AccumulateCall *acc = nullptr);
 }  // namespace ep
 
 struct ep_staging {
@@ -95,6 +107,11 @@ struct ep_staging {
     std::vector<uint32_t> offs_sent;  // [nbuf] epoch of the last mirror queued (may still be in flight)
     std::vector<uint32_t> in_epoch;   // [nbuf] epoch of the last duplex dispatch (off_in valid)
     ep::Exchange *xchg = nullptr;
+    // EP_MODE_ACCUMULATE: per buffer set the fp32 partial sums [T][H] (grown on demand),
+    // and the landed-set words of its passes [nbuf][kMaskWords]
+    float *dev_acc[ep::kMaxBuffers] = {};
+    size_t acc_bytes[ep::kMaxBuffers] = {};
+    uint32_t *dev_masks = nullptr;
 
     size_t R() const { return (size_t)num_ranks; }
     size_t nb() const { return (size_t)num_buffers; }

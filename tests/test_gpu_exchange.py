@@ -16,6 +16,7 @@ import torch
 import oracle
 import paper_2609_40093_amd as ep
 from gpu_cases import make_case, say
+from paper_2609_40093_amd import synth
 
 pytestmark = pytest.mark.gpu
 
@@ -161,6 +162,107 @@ def test_ready_senders_land_before_a_late_one(per_sender):
     st.close()
 
 
+ACC = ep.MODE_ACCUMULATE
+# return delays of the 8 senders (us after the round is posted)
+ARRIVALS = {
+    "at_once": [0] * 8,
+    "first_late": [250_000] + [0] * 7,
+    "last_late": [0] * 7 + [250_000],
+    "reversed": [(8 - r) * 30_000 for r in range(8)],
+    "staggered": [(r * 104729) % 150_000 for r in range(8)],
+}
+
+
+@pytest.mark.parametrize("arrival", sorted(ARRIVALS))
+@pytest.mark.parametrize("mode", [PS | ACC, DUP | PS | ACC, DUP | RO | PS | ACC],
+                         ids=["per_sender_acc", "duplex_per_sender_acc", "duplex_remote_only_per_sender_acc"])
+def test_accumulate_equals_single_reduction(mode, arrival):
+    """EP_MODE_ACCUMULATE reduces each sender's rows as they land, yet every token's rows
+    go in slot order: the output equals the single reduction of the same landed rows bit
+    for bit (bf16 and fp32), whatever the arrival order, and the oracle within tolerance."""
+    T, H, E, k, R, me = 1000, 512, 64, 8, 8, 3
+    case = make_case("accumulate", T, H, E, k, R, "skewed", seed=23)
+    rows = T * k
+    lay_o = oracle.layout(case.topk_idx, E, R)
+    ro = lay_o.rank_offsets
+    st = ep.Staging("pinned", rows, H, R, num_buffers=2, chunk_bytes=1 << 20)
+    st.set_mode(mode, self_rank=me)
+    peers = ep.SimPeers(st, echo=True)
+    peers.set_delays(inbound_us=[0] * R, return_us=ARRIVALS[arrival])
+    idx = torch.from_numpy(case.topk_idx).to(DEV)
+    w = torch.from_numpy(case.topk_w).to(DEV)
+    lay = ep.dispatch_layout(idx, E, R)
+    rng = np.random.default_rng(6)
+    for rnd, dt in enumerate((torch.bfloat16, torch.float32)):
+        buf, epoch = rnd % 2, 50 + rnd
+        say(f"accumulate mode {mode} arrival {arrival} round {rnd}")
+        xr = case.x ^ np.uint16(rnd + 1)
+        if mode & DUP:
+            rin = [int(rng.integers(0, 300)) for _ in range(R)]
+            rin[me] = 0
+            st.set_inbound(buf, rin)
+            n_in = sum(rin) + int(ro[me + 1] - ro[me])
+            st.host_array("in", buf)[:n_in] = synth.normal_bf16_rows(np.random.SeedSequence([9, rnd]), n_in, H)
+        peers.post(buf, epoch, rows)
+        ep.dispatch(bits(xr), lay.slot_pos, st, topk=k, buf=buf, epoch=epoch, rank_offsets=lay.rank_offsets)
+        out = ep.combine(st, lay.slot_pos, w, out_dtype=dt, buf=buf, epoch=epoch, rank_offsets=lay.rank_offsets)
+        st.status()
+        peers.drain()
+        ref = torch.empty_like(out)
+        ep.combine_rows(st.read_device("recv", rows, buf), lay.slot_pos, w, ref)
+        iv = torch.int16 if dt == torch.bfloat16 else torch.int32
+        assert torch.equal(out.view(iv), ref.view(iv)), "accumulated combine != single reduction"
+        exact, _, _ = oracle.combine(oracle.pack(xr, lay_o.slot_pos, k), lay_o.slot_pos, case.topk_w)
+        got = out.float().cpu().numpy().astype(np.float64)
+        err = np.abs(got - exact)
+        assert err.max() <= 2e-2 and err.mean() <= 2e-3
+    peers.close()
+    st.close()
+
+
+def test_accumulate_reduces_before_a_late_sender_lands():
+    """Sender 1 is held back 0.6 s.  Meanwhile every token none of whose rows comes from it
+    is already final in the output (read from another stream while the combine still waits),
+    and every other token is still unwritten."""
+    T, H, E, k, R = 2048, 1024, 32, 2, 4
+    case = make_case("acc_late", T, H, E, k, R, "random", seed=24)
+    rows = T * k
+    st = ep.Staging("pinned", rows, H, R, num_buffers=1)
+    st.set_mode(PS | ACC)
+    peers = ep.SimPeers(st, echo=True)
+    peers.set_delays(return_us=[0, 600_000, 0, 0])
+    idx = torch.from_numpy(case.topk_idx).to(DEV)
+    lay = ep.dispatch_layout(idx, E, R)
+    ro = lay.rank_offsets.cpu().numpy()
+    w = torch.from_numpy(case.topk_w).to(DEV)
+    out = torch.full((T, H), float("nan"), dtype=torch.float32, device=DEV)
+    torch.cuda.synchronize()
+    epoch = 5
+    say("accumulate with a late sender")
+    peers.post(0, epoch, rows)
+    ep.dispatch(bits(case.x), lay.slot_pos, st, topk=k, epoch=epoch, rank_offsets=lay.rank_offsets)
+    ep.combine(st, lay.slot_pos, w, out=out, epoch=epoch, rank_offsets=lay.rank_offsets)
+    rl = st.host_array("recv_landed")
+    assert wait_host(lambda: all(rl[r] == epoch for r in (0, 2, 3) if ro[r + 1] > ro[r]), 5.0)
+    time.sleep(0.1)  # the passes for the ready senders run within milliseconds
+    side = torch.cuda.Stream()
+    snap = torch.empty((T, H), dtype=torch.float32, pin_memory=True)
+    with torch.cuda.stream(side):
+        snap.copy_(out, non_blocking=True)
+    side.synchronize()
+    assert rl[1] != epoch, "the late sender landed before the snapshot"
+    st.status()
+    peers.drain()
+    final = out.cpu()
+    sender = np.searchsorted(ro, lay.slot_pos.cpu().numpy(), side="right").reshape(T, k) - 1
+    early = torch.from_numpy(~(sender == 1).any(axis=1))
+    assert early.any() and (~early).any()
+    assert torch.equal(snap[early], final[early]), "tokens of landed senders not final before the late one"
+    assert torch.isnan(snap[~early]).all(), "a token waiting for the late sender was written early"
+    peers.close()
+    st.close()
+
+
 def test_exchange_argument_errors():
     say("exchange argument errors")
     hbm = ep.Staging("hbm", 64, 64, 4, num_buffers=1)
@@ -170,6 +272,8 @@ def test_exchange_argument_errors():
     st = ep.Staging("pinned", 64, 64, 4, num_buffers=1)
     with pytest.raises(ep.EPError, match="needs EP_MODE_DUPLEX"):
         st.set_mode(RO)
+    with pytest.raises(ep.EPError, match="needs EP_MODE_PER_SENDER"):
+        st.set_mode(ep.MODE_ACCUMULATE)
     with pytest.raises(ep.EPError, match="self_rank"):
         st.set_mode(PS, self_rank=4)
     with pytest.raises(ep.EPError, match="exceed"):
