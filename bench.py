@@ -303,12 +303,14 @@ def main():
 
 
 PINNED_MODES = (
-    # name, mode bits (EP_MODE_*: 1 per-sender, 2 duplex, 4 remote-only)
+    # name, mode bits (EP_MODE_*: 1 per-sender, 2 duplex, 4 remote-only, 8 accumulate as senders land)
     ("default", 0),
     ("per_sender", 1),
     ("duplex", 2),
     ("duplex_per_sender", 3),
     ("duplex_remote_only_per_sender", 7),
+    ("per_sender_accumulate", 9),
+    ("duplex_per_sender_accumulate", 11),
 )
 
 
