@@ -94,7 +94,7 @@ __global__ __launch_bounds__(256) void pack_kernel(const u32x4 *__restrict__ x, 
 // One wave per (token, chunk, slot), the k waves of a chunk adjacent: each wave writes a
 // single destination row.
 template <int U, bool EXACT>
-__global__ __launch_bounds__(256) void pack_slot_kernel(const u32x4 *__restrict__ x, int64_t T, PackGeom pg, int32_t k,
+__global__ __launch_bounds__(1024) void pack_slot_kernel(const u32x4 *__restrict__ x, int64_t T, PackGeom pg, int32_t k,
                                                         const int32_t *__restrict__ slot_pos,
                                                         u32x4 *__restrict__ packed, int64_t max_rows,
                                                         uint32_t *epoch_word, uint32_t epoch, RoundSel sel,
@@ -131,11 +131,11 @@ __global__ __launch_bounds__(256) void pack_slot_kernel(const u32x4 *__restrict_
 }
 
 template <int U, bool EXACT>
-void launch_pack_u(bool per_slot, dim3 grid, hipStream_t stream, TraceSlot ts, const u32x4 *x, int64_t T,
+void launch_pack_u(bool per_slot, dim3 grid, dim3 block, hipStream_t stream, TraceSlot ts, const u32x4 *x, int64_t T,
                    const PackGeom &pg, int32_t k, const int32_t *slot_pos, u32x4 *packed, int64_t max_rows,
                    uint32_t *epoch_word, uint32_t epoch, RoundSel sel, bool fence_system) {
     if (per_slot)
-        hipExtLaunchKernelGGL(pack_slot_kernel<U, EXACT>, grid, dim3(256), 0, stream, ts.start, ts.stop, 0, x, T, pg,
+        hipExtLaunchKernelGGL(pack_slot_kernel<U, EXACT>, grid, block, 0, stream, ts.start, ts.stop, 0, x, T, pg,
                               k, slot_pos, packed, max_rows, epoch_word, epoch, sel, fence_system);
     else
         hipExtLaunchKernelGGL(pack_kernel<U, EXACT>, grid, dim3(256), 0, stream, ts.start, ts.stop, 0, x, T, pg, k,
@@ -166,7 +166,12 @@ hipError_t launch_pack(const void *x, int64_t T, int32_t H, int32_t k, const int
     pg.gpc = exact ? exact : (pg.G < 16 ? pg.G : 16);
     pg.chunks = (pg.G + pg.gpc - 1) / pg.gpc;
     const int64_t items = (per_slot ? T * k : T) * pg.chunks;
-    const int64_t blocks = (items + 3) / 4;  // 4 waves per workgroup
+    // per-slot waves of one token chunk share its row through L2 only inside one workgroup
+    // (consecutive workgroups run on different XCDs, each with its own L2): for k = 8 or 16
+    // a workgroup of k waves holds them all, so the row is fetched from HBM once (4-wave
+    // workgroups fetched it twice at k = 8; measured on MI355X)
+    const int waves = per_slot && (k == 8 || k == 16) ? k : 4;
+    const int64_t blocks = (items + waves - 1) / waves;
     if (blocks > INT32_MAX)
         return hipErrorInvalidValue;
     const dim3 grid((unsigned)blocks);
@@ -174,7 +179,7 @@ hipError_t launch_pack(const void *x, int64_t T, int32_t H, int32_t k, const int
     u32x4 *pv = static_cast<u32x4 *>(packed);
     (void)hipGetLastError();  // drop an error left by an earlier, already reported call
     TraceSlot ts = trace_acquire();
-#define EP_PACK_ARGS per_slot, grid, stream, ts, xv, T, pg, k, slot_pos, pv, max_rows, epoch_word, epoch, sel, fence_system
+#define EP_PACK_ARGS per_slot, grid, dim3(per_slot ? waves * kWave : 256), stream, ts, xv, T, pg, k, slot_pos, pv, max_rows, epoch_word, epoch, sel, fence_system
     switch (exact) {
     case 16: launch_pack_u<16, true>(EP_PACK_ARGS); break;
     case 15: launch_pack_u<15, true>(EP_PACK_ARGS); break;

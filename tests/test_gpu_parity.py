@@ -113,6 +113,10 @@ CASES = [
     ("rows_16_groups", 200, 8192, 8, 2, 4, "random"),
     ("rows_18_groups_two_chunks", 100, 9216, 16, 2, 4, "random"),
     ("rows_17_groups_generic", 120, 8704, 16, 4, 4, "random"),
+    # per-slot pack in workgroups of k waves (k = 8, 16), exact and generic row lengths
+    ("k16_sixteen_wave_pack", 500, 2048, 64, 16, 8, "random"),
+    ("k16_generic_rows", 150, 8704, 32, 16, 4, "random"),
+    ("k8_generic_rows", 200, 8704, 32, 8, 4, "random"),
 ]
 
 
