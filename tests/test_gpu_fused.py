@@ -389,3 +389,41 @@ def test_fused_dispatch_and_combine_replay_in_a_graph():
         mx, mean = combine_errors(out.view(torch.int16).cpu().numpy().view(np.uint16), exact)
         assert mx <= TOL_MAX_ABS and mean <= TOL_MEAN_ABS, f"replay {rep}: combine {mx} {mean}"
     st.close()
+
+
+def _random_fused_shapes(n=48, seed=2024):
+    """Seeded shapes inside the one kernel's limits: every k, expert counts from 1 to 256
+    with a rank count dividing them, every row length, token counts up to each limit."""
+    rng = np.random.default_rng(seed)
+    shapes = []
+    while len(shapes) < n:
+        k = int(rng.choice([1, 2, 4, 8]))
+        E = int(rng.integers(max(k, 1), 257))
+        divisors = [r for r in range(1, min(E, 32) + 1) if E % r == 0]
+        R = int(rng.choice(divisors))
+        G = int(rng.choice([1, 2, 4, 8, 14, 16]))
+        H = 512 * G
+        limit = 65536 if (E <= 64 and k <= 4) else (16384 if H <= 4096 else 8192)
+        T = int(rng.integers(1, min(limit // k, 20000) + 1))
+        if T * H * 2 * (k + 1) > (1 << 28):   # keep each case under 256 MiB of rows
+            continue
+        kind = str(rng.choice(["random", "skewed", "firstk"]))
+        shapes.append((f"r{len(shapes)}_T{T}_H{H}_E{E}_k{k}_R{R}_{kind}", T, H, E, k, R, kind))
+    return shapes
+
+
+@pytest.mark.parametrize("spec", _random_fused_shapes(), ids=lambda c: c[0])
+def test_fused_random_shapes(spec):
+    name, T, H, E, k, R, kind = spec
+    case = make_case(name, T, H, E, k, R, kind, seed=len(name) + T)
+    say(f"fused random shape {name}")
+    ref = oracle.layout(case.topk_idx, E, R)
+    st = ep.Staging("hbm", T * k, H, R, num_buffers=1)
+    lay, kernels = run_fused(to_dev(case.topk_idx), to_dev(case.x.view(np.int16)), E, R, st)
+    assert "layout_pack" in kernels, kernels
+    ep.layout_status(lay)
+    for key in LAYOUT_KEYS:
+        assert np.array_equal(getattr(lay, key).cpu().numpy(), getattr(ref, key)), f"{key} differs"
+    packed = st.read_device("send", T * k).cpu().numpy().view(np.uint16)
+    assert packed.tobytes() == oracle.pack(case.x, ref.slot_pos, k).tobytes(), "packed rows differ"
+    st.close()
