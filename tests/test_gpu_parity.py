@@ -126,6 +126,31 @@ def test_parity_shapes(spec):
     check_case(make_case(name, T, H, E, k, R, kind, seed=len(name)))
 
 
+def _random_shapes(n=40, seed=77):
+    """Seeded shapes for the two-kernel path: any row length that is a multiple of 8 (whole
+    groups or not), E up to 2048 with R dividing E, k up to 32, token counts up to 5000."""
+    rng = np.random.default_rng(seed)
+    shapes = []
+    while len(shapes) < n:
+        E = int(rng.choice([int(rng.integers(1, 65)), int(rng.integers(65, 513)), int(rng.integers(513, 2049))]))
+        k = int(min(E, rng.choice([1, 2, 3, 4, 6, 8, 12, 16, 32])))
+        divisors = [r for r in range(1, min(E, 64) + 1) if E % r == 0]
+        R = int(rng.choice(divisors))
+        H = 8 * int(rng.integers(1, 1025))
+        T = int(rng.integers(1, 5001))
+        if T * H * 2 * (k + 1) > (1 << 27):   # under 128 MiB of rows (the oracle's combine runs in fp64)
+            continue
+        kind = str(rng.choice(["random", "skewed", "firstk"]))
+        shapes.append((f"r{len(shapes)}_T{T}_H{H}_E{E}_k{k}_R{R}_{kind}", T, H, E, k, R, kind))
+    return shapes
+
+
+@pytest.mark.parametrize("spec", _random_shapes(), ids=lambda c: c[0])
+def test_parity_random_shapes(spec):
+    name, T, H, E, k, R, kind = spec
+    check_case(make_case(name, T, H, E, k, R, kind, seed=T + H))
+
+
 @pytest.mark.parametrize("name", ["tiny", "coarse", "fine", "decode"])
 def test_parity_workloads(name):
     check_case(from_config(name))
