@@ -8,7 +8,9 @@
 // and pack.  A workgroup of W waves owns W*tpw consecutive tokens (a run of tpw per
 // wave); W is 4, 8 or 16 by the number of routing entries (each workgroup counts all of
 // them, so fewer, larger workgroups for more entries; more, smaller ones for few -- less
-// of the kernel waits on its last workgroups):
+// of the kernel waits on its last workgroups).  Below 1024 tokens a row is split over S
+// waves instead (each moves 1/S of it; W = m*S for m tokens, one per S waves), so that
+// the stores of few tokens still reach every compute unit:
 //   A. each wave issues the loads of its first ids, then those of its first token row
 //      (they do not depend on the layout; vector loads complete in order, so the ids
 //      come first);
@@ -25,8 +27,9 @@
 //   D. wave 0 ranks the workgroup's own entries in flat order (ballot match-any and a
 //      masked popcount, as the layout kernel does: stable), stores slot_pos / row_src and
 //      keeps the rows in LDS;
-//   E. each wave stores its tokens' rows to their k packed rows (non-temporal; a row is
-//      U groups of 64 16-byte vectors, one per lane, all loads in flight together).
+//   E. each wave stores its tokens' rows (or its part of one) to their k packed rows
+//      (non-temporal; U groups of 64 16-byte vectors, one per lane, all loads in flight
+//      together).
 // The outputs equal those of the layout kernel followed by the pack kernel, bit for bit.
 // Workgroups never wait on each other, so nothing needs them resident together.
 //
@@ -35,7 +38,8 @@
 // top-8), T*k <= 65536 for E <= 64 and k <= 4, else T*k <= 16384 for rows up to 8 KiB and
 // 8192 for longer ones (every workgroup reads and counts every id before its stores:
 // beyond that the layout kernel's exchange of totals costs less), rows of 1, 2, 4, 8, 14
-// or 16 groups (H = 512 * groups), a 16-byte aligned routing array.
+// or 16 groups (H = 512 * groups), a 16-byte aligned routing array.  The split runs of
+// fewer than 1024 tokens keep the same limits.
 #include "ep_internal.h"
 #include "wave.h"
 
@@ -54,6 +58,7 @@ constexpr int kFMaxOwn = 256;                // entries one workgroup owns (LDS 
 constexpr int kFOwnRounds = kFMaxOwn / kWave;
 constexpr int kFBatch = 4;                   // 16-byte id loads in flight per lane
 constexpr int kFMaxWaves = 4096;             // waves in flight over the device (16 per CU)
+constexpr int64_t kFSplitBelow = 1024;       // tokens below which rows are split over waves
 
 typedef int32_t i32x4 __attribute__((ext_vector_type(4)));
 
@@ -109,9 +114,9 @@ __device__ __forceinline__ bool halves_repeat(i32x4 a, i32x4 b, int E) {
 // MULTI: more ids than one batch of the workgroup's loads (the count loops).  Instances
 // without the loop have only straight-line loads, so the compiler's waits stay exact and
 // no wave waits for its token row before the count's barrier.  WIDE: more than 64
-// experts (four per lane in step C).
+// experts (four per lane in step C).  U: groups per wave (the row's, or 1/split of them).
 template <int U, int K, bool MULTI, bool WIDE>
-__global__ __launch_bounds__(kFMaxThreads) void layout_pack_kernel(FusedArgs a, int32_t tpw) {
+__global__ __launch_bounds__(kFMaxThreads) void layout_pack_kernel(FusedArgs a, int32_t tpw, int32_t split) {
     constexpr int ME = WIDE ? kFMaxE : kFNarrowE;  // counters per copy
     __shared__ int s_all[kFCopies * ME];
     __shared__ int s_pre[kFCopies * ME];
@@ -122,8 +127,10 @@ __global__ __launch_bounds__(kFMaxThreads) void layout_pack_kernel(FusedArgs a, 
     const int tid = threadIdx.x, lane = tid & (kWave - 1), w = tid / kWave;
     const int threads = blockDim.x, waves = threads / kWave;
     const int64_t slots = a.T * K;
-    const int64_t tok0 = (int64_t)blockIdx.x * waves * tpw;
-    const int64_t tok1 = min(a.T, tok0 + (int64_t)waves * tpw);
+    const int runs = waves / split;  // token runs of tpw tokens (split == 1: one per wave)
+    const int64_t tok0 = (int64_t)blockIdx.x * runs * tpw;  // runs*tpw*K: a multiple of 4
+    const int64_t tok1 = min(a.T, tok0 + (int64_t)runs * tpw);
+    const int32_t col = (w % split) * U * kWave;  // this wave's first vector of a row
     const int64_t ent0 = tok0 * K, ent1 = tok1 * K;
     const int32_t V = a.H / 8;
     const u32x4 *x = static_cast<const u32x4 *>(a.x);
@@ -147,10 +154,10 @@ __global__ __launch_bounds__(kFMaxThreads) void layout_pack_kernel(FusedArgs a, 
     const int64_t ti = full * 4 + lane;
     const int tail_id = a.topk_idx[min(ti, slots - 1)];
     const int tail_next = a.topk_idx[min(ti + 1, slots - 1)];
-    const int64_t wtok = tok0 + (int64_t)w * tpw;
+    const int64_t wtok = tok0 + (int64_t)(w / split) * tpw;
     u32x4 d[U];
     {
-        const u32x4 *src = x + min(wtok, tok1 - 1) * V + lane;
+        const u32x4 *src = x + min(wtok, tok1 - 1) * V + col + lane;
 #pragma unroll
         for (int u = 0; u < U; ++u)
             d[u] = __builtin_nontemporal_load(src + u * kWave);
@@ -338,14 +345,14 @@ __global__ __launch_bounds__(kFMaxThreads) void layout_pack_kernel(FusedArgs a, 
     }
     __syncthreads();
 
-    // E. store each token row to its k packed rows
+    // E. store each token row (this wave's part of it) to its k packed rows
     u32x4 *packed = static_cast<u32x4 *>(a.packed);
     for (int j0 = 0; j0 < tpw; ++j0) {
         const int64_t t = wtok + j0;
         if (t >= tok1)
             break;
         if (j0 > 0) {
-            const u32x4 *src = x + t * V + lane;
+            const u32x4 *src = x + t * V + col + lane;
 #pragma unroll
             for (int u = 0; u < U; ++u)
                 d[u] = __builtin_nontemporal_load(src + u * kWave);
@@ -355,7 +362,7 @@ __global__ __launch_bounds__(kFMaxThreads) void layout_pack_kernel(FusedArgs a, 
             const int64_t p = s_pos[(t - tok0) * K + j];
             if (p < 0 || p >= a.max_rows)
                 continue;
-            u32x4 *dst = packed + p * V + lane;
+            u32x4 *dst = packed + p * V + col + lane;
 #pragma unroll
             for (int u = 0; u < U; ++u)
                 __builtin_nontemporal_store(d[u], dst + u * kWave);
@@ -364,16 +371,17 @@ __global__ __launch_bounds__(kFMaxThreads) void layout_pack_kernel(FusedArgs a, 
 }
 
 template <int U, int K, bool MULTI, bool WIDE>
-void launch_one(const FusedArgs &a, int32_t tpw, unsigned blocks, int threads, hipStream_t stream, TraceSlot ts) {
+void launch_one(const FusedArgs &a, int32_t tpw, int32_t split, unsigned blocks, int threads, hipStream_t stream,
+                TraceSlot ts) {
     hipExtLaunchKernelGGL((layout_pack_kernel<U, K, MULTI, WIDE>), dim3(blocks), dim3(threads), 0, stream, ts.start,
-                          ts.stop, 0, a, tpw);
+                          ts.stop, 0, a, tpw, split);
 }
 
 // Picks the instance: the count loop only where one batch of loads does not cover every
 // id (never within the wide limits: at most 16384 ids, 1024 threads x 16), four experts
 // per lane above 64 experts.
 template <int U>
-hipError_t launch_k(const FusedArgs &a, int32_t tpw, unsigned blocks, int threads, hipStream_t stream,
+hipError_t launch_k(const FusedArgs &a, int32_t tpw, int32_t split, unsigned blocks, int threads, hipStream_t stream,
                     TraceSlot ts) {
     const bool multi = a.T * a.k > (int64_t)threads * kFBatch * 4;  // one batch: kFBatch 4-id groups per thread
     const bool wide = a.E > kFNarrowE;
@@ -381,26 +389,77 @@ hipError_t launch_k(const FusedArgs &a, int32_t tpw, unsigned blocks, int thread
         return hipErrorInvalidValue;  // excluded by the limits
     switch (a.k) {
     case 1:
-        wide ? launch_one<U, 1, false, true>(a, tpw, blocks, threads, stream, ts)
-             : (multi ? launch_one<U, 1, true, false>(a, tpw, blocks, threads, stream, ts)
-                      : launch_one<U, 1, false, false>(a, tpw, blocks, threads, stream, ts));
+        wide ? launch_one<U, 1, false, true>(a, tpw, split, blocks, threads, stream, ts)
+             : (multi ? launch_one<U, 1, true, false>(a, tpw, split, blocks, threads, stream, ts)
+                      : launch_one<U, 1, false, false>(a, tpw, split, blocks, threads, stream, ts));
         break;
     case 2:
-        wide ? launch_one<U, 2, false, true>(a, tpw, blocks, threads, stream, ts)
-             : (multi ? launch_one<U, 2, true, false>(a, tpw, blocks, threads, stream, ts)
-                      : launch_one<U, 2, false, false>(a, tpw, blocks, threads, stream, ts));
+        wide ? launch_one<U, 2, false, true>(a, tpw, split, blocks, threads, stream, ts)
+             : (multi ? launch_one<U, 2, true, false>(a, tpw, split, blocks, threads, stream, ts)
+                      : launch_one<U, 2, false, false>(a, tpw, split, blocks, threads, stream, ts));
         break;
     case 4:
-        wide ? launch_one<U, 4, false, true>(a, tpw, blocks, threads, stream, ts)
-             : (multi ? launch_one<U, 4, true, false>(a, tpw, blocks, threads, stream, ts)
-                      : launch_one<U, 4, false, false>(a, tpw, blocks, threads, stream, ts));
+        wide ? launch_one<U, 4, false, true>(a, tpw, split, blocks, threads, stream, ts)
+             : (multi ? launch_one<U, 4, true, false>(a, tpw, split, blocks, threads, stream, ts)
+                      : launch_one<U, 4, false, false>(a, tpw, split, blocks, threads, stream, ts));
         break;
     default:
-        wide ? launch_one<U, 8, false, true>(a, tpw, blocks, threads, stream, ts)
-             : launch_one<U, 8, false, false>(a, tpw, blocks, threads, stream, ts);
+        wide ? launch_one<U, 8, false, true>(a, tpw, split, blocks, threads, stream, ts)
+             : launch_one<U, 8, false, false>(a, tpw, split, blocks, threads, stream, ts);
         break;
     }
     return hipSuccess;
+}
+
+// Workgroups of one call.  Below kFSplitBelow tokens a row is split over the fewest waves
+// S (dividing its G groups, with an instance for G/S groups) that make the call at least
+// kFSplitBelow waves, else over the most; a workgroup holds m tokens (m*S waves: at least
+// 4, and enough threads that one batch of id loads covers every id; at most 16; m*k a
+// multiple of 4, since step B splits the ids before the workgroup's own at whole 4-id
+// groups).  Split
+// rows measured on MI355X, 256 experts top-8, 14 KiB rows: 256 tokens 9.8 against 11.4 us,
+// 512 tokens 16.1 against 16.9 us.  Otherwise 4, 8 or 16 waves by the entries (4 or 8
+// win up to 8192 entries, 16 above), with tpw tokens per wave so that the workgroups hold
+// at most kFMaxWaves waves.
+struct FusedGeom {
+    int32_t split = 1, waves = 4, tpw = 1;
+    int64_t blocks = 0;
+};
+
+FusedGeom fused_geometry(int64_t T, int32_t k, int G) {
+    FusedGeom g;
+    const int64_t slots = T * k;
+    const int64_t ids_per_wave = (int64_t)kWave * kFBatch * 4;  // one batch of 16-byte id loads
+    if (T < kFSplitBelow) {
+        int split = 1;
+        for (int d : {2, 4, 7, 8, 14, 16}) {
+            const int u = G % d == 0 ? G / d : 0;
+            if (u == 1 || u == 2 || u == 4 || u == 8) {
+                split = d;
+                if (T * d >= kFSplitBelow)
+                    break;
+            }
+        }
+        if (split > 1) {
+            int64_t m = split >= 4 ? 1 : 4 / split;
+            m = std::max<int64_t>(m, (slots + split * ids_per_wave - 1) / (split * ids_per_wave));
+            const int64_t q = k < 4 ? 4 / k : 1;  // m*k a multiple of 4
+            m = (m + q - 1) / q * q;
+            if (m * split <= 16) {
+                g.split = split;
+                g.waves = (int32_t)(m * split);
+                g.tpw = 1;
+                g.blocks = (T + m - 1) / m;
+                return g;
+            }
+        }
+    }
+    g.waves = slots <= 4096 ? 4 : (slots <= 8192 ? 8 : 16);
+    const int64_t max_blocks = kFMaxWaves / g.waves;
+    const int64_t per_block_min = (T + max_blocks - 1) / max_blocks;
+    g.tpw = (int32_t)((per_block_min + g.waves - 1) / g.waves);
+    g.blocks = (T + (int64_t)g.waves * g.tpw - 1) / ((int64_t)g.waves * g.tpw);
+    return g;
 }
 
 }  // namespace
@@ -421,29 +480,22 @@ bool fused_layout_pack_fits(int64_t T, int32_t k, int32_t E, int32_t H, const vo
 hipError_t launch_layout_pack(const FusedArgs &a, hipStream_t stream) {
     if (!fused_layout_pack_fits(a.T, a.k, a.E, a.H, a.topk_idx) || a.R < 1 || a.E % a.R != 0)
         return hipErrorInvalidValue;
-    // workgroup size by the entries every workgroup counts (measured on MI355X: 4 or 8
-    // waves win up to 8192 entries, 16 above); tokens per wave: enough that the workgroups
-    // hold at most kFMaxWaves waves
-    const int64_t slots = a.T * a.k;
-    const int waves = slots <= 4096 ? 4 : (slots <= 8192 ? 8 : 16);
-    const int64_t max_blocks = kFMaxWaves / waves;
-    const int64_t per_block_min = (a.T + max_blocks - 1) / max_blocks;
-    const int32_t tpw = (int32_t)((per_block_min + waves - 1) / waves);
-    const int64_t blocks = (a.T + (int64_t)waves * tpw - 1) / ((int64_t)waves * tpw);
-    if ((int64_t)waves * tpw * a.k > kFMaxOwn)
+    const int G = a.H / 512;
+    const FusedGeom g = fused_geometry(a.T, a.k, G);
+    if ((int64_t)(g.waves / g.split) * g.tpw * a.k > kFMaxOwn || g.blocks > INT32_MAX)
         return hipErrorInvalidValue;  // excluded by the limits above
     (void)hipGetLastError();  // drop an error left by an earlier, already reported call
     TraceSlot ts = trace_acquire();
-    const unsigned nb = (unsigned)blocks;
-    const int threads = waves * kWave;
+    const unsigned nb = (unsigned)g.blocks;
+    const int threads = g.waves * kWave;
     hipError_t err;
-    switch (a.H / 512) {
-    case 1: err = launch_k<1>(a, tpw, nb, threads, stream, ts); break;
-    case 2: err = launch_k<2>(a, tpw, nb, threads, stream, ts); break;
-    case 4: err = launch_k<4>(a, tpw, nb, threads, stream, ts); break;
-    case 8: err = launch_k<8>(a, tpw, nb, threads, stream, ts); break;
-    case 14: err = launch_k<14>(a, tpw, nb, threads, stream, ts); break;
-    default: err = launch_k<16>(a, tpw, nb, threads, stream, ts); break;
+    switch (G / g.split) {  // groups per wave
+    case 1: err = launch_k<1>(a, g.tpw, g.split, nb, threads, stream, ts); break;
+    case 2: err = launch_k<2>(a, g.tpw, g.split, nb, threads, stream, ts); break;
+    case 4: err = launch_k<4>(a, g.tpw, g.split, nb, threads, stream, ts); break;
+    case 8: err = launch_k<8>(a, g.tpw, g.split, nb, threads, stream, ts); break;
+    case 14: err = launch_k<14>(a, g.tpw, g.split, nb, threads, stream, ts); break;
+    default: err = launch_k<16>(a, g.tpw, g.split, nb, threads, stream, ts); break;
     }
     if (err != hipSuccess)
         return err;  // nothing was launched (unreachable within the limits)

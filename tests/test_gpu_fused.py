@@ -90,6 +90,13 @@ FUSED_CASES = [
     ("e200_empty_experts", 999, 512, 200, 4, 4, "firstk"),
     ("rows14_k2", 200, 7168, 16, 2, 4, "random"),
     ("rows14_e128_k1", 600, 7168, 128, 1, 4, "random"),
+    # below 1024 tokens a row is split over waves: 14 waves of one group each, two tokens
+    # of 7 waves each (the ids need 14 waves' loads), and each side of the 1024-token switch
+    ("split14_rows14", 100, 7168, 16, 2, 4, "random"),
+    ("split7_two_tokens_per_group", 1000, 7168, 256, 8, 8, "skewed"),
+    ("split_tokens_1023", 1023, 1024, 8, 2, 4, "random"),
+    ("split_k1_four_tokens_per_group", 300, 2048, 16, 1, 4, "random"),  # m*k kept a multiple of 4
+    ("split_tokens_1024", 1024, 1024, 8, 2, 4, "random"),
 ]
 
 
