@@ -50,21 +50,25 @@ def test_pair_roofline_sums_bytes_and_time():
     assert bench.pair_roofline(two)["kernels"] == ["pack", "combine"]
 
 
-@pytest.mark.parametrize("kernel", ["layout_pack", "pack", "combine"])
-def test_committed_traffic_is_fresh_and_close_to_the_definition(kernel, monkeypatch):
+TRAFFIC_FILES = sorted(f for f in os.listdir(os.path.join(ROOT, "profiles"))
+                       if f.startswith("traffic_") and f.endswith(".json"))
+
+
+@pytest.mark.parametrize("fname", TRAFFIC_FILES)
+def test_committed_traffic_is_fresh_and_close_to_the_definition(fname, monkeypatch):
     """A committed counter figure is used only while the kernel's sources hash as when it
     was taken; when used, it is within 2% of the algorithmic bytes (no wasted re-reads)."""
-    path = os.path.join(ROOT, "profiles", f"traffic_{kernel}_coarse.json")
-    if not os.path.exists(path):
-        pytest.skip("no committed counter summary for this kernel")
-    traffic = bench.committed_traffic("coarse", kernel)
+    rec = json.load(open(os.path.join(ROOT, "profiles", fname)))
+    kernel, workload = rec["kernel"], rec["workload"]
+    assert fname == f"traffic_{kernel}_{workload}.json"
+    traffic = bench.committed_traffic(workload, kernel)
     if traffic is None:
         pytest.skip("the kernel changed since its counters were taken (the bench reports null)")
-    want = bench.algorithmic_bytes(synth.config("coarse"))[kernel]
+    want = bench.algorithmic_bytes(synth.config(workload))[kernel]
     assert abs(traffic - want) <= 0.02 * want
-    assert json.load(open(path))["source_sha256"] == bench.source_hash(kernel)
+    assert rec["source_sha256"] == bench.source_hash(kernel)
     monkeypatch.setattr(bench, "source_hash", lambda k: "0" * 16)
-    assert bench.committed_traffic("coarse", kernel) is None
+    assert bench.committed_traffic(workload, kernel) is None
 
 
 def test_kernel_hash_covers_its_headers(tmp_path, monkeypatch):
