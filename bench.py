@@ -348,6 +348,21 @@ def pinned_legs(st, x, lay, w, out, k, leg_bytes, peaks, calls, epoch0) -> dict:
     return res
 
 
+def staging_flags(st) -> dict:
+    """Every host flag word of a pinned staging, per buffer set (reported with a failed mode)."""
+    import ctypes
+
+    def words(ptr, n):
+        return list((ctypes.c_uint32 * n).from_address(ptr)) if ptr and n > 0 else None
+    out = {}
+    for b, v in enumerate(st.views):
+        R = v.num_ranks
+        out[str(b)] = {"mode": v.mode, "send": words(v.send_flags, v.max_chunks), "recv": words(v.recv_flags, R),
+                       "in": words(v.in_flags, R), "ret": words(v.ret_flags, R), "in_landed": words(v.in_landed, R),
+                       "recv_landed": words(v.recv_landed, R)}
+    return out
+
+
 def bench_pinned(cfg, inp, y, args, dev) -> dict:
     """The same layer with pinned host staging, in each exchange mode.  Simulated peers
     announce their rows at once (no skew).  In the duplex modes every sender r sends this
@@ -386,41 +401,48 @@ def bench_pinned(cfg, inp, y, args, dev) -> dict:
                 inbound_rows = int(rin.sum()) + int(counts[me])
                 st.host_array("in", b)[:inbound_rows] = y[:inbound_rows]
         peers = ep.SimPeers(st, echo=False)
+        try:
 
-        def step(i):
-            buf, epoch = i % nbuf, i + 1
-            ep.dispatch_layout(idx, E, R, out=lay)
-            peers.post(buf, epoch, n)
-            ep.dispatch(x, lay.slot_pos, st, topk=k, buf=buf, epoch=epoch, rank_offsets=lay.rank_offsets)
-            ep.combine(st, lay.slot_pos, w, out=out, buf=buf, epoch=epoch, rank_offsets=lay.rank_offsets)
+            def step(i):
+                buf, epoch = i % nbuf, i + 1
+                ep.dispatch_layout(idx, E, R, out=lay)
+                peers.post(buf, epoch, n)
+                ep.dispatch(x, lay.slot_pos, st, topk=k, buf=buf, epoch=epoch, rank_offsets=lay.rank_offsets)
+                ep.combine(st, lay.slot_pos, w, out=out, buf=buf, epoch=epoch, rank_offsets=lay.rank_offsets)
 
-        for i in range(args.warmup):
-            step(i)
-        st.status()
-        peers.drain()
-        torch.cuda.synchronize()
-        t0 = time.perf_counter()
-        for i in range(steps):
-            step(args.warmup + i)
-        st.status()
-        t1 = time.perf_counter()
-        peers.drain()
-        ms = (t1 - t0) * 1e3 / steps
-        legs = {}
-        if mode == 0:
-            legs = pinned_legs(st, x, lay, w, out, k, n * rb, peaks, steps, args.warmup + steps)
-            # breakdown pass (not timed): the kernels, each bracketed by its launch events
-            ep.trace_reset()
-            ep.trace_enable(True)
-            for i in range(steps):  # epochs above the flags pinned_legs raised
-                step(args.warmup + 3 * steps + 200 + i)
+            for i in range(args.warmup):
+                step(i)
             st.status()
             peers.drain()
-            ep.trace_enable(False)
-            ks = ep.trace_read()
-            legs["kernels_avg_us"] = {kn: round(ks[kn]["mean_ms"] * 1e3, 2) for kn in
-                                      ("wait_d2h", "wait_recv", "release_signal", "pack", "combine", "layout")
-                                      if kn in ks}
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            for i in range(steps):
+                step(args.warmup + i)
+            st.status()
+            t1 = time.perf_counter()
+            peers.drain()
+            ms = (t1 - t0) * 1e3 / steps
+            legs = {}
+            if mode == 0:
+                legs = pinned_legs(st, x, lay, w, out, k, n * rb, peaks, steps, args.warmup + steps)
+                # breakdown pass (not timed): the kernels, each bracketed by its launch events
+                ep.trace_reset()
+                ep.trace_enable(True)
+                for i in range(steps):  # epochs above the flags pinned_legs raised
+                    step(args.warmup + 3 * steps + 200 + i)
+                st.status()
+                peers.drain()
+                ep.trace_enable(False)
+                ks = ep.trace_read()
+                legs["kernels_avg_us"] = {kn: round(ks[kn]["mean_ms"] * 1e3, 2) for kn in
+                                          ("wait_d2h", "wait_recv", "release_signal", "pack", "combine", "layout")
+                                          if kn in ks}
+        except ep.EPError as e:
+            # a failed mode is reported with its flag words, and the others still run
+            modes[name] = {"mode_bits": mode, "error": str(e), "flags": staging_flags(st)}
+            peers.close()
+            st.close()
+            continue
         peers.close()
         st.close()
         self_rows = int(counts[me]) if mode & ep.MODE_REMOTE_ONLY else 0
@@ -446,9 +468,15 @@ def bench_pinned(cfg, inp, y, args, dev) -> dict:
                                         "(dispatch: pack + device->host leg + flag wait; combine: flag wait with the "
                                         "flags already up + host->device leg + reduction), so each rate is a lower "
                                         "bound on the leg's own; kernel times from a separate traced pass")
-    dense = bench_dense(cfg, inp, args, dev, peaks)
-    graph = bench_graph(["decode", cfg.name], args, dev, peaks)
-    decode_latency = bench_decode_latency(args, dev)
+
+    def section(fn, *a):  # a failed section is reported, and the others still run
+        try:
+            return fn(*a)
+        except ep.EPError as e:
+            return {"error": str(e)}
+    dense = section(bench_dense, cfg, inp, args, dev, peaks)
+    graph = section(bench_graph, ["decode", cfg.name], args, dev, peaks)
+    decode_latency = section(bench_decode_latency, args, dev)
     return {
         "decode_dispatch_host_latency": decode_latency,
         "graph_replayed_rounds": graph,

@@ -88,3 +88,17 @@ def test_refuses_more_than_one_gpu():
                        text=True, timeout=120)
     assert r.returncode == 2
     assert "exactly one GPU" in json.loads(r.stdout.strip().splitlines()[-1])["error"]
+
+
+def test_a_failed_pinned_mode_reports_its_flag_words():
+    """bench.staging_flags reads every host flag word of each buffer set (absent kinds: None)."""
+    import ctypes
+    import types
+    send, recv = (ctypes.c_uint32 * 2)(5, 6), (ctypes.c_uint32 * 3)(1, 2, 3)
+    landed = (ctypes.c_uint32 * 3)(7, 0, 7)
+    v = types.SimpleNamespace(num_ranks=3, max_chunks=2, mode=9, send_flags=ctypes.addressof(send),
+                              recv_flags=ctypes.addressof(recv), in_flags=None, ret_flags=None, in_landed=None,
+                              recv_landed=ctypes.addressof(landed))
+    got = bench.staging_flags(types.SimpleNamespace(views=[v]))
+    assert got == {"0": {"mode": 9, "send": [5, 6], "recv": [1, 2, 3], "in": None, "ret": None, "in_landed": None,
+                         "recv_landed": [7, 0, 7]}}
