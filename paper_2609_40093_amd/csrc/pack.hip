@@ -163,6 +163,18 @@ hipError_t launch_pack(const void *x, int64_t T, int32_t H, int32_t k, const int
                 exact = u >= (pg.G < 4 ? pg.G : 4) ? u : 0;  // no short chunks for long rows
                 break;
             }
+    // few tokens: shorter chunks, so that the launch keeps about 1024 waves (measured on
+    // MI355X, top-2 of 14 KiB rows: 128 tokens 2.8 against 3.8 us, 512 tokens 5.5 against 6.0)
+    if (exact > 1) {
+        const int64_t per_chunk = per_slot ? T * k : T;
+        if (per_chunk * (pg.G / exact) < 1024)
+            for (int u : kExactU)
+                if (u < exact && pg.G % u == 0) {
+                    exact = u;
+                    if (per_chunk * (pg.G / u) >= 1024)
+                        break;
+                }
+    }
     pg.gpc = exact ? exact : (pg.G < 16 ? pg.G : 16);
     pg.chunks = (pg.G + pg.gpc - 1) / pg.gpc;
     const int64_t items = (per_slot ? T * k : T) * pg.chunks;
