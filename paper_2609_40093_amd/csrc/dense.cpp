@@ -132,7 +132,8 @@ struct ep_dense {
     int64_t row_bytes = 0, block_row_bytes = 0;
     void *host_ag[kDenseMaxBuffers] = {}, *dev_gathered[kDenseMaxBuffers] = {};
     void *host_rs_out[kDenseMaxBuffers] = {}, *host_rs_in[kDenseMaxBuffers] = {}, *dev_rs_in[kDenseMaxBuffers] = {};
-    // coherent pinned: ag, ag_landed, rs_out, rs_in, rs_landed [nbuf][R] each, then status
+    // coherent pinned: ag, ag_landed, rs_out, rs_in, rs_landed [nbuf][R] each, then the
+    // status block (ep::kStatusWords words)
     uint32_t *flags = nullptr;
     char *dev_epoch = nullptr;
     hipEvent_t ev_sysrel = nullptr;
@@ -250,7 +251,7 @@ extern "C" ep_status ep_dense_alloc(int64_t max_tokens, int32_t hidden, int32_t 
         EP_DENSE_HIP(hipHostMalloc(&d->host_rs_in[b], rs_bytes, hipHostMallocDefault));
         EP_DENSE_HIP(hipMalloc(&d->dev_rs_in[b], rs_bytes));
     }
-    const size_t words = (size_t)5 * num_buffers * num_ranks + 1;
+    const size_t words = (size_t)5 * num_buffers * num_ranks + ep::kStatusWords;
     EP_DENSE_HIP(hipHostMalloc((void **)&d->flags, words * sizeof(uint32_t), hipHostMallocCoherent));
     std::memset(d->flags, 0, words * sizeof(uint32_t));
     EP_DENSE_HIP(hipMalloc((void **)&d->dev_epoch, kDenseMaxBuffers * ep::kEpochStride));
@@ -321,12 +322,24 @@ extern "C" ep_status ep_dense_status(ep_dense *d, hipStream_t stream) {
     if (!d)
         return fail(EP_ERR_INVALID_ARG, "ep_dense_status: NULL staging");
     EP_HIP(hipStreamSynchronize(stream));
-    const uint32_t word = __atomic_exchange_n(d->status(), 0u, __ATOMIC_ACQ_REL);
-    if (word == EP_ERR_TIMEOUT)
-        return fail(EP_ERR_TIMEOUT, "a completion-flag wait expired after %lld us", (long long)d->timeout_us);
-    if (word != 0)
-        return fail(EP_ERR_HIP, "dense staging status word %u", word);
-    return EP_OK;
+    struct Namer : ep::FlagNamer {
+        const ep_dense *d;
+        explicit Namer(const ep_dense *dd) : d(dd) {}
+        std::string operator()(const uint32_t *f) const override {
+            static const char *names[5] = {"ag_flags", "ag_landed", "rs_out_flags", "rs_in_flags", "rs_landed"};
+            for (int w = 0; w < 5; ++w)
+                for (int b = 0; b < d->nbuf; ++b) {
+                    const uint32_t *base = d->fl(w, b);
+                    if (f >= base && f < base + d->R) {
+                        char buf[80];
+                        std::snprintf(buf, sizeof buf, "%s[buf %d][rank %d]", names[w], b, (int)(f - base));
+                        return buf;
+                    }
+                }
+            return "";
+        }
+    };
+    return ep::take_status(d->status(), d->timeout_us, Namer(d));
 }
 
 extern "C" ep_status ep_dense_bytes(ep_dense *d, int64_t *up, int64_t *down) {
@@ -350,8 +363,8 @@ extern "C" ep_status ep_allgather(ep_dense *d, int32_t buf, uint32_t epoch, cons
         return fail(EP_ERR_INVALID_ARG, "%s: x must be a non-NULL 16-byte aligned pointer", who);
     ep::Exchange &x = *d->xchg;
     std::string err;
-    ep::XSlot *slot = x.begin(d->timeout_us, err);
-    if (!slot)
+    const int slot = x.begin(d->timeout_us, err);
+    if (slot < 0)
         return fail(EP_ERR_TIMEOUT, "%s: %s", who, err.c_str());
     char *hag = static_cast<char *>(d->host_ag[buf]);
     char *dg = static_cast<char *>(d->dev_gathered[buf]);
@@ -360,34 +373,30 @@ extern "C" ep_status ep_allgather(ep_dense *d, int32_t buf, uint32_t epoch, cons
 
     // own shard: into the gathered buffer (HBM copy) and once into host memory (SDMA)
     EP_HIP(hipMemcpyAsync(dg + me * shard, x_dev, (size_t)shard, hipMemcpyDeviceToDevice, stream));
-    hsa_signal_t start{}, sent{}, flag_done{};
-    if (!x.signal(*slot, 1, start, err) || !x.signal(*slot, 1, sent, err) || !x.signal(*slot, 1, flag_done, err))
+    hsa_signal_t start{}, sent{};
+    if (!x.start_signal(slot, start, err))
         return fail(EP_ERR_HIP, "%s: %s", who, err.c_str());
     EP_HIP(hipEventRecord(d->ev_sysrel, stream));
     EP_HIP(ep::launch_stamp_release(ew, epoch, ep::DmaEngines::value_pointer(start), stream));
-    if (!x.dma.copy(x.dma.out_engine(), hag + me * shard, true, x_dev, false, (size_t)shard, &start, 1, sent, err) ||
-        !x.dma.copy(x.dma.out_engine(), d->ag(buf) + me, true, ew, false, sizeof(uint32_t), &sent, 1, flag_done, err))
+    x.arm(slot, start);
+    if (!x.copy(slot, x.dma.out_engine(), hag + me * shard, true, x_dev, false, (size_t)shard, &start, 1, &sent, err) ||
+        !x.copy(slot, x.dma.out_engine(), d->ag(buf) + me, true, ew, false, sizeof(uint32_t), &sent, 1, nullptr, err))
         return fail(EP_ERR_HIP, "%s: %s", who, err.c_str());
     d->bytes_up += shard;
     ep::GateArgs waits;
     init_waits(waits, d, epoch);
     add_wait(waits, d->ag(buf) + me);
-    slot->finish.push_back({d->ag(buf) + me, epoch});
 
     // the other shards, each as soon as its rank's flag is in
     std::vector<ep::InCopy> plan;
-    hsa_signal_t landed_done{};
-    if (R > 1 && !x.signal(*slot, R - 1, landed_done, err))
-        return fail(EP_ERR_HIP, "%s: %s", who, err.c_str());
     for (int r = 0; r < R; ++r) {
         if (r == me)
             continue;
-        hsa_signal_t dn{};
-        if (!x.signal(*slot, 1, dn, err))
+        ep::InCopy c;
+        if (!x.in_copy(slot, d->ag(buf) + r, dg + r * shard, hag + r * shard, shard, d->ag_landed(buf) + r, c, err))
             return fail(EP_ERR_HIP, "%s: %s", who, err.c_str());
-        plan.push_back({d->ag(buf) + r, dg + r * shard, hag + r * shard, shard, dn, d->ag_landed(buf) + r});
+        plan.push_back(c);
         add_wait(waits, d->ag_landed(buf) + r);
-        slot->finish.push_back({d->ag_landed(buf) + r, epoch});
         d->bytes_down += shard;
     }
     if (!plan.empty()) {
@@ -397,10 +406,9 @@ extern "C" ep_status ep_allgather(ep_dense *d, int32_t buf, uint32_t epoch, cons
         j.per_sender = d->mode & EP_MODE_PER_SENDER;
         j.start = start;
         j.epoch_word = ew;
-        j.landed_done = landed_done;
         j.status = d->status();
         j.deadline = std::chrono::steady_clock::now() + std::chrono::microseconds(d->timeout_us);
-        x.courier.post(std::move(j));
+        x.post(slot, std::move(j));
     }
     EP_HIP(ep::launch_gate("wait_allgather", waits, stream));
     return EP_OK;
@@ -422,8 +430,8 @@ extern "C" ep_status ep_reducescatter(ep_dense *d, int32_t buf, uint32_t epoch, 
         return fail(EP_ERR_INVALID_ARG, "%s: blocks and out must be non-NULL 16-byte aligned pointers", who);
     ep::Exchange &x = *d->xchg;
     std::string err;
-    ep::XSlot *slot = x.begin(d->timeout_us, err);
-    if (!slot)
+    const int slot = x.begin(d->timeout_us, err);
+    if (slot < 0)
         return fail(EP_ERR_TIMEOUT, "%s: %s", who, err.c_str());
     const int me = d->me, R = d->R;
     const char *blocks = static_cast<const char *>(blocks_dev);
@@ -435,24 +443,23 @@ extern "C" ep_status ep_reducescatter(ep_dense *d, int32_t buf, uint32_t epoch, 
     init_waits(waits, d, epoch);
 
     // ---- up: this rank's blocks for the other ranks, each flagged as soon as written
-    hsa_signal_t start{}, out_done{};
-    if (!x.signal(*slot, 1, start, err) || (R > 1 && !x.signal(*slot, R - 1, out_done, err)))
+    hsa_signal_t start{};
+    if (!x.start_signal(slot, start, err))
         return fail(EP_ERR_HIP, "%s: %s", who, err.c_str());
     EP_HIP(hipEventRecord(d->ev_sysrel, stream));
     EP_HIP(ep::launch_stamp_release(ew, epoch, ep::DmaEngines::value_pointer(start), stream));
+    x.arm(slot, start);
     for (int r = 0; r < R; ++r) {
         if (r == me)
             continue;
         hsa_signal_t dn{};
-        if (!x.signal(*slot, 1, dn, err) ||
-            !x.dma.copy(x.dma.out_engine(), hout + r * block, true, blocks + r * block, false, (size_t)block, &start, 1,
-                        dn, err) ||
-            !x.dma.copy(x.dma.out_engine(), d->rs_out(buf) + r, true, ew, false, sizeof(uint32_t), &dn, 1, out_done,
-                        err))
+        if (!x.copy(slot, x.dma.out_engine(), hout + r * block, true, blocks + r * block, false, (size_t)block, &start,
+                    1, &dn, err) ||
+            !x.copy(slot, x.dma.out_engine(), d->rs_out(buf) + r, true, ew, false, sizeof(uint32_t), &dn, 1, nullptr,
+                    err))
             return fail(EP_ERR_HIP, "%s: %s", who, err.c_str());
         d->bytes_up += block;
         add_wait(waits, d->rs_out(buf) + r);
-        slot->finish.push_back({d->rs_out(buf) + r, epoch});
     }
 
     // ---- down: the blocks for this rank's shard (or their host-side sum)
@@ -464,26 +471,24 @@ extern "C" ep_status ep_reducescatter(ep_dense *d, int32_t buf, uint32_t epoch, 
     j.status = d->status();
     j.deadline = std::chrono::steady_clock::now() + std::chrono::microseconds(d->timeout_us);
     if (R > 1 && !reduce_on_host) {
-        if (!x.signal(*slot, R - 1, j.landed_done, err))
-            return fail(EP_ERR_HIP, "%s: %s", who, err.c_str());
         j.per_sender = d->mode & EP_MODE_PER_SENDER;
         for (int r = 0; r < R; ++r) {
             bl.ptr[bl.n++] = r == me ? blocks + me * block : din + r * block;  // summed in rank order
             if (r == me)
                 continue;
-            hsa_signal_t dn{};
-            if (!x.signal(*slot, 1, dn, err))
+            ep::InCopy c;
+            if (!x.in_copy(slot, d->rs_in(buf) + r, din + r * block, hin + r * block, block, d->rs_landed(buf) + r, c,
+                           err))
                 return fail(EP_ERR_HIP, "%s: %s", who, err.c_str());
-            j.copies.push_back({d->rs_in(buf) + r, din + r * block, hin + r * block, block, dn, d->rs_landed(buf) + r});
+            j.copies.push_back(c);
             add_wait(waits, d->rs_landed(buf) + r);
-            slot->finish.push_back({d->rs_landed(buf) + r, epoch});
             d->bytes_down += block;
         }
     } else if (R > 1) {
         // partial host reduction: once every remote block is in, the host sums them (fp32,
         // rank order) into this rank's own slot of the host buffer, which then goes down
-        hsa_signal_t dn{};
-        if (!x.signal(*slot, 1, j.landed_done, err) || !x.signal(*slot, 1, dn, err))
+        ep::InCopy own;
+        if (!x.in_copy(slot, nullptr, din + me * block, hin + me * block, block, d->rs_landed(buf) + me, own, err))
             return fail(EP_ERR_HIP, "%s: %s", who, err.c_str());
         j.per_sender = false;
         for (int r = 0; r < R; ++r)
@@ -528,17 +533,15 @@ extern "C" ep_status ep_reducescatter(ep_dense *d, int32_t buf, uint32_t epoch, 
             ep::trace_host("host_reduce",
                            std::chrono::duration<double, std::milli>(std::chrono::steady_clock::now() - t0).count());
         };
-        j.copies.push_back({nullptr, din + me * block, hin + me * block, block, dn, d->rs_landed(buf) + me});
+        j.copies.push_back(own);
         add_wait(waits, d->rs_landed(buf) + me);
-        slot->finish.push_back({d->rs_landed(buf) + me, epoch});
         d->bytes_down += block;
         bl.ptr[bl.n++] = blocks + me * block;
         bl.ptr[bl.n++] = din + me * block;
     } else {
         bl.ptr[bl.n++] = blocks;
     }
-    if (!j.copies.empty())
-        x.courier.post(std::move(j));
+    x.post(slot, std::move(j));
     EP_HIP(ep::launch_gate("wait_reducescatter", waits, stream));
     EP_HIP(ep::launch_block_reduce(bl, d->f32_blocks, T * d->hidden, out_dev, out_dtype == EP_OUT_F32, stream));
     return EP_OK;

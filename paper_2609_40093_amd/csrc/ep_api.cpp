@@ -603,6 +603,68 @@ extern "C" ep_status ep_staging_set_wait(ep_staging *s, int64_t timeout_us, int3
     return EP_OK;
 }
 
+namespace {
+
+// Names a flag word of a staging by its array, buffer set and index.
+struct StagingFlagNamer : ep::FlagNamer {
+    const ep_staging *s;
+    explicit StagingFlagNamer(const ep_staging *st) : s(st) {}
+    std::string operator()(const uint32_t *f) const override {
+        struct Arr {
+            const char *name, *index;
+            uint32_t *(ep_staging::*at)(int) const;
+            size_t len;
+        };
+        const size_t R = s->R();
+        const Arr arrs[] = {{"send_flags", "chunk", &ep_staging::send_flags, (size_t)s->max_chunks},
+                            {"recv_flags", "rank", &ep_staging::recv_flags, R},
+                            {"in_flags", "rank", &ep_staging::in_flags, R},
+                            {"ret_flags", "rank", &ep_staging::ret_flags, R},
+                            {"in_landed", "rank", &ep_staging::in_landed, R},
+                            {"recv_landed", "rank", &ep_staging::recv_landed, R},
+                            {"send_credits", "rank", &ep_staging::send_credit, R},
+                            {"recv_credit", "word", &ep_staging::recv_credit, 1}};
+        for (const Arr &a : arrs)
+            for (int b = 0; b < s->num_buffers; ++b) {
+                const uint32_t *base = (s->*a.at)(b);
+                if (f >= base && f < base + a.len) {
+                    char buf[96];
+                    std::snprintf(buf, sizeof buf, "%s[buf %d][%s %d]", a.name, b, a.index, (int)(f - base));
+                    return buf;
+                }
+            }
+        return "";
+    }
+};
+
+}  // namespace
+
+namespace ep {
+
+ep_status take_status(uint32_t *block, int64_t timeout_us, const FlagNamer &name_flag) {
+    const uint32_t word = __atomic_exchange_n(block, 0u, __ATOMIC_ACQ_REL);
+    if (word == 0)
+        return EP_OK;
+    uint32_t d[kStatusWords];
+    for (int i = 1; i < kStatusWords; ++i)
+        d[i] = __atomic_exchange_n(block + i, 0u, __ATOMIC_RELAXED);
+    if (word != EP_ERR_TIMEOUT)
+        return fail(EP_ERR_HIP, "unexpected staging status word %u", word);
+    const uint32_t *flag = reinterpret_cast<const uint32_t *>((uint64_t)d[2] | ((uint64_t)d[3] << 32));
+    std::string name = flag ? name_flag(flag) : std::string();
+    if (name.empty()) {
+        char buf[40];
+        std::snprintf(buf, sizeof buf, "the flag at %p", (const void *)flag);
+        name = buf;
+    }
+    return fail(EP_ERR_TIMEOUT,
+                "a completion-flag wait expired after %lld us: %s gave up on %s, which last read %u "
+                "(waited for %u)",
+                (long long)timeout_us, wait_site_name(d[1]), name.c_str(), d[4], d[5]);
+}
+
+}  // namespace ep
+
 extern "C" ep_status ep_staging_status(ep_staging *s, hipStream_t stream) {
     if (!s)
         return fail(EP_ERR_INVALID_ARG, "ep_staging_status: staging is NULL");
@@ -614,13 +676,7 @@ extern "C" ep_status ep_staging_status(ep_staging *s, hipStream_t stream) {
         if (side) EP_HIP(hipStreamSynchronize(side));
     if (!s->flags)
         return EP_OK;
-    const uint32_t word = __atomic_exchange_n(s->status(), 0u, __ATOMIC_ACQ_REL);
-    if (word == EP_ERR_TIMEOUT)
-        return fail(EP_ERR_TIMEOUT, "a completion-flag wait expired after %lld us",
-                    (long long)s->timeout_us);
-    if (word != 0)
-        return fail(EP_ERR_HIP, "unexpected staging status word %u", word);
-    return EP_OK;
+    return ep::take_status(s->status(), s->timeout_us, StagingFlagNamer(s));
 }
 
 // --------------------------------------------------------------- dispatch / combine
@@ -661,8 +717,7 @@ ep_status dispatch_default_legs(ep_staging *s, int32_t buf, uint32_t epoch, int6
             return fail(EP_ERR_TIMEOUT, "ep_dispatch: %s", err.c_str());
         EP_HIP(hipEventRecord(s->ev_sysrel, stream));
         EP_HIP(ep::launch_release_signal(round.start_value, stream));
-        if (!s->lane->submit(round, hdst, dsrc, bytes, s->chunk_bytes, s->send_flags(buf), s->epoch_word(buf),
-                             epoch, err))
+        if (!s->lane->submit(round, hdst, dsrc, bytes, s->chunk_bytes, s->send_flags(buf), s->epoch_word(buf), err))
             return fail(EP_ERR_HIP, "ep_dispatch: %s", err.c_str());
         const int64_t ticks = s->timeout_us * s->wall_clock_khz / 1000;
         EP_HIP(ep::launch_wait_flags("wait_d2h", s->send_flags(buf) + (chunks - 1), 1, epoch, ticks,

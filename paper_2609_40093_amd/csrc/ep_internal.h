@@ -4,6 +4,8 @@
 #include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 
+#include "status_block.h"
+
 #include <algorithm>
 #include <cstddef>
 #include <cstdint>
@@ -157,7 +159,8 @@ hipError_t launch_accumulate(const void *recv, const int32_t *slot_pos, const fl
                              float *acc, void *out, bool out_f32, int64_t max_rows, hipStream_t stream);
 
 // One lane per flag polls flags[i] until (int32)(flags[i] - epoch) >= 0, at most
-// timeout_ticks of the constant-rate wall clock; on expiry stores EP_ERR_TIMEOUT to *status.
+// timeout_ticks of the constant-rate wall clock; on expiry records the timeout in the
+// status block (kStatusWords words at `status`).
 hipError_t launch_wait_flags(const char *name, const uint32_t *flags, int32_t n, uint32_t epoch,
                              int64_t timeout_ticks, int32_t sleep_units, uint32_t *status,
                              hipStream_t stream);
@@ -176,7 +179,8 @@ struct GateArgs {
     uint32_t epoch = 0;
     int32_t sleep_units = 2;
     int64_t timeout_ticks = 0;
-    uint32_t *status = nullptr;
+    uint32_t *status = nullptr;  // status block (kStatusWords words)
+    uint32_t site = 0;           // set by launch_gate from its name
 };
 hipError_t launch_gate(const char *name, const GateArgs &g, hipStream_t stream);
 // Stores `epoch` into *epoch_word, then 0 into *value (a DMA start signal).

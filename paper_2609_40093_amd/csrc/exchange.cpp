@@ -79,9 +79,9 @@ ep_status wait_offsets(ep_staging *s, int b, uint32_t epoch, int64_t rows, const
     return EP_OK;
 }
 
-// Hands a call's inbound copies to the courier.
-void post_inbound(Exchange &x, const ep_staging *s, std::vector<InCopy> &&plan, uint32_t epoch, bool per_sender,
-                  hsa_signal_t start, const uint32_t *epoch_word, hsa_signal_t landed_done) {
+// Hands a call's inbound copies to the courier (which arms their signals in `slot`).
+void post_inbound(Exchange &x, int slot, const ep_staging *s, std::vector<InCopy> &&plan, uint32_t epoch,
+                  bool per_sender, hsa_signal_t start, const uint32_t *epoch_word) {
     if (plan.empty())
         return;
     InJob j;
@@ -90,10 +90,9 @@ void post_inbound(Exchange &x, const ep_staging *s, std::vector<InCopy> &&plan, 
     j.per_sender = per_sender;
     j.start = start;
     j.epoch_word = epoch_word;
-    j.landed_done = landed_done;
     j.status = s->status();
     j.deadline = std::chrono::steady_clock::now() + std::chrono::microseconds(s->timeout_us);
-    x.courier.post(std::move(j));
+    x.post(slot, std::move(j));
 }
 
 struct Batch {
@@ -115,9 +114,9 @@ void init_gate(GateArgs &g, const ep_staging *s, uint32_t epoch) {
 }
 
 // Flag copy: *flag = epoch (read from the device epoch word) on `engine` after `deps`.
-bool flag_copy(Exchange &x, uint32_t engine, uint32_t *flag, const uint32_t *epoch_word, const hsa_signal_t *deps,
-               int ndeps, hsa_signal_t done, std::string &err) {
-    return x.dma.copy(engine, flag, true, epoch_word, false, sizeof(uint32_t), deps, ndeps, done, err);
+bool flag_copy(Exchange &x, int slot, uint32_t engine, uint32_t *flag, const uint32_t *epoch_word,
+               const hsa_signal_t *deps, int ndeps, std::string &err) {
+    return x.copy(slot, engine, flag, true, epoch_word, false, sizeof(uint32_t), deps, ndeps, nullptr, err);
 }
 
 }  // namespace
@@ -164,8 +163,8 @@ ep_status exchange_dispatch(ep_staging *s, int b, uint32_t epoch, int64_t rows, 
                         (long long)off[R], (long long)s->max_rows);
     }
 
-    XSlot *slot = x.begin(s->timeout_us, err);
-    if (!slot)
+    const int slot = x.begin(s->timeout_us, err);
+    if (slot < 0)
         return fail(EP_ERR_TIMEOUT, "%s: %s", who, err.c_str());
     const uint32_t *ew = s->epoch_word(b);
     char *dsend = static_cast<char *>(s->dev_send[b]);
@@ -174,10 +173,11 @@ ep_status exchange_dispatch(ep_staging *s, int b, uint32_t epoch, int64_t rows, 
     // ---- outbound: packed rows -> host send buffer, chunk flags (own segment skipped in
     //      remote-only mode; its chunks' flags are raised all the same)
     hsa_signal_t start{};
-    if (!x.signal(*slot, 1, start, err))
+    if (!x.start_signal(slot, start, err))
         return fail(EP_ERR_HIP, "%s: %s", who, err.c_str());
     EP_HIP(hipEventRecord(s->ev_sysrel, stream));
     EP_HIP(launch_release_signal(DmaEngines::value_pointer(start), stream));
+    x.arm(slot, start);
     const int64_t bytes = rows * rb, chunk = s->chunk_bytes;
     const int64_t chunks = (bytes + chunk - 1) / chunk;
     std::vector<std::pair<int64_t, int64_t>> ranges;
@@ -190,9 +190,6 @@ ep_status exchange_dispatch(ep_staging *s, int b, uint32_t epoch, int64_t rows, 
     Batch bt;
     init_gate(bt.waits, s, epoch);
     if (chunks > 0) {
-        hsa_signal_t flags_done{};
-        if (!x.signal(*slot, chunks, flags_done, err))
-            return fail(EP_ERR_HIP, "%s: %s", who, err.c_str());
         const uint32_t out = x.dma.out_engine();
         for (int64_t c = 0; c < chunks; ++c) {
             const int64_t lo = c * chunk, hi = std::min(bytes, lo + chunk);
@@ -202,17 +199,14 @@ ep_status exchange_dispatch(ep_staging *s, int b, uint32_t epoch, int64_t rows, 
                 const int64_t a = std::max(rg.first, lo), e = std::min(rg.second, hi);
                 if (a >= e)
                     continue;
-                hsa_signal_t d{};
-                if (!x.signal(*slot, 1, d, err) ||
-                    !x.dma.copy(out, hsend + a, true, dsend + a, false, (size_t)(e - a), &start, 1, d, err))
+                if (!x.copy(slot, out, hsend + a, true, dsend + a, false, (size_t)(e - a), &start, 1, &deps[nd], err))
                     return fail(EP_ERR_HIP, "%s: %s", who, err.c_str());
-                deps[nd++] = d;
+                ++nd;
             }
-            if (!flag_copy(x, out, s->send_flags(b) + c, ew, deps, nd ? nd : 1, flags_done, err))
+            if (!flag_copy(x, slot, out, s->send_flags(b) + c, ew, deps, nd ? nd : 1, err))
                 return fail(EP_ERR_HIP, "%s: %s", who, err.c_str());
         }
         bt.add_wait(s->send_flags(b) + (chunks - 1));
-        slot->finish.push_back({s->send_flags(b) + (chunks - 1), epoch});
     }
 
     // ---- inbound (duplex): every sender's rows -> dev_in on the inbound engine, each
@@ -220,12 +214,6 @@ ep_status exchange_dispatch(ep_staging *s, int b, uint32_t epoch, int64_t rows, 
     if (duplex) {
         char *din = static_cast<char *>(s->dev_in[b]);
         char *hin = static_cast<char *>(s->host_in[b]);
-        int copies = 0;
-        for (int r = 0; r < R; ++r)
-            copies += rin[r] > 0 && !(r == me && remote_only);
-        hsa_signal_t landed_done{};
-        if (copies > 0 && !x.signal(*slot, copies, landed_done, err))
-            return fail(EP_ERR_HIP, "%s: %s", who, err.c_str());
         std::vector<InCopy> plan;
         for (int r = 0; r < R; ++r) {
             if (rin[r] == 0)
@@ -239,14 +227,13 @@ ep_status exchange_dispatch(ep_staging *s, int b, uint32_t epoch, int64_t rows, 
             // own segment: back from the host send buffer once its last chunk's flag is up
             const uint32_t *ready = r == me ? s->send_flags(b) + ((ro[me + 1] * rb - 1) / chunk) : s->in_flags(b) + r;
             const char *src = r == me ? hsend + ro[me] * rb : hin + off[r] * rb;
-            hsa_signal_t d{};
-            if (!x.signal(*slot, 1, d, err))
+            InCopy c;
+            if (!x.in_copy(slot, ready, dst, src, len, s->in_landed(b) + r, c, err))
                 return fail(EP_ERR_HIP, "%s: %s", who, err.c_str());
-            plan.push_back({ready, dst, src, len, d, s->in_landed(b) + r});
+            plan.push_back(c);
             bt.add_wait(s->in_landed(b) + r);
-            slot->finish.push_back({s->in_landed(b) + r, epoch});
         }
-        post_inbound(x, s, std::move(plan), epoch, per_sender, start, ew, landed_done);
+        post_inbound(x, slot, s, std::move(plan), epoch, per_sender, start, ew);
         s->in_epoch[(size_t)b] = epoch;
     }
     EP_HIP(launch_gate("wait_dispatch", bt.waits, stream));
@@ -281,8 +268,8 @@ ep_status exchange_combine(ep_staging *s, int b, uint32_t epoch, int64_t rows, c
                     "on the same buffer set", who, epoch);
     Exchange &x = *s->xchg;
     std::string err;
-    XSlot *slot = x.begin(s->timeout_us, err);
-    if (!slot)
+    const int slot = x.begin(s->timeout_us, err);
+    if (slot < 0)
         return fail(EP_ERR_TIMEOUT, "%s: %s", who, err.c_str());
     uint32_t *ew = s->epoch_word(b);
     char *din = static_cast<char *>(s->dev_in[b]);
@@ -293,45 +280,32 @@ ep_status exchange_combine(ep_staging *s, int b, uint32_t epoch, int64_t rows, c
     // the flag copies of this call read the epoch word: stamp it, then start the
     // outbound copies (after a system-scope release of the expert results in dev_in)
     hsa_signal_t start{};
-    if (!x.signal(*slot, 1, start, err))
+    if (!x.start_signal(slot, start, err))
         return fail(EP_ERR_HIP, "%s: %s", who, err.c_str());
     EP_HIP(hipEventRecord(s->ev_sysrel, stream));
     EP_HIP(launch_stamp_release(ew, epoch, DmaEngines::value_pointer(start), stream));
+    x.arm(slot, start);
     Batch bt;
     init_gate(bt.waits, s, epoch);
 
     // ---- outbound (duplex): this rank's results for sender r's rows -> host_ret
     if (duplex) {
-        int copies = 0;
-        for (int r = 0; r < R; ++r)
-            copies += rin[r] > 0 && !(r == me && remote_only);
-        hsa_signal_t ret_done{};
-        if (copies > 0 && !x.signal(*slot, copies, ret_done, err))
-            return fail(EP_ERR_HIP, "%s: %s", who, err.c_str());
         const uint32_t out = x.dma.out_engine();
         for (int r = 0; r < R; ++r) {
             if (rin[r] == 0 || (r == me && remote_only))
                 continue;
             hsa_signal_t d{};
-            if (!x.signal(*slot, 1, d, err) ||
-                !x.dma.copy(out, hret + off[r] * rb, true, din + off[r] * rb, false, (size_t)(rin[r] * rb), &start, 1,
-                            d, err) ||
-                !flag_copy(x, out, s->ret_flags(b) + r, ew, &d, 1, ret_done, err))
+            if (!x.copy(slot, out, hret + off[r] * rb, true, din + off[r] * rb, false, (size_t)(rin[r] * rb), &start,
+                        1, &d, err) ||
+                !flag_copy(x, slot, out, s->ret_flags(b) + r, ew, &d, 1, err))
                 return fail(EP_ERR_HIP, "%s: %s", who, err.c_str());
             bt.add_wait(s->ret_flags(b) + r);
-            slot->finish.push_back({s->ret_flags(b) + r, epoch});
         }
     }
 
     // ---- inbound: sender r's returned rows for this rank's segment r -> dev_recv, on the
     //      inbound engine as each sender's flag arrives (the courier)
     uint32_t base = 0;  // senders whose rows need no wait: none, or copied inside HBM
-    int copies = 0;
-    for (int r = 0; r < R; ++r)
-        copies += ro[r + 1] > ro[r] && !(r == me && remote_only);
-    hsa_signal_t landed_done{};
-    if (copies > 0 && !x.signal(*slot, copies, landed_done, err))
-        return fail(EP_ERR_HIP, "%s: %s", who, err.c_str());
     std::vector<InCopy> plan;
     for (int r = 0; r < R; ++r) {
         const int64_t n = ro[r + 1] - ro[r];
@@ -348,15 +322,14 @@ ep_status exchange_combine(ep_staging *s, int b, uint32_t epoch, int64_t rows, c
         const bool own_dup = r == me && duplex;  // own results come back from host_ret
         const uint32_t *ready = own_dup ? s->ret_flags(b) + me : s->recv_flags(b) + r;
         const char *src = own_dup ? hret + off[me] * rb : hrecv + ro[r] * rb;
-        hsa_signal_t d{};
-        if (!x.signal(*slot, 1, d, err))
+        InCopy c;
+        if (!x.in_copy(slot, ready, dst, src, n * rb, s->recv_landed(b) + r, c, err))
             return fail(EP_ERR_HIP, "%s: %s", who, err.c_str());
-        plan.push_back({ready, dst, src, n * rb, d, s->recv_landed(b) + r});
+        plan.push_back(c);
         if (!acc)
             bt.add_wait(s->recv_landed(b) + r);
-        slot->finish.push_back({s->recv_landed(b) + r, epoch});
     }
-    post_inbound(x, s, std::move(plan), epoch, per_sender, start, ew, landed_done);
+    post_inbound(x, slot, s, std::move(plan), epoch, per_sender, start, ew);
     if (!acc) {
         EP_HIP(launch_gate("wait_combine", bt.waits, stream));
         return EP_OK;

@@ -5,6 +5,8 @@
 
 #include "ep.h"
 #include "sdma.h"
+#include "signal_slots.h"
+#include "status_block.h"
 
 #include <immintrin.h>
 
@@ -20,17 +22,9 @@
 
 namespace ep {
 
-// Signals and completion flags of one call (a dispatch or a combine).  A slot is reused
-// only once every flag its previous call raised holds that call's epoch, i.e. once every
-// copy of that call has landed and no engine still polls one of its signals.
-struct XSlot {
-    std::vector<hsa_signal_t> sigs;
-    size_t used = 0;
-    std::vector<std::pair<const uint32_t *, uint32_t>> finish;
-};
-
 // One host->device copy of a sender's rows: queued once *ready holds the epoch, then a
-// 4-byte copy of the epoch into *landed.
+// 4-byte copy of the epoch into *landed.  Each of the two copies has its own completion
+// signal (done, landed_done), armed in the call's signal slot when the job is posted.
 struct InCopy {
     const uint32_t *ready;
     char *dst;
@@ -38,6 +32,7 @@ struct InCopy {
     int64_t len;
     hsa_signal_t done;
     uint32_t *landed;
+    hsa_signal_t landed_done;
 };
 
 // The host->device copies of one call.  They all go to the one inbound engine and all
@@ -50,7 +45,6 @@ struct InJob {
     bool per_sender = false;
     hsa_signal_t start{};
     const uint32_t *epoch_word = nullptr;
-    hsa_signal_t landed_done{};
     uint32_t *status = nullptr;
     std::chrono::steady_clock::time_point deadline;
 };
@@ -63,6 +57,11 @@ struct InJob {
 // engine, a copy is queued only once its sender's flag (host memory, read without a PCIe
 // round trip) holds the epoch.  With the all-senders policy a call's copies are queued
 // together when the last flag is in.
+// Jobs are served strictly in the order they were posted: no copy of a call is queued
+// before every copy of the calls posted earlier.  A call's copies wait for its start
+// signal, which the caller's stream releases only after the earlier calls' copies have
+// landed; a copy queued ahead of them on the in-order engine would wait for a release that
+// cannot come until the copies behind it have run.
 class Courier {
 public:
     void start(DmaEngines *dma) {
@@ -103,12 +102,18 @@ private:
         return !f || (int32_t)(__atomic_load_n(f, __ATOMIC_ACQUIRE) - j.epoch) >= 0;
     }
     static bool ready(const InJob &j, const InCopy &c) { return flag_ready(j, c.ready); }
+    // A copy that cannot be submitted gets its completion signal stored 0 by the host, so
+    // that nothing waits for it (the staging's status records the failure).
     bool submit(InJob &j, const InCopy &c) {
         std::string err;
         const uint32_t eng = dma_->in_engine(0);
-        if (dma_->copy(eng, c.dst, false, c.src, true, (size_t)c.len, &j.start, 1, c.done, err) &&
-            dma_->copy(eng, c.landed, true, j.epoch_word, false, sizeof(uint32_t), &c.done, 1, j.landed_done, err))
+        const bool data = dma_->copy(eng, c.dst, false, c.src, true, (size_t)c.len, &j.start, 1, c.done, err);
+        if (!data)
+            hsa_signal_store_screlease(c.done, 0);
+        if (data && dma_->copy(eng, c.landed, true, j.epoch_word, false, sizeof(uint32_t), &c.done, 1, c.landed_done,
+                               err))
             return true;
+        hsa_signal_store_screlease(c.landed_done, 0);
         __atomic_store_n(j.status, (uint32_t)EP_ERR_HIP, __ATOMIC_RELEASE);
         return false;
     }
@@ -126,7 +131,7 @@ private:
             if (late)
                 for (const uint32_t *f : j.ready_all)
                     if (!flag_ready(j, f))
-                        __atomic_store_n(j.status, (uint32_t)EP_ERR_TIMEOUT, __ATOMIC_RELEASE);
+                        record_host_timeout(j.status, kSiteCourier, f, j.epoch);
             if (j.before_copies)
                 j.before_copies();
             j.before_copies = nullptr;
@@ -134,7 +139,7 @@ private:
         for (size_t i = 0; i < j.copies.size();) {
             if (late || (j.per_sender ? ready(j, j.copies[i]) : all)) {
                 if (late && !ready(j, j.copies[i]))
-                    __atomic_store_n(j.status, (uint32_t)EP_ERR_TIMEOUT, __ATOMIC_RELEASE);
+                    record_host_timeout(j.status, kSiteCourier, j.copies[i].ready, j.epoch);
                 submit(j, j.copies[i]);  // queued even when late, so no wait on the device hangs
                 j.copies.erase(j.copies.begin() + (std::ptrdiff_t)i);
             } else {
@@ -157,12 +162,9 @@ private:
                 continue;
             }
             lk.unlock();
-            for (size_t i = 0; i < active_.size();) {
-                if (progress(active_[i]))
-                    active_.erase(active_.begin() + (std::ptrdiff_t)i);
-                else
-                    ++i;
-            }
+            // the oldest job first; a later one only once the earlier ones are all queued
+            while (!active_.empty() && progress(active_.front()))
+                active_.erase(active_.begin());
             for (int p = 0; p < 64; ++p)
                 _mm_pause();
             lk.lock();
@@ -182,76 +184,71 @@ class Exchange {
 public:
     DmaEngines dma;
     Courier courier;
+    SignalSlots slots;
 
     bool init(int device, int nslots, std::string &err) {
         if (!dma.init(device, err))
             return false;
-        slots_.resize((size_t)nslots);
+        slots.init(nslots);
         courier.start(&dma);
         return true;
     }
+    // The same on engines chosen by the caller.
+    void init_with(hsa_agent_t gpu, hsa_agent_t cpu, uint32_t out, const std::vector<uint32_t> &in, int nslots) {
+        dma.init_with(gpu, cpu, out, in);
+        slots.init(nslots);
+        courier.start(&dma);
+    }
 
-    // Waits (bounded) for every copy of every slot to land, then frees the signals.  Call
-    // it after the streams that start the copies have run and before freeing the buffers
-    // the copies touch.
+    // Queues every copy the courier still holds, waits (bounded) for every copy of every
+    // call to land, then frees the signals (or leaves them allocated if one did not land:
+    // an engine may still decrement it).  Call it after the streams that release the
+    // calls' start signals have run and before freeing the buffers the copies touch.
     void release() {
         courier.stop();
-        const auto t0 = std::chrono::steady_clock::now();
-        bool drained = true;
-        uint32_t spins = 0;
-        for (XSlot &s : slots_)
-            for (const auto &f : s.finish)
-                while (drained && (int32_t)(__atomic_load_n(f.first, __ATOMIC_ACQUIRE) - f.second) < 0)
-                    if (++spins % 1024 == 0) {
-                        std::this_thread::yield();
-                        drained = std::chrono::steady_clock::now() - t0 < std::chrono::microseconds(kReleaseDrainUs);
-                    }
-        if (drained)  // otherwise a copy may still wait on these signals: keep them alive
-            for (XSlot &s : slots_)
-                for (hsa_signal_t g : s.sigs)
-                    hsa_signal_destroy(g);
-        slots_.clear();
+        std::string err;
+        slots.destroy(slots.drain(kReleaseDrainUs, err));
         dma.release();
     }
 
-    XSlot *begin(int64_t timeout_us, std::string &err) {
-        XSlot &s = slots_[(size_t)next_];
-        const auto t0 = std::chrono::steady_clock::now();
-        uint32_t spins = 0;
-        for (const auto &f : s.finish) {
-            while ((int32_t)(__atomic_load_n(f.first, __ATOMIC_ACQUIRE) - f.second) < 0) {
-                _mm_pause();
-                if (++spins % 1024 == 0) {
-                    std::this_thread::yield();
-                    if (std::chrono::steady_clock::now() - t0 > std::chrono::microseconds(timeout_us)) {
-                        err = "the host legs of an earlier round did not finish";
-                        return nullptr;
-                    }
-                }
-            }
-        }
-        s.finish.clear();
-        s.used = 0;
-        next_ = (next_ + 1) % (int)slots_.size();
-        return &s;
-    }
+    // Reserves the signal slot of a call (see SignalSlots::begin); -1 with err on timeout.
+    int begin(int64_t timeout_us, std::string &err) { return slots.begin(timeout_us, err); }
 
-    // A signal of this call with the given initial value (reset if reused).
-    bool signal(XSlot &s, int64_t initial, hsa_signal_t &out, std::string &err) {
-        if (s.used == s.sigs.size()) {
-            hsa_signal_t g{};
-            if (!dma.make_signal(g, err))
-                return false;
-            s.sigs.push_back(g);
-        }
-        out = s.sigs[s.used++];
-        hsa_signal_store_relaxed(out, initial);
+    // A start signal of call `slot` (value 1; the caller's stream stores 0 into it).  Arm it
+    // once the kernel that releases it has been enqueued.
+    bool start_signal(int slot, hsa_signal_t &out, std::string &err) { return slots.take(slot, out, err); }
+    void arm(int slot, hsa_signal_t g) { slots.arm(slot, g); }
+
+    // One copy of call `slot` with a completion signal of its own (returned in *done when
+    // non-null), armed once submitted.
+    bool copy(int slot, uint32_t engine, void *dst, bool dst_host, const void *src, bool src_host, size_t len,
+              const hsa_signal_t *deps, int ndeps, hsa_signal_t *done, std::string &err) {
+        hsa_signal_t g{};
+        if (!slots.take(slot, g, err) || !dma.copy(engine, dst, dst_host, src, src_host, len, deps, ndeps, g, err))
+            return false;
+        slots.arm(slot, g);
+        if (done)
+            *done = g;
         return true;
     }
 
-private:
-    std::vector<XSlot> slots_;
-    int next_ = 0;
+    // An inbound copy of call `slot` for the courier: its two completion signals.
+    bool in_copy(int slot, const uint32_t *ready, char *dst, const char *src, int64_t len, uint32_t *landed,
+                 InCopy &out, std::string &err) {
+        out = InCopy{ready, dst, src, len, {}, landed, {}};
+        return slots.take(slot, out.done, err) && slots.take(slot, out.landed_done, err);
+    }
+    // Hands a call's inbound copies to the courier and arms their signals (the courier
+    // submits every copy it is given, or stores 0 into the signals of one it cannot).
+    void post(int slot, InJob &&j) {
+        if (j.copies.empty())
+            return;
+        for (const InCopy &c : j.copies) {
+            slots.arm(slot, c.done);
+            slots.arm(slot, c.landed_done);
+        }
+        courier.post(std::move(j));
+    }
 };
 
 }  // namespace ep

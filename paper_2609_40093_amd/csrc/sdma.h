@@ -1,17 +1,23 @@
-// sdma.h -- device->host leg on one SDMA engine, driven through the ROCr runtime.
+// sdma.h -- device<->host legs on SDMA engines, driven through the ROCr runtime.
 //
 // The HIP runtime may run a device->host hipMemcpyAsync as a copy kernel on the compute
-// units; this lane submits the leg to a chosen SDMA engine instead (Sec. 4.3 of the
+// units; these classes submit the legs to chosen SDMA engines instead (Sec. 4.3 of the
 // paper: bulk data moves on DMA engines so that no compute unit is spent on it).
 //
-// Ordering, per round:
+// SdmaLane (the default device->host leg), per round:
 //   stream:  pack kernel -> event with system-scope release (every XCD's L2 written
 //            back) -> 1-wave kernel storing 0 into the round's start signal
-//   SDMA:    [poll start signal == 0] copy chunk 0 -> [poll chunk 0 done] copy epoch word
+//   SDMA:    [poll start == 0] copy chunk 0 -> [poll chunk 0 done] copy epoch word
 //            -> send flag 0 -> copy chunk 1 -> ... (one engine, in order)
 //   stream:  bounded wait until the last chunk's flag holds the epoch
-// Signals of a round are reused only once that round's last flag is seen on the host.
+// Every copy has a completion signal of its own, and a round's signals are reused only
+// once each of them reads 0 (signal_slots.h).
+//
+// Agent discovery needs the HIP runtime (sdma.cpp); everything else uses only ROCr
+// (sdma_lane.cpp), and init_with() takes agents and engines found elsewhere.
 #pragma once
+
+#include "signal_slots.h"
 
 #include <hsa/hsa.h>
 #include <hsa/hsa_ext_amd.h>
@@ -25,58 +31,61 @@ namespace ep {
 // Longest a release waits for copies still in flight before it frees their signals.
 constexpr int64_t kReleaseDrainUs = 5ll * 1000 * 1000;
 
+// The ROCr GPU agent of HIP device `device` (matched by PCI location) and its nearest CPU
+// agent.  Takes a ROCr reference (hsa_init) that the caller drops with hsa_shut_down.
+bool find_agents(int device, hsa_agent_t &gpu, hsa_agent_t &cpu, std::string &err);
+
 class SdmaLane {
 public:
     // Finds the GPU agent of HIP device `device`, its nearest CPU agent and a free SDMA
     // engine for device->host copies.  Returns false with `err` set on failure.
     bool init(int device, int slots, std::string &err);
+    // The same with agents and an engine chosen by the caller (engine 0: the runtime
+    // picks); takes no ROCr reference.
+    void init_with(hsa_agent_t gpu, hsa_agent_t cpu, uint32_t engine, int slots);
+    // Waits (bounded) for every copy in flight, then frees the signals (or leaves them
+    // allocated if a copy did not land in time).
     void release();
 
     struct Round {
+        hsa_signal_t start{};             // released by the stream (value pointer below)
         int64_t *start_value = nullptr;  // device-writable value of the start signal
         int slot = -1;
     };
-    // Reserves a slot whose previous round has finished (its last flag reached its epoch),
-    // waiting on the host for at most timeout_us.  Resets the slot's start signal.
+    // Reserves a slot whose previous round has fully retired (every completion signal at
+    // 0), waiting on the host for at most timeout_us, and takes its start signal.
     bool begin(Round &r, int64_t timeout_us, std::string &err);
-    // Submits the chunk copies and the flag copies of a round (after the stream work that
-    // releases the start signal has been enqueued).
+    // Submits the chunk copies and the flag copies of a round.  Call it after the stream
+    // work that stores 0 into r.start has been enqueued.
     bool submit(const Round &r, void *host_dst, const void *dev_src, int64_t bytes, int64_t chunk_bytes,
-                uint32_t *flags, const uint32_t *epoch_word, uint32_t epoch, std::string &err);
-    // Waits on the host (at most timeout_us in all) until every submitted round's last flag
-    // holds its epoch, i.e. until no copy of this lane is still in flight.  Call it after
-    // the streams that release the rounds' start signals have run, before freeing the
-    // buffers the copies touch.  Returns false if a round did not finish in time.
-    bool drain(int64_t timeout_us);
+                uint32_t *flags, const uint32_t *epoch_word, std::string &err);
+    // Waits on the host (at most timeout_us in all) until every submitted copy has
+    // landed.  Call it after the streams that release the rounds' start signals have run.
+    bool drain(int64_t timeout_us, std::string &err);
 
     const char *engine_name() const { return engine_name_.c_str(); }
 
 private:
-    struct Slot {
-        hsa_signal_t start{};
-        std::vector<hsa_signal_t> done;  // one per chunk, grown on demand
-        volatile uint32_t *last_flag = nullptr;
-        uint32_t epoch = 0;
-        bool busy = false;
-    };
-    bool ensure_done_signals(Slot &s, int64_t n, std::string &err);
+    bool copy(int slot, void *dst, const void *src, size_t len, const hsa_signal_t *dep, hsa_signal_t *done,
+              std::string &err);
 
     hsa_agent_t gpu_{}, cpu_{};
     uint32_t engine_ = 0;  // hsa_amd_sdma_engine_id_t bit, 0 = let the runtime choose
     std::string engine_name_;
-    std::vector<Slot> slots_;
-    int next_ = 0;
-    bool ready_ = false;
+    SignalSlots slots_;
+    bool ready_ = false, owns_rocr_ = false;
 };
 
-// SDMA engines of one GPU for the exchange legs (device->host and host->device), driven
-// through ROCr.  Copies run on an engine named by its id bit, after dependency signals
-// reach 0, and decrement a completion signal when they land.  One engine carries the
-// device->host direction and the first other engine the host->device direction (the
-// callers queue every inbound copy on that one engine).
+// SDMA engines of one GPU for the exchange legs (device->host and host->device).  Copies
+// run on an engine named by its id bit, after dependency signals reach 0, and decrement
+// their completion signal when they land.  One engine carries the device->host direction
+// and the first other engine the host->device direction (the callers queue every inbound
+// copy on that one engine).
 class DmaEngines {
 public:
     bool init(int device, std::string &err);
+    // Agents and engines chosen by the caller (no ROCr reference taken).
+    void init_with(hsa_agent_t gpu, hsa_agent_t cpu, uint32_t out_engine, const std::vector<uint32_t> &in_engines);
     void release();
 
     uint32_t out_engine() const { return out_; }
@@ -85,20 +94,17 @@ public:
     int in_engines() const { return (int)in_.size(); }
     const std::string &describe() const { return desc_; }
 
-    // A GPU-only signal with value 1 (the device stores 0 into it to start a copy, or a
-    // copy decrements it when it lands).
-    bool make_signal(hsa_signal_t &sig, std::string &err);
     static int64_t *value_pointer(hsa_signal_t sig);
     // One copy of len bytes; dst_host / src_host say which side is pinned host memory.
     bool copy(uint32_t engine, void *dst, bool dst_host, const void *src, bool src_host, size_t len,
-              const hsa_signal_t *deps, int ndeps, hsa_signal_t done, std::string &err);
+              const hsa_signal_t *deps, int ndeps, hsa_signal_t done, std::string &err) const;
 
 private:
     hsa_agent_t gpu_{}, cpu_{};
     uint32_t out_ = 0;
     std::vector<uint32_t> in_;
     std::string desc_;
-    bool ready_ = false;
+    bool ready_ = false, owns_rocr_ = false;
 };
 
 }  // namespace ep

@@ -9,8 +9,9 @@
 // wait_flags_kernel: one lane per remote sender polls its flag with system-scope loads
 // (they bypass the GPU caches and cross PCIe) and sleeps between polls, instead of a
 // large thread block spinning.  The wait is bounded by the constant-rate wall clock; on
-// expiry the kernel records a timeout in the host status word and exits, so the stream
-// never hangs on a flag that does not come.
+// expiry the kernel records the timeout in the host status block (where it waited, the
+// flag, the value it last read and the value it wanted) and exits, so the stream never
+// hangs on a flag that does not come.
 #include "ep_internal.h"
 
 namespace ep {
@@ -18,24 +19,46 @@ namespace {
 
 constexpr uint32_t kStatusTimeout = 5u;  // EP_ERR_TIMEOUT
 
+// Records an expired wait in the status block: the details first, then the status word
+// with release order (one lane per wave calls it).
+__device__ void record_timeout(uint32_t *status, uint32_t site, const uint32_t *flag, uint32_t seen, uint32_t want) {
+    const uint64_t a = reinterpret_cast<uint64_t>(flag);
+    __hip_atomic_store(status + 1, site, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+    __hip_atomic_store(status + 2, (uint32_t)a, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+    __hip_atomic_store(status + 3, (uint32_t)(a >> 32), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+    __hip_atomic_store(status + 4, seen, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+    __hip_atomic_store(status + 5, want, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+    __hip_atomic_store(status, kStatusTimeout, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_SYSTEM);
+}
+
+// The lowest lane of the wave for which `pending` holds (-1 if none).
+__device__ inline int first_lane(bool pending) {
+    const uint64_t m = __ballot(pending);
+    return m ? __builtin_ctzll(m) : -1;
+}
+
 __global__ __launch_bounds__(64) void wait_flags_kernel(const uint32_t *flags, int32_t n,
                                                         uint32_t epoch, int64_t timeout_ticks,
-                                                        int32_t sleep_units, uint32_t *status) {
+                                                        int32_t sleep_units, uint32_t *status, uint32_t site) {
     const int32_t i = blockIdx.x * blockDim.x + threadIdx.x;
-    if (i >= n)
-        return;
+    bool done = i >= n;
+    uint32_t seen = 0;
     const int64_t t0 = wall_clock64();
-    for (;;) {
-        const uint32_t f = __hip_atomic_load(flags + i, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_SYSTEM);
-        if ((int32_t)(f - epoch) >= 0)
-            break;
+    bool late = false;
+    while (!__all(done)) {
+        if (!done) {
+            seen = __hip_atomic_load(flags + i, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_SYSTEM);
+            done = (int32_t)(seen - epoch) >= 0;
+        }
         if (wall_clock64() - t0 > timeout_ticks) {
-            __hip_atomic_store(status, kStatusTimeout, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+            late = true;
             break;
         }
         for (int32_t s = 0; s < sleep_units; ++s)
             __builtin_amdgcn_s_sleep(1);
     }
+    if (late && (int)threadIdx.x == first_lane(!done))
+        record_timeout(status, site, flags + i, seen, epoch);
 }
 
 // Releases a DMA-engine dependency: stores 0 into a signal value the engine polls.
@@ -54,12 +77,13 @@ __global__ __launch_bounds__(64) void gate_kernel(GateArgs g) {
     const int i = threadIdx.x;
     bool done = i >= g.n;
     bool released = done || g.all || !g.release[i];
+    uint32_t seen = 0;
     const int64_t t0 = wall_clock64();
     bool late = false;
     while (!__all(done)) {
         if (!done) {
-            const uint32_t f = __hip_atomic_load(g.flag[i], __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_SYSTEM);
-            if ((int32_t)(f - g.epoch) >= 0) {
+            seen = __hip_atomic_load(g.flag[i], __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_SYSTEM);
+            if ((int32_t)(seen - g.epoch) >= 0) {
                 done = true;
                 if (!released) {
                     __hip_atomic_store(g.release[i], (int64_t)0, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_SYSTEM);
@@ -75,8 +99,8 @@ __global__ __launch_bounds__(64) void gate_kernel(GateArgs g) {
             __builtin_amdgcn_s_sleep(1);
     }
     if (late) {
-        if (i == 0)
-            __hip_atomic_store(g.status, kStatusTimeout, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+        if (i == first_lane(!done))
+            record_timeout(g.status, g.site, g.flag[i], seen, g.epoch);
         if (!released)
             __hip_atomic_store(g.release[i], (int64_t)0, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_SYSTEM);
     }
@@ -112,24 +136,29 @@ __global__ __launch_bounds__(64) void round_advance_kernel(uint32_t *round) {
 // per flag, pausing between polls, bounded by the wall clock).
 __global__ __launch_bounds__(64) void round_gate_kernel(const uint32_t *round_ptr, const uint32_t *flags,
                                                         int32_t stride, int32_t n, int32_t delta, int64_t timeout_ticks,
-                                                        int32_t sleep_units, uint32_t *status) {
+                                                        int32_t sleep_units, uint32_t *status, uint32_t site) {
     const int32_t i = threadIdx.x;
-    if (i >= n)
-        return;
     const uint32_t round = __hip_atomic_load(round_ptr, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     const uint32_t want = round + (uint32_t)delta;
     const uint32_t *f = flags + (round & 1u) * (uint32_t)stride + i;
+    bool done = i >= n;
+    uint32_t seen = 0;
     const int64_t t0 = wall_clock64();
-    for (;;) {
-        if ((int32_t)(__hip_atomic_load(f, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_SYSTEM) - want) >= 0)
-            break;
+    bool late = false;
+    while (!__all(done)) {
+        if (!done) {
+            seen = __hip_atomic_load(f, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_SYSTEM);
+            done = (int32_t)(seen - want) >= 0;
+        }
         if (wall_clock64() - t0 > timeout_ticks) {
-            __hip_atomic_store(status, kStatusTimeout, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+            late = true;
             break;
         }
         for (int32_t s = 0; s < sleep_units; ++s)
             __builtin_amdgcn_s_sleep(1);
     }
+    if (late && i == first_lane(!done))
+        record_timeout(status, site, f, seen, want);
 }
 
 // Publishes the round: after a system-scope release, words[(round % 2) * stride + i] =
@@ -170,8 +199,10 @@ __global__ __launch_bounds__(64) void landed_set_kernel(const uint32_t *landed, 
         if (m != start || m == full)
             break;
         if (wall_clock64() - t0 > timeout_ticks) {
-            if (lane == 0)
-                __hip_atomic_store(status, kStatusTimeout, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+            const bool missing = lane < R && !((m >> lane) & 1u);
+            if (lane == first_lane(missing))
+                record_timeout(status, kSiteLandedSet, landed + lane,
+                               __hip_atomic_load(landed + lane, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM), epoch);
             m = full;
             break;
         }
@@ -222,7 +253,7 @@ hipError_t launch_round_gate(const char *name, const uint32_t *round, const uint
     (void)hipGetLastError();
     TraceSlot ts = trace_acquire();
     hipExtLaunchKernelGGL(round_gate_kernel, dim3(1), dim3(64), 0, stream, ts.start, ts.stop, 0, round, flags, stride,
-                          n, delta, timeout_ticks, sleep_units, status);
+                          n, delta, timeout_ticks, sleep_units, status, wait_site(name));
     hipError_t err = hipGetLastError();
     if (err == hipSuccess)
         trace_submit(name, ts);
@@ -249,7 +280,9 @@ hipError_t launch_gate(const char *name, const GateArgs &g, hipStream_t stream) 
         return g.n == 0 ? hipSuccess : hipErrorInvalidValue;
     (void)hipGetLastError();
     TraceSlot ts = trace_acquire();
-    hipExtLaunchKernelGGL(gate_kernel, dim3(1), dim3(64), 0, stream, ts.start, ts.stop, 0, g);
+    GateArgs named = g;
+    named.site = wait_site(name);
+    hipExtLaunchKernelGGL(gate_kernel, dim3(1), dim3(64), 0, stream, ts.start, ts.stop, 0, named);
     hipError_t err = hipGetLastError();
     if (err == hipSuccess)
         trace_submit(name, ts);
@@ -299,11 +332,31 @@ hipError_t launch_wait_flags(const char *name, const uint32_t *flags, int32_t n,
     (void)hipGetLastError();  // drop an error left by an earlier, already reported call
     TraceSlot ts = trace_acquire();
     hipExtLaunchKernelGGL(wait_flags_kernel, dim3((unsigned)((n + 63) / 64)), dim3(64), 0, stream,
-                          ts.start, ts.stop, 0, flags, n, epoch, timeout_ticks, sleep_units, status);
+                          ts.start, ts.stop, 0, flags, n, epoch, timeout_ticks, sleep_units, status, wait_site(name));
     hipError_t err = hipGetLastError();
     if (err == hipSuccess)
         trace_submit(name, ts);
     return err;
 }
+
+namespace {
+constexpr const char *kSiteNames[kSiteCount] = {
+    "unknown wait",  "wait_d2h",      "wait_recv",    "wait_dispatch",  "wait_combine",       "wait_returned_out",
+    "landed_set",    "wait_credits",  "wait_returned", "wait_allgather", "wait_reducescatter", "the inbound-copy courier",
+};
+}  // namespace
+
+uint32_t wait_site(const char *launch_name) {
+    for (uint32_t i = 1; i < kSiteCount; ++i) {
+        const char *a = kSiteNames[i], *b = launch_name;
+        while (*a && *a == *b)
+            ++a, ++b;
+        if (!*a && !*b)
+            return i;
+    }
+    return kSiteUnknown;
+}
+
+const char *wait_site_name(uint32_t site) { return site < kSiteCount ? kSiteNames[site] : kSiteNames[0]; }
 
 }  // namespace ep

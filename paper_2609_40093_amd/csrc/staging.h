@@ -6,6 +6,7 @@
 #include "ep.h"
 #include "ep_internal.h"
 #include "sdma.h"
+#include "status_block.h"
 
 #include <cstdint>
 #include <string>
@@ -17,6 +18,15 @@ namespace ep {
 ep_status fail(ep_status st, const char *fmt, ...);
 // Map a HIP error to EP_ERR_OOM / EP_ERR_HIP (and clear it from the runtime).
 ep_status hip_fail(hipError_t e, const char *what);
+
+// Takes and clears a status block (kStatusWords words): EP_OK, or the error it holds, with
+// the expired wait described in ep_last_error; `name_flag` names the flag word at an
+// address ("recv_landed[buf 1][rank 3]"), or returns "" for one it does not know.
+struct FlagNamer {
+    virtual std::string operator()(const uint32_t *flag) const = 0;
+    virtual ~FlagNamer() = default;
+};
+ep_status take_status(uint32_t *block, int64_t timeout_us, const FlagNamer &name_flag);
 
 #define EP_HIP(call)                                                                                \
     do {                                                                                            \
@@ -78,7 +88,8 @@ struct ep_staging {
     int64_t row_bytes = 0, buffer_bytes = 0, chunk_bytes = 0;
     void *dev_send[ep::kMaxBuffers] = {}, *dev_recv[ep::kMaxBuffers] = {};
     void *host_send[ep::kMaxBuffers] = {}, *host_recv[ep::kMaxBuffers] = {};
-    // coherent pinned words: send [nbuf][max_chunks], recv [nbuf][R], status, then
+    // coherent pinned words: send [nbuf][max_chunks], recv [nbuf][R], the status block
+    // (ep::kStatusWords words, status_block.h), then
     // inbound [nbuf][R], returned-out [nbuf][R], inbound-landed [nbuf][R],
     // recv-landed [nbuf][R], offsets mirror [nbuf][R+2], send credits [nbuf][R],
     // recv credits [nbuf]
@@ -118,7 +129,7 @@ struct ep_staging {
     uint32_t *send_flags(int b) const { return flags + (size_t)b * max_chunks; }
     uint32_t *recv_flags(int b) const { return flags + nb() * max_chunks + (size_t)b * R(); }
     uint32_t *status() const { return flags + nb() * (max_chunks + R()); }
-    uint32_t *ext_base() const { return status() + 1; }
+    uint32_t *ext_base() const { return status() + ep::kStatusWords; }
     uint32_t *in_flags(int b) const { return ext_base() + (size_t)b * R(); }
     uint32_t *ret_flags(int b) const { return ext_base() + nb() * R() + (size_t)b * R(); }
     uint32_t *in_landed(int b) const { return ext_base() + 2 * nb() * R() + (size_t)b * R(); }
@@ -127,7 +138,7 @@ struct ep_staging {
     uint32_t *send_credit(int b) const { return mirror(0) + nb() * (R() + 2) + (size_t)b * R(); }
     uint32_t *recv_credit(int b) const { return send_credit(0) + nb() * R() + (size_t)b; }
     static size_t flag_words_for(int nbuf, int max_chunks, int R) {
-        return (size_t)nbuf * (max_chunks + R) + 1 + 4 * (size_t)nbuf * R + (size_t)nbuf * (R + 2) +
+        return (size_t)nbuf * (max_chunks + R) + ep::kStatusWords + 4 * (size_t)nbuf * R + (size_t)nbuf * (R + 2) +
                (size_t)nbuf * R + (size_t)nbuf;
     }
     uint32_t *epoch_word(int b) const { return reinterpret_cast<uint32_t *>(dev_epoch + b * ep::kEpochStride); }

@@ -1,0 +1,675 @@
+// dma_slots_test.cpp -- host-only test of the SDMA lane's and the exchange's signal
+// handling (sdma.h, exchange.h, signal_slots.h) against a stand-in for the ROCr runtime.
+//
+// The stand-in keeps the documented contract of an async copy: it starts once every
+// dependency signal reads exactly 0, it writes its bytes, and afterwards it decrements
+// its completion signal.  Each engine runs its copies in order on a thread of its own, and
+// it applies a copy's decrement after a random delay, with the copied bytes (a flag word
+// included) already visible to the host: the window in which a host that has seen a flag
+// may still get that copy's decrement later.  The stand-in records as violations:
+//   - a decrement landing on a signal whose value was stored again (reset for a new call),
+//     or on a destroyed signal (its handle is handed out again by the next create);
+//   - a dependency reading below 0 (an engine waiting for 0 would never start the copy);
+//   - an engine waiting longer than the test allows.
+// Destroyed handles are recycled last-in first-out, as a signal pool would.
+//
+// Usage: dma_slots_test lane|exchange|order|bounded|old_rule [seed]; prints
+// "violations N" and exits 0 when N == 0 and every check of the scenario held.
+#include "exchange.h"
+#include "sdma.h"
+#include "signal_slots.h"
+
+#include <atomic>
+#include <chrono>
+#include <condition_variable>
+#include <cstdio>
+#include <cstdlib>
+#include <cstring>
+#include <deque>
+#include <map>
+#include <memory>
+#include <mutex>
+#include <random>
+#include <string>
+#include <thread>
+#include <vector>
+
+namespace {
+
+using Clock = std::chrono::steady_clock;
+
+std::atomic<int> g_violations{0};
+std::mutex g_log_mu;
+void violation(const char *what, uint64_t h) {
+    ++g_violations;
+    std::lock_guard<std::mutex> lk(g_log_mu);
+    if (g_violations <= 10)
+        std::printf("violation: %s (signal %llu)\n", what, (unsigned long long)h);
+}
+
+// ---------------------------------------------------------------- stand-in signals
+
+constexpr size_t kMaxSignals = 1 << 16;
+struct FakeSignal {
+    volatile int64_t value;
+    std::atomic<uint64_t> gen;  // bumped by every host store and by destroy
+    std::atomic<bool> alive;
+};
+FakeSignal g_sig[kMaxSignals];
+std::mutex g_sig_mu;
+std::vector<uint64_t> g_free;  // recycled handles, last in first out
+uint64_t g_next = 1;
+std::atomic<int64_t> g_created{0}, g_destroyed{0};
+
+FakeSignal &sig(hsa_signal_t s) { return g_sig[s.handle]; }
+
+std::atomic<int> g_delay_max_us{200};
+thread_local std::mt19937 t_rng{12345};
+int rand_delay_us() {
+    const int m = g_delay_max_us.load();
+    if (m <= 0)
+        return 0;
+    std::uniform_int_distribution<int> d(0, 9);
+    const int pick = d(t_rng);
+    std::uniform_int_distribution<int> u(0, m);
+    return pick < 6 ? 0 : u(t_rng);  // most decrements at once, some late
+}
+
+// ---------------------------------------------------------------- stand-in engines
+
+struct Copy {
+    void *dst;
+    const void *src;
+    size_t len;
+    std::vector<hsa_signal_t> deps;
+    hsa_signal_t done;
+    uint64_t done_gen;
+};
+
+class Engine {
+public:
+    explicit Engine(uint32_t id) : id_(id), th_([this] { run(); }) {}
+    ~Engine() {
+        {
+            std::lock_guard<std::mutex> lk(mu_);
+            stop_ = true;
+        }
+        cv_.notify_all();
+        th_.join();
+    }
+    void push(Copy c) {
+        {
+            std::lock_guard<std::mutex> lk(mu_);
+            q_.push_back(std::move(c));
+        }
+        cv_.notify_all();
+    }
+    bool idle() {
+        std::lock_guard<std::mutex> lk(mu_);
+        return q_.empty() && !busy_;
+    }
+
+private:
+    void run() {
+        t_rng.seed(1000 + id_);
+        for (;;) {
+            Copy c;
+            {
+                std::unique_lock<std::mutex> lk(mu_);
+                cv_.wait(lk, [&] { return stop_ || !q_.empty(); });
+                if (stop_ && q_.empty())
+                    return;
+                c = q_.front();
+                q_.pop_front();
+                busy_ = true;
+            }
+            const auto t0 = Clock::now();
+            bool stuck = false;
+            for (hsa_signal_t d : c.deps) {
+                for (;;) {
+                    const int64_t v = __atomic_load_n(&sig(d).value, __ATOMIC_ACQUIRE);
+                    if (v == 0)
+                        break;
+                    if (v < 0) {
+                        violation("a dependency reads below 0: the copy would never start", d.handle);
+                        stuck = true;
+                        break;
+                    }
+                    if (Clock::now() - t0 > std::chrono::seconds(5)) {
+                        violation("a copy waited 5 s for a dependency", d.handle);
+                        stuck = true;
+                        break;
+                    }
+                    std::this_thread::yield();
+                }
+                if (stuck)
+                    break;
+            }
+            if (!stuck) {
+                if (c.len == sizeof(uint32_t))  // flag words: one visible store
+                    __atomic_store_n(static_cast<uint32_t *>(c.dst), *static_cast<const volatile uint32_t *>(c.src),
+                                     __ATOMIC_RELEASE);
+                else {
+                    std::memcpy(c.dst, c.src, c.len);
+                    __atomic_thread_fence(__ATOMIC_RELEASE);
+                }
+                const int us = rand_delay_us();
+                if (us > 0)
+                    std::this_thread::sleep_for(std::chrono::microseconds(us));
+                FakeSignal &f = sig(c.done);
+                if (!f.alive.load())
+                    violation("a completion decrement landed on a destroyed signal", c.done.handle);
+                else if (f.gen.load() != c.done_gen)
+                    violation("a completion decrement landed after the signal was reset for a new call",
+                              c.done.handle);
+                __atomic_fetch_sub(&f.value, 1, __ATOMIC_ACQ_REL);
+            }
+            std::lock_guard<std::mutex> lk(mu_);
+            busy_ = false;
+        }
+    }
+
+    uint32_t id_;
+    std::mutex mu_;
+    std::condition_variable cv_;
+    std::deque<Copy> q_;
+    bool stop_ = false, busy_ = false;
+    std::thread th_;
+};
+
+std::mutex g_eng_mu;
+std::map<uint32_t, std::unique_ptr<Engine>> g_engines;
+Engine &engine(uint32_t id) {
+    std::lock_guard<std::mutex> lk(g_eng_mu);
+    auto &e = g_engines[id];
+    if (!e)
+        e.reset(new Engine(id));
+    return *e;
+}
+void stop_engines() {
+    std::lock_guard<std::mutex> lk(g_eng_mu);
+    g_engines.clear();
+}
+
+hsa_status_t submit(void *dst, const void *src, size_t len, uint32_t ndeps, const hsa_signal_t *deps,
+                    hsa_signal_t done, uint32_t eng) {
+    if (!dst || !src || !done.handle)
+        return HSA_STATUS_ERROR_INVALID_ARGUMENT;
+    Copy c{dst, src, len, std::vector<hsa_signal_t>(deps, deps + ndeps), done, sig(done).gen.load()};
+    engine(eng).push(std::move(c));
+    return HSA_STATUS_SUCCESS;
+}
+
+}  // namespace
+
+// ---------------------------------------------------------------- the ROCr entry points used
+
+extern "C" {
+
+hsa_status_t hsa_amd_signal_create(hsa_signal_value_t initial_value, uint32_t, const hsa_agent_t *, uint64_t,
+                                   hsa_signal_t *signal) {
+    std::lock_guard<std::mutex> lk(g_sig_mu);
+    uint64_t h;
+    if (!g_free.empty()) {
+        h = g_free.back();
+        g_free.pop_back();
+    } else {
+        if (g_next >= kMaxSignals)
+            return HSA_STATUS_ERROR_OUT_OF_RESOURCES;
+        h = g_next++;
+    }
+    g_sig[h].value = initial_value;
+    g_sig[h].gen.fetch_add(1);
+    g_sig[h].alive.store(true);
+    signal->handle = h;
+    ++g_created;
+    return HSA_STATUS_SUCCESS;
+}
+
+hsa_status_t hsa_signal_destroy(hsa_signal_t s) {
+    std::lock_guard<std::mutex> lk(g_sig_mu);
+    sig(s).alive.store(false);
+    sig(s).gen.fetch_add(1);
+    g_free.push_back(s.handle);
+    ++g_destroyed;
+    return HSA_STATUS_SUCCESS;
+}
+
+void hsa_signal_store_relaxed(hsa_signal_t s, hsa_signal_value_t v) {
+    sig(s).gen.fetch_add(1);
+    __atomic_store_n(&sig(s).value, v, __ATOMIC_RELAXED);
+}
+
+void hsa_signal_store_screlease(hsa_signal_t s, hsa_signal_value_t v) {
+    sig(s).gen.fetch_add(1);
+    __atomic_store_n(&sig(s).value, v, __ATOMIC_RELEASE);
+}
+
+hsa_signal_value_t hsa_signal_load_scacquire(hsa_signal_t s) { return __atomic_load_n(&sig(s).value, __ATOMIC_ACQUIRE); }
+
+hsa_status_t hsa_amd_signal_value_pointer(hsa_signal_t s, volatile hsa_signal_value_t **p) {
+    *p = &sig(s).value;
+    return HSA_STATUS_SUCCESS;
+}
+
+hsa_status_t hsa_amd_memory_async_copy_on_engine(void *dst, hsa_agent_t, const void *src, hsa_agent_t, size_t size,
+                                                 uint32_t ndeps, const hsa_signal_t *deps, hsa_signal_t done,
+                                                 hsa_amd_sdma_engine_id_t engine_id, bool) {
+    return submit(dst, src, size, ndeps, deps, done, (uint32_t)engine_id);
+}
+
+hsa_status_t hsa_amd_memory_async_copy(void *dst, hsa_agent_t, const void *src, hsa_agent_t, size_t size,
+                                       uint32_t ndeps, const hsa_signal_t *deps, hsa_signal_t done) {
+    return submit(dst, src, size, ndeps, deps, done, 0);
+}
+
+hsa_status_t hsa_shut_down() { return HSA_STATUS_SUCCESS; }
+
+}  // extern "C"
+
+// ---------------------------------------------------------------- the caller's stream
+
+namespace {
+
+// Work the caller's stream does in order: store 0 into a start signal (the release
+// kernel), or wait for a flag word to reach an epoch (the wait kernel).
+class Stream {
+public:
+    Stream() : th_([this] { run(); }) {}
+    ~Stream() {
+        finish();
+        {
+            std::lock_guard<std::mutex> lk(mu_);
+            stop_ = true;
+        }
+        cv_.notify_all();
+        th_.join();
+    }
+    void release(int64_t *value) { push({value, nullptr, 0}); }
+    void wait(const uint32_t *flag, uint32_t epoch) { push({nullptr, flag, epoch}); }
+    void finish() {
+        std::unique_lock<std::mutex> lk(mu_);
+        done_cv_.wait(lk, [&] { return q_.empty() && !busy_; });
+    }
+
+private:
+    struct Item {
+        int64_t *value;
+        const uint32_t *flag;
+        uint32_t epoch;
+    };
+    void push(Item it) {
+        {
+            std::lock_guard<std::mutex> lk(mu_);
+            q_.push_back(it);
+        }
+        cv_.notify_all();
+    }
+    void run() {
+        std::mt19937 rng(77);
+        for (;;) {
+            Item it;
+            {
+                std::unique_lock<std::mutex> lk(mu_);
+                cv_.wait(lk, [&] { return stop_ || !q_.empty(); });
+                if (q_.empty())
+                    return;
+                it = q_.front();
+                q_.pop_front();
+                busy_ = true;
+            }
+            if (it.value) {
+                std::this_thread::sleep_for(std::chrono::microseconds(rng() % 50));
+                __atomic_store_n(it.value, (int64_t)0, __ATOMIC_RELEASE);
+            } else {
+                const auto t0 = Clock::now();
+                while ((int32_t)(__atomic_load_n(it.flag, __ATOMIC_ACQUIRE) - it.epoch) < 0) {
+                    if (Clock::now() - t0 > std::chrono::seconds(5)) {
+                        violation("the stream waited 5 s for a flag", 0);
+                        break;
+                    }
+                    std::this_thread::yield();
+                }
+            }
+            {
+                std::lock_guard<std::mutex> lk(mu_);
+                busy_ = false;
+            }
+            done_cv_.notify_all();
+        }
+    }
+    std::mutex mu_;
+    std::condition_variable cv_, done_cv_;
+    std::deque<Item> q_;
+    bool stop_ = false, busy_ = false;
+    std::thread th_;
+};
+
+int g_checks_failed = 0;
+void check(bool ok, const char *what) {
+    if (!ok) {
+        ++g_checks_failed;
+        std::printf("check failed: %s\n", what);
+    }
+}
+
+const hsa_agent_t kGpu{1}, kCpu{2};
+
+// ---------------------------------------------------------------- scenarios
+
+// Rounds of the default device->host leg with a chunk count that changes from round to
+// round (so a signal's role in one round differs from its role in the last round on the
+// same slot), the host running ahead of the copies, and lanes created and released
+// between batches (destroyed handles recycled).
+void scenario_lane(uint32_t seed) {
+    std::mt19937 rng(seed);
+    for (int batch = 0; batch < 6; ++batch) {
+        ep::SdmaLane lane;
+        lane.init_with(kGpu, kCpu, 1u, 4);
+        Stream stream;
+        struct R {
+            std::vector<uint8_t> src, dst;
+            std::vector<uint32_t> flags;
+            uint32_t epoch_word;
+            uint32_t epoch;
+        };
+        std::vector<std::unique_ptr<R>> rounds;
+        for (int i = 0; i < 60; ++i) {
+            const int64_t chunk = 256, chunks = 1 + rng() % 6;
+            const int64_t bytes = (chunks - 1) * chunk + 1 + rng() % chunk;
+            std::unique_ptr<R> r(new R);
+            r->src.resize((size_t)bytes);
+            for (auto &b : r->src)
+                b = (uint8_t)rng();
+            r->dst.assign((size_t)bytes, 0);
+            r->flags.assign((size_t)chunks, 0);
+            r->epoch = (uint32_t)(batch * 1000 + i + 1);
+            r->epoch_word = r->epoch;
+            ep::SdmaLane::Round round;
+            std::string err;
+            if (!lane.begin(round, 5 * 1000 * 1000, err)) {
+                check(false, err.c_str());
+                break;
+            }
+            stream.release(round.start_value);
+            if (!lane.submit(round, r->dst.data(), r->src.data(), bytes, chunk, r->flags.data(), &r->epoch_word, err)) {
+                check(false, err.c_str());
+                break;
+            }
+            stream.wait(&r->flags[(size_t)chunks - 1], r->epoch);
+            rounds.push_back(std::move(r));
+        }
+        stream.finish();
+        std::string err;
+        check(lane.drain(5 * 1000 * 1000, err), "the lane drains");
+        for (auto &r : rounds) {
+            check(r->dst == r->src, "every round's bytes landed");
+            for (uint32_t f : r->flags)
+                check(f == r->epoch, "every chunk flag holds its round's epoch");
+        }
+        lane.release();
+    }
+}
+
+// Calls of the exchange modes: outbound copies with flag copies on one engine, inbound
+// copies queued by the courier as simulated senders raise their flags at random times,
+// with the number of copies per call changing from call to call; exchanges created and
+// released between batches.
+void scenario_exchange(uint32_t seed) {
+    std::mt19937 rng(seed);
+    for (int batch = 0; batch < 6; ++batch) {
+        ep::Exchange x;
+        x.init_with(kGpu, kCpu, 1u, {2u}, 4);
+        Stream stream;
+        uint32_t status[ep::kStatusWords] = {};
+        struct Call {
+            std::vector<std::vector<uint8_t>> out_src, out_dst, in_src, in_dst;
+            std::vector<uint32_t> out_flags, ready, landed;
+            uint32_t epoch, epoch_word;
+        };
+        std::vector<std::unique_ptr<Call>> calls;
+        std::vector<std::thread> senders;
+        for (int i = 0; i < 50; ++i) {
+            std::unique_ptr<Call> c(new Call);
+            c->epoch = c->epoch_word = (uint32_t)(batch * 1000 + i + 1);
+            const int nout = (int)(rng() % 4), nin = 1 + (int)(rng() % 6);
+            for (int k = 0; k < nout; ++k) {
+                c->out_src.emplace_back(64 + rng() % 512);
+                for (auto &b : c->out_src.back())
+                    b = (uint8_t)rng();
+                c->out_dst.emplace_back(c->out_src.back().size(), 0);
+            }
+            for (int k = 0; k < nin; ++k) {
+                c->in_src.emplace_back(64 + rng() % 512);
+                for (auto &b : c->in_src.back())
+                    b = (uint8_t)rng();
+                c->in_dst.emplace_back(c->in_src.back().size(), 0);
+            }
+            c->out_flags.assign((size_t)nout, 0);
+            c->ready.assign((size_t)nin, 0);
+            c->landed.assign((size_t)nin, 0);
+            std::string err;
+            const int slot = x.begin(5 * 1000 * 1000, err);
+            if (slot < 0) {
+                check(false, err.c_str());
+                break;
+            }
+            hsa_signal_t start{};
+            check(x.start_signal(slot, start, err), "start signal");
+            stream.release(ep::DmaEngines::value_pointer(start));
+            x.arm(slot, start);
+            for (int k = 0; k < nout; ++k) {
+                hsa_signal_t d{};
+                check(x.copy(slot, 1u, c->out_dst[(size_t)k].data(), true, c->out_src[(size_t)k].data(), false,
+                             c->out_src[(size_t)k].size(), &start, 1, &d, err) &&
+                          x.copy(slot, 1u, &c->out_flags[(size_t)k], true, &c->epoch_word, false, sizeof(uint32_t),
+                                 &d, 1, nullptr, err),
+                      "outbound copies submitted");
+                stream.wait(&c->out_flags[(size_t)k], c->epoch);
+            }
+            ep::InJob j;
+            j.epoch = c->epoch;
+            j.per_sender = rng() % 2;
+            j.start = start;
+            j.epoch_word = &c->epoch_word;
+            j.status = status;
+            j.deadline = Clock::now() + std::chrono::seconds(5);
+            for (int k = 0; k < nin; ++k) {
+                ep::InCopy ic;
+                check(x.in_copy(slot, &c->ready[(size_t)k], reinterpret_cast<char *>(c->in_dst[(size_t)k].data()),
+                                reinterpret_cast<const char *>(c->in_src[(size_t)k].data()),
+                                (int64_t)c->in_src[(size_t)k].size(), &c->landed[(size_t)k], ic, err),
+                      "inbound copy signals");
+                j.copies.push_back(ic);
+                stream.wait(&c->landed[(size_t)k], c->epoch);
+            }
+            x.post(slot, std::move(j));
+            // the senders raise their flags in a random order, a little later
+            Call *cp = c.get();
+            const uint32_t sseed = (uint32_t)rng();
+            senders.emplace_back([cp, nin, sseed] {
+                std::mt19937 r(sseed);
+                std::vector<int> order((size_t)nin);
+                for (int k = 0; k < nin; ++k)
+                    order[(size_t)k] = k;
+                std::shuffle(order.begin(), order.end(), r);
+                for (int k : order) {
+                    std::this_thread::sleep_for(std::chrono::microseconds(r() % 300));
+                    __atomic_store_n(&cp->ready[(size_t)k], cp->epoch, __ATOMIC_RELEASE);
+                }
+            });
+            calls.push_back(std::move(c));
+        }
+        for (auto &t : senders)
+            t.join();
+        stream.finish();
+        x.release();
+        check(status[0] == 0, "no courier timeout");
+        for (auto &c : calls) {
+            check(c->out_dst == c->out_src, "outbound bytes landed");
+            check(c->in_dst == c->in_src, "inbound bytes landed");
+            for (uint32_t f : c->out_flags)
+                check(f == c->epoch, "outbound flags hold the epoch");
+            for (uint32_t f : c->landed)
+                check(f == c->epoch, "landed flags hold the epoch");
+        }
+    }
+}
+
+// Two calls whose senders answer out of order: the first call's sender is 50 ms late, the
+// second call's sender has answered before the second call is even posted.  The second
+// call's copy must not be queued on the in-order inbound engine ahead of the first call's
+// (it waits for a start signal that the stream releases only after the first call's rows
+// have landed).  Both calls must finish in about the late sender's delay, well inside the
+// stream's 5 s bound.
+void scenario_order() {
+    ep::Exchange x;
+    x.init_with(kGpu, kCpu, 1u, {2u}, 4);
+    Stream stream;
+    uint32_t status[ep::kStatusWords] = {};
+    std::vector<uint8_t> src[2], dst[2];
+    uint32_t ready[2] = {0, 0}, landed[2] = {0, 0}, epoch_word[2] = {1, 2};
+    const auto t0 = Clock::now();
+    for (int c = 0; c < 2; ++c) {
+        src[c].assign(4096, (uint8_t)(c + 1));
+        dst[c].assign(4096, 0);
+        if (c == 1)
+            __atomic_store_n(&ready[1], 2u, __ATOMIC_RELEASE);  // the second call's sender is early
+        std::string err;
+        const int slot = x.begin(1000 * 1000, err);
+        hsa_signal_t start{};
+        check(slot >= 0 && x.start_signal(slot, start, err), "slot and start signal");
+        stream.release(ep::DmaEngines::value_pointer(start));
+        x.arm(slot, start);
+        ep::InJob j;
+        j.epoch = (uint32_t)(c + 1);
+        j.per_sender = true;
+        j.start = start;
+        j.epoch_word = &epoch_word[c];
+        j.status = status;
+        j.deadline = Clock::now() + std::chrono::seconds(5);
+        ep::InCopy ic;
+        check(x.in_copy(slot, &ready[c], reinterpret_cast<char *>(dst[c].data()),
+                        reinterpret_cast<const char *>(src[c].data()), 4096, &landed[c], ic, err),
+              "inbound copy");
+        j.copies.push_back(ic);
+        x.post(slot, std::move(j));
+        stream.wait(&landed[c], (uint32_t)(c + 1));
+    }
+    std::thread late([&] {
+        std::this_thread::sleep_for(std::chrono::milliseconds(50));
+        __atomic_store_n(&ready[0], 1u, __ATOMIC_RELEASE);
+    });
+    late.join();
+    stream.finish();
+    const double ms = std::chrono::duration<double, std::milli>(Clock::now() - t0).count();
+    check(ms < 1000.0, "both calls finished within a second (no wait for the bound)");
+    check(landed[0] == 1 && landed[1] == 2 && dst[0] == src[0] && dst[1] == src[1], "both calls' rows landed");
+    check(status[0] == 0, "no timeout recorded");
+    x.release();
+    std::printf("out-of-order senders: %.1f ms\n", ms);
+}
+
+// A slot whose previous call left a signal that never reaches 0 is not handed out: begin()
+// gives up after its bound with a message, and succeeds once the signal retires.
+void scenario_bounded() {
+    ep::SignalSlots slots;
+    slots.init(2);
+    std::string err;
+    const int a = slots.begin(1000, err);
+    hsa_signal_t g{};
+    check(a == 0 && slots.take(a, g, err), "first call");
+    slots.arm(a, g);
+    check(slots.begin(1000, err) == 1, "the other slot is free");
+    const auto t0 = Clock::now();
+    check(slots.begin(20000, err) == -1, "the pending slot is refused");
+    check(Clock::now() - t0 >= std::chrono::milliseconds(20), "after waiting for its bound");
+    check(err.find("still reads 1") != std::string::npos, "the message names the pending value");
+    hsa_signal_store_screlease(g, 0);
+    check(slots.begin(1000, err) == 0, "reused once the signal reads 0");
+    // a negative value (a failed copy) is reported once, then the slot is usable
+    check(slots.take(0, g, err), "take");
+    slots.arm(0, g);
+    hsa_signal_store_screlease(g, -1);
+    check(slots.begin(1000, err) == 1, "slot 1");
+    check(slots.begin(1000, err) == -1 && err.find("failed copy") != std::string::npos, "failed copy reported");
+    check(slots.begin(1000, err) == 0, "then usable");
+    // destroy leaves signals alone when the drain did not succeed
+    check(slots.take(0, g, err), "take");
+    slots.arm(0, g);
+    const int64_t before = g_destroyed.load();
+    check(!slots.drain(1000, err), "drain gives up on a pending signal");
+    slots.destroy(false);
+    check(g_destroyed.load() == before, "no signal destroyed while one may still be decremented");
+}
+
+// The reuse rule this library had before, replayed directly against the stand-in: one
+// completion signal shared by two flag copies, reset for the next call as soon as the
+// host sees the flags.  With late decrements the stand-in must report a violation; this
+// scenario checks the harness, and is expected to fail.
+void scenario_old_rule(uint32_t seed) {
+    std::mt19937 rng(seed);
+    g_delay_max_us = 2000;
+    hsa_signal_t start{}, d0{}, d1{}, shared{};
+    for (hsa_signal_t *s : {&start, &d0, &d1, &shared})
+        hsa_amd_signal_create(1, 0, nullptr, 0, s);
+    uint32_t epoch_word = 0, flags[2] = {0, 0};
+    std::vector<uint8_t> src(256, 7), dst(256);
+    for (int call = 1; call <= 200 && g_violations == 0; ++call) {
+        // the next call re-initialises every signal of the slot, whatever role it had
+        for (hsa_signal_t s : {start, d0, d1})
+            hsa_signal_store_relaxed(s, 1);
+        hsa_signal_store_relaxed(shared, 2);
+        epoch_word = (uint32_t)call;
+        submit(dst.data(), src.data(), 128, 1, &start, d0, 1);
+        submit(&flags[0], &epoch_word, 4, 1, &d0, shared, 1);
+        submit(dst.data() + 128, src.data() + 128, 128, 1, &start, d1, 1);
+        submit(&flags[1], &epoch_word, 4, 1, &d1, shared, 1);
+        hsa_signal_store_screlease(start, 0);
+        const auto t0 = Clock::now();
+        while (__atomic_load_n(&flags[1], __ATOMIC_ACQUIRE) != (uint32_t)call &&
+               Clock::now() - t0 < std::chrono::seconds(2))
+            std::this_thread::yield();
+        // roles shift: the shared completion signal becomes the first chunk's signal
+        if (rng() % 2)
+            std::swap(d0, shared);
+    }
+    g_delay_max_us = 200;
+}
+
+}  // namespace
+
+int main(int argc, char **argv) {
+    const std::string what = argc > 1 ? argv[1] : "";
+    const uint32_t seed = argc > 2 ? (uint32_t)std::strtoul(argv[2], nullptr, 10) : 1u;
+    if (what == "lane")
+        scenario_lane(seed);
+    else if (what == "exchange")
+        scenario_exchange(seed);
+    else if (what == "order")
+        scenario_order();
+    else if (what == "bounded")
+        scenario_bounded();
+    else if (what == "old_rule")
+        scenario_old_rule(seed);
+    else {
+        std::printf("usage: %s lane|exchange|order|bounded|old_rule [seed]\n", argv[0]);
+        return 2;
+    }
+    // let every queued copy finish before the engines stop
+    for (;;) {
+        bool idle = true;
+        {
+            std::lock_guard<std::mutex> lk(g_eng_mu);
+            for (auto &e : g_engines)
+                idle = idle && e.second->idle();
+        }
+        if (idle)
+            break;
+        std::this_thread::sleep_for(std::chrono::milliseconds(1));
+    }
+    stop_engines();
+    std::printf("violations %d checks_failed %d signals created %lld destroyed %lld\n", g_violations.load(),
+                g_checks_failed, (long long)g_created.load(), (long long)g_destroyed.load());
+    return g_violations == 0 && g_checks_failed == 0 ? 0 : 1;
+}

@@ -1,0 +1,82 @@
+"""The SDMA legs' signal handling on the host, against a stand-in ROCr runtime
+(tests/host/dma_slots_test.cpp): no GPU, no HIP.
+
+The stand-in keeps the documented contract of an async copy (it starts once every
+dependency signal reads 0, and decrements its completion signal after its bytes are
+visible) and applies decrements late, after the flag the copy wrote can already be seen.
+It records a violation when a decrement lands on a signal that was reset or destroyed
+since, or when a dependency drops below 0 (an engine would then never start the copy).
+
+Cases:
+- lane: rounds of the default device->host leg with the chunk count changing between
+  rounds (signal roles shift), lanes created and released between batches;
+- exchange: calls with outbound and inbound copies (courier, per-sender and all-senders
+  jobs), senders answering in random order, exchanges recreated between batches;
+- order: a later call's sender answers before an earlier call's; both calls finish
+  without waiting for the bound (the courier serves jobs in call order);
+- bounded: a slot with a signal that never retires is refused after its bound, with a
+  message; a failed copy (negative value) is reported once; nothing is destroyed while a
+  decrement may still come;
+- old_rule: the reuse rule of the earlier revision (a completion signal shared by two
+  copies, reset as soon as the flags are seen) replayed against the stand-in, which must
+  report the late decrement: the harness does catch the failure mode.
+"""
+import os
+import shutil
+import subprocess
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+CSRC = os.path.join(ROOT, "paper_2609_40093_amd", "csrc")
+ROCM_INCLUDE = "/opt/rocm/include"
+
+
+@pytest.fixture(scope="module")
+def binary(tmp_path_factory):
+    gxx = shutil.which("g++")
+    if not gxx or not os.path.exists(os.path.join(ROCM_INCLUDE, "hsa", "hsa.h")):
+        pytest.skip("needs g++ and the ROCr headers")
+    out = str(tmp_path_factory.mktemp("dma") / "dma_slots_test")
+    cmd = [gxx, "-std=c++17", "-O1", "-g", "-Wall", "-D__HIP_PLATFORM_AMD__", "-I", ROCM_INCLUDE,
+           "-I", os.path.join(ROOT, "include"), "-I", CSRC,
+           os.path.join(ROOT, "tests", "host", "dma_slots_test.cpp"), os.path.join(CSRC, "sdma_lane.cpp"),
+           "-o", out, "-lpthread"]
+    res = subprocess.run(cmd, capture_output=True, text=True)
+    assert res.returncode == 0, res.stderr[-4000:]
+    return out
+
+
+def run(binary, *args, timeout=120):
+    res = subprocess.run([binary, *map(str, args)], capture_output=True, text=True, timeout=timeout)
+    return res.returncode, res.stdout + res.stderr
+
+
+@pytest.mark.parametrize("seed", [1, 2, 3])
+def test_lane_rounds_never_reset_a_pending_signal(binary, seed):
+    rc, out = run(binary, "lane", seed)
+    assert rc == 0, out
+    assert "violations 0 checks_failed 0" in out
+
+
+@pytest.mark.parametrize("seed", [1, 2, 3])
+def test_exchange_calls_never_reset_a_pending_signal(binary, seed):
+    rc, out = run(binary, "exchange", seed)
+    assert rc == 0, out
+    assert "violations 0 checks_failed 0" in out
+
+
+def test_senders_out_of_call_order_do_not_stall_the_inbound_engine(binary):
+    rc, out = run(binary, "order", timeout=60)
+    assert rc == 0, out
+
+
+def test_slot_reuse_is_bounded_and_reported(binary):
+    rc, out = run(binary, "bounded", timeout=60)
+    assert rc == 0, out
+
+
+def test_harness_catches_the_shared_signal_rule(binary):
+    rc, out = run(binary, "old_rule", 1, timeout=60)
+    assert rc == 1, out
+    assert "decrement landed after the signal was reset" in out

@@ -83,7 +83,11 @@ def test_stale_epoch_is_not_consumed():
     with pytest.raises(ep.EPError) as ei:
         st.status()
     assert ei.value.status == 5                      # EP_ERR_TIMEOUT
-    st.status()                                      # the status word was cleared
+    # the message names the wait, the flag it gave up on, what it read and what it wanted
+    msg = str(ei.value)
+    assert "wait_recv gave up on recv_flags[buf 0][rank " in msg, msg
+    assert "last read 4 (waited for 5)" in msg, msg
+    st.status()                                      # the status block was cleared
     st.host_array("recv_flags", 0)[:] = 5
     st.set_wait(timeout_us=5_000_000)
     out = ep.combine(st, lay.slot_pos, w, epoch=5)
