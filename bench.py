@@ -153,7 +153,7 @@ def main():
     #      kernels are timed live with HIP events on the stream they run on
     for i in range(args.warmup):
         step(i)
-    ep.layout_status(sets[0]["lay"])
+    ep.layout_validate(sets[0]["lay"])
     torch.cuda.synchronize()
     ep.trace_reset()
     torch.cuda.synchronize()
@@ -527,7 +527,7 @@ def bench_decode_latency(args, dev, rounds: int = 60) -> dict:
         if i >= args.warmup:
             lat.append((t1 - t0) * 1e6)
     st.status()
-    ep.layout_status(lay)
+    ep.layout_validate(lay)
     st.close()
     lat = np.array(lat)
     return {

@@ -33,12 +33,12 @@
  *     pointers on the current HIP device; the caller owns them.  bf16 data is passed as
  *     raw 16-bit patterns.  Byte offsets are 64-bit; rows are never assumed < 2^31 bytes.
  *   - Every call only enqueues work on `stream` (0 = the null stream) and returns; the
- *     outputs are valid once `stream` has reached that point.  Only ep_layout_status,
+ *     outputs are valid once `stream` has reached that point.  Only ep_layout_validate,
  *     ep_staging_status, ep_staging_alloc/free and ep_trace_read block.
  *   - Argument errors a host can see are reported synchronously and nothing is enqueued.
  *     Errors that depend on device data (an expert id out of range, a token row naming
  *     an expert twice, a flag wait that expired) are recorded in a status word and read
- *     by ep_layout_status / ep_staging_status.  No call throws.
+ *     by ep_layout_validate / ep_staging_status.  No call throws.
  *   - ep_last_error() returns this thread's text for the last non-OK status.
  *   - Calls on one ep_staging must not overlap from several host threads.
  */
@@ -54,7 +54,7 @@
 extern "C" {
 #endif
 
-#define EP_ABI_VERSION 3
+#define EP_ABI_VERSION 4
 #define EP_MAX_EXPERTS 2048 /* largest E the layout kernels accept */
 
 typedef enum {
@@ -84,7 +84,10 @@ const char *ep_last_error(void);
 
 /* ------------------------------------------------------------------------- layout */
 
-/* Bytes of device workspace ep_dispatch_layout needs for T tokens, top-k, E experts. */
+/* Bytes of device workspace ep_dispatch_layout needs for T tokens, top-k, E experts
+ * (the grouping of Sec. 4.3 counts every routing entry; the workspace holds its partial
+ * counts and its status).  bytes: host out; EP_ERR_INVALID_ARG for sizes the layout does
+ * not accept. */
 ep_status ep_layout_workspace_bytes(int64_t num_tokens, int32_t topk, int32_t num_experts,
                                     size_t *bytes /* host out */);
 
@@ -101,7 +104,7 @@ ep_status ep_layout_workspace_bytes(int64_t num_tokens, int32_t topk, int32_t nu
  *   workspace       device scratch of ep_layout_workspace_bytes() bytes, zero-filled
  *                   before its first use (e.g. hipMemset) and otherwise left alone between
  *                   calls: it carries a call counter from one call to the next, the
- *                   tiles' exchanged totals, and the status read by ep_layout_status.
+ *                   tiles' exchanged totals, and the status read by ep_layout_validate.
  *                   Calls that share a workspace must be ordered (same stream or events).
  * Requires T >= 0, T*k < 2^31, 1 <= k <= E <= EP_MAX_EXPERTS, R >= 1, E % R == 0.
  * T == 0 is valid: counts and offsets are written as zeros.  With an invalid expert id
@@ -114,17 +117,23 @@ ep_status ep_dispatch_layout(const int32_t *topk_idx, int64_t num_tokens, int32_
                              int32_t *slot_pos, int32_t *row_src,
                              void *workspace, size_t workspace_bytes, hipStream_t stream);
 
-/* Synchronizes `stream`, then reads the status word the last layout on `workspace` left:
+/* Validation of the routing a layout consumed (Sec. 4.3: every routing entry names one
+ * of the E experts, each at most once per token).  Synchronizes `stream`, then reads the
+ * status word the last layout on `workspace` left:
  * EP_OK, or EP_ERR_BAD_ROUTING (an id outside [0,E) or an expert repeated in a row), or
  * EP_ERR_TIMEOUT if a layout's workgroups could not all run at once within a second (the
  * device was held by other work); that state sticks until the workspace is zero-filled
  * again, and the outputs of the call that timed out are unspecified (stores stay inside
  * the arrays). */
-ep_status ep_layout_status(const void *workspace, hipStream_t stream);
+ep_status ep_layout_validate(const void *workspace, hipStream_t stream);
 
 /* ------------------------------------------------------------------------ staging */
 
-/* Allocates the staging of one rank.
+/* Allocates the staging of one rank: the buffers every dispatch and combine moves rows
+ * through.  With host staging the bounce buffers are pinned host memory, the one medium
+ * that ranks without peer-to-peer access all reach over PCIe (Sec. 4.2), and the
+ * completion flags are separate words in coherent host memory, each written by one
+ * party only (Sec. 4.4).
  *   kind         EP_STAGING_HBM or EP_STAGING_PINNED_HOST.
  *   max_rows     rows per buffer (>= T*k of every later call), hidden = H (multiple of 8).
  *   num_ranks    R: number of senders whose completion flags ep_combine waits for.
@@ -138,10 +147,12 @@ ep_status ep_layout_status(const void *workspace, hipStream_t stream);
 ep_status ep_staging_alloc(ep_staging_kind kind, int64_t max_rows, int32_t hidden,
                            int32_t num_ranks, int32_t num_buffers, int64_t chunk_bytes,
                            ep_staging **out);
-/* Frees a staging (NULL is a no-op).  Blocks: synchronises the staging's device, waits
- * for every SDMA copy still in flight (queued copies whose flags never came are started
- * first, so that none writes freed memory; at most 5 s in all), then frees the buffers.
- * Stop simulated peers of the staging (ep_sim_peers_stop) before. */
+/* Frees a staging (NULL is a no-op): the pinned buffers and flag words of Sec. 4.2 and
+ * Sec. 4.4.  Blocks: synchronises the staging's device, waits for every SDMA copy still in
+ * flight (queued copies whose flags never came are started first, so that none writes
+ * freed memory; at most 5 s in all, after which the copies' completion signals are left
+ * allocated rather than freed under an engine), then frees the buffers.  Stop simulated
+ * peers of the staging (ep_sim_peers_stop) before. */
 ep_status ep_staging_free(ep_staging *s);
 
 typedef struct {
@@ -166,15 +177,21 @@ typedef struct {
     uint32_t *recv_credit;        /* host word: this rank sets the round once it consumed this recv buffer */
 } ep_staging_view;
 
-/* Pointers and sizes of buffer set `buf` (host pointers are usable from the host). */
-ep_status ep_staging_get(ep_staging *s, int32_t buf, ep_staging_view *view);
+/* Pointers and sizes of buffer set `buf` (host pointers are usable from the host): the
+ * device send/recv buffers, the pinned bounce buffers that stand for the shared host
+ * medium of Sec. 4.2 (NULL with HBM staging), and the flag words of Sec. 4.4 that the
+ * other ranks (here: simulated peers on the host) write.  The view is owned by the
+ * caller; the pointers stay valid until ep_staging_free. */
+ep_status ep_staging_ptrs(ep_staging *s, int32_t buf, ep_staging_view *view);
 
 /* Bounded flag wait used by ep_combine with host staging: give up after timeout_us
  * microseconds (default 10 s), pausing sleep_units*64 cycles between polls (default 2). */
 ep_status ep_staging_set_wait(ep_staging *s, int64_t timeout_us, int32_t sleep_units);
 
 /* Synchronizes the staging's streams and `stream`, then returns and clears its status
- * word: EP_OK, or EP_ERR_TIMEOUT if a flag wait expired since the last call. */
+ * block: EP_OK, or EP_ERR_TIMEOUT if a bounded flag wait (Sec. 4.4) expired since the last
+ * call; ep_last_error then names the wait, the flag array, buffer set and index it gave
+ * up on, the value it last read and the value it waited for. */
 ep_status ep_staging_status(ep_staging *s, hipStream_t stream);
 
 /* Exchange modes of a PINNED_HOST staging (bit flags; 0 = the default legs above).
@@ -223,7 +240,9 @@ ep_status ep_staging_set_inbound(ep_staging *s, int32_t buf, const int64_t *rows
 
 /* --------------------------------------------------------------- dispatch / combine */
 
-/* Dispatch of one round (epoch) into buffer set `buf`:
+/* Dispatch of one round (epoch) into buffer set `buf` (Sec. 2.2: a DMA engine moves only
+ * contiguous regions, so the routed rows are packed first; Sec. 4.3: the host leg runs on
+ * a DMA engine in chunks; Sec. 4.4: one completion flag per chunk, apart from the data):
  *   packed[slot_pos[t*k+j]][:] = x[t][:] for every token t and slot j   (bf16 byte copy)
  * into the staging's HBM send buffer.  x_dev: bf16 [T][H]; slot_pos: int32 [T*k] from
  * ep_dispatch_layout; rows with slot_pos outside [0, max_rows) are skipped.
@@ -258,7 +277,9 @@ ep_status ep_dispatch_fused(const int32_t *topk_idx, int64_t num_tokens, int32_t
                             const void *x_dev, int32_t hidden, ep_staging *s, int32_t buf, uint32_t epoch,
                             hipStream_t stream);
 
-/* Combine of one round from buffer set `buf`:
+/* Combine of one round from buffer set `buf` (Sec. 4.4: wait for every sender's flag,
+ * polling sparingly; Sec. 4.3: the gate-weighted reduction runs on the GPU, a DMA engine
+ * cannot add):
  *   out[t][:] = sum_{j<k} topk_w[t*k+j] * recv[slot_pos[t*k+j]][:]
  * accumulated in fp32 with fused multiply-adds in slot order j = 0..k-1, then rounded
  * to nearest-even bf16 (EP_OUT_BF16) or stored as fp32 (EP_OUT_F32).  recv holds the

@@ -15,7 +15,7 @@ EP_STAGING_HBM, EP_STAGING_PINNED_HOST = 0, 1
 EP_OUT_BF16, EP_OUT_F32 = 0, 1
 EP_SIM_FLAGS_ONLY, EP_SIM_ECHO = 0, 1
 EP_MODE_PER_SENDER, EP_MODE_DUPLEX, EP_MODE_REMOTE_ONLY, EP_MODE_ACCUMULATE = 1, 2, 4, 8
-ABI_VERSION = 3
+ABI_VERSION = 4
 EP_MAX_EXPERTS = 2048
 
 c_i32, c_i64, c_u32, c_size, c_vp = ctypes.c_int32, ctypes.c_int64, ctypes.c_uint32, ctypes.c_size_t, ctypes.c_void_p
@@ -55,10 +55,10 @@ SIGNATURES = {
     "ep_layout_workspace_bytes": (c_i32, [c_i64, c_i32, c_i32, ctypes.POINTER(c_size)]),
     "ep_dispatch_layout": (c_i32, [c_vp, c_i64, c_i32, c_i32, c_i32, c_vp, c_vp, c_vp, c_vp, c_vp, c_vp,
                                    c_vp, c_size, c_vp]),
-    "ep_layout_status": (c_i32, [c_vp, c_vp]),
+    "ep_layout_validate": (c_i32, [c_vp, c_vp]),
     "ep_staging_alloc": (c_i32, [c_i32, c_i64, c_i32, c_i32, c_i32, c_i64, ctypes.POINTER(c_vp)]),
     "ep_staging_free": (c_i32, [c_vp]),
-    "ep_staging_get": (c_i32, [c_vp, c_i32, ctypes.POINTER(StagingView)]),
+    "ep_staging_ptrs": (c_i32, [c_vp, c_i32, ctypes.POINTER(StagingView)]),
     "ep_staging_set_wait": (c_i32, [c_vp, c_i64, c_i32]),
     "ep_staging_status": (c_i32, [c_vp, c_vp]),
     "ep_staging_set_mode": (c_i32, [c_vp, c_u32, c_i32]),

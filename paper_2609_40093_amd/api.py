@@ -21,7 +21,7 @@ from ._lib import (EP_OK, EP_ERR_BAD_ROUTING, EP_ERR_TIMEOUT, EP_STAGING_HBM, EP
 MODE_PER_SENDER, MODE_DUPLEX, MODE_REMOTE_ONLY = _lib.EP_MODE_PER_SENDER, _lib.EP_MODE_DUPLEX, _lib.EP_MODE_REMOTE_ONLY
 MODE_ACCUMULATE = _lib.EP_MODE_ACCUMULATE
 
-__all__ = ["EPError", "Layout", "Staging", "SimPeers", "dispatch_layout", "layout_status", "dispatch",
+__all__ = ["EPError", "Layout", "Staging", "SimPeers", "dispatch_layout", "layout_validate", "dispatch",
            "combine", "trace_enable", "trace_read", "trace_reset", "copy_probe", "workspace_bytes",
            "pcie_probe", "MODE_PER_SENDER", "MODE_DUPLEX", "MODE_REMOTE_ONLY", "MODE_ACCUMULATE", "LocalLayout",
            "dispatch_layout_local", "pack", "combine_rows", "Dense", "allgather", "reducescatter",
@@ -203,9 +203,9 @@ def combine_rows(y: torch.Tensor, slot_pos: torch.Tensor, topk_w: torch.Tensor, 
     return out
 
 
-def layout_status(layout: Layout, stream=None) -> None:
+def layout_validate(layout: Layout, stream=None) -> None:
     """Synchronizes and raises EPError(EP_ERR_BAD_ROUTING) if the routing was rejected."""
-    _check(_lib_handle().ep_layout_status(_ptr(layout.workspace), _stream_ptr(stream)), "ep_layout_status")
+    _check(_lib_handle().ep_layout_validate(_ptr(layout.workspace), _stream_ptr(stream)), "ep_layout_validate")
 
 
 class Staging:
@@ -229,7 +229,7 @@ class Staging:
 
     def _view(self, buf: int) -> _lib.StagingView:
         v = _lib.StagingView()
-        _check(_lib_handle().ep_staging_get(self.handle, buf, ctypes.byref(v)), "ep_staging_get")
+        _check(_lib_handle().ep_staging_ptrs(self.handle, buf, ctypes.byref(v)), "ep_staging_ptrs")
         return v
 
     def close(self):

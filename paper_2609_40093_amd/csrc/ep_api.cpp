@@ -312,9 +312,9 @@ extern "C" ep_status ep_combine_rows(const void *y_dev, int64_t max_rows, const 
     return EP_OK;
 }
 
-extern "C" ep_status ep_layout_status(const void *workspace, hipStream_t stream) {
+extern "C" ep_status ep_layout_validate(const void *workspace, hipStream_t stream) {
     if (!workspace)
-        return fail(EP_ERR_INVALID_ARG, "ep_layout_status: workspace is NULL");
+        return fail(EP_ERR_INVALID_ARG, "ep_layout_validate: workspace is NULL");
     EP_HIP(hipStreamSynchronize(stream));
     uint32_t word = 0, timed_out = 0;
     EP_HIP(hipMemcpy(&word, workspace, sizeof word, hipMemcpyDeviceToHost));
@@ -478,11 +478,11 @@ extern "C" ep_status ep_staging_free(ep_staging *s) {
     return EP_OK;
 }
 
-extern "C" ep_status ep_staging_get(ep_staging *s, int32_t buf, ep_staging_view *v) {
+extern "C" ep_status ep_staging_ptrs(ep_staging *s, int32_t buf, ep_staging_view *v) {
     if (!s || !v)
-        return fail(EP_ERR_INVALID_ARG, "ep_staging_get: NULL argument");
+        return fail(EP_ERR_INVALID_ARG, "ep_staging_ptrs: NULL argument");
     if (buf < 0 || buf >= s->num_buffers)
-        return fail(EP_ERR_INVALID_ARG, "ep_staging_get: buffer %d of %d", buf, s->num_buffers);
+        return fail(EP_ERR_INVALID_ARG, "ep_staging_ptrs: buffer %d of %d", buf, s->num_buffers);
     const bool pinned = s->kind == EP_STAGING_PINNED_HOST;
     v->kind = s->kind;
     v->num_ranks = s->num_ranks;

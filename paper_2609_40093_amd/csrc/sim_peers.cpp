@@ -92,7 +92,7 @@ struct ep_sim_peers {
     void run_graph() {
         for (uint32_t r = 1;; ++r) {
             ep_staging_view v;
-            if (ep_staging_get(s, (int32_t)(r & 1u), &v) != EP_OK)
+            if (ep_staging_ptrs(s, (int32_t)(r & 1u), &v) != EP_OK)
                 return;
             if (!wait_word(v.send_flags, r) || !wait_word(v.recv_credit, r - 2u))
                 return;
@@ -152,7 +152,7 @@ struct ep_sim_peers {
             return;
         }
         ep_staging_view v;
-        if (ep_staging_get(s, r.buf, &v) != EP_OK)
+        if (ep_staging_ptrs(s, r.buf, &v) != EP_OK)
             return;
         if ((v.mode & EP_MODE_DUPLEX) && v.in_flags) {
             for (int i : by_delay(r.inbound_us)) {
@@ -196,7 +196,7 @@ extern "C" ep_status ep_sim_peers_start(ep_staging *s, ep_sim_mode mode, ep_sim_
     if (!s || !out || (mode != EP_SIM_FLAGS_ONLY && mode != EP_SIM_ECHO))
         return EP_ERR_INVALID_ARG;
     ep_staging_view v;
-    if (ep_staging_get(s, 0, &v) != EP_OK || v.kind != EP_STAGING_PINNED_HOST)
+    if (ep_staging_ptrs(s, 0, &v) != EP_OK || v.kind != EP_STAGING_PINNED_HOST)
         return EP_ERR_INVALID_ARG;
     ep_sim_peers *p = new ep_sim_peers();
     p->s = s;
@@ -211,7 +211,7 @@ extern "C" ep_status ep_sim_peers_post(ep_sim_peers *p, int32_t buf, uint32_t ep
     if (!p || p->dense || rows < 0 || delay_us < 0)
         return EP_ERR_INVALID_ARG;
     ep_staging_view v;
-    if (ep_staging_get(p->s, buf, &v) != EP_OK || rows > v.max_rows)
+    if (ep_staging_ptrs(p->s, buf, &v) != EP_OK || rows > v.max_rows)
         return EP_ERR_INVALID_ARG;
     {
         std::lock_guard<std::mutex> lk(p->mu);
@@ -232,7 +232,7 @@ int sim_ranks(ep_sim_peers *p) {
         return ep_dense_get(p->dense, 0, &v) == EP_OK ? v.num_ranks : -1;
     }
     ep_staging_view v;
-    return ep_staging_get(p->s, 0, &v) == EP_OK ? v.num_ranks : -1;
+    return ep_staging_ptrs(p->s, 0, &v) == EP_OK ? v.num_ranks : -1;
 }
 }  // namespace
 
@@ -291,7 +291,7 @@ extern "C" ep_status ep_sim_graph_start(ep_staging *s, int64_t rows, int64_t del
     if (!s || !out || rows < 0 || delay_us < 0)
         return EP_ERR_INVALID_ARG;
     ep_staging_view v;
-    if (ep_staging_get(s, 0, &v) != EP_OK || v.kind != EP_STAGING_PINNED_HOST || v.num_buffers != 2 ||
+    if (ep_staging_ptrs(s, 0, &v) != EP_OK || v.kind != EP_STAGING_PINNED_HOST || v.num_buffers != 2 ||
         rows > v.max_rows)
         return EP_ERR_INVALID_ARG;
     ep_sim_peers *p = new ep_sim_peers();

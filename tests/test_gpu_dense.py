@@ -90,11 +90,11 @@ def test_window_layout_routing_errors():
     idx = np.array([[0, 1], [2, 2], [3, 0]], np.int32)       # a duplicate outside the window
     lay = ep.dispatch_layout_local(torch.from_numpy(idx).to(DEV), 4, 0, 2)
     with pytest.raises(ep.EPError, match="repeated"):
-        ep.layout_status(lay)
+        ep.layout_validate(lay)
     idx = np.array([[0, 1], [9, 2]], np.int32)
     lay = ep.dispatch_layout_local(torch.from_numpy(idx).to(DEV), 4, 0, 2)
     with pytest.raises(ep.EPError, match="outside"):
-        ep.layout_status(lay)
+        ep.layout_validate(lay)
 
 
 def run_dense_layer(R, me, T, H, E, k, block_dtype, per_sender, on_host, rounds=2, seed=0):

@@ -20,7 +20,7 @@ def test_out_of_range_ids_are_reported():
     idx[4321, 0] = -3
     lay = ep.dispatch_layout(torch.from_numpy(idx).to(DEV), 16, 4)
     with pytest.raises(ep.EPError) as ei:
-        ep.layout_status(lay)
+        ep.layout_validate(lay)
     assert ei.value.status == 2 and "outside" in str(ei.value)
     sp = lay.slot_pos.cpu().numpy()
     assert sp[17 * 2 + 1] == -1 and sp[4321 * 2] == -1
@@ -40,11 +40,11 @@ def test_duplicate_expert_in_a_row_is_reported():
     idx[100, 3] = idx[100, 0]
     lay = ep.dispatch_layout(torch.from_numpy(idx).to(DEV), 16, 4)
     with pytest.raises(ep.EPError) as ei:
-        ep.layout_status(lay)
+        ep.layout_validate(lay)
     assert ei.value.status == 2 and "repeated" in str(ei.value)
     # the next good routing on the same workspace clears the status
     lay = ep.dispatch_layout(torch.from_numpy(case.topk_idx).to(DEV), 16, 4, out=lay)
-    ep.layout_status(lay)
+    ep.layout_validate(lay)
 
 
 def test_host_checked_arguments():

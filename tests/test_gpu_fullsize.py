@@ -49,7 +49,7 @@ def test_prefill_full_size(prefill, staging):
     say(f"prefill full size, {staging} staging: layout")
     idx = torch.from_numpy(inp.topk_idx).to(DEV)
     lay = ep.dispatch_layout(idx, E, R)
-    ep.layout_status(lay)
+    ep.layout_validate(lay)
     for key in ("expert_counts", "expert_offsets", "rank_counts", "rank_offsets", "slot_pos", "row_src"):
         assert np.array_equal(getattr(lay, key).cpu().numpy(), getattr(ref, key)), key
 
@@ -139,7 +139,7 @@ def test_coarse_layer_as_the_benchmark_runs_it():
     assert "layout_pack" in ep.trace_read(), "the one-kernel dispatch did not run"
     ep.trace_reset()
     for b, s in enumerate(sets):
-        ep.layout_status(s["lay"])
+        ep.layout_validate(s["lay"])
         for key in ("expert_counts", "expert_offsets", "rank_counts", "rank_offsets", "slot_pos", "row_src"):
             assert np.array_equal(getattr(s["lay"], key).cpu().numpy(), getattr(ref, key)), f"set {b}: {key}"
         packed = st.read_device("send", n, buf=b).cpu().numpy().view(np.uint16)

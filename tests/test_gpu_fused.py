@@ -112,7 +112,7 @@ def test_fused_matches_oracle_and_two_calls(spec):
     st = ep.Staging("hbm", T * k, H, R, num_buffers=2)
     lay, kernels = run_fused(idx_d, x_d, E, R, st, buf=1)
     assert "layout_pack" in kernels and "layout" not in kernels and "pack" not in kernels, kernels
-    ep.layout_status(lay)
+    ep.layout_validate(lay)
     got = layout_np(lay)
     for key in LAYOUT_KEYS:
         assert np.array_equal(got[key], getattr(ref, key)), f"{key} differs from the oracle"
@@ -134,7 +134,7 @@ def test_fused_workloads_tiny_and_coarse():
         st = ep.Staging("hbm", case.slots, case.H, case.R, num_buffers=1)
         lay, kernels = run_fused(to_dev(case.topk_idx), to_dev(case.x.view(np.int16)), case.E, case.R, st)
         assert "layout_pack" in kernels
-        ep.layout_status(lay)
+        ep.layout_validate(lay)
         assert np.array_equal(lay.slot_pos.cpu().numpy(), ref.slot_pos)
         assert np.array_equal(lay.rank_offsets.cpu().numpy(), ref.rank_offsets)
         packed = st.read_device("send", case.slots).cpu().numpy().view(np.uint16)
@@ -152,7 +152,7 @@ def test_fused_repeated_calls_reuse_buffers():
         say(f"fused round {r}")
         lay = ep.dispatch_fused(to_dev(case.x.view(np.int16)), to_dev(case.topk_idx), E, R, st, buf=r % 2,
                                 epoch=r + 1, out=lay)
-        ep.layout_status(lay)
+        ep.layout_validate(lay)
         ref = oracle.layout(case.topk_idx, E, R)
         assert np.array_equal(lay.slot_pos.cpu().numpy(), ref.slot_pos), f"round {r}"
         assert np.array_equal(lay.expert_counts.cpu().numpy(), ref.expert_counts), f"round {r}"
@@ -183,7 +183,7 @@ def test_fallback_runs_two_kernels(spec):
     st = ep.Staging("hbm", T * k, H, R, num_buffers=1)
     lay, kernels = run_fused(to_dev(case.topk_idx), to_dev(case.x.view(np.int16)), E, R, st)
     assert "layout_pack" not in kernels and {"layout", "pack"} <= kernels, kernels
-    ep.layout_status(lay)
+    ep.layout_validate(lay)
     assert np.array_equal(lay.slot_pos.cpu().numpy(), ref.slot_pos)
     packed = st.read_device("send", T * k).cpu().numpy().view(np.uint16)
     assert packed.tobytes() == oracle.pack(case.x, ref.slot_pos, k).tobytes()
@@ -201,7 +201,7 @@ def test_misaligned_routing_falls_back():
     st = ep.Staging("hbm", T * k, H, R, num_buffers=1)
     lay, kernels = run_fused(idx_d, to_dev(case.x.view(np.int16)), E, R, st)
     assert "layout_pack" not in kernels
-    ep.layout_status(lay)
+    ep.layout_validate(lay)
     ref = oracle.layout(case.topk_idx, E, R)
     assert np.array_equal(lay.slot_pos.cpu().numpy(), ref.slot_pos)
     st.close()
@@ -224,7 +224,7 @@ def test_fused_routing_errors_match_two_calls(k, E):
     lay, kernels = run_fused(idx_d, x_d, E, R, st, buf=0)
     assert "layout_pack" in kernels
     with pytest.raises(ep.EPError) as ei:
-        ep.layout_status(lay)
+        ep.layout_validate(lay)
     assert ei.value.status == 2
     msg = str(ei.value)
     assert "outside" in msg and (k == 1 or "repeated" in msg), msg
@@ -232,7 +232,7 @@ def test_fused_routing_errors_match_two_calls(k, E):
     assert got["slot_pos"][5 * k] == -1 and got["slot_pos"][321 * k + k - 1] == -1
     lay2 = run_two_calls(idx_d, x_d, E, R, st, k, buf=1)
     with pytest.raises(ep.EPError):
-        ep.layout_status(lay2)
+        ep.layout_validate(lay2)
     for key in LAYOUT_KEYS:
         if key == "row_src":   # rows no slot maps to are left unwritten by both paths
             continue
@@ -244,7 +244,7 @@ def test_fused_routing_errors_match_two_calls(k, E):
     assert a.tobytes() == b.tobytes()
     # the next good routing on the same workspace clears the status
     lay = ep.dispatch_fused(x_d, to_dev(case.topk_idx), E, R, st, out=lay)
-    ep.layout_status(lay)
+    ep.layout_validate(lay)
     st.close()
 
 
@@ -263,10 +263,10 @@ def test_fused_k8_repeated_expert(first, second):
     lay, kernels = run_fused(idx_d, x_d, E, R, st, buf=0)
     assert "layout_pack" in kernels
     with pytest.raises(ep.EPError, match="repeated"):
-        ep.layout_status(lay)
+        ep.layout_validate(lay)
     lay2 = run_two_calls(idx_d, x_d, E, R, st, 8, buf=1)
     with pytest.raises(ep.EPError, match="repeated"):
-        ep.layout_status(lay2)
+        ep.layout_validate(lay2)
     for key in LAYOUT_KEYS:
         assert np.array_equal(getattr(lay2, key).cpu().numpy(), getattr(lay, key).cpu().numpy()), key
     st.close()
@@ -386,7 +386,7 @@ def test_fused_dispatch_and_combine_replay_in_a_graph():
         w.copy_(to_dev(case.topk_w))
         g.replay()
         torch.cuda.synchronize()
-        ep.layout_status(lay)
+        ep.layout_validate(lay)
         ref = oracle.layout(case.topk_idx, E, R)
         for key in LAYOUT_KEYS:
             assert np.array_equal(getattr(lay, key).cpu().numpy(), getattr(ref, key)), f"replay {rep}: {key}"
@@ -428,7 +428,7 @@ def test_fused_random_shapes(spec):
     st = ep.Staging("hbm", T * k, H, R, num_buffers=1)
     lay, kernels = run_fused(to_dev(case.topk_idx), to_dev(case.x.view(np.int16)), E, R, st)
     assert "layout_pack" in kernels, kernels
-    ep.layout_status(lay)
+    ep.layout_validate(lay)
     for key in LAYOUT_KEYS:
         assert np.array_equal(getattr(lay, key).cpu().numpy(), getattr(ref, key)), f"{key} differs"
     packed = st.read_device("send", T * k).cpu().numpy().view(np.uint16)

@@ -39,7 +39,7 @@ def run_hip(case, out_f32=False):
     """layout -> dispatch -> combine through libep with HBM staging."""
     idx = torch.from_numpy(case.topk_idx).to(DEV)
     lay = ep.dispatch_layout(idx, case.E, case.R)
-    ep.layout_status(lay)
+    ep.layout_validate(lay)
     st = ep.Staging("hbm", max(1, case.slots), case.H, case.R, num_buffers=1)
     ep.dispatch(dev_bits(case.x), lay.slot_pos, st, topk=case.k)
     packed = host_bits(st.read_device("send", case.slots))
@@ -161,7 +161,7 @@ def test_empty_batch():
     say("empty batch")
     idx = torch.zeros((0, 2), dtype=torch.int32, device=DEV)
     lay = ep.dispatch_layout(idx, 8, 4)
-    ep.layout_status(lay)
+    ep.layout_validate(lay)
     assert lay.expert_counts.cpu().tolist() == [0] * 8
     assert lay.expert_offsets.cpu().tolist() == [0] * 9
     assert lay.rank_offsets.cpu().tolist() == [0] * 5
@@ -186,7 +186,7 @@ def test_layout_deterministic():
         if first is None:
             first = cur
         assert np.array_equal(cur, first)
-    ep.layout_status(lay)
+    ep.layout_validate(lay)
 
 
 def test_workspace_reused_across_sizes():
@@ -207,7 +207,7 @@ def test_workspace_reused_across_sizes():
         st = lib.ep_dispatch_layout(api._ptr(idx), T, k, E, R, *[api._ptr(t) for t in outs],
                                     api._ptr(ws), ws.numel(), api._stream_ptr(None))
         assert st == 0, lib.ep_last_error()
-        assert lib.ep_layout_status(api._ptr(ws), api._stream_ptr(None)) == 0, lib.ep_last_error()
+        assert lib.ep_layout_validate(api._ptr(ws), api._stream_ptr(None)) == 0, lib.ep_last_error()
         for got, key in zip(outs, ("expert_counts", "expert_offsets", "rank_counts", "rank_offsets",
                                    "slot_pos", "row_src")):
             assert np.array_equal(got.cpu().numpy(), getattr(want, key)), f"step {step}: {key} differs"

@@ -25,7 +25,7 @@ def dev_bits(a):
 
 def layout_of(case):
     lay = ep.dispatch_layout(torch.from_numpy(case.topk_idx).to(DEV), case.E, case.R)
-    ep.layout_status(lay)
+    ep.layout_validate(lay)
     return lay
 
 
