@@ -37,10 +37,12 @@ def parse():
     p.add_argument("--gpus", type=int, default=1)
     p.add_argument("--steps", type=int, default=200)
     p.add_argument("--warmup", type=int, default=10)
-    p.add_argument("--workload", default="coarse", help="synth config name (default: the coarse-expert layer)")
+    p.add_argument("--workload", default="prefill",
+                   help="synth config name (default: the large prefill layer, T=32768, H=7168, top-8 of 256)")
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--no-pinned", action="store_true")
-    p.add_argument("--cpu-seconds", type=float, default=10.0)
+    p.add_argument("--cpu-seconds", type=float, default=10.0,
+                   help="least host time spent on each CPU-baseline figure (whole layers only)")
     p.add_argument("--chunk-mib", type=int, default=16, help="device->host DMA chunk of the pinned legs")
     return p.parse_args()
 
@@ -129,11 +131,10 @@ def main():
     torch.cuda.synchronize()
 
     def step(i, trace=None, fused=True):
-        """One layer; `trace` names the call ("dispatch" or "combine") whose kernels are
-        bracketed by timing events, so that measuring costs the host almost nothing.
-        fused=False: layout and dispatch as two calls (two kernels)."""
+        """One layer; `trace` names the call ("dispatch", "combine" or "both") whose kernels
+        are bracketed by timing events.  fused=False: layout and dispatch as two calls."""
         st = sets[i % nsets]
-        if trace == "dispatch":
+        if trace in ("dispatch", "both"):
             ep.trace_enable(True)
         if fused:
             st["lay"] = ep.dispatch_fused(st["x"], st["idx"], E, R, staging, buf=i % nsets, epoch=i + 1,
@@ -146,7 +147,7 @@ def main():
         elif trace == "combine":
             ep.trace_enable(True)
         ep.combine(staging, st["lay"].slot_pos, st["w"], out=st["out"], buf=i % nsets, epoch=i + 1)
-        if trace == "combine":
+        if trace in ("combine", "both"):
             ep.trace_enable(False)
 
     # ---- HBM staging: warmup, then exactly K timed steps; the dispatch and combine
@@ -155,57 +156,76 @@ def main():
         step(i)
     ep.layout_validate(sets[0]["lay"])
     torch.cuda.synchronize()
+    probe0 = time.perf_counter()
+    step(args.warmup)
+    torch.cuda.synchronize()
+    probe_us = (time.perf_counter() - probe0) * 1e6
+    # Events cost the stream ~2 us per traced launch: on layers of a few hundred us or
+    # more, every kernel of every timed step carries them (< 1% of the step); on shorter
+    # layers one step in eight does, alternating between the dispatch and the combine.
+    every = probe_us > 300.0
+    cadence = ("both",) if every else ("dispatch", None, None, None, "combine", None, None, None)
     ep.trace_reset()
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    # one step in eight carries timing events (they cost the stream ~2 us per traced
-    # launch), alternating between the dispatch and the combine
     for i in range(args.steps):
-        step(args.warmup + i, trace=("dispatch", None, None, None, "combine", None, None, None)[i % 8])
+        step(args.warmup + i, trace=cadence[i % len(cadence)])
     t_issue = time.perf_counter()
     torch.cuda.synchronize()
     t1 = time.perf_counter()
-    kstats = ep.trace_read()
+    timed_stats = ep.trace_read()
     ms_per_step = (t1 - t0) * 1e3 / args.steps
     value = 2 * payload / (ms_per_step * 1e-3) / 1e9
     issue_us = (t_issue - t0) * 1e6 / args.steps
     # warm cache, beside the headline: every step on buffer set 0 (inputs and staging
-    # stay in the 256 MB memory-side cache between steps)
-    for i in range(args.warmup):
-        step(i * nsets)
-    torch.cuda.synchronize()
-    w0 = time.perf_counter()
-    for i in range(args.steps):
-        step((args.warmup + i) * nsets)
-    torch.cuda.synchronize()
-    warm_ms = (time.perf_counter() - w0) * 1e3 / args.steps
-    # breakdown pass (not timed): every kernel of every step bracketed by events
+    # stay in the 256 MB memory-side cache between steps); meaningless when one set is
+    # larger than that cache
+    warm = None
+    if step_bytes < MALL_BYTES:
+        for i in range(args.warmup):
+            step(i * nsets)
+        torch.cuda.synchronize()
+        w0 = time.perf_counter()
+        for i in range(args.steps):
+            step((args.warmup + i) * nsets)
+        torch.cuda.synchronize()
+        warm = (time.perf_counter() - w0) * 1e3 / args.steps
+    # breakdown pass (not timed): every kernel of at least 50 steps bracketed by events
+    breakdown_steps = max(args.steps, 50)
     ep.trace_reset()
     ep.trace_enable(True)
-    for i in range(args.steps):
+    for i in range(breakdown_steps):
         step(args.warmup + args.steps + i)
     torch.cuda.synchronize()
     ep.trace_enable(False)
     breakdown = ep.trace_read()
+    # the roofline's launch averages: every launch of the timed region when every one was
+    # traced, else the breakdown pass (every launch of its steps)
+    kstats = dict(timed_stats) if every else dict(breakdown)
     for name, st_ in breakdown.items():
-        if name not in kstats:
-            kstats[name] = st_
-    # the two-kernel path (layout, then pack) on the same steps, for comparison
-    for i in range(args.warmup):
-        step(i, fused=False)
-    torch.cuda.synchronize()
-    u0 = time.perf_counter()
-    for i in range(args.steps):
-        step(args.warmup + i, fused=False)
-    torch.cuda.synchronize()
-    two_ms = (time.perf_counter() - u0) * 1e3 / args.steps
-    ep.trace_reset()
-    ep.trace_enable(True)
-    for i in range(args.steps):
-        step(args.warmup + args.steps + i, fused=False)
-    torch.cuda.synchronize()
-    ep.trace_enable(False)
-    two_kernels = {name: round(st_["mean_ms"] * 1e3, 3) for name, st_ in ep.trace_read().items()}
+        kstats.setdefault(name, st_)
+    # the two-kernel path (layout, then pack) on the same steps, for comparison, when the
+    # one-kernel dispatch covered this layer (its kernel shows in the trace)
+    two = None
+    if "layout_pack" in kstats:
+        for i in range(args.warmup):
+            step(i, fused=False)
+        torch.cuda.synchronize()
+        u0 = time.perf_counter()
+        for i in range(args.steps):
+            step(args.warmup + i, fused=False)
+        torch.cuda.synchronize()
+        two_ms = (time.perf_counter() - u0) * 1e3 / args.steps
+        ep.trace_reset()
+        ep.trace_enable(True)
+        for i in range(args.steps):
+            step(args.warmup + args.steps + i, fused=False)
+        torch.cuda.synchronize()
+        ep.trace_enable(False)
+        two = {"note": "the same layer with layout and pack as two calls (two kernels); event-bracketed kernel "
+                       "averages",
+               "us_per_layer": round(two_ms * 1e3, 2), "payload_GBps": round(2 * payload / (two_ms * 1e-3) / 1e9, 1),
+               "kernel_avg_us": {name: round(st_["mean_ms"] * 1e3, 3) for name, st_ in ep.trace_read().items()}}
 
     abytes = algorithmic_bytes(cfg)
     kernels = {}
@@ -214,7 +234,8 @@ def main():
         entry = {"launches": st["count"], "avg_us": round(us, 3),
                  "p10_us": round(st["p10_ms"] * 1e3, 3), "p50_us": round(st["p50_ms"] * 1e3, 3),
                  "p90_us": round(st["p90_ms"] * 1e3, 3),
-                 "measured": "timed region" if name in TIMED_KERNELS else "breakdown pass"}
+                 "measured": ("timed region, every launch" if every else "breakdown pass, every launch")
+                 if name in timed_stats or name in breakdown else "breakdown pass"}
         if name in abytes and us > 0:
             entry["algorithmic_bytes"] = abytes[name]
             entry["GBps"] = round(abytes[name] / (us * 1e-6) / 1e9, 1)
@@ -271,31 +292,32 @@ def main():
             "traffic": traffic,
             "algorithmic_bytes_per_launch": dk.get("algorithmic_bytes"),
             "avg_launch_us": dk.get("avg_us"),
+            "p50_launch_us": dk.get("p50_us"),
+            "launches_averaged": dk.get("launches"),
+            "measured": dk.get("measured"),
             "dispatch_and_combine": pair_roofline(kernels),
         },
         "kernels": kernels,
-        "warm_cache": {
-            "note": "the same steps on one buffer set: inputs and staging stay in the memory-side cache "
-                    "(the headline rotates sets so that they do not)",
-            "us_per_layer": round(warm_ms * 1e3, 2),
-            "payload_GBps": round(2 * payload / (warm_ms * 1e-3) / 1e9, 1),
-        },
-        "two_kernel_dispatch": {
-            "note": "the same layer with layout and pack as two calls (two kernels); event-bracketed kernel averages",
-            "us_per_layer": round(two_ms * 1e3, 2),
-            "payload_GBps": round(2 * payload / (two_ms * 1e-3) / 1e9, 1),
-            "kernel_avg_us": two_kernels,
-        },
         "hbm_copy_probe_GBps": round(copy_gbps, 1),
         "same_bytes_copy": dict(same_copy, kernel=dominant,
                                 kernel_speed_vs_copy=round(same_copy["avg_us"] / dk["avg_us"], 3)),
     }
+    if warm is not None:
+        result["warm_cache"] = {
+            "note": "the same steps on one buffer set: inputs and staging stay in the memory-side cache "
+                    "(the headline rotates sets so that they do not)",
+            "us_per_layer": round(warm * 1e3, 2),
+            "payload_GBps": round(2 * payload / (warm * 1e-3) / 1e9, 1),
+        }
+    if two is not None:
+        result["two_kernel_dispatch"] = two
 
     # ---- pinned host staging: the same layer with SDMA legs, host flags, simulated peers
     if not args.no_pinned:
         result["pinned_staging"] = bench_pinned(cfg, inp, y, args, dev)
 
-    # ---- CPU baseline: the oracle, single-threaded, on whole layers of the same workload
+    # ---- CPU baseline: the oracle on whole layers of the same workload, on all the host
+    #      cores this process may use, and on one
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(cfg, inp, y, args.cpu_seconds)
 
@@ -749,24 +771,68 @@ def same_bytes_copy(dev, nbytes: int, nsets: int, launches: int = 40) -> dict:
             "p50_us": round(st["p50_ms"] * 1e3, 3), "GBps": round(2 * half / (us * 1e-6) / 1e9, 1)}
 
 
+def cpu_model() -> str:
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
 def cpu_baseline(cfg, inp, y, seconds: float) -> dict:
-    """The oracle as it stands (plain C, one thread) over whole layers of the workload."""
+    """The oracle as it stands (plain C, fp64 sums) over whole layers of the workload: its
+    layout, pack and combine, on every host core this process may use (the oracle's token
+    loops split over threads, outputs identical to one thread's), and on one thread.  The
+    output arrays are allocated and touched once before the clock starts, so that the
+    figure is the oracle's work and not the host's first-touch page faults; each figure
+    runs whole layers until `seconds` have passed (at least one)."""
+    import numpy as np
+
     import oracle
-    oracle.load()
-    passes, t0 = 0, time.perf_counter()
-    while True:
-        lay = oracle.layout(inp.topk_idx, cfg.E, cfg.R)
-        oracle.pack(inp.x, lay.slot_pos, cfg.k)
-        oracle.combine(y, lay.slot_pos, inp.topk_w)
-        passes += 1
-        el = time.perf_counter() - t0
-        if el >= seconds:
-            break
-    return {"value": round(2 * cfg.payload_bytes * passes / el / 1e9, 4), "unit": "GB/s", "cores": 1,
-            "kind": "oracle",
-            "sample": f"{passes} whole {cfg.name} layers (layout + pack + combine with fp64 sums), "
-                      f"{el:.1f} s on one host thread",
-            "us_per_layer": round(el / passes * 1e6, 1)}
+    lib = oracle.load()
+    T, H, k = cfg.T, cfg.H, cfg.k
+    x = np.ascontiguousarray(inp.x)
+    w = np.ascontiguousarray(inp.topk_w)
+    y = np.ascontiguousarray(y)
+    packed = np.empty((max(T * k, 1), H), np.uint16)
+    exact = np.empty((max(T, 1), H), np.float64)
+    b16 = np.empty((max(T, 1), H), np.uint16)
+    f32 = np.empty((max(T, 1), H), np.float32)
+    for a in (packed, exact, b16, f32):
+        a.fill(0)
+
+    def layers(threads: int):
+        oracle.set_threads(threads)
+        passes, t0 = 0, time.perf_counter()
+        try:
+            while True:
+                lay = oracle.layout(inp.topk_idx, cfg.E, cfg.R, lib=lib)
+                sp = np.ascontiguousarray(lay.slot_pos)
+                lib.ep_oracle_pack(x, T, H, k, sp, packed)
+                lib.ep_oracle_combine(y, sp, w, T, H, k, exact.ctypes.data, b16.ctypes.data, f32.ctypes.data)
+                passes += 1
+                el = time.perf_counter() - t0
+                if el >= seconds:
+                    return passes, el
+        finally:
+            oracle.set_threads(1)
+
+    cores = len(os.sched_getaffinity(0))
+    res = {}
+    for name, threads in (("all_cores", cores), ("single_thread", 1)):
+        passes, el = layers(threads)
+        res[name] = {"value": round(2 * cfg.payload_bytes * passes / el / 1e9, 4), "unit": "GB/s",
+                     "cores": threads, "us_per_layer": round(el / passes * 1e6, 1),
+                     "sample": f"{passes} whole {cfg.name} layer(s) (layout + pack + combine with fp64 sums), "
+                               f"{el:.1f} s on {threads} host thread(s)"}
+    top = dict(res["all_cores"])
+    top.update(kind="oracle", cpu_model=cpu_model(), cores_available=cores,
+               single_thread=res["single_thread"],
+               note="the oracle's token loops of pack and combine split over threads (OpenMP); its layout's "
+                    "counting pass runs on one thread; outputs identical for any thread count")
+    return top
 
 
 if __name__ == "__main__":

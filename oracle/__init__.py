@@ -28,7 +28,7 @@ import numpy as np
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _SRC = os.path.join(_HERE, "ep_oracle.c")
 LIB_PATH = os.path.join(_HERE, "libep_oracle.so")
-CFLAGS = ["-O2", "-std=c99", "-fPIC", "-shared", "-ffp-contract=off", "-fno-fast-math"]
+CFLAGS = ["-O2", "-std=c99", "-fPIC", "-shared", "-ffp-contract=off", "-fno-fast-math", "-fopenmp"]
 
 OK, INVALID_ARG, BAD_ROUTING = 0, 1, 2
 
@@ -63,6 +63,8 @@ def _bind(lib):
     lib.ep_oracle_local_layout.restype = ctypes.c_int
     lib.ep_oracle_local_layout.argtypes = [i32p, ctypes.c_int64, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32,
                                            ctypes.c_int32, i32p, i32p, i32p, vp]
+    lib.ep_oracle_set_threads.restype = ctypes.c_int
+    lib.ep_oracle_set_threads.argtypes = [ctypes.c_int]
     lib.ep_oracle_block_reduce.restype = None
     lib.ep_oracle_block_reduce.argtypes = [f64p, ctypes.c_int32, ctypes.c_int64, vp, vp, vp]
     return lib
@@ -149,6 +151,13 @@ def combine(y: np.ndarray, slot_pos: np.ndarray, topk_w: np.ndarray, lib=None):
                               w.reshape(-1), T, H, k, exact.ctypes.data, b16.ctypes.data,
                               f32.ctypes.data)
     return exact, b16, f32
+
+
+def set_threads(threads: int, lib=None) -> int:
+    """Host threads for pack and combine (1: the plain single-threaded oracle); the outputs
+    are the same for any count.  Returns the count in effect."""
+    lib = lib or load()
+    return int(lib.ep_oracle_set_threads(int(threads)))
 
 
 def double_to_bf16(v: np.ndarray, lib=None) -> np.ndarray:

@@ -10,6 +10,22 @@
 #include <math.h>
 #include <stdlib.h>
 #include <string.h>
+#ifdef _OPENMP
+#include <omp.h>
+#endif
+
+/* Threads over which pack and combine split their tokens (ep_oracle_set_threads). */
+static int g_threads = 1;
+
+int ep_oracle_set_threads(int threads) {
+#ifdef _OPENMP
+    g_threads = threads > 0 ? threads : 1;
+#else
+    (void)threads;
+    g_threads = 1;
+#endif
+    return g_threads;
+}
 
 /* ---- bf16 <-> double ------------------------------------------------------------ */
 
@@ -123,6 +139,8 @@ int ep_oracle_layout(const int32_t *topk_idx, int64_t T, int32_t k, int32_t E, i
 void ep_oracle_pack(const uint16_t *x, int64_t T, int32_t H, int32_t k,
                     const int32_t *slot_pos, uint16_t *packed) {
     const size_t row_bytes = (size_t)H * sizeof(uint16_t);
+    /* tokens are independent: each row is written by the thread of its token */
+#pragma omp parallel for schedule(static) num_threads(g_threads)
     for (int64_t t = 0; t < T; ++t)
         for (int32_t j = 0; j < k; ++j) {
             int64_t p = slot_pos[t * k + j];
@@ -135,9 +153,14 @@ void ep_oracle_pack(const uint16_t *x, int64_t T, int32_t H, int32_t k,
 void ep_oracle_combine(const uint16_t *y, const int32_t *slot_pos, const float *topk_w,
                        int64_t T, int32_t H, int32_t k,
                        double *out_exact, uint16_t *out_bf16, float *out_f32) {
+    /* tokens are independent: each token's sums are formed by one thread, in the order
+     * below, whatever the thread count */
+#pragma omp parallel num_threads(g_threads)
+    {
     double *acc = (double *)malloc(sizeof(double) * (size_t)(H > 0 ? H : 1));
     if (!acc)
         abort();
+#pragma omp for schedule(static)
     for (int64_t t = 0; t < T; ++t) {
         for (int32_t h = 0; h < H; ++h)
             acc[h] = 0.0;
@@ -162,6 +185,7 @@ void ep_oracle_combine(const uint16_t *y, const int32_t *slot_pos, const float *
         }
     }
     free(acc);
+    }
 }
 
 int ep_oracle_local_layout(const int32_t *topk_idx, int64_t N, int32_t k, int32_t E, int32_t e_lo,

@@ -93,6 +93,12 @@ uint16_t ep_oracle_double_to_bf16(double v);
 /* Element-wise ep_oracle_double_to_bf16 over n values. */
 void ep_oracle_double_to_bf16_n(const double *v, int64_t n, uint16_t *out);
 
+/* Host threads over which ep_oracle_pack and ep_oracle_combine split their tokens (1 by
+ * default: the plain single-threaded oracle).  Each token's rows and sums are computed by
+ * one thread exactly as in the single-threaded loops, so the outputs do not depend on the
+ * count.  Returns the count in effect (1 when the library was built without OpenMP). */
+int ep_oracle_set_threads(int threads);
+
 #ifdef __cplusplus
 }
 #endif

@@ -14,9 +14,8 @@ Recipe (numpy PCG64, ``SeedSequence(seed).spawn(4)``):
   bias / Zipf rank permutation, stream 3 -> returned expert outputs y.
   Large arrays are drawn in fixed row blocks, each block with its own spawned seed, so
   the result does not depend on how many threads draw them.
-  bf16 values are float32 normals truncated to their upper 16 bits (round toward zero):
-  a bf16-representable sample of the same distribution, produced without the rounding
-  step that the combine itself performs.
+  bf16 values are float32 normals rounded to the nearest bf16 value, ties to even (the
+  samples are finite, so the rounding never reaches infinity or NaN).
 """
 from __future__ import annotations
 
@@ -105,7 +104,8 @@ def normal_bf16_rows(ss: np.random.SeedSequence, rows: int, cols: int,
         np.random.default_rng(child).standard_normal(out=buf, dtype=np.float32)
         lo, hi = max(r0, row_begin), min(r1, row_end)
         bits = buf[lo - r0:hi - r0].view(np.uint32)
-        out[lo - row_begin:hi - row_begin] = (bits >> 16).astype(np.uint16)
+        bits = bits + (np.uint32(0x7FFF) + ((bits >> np.uint32(16)) & np.uint32(1)))
+        out[lo - row_begin:hi - row_begin] = (bits >> np.uint32(16)).astype(np.uint16)
 
     blocks = range(first, last + 1)
     if len(blocks) == 1:

@@ -103,3 +103,38 @@ def oracle_reference(case: Case):
     packed = oracle.pack(case.x, lay.slot_pos, case.k)
     exact, b16, f32 = oracle.combine(case.y, lay.slot_pos, case.topk_w)
     return lay, packed, exact, b16, f32
+
+
+def compare_packed_rows(get_rows, x: np.ndarray, row_src: np.ndarray, k: int, rows: int, what: str,
+                        chunk: int = 16384) -> None:
+    """Every packed row against the pack definition, `chunk` rows at a time: get_rows(r0,
+    r1) returns rows [r0, r1) as uint16 [r1-r0, H] (copied from the device or read from a
+    host bounce buffer); row p must equal x[row_src[p] // k] bit for bit."""
+    for r0 in range(0, rows, chunk):
+        r1 = min(rows, r0 + chunk)
+        got = get_rows(r0, r1)
+        want = oracle.pack_rows(x, row_src, k, np.arange(r0, r1))
+        if not np.array_equal(got, want):
+            bad = np.nonzero((got != want).any(axis=1))[0]
+            raise AssertionError(f"{what}: {len(bad)} packed rows differ in [{r0}, {r1}), first at row {r0 + bad[0]}")
+
+
+def compare_combine(get_tokens, y: np.ndarray, slot_pos: np.ndarray, topk_w: np.ndarray, what: str,
+                    chunk: int = 2048) -> None:
+    """Every combined token against the oracle's exact sums, `chunk` tokens at a time:
+    get_tokens(t0, t1) returns the bf16 bits of tokens [t0, t1).  Each chunk and the whole
+    output must be within max abs TOL_MAX_ABS, and the whole output within mean abs
+    TOL_MEAN_ABS."""
+    T, k = topk_w.shape
+    total, count, worst = 0.0, 0, 0.0
+    for t0 in range(0, T, chunk):
+        t1 = min(T, t0 + chunk)
+        slots = slot_pos[t0 * k:t1 * k]
+        exact, _, _ = oracle.combine_tokens(y[slots], topk_w[t0:t1])
+        got = synth.bf16_bits_to_f32(get_tokens(t0, t1)).astype(np.float64)
+        err = np.abs(got - exact)
+        worst = max(worst, float(err.max()) if err.size else 0.0)
+        total += float(err.sum())
+        count += err.size
+    mean = total / max(count, 1)
+    assert worst <= TOL_MAX_ABS and mean <= TOL_MEAN_ABS, f"{what}: combine error max {worst} mean {mean}"

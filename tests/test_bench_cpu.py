@@ -102,3 +102,25 @@ def test_a_failed_pinned_mode_reports_its_flag_words():
     got = bench.staging_flags(types.SimpleNamespace(views=[v]))
     assert got == {"0": {"mode": 9, "send": [5, 6], "recv": [1, 2, 3], "in": None, "ret": None, "in_landed": None,
                          "recv_landed": [7, 0, 7]}}
+
+
+def test_cpu_baseline_reports_all_cores_and_one():
+    """The CPU baseline times the oracle on whole layers on every core this process may use
+    and on one thread, and names the host's CPU model."""
+    cfg = synth.config("tiny")
+    inp = synth.make_inputs(cfg)
+    r = bench.cpu_baseline(cfg, inp, inp.expert_outputs(), 0.2)
+    assert r["kind"] == "oracle" and r["unit"] == "GB/s" and r["value"] > 0
+    assert r["cores"] == len(os.sched_getaffinity(0)) == r["cores_available"]
+    assert r["single_thread"]["cores"] == 1 and r["single_thread"]["value"] > 0
+    assert r["cpu_model"] and "whole tiny layer" in r["sample"]
+
+
+def test_default_workload_is_the_prefill_layer():
+    assert bench.parse.__defaults__ is None
+    old = sys.argv
+    try:
+        sys.argv = ["bench.py"]
+        assert bench.parse().workload == "prefill"
+    finally:
+        sys.argv = old
