@@ -199,9 +199,10 @@ def main():
     torch.cuda.synchronize()
     ep.trace_enable(False)
     breakdown = ep.trace_read()
-    # the roofline's launch averages: every launch of the timed region when every one was
-    # traced, else the breakdown pass (every launch of its steps)
-    kstats = dict(timed_stats) if every else dict(breakdown)
+    # the roofline's launch averages come from the timed region (every launch of it on long
+    # layers; one step in eight on short ones, where events on every launch would stretch
+    # the kernels they bracket); other kernels from the breakdown pass
+    kstats = dict(timed_stats)
     for name, st_ in breakdown.items():
         kstats.setdefault(name, st_)
     # the two-kernel path (layout, then pack) on the same steps, for comparison, when the
@@ -234,8 +235,8 @@ def main():
         entry = {"launches": st["count"], "avg_us": round(us, 3),
                  "p10_us": round(st["p10_ms"] * 1e3, 3), "p50_us": round(st["p50_ms"] * 1e3, 3),
                  "p90_us": round(st["p90_ms"] * 1e3, 3),
-                 "measured": ("timed region, every launch" if every else "breakdown pass, every launch")
-                 if name in timed_stats or name in breakdown else "breakdown pass"}
+                 "measured": ("timed region, every launch" if every else "timed region, one step in eight")
+                 if name in timed_stats else "breakdown pass"}
         if name in abytes and us > 0:
             entry["algorithmic_bytes"] = abytes[name]
             entry["GBps"] = round(abytes[name] / (us * 1e-6) / 1e9, 1)
@@ -260,6 +261,7 @@ def main():
     copy_gbps = 2 * (1 << 30) * 5 / (ev0.elapsed_time(ev1) * 1e-3) / 1e9
     del a, b
     same_copy = same_bytes_copy(dev, abytes[dominant], nsets)
+    ceilings = streaming_ceilings(cfg, dev)
 
     result = {
         "metric": METRIC,
@@ -301,6 +303,7 @@ def main():
         "hbm_copy_probe_GBps": round(copy_gbps, 1),
         "same_bytes_copy": dict(same_copy, kernel=dominant,
                                 kernel_speed_vs_copy=round(same_copy["avg_us"] / dk["avg_us"], 3)),
+        "streaming_ceilings": ceilings,
     }
     if warm is not None:
         result["warm_cache"] = {
@@ -769,6 +772,55 @@ def same_bytes_copy(dev, nbytes: int, nsets: int, launches: int = 40) -> dict:
     us = st["mean_ms"] * 1e3
     return {"bytes_per_launch": 2 * half, "launches": st["count"], "avg_us": round(us, 3),
             "p50_us": round(st["p50_ms"] * 1e3, 3), "GBps": round(2 * half / (us * 1e-6) / 1e9, 1)}
+
+
+def streaming_ceilings(cfg, dev, launches: int = 10) -> dict:
+    """What plain streaming code attains at this layer's size (ep_stream_probe): every mix
+    moves the rows of one dispatch, (k+1)*T rows of 2H bytes, over sequential addresses --
+    1 read : k writes like the pack, k reads : 1 write like the combine, copy 1:1,
+    read-only and write-only -- on buffer sets rotated past the memory-side cache, each
+    launch timed by events.  Fractions are of the 8 TB/s peak."""
+    import torch
+
+    import paper_2609_40093_amd as ep
+    T, H, k = cfg.T, cfg.H, cfg.k
+    row = 2 * H
+    if row % 1024 or row // 1024 not in (1, 2, 4, 8, 14, 16):
+        return {"note": f"rows of {row} bytes: no probe instance"}
+    rows = (k + 1) * T
+    set_bytes = rows * row
+    nsets = max(1, min(8, -(-3 * MALL_BYTES // set_bytes)))
+    src = torch.empty(nsets * set_bytes, dtype=torch.uint8, device=dev)
+    dst = torch.empty(nsets * set_bytes, dtype=torch.uint8, device=dev)
+    src.fill_(1)
+    mixes = {f"pack_like_1_to_{k}": (T, 1, k), f"combine_like_{k}_to_1": (T, k, 1),
+             "copy_1_to_1": (rows // 2, 1, 1), "read_only": (rows, 1, 0), "write_only": (rows, 0, 1)}
+    res = {}
+    for name, (units, r, w) in mixes.items():
+        def launch(j):
+            off = (j % nsets) * set_bytes
+            ep.stream_probe(dst[off:], src[off:], units, row, r, w)
+        for j in range(2):
+            launch(j)
+        torch.cuda.synchronize()
+        ep.trace_reset()
+        ep.trace_enable(True)
+        for j in range(launches):
+            launch(j)
+        torch.cuda.synchronize()
+        ep.trace_enable(False)
+        st = ep.trace_read()["stream_probe"]
+        ep.trace_reset()
+        us = st["mean_ms"] * 1e3
+        nbytes = units * (r + w) * row
+        gbps = nbytes / (us * 1e-6) / 1e9
+        res[name] = {"units": units, "reads": r, "writes": w, "row_bytes": row, "bytes_per_launch": nbytes,
+                     "launches": st["count"], "avg_us": round(us, 2), "GBps": round(gbps, 1),
+                     "frac": round(gbps / HBM_PEAK_GBPS, 4)}
+    del src, dst
+    res["note"] = ("ep_stream_probe over sequential addresses, non-temporal 16-byte vectors, one wave per unit; "
+                   "buffer sets rotated past the 256 MB memory-side cache")
+    return res
 
 
 def cpu_model() -> str:

@@ -103,9 +103,11 @@ ep_status ep_layout_workspace_bytes(int64_t num_tokens, int32_t topk, int32_t nu
  *   row_src         int32 [T*k] or NULL: inverse of slot_pos (row p came from slot row_src[p]).
  *   workspace       device scratch of ep_layout_workspace_bytes() bytes, zero-filled
  *                   before its first use (e.g. hipMemset) and otherwise left alone between
- *                   calls: it carries a call counter from one call to the next, the
- *                   tiles' exchanged totals, and the status read by ep_layout_validate.
- *                   Calls that share a workspace must be ordered (same stream or events).
+ *                   calls: it holds the partial counts of the tiles of the routing array,
+ *                   a counter that every call leaves at 0, and the status read by
+ *                   ep_layout_validate.  Calls that share a workspace must be ordered
+ *                   (same stream or events).  No workgroup of a layout waits for another,
+ *                   so a layout completes whatever else the device runs.
  * Requires T >= 0, T*k < 2^31, 1 <= k <= E <= EP_MAX_EXPERTS, R >= 1, E % R == 0.
  * T == 0 is valid: counts and offsets are written as zeros.  With an invalid expert id
  * the outputs are unspecified but every write stays inside the arrays above, and the
@@ -119,12 +121,8 @@ ep_status ep_dispatch_layout(const int32_t *topk_idx, int64_t num_tokens, int32_
 
 /* Validation of the routing a layout consumed (Sec. 4.3: every routing entry names one
  * of the E experts, each at most once per token).  Synchronizes `stream`, then reads the
- * status word the last layout on `workspace` left:
- * EP_OK, or EP_ERR_BAD_ROUTING (an id outside [0,E) or an expert repeated in a row), or
- * EP_ERR_TIMEOUT if a layout's workgroups could not all run at once within a second (the
- * device was held by other work); that state sticks until the workspace is zero-filled
- * again, and the outputs of the call that timed out are unspecified (stores stay inside
- * the arrays). */
+ * status word the last layout on `workspace` left: EP_OK, or EP_ERR_BAD_ROUTING (an id
+ * outside [0,E) or an expert repeated in a row). */
 ep_status ep_layout_validate(const void *workspace, hipStream_t stream);
 
 /* ------------------------------------------------------------------------ staging */
@@ -443,6 +441,18 @@ ep_status ep_trace_reset(void);
 /* A plain streaming copy kernel (16-byte vectors): the attainable-bandwidth probe and
  * the calibration for hardware byte counters.  bytes must be a multiple of 16. */
 ep_status ep_copy_probe(void *dst_dev, const void *src_dev, size_t bytes, hipStream_t stream);
+
+/* Streaming probe of one read:write mix, over sequential addresses: `units` units, each
+ * reading `reads` rows of row_bytes (unit u: src rows [u*reads, (u+1)*reads)) and writing
+ * `writes` rows (dst rows [u*writes, (u+1)*writes)), every written row the XOR of the rows
+ * read.  1:k has the traffic of the dispatch's pack, k:1 that of the combine, 1:0 is
+ * read-only, 0:1 write-only: what plain streaming code attains, beside which the path's
+ * kernels are judged.  row_bytes = 1024 * g, g in {1, 2, 4, 8, 14, 16}; reads, writes in
+ * 0..64, not both 0.  src: units*reads*row_bytes bytes (may be NULL when reads == 0);
+ * dst: units*writes*row_bytes bytes, or 1 KiB when writes == 0.  Traced as
+ * "stream_probe". */
+ep_status ep_stream_probe(void *dst_dev, const void *src_dev, int64_t units, int32_t row_bytes, int32_t reads,
+                          int32_t writes, hipStream_t stream);
 
 /* PCIe probe on the SDMA engines the exchange uses: `dirs` bit 0 moves `bytes`
  * device->host (dev -> host), bit 1 host->device (host + bytes -> dev + bytes), both

@@ -6,8 +6,9 @@ re-exported lazily so that ``paper_2609_40093_amd.synth`` (input generation only
 imported without torch or a GPU.
 """
 
-_API = ("EPError", "Layout", "Staging", "SimPeers", "dispatch_layout", "layout_validate", "dispatch", "dispatch_fused", "combine",
-        "trace_enable", "trace_read", "trace_reset", "copy_probe", "workspace_bytes", "pcie_probe",
+_API = ("EPError", "Layout", "Staging", "SimPeers", "dispatch_layout", "layout_validate", "dispatch", "dispatch_fused",
+        "combine", "trace_enable", "trace_read", "trace_reset", "copy_probe", "stream_probe", "workspace_bytes",
+        "pcie_probe",
         "MODE_PER_SENDER", "MODE_DUPLEX", "MODE_REMOTE_ONLY", "MODE_ACCUMULATE", "LocalLayout", "dispatch_layout_local", "pack",
         "combine_rows", "Dense", "allgather", "reducescatter", "round_advance", "round_read", "dispatch_graph",
         "combine_graph")

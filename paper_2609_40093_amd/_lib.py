@@ -89,6 +89,7 @@ SIGNATURES = {
     "ep_trace_read": (c_i32, [ctypes.POINTER(TraceStat), c_i32, ctypes.POINTER(c_i32)]),
     "ep_trace_reset": (c_i32, []),
     "ep_copy_probe": (c_i32, [c_vp, c_vp, c_size, c_vp]),
+    "ep_stream_probe": (c_i32, [c_vp, c_vp, c_i64, c_i32, c_i32, c_i32, c_vp]),
     "ep_memcpy": (c_i32, [c_vp, c_vp, c_size, c_vp]),
     "ep_pcie_probe": (c_i32, [c_vp, c_vp, c_size, c_i32, ctypes.POINTER(ctypes.c_double)]),
     "ep_sim_peers_start": (c_i32, [c_vp, c_i32, ctypes.POINTER(c_vp)]),

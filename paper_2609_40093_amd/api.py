@@ -22,7 +22,7 @@ MODE_PER_SENDER, MODE_DUPLEX, MODE_REMOTE_ONLY = _lib.EP_MODE_PER_SENDER, _lib.E
 MODE_ACCUMULATE = _lib.EP_MODE_ACCUMULATE
 
 __all__ = ["EPError", "Layout", "Staging", "SimPeers", "dispatch_layout", "layout_validate", "dispatch",
-           "combine", "trace_enable", "trace_read", "trace_reset", "copy_probe", "workspace_bytes",
+           "combine", "trace_enable", "trace_read", "trace_reset", "copy_probe", "stream_probe", "workspace_bytes",
            "pcie_probe", "MODE_PER_SENDER", "MODE_DUPLEX", "MODE_REMOTE_ONLY", "MODE_ACCUMULATE", "LocalLayout",
            "dispatch_layout_local", "pack", "combine_rows", "Dense", "allgather", "reducescatter",
            "round_advance", "round_read", "dispatch_graph", "combine_graph"]
@@ -601,6 +601,17 @@ def copy_probe(dst: torch.Tensor, src: torch.Tensor, stream=None) -> None:
     if dst.numel() * dst.element_size() < nbytes:
         raise ValueError("dst smaller than src")
     _check(_lib_handle().ep_copy_probe(_ptr(dst), _ptr(src), nbytes, _stream_ptr(stream)), "ep_copy_probe")
+
+
+def stream_probe(dst: torch.Tensor, src: Optional[torch.Tensor], units: int, row_bytes: int, reads: int, writes: int,
+                 stream=None) -> None:
+    """ep_stream_probe: `units` units each reading `reads` rows and writing `writes` rows of
+    row_bytes (sequential addresses), on device tensors large enough for them."""
+    need_src, need_dst = units * reads * row_bytes, units * writes * row_bytes if writes else 1024
+    if dst.nbytes < need_dst or (reads and (src is None or src.nbytes < need_src)):
+        raise ValueError("stream_probe: buffers too small for the units asked for")
+    _check(_lib_handle().ep_stream_probe(_ptr(dst), _ptr(src) if reads else None, units, row_bytes, reads, writes,
+                                         _stream_ptr(stream)), "ep_stream_probe")
 
 
 def pcie_probe(host: torch.Tensor, dev: torch.Tensor, nbytes: int, dirs: int) -> float:

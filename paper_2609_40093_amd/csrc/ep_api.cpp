@@ -178,7 +178,7 @@ extern "C" ep_status ep_layout_workspace_bytes(int64_t num_tokens, int32_t topk,
     return EP_OK;
 }
 
-namespace {
+namespace ep {
 
 // Host-visible argument checks of a dispatch layout call.
 ep_status check_layout_args(const char *who, int64_t T, int32_t k, int32_t E, int32_t R, const int32_t *topk_idx,
@@ -200,20 +200,10 @@ ep_status check_layout_args(const char *who, int64_t T, int32_t k, int32_t E, in
     return EP_OK;
 }
 
-}  // namespace
-
-extern "C" ep_status ep_dispatch_layout(const int32_t *topk_idx, int64_t num_tokens, int32_t topk,
-                                        int32_t num_experts, int32_t num_ranks, int32_t *expert_counts,
-                                        int32_t *expert_offsets, int32_t *rank_counts,
-                                        int32_t *rank_offsets, int32_t *slot_pos, int32_t *row_src,
-                                        void *workspace, size_t workspace_bytes, hipStream_t stream) {
-    const int64_t T = num_tokens;
-    const int32_t k = topk, E = num_experts, R = num_ranks;
-    const ep_status st = check_layout_args("ep_dispatch_layout", T, k, E, R, topk_idx, expert_counts, expert_offsets,
-                                           rank_counts, rank_offsets, slot_pos, workspace, workspace_bytes);
-    if (st != EP_OK)
-        return st;
-    ep::LayoutArgs a{};
+LayoutArgs layout_args(const int32_t *topk_idx, int64_t T, int32_t k, int32_t E, int32_t R, int32_t *expert_counts,
+                       int32_t *expert_offsets, int32_t *rank_counts, int32_t *rank_offsets, int32_t *slot_pos,
+                       int32_t *row_src, void *workspace) {
+    LayoutArgs a{};
     a.topk_idx = topk_idx;
     a.slots = T * k;
     a.k = k;
@@ -229,12 +219,28 @@ extern "C" ep_status ep_dispatch_layout(const int32_t *topk_idx, int64_t num_tok
     a.rank_offsets = rank_offsets;
     a.slot_pos = slot_pos;
     a.row_src = row_src;
-    char *ws = static_cast<char *>(workspace);
-    a.status = reinterpret_cast<uint32_t *>(ws);
-    a.epoch = reinterpret_cast<uint32_t *>(ws + ep::kWorkspaceEpoch);
-    a.timed_out = reinterpret_cast<uint32_t *>(ws + ep::kWorkspaceTimeout);
-    a.tile_words = reinterpret_cast<uint64_t *>(ws + ep::kWorkspaceHeader);
-    EP_HIP(ep::launch_layout(a, stream));
+    layout_workspace(a, workspace);
+    return a;
+}
+
+}  // namespace ep
+
+using ep::check_layout_args;
+
+extern "C" ep_status ep_dispatch_layout(const int32_t *topk_idx, int64_t num_tokens, int32_t topk,
+                                        int32_t num_experts, int32_t num_ranks, int32_t *expert_counts,
+                                        int32_t *expert_offsets, int32_t *rank_counts,
+                                        int32_t *rank_offsets, int32_t *slot_pos, int32_t *row_src,
+                                        void *workspace, size_t workspace_bytes, hipStream_t stream) {
+    const int64_t T = num_tokens;
+    const int32_t k = topk, E = num_experts, R = num_ranks;
+    const ep_status st = check_layout_args("ep_dispatch_layout", T, k, E, R, topk_idx, expert_counts, expert_offsets,
+                                           rank_counts, rank_offsets, slot_pos, workspace, workspace_bytes);
+    if (st != EP_OK)
+        return st;
+    EP_HIP(ep::launch_layout(ep::layout_args(topk_idx, T, k, E, R, expert_counts, expert_offsets, rank_counts,
+                                             rank_offsets, slot_pos, row_src, workspace),
+                             stream));
     return EP_OK;
 }
 
@@ -278,10 +284,7 @@ extern "C" ep_status ep_dispatch_layout_local(const int32_t *topk_idx, int64_t n
     a.rank_offsets = reinterpret_cast<int32_t *>(ws + ep::kWorkspaceScratch + 4); // [2]
     a.slot_pos = slot_pos;
     a.row_src = row_src;
-    a.status = reinterpret_cast<uint32_t *>(ws);
-    a.epoch = reinterpret_cast<uint32_t *>(ws + ep::kWorkspaceEpoch);
-    a.timed_out = reinterpret_cast<uint32_t *>(ws + ep::kWorkspaceTimeout);
-    a.tile_words = reinterpret_cast<uint64_t *>(ws + ep::kWorkspaceHeader);
+    ep::layout_workspace(a, workspace);
     EP_HIP(ep::launch_layout(a, stream));
     return EP_OK;
 }
@@ -316,13 +319,8 @@ extern "C" ep_status ep_layout_validate(const void *workspace, hipStream_t strea
     if (!workspace)
         return fail(EP_ERR_INVALID_ARG, "ep_layout_validate: workspace is NULL");
     EP_HIP(hipStreamSynchronize(stream));
-    uint32_t word = 0, timed_out = 0;
+    uint32_t word = 0;
     EP_HIP(hipMemcpy(&word, workspace, sizeof word, hipMemcpyDeviceToHost));
-    EP_HIP(hipMemcpy(&timed_out, static_cast<const char *>(workspace) + ep::kWorkspaceTimeout, sizeof timed_out,
-                     hipMemcpyDeviceToHost));
-    if (timed_out)
-        return fail(EP_ERR_TIMEOUT, "a layout on this workspace gave up waiting for the totals of other "
-                                    "workgroups; zero-fill the workspace before using it again");
     if (word == 0)
         return EP_OK;
     return fail(EP_ERR_BAD_ROUTING, "routing rejected:%s%s",
@@ -1025,6 +1023,20 @@ extern "C" ep_status ep_copy_probe(void *dst_dev, const void *src_dev, size_t by
     if (bytes % 16 != 0 || (bytes && (!dst_dev || !src_dev || !aligned16(dst_dev) || !aligned16(src_dev))))
         return fail(EP_ERR_INVALID_ARG, "ep_copy_probe: 16-byte aligned pointers and a multiple of 16 bytes");
     EP_HIP(ep::launch_copy(dst_dev, src_dev, bytes, stream));
+    return EP_OK;
+}
+
+extern "C" ep_status ep_stream_probe(void *dst_dev, const void *src_dev, int64_t units, int32_t row_bytes,
+                                     int32_t reads, int32_t writes, hipStream_t stream) {
+    const int g = row_bytes / 1024;
+    const bool shape = row_bytes > 0 && row_bytes % 1024 == 0 &&
+                       (g == 1 || g == 2 || g == 4 || g == 8 || g == 14 || g == 16);
+    if (units < 0 || !shape || reads < 0 || writes < 0 || reads + writes == 0 || reads > 64 || writes > 64)
+        return fail(EP_ERR_INVALID_ARG, "ep_stream_probe: need units >= 0, row_bytes = 1024 * {1,2,4,8,14,16}, "
+                                        "0 <= reads, writes <= 64, reads + writes > 0");
+    if (units > 0 && (!dst_dev || !aligned16(dst_dev) || (reads > 0 && (!src_dev || !aligned16(src_dev)))))
+        return fail(EP_ERR_INVALID_ARG, "ep_stream_probe: 16-byte aligned src (when reading) and dst are required");
+    EP_HIP(ep::launch_stream_probe(dst_dev, src_dev, units, row_bytes, reads, writes, stream));
     return EP_OK;
 }
 

@@ -19,42 +19,32 @@ constexpr int kWave = 64;
 
 // ---- layout geometry -----------------------------------------------------------
 // The routing array is cut into tiles, one workgroup each; a workgroup has W waves and
-// each wave walks `rounds` rounds of 64 entries.  All tiles' workgroups are resident at
-// once (at most kLayoutMaxTiles of them, never more than the device's compute units):
-// each publishes its per-expert totals and reads everyone else's before ranking.
+// each wave walks `rounds` rounds of 64 entries.  W = 16 while 16 rows of per-wave
+// counters fit in LDS (E <= 512), else 4.  One tile when it covers every entry in at most
+// 4 rounds (W = 16) or 8 rounds (W = 4): one kernel then does the whole layout.  Otherwise
+// as many tiles as keep the tile counts at most 16K words (the last workgroup of the
+// count kernel reads and rewrites them all) and at most 1024 tiles, with as few rounds as
+// that allows.  No tile waits for another, so the tile count is not tied to the device.
 constexpr int kMaxExperts = 2048;
-constexpr int kLayoutMaxTiles = 256;
 constexpr int kLayoutRankCache = 8;  // rounds whose ids and in-wave ranks stay in registers
 struct LayoutGeom {
     int waves;
     int rounds;
     int64_t tiles;
 };
-// Smallest tiles (most workgroups) such that the tile count stays within max_tiles and
-// the cross-tile gather reads at most 16 words per thread; W = 16 only while 16 rows of
-// per-wave counters fit in LDS (E <= 512).
-inline LayoutGeom layout_geometry(int64_t slots, int32_t experts, int64_t max_tiles) {
-    struct Cand {
-        int waves, rounds;
-    };
-    static constexpr Cand kCands[] = {{4, 1}, {4, 2}, {4, 4}, {4, 8}, {16, 1}, {16, 2}, {16, 4}, {16, 8}};
-    const bool wide = experts <= 512;
-    const int64_t cols = (int64_t)experts + 1;
-    for (const Cand &c : kCands) {
-        if (wide ? (c.waves == 4 && c.rounds > 2) : c.waves == 16)
-            continue;
-        const int64_t tile = (int64_t)kWave * c.waves * c.rounds;
-        const int64_t tiles = slots > tile ? (slots + tile - 1) / tile : 1;
-        if (tiles <= max_tiles && tiles * cols <= 16 * kWave * c.waves)
-            return {c.waves, c.rounds, tiles};
-    }
-    const int waves = wide ? 16 : 4;
+inline LayoutGeom layout_geometry(int64_t slots, int32_t experts) {
+    const int waves = experts <= 512 ? 16 : 4;
     const int64_t per_round = (int64_t)kWave * waves;
-    int64_t cap = 64 * per_round / cols;
-    cap = cap < 1 ? 1 : (cap > max_tiles ? max_tiles : cap);
-    const int64_t rounds = (slots + per_round * cap - 1) / (per_round * cap);
+    const int64_t one_tile_rounds = waves == 16 ? 4 : 8;
+    if (slots <= per_round * one_tile_rounds) {
+        const int64_t rounds = slots > 0 ? (slots + per_round - 1) / per_round : 1;
+        return {waves, (int)rounds, 1};
+    }
+    int64_t max_tiles = 16384 / (experts > 0 ? experts : 1);
+    max_tiles = max_tiles < 2 ? 2 : (max_tiles > 1024 ? 1024 : max_tiles);
+    const int64_t rounds = (slots + per_round * max_tiles - 1) / (per_round * max_tiles);
     const int64_t tiles = (slots + per_round * rounds - 1) / (per_round * rounds);
-    return {waves, (int)(rounds < 1 ? 1 : rounds), tiles < 1 ? 1 : tiles};
+    return {waves, (int)rounds, tiles};
 }
 
 // Routing status bits left in the layout workspace's status word.
@@ -63,18 +53,17 @@ constexpr uint32_t kRoutingDuplicate = 2u;
 
 // Layout workspace (zero-filled before its first use):
 //   byte   0  uint32 routing status of the last call
-//   byte  64  uint32 epoch: calls on this workspace so far that used several tiles
-//   byte 128  uint32 nonzero once a workgroup gave up waiting for another's totals
+//   byte  64  uint32 ticket of the multi-tile count kernel (0 between calls)
 //   byte 192  int32 [3] rank count/offsets of a window layout (one segment)
-//   byte 256  uint64 [tiles][E+1] words (epoch+1) << 32 | value: a tile's per-expert
-//             totals, then its routing error bits
+//   byte 256  int32 [tiles][E] each tile's counts per expert, then (after the count
+//             kernel) the rows of each expert in earlier tiles; then uint32 [tiles] the
+//             tiles' routing error bits
 constexpr size_t kWorkspaceHeader = 256;
-constexpr size_t kWorkspaceEpoch = 64;
-constexpr size_t kWorkspaceTimeout = 128;
+constexpr size_t kWorkspaceTicket = 64;
 constexpr size_t kWorkspaceScratch = 192;  // 3 words the one-segment local layout writes
 inline size_t layout_workspace_bytes(int64_t slots, int32_t experts) {
-    const LayoutGeom g = layout_geometry(slots, experts, kLayoutMaxTiles);
-    return kWorkspaceHeader + (g.tiles > 1 ? (size_t)g.tiles * ((size_t)experts + 1) * sizeof(uint64_t) : 0);
+    const LayoutGeom g = layout_geometry(slots, experts);
+    return kWorkspaceHeader + (g.tiles > 1 ? (size_t)g.tiles * ((size_t)experts + 1) * sizeof(int32_t) : 0);
 }
 
 // ---- timing events (tracing) -----------------------------------------------------
@@ -100,11 +89,19 @@ struct LayoutArgs {
     int32_t *expert_counts, *expert_offsets, *rank_counts, *rank_offsets;
     int32_t *slot_pos, *row_src;
     uint32_t *status;        // workspace byte 0
-    uint32_t *epoch;         // workspace byte 64
-    uint32_t *timed_out;     // workspace byte 128
-    uint64_t *tile_words;    // workspace byte 256
-    int64_t timeout_ticks;   // wall-clock ticks a workgroup waits for the others' totals
+    uint32_t *ticket;        // workspace byte 64
+    int32_t *tile_counts;    // workspace byte 256: [tiles][E]
+    uint32_t *tile_errs;     // [tiles], after tile_counts
 };
+// Sets the workspace pointers of `a` (a.E and a.slots set) from the workspace base.
+inline void layout_workspace(LayoutArgs &a, void *workspace) {
+    char *ws = static_cast<char *>(workspace);
+    const LayoutGeom g = layout_geometry(a.slots, a.E);
+    a.status = reinterpret_cast<uint32_t *>(ws);
+    a.ticket = reinterpret_cast<uint32_t *>(ws + kWorkspaceTicket);
+    a.tile_counts = reinterpret_cast<int32_t *>(ws + kWorkspaceHeader);
+    a.tile_errs = reinterpret_cast<uint32_t *>(a.tile_counts + g.tiles * (int64_t)a.E);
+}
 hipError_t launch_layout(LayoutArgs a, hipStream_t stream);
 
 // Layout and pack in one kernel for small expert counts (see fused.hip).  Same outputs
@@ -212,5 +209,9 @@ hipError_t launch_round_gate(const char *name, const uint32_t *round, const uint
 hipError_t launch_round_stamp(const uint32_t *round, uint32_t *words, int32_t stride, int32_t n, hipStream_t stream);
 
 hipError_t launch_copy(void *dst, const void *src, size_t bytes, hipStream_t stream);
+// Streaming probe of a given read:write mix (copy.hip); row_bytes = 1024 * g with g in
+// {1, 2, 4, 8, 14, 16}.
+hipError_t launch_stream_probe(void *dst, const void *src, int64_t units, int32_t row_bytes, int32_t reads,
+                               int32_t writes, hipStream_t stream);
 
 }  // namespace ep

@@ -28,6 +28,16 @@ struct FlagNamer {
 };
 ep_status take_status(uint32_t *block, int64_t timeout_us, const FlagNamer &name_flag);
 
+// Host-visible argument checks of a dispatch layout call (sizes, NULL pointers, the
+// workspace's size), and the kernel arguments of one with its workspace at `workspace`.
+ep_status check_layout_args(const char *who, int64_t T, int32_t k, int32_t E, int32_t R, const int32_t *topk_idx,
+                            const int32_t *expert_counts, const int32_t *expert_offsets, const int32_t *rank_counts,
+                            const int32_t *rank_offsets, const int32_t *slot_pos, const void *workspace,
+                            size_t workspace_bytes);
+LayoutArgs layout_args(const int32_t *topk_idx, int64_t T, int32_t k, int32_t E, int32_t R, int32_t *expert_counts,
+                       int32_t *expert_offsets, int32_t *rank_counts, int32_t *rank_offsets, int32_t *slot_pos,
+                       int32_t *row_src, void *workspace);
+
 #define EP_HIP(call)                                                                                \
     do {                                                                                            \
         hipError_t e_ = (call);                                                                     \

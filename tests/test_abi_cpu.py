@@ -78,9 +78,11 @@ def test_workspace_bytes(lib):
     assert lib.ep_layout_workspace_bytes(128, 2, 16, ctypes.byref(n)) == 0
     assert n.value == 256                           # one tile: header only
     assert lib.ep_layout_workspace_bytes(4096, 2, 8, ctypes.byref(n)) == 0
-    assert n.value == 256 + 32 * 9 * 8              # 32 tiles of 4 x 64 entries: 8 totals + error word
+    assert n.value == 256 + 8 * 9 * 4               # 8 tiles of 16 x 64 entries: 8 counts + error word
     assert lib.ep_layout_workspace_bytes(32768, 8, 256, ctypes.byref(n)) == 0
-    assert n.value == 256 + 32 * 257 * 8            # 32 tiles of 16 x 8 x 64 entries
+    assert n.value == 256 + 64 * 257 * 4            # 64 tiles of 16 x 4 x 64 entries (16K counts)
+    assert lib.ep_layout_workspace_bytes(20000, 4, 2048, ctypes.byref(n)) == 0
+    assert n.value == 256 + 8 * 2049 * 4            # 8 tiles of 4 x 40 x 64 entries
     assert lib.ep_layout_workspace_bytes(-1, 2, 16, ctypes.byref(n)) == _lib.EP_ERR_INVALID_ARG
     assert lib.ep_layout_workspace_bytes(4, 2, 4096, ctypes.byref(n)) == _lib.EP_ERR_INVALID_ARG
     assert b"bad sizes" in lib.ep_last_error()
@@ -163,3 +165,4 @@ def test_binding_rejects_host_tensors_before_the_library():
     import paper_2609_40093_amd as ep
     with pytest.raises(ValueError, match="must be a device tensor"):
         ep.copy_probe(torch.empty(64, dtype=torch.uint8), torch.empty(64, dtype=torch.uint8))
+
