@@ -125,6 +125,24 @@ ep_status ep_dispatch_layout(const int32_t *topk_idx, int64_t num_tokens, int32_
  * outside [0,E) or an expert repeated in a row). */
 ep_status ep_layout_validate(const void *workspace, hipStream_t stream);
 
+/* For callers that cannot allocate device memory (code under HIP graph capture, serving
+ * loops that must not allocate, harnesses that forbid hipMalloc): ep_dispatch_layout with
+ * no workspace argument.  The layout's scratch is the library's own, a fixed 128 KiB
+ * array per GPU (held until the process ends), which fits every size ep_dispatch_layout
+ * accepts; sizes beyond it are refused with EP_ERR_INVALID_ARG.  Arguments, outputs and
+ * results as ep_dispatch_layout, bit for bit, except:
+ *   status_dev  device uint32 the routing status is written to (0, or bit 0 an id outside
+ *               [0,E), bit 1 an expert repeated within a token row), as ep_layout_validate
+ *               would report it; caller-owned, valid once `stream` has reached the call.
+ * The call allocates nothing.  Every call on one GPU shares that GPU's scratch: calls that
+ * overlap on one GPU (other streams or host threads without ordering) race. */
+ep_status ep_dispatch_layout_static(const int32_t *topk_idx, int64_t num_tokens, int32_t topk,
+                                    int32_t num_experts, int32_t num_ranks,
+                                    int32_t *expert_counts, int32_t *expert_offsets,
+                                    int32_t *rank_counts, int32_t *rank_offsets,
+                                    int32_t *slot_pos, int32_t *row_src, uint32_t *status_dev,
+                                    hipStream_t stream);
+
 /* ------------------------------------------------------------------------ staging */
 
 /* Allocates the staging of one rank: the buffers every dispatch and combine moves rows

@@ -55,6 +55,8 @@ SIGNATURES = {
     "ep_layout_workspace_bytes": (c_i32, [c_i64, c_i32, c_i32, ctypes.POINTER(c_size)]),
     "ep_dispatch_layout": (c_i32, [c_vp, c_i64, c_i32, c_i32, c_i32, c_vp, c_vp, c_vp, c_vp, c_vp, c_vp,
                                    c_vp, c_size, c_vp]),
+    "ep_dispatch_layout_static": (c_i32, [c_vp, c_i64, c_i32, c_i32, c_i32, c_vp, c_vp, c_vp, c_vp, c_vp, c_vp,
+                                          c_vp, c_vp]),
     "ep_layout_validate": (c_i32, [c_vp, c_vp]),
     "ep_staging_alloc": (c_i32, [c_i32, c_i64, c_i32, c_i32, c_i32, c_i64, ctypes.POINTER(c_vp)]),
     "ep_staging_free": (c_i32, [c_vp]),

@@ -166,3 +166,14 @@ def test_binding_rejects_host_tensors_before_the_library():
     with pytest.raises(ValueError, match="must be a device tensor"):
         ep.copy_probe(torch.empty(64, dtype=torch.uint8), torch.empty(64, dtype=torch.uint8))
 
+
+@pytest.mark.parametrize("T,k,E,R", [(-1, 2, 8, 4), (4, 0, 8, 4), (4, 9, 8, 4), (4, 2, 8, 3), (4, 2, 4096, 8),
+                                     (1 << 30, 8, 16, 4)])
+def test_static_layout_rejects_bad_arguments_before_the_device(lib, T, k, E, R):
+    """ep_dispatch_layout_static checks every argument before it touches a device."""
+    dummy = ctypes.c_void_p(16)   # never dereferenced: the call must fail first
+    st = lib.ep_dispatch_layout_static(dummy, T, k, E, R, dummy, dummy, dummy, dummy, dummy, None, dummy, None)
+    assert st == _lib.EP_ERR_INVALID_ARG
+    assert b"ep_dispatch_layout_static" in lib.ep_last_error()
+    st = lib.ep_dispatch_layout_static(dummy, 4, 2, 8, 4, dummy, dummy, dummy, dummy, dummy, None, None, None)
+    assert st == _lib.EP_ERR_INVALID_ARG and b"status_dev" in lib.ep_last_error()
