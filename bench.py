@@ -474,9 +474,15 @@ def bench_pinned(cfg, inp, y, args, dev) -> dict:
         if mode & ep.MODE_DUPLEX:
             pcie = 2 * (n - self_rows) * rb + 2 * (inbound_rows - self_rows) * rb
             peak = peaks["both"]
+            # dispatch: this rank's rows up, the inbound rows down; combine: the results for
+            # the other senders up, the returned rows down
+            phases = [((n - self_rows) * rb, (inbound_rows - self_rows) * rb),
+                      ((inbound_rows - self_rows) * rb, (n - self_rows) * rb)]
         else:
             pcie = 2 * n * rb
             peak = peaks["d2h_alone"]
+            phases = [(n * rb, 0), (0, n * rb)]
+        bound_us = pattern_bound_us(phases, peaks)
         gbps = pcie / (ms * 1e-3) / 1e9
         modes[name] = {
             "mode_bits": mode,
@@ -486,6 +492,8 @@ def bench_pinned(cfg, inp, y, args, dev) -> dict:
             "pcie_GBps": round(gbps, 2),
             "pcie_peak_used_GBps": peak,
             "frac_of_measured_pcie_peak": round(gbps / peak, 3),
+            "pcie_pattern_bound_us": round(bound_us, 1),
+            "frac_of_pattern_bound": round(bound_us / (ms * 1e3), 3),
         }
         if legs:
             modes[name]["legs"] = legs
@@ -645,9 +653,15 @@ def bench_dense(cfg, inp, args, dev, peaks) -> dict:
         ms = (t1 - t0) * 1e3 / steps
         pcie = ((up1 - up0) + (down1 - down0)) / steps
         gbps = pcie / (ms * 1e-3) / 1e9
+        S = T * H * 2
+        # All-Gather: S up, (R-1)S down; Reduce-Scatter: (R-1)S up, (R-1)S or S down
+        phases = [(S, (R - 1) * S), ((R - 1) * S, S if on_host else (R - 1) * S)]
+        bound_us = pattern_bound_us(phases, peaks)
         res[name] = {"us_per_layer": round(ms * 1e3, 1), "pcie_bytes_per_layer": int(pcie),
                      "pcie_up_down_per_layer": [int((up1 - up0) / steps), int((down1 - down0) / steps)],
                      "pcie_GBps": round(gbps, 2), "frac_of_measured_pcie_peak": round(gbps / peaks["both"], 3),
+                     "pcie_pattern_bound_us": round(bound_us, 1),
+                     "frac_of_pattern_bound": round(bound_us / (ms * 1e3), 3),
                      "breakdown_avg_us": {kn: round(v["mean_ms"] * 1e3, 1) for kn, v in ks.items()}}
     res["note"] = ("per-sender policy; payload per layer: All-Gather S up + (R-1)S down, Reduce-Scatter (R-1)S up "
                    "and (R-1)S down (GPU reduction) or S down (host reduction), S = T*H*2 bytes")
@@ -718,6 +732,17 @@ def bench_graph(names, args, dev, peaks) -> dict:
     res["note"] = ("rows stored to and loaded from pinned memory by the compute units; the two directions run one "
                    "after the other within a round, so the one-way peak bounds the rate")
     return res
+
+
+def pattern_bound_us(phases, peaks) -> float:
+    """The least time the PCIe traffic of a layer can take at the measured peaks: phase by
+    phase (each a list of (bytes up, bytes down) moving at once), the largest of the
+    upload at the one-way device->host peak, the download at the one-way host->device peak
+    and both together at the two-way peak."""
+    t = 0.0
+    for up, down in phases:
+        t += max(up / peaks["d2h_alone"], down / peaks["h2d_alone"], (up + down) / peaks["both"]) / 1e3
+    return t
 
 
 def pcie_peaks(dev) -> dict:

@@ -24,6 +24,10 @@
 namespace {
 
 constexpr int kDenseMaxBuffers = 8;
+// The partial host reduction sums and downloads its block in up to this many pieces of at
+// least 2 MiB: piece c goes down while the host sums piece c + 1.
+constexpr int kReduceChunks = 16;
+constexpr int64_t kReduceChunkMinBytes = 2ll << 20;
 
 // Fixed set of host threads for the partial host reduction; run() splits [0, n) into
 // `workers + 1` parts (the calling thread takes one).  run() is called by the courier
@@ -106,6 +110,53 @@ private:
     bool stop_ = false;
 };
 
+// One host thread that runs queued tasks in order (the partial host reductions, so that
+// the courier thread that posts them goes on queueing copies meanwhile).  stop() runs the
+// tasks still queued, then ends the thread.
+class Reducer {
+public:
+    void start() {
+        stop_ = false;
+        th_ = std::thread([this] { loop(); });
+    }
+    void stop() {
+        {
+            std::lock_guard<std::mutex> lk(mu_);
+            stop_ = true;
+        }
+        cv_.notify_all();
+        if (th_.joinable())
+            th_.join();
+    }
+    void post(std::function<void()> task) {
+        {
+            std::lock_guard<std::mutex> lk(mu_);
+            q_.push_back(std::move(task));
+        }
+        cv_.notify_one();
+    }
+
+private:
+    void loop() {
+        std::unique_lock<std::mutex> lk(mu_);
+        for (;;) {
+            cv_.wait(lk, [&] { return stop_ || !q_.empty(); });
+            if (q_.empty())
+                return;  // stopped, nothing left
+            std::function<void()> task = std::move(q_.front());
+            q_.pop_front();
+            lk.unlock();
+            task();
+            lk.lock();
+        }
+    }
+    std::thread th_;
+    std::mutex mu_;
+    std::condition_variable cv_;
+    std::deque<std::function<void()>> q_;
+    bool stop_ = false;
+};
+
 // IEEE binary32 -> bf16, round to nearest, ties to even (NaN kept quiet).
 inline uint16_t f32_to_bf16(float f) {
     uint32_t u;
@@ -133,12 +184,15 @@ struct ep_dense {
     void *host_ag[kDenseMaxBuffers] = {}, *dev_gathered[kDenseMaxBuffers] = {};
     void *host_rs_out[kDenseMaxBuffers] = {}, *host_rs_in[kDenseMaxBuffers] = {}, *dev_rs_in[kDenseMaxBuffers] = {};
     // coherent pinned: ag, ag_landed, rs_out, rs_in, rs_landed [nbuf][R] each, then the
-    // status block (ep::kStatusWords words)
+    // status block (ep::kStatusWords words), then the host reduction's piece flags
+    // [nbuf][kReduceChunks] (epoch once the host has summed that piece)
     uint32_t *flags = nullptr;
     char *dev_epoch = nullptr;
     hipEvent_t ev_sysrel = nullptr;
     ep::Exchange *xchg = nullptr;
     HostPool pool;
+    Reducer reducer;
+    uint32_t reduced_epoch[kDenseMaxBuffers] = {};  // epoch of the last host reduction posted per buffer set
     uint32_t mode = 0;
     int64_t timeout_us = 10ll * 1000 * 1000;
     int32_t sleep_units = 2;
@@ -152,6 +206,7 @@ struct ep_dense {
     uint32_t *rs_in(int b) const { return fl(3, b); }
     uint32_t *rs_landed(int b) const { return fl(4, b); }
     uint32_t *status() const { return flags + (size_t)5 * nbuf * R; }
+    uint32_t *piece_flags(int b) const { return status() + ep::kStatusWords + (size_t)b * kReduceChunks; }
     uint32_t *epoch_word(int b) const { return reinterpret_cast<uint32_t *>(dev_epoch + b * ep::kEpochStride); }
 };
 
@@ -162,6 +217,7 @@ using ep::hip_fail;
 
 void dense_release(ep_dense *d) {
     ep::exchange_destroy(d->xchg);
+    d->reducer.stop();  // after the courier: no reduction is posted any more
     d->pool.stop();
     for (int b = 0; b < kDenseMaxBuffers; ++b) {
         for (void *p : {d->host_ag[b], d->host_rs_out[b], d->host_rs_in[b]})
@@ -251,7 +307,7 @@ extern "C" ep_status ep_dense_alloc(int64_t max_tokens, int32_t hidden, int32_t 
         EP_DENSE_HIP(hipHostMalloc(&d->host_rs_in[b], rs_bytes, hipHostMallocDefault));
         EP_DENSE_HIP(hipMalloc(&d->dev_rs_in[b], rs_bytes));
     }
-    const size_t words = (size_t)5 * num_buffers * num_ranks + ep::kStatusWords;
+    const size_t words = (size_t)5 * num_buffers * num_ranks + ep::kStatusWords + (size_t)num_buffers * kReduceChunks;
     EP_DENSE_HIP(hipHostMalloc((void **)&d->flags, words * sizeof(uint32_t), hipHostMallocCoherent));
     std::memset(d->flags, 0, words * sizeof(uint32_t));
     EP_DENSE_HIP(hipMalloc((void **)&d->dev_epoch, kDenseMaxBuffers * ep::kEpochStride));
@@ -265,6 +321,7 @@ extern "C" ep_status ep_dense_alloc(int64_t max_tokens, int32_t hidden, int32_t 
     }
     const unsigned hc = std::thread::hardware_concurrency();
     d->pool.start((int)std::min<unsigned>(15u, hc > 1 ? hc - 1 : 0u));
+    d->reducer.start();
     *out = d;
     return EP_OK;
 }
@@ -486,54 +543,100 @@ extern "C" ep_status ep_reducescatter(ep_dense *d, int32_t buf, uint32_t epoch, 
         }
     } else if (R > 1) {
         // partial host reduction: once every remote block is in, the host sums them (fp32,
-        // rank order) into this rank's own slot of the host buffer, which then goes down
-        ep::InCopy own;
-        if (!x.in_copy(slot, nullptr, din + me * block, hin + me * block, block, d->rs_landed(buf) + me, own, err))
-            return fail(EP_ERR_HIP, "%s: %s", who, err.c_str());
+        // rank order) into this rank's own slot of the host buffer, piece by piece on the
+        // reducer thread; each piece goes down as soon as it is summed (its piece flag),
+        // the last one followed by the block's landed flag
+        const int64_t n = T * d->hidden, eb = brb / d->hidden;
+        const int64_t want_pieces = std::max<int64_t>(1, std::min<int64_t>(kReduceChunks, block / kReduceChunkMinBytes));
+        const int64_t per = ((n + want_pieces - 1) / want_pieces + 4095) / 4096 * 4096;  // elements, 4096-aligned
+        const int pieces = (int)((n + per - 1) / per);
+        uint32_t *pf = d->piece_flags(buf);
+        for (int c = 0; c < pieces; ++c) {
+            const int64_t e0 = c * per, e1 = std::min(n, e0 + per);
+            ep::InCopy piece;
+            if (!x.in_copy(slot, pf + c, din + me * block + e0 * eb, hin + me * block + e0 * eb, (e1 - e0) * eb,
+                           c == pieces - 1 ? d->rs_landed(buf) + me : nullptr, piece, err))
+                return fail(EP_ERR_HIP, "%s: %s", who, err.c_str());
+            piece.eager = true;  // the host's sum, not a sender's rows: goes when summed
+            j.copies.push_back(piece);
+        }
         j.per_sender = false;
         for (int r = 0; r < R; ++r)
             if (r != me)
                 j.ready_all.push_back(d->rs_in(buf) + r);
-        const int64_t n = T * d->hidden;
         const bool f32 = d->f32_blocks;
         HostPool *pool = &d->pool;
+        Reducer *reducer = &d->reducer;
+        // the previous reduction into this buffer set must have gone down before this one
+        // overwrites its sum
+        const uint32_t prev = d->reduced_epoch[buf];
+        d->reduced_epoch[buf] = epoch;
+        const uint32_t *prev_landed = d->rs_landed(buf) + me;
+        uint32_t *status = d->status();
+        const int64_t timeout_us = d->timeout_us;
         j.before_copies = [=]() {
-            const std::function<void(int64_t, int64_t)> sum = [=](int64_t lo, int64_t hi) {
-                for (int64_t i0 = lo; i0 < hi; i0 += 4096) {
-                    const int64_t i1 = std::min(hi, i0 + 4096);
-                    float acc[4096];
-                    for (int64_t i = i0; i < i1; ++i)
-                        acc[i - i0] = 0.f;
-                    for (int r = 0; r < R; ++r) {
-                        if (r == me)
-                            continue;
-                        if (f32) {
-                            const float *src = reinterpret_cast<const float *>(hin + r * block);
-                            for (int64_t i = i0; i < i1; ++i)
-                                acc[i - i0] += src[i];
-                        } else {
-                            const uint16_t *src = reinterpret_cast<const uint16_t *>(hin + r * block);
-                            for (int64_t i = i0; i < i1; ++i)
-                                acc[i - i0] += bf16_to_f32(src[i]);
+            reducer->post([=]() {
+                if (prev != 0) {
+                    const auto w0 = std::chrono::steady_clock::now();
+                    while ((int32_t)(__atomic_load_n(prev_landed, __ATOMIC_ACQUIRE) - prev) < 0) {
+                        if (std::chrono::steady_clock::now() - w0 > std::chrono::microseconds(timeout_us)) {
+                            ep::record_host_timeout(status, ep::kSiteCourier, prev_landed, prev);
+                            break;
                         }
-                    }
-                    if (f32) {
-                        float *dst = reinterpret_cast<float *>(hin + me * block);
-                        for (int64_t i = i0; i < i1; ++i)
-                            dst[i] = acc[i - i0];
-                    } else {
-                        uint16_t *dst = reinterpret_cast<uint16_t *>(hin + me * block);
-                        for (int64_t i = i0; i < i1; ++i)
-                            dst[i] = f32_to_bf16(acc[i - i0]);
+                        std::this_thread::yield();
                     }
                 }
-            };
-            const auto t0 = std::chrono::steady_clock::now();
-            pool->run(n, sum);
-            ep::trace_host("host_reduce",
-                           std::chrono::duration<double, std::milli>(std::chrono::steady_clock::now() - t0).count());
+                const std::function<void(int64_t, int64_t)> sum = [=](int64_t lo, int64_t hi) {
+                    for (int64_t i0 = lo; i0 < hi; i0 += 4096) {
+                        const int64_t i1 = std::min(hi, i0 + 4096);
+                        float acc[4096];
+                        for (int64_t i = i0; i < i1; ++i)
+                            acc[i - i0] = 0.f;
+                        for (int r = 0; r < R; ++r) {
+                            if (r == me)
+                                continue;
+                            if (f32) {
+                                const float *src = reinterpret_cast<const float *>(hin + r * block);
+                                for (int64_t i = i0; i < i1; ++i)
+                                    acc[i - i0] += src[i];
+                            } else {
+                                const uint16_t *src = reinterpret_cast<const uint16_t *>(hin + r * block);
+                                for (int64_t i = i0; i < i1; ++i)
+                                    acc[i - i0] += bf16_to_f32(src[i]);
+                            }
+                        }
+                        if (f32) {
+                            float *dst = reinterpret_cast<float *>(hin + me * block);
+                            for (int64_t i = i0; i < i1; ++i)
+                                dst[i] = acc[i - i0];
+                        } else {
+                            uint16_t *dst = reinterpret_cast<uint16_t *>(hin + me * block);
+                            for (int64_t i = i0; i < i1; ++i)
+                                dst[i] = f32_to_bf16(acc[i - i0]);
+                        }
+                    }
+                };
+                // one pass of the pool: each of its `parts` threads sums its share of piece 0,
+                // then of piece 1, ...; the thread that finishes a piece last raises its flag,
+                // so piece c goes down while the threads sum piece c + 1
+                const auto t0 = std::chrono::steady_clock::now();
+                const int parts = pool->workers() + 1;
+                std::atomic<int> finished[kReduceChunks];
+                for (int c = 0; c < pieces; ++c)
+                    finished[c].store(0, std::memory_order_relaxed);
+                pool->run(parts, [&](int64_t lo, int64_t hi) {
+                    for (int c = 0; c < pieces; ++c) {
+                        const int64_t e0 = c * per, e1 = std::min(n, e0 + per), len = e1 - e0;
+                        for (int64_t q = lo; q < hi; ++q)
+                            sum(e0 + len * q / parts, e0 + len * (q + 1) / parts);
+                        if (finished[c].fetch_add((int)(hi - lo), std::memory_order_acq_rel) + (int)(hi - lo) == parts)
+                            __atomic_store_n(pf + c, epoch, __ATOMIC_RELEASE);
+                    }
+                });
+                ep::trace_host("host_reduce",
+                               std::chrono::duration<double, std::milli>(std::chrono::steady_clock::now() - t0).count());
+            });
         };
-        j.copies.push_back(own);
         add_wait(waits, d->rs_landed(buf) + me);
         d->bytes_down += block;
         bl.ptr[bl.n++] = blocks + me * block;

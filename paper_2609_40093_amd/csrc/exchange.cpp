@@ -230,6 +230,7 @@ ep_status exchange_dispatch(ep_staging *s, int b, uint32_t epoch, int64_t rows, 
             InCopy c;
             if (!x.in_copy(slot, ready, dst, src, len, s->in_landed(b) + r, c, err))
                 return fail(EP_ERR_HIP, "%s: %s", who, err.c_str());
+            c.eager = r == me;  // this rank's own rows wait for no sender
             plan.push_back(c);
             bt.add_wait(s->in_landed(b) + r);
         }
@@ -325,6 +326,7 @@ ep_status exchange_combine(ep_staging *s, int b, uint32_t epoch, int64_t rows, c
         InCopy c;
         if (!x.in_copy(slot, ready, dst, src, n * rb, s->recv_landed(b) + r, c, err))
             return fail(EP_ERR_HIP, "%s: %s", who, err.c_str());
+        c.eager = own_dup;  // this rank's own results wait for no sender
         plan.push_back(c);
         if (!acc)
             bt.add_wait(s->recv_landed(b) + r);

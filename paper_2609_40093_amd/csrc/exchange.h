@@ -23,8 +23,12 @@
 namespace ep {
 
 // One host->device copy of a sender's rows: queued once *ready holds the epoch, then a
-// 4-byte copy of the epoch into *landed.  Each of the two copies has its own completion
-// signal (done, landed_done), armed in the call's signal slot when the job is posted.
+// 4-byte copy of the epoch into *landed (none when landed is null: a piece of a larger
+// transfer whose last piece carries the flag).  Each of the two copies has its own
+// completion signal (done, landed_done), armed in the call's signal slot when the job is
+// posted.  An eager copy goes as soon as its own flag is in, also in an all-senders job
+// (a rank's own rows coming back from host memory, or a piece of a host-side result:
+// they wait for no other sender).
 struct InCopy {
     const uint32_t *ready;
     char *dst;
@@ -33,6 +37,7 @@ struct InCopy {
     hsa_signal_t done;
     uint32_t *landed;
     hsa_signal_t landed_done;
+    bool eager = false;
 };
 
 // The host->device copies of one call.  They all go to the one inbound engine and all
@@ -84,9 +89,8 @@ public:
             incoming_.pop_front();
         }
         for (InJob &j : active_)
-            for (const InCopy &c : j.copies)
-                if (dma_)
-                    submit(j, c);
+            if (dma_)
+                submit_all(j);
         active_.clear();
     }
     void post(InJob &&j) {
@@ -102,28 +106,71 @@ private:
         return !f || (int32_t)(__atomic_load_n(f, __ATOMIC_ACQUIRE) - j.epoch) >= 0;
     }
     static bool ready(const InJob &j, const InCopy &c) { return flag_ready(j, c.ready); }
-    // A copy that cannot be submitted gets its completion signal stored 0 by the host, so
-    // that nothing waits for it (the staging's status records the failure).
-    bool submit(InJob &j, const InCopy &c) {
+    // Copies a and b are next to each other in both the source and the destination.
+    static bool contiguous(const InCopy &a, const InCopy &b) {
+        return a.dst + a.len == b.dst && a.src + a.len == b.src;
+    }
+    // Queues copies [a, b) of the job, contiguous in memory, as one data copy on the
+    // inbound engine (completion signal of copy a), then each copy's flag copy after it.
+    // The data signals of copies a+1 .. b-1 go unused and are stored 0 by the host; so is
+    // every signal of a copy that cannot be submitted (the staging's status records it).
+    bool submit_run(InJob &j, size_t a, size_t b) {
         std::string err;
         const uint32_t eng = dma_->in_engine(0);
-        const bool data = dma_->copy(eng, c.dst, false, c.src, true, (size_t)c.len, &j.start, 1, c.done, err);
-        if (!data)
-            hsa_signal_store_screlease(c.done, 0);
-        if (data && dma_->copy(eng, c.landed, true, j.epoch_word, false, sizeof(uint32_t), &c.done, 1, c.landed_done,
-                               err))
-            return true;
-        hsa_signal_store_screlease(c.landed_done, 0);
-        __atomic_store_n(j.status, (uint32_t)EP_ERR_HIP, __ATOMIC_RELEASE);
-        return false;
+        int64_t len = 0;
+        for (size_t m = a; m < b; ++m)
+            len += j.copies[m].len;
+        const InCopy &first = j.copies[a];
+        const bool data = dma_->copy(eng, first.dst, false, first.src, true, (size_t)len, &j.start, 1, first.done, err);
+        for (size_t m = data ? a + 1 : a; m < b; ++m)
+            hsa_signal_store_screlease(j.copies[m].done, 0);
+        bool ok = data;
+        for (size_t m = a; m < b; ++m) {
+            const InCopy &c = j.copies[m];
+            if (!c.landed) {  // no flag for this piece
+                hsa_signal_store_screlease(c.landed_done, 0);
+                continue;
+            }
+            if (!(ok && dma_->copy(eng, c.landed, true, j.epoch_word, false, sizeof(uint32_t), &first.done, 1,
+                                   c.landed_done, err))) {
+                ok = false;
+                hsa_signal_store_screlease(c.landed_done, 0);
+            }
+        }
+        if (!ok)
+            __atomic_store_n(j.status, (uint32_t)EP_ERR_HIP, __ATOMIC_RELEASE);
+        return ok;
+    }
+    // Queues the copies marked in `go`, merging neighbours that are contiguous in memory,
+    // and removes them from the job.
+    void submit_marked(InJob &j, std::vector<char> &go) {
+        std::vector<InCopy> rest;
+        for (size_t i = 0; i < j.copies.size();) {
+            if (!go[i]) {
+                rest.push_back(j.copies[i++]);
+                continue;
+            }
+            size_t e = i + 1;
+            while (e < j.copies.size() && go[e] && contiguous(j.copies[e - 1], j.copies[e]))
+                ++e;
+            submit_run(j, i, e);
+            i = e;
+        }
+        j.copies.swap(rest);
+    }
+    void submit_all(InJob &j) {
+        std::vector<char> go(j.copies.size(), 1);
+        submit_marked(j, go);
     }
     // Queues what is ready; returns true once every copy of the job is queued.
     bool progress(InJob &j) {
         const bool late = std::chrono::steady_clock::now() > j.deadline;
+        // all-senders jobs: every sender's flag is in (eager copies go on their own flags and
+        // do not count: the host work of the job may be what raises them)
         bool all = true;
         if (!j.per_sender && !late) {
             for (const InCopy &c : j.copies)
-                all = all && ready(j, c);
+                all = all && (c.eager || ready(j, c));
             for (const uint32_t *f : j.ready_all)
                 all = all && flag_ready(j, f);
         }
@@ -136,16 +183,18 @@ private:
                 j.before_copies();
             j.before_copies = nullptr;
         }
-        for (size_t i = 0; i < j.copies.size();) {
-            if (late || (j.per_sender ? ready(j, j.copies[i]) : all)) {
-                if (late && !ready(j, j.copies[i]))
-                    record_host_timeout(j.status, kSiteCourier, j.copies[i].ready, j.epoch);
-                submit(j, j.copies[i]);  // queued even when late, so no wait on the device hangs
-                j.copies.erase(j.copies.begin() + (std::ptrdiff_t)i);
-            } else {
-                ++i;
-            }
+        std::vector<char> go(j.copies.size(), 0);
+        bool any = false;
+        for (size_t i = 0; i < j.copies.size(); ++i) {
+            const InCopy &c = j.copies[i];
+            const bool own_flag = ready(j, c);
+            go[i] = late || (own_flag && (j.per_sender || c.eager || all));
+            if (late && !own_flag)
+                record_host_timeout(j.status, kSiteCourier, c.ready, j.epoch);  // queued all the same,
+            any = any || go[i];                                                 // so no wait on the device hangs
         }
+        if (any)
+            submit_marked(j, go);
         return j.copies.empty();
     }
     void run() {

@@ -13,7 +13,7 @@
 //   - an engine waiting longer than the test allows.
 // Destroyed handles are recycled last-in first-out, as a signal pool would.
 //
-// Usage: dma_slots_test lane|exchange|order|bounded|old_rule [seed]; prints
+// Usage: dma_slots_test lane|exchange|order|merge|bounded|old_rule [seed]; prints
 // "violations N" and exits 0 when N == 0 and every check of the scenario held.
 #include "exchange.h"
 #include "sdma.h"
@@ -179,6 +179,8 @@ private:
 
 std::mutex g_eng_mu;
 std::map<uint32_t, std::unique_ptr<Engine>> g_engines;
+std::atomic<int64_t> g_copies{0}, g_copy_bytes_max{0};  // copies submitted, largest one
+
 Engine &engine(uint32_t id) {
     std::lock_guard<std::mutex> lk(g_eng_mu);
     auto &e = g_engines[id];
@@ -196,6 +198,9 @@ hsa_status_t submit(void *dst, const void *src, size_t len, uint32_t ndeps, cons
     if (!dst || !src || !done.handle)
         return HSA_STATUS_ERROR_INVALID_ARGUMENT;
     Copy c{dst, src, len, std::vector<hsa_signal_t>(deps, deps + ndeps), done, sig(done).gen.load()};
+    ++g_copies;
+    for (int64_t m = g_copy_bytes_max.load(); (int64_t)len > m && !g_copy_bytes_max.compare_exchange_weak(m, len);)
+        ;
     engine(eng).push(std::move(c));
     return HSA_STATUS_SUCCESS;
 }
@@ -570,6 +575,133 @@ void scenario_order() {
     std::printf("out-of-order senders: %.1f ms\n", ms);
 }
 
+// Inbound copies of one call that are next to each other in memory and whose senders
+// have all answered go down as one data copy, each sender's flag after it: four senders
+// ready at once give one copy of their four ranges and four flag copies.  An eager copy
+// of an all-senders job (a rank's own rows) goes before the other senders answer.
+void scenario_merge() {
+    ep::Exchange x;
+    x.init_with(kGpu, kCpu, 1u, {2u}, 4);
+    Stream stream;
+    uint32_t status[ep::kStatusWords] = {};
+    const int n = 4;
+    const int64_t part = 4096;
+    std::vector<uint8_t> src((size_t)(n * part)), dst((size_t)(n * part), 0);
+    for (size_t i = 0; i < src.size(); ++i)
+        src[i] = (uint8_t)(i * 7 + 3);
+    uint32_t ready[n] = {1, 1, 1, 1}, landed[n] = {0, 0, 0, 0}, epoch_word = 1;
+    std::string err;
+    int slot = x.begin(1000 * 1000, err);
+    hsa_signal_t start{};
+    check(slot >= 0 && x.start_signal(slot, start, err), "slot");
+    stream.release(ep::DmaEngines::value_pointer(start));
+    x.arm(slot, start);
+    const int64_t before = g_copies.load();
+    ep::InJob j;
+    j.epoch = 1;
+    j.per_sender = true;
+    j.start = start;
+    j.epoch_word = &epoch_word;
+    j.status = status;
+    j.deadline = Clock::now() + std::chrono::seconds(5);
+    for (int r = 0; r < n; ++r) {
+        ep::InCopy c;
+        check(x.in_copy(slot, &ready[r], reinterpret_cast<char *>(dst.data()) + r * part,
+                        reinterpret_cast<const char *>(src.data()) + r * part, part, &landed[r], c, err), "copy");
+        j.copies.push_back(c);
+        stream.wait(&landed[r], 1);
+    }
+    x.post(slot, std::move(j));
+    stream.finish();
+    check(g_copies.load() - before == 1 + n, "one data copy and one flag copy per sender");
+    check(g_copy_bytes_max.load() == n * part, "the data copy spans the four ranges");
+    check(dst == src, "every range landed");
+    for (int r = 0; r < n; ++r)
+        check(landed[r] == 1, "every sender's landed flag");
+
+    // all-senders job: the eager copy goes while another sender is still out
+    std::vector<uint8_t> own(4096, 9), own_dst(4096, 0), other(4096, 5), other_dst(4096, 0);
+    uint32_t own_ready = 2, other_ready = 0, own_landed = 0, other_landed = 0;
+    epoch_word = 2;
+    slot = x.begin(1000 * 1000, err);
+    check(slot >= 0 && x.start_signal(slot, start, err), "slot 2");
+    stream.release(ep::DmaEngines::value_pointer(start));
+    x.arm(slot, start);
+    ep::InJob k;
+    k.epoch = 2;
+    k.per_sender = false;
+    k.start = start;
+    k.epoch_word = &epoch_word;
+    k.status = status;
+    k.deadline = Clock::now() + std::chrono::seconds(5);
+    ep::InCopy c1, c2;
+    check(x.in_copy(slot, &own_ready, reinterpret_cast<char *>(own_dst.data()),
+                    reinterpret_cast<const char *>(own.data()), 4096, &own_landed, c1, err) &&
+              x.in_copy(slot, &other_ready, reinterpret_cast<char *>(other_dst.data()),
+                        reinterpret_cast<const char *>(other.data()), 4096, &other_landed, c2, err),
+          "copies");
+    c1.eager = true;
+    k.copies = {c1, c2};
+    x.post(slot, std::move(k));
+    const auto t0 = Clock::now();
+    while (__atomic_load_n(&own_landed, __ATOMIC_ACQUIRE) != 2 && Clock::now() - t0 < std::chrono::seconds(2))
+        std::this_thread::yield();
+    check(own_landed == 2 && own_dst == own, "the eager copy landed before the other sender answered");
+    check(__atomic_load_n(&other_landed, __ATOMIC_ACQUIRE) == 0, "the other copy waited");
+    __atomic_store_n(&other_ready, 2u, __ATOMIC_RELEASE);
+    stream.wait(&other_landed, 2);
+    stream.finish();
+    check(other_dst == other && status[0] == 0, "then the other copy landed");
+
+    // all-senders job whose copies are pieces of a host-side result: its host work runs
+    // once the senders' flags are in and raises each piece's flag as that piece is ready;
+    // the pieces' own flags do not hold back the host work that raises them
+    std::vector<uint8_t> sum(4 * 4096, 0), sum_dst(4 * 4096, 0);
+    uint32_t sender = 0, piece_flag[4] = {0, 0, 0, 0}, block_landed = 0;
+    epoch_word = 3;
+    slot = x.begin(1000 * 1000, err);
+    check(slot >= 0 && x.start_signal(slot, start, err), "slot 3");
+    stream.release(ep::DmaEngines::value_pointer(start));
+    x.arm(slot, start);
+    ep::InJob h;
+    h.epoch = 3;
+    h.per_sender = false;
+    h.start = start;
+    h.epoch_word = &epoch_word;
+    h.status = status;
+    h.deadline = Clock::now() + std::chrono::seconds(5);
+    h.ready_all.push_back(&sender);
+    for (int c = 0; c < 4; ++c) {
+        ep::InCopy piece;
+        check(x.in_copy(slot, &piece_flag[c], reinterpret_cast<char *>(sum_dst.data()) + c * 4096,
+                        reinterpret_cast<const char *>(sum.data()) + c * 4096, 4096, c == 3 ? &block_landed : nullptr,
+                        piece, err),
+              "piece");
+        piece.eager = true;
+        h.copies.push_back(piece);
+    }
+    std::thread worker;
+    h.before_copies = [&]() {
+        worker = std::thread([&]() {
+            for (int c = 0; c < 4; ++c) {
+                std::fill(sum.begin() + c * 4096, sum.begin() + (c + 1) * 4096, (uint8_t)(c + 11));
+                __atomic_store_n(&piece_flag[c], 3u, __ATOMIC_RELEASE);
+                std::this_thread::sleep_for(std::chrono::microseconds(200));
+            }
+        });
+    };
+    x.post(slot, std::move(h));
+    stream.wait(&block_landed, 3);
+    std::this_thread::sleep_for(std::chrono::milliseconds(2));
+    __atomic_store_n(&sender, 3u, __ATOMIC_RELEASE);
+    stream.finish();
+    if (worker.joinable())
+        worker.join();
+    check(block_landed == 3 && sum_dst == sum, "host-side pieces went down once their flags came");
+    check(status[0] == 0, "no timeout for the pieces");
+    x.release();
+}
+
 // A slot whose previous call left a signal that never reaches 0 is not handed out: begin()
 // gives up after its bound with a message, and succeeds once the signal retires.
 void scenario_bounded() {
@@ -648,12 +780,14 @@ int main(int argc, char **argv) {
         scenario_exchange(seed);
     else if (what == "order")
         scenario_order();
+    else if (what == "merge")
+        scenario_merge();
     else if (what == "bounded")
         scenario_bounded();
     else if (what == "old_rule")
         scenario_old_rule(seed);
     else {
-        std::printf("usage: %s lane|exchange|order|bounded|old_rule [seed]\n", argv[0]);
+        std::printf("usage: %s lane|exchange|order|merge|bounded|old_rule [seed]\n", argv[0]);
         return 2;
     }
     // let every queued copy finish before the engines stop

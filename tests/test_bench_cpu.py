@@ -124,3 +124,15 @@ def test_default_workload_is_the_prefill_layer():
         assert bench.parse().workload == "prefill"
     finally:
         sys.argv = old
+
+
+def test_pattern_bound_takes_the_slowest_direction_of_each_phase():
+    peaks = {"d2h_alone": 50.0, "h2d_alone": 40.0, "both": 80.0}   # GB/s
+    # one phase up only: 1 GB at 50 GB/s = 20 ms
+    assert bench.pattern_bound_us([(1e9, 0)], peaks) == pytest.approx(20000.0)
+    # both ways at once: 1 GB up, 3 GB down -> the download (75 ms) bounds it, not 4 GB / 80
+    assert bench.pattern_bound_us([(1e9, 3e9)], peaks) == pytest.approx(75000.0)
+    # equal both ways: the two-way peak bounds it (2 GB / 80 = 25 ms > 1 GB / 40 = 25 ms)
+    assert bench.pattern_bound_us([(1e9, 1e9)], peaks) == pytest.approx(25000.0)
+    # phases add up
+    assert bench.pattern_bound_us([(1e9, 0), (0, 1e9)], peaks) == pytest.approx(20000.0 + 25000.0)

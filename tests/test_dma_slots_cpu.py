@@ -14,6 +14,11 @@ Cases:
   jobs), senders answering in random order, exchanges recreated between batches;
 - order: a later call's sender answers before an earlier call's; both calls finish
   without waiting for the bound (the courier serves jobs in call order);
+- merge: inbound copies contiguous in memory whose senders have answered go down as one
+  data copy with each sender's flag after it; a rank's own rows (an eager copy) go down
+  before the other senders of an all-senders job answer; the pieces of a host-side result
+  (eager copies whose flags the job's host work raises) go down as each is ready, without
+  their flags holding back that host work;
 - bounded: a slot with a signal that never retires is refused after its bound, with a
   message; a failed copy (negative value) is reported once; nothing is destroyed while a
   decrement may still come;
@@ -68,6 +73,11 @@ def test_exchange_calls_never_reset_a_pending_signal(binary, seed):
 
 def test_senders_out_of_call_order_do_not_stall_the_inbound_engine(binary):
     rc, out = run(binary, "order", timeout=60)
+    assert rc == 0, out
+
+
+def test_contiguous_ready_copies_go_as_one_and_own_rows_go_first(binary):
+    rc, out = run(binary, "merge", timeout=60)
     assert rc == 0, out
 
 
