@@ -53,13 +53,11 @@ constexpr uint32_t kRoutingDuplicate = 2u;
 
 // Layout workspace (zero-filled before its first use):
 //   byte   0  uint32 routing status of the last call
-//   byte  64  uint32 ticket of the multi-tile count kernel (0 between calls)
 //   byte 192  int32 [3] rank count/offsets of a window layout (one segment)
-//   byte 256  int32 [tiles][E] each tile's counts per expert, then (after the count
-//             kernel) the rows of each expert in earlier tiles; then uint32 [tiles] the
-//             tiles' routing error bits
+//   byte 256  int32 [tiles][E] each tile's counts per expert (written by the count
+//             kernel, read by the rank kernel); then uint32 [tiles] the tiles' routing
+//             error bits
 constexpr size_t kWorkspaceHeader = 256;
-constexpr size_t kWorkspaceTicket = 64;
 constexpr size_t kWorkspaceScratch = 192;  // 3 words the one-segment local layout writes
 inline size_t layout_workspace_bytes(int64_t slots, int32_t experts) {
     const LayoutGeom g = layout_geometry(slots, experts);
@@ -89,7 +87,6 @@ struct LayoutArgs {
     int32_t *expert_counts, *expert_offsets, *rank_counts, *rank_offsets;
     int32_t *slot_pos, *row_src;
     uint32_t *status;        // workspace byte 0
-    uint32_t *ticket;        // workspace byte 64
     int32_t *tile_counts;    // workspace byte 256: [tiles][E]
     uint32_t *tile_errs;     // [tiles], after tile_counts
 };
@@ -98,7 +95,6 @@ inline void layout_workspace(LayoutArgs &a, void *workspace) {
     char *ws = static_cast<char *>(workspace);
     const LayoutGeom g = layout_geometry(a.slots, a.E);
     a.status = reinterpret_cast<uint32_t *>(ws);
-    a.ticket = reinterpret_cast<uint32_t *>(ws + kWorkspaceTicket);
     a.tile_counts = reinterpret_cast<int32_t *>(ws + kWorkspaceHeader);
     a.tile_errs = reinterpret_cast<uint32_t *>(a.tile_counts + g.tiles * (int64_t)a.E);
 }

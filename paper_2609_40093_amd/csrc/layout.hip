@@ -20,15 +20,17 @@
 // on which workgroups the device runs at once):
 //   count  each tile counts its entries per expert, checks the routing (ids outside [0,E),
 //          an expert twice in one token row) and stores its counts and error bits in the
-//          workspace.  The workgroup that finishes last (a ticket taken with one atomic
-//          add after a release fence) turns every expert's column of tile counts into
-//          exclusive prefixes in place, scans the expert totals, writes the counts,
-//          offsets and status, and puts the ticket back to 0 for the next call.
-//   rank   each tile counts its entries again (the same ballots), and writes every
-//          position: expert offset + rows of the expert in earlier tiles + in earlier
-//          waves + the entry's rank inside its wave.
-// Cross-tile traffic: tiles x (E+1) words written, read and rewritten once by the last
-// workgroup, and E words read per tile by the rank kernel.
+//          workspace.
+//   rank   each tile reads every tile's counts (a thread per run of tiles of an expert's
+//          column, 16 loads in flight), which gives the expert totals and the rows of each
+//          expert in earlier tiles; scans the totals; counts its own entries again (the
+//          same ballots) and writes every position: expert offset + rows of the expert in
+//          earlier tiles + in earlier waves + the entry's rank inside its wave.  Tile 0
+//          also writes the counts, offsets and status.
+// The kernel boundary orders the count kernel's stores before the rank kernel's loads: no
+// fence, atomic or counter is involved, so a layout captured in a graph replays as it runs.
+// Cross-tile traffic: tiles x E words written once, read by every rank workgroup (from L2
+// after its XCD's first miss), and tiles error words read by tile 0.
 #include "ep_internal.h"
 #include "wave.h"
 
@@ -257,13 +259,69 @@ __device__ void write_totals(const LayoutArgs &a, const int *tot, const int *off
 }
 
 enum LayoutPass { kWhole = 0, kCountPass = 1, kRankPass = 2 };
-constexpr int kLastBatch = 16;  // tile counts the last workgroup's threads load at once
+constexpr int kLastBatch = 16;  // tile counts a thread loads at once
 
-// LDS of every pass: wave_cnt [W][E], offs [E+1], tot [E], wave_sum [W], flags [4],
-// part [W*64] (the last workgroup's partial column sums).
+// LDS of every pass: wave_cnt [W][E], offs [E+1], tot [E], pre [E], wave_sum [W], flags [4],
+// part and part_pre [W*64] (partial column sums of the rank pass).
 template <int W>
 constexpr size_t layout_lds_ints(int E) {
-    return (size_t)W * E + (E + 1) + E + W + 4 + W * kWave;
+    return (size_t)W * E + (E + 1) + 2 * E + W + 4 + 2 * W * kWave;
+}
+
+// Rank pass: every tile's counts, summed per expert into tot[e] (all tiles) and pre[e]
+// (tiles before `tile`).  Column e's tiles are split into `groups` runs, one thread per
+// (run, column); the runs' sums meet in LDS.  Tile 0 also ORs every tile's error bits into
+// flags[0].  Ends with the workgroup synchronised.
+template <int W>
+__device__ void sum_tile_counts(const LayoutArgs &a, int tiles, int tile, int tid, int *tot, int *pre, int *part,
+                                int *part_pre, int *flags) {
+    constexpr int kThreads = W * kWave;
+    const int E = a.E;
+    const int groups = E < kThreads ? kThreads / E : 1;
+    const int per = (tiles + groups - 1) / groups;
+    for (int q = tid; q < groups * E; q += kThreads) {
+        const int g = q / E, e = q - g * E;
+        const int t_end = min(tiles, (g + 1) * per);
+        int s = 0, b = 0;
+        for (int t0 = g * per; t0 < t_end; t0 += kLastBatch) {
+            int held[kLastBatch];
+#pragma unroll
+            for (int u = 0; u < kLastBatch; ++u)  // kLastBatch loads in flight
+                held[u] = t0 + u < t_end ? a.tile_counts[(int64_t)(t0 + u) * E + e] : 0;
+#pragma unroll
+            for (int u = 0; u < kLastBatch; ++u) {
+                s += held[u];
+                b += t0 + u < tile ? held[u] : 0;
+            }
+        }
+        if (groups > 1) {
+            part[q] = s;
+            part_pre[q] = b;
+        } else {
+            tot[e] = s;
+            pre[e] = b;
+        }
+    }
+    if (tile == 0) {
+        uint32_t err_bits = 0;
+        for (int t = tid; t < tiles; t += kThreads)
+            err_bits |= a.tile_errs[t];
+        if (err_bits)
+            atomicOr(&flags[0], (int)err_bits);
+    }
+    __syncthreads();
+    if (groups > 1) {
+        for (int e = tid; e < E; e += kThreads) {
+            int s = 0, b = 0;
+            for (int g = 0; g < groups; ++g) {
+                s += part[g * E + e];
+                b += part_pre[g * E + e];
+            }
+            tot[e] = s;
+            pre[e] = b;
+        }
+        __syncthreads();
+    }
 }
 
 template <int W, int kPass>
@@ -274,9 +332,11 @@ __global__ __launch_bounds__(W * 64) void layout_kernel(LayoutArgs a, int32_t ro
     int *wave_cnt = lds;            // [W][E]: per-wave counts, then per-wave first rows
     int *offs = wave_cnt + W * E;   // [E+1] exclusive expert offsets
     int *tot = offs + E + 1;        // [E] rows per expert
-    int *wave_sum = tot + E;        // [W] scan carries
-    int *flags = wave_sum + W;      // [0] error bits [1] last-workgroup ticket
+    int *pre = tot + E;             // [E] rows per expert in earlier tiles (rank pass)
+    int *wave_sum = pre + E;        // [W] scan carries
+    int *flags = wave_sum + W;      // [0] error bits
     int *part = flags + 4;          // [kThreads]
+    int *part_pre = part + kThreads;  // [kThreads]
     const int tid = threadIdx.x, lane = tid & (kWave - 1), w = tid / kWave;
     const int tile = blockIdx.x;
     const int64_t run_begin = ((int64_t)tile * W + w) * rounds * kWave;
@@ -302,12 +362,18 @@ __global__ __launch_bounds__(W * 64) void layout_kernel(LayoutArgs a, int32_t ro
         flags[tid] = 0;
     __syncthreads();
 
+    if (kPass == kRankPass) {
+        sum_tile_counts<W>(a, tiles, tile, tid, tot, pre, part, part_pre, flags);
+        scan_experts<W>(E, tot, offs, wave_sum, tid);
+        if (tile == 0)
+            write_totals<W>(a, tot, offs, (uint32_t)flags[0], tid);
+    }
+
     count_tile<W, kPass != kRankPass>(a, run_begin, rounds, lane, wave_cnt, w, flags, ids, halo, rank);
     __syncthreads();
 
     if (kPass == kCountPass) {
-        // this tile's counts and error bits, all stored by wave 0: its one release fence
-        // (which writes back this XCD's L2) then covers every store the ticket publishes
+        // this tile's counts and error bits, for the rank kernel
         if (w == 0) {
             int32_t *counts = a.tile_counts + (int64_t)tile * E;
             for (int e = lane; e < E; e += kWave) {
@@ -319,83 +385,7 @@ __global__ __launch_bounds__(W * 64) void layout_kernel(LayoutArgs a, int32_t ro
             }
             if (lane == 0)
                 a.tile_errs[tile] = (uint32_t)flags[0];
-            __threadfence();
-            if (lane == 0) {
-                const uint32_t ticket = atomicAdd(a.ticket, 1u);
-                if (ticket == (uint32_t)(tiles - 1))
-                    __threadfence();  // acquire: the other tiles' counts, for the whole CU
-                flags[1] = (int)ticket;
-            }
         }
-        __syncthreads();
-        if (flags[1] != tiles - 1)
-            return;
-        // last workgroup: every tile's counts are in memory (the fence after the ticket
-        // pairs with each tile's fence before it).  Column e's tiles are split into
-        // `groups` runs, one thread per (run, column); each run's sum goes to LDS, then
-        // each thread rewrites its run as exclusive prefixes.
-        const int groups = E < kThreads ? kThreads / E : 1;
-        const int per = (tiles + groups - 1) / groups;
-        // runs of at most kLastBatch tiles stay in registers between the two passes
-        int held[kLastBatch];
-        for (int q = tid; q < groups * E; q += kThreads) {
-            const int g = q / E, e = q - g * E;
-            const int t_end = min(tiles, (g + 1) * per);
-            int s = 0;
-            for (int t0 = g * per; t0 < t_end; t0 += kLastBatch) {
-#pragma unroll
-                for (int u = 0; u < kLastBatch; ++u)  // kLastBatch loads in flight
-                    held[u] = t0 + u < t_end ? a.tile_counts[(int64_t)(t0 + u) * E + e] : 0;
-#pragma unroll
-                for (int u = 0; u < kLastBatch; ++u)
-                    s += held[u];
-            }
-            if (groups > 1)
-                part[q] = s;
-            else
-                tot[e] = s;
-        }
-        uint32_t err_bits = 0;
-        for (int t = tid; t < tiles; t += kThreads)
-            err_bits |= a.tile_errs[t];
-        if (err_bits)
-            atomicOr(&flags[0], (int)err_bits);
-        __syncthreads();
-        if (groups > 1)
-            for (int e = tid; e < E; e += kThreads) {
-                int s = 0;
-                for (int g = 0; g < groups; ++g)
-                    s += part[g * E + e];
-                tot[e] = s;
-            }
-        __syncthreads();
-        scan_experts<W>(E, tot, offs, wave_sum, tid);
-        write_totals<W>(a, tot, offs, (uint32_t)flags[0], tid);
-        // each run rewritten as exclusive prefixes: from the registers when the thread has
-        // one run of at most kLastBatch tiles, else read again
-        const bool one_run = groups * E <= kThreads && per <= kLastBatch;
-        for (int q = tid; q < groups * E; q += kThreads) {
-            const int g = q / E, e = q - g * E;
-            int run = 0;
-            for (int h = 0; h < g; ++h)
-                run += part[h * E + e];
-            const int t_end = min(tiles, (g + 1) * per);
-            for (int t0 = g * per; t0 < t_end; t0 += kLastBatch) {
-                if (!one_run) {
-#pragma unroll
-                    for (int u = 0; u < kLastBatch; ++u)
-                        held[u] = t0 + u < t_end ? a.tile_counts[(int64_t)(t0 + u) * E + e] : 0;
-                }
-#pragma unroll
-                for (int u = 0; u < kLastBatch; ++u)
-                    if (t0 + u < t_end) {
-                        a.tile_counts[(int64_t)(t0 + u) * E + e] = run;
-                        run += held[u];
-                    }
-            }
-        }
-        if (tid == 0)
-            __hip_atomic_store(a.ticket, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         return;
     }
 
@@ -412,9 +402,8 @@ __global__ __launch_bounds__(W * 64) void layout_kernel(LayoutArgs a, int32_t ro
         scan_experts<W>(E, tot, offs, wave_sum, tid);
         write_totals<W>(a, tot, offs, (uint32_t)flags[0], tid);
     }
-    const int32_t *pre = kPass == kRankPass ? a.tile_counts + (int64_t)tile * E : nullptr;
     for (int e = tid; e < E; e += kThreads) {
-        int base = kPass == kRankPass ? a.expert_offsets[e] + pre[e] : offs[e];
+        int base = kPass == kRankPass ? offs[e] + pre[e] : offs[e];
 #pragma unroll
         for (int v = 0; v < W; ++v) {
             const int c = wave_cnt[v * E + e];

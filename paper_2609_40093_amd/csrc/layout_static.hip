@@ -2,8 +2,8 @@
 // argument, for callers that cannot allocate device memory (code under HIP graph capture,
 // serving loops that must not allocate, harnesses that forbid it).
 //
-// The layout kernels' scratch (the ticket of the multi-tile count kernel and the tiles'
-// counts and error bits) is a file-scope device array of this library, one copy per GPU,
+// The layout kernels' scratch (the status word and the tiles' counts and error bits of a
+// multi-tile layout) is a file-scope device array of this library, one copy per GPU,
 // held until the process ends.  Its size is fixed: the layout geometry keeps the tile
 // counts at 16K words and the tiles at 1024 at most, whatever the number of routing
 // entries, so one array serves every size ep_dispatch_layout accepts.
@@ -12,10 +12,10 @@
 // a device address): the device address is read once per device with hipGetSymbolAddress,
 // with that device current, and kept; kernels get that address.
 //
-// Every call on one GPU shares that GPU's array.  The ticket must read 0 when a call
-// starts: the array starts zeroed, and every layout puts the ticket back to 0 before it
-// ends.  Calls that overlap on one GPU (other streams, or other host threads, without
-// ordering between them) race on the array.
+// Every call on one GPU shares that GPU's array, which keeps the last call's contents;
+// no call reads what an earlier one left there (the count kernel writes every tile count
+// the rank kernel reads).  Calls that overlap on one GPU (other streams, or other host
+// threads, without ordering between them) race on the array.
 #include "ep.h"
 #include "ep_internal.h"
 #include "staging.h"
