@@ -262,6 +262,7 @@ def main():
     del a, b
     same_copy = same_bytes_copy(dev, abytes[dominant], nsets)
     ceilings = streaming_ceilings(cfg, dev)
+    dest_streams = pack_destination_streams(cfg, staging, [st["x"] for st in sets], nsets, dev)
 
     result = {
         "metric": METRIC,
@@ -304,6 +305,7 @@ def main():
         "same_bytes_copy": dict(same_copy, kernel=dominant,
                                 kernel_speed_vs_copy=round(same_copy["avg_us"] / dk["avg_us"], 3)),
         "streaming_ceilings": ceilings,
+        "pack_destination_streams": dest_streams,
     }
     if warm is not None:
         result["warm_cache"] = {
@@ -747,17 +749,25 @@ def pattern_bound_us(phases, peaks) -> float:
 
 def pcie_peaks(dev) -> dict:
     """SDMA copies of 1 GiB between pinned host memory and HBM on the exchange's engines
-    (ep_pcie_probe): each direction alone and both at once on two engines."""
+    (ep_pcie_probe, best of four timed runs): each direction alone and both at once on two
+    engines, on two separately allocated pinned buffers, the faster of the two per
+    direction.  A probe on one buffer has now and then measured about half the
+    host->device rate that the exchange's own legs reach in the same run; the other buffer
+    keeps such an outlier out of the peak."""
     import torch
 
     import paper_2609_40093_amd as ep
     nbytes = 1 << 30
-    host = torch.empty(2 * nbytes, dtype=torch.uint8, pin_memory=True)
+    hosts = [torch.empty(2 * nbytes, dtype=torch.uint8, pin_memory=True) for _ in range(2)]
     devb = torch.empty(2 * nbytes, dtype=torch.uint8, device=dev)
-    res = {"d2h_alone": round(ep.pcie_probe(host, devb, nbytes, 1), 2),
-           "h2d_alone": round(ep.pcie_probe(host, devb, nbytes, 2), 2),
-           "both": round(ep.pcie_probe(host, devb, nbytes, 3), 2)}
-    del host, devb
+    runs = []
+    for host in hosts:
+        runs.append({"d2h_alone": round(ep.pcie_probe(host, devb, nbytes, 1), 2),
+                     "h2d_alone": round(ep.pcie_probe(host, devb, nbytes, 2), 2),
+                     "both": round(ep.pcie_probe(host, devb, nbytes, 3), 2)})
+    del hosts, devb
+    res = {key: max(r[key] for r in runs) for key in runs[0]}
+    res["per_buffer"] = runs
     return res
 
 
@@ -845,6 +855,51 @@ def streaming_ceilings(cfg, dev, launches: int = 10) -> dict:
     del src, dst
     res["note"] = ("ep_stream_probe over sequential addresses, non-temporal 16-byte vectors, one wave per unit; "
                    "buffer sets rotated past the 256 MB memory-side cache")
+    return res
+
+
+def pack_destination_streams(cfg, staging, xs, nsets: int, dev, launches: int = 6) -> dict:
+    """The path's own pack (ep_dispatch on HBM staging) with synthetic routings whose rows go
+    to S destination regions, each entry to a region drawn uniformly and rows grouped
+    stably by region as the layout groups them by expert -- S = 1 is the identity (each
+    token's k rows side by side), S = E the uniform routing over the layer's experts.  The
+    pack's bytes do not change with S; its time shows what HBM gives for S concurrent
+    write streams.  Launches rotate over the layer's buffer sets and are timed by events."""
+    import numpy as np
+    import torch
+
+    import paper_2609_40093_amd as ep
+    T, H, k, E = cfg.T, cfg.H, cfg.k, cfg.E
+    n = T * k
+    nbytes = T * 2 * H + n * 2 * H + 4 * n
+    rng = np.random.default_rng(20260601)
+    res = {}
+    for S in sorted({1, 8, 32, E}):
+        if S == 1:
+            pos = np.arange(n, dtype=np.int32)
+        else:
+            region = rng.integers(0, S, size=n)
+            pos = np.empty(n, dtype=np.int32)
+            pos[np.argsort(region, kind="stable")] = np.arange(n, dtype=np.int32)
+        sp = torch.from_numpy(pos).to(dev)
+        for j in range(2):
+            ep.dispatch(xs[j % len(xs)], sp, staging, topk=k, buf=j % nsets, epoch=1)
+        torch.cuda.synchronize()
+        ep.trace_reset()
+        ep.trace_enable(True)
+        for j in range(launches):
+            ep.dispatch(xs[j % len(xs)], sp, staging, topk=k, buf=j % nsets, epoch=1)
+        torch.cuda.synchronize()
+        ep.trace_enable(False)
+        st = ep.trace_read()["pack"]
+        ep.trace_reset()
+        us = st["mean_ms"] * 1e3
+        gbps = nbytes / (us * 1e-6) / 1e9
+        res[f"streams_{S}"] = {"launches": st["count"], "avg_us": round(us, 2), "GBps": round(gbps, 1),
+                               "frac": round(gbps / HBM_PEAK_GBPS, 4)}
+        del sp
+    res["note"] = ("ep_dispatch's pack on synthetic routings to S regions (uniform); the layer's own routing "
+                   "is skewed over its experts and sits between these figures")
     return res
 
 

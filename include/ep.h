@@ -474,8 +474,9 @@ ep_status ep_stream_probe(void *dst_dev, const void *src_dev, int64_t units, int
 
 /* PCIe probe on the SDMA engines the exchange uses: `dirs` bit 0 moves `bytes`
  * device->host (dev -> host), bit 1 host->device (host + bytes -> dev + bytes), both
- * bits at once on two engines.  host: pinned, dev: device, 2*bytes each.  Blocks; writes
- * the host-timed aggregate rate in GB/s (1e9 B/s) to *gbps. */
+ * bits at once on two engines.  host: pinned, dev: device, 2*bytes each.  Blocks; runs the
+ * copies five times (the first warms the engines) and writes the best host-timed aggregate
+ * rate of the other four in GB/s (1e9 B/s) to *gbps. */
 ep_status ep_pcie_probe(void *host, void *dev, size_t bytes, int32_t dirs, double *gbps);
 
 /* hipMemcpyAsync(kind = default) passthrough for bindings that hold raw pointers. */

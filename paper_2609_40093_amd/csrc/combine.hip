@@ -291,8 +291,13 @@ hipError_t launch_combine(const void *recv, const int32_t *slot_pos, const float
         hipLaunchKernelGGL(zero_fill_kernel, dim3((unsigned)blocks), dim3(256), 0, stream, static_cast<u32x4 *>(out), n);
         return hipGetLastError();
     }
-    // KC*U 16-byte loads per lane in flight: 16 for k >= 4, 4 for k = 2 and 3 (two-group
-    // chunks: more waves, which measured faster on MI355X than four-group chunks there)
+    // KC*U 16-byte loads per lane in flight: 16 for k >= 4 (8 for k >= 8 with rows of at
+    // least 12 KiB), 4 for k = 2 and 3.  Measured on MI355X: at k = 8 and 14 KiB rows,
+    // one-group chunks (twice the waves) beat two-group chunks by 2% at 32768 tokens and
+    // 1% at 16384, and tie at a few thousand; with 4 KiB rows two-group chunks are ahead
+    // by 1%.  At k = 2, two-group chunks beat four-group ones.
+    if (k >= 8 && V >= 768)
+        return launch_uk<1, 8>(recv, slot_pos, topk_w, T, V, k, out, out_f32, max_rows, stream, sel);
     if (k >= 8)
         return launch_uk<2, 8>(recv, slot_pos, topk_w, T, V, k, out, out_f32, max_rows, stream, sel);
     if (k >= 4)

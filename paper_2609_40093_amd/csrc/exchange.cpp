@@ -397,7 +397,7 @@ extern "C" ep_status ep_pcie_probe(void *host, void *dev, size_t bytes, int32_t 
     char *h = static_cast<char *>(host), *d = static_cast<char *>(dev);
     double best = 0.0;
     ep_status st = EP_OK;
-    for (int rep = 0; rep < 3 && st == EP_OK; ++rep) {  // first run warms the engines
+    for (int rep = 0; rep < 5 && st == EP_OK; ++rep) {  // first run warms the engines
         for (hsa_signal_t g : sig)
             hsa_signal_store_relaxed(g, 1);
         const auto t0 = std::chrono::steady_clock::now();
