@@ -30,6 +30,12 @@ METRIC = "dispatch & combine GB/s token payload (μs/MoE layer) + % HBM/PCIe roo
 HBM_PEAK_GBPS = 8000.0      # MI355X HBM3E
 PCIE_PEAK_GBPS = 64.0       # PCIe Gen5 x16, per direction
 MALL_BYTES = 256 << 20
+_T0 = time.perf_counter()
+
+
+def progress(msg: str) -> None:
+    """One line on stderr as each part of the run ends (the JSON line alone goes to stdout)."""
+    print(f"[bench +{time.perf_counter() - _T0:6.1f}s] {msg}", file=sys.stderr, flush=True)
 
 
 def parse():
@@ -110,6 +116,7 @@ def main():
     cfg = synth.config(args.workload)
     inp = synth.make_inputs(cfg)
     y = inp.expert_outputs()
+    progress(f"{cfg.name} layer inputs generated")
     T, H, E, k, R = cfg.T, cfg.H, cfg.E, cfg.k, cfg.R
     n = cfg.slots
     payload = cfg.payload_bytes
@@ -175,6 +182,7 @@ def main():
     t1 = time.perf_counter()
     timed_stats = ep.trace_read()
     ms_per_step = (t1 - t0) * 1e3 / args.steps
+    progress(f"{args.steps} timed steps: {ms_per_step * 1e3:.1f} us per layer")
     value = 2 * payload / (ms_per_step * 1e-3) / 1e9
     issue_us = (t_issue - t0) * 1e6 / args.steps
     # warm cache, beside the headline: every step on buffer set 0 (inputs and staging
@@ -199,6 +207,7 @@ def main():
     torch.cuda.synchronize()
     ep.trace_enable(False)
     breakdown = ep.trace_read()
+    progress(f"breakdown pass ({breakdown_steps} traced steps) done")
     # the roofline's launch averages come from the timed region (every launch of it on long
     # layers; one step in eight on short ones, where events on every launch would stretch
     # the kernels they bracket); other kernels from the breakdown pass
@@ -263,6 +272,7 @@ def main():
     same_copy = same_bytes_copy(dev, abytes[dominant], nsets)
     ceilings = streaming_ceilings(cfg, dev)
     dest_streams = pack_destination_streams(cfg, staging, [st["x"] for st in sets], nsets, dev)
+    progress("copy probes, streaming ceilings and pack destination streams done")
 
     result = {
         "metric": METRIC,
@@ -320,11 +330,13 @@ def main():
     # ---- pinned host staging: the same layer with SDMA legs, host flags, simulated peers
     if not args.no_pinned:
         result["pinned_staging"] = bench_pinned(cfg, inp, y, args, dev)
+        progress("pinned staging done")
 
     # ---- CPU baseline: the oracle on whole layers of the same workload, on all the host
     #      cores this process may use, and on one
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(cfg, inp, y, args.cpu_seconds)
+        progress("CPU baseline done")
 
     print(json.dumps(result))
 
@@ -472,6 +484,7 @@ def bench_pinned(cfg, inp, y, args, dev) -> dict:
             continue
         peers.close()
         st.close()
+        progress(f"pinned mode {name}: {ms * 1e3:.0f} us per layer")
         self_rows = int(counts[me]) if mode & ep.MODE_REMOTE_ONLY else 0
         if mode & ep.MODE_DUPLEX:
             pcie = 2 * (n - self_rows) * rb + 2 * (inbound_rows - self_rows) * rb
@@ -510,7 +523,9 @@ def bench_pinned(cfg, inp, y, args, dev) -> dict:
         except ep.EPError as e:
             return {"error": str(e)}
     dense = section(bench_dense, cfg, inp, args, dev, peaks)
+    progress("dense All-Gather / Reduce-Scatter layer done")
     graph = section(bench_graph, ["decode", cfg.name], args, dev, peaks)
+    progress("graph-replayed rounds done")
     decode_latency = section(bench_decode_latency, args, dev)
     return {
         "decode_dispatch_host_latency": decode_latency,
