@@ -860,11 +860,16 @@ def streaming_ceilings(cfg, dev, launches: int = 10) -> dict:
     src.fill_(1)
     mixes = {f"pack_like_1_to_{k}": (T, 1, k), f"combine_like_{k}_to_1": (T, k, 1),
              "copy_1_to_1": (rows // 2, 1, 1), "read_only": (rows, 1, 0), "write_only": (rows, 0, 1)}
-    res = {}
+    runs = []
     for name, (units, r, w) in mixes.items():
+        runs.append((name, units, r, w, False))
+        if w:  # the same mix with the pack's other store policy
+            runs.append((name + "_write_through", units, r, w, True))
+    res = {}
+    for name, units, r, w, wt in runs:
         def launch(j):
             off = (j % nsets) * set_bytes
-            ep.stream_probe(dst[off:], src[off:], units, row, r, w)
+            ep.stream_probe(dst[off:], src[off:], units, row, r, w, write_through=wt)
         for j in range(2):
             launch(j)
         torch.cuda.synchronize()
@@ -883,8 +888,9 @@ def streaming_ceilings(cfg, dev, launches: int = 10) -> dict:
                      "launches": st["count"], "avg_us": round(us, 2), "GBps": round(gbps, 1),
                      "frac": round(gbps / HBM_PEAK_GBPS, 4)}
     del src, dst
-    res["note"] = ("ep_stream_probe over sequential addresses, non-temporal 16-byte vectors, one wave per unit; "
-                   "buffer sets rotated past the 256 MB memory-side cache")
+    res["note"] = ("ep_stream_probe over sequential addresses, 16-byte vectors, one wave per unit, non-temporal "
+                   "stores (names ending _write_through: device-scope write-through stores); buffer sets rotated "
+                   "past the 256 MB memory-side cache")
     return res
 
 

@@ -7,7 +7,8 @@
 //                  consecutive rows (each written row the XOR of the rows read), so the
 //                  traffic has the read:write mix of a kernel of the path with none of its
 //                  routing -- 1:k like the dispatch's pack, k:1 like the combine, 1:0
-//                  read-only, 0:1 write-only -- over sequential addresses.
+//                  read-only, 0:1 write-only -- over sequential addresses, with either of
+//                  the pack's two store policies (RowStore).
 #include "ep_internal.h"
 
 namespace ep {
@@ -39,7 +40,7 @@ constexpr int kStreamMaxGroups = 16;  // 64-vector groups per row the probe hold
 // With no row to write, the XOR of everything read is stored (one 16-byte vector per
 // wave, into dst[unit % 64]) only if it equals a value that normal data does not give, so
 // the loads cannot be dropped.
-template <int G>
+template <int G, bool WT>
 __global__ __launch_bounds__(256) void stream_kernel(u32x4 *__restrict__ dst, const u32x4 *__restrict__ src,
                                                      int64_t units, int32_t reads, int32_t writes) {
     const int lane = threadIdx.x & 63;
@@ -70,34 +71,36 @@ __global__ __launch_bounds__(256) void stream_kernel(u32x4 *__restrict__ dst, co
             dst[unit % 64] = f;
         return;
     }
-    u32x4 *out = dst + unit * writes * kRow + lane;
-    for (int w = 0; w < writes; ++w)
+    u32x4 *out = dst + unit * writes * kRow;
+    for (int w = 0; w < writes; ++w) {
+        const RowStore<WT> row(out + w * kRow, (uint32_t)(kRow * 16));
 #pragma unroll
         for (int g = 0; g < G; ++g)
-            __builtin_nontemporal_store(acc[g], out + w * kRow + g * 64);
+            row.put(acc[g], g * 64 + lane);
+    }
 }
 
 }  // namespace
 
 hipError_t launch_stream_probe(void *dst, const void *src, int64_t units, int32_t row_bytes, int32_t reads,
-                               int32_t writes, hipStream_t stream) {
+                               int32_t writes, bool write_through, hipStream_t stream) {
     const int groups = row_bytes / 1024;
     if (units <= 0)
         return hipSuccess;
     const unsigned blocks = (unsigned)((units * 64 + 255) / 256);
     (void)hipGetLastError();
     TraceSlot ts = trace_acquire();
-    auto go = [&](auto kern) {
-        hipExtLaunchKernelGGL(kern, dim3(blocks), dim3(256), 0, stream, ts.start, ts.stop, 0, (u32x4 *)dst,
-                              (const u32x4 *)src, units, reads, writes);
+    auto go = [&](auto nt_kern, auto wt_kern) {
+        hipExtLaunchKernelGGL(write_through ? wt_kern : nt_kern, dim3(blocks), dim3(256), 0, stream, ts.start, ts.stop,
+                              0, (u32x4 *)dst, (const u32x4 *)src, units, reads, writes);
     };
     switch (groups) {
-    case 1: go(stream_kernel<1>); break;
-    case 2: go(stream_kernel<2>); break;
-    case 4: go(stream_kernel<4>); break;
-    case 8: go(stream_kernel<8>); break;
-    case 14: go(stream_kernel<14>); break;
-    case 16: go(stream_kernel<16>); break;
+    case 1: go(stream_kernel<1, false>, stream_kernel<1, true>); break;
+    case 2: go(stream_kernel<2, false>, stream_kernel<2, true>); break;
+    case 4: go(stream_kernel<4, false>, stream_kernel<4, true>); break;
+    case 8: go(stream_kernel<8, false>, stream_kernel<8, true>); break;
+    case 14: go(stream_kernel<14, false>, stream_kernel<14, true>); break;
+    case 16: go(stream_kernel<16, false>, stream_kernel<16, true>); break;
     default: return hipErrorInvalidValue;
     }
     hipError_t err = hipGetLastError();

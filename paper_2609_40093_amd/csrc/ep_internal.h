@@ -17,6 +17,39 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int kWave = 64;
 
+// Stores of one packed row (the dispatch's write stream) from a wave-uniform base, under
+// one of two policies picked by the bytes a launch writes (measured on MI355X, rows of 4 and
+// 14 KiB, inputs rotated past the memory-side cache):
+//   WT = false: non-temporal stores -- faster below 2 GiB per launch (up to 20% at 0.1-1 GiB);
+//   WT = true:  16-byte buffer stores at device scope (sc1: written through the XCD's L2
+//               rather than held there dirty) -- 1.5-2.5% faster from 2 GiB up, where the
+//               non-temporal rate falls with the size of the stream.
+// The buffer range of a write-through row is the `bytes` from `base` on: a store past it is
+// dropped by the hardware.
+constexpr int64_t kWriteThroughBytes = 2ll << 30;
+template <bool WT>
+struct RowStore;
+template <>
+struct RowStore<false> {
+    u32x4 *base;
+    __device__ __forceinline__ RowStore(u32x4 *b, uint32_t) : base(b) {}
+    __device__ __forceinline__ void put(u32x4 v, uint32_t vec) const { __builtin_nontemporal_store(v, base + vec); }
+};
+template <>
+struct RowStore<true> {
+    __amdgpu_buffer_rsrc_t rsrc;
+    __device__ __forceinline__ RowStore(u32x4 *b, uint32_t bytes) {
+        const uint64_t a = reinterpret_cast<uint64_t>(b);
+        const uint64_t u = ((uint64_t)__builtin_amdgcn_readfirstlane((uint32_t)(a >> 32)) << 32) |
+                           (uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)a);
+        rsrc = __builtin_amdgcn_make_buffer_rsrc(reinterpret_cast<void *>(u), 0,
+                                                 (int)__builtin_amdgcn_readfirstlane(bytes), 0x00020000);
+    }
+    __device__ __forceinline__ void put(u32x4 v, uint32_t vec) const {
+        __builtin_amdgcn_raw_buffer_store_b128(v, rsrc, vec * 16u, 0, 16 /* sc1 */);
+    }
+};
+
 // ---- layout geometry -----------------------------------------------------------
 // The routing array is cut into tiles, one workgroup each; a workgroup has W waves and
 // each wave walks `rounds` rounds of 64 entries.  W = 16 while 16 rows of per-wave
@@ -208,6 +241,6 @@ hipError_t launch_copy(void *dst, const void *src, size_t bytes, hipStream_t str
 // Streaming probe of a given read:write mix (copy.hip); row_bytes = 1024 * g with g in
 // {1, 2, 4, 8, 14, 16}.
 hipError_t launch_stream_probe(void *dst, const void *src, int64_t units, int32_t row_bytes, int32_t reads,
-                               int32_t writes, hipStream_t stream);
+                               int32_t writes, bool write_through, hipStream_t stream);
 
 }  // namespace ep

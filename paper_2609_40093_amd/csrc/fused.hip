@@ -362,10 +362,10 @@ __global__ __launch_bounds__(kFMaxThreads) void layout_pack_kernel(FusedArgs a, 
             const int64_t p = s_pos[(t - tok0) * K + j];
             if (p < 0 || p >= a.max_rows)
                 continue;
-            u32x4 *dst = packed + p * V + col + lane;
+            const RowStore<false> dst(packed + p * V + col, (uint32_t)(V - col) * 16u);
 #pragma unroll
             for (int u = 0; u < U; ++u)
-                __builtin_nontemporal_store(d[u], dst + u * kWave);
+                dst.put(d[u], u * kWave + lane);
         }
     }
 }

@@ -67,7 +67,7 @@ def test_binding_covers_every_symbol():
 
 
 def test_status_names(lib):
-    assert lib.ep_abi_version() == _lib.ABI_VERSION == 4
+    assert lib.ep_abi_version() == _lib.ABI_VERSION == 5
     assert lib.ep_status_name(0) == b"EP_OK"
     assert lib.ep_status_name(5) == b"EP_ERR_TIMEOUT"
     assert lib.ep_status_name(99) == b"EP_ERR_UNKNOWN"
