@@ -14,7 +14,7 @@ import torch
 
 import oracle
 import paper_2609_40093_amd as ep
-from gpu_cases import TOL_MAX_ABS, TOL_MEAN_ABS, combine_errors, compare_combine, compare_packed_rows, say
+from gpu_cases import TOL_MAX_ABS, TOL_MEAN_ABS, combine_errors, compare_combine, compare_packed_rows, routing, say
 from paper_2609_40093_amd import synth
 
 pytestmark = pytest.mark.gpu
@@ -128,3 +128,27 @@ def test_coarse_layer_as_the_benchmark_runs_it():
         mx, mean = combine_errors(s["out"].view(torch.int16).cpu().numpy().view(np.uint16), exact)
         assert mx <= TOL_MAX_ABS and mean <= TOL_MEAN_ABS, f"set {b}: combine max {mx} mean {mean}"
     st.close()
+
+
+@pytest.mark.parametrize("k,H,T", [(8, 7176, 18720), (2, 7168, 74900), (2, 7176, 74820)])
+def test_write_through_pack_instances(k, H, T):
+    """Pack launches that write 2 GiB or more use the write-through store instances: the
+    per-slot kernel with rows that are not whole 64-vector groups (H = 7176), and the
+    one-wave-per-chunk kernel (k = 2) with whole-group and with ragged rows.  Every packed
+    row is compared with the pack definition."""
+    E, R = 64, 8
+    n = T * k
+    assert n * 2 * H >= 2 << 30, "the case must write at least 2 GiB"
+    say(f"write-through pack instance: T={T} H={H} k={k}")
+    idx = routing("random", T, E, k, seed=T)
+    ref = oracle.layout(idx, E, R)
+    assert ref.status == oracle.OK
+    x = synth.normal_bf16_rows(np.random.SeedSequence([11, T, H, k]), T, H)
+    x_d = torch.from_numpy(x.view(np.int16)).to(DEV)
+    sp_d = torch.from_numpy(ref.slot_pos).to(DEV)
+    out = torch.empty((n, H), dtype=torch.int16, device=DEV)
+    ep.pack(x_d, sp_d, out, topk=k)
+    torch.cuda.synchronize()
+    del x_d
+    compare_packed_rows(lambda r0, r1: out[r0:r1].cpu().numpy().view(np.uint16), x, ref.row_src, k, n,
+                        f"write-through pack T={T} H={H} k={k}")
