@@ -437,7 +437,8 @@ extern "C" ep_status ep_allgather(ep_dense *d, int32_t buf, uint32_t epoch, cons
     EP_HIP(ep::launch_stamp_release(ew, epoch, ep::DmaEngines::value_pointer(start), stream));
     x.arm(slot, start);
     if (!x.copy(slot, x.dma.out_engine(), hag + me * shard, true, x_dev, false, (size_t)shard, &start, 1, &sent, err) ||
-        !x.copy(slot, x.dma.out_engine(), d->ag(buf) + me, true, ew, false, sizeof(uint32_t), &sent, 1, nullptr, err))
+        !x.copy(slot, x.dma.out_flag_engine(), d->ag(buf) + me, true, ew, false, sizeof(uint32_t), &sent, 1, nullptr,
+                err))
         return fail(EP_ERR_HIP, "%s: %s", who, err.c_str());
     d->bytes_up += shard;
     ep::GateArgs waits;
@@ -463,6 +464,7 @@ extern "C" ep_status ep_allgather(ep_dense *d, int32_t buf, uint32_t epoch, cons
         j.per_sender = d->mode & EP_MODE_PER_SENDER;
         j.start = start;
         j.epoch_word = ew;
+        j.epoch_words = ep::kEpochRowWords;
         j.status = d->status();
         j.deadline = std::chrono::steady_clock::now() + std::chrono::microseconds(d->timeout_us);
         x.post(slot, std::move(j));
@@ -512,7 +514,7 @@ extern "C" ep_status ep_reducescatter(ep_dense *d, int32_t buf, uint32_t epoch, 
         hsa_signal_t dn{};
         if (!x.copy(slot, x.dma.out_engine(), hout + r * block, true, blocks + r * block, false, (size_t)block, &start,
                     1, &dn, err) ||
-            !x.copy(slot, x.dma.out_engine(), d->rs_out(buf) + r, true, ew, false, sizeof(uint32_t), &dn, 1, nullptr,
+            !x.copy(slot, x.dma.out_flag_engine(), d->rs_out(buf) + r, true, ew, false, sizeof(uint32_t), &dn, 1, nullptr,
                     err))
             return fail(EP_ERR_HIP, "%s: %s", who, err.c_str());
         d->bytes_up += block;
@@ -525,6 +527,7 @@ extern "C" ep_status ep_reducescatter(ep_dense *d, int32_t buf, uint32_t epoch, 
     j.epoch = epoch;
     j.start = start;
     j.epoch_word = ew;
+    j.epoch_words = ep::kEpochRowWords;
     j.status = d->status();
     j.deadline = std::chrono::steady_clock::now() + std::chrono::microseconds(d->timeout_us);
     if (R > 1 && !reduce_on_host) {

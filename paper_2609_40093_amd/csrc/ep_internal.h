@@ -209,7 +209,11 @@ struct GateArgs {
     uint32_t site = 0;           // set by launch_gate from its name
 };
 hipError_t launch_gate(const char *name, const GateArgs &g, hipStream_t stream);
-// Stores `epoch` into *epoch_word, then 0 into *value (a DMA start signal).
+// Words of a buffer set's device epoch row: the sources of the DMA flag copies, one word
+// per flag of a merged flag copy.
+constexpr int kEpochRowWords = 64;
+// Stores `epoch` into the kEpochRowWords words of epoch_word[], then 0 into *value (a DMA
+// start signal).
 hipError_t launch_stamp_release(uint32_t *epoch_word, uint32_t epoch, int64_t *value, hipStream_t stream);
 // Copies n int32 from device memory to host words host[0..n), then stores `epoch` in host[n].
 hipError_t launch_mirror(const int32_t *src, int32_t n, uint32_t *host, uint32_t epoch, hipStream_t stream);

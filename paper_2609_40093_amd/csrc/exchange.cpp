@@ -90,6 +90,7 @@ void post_inbound(Exchange &x, int slot, const ep_staging *s, std::vector<InCopy
     j.per_sender = per_sender;
     j.start = start;
     j.epoch_word = epoch_word;
+    j.epoch_words = kEpochRowWords;  // every call that posts inbound copies stamps the whole row
     j.status = s->status();
     j.deadline = std::chrono::steady_clock::now() + std::chrono::microseconds(s->timeout_us);
     x.post(slot, std::move(j));
@@ -166,7 +167,7 @@ ep_status exchange_dispatch(ep_staging *s, int b, uint32_t epoch, int64_t rows, 
     const int slot = x.begin(s->timeout_us, err);
     if (slot < 0)
         return fail(EP_ERR_TIMEOUT, "%s: %s", who, err.c_str());
-    const uint32_t *ew = s->epoch_word(b);
+    uint32_t *ew = s->epoch_word(b);
     char *dsend = static_cast<char *>(s->dev_send[b]);
     char *hsend = static_cast<char *>(s->host_send[b]);
 
@@ -176,7 +177,7 @@ ep_status exchange_dispatch(ep_staging *s, int b, uint32_t epoch, int64_t rows, 
     if (!x.start_signal(slot, start, err))
         return fail(EP_ERR_HIP, "%s: %s", who, err.c_str());
     EP_HIP(hipEventRecord(s->ev_sysrel, stream));
-    EP_HIP(launch_release_signal(DmaEngines::value_pointer(start), stream));
+    EP_HIP(launch_stamp_release(ew, epoch, DmaEngines::value_pointer(start), stream));  // the flags' epoch row
     x.arm(slot, start);
     const int64_t bytes = rows * rb, chunk = s->chunk_bytes;
     const int64_t chunks = (bytes + chunk - 1) / chunk;
@@ -203,7 +204,7 @@ ep_status exchange_dispatch(ep_staging *s, int b, uint32_t epoch, int64_t rows, 
                     return fail(EP_ERR_HIP, "%s: %s", who, err.c_str());
                 ++nd;
             }
-            if (!flag_copy(x, slot, out, s->send_flags(b) + c, ew, deps, nd ? nd : 1, err))
+            if (!flag_copy(x, slot, x.dma.out_flag_engine(), s->send_flags(b) + c, ew, deps, nd ? nd : 1, err))
                 return fail(EP_ERR_HIP, "%s: %s", who, err.c_str());
         }
         bt.add_wait(s->send_flags(b) + (chunks - 1));
@@ -298,7 +299,7 @@ ep_status exchange_combine(ep_staging *s, int b, uint32_t epoch, int64_t rows, c
             hsa_signal_t d{};
             if (!x.copy(slot, out, hret + off[r] * rb, true, din + off[r] * rb, false, (size_t)(rin[r] * rb), &start,
                         1, &d, err) ||
-                !flag_copy(x, slot, out, s->ret_flags(b) + r, ew, &d, 1, err))
+                !flag_copy(x, slot, x.dma.out_flag_engine(), s->ret_flags(b) + r, ew, &d, 1, err))
                 return fail(EP_ERR_HIP, "%s: %s", who, err.c_str());
             bt.add_wait(s->ret_flags(b) + r);
         }

@@ -49,7 +49,8 @@ struct InJob {
     uint32_t epoch = 0;
     bool per_sender = false;
     hsa_signal_t start{};
-    const uint32_t *epoch_word = nullptr;
+    const uint32_t *epoch_word = nullptr;  // source of the landed flags: epoch_words words of the epoch
+    int epoch_words = 1;
     uint32_t *status = nullptr;
     std::chrono::steady_clock::time_point deadline;
 };
@@ -111,9 +112,11 @@ private:
         return a.dst + a.len == b.dst && a.src + a.len == b.src;
     }
     // Queues copies [a, b) of the job, contiguous in memory, as one data copy on the
-    // inbound engine (completion signal of copy a), then each copy's flag copy after it.
-    // The data signals of copies a+1 .. b-1 go unused and are stored 0 by the host; so is
-    // every signal of a copy that cannot be submitted (the staging's status records it).
+    // inbound engine (completion signal of copy a), then their landed flags on the inbound
+    // flag engine after it: flags of neighbouring copies that are neighbouring words go as
+    // one copy of up to epoch_words words (completion signal of its first copy).  The
+    // signals that go unused are stored 0 by the host; so is every signal of a copy that
+    // cannot be submitted (the staging's status records it).
     bool submit_run(InJob &j, size_t a, size_t b) {
         std::string err;
         const uint32_t eng = dma_->in_engine(0);
@@ -125,17 +128,25 @@ private:
         for (size_t m = data ? a + 1 : a; m < b; ++m)
             hsa_signal_store_screlease(j.copies[m].done, 0);
         bool ok = data;
-        for (size_t m = a; m < b; ++m) {
+        const uint32_t feng = dma_->in_flag_engine();
+        for (size_t m = a; m < b;) {
             const InCopy &c = j.copies[m];
             if (!c.landed) {  // no flag for this piece
                 hsa_signal_store_screlease(c.landed_done, 0);
+                ++m;
                 continue;
             }
-            if (!(ok && dma_->copy(eng, c.landed, true, j.epoch_word, false, sizeof(uint32_t), &first.done, 1,
-                                   c.landed_done, err))) {
+            size_t e = m + 1;
+            while (e < b && (int)(e - m) < j.epoch_words && j.copies[e].landed == c.landed + (e - m))
+                ++e;
+            if (!(ok && dma_->copy(feng, c.landed, true, j.epoch_word, false, (e - m) * sizeof(uint32_t), &first.done,
+                                   1, c.landed_done, err))) {
                 ok = false;
                 hsa_signal_store_screlease(c.landed_done, 0);
             }
+            for (size_t q = m + 1; q < e; ++q)
+                hsa_signal_store_screlease(j.copies[q].landed_done, 0);
+            m = e;
         }
         if (!ok)
             __atomic_store_n(j.status, (uint32_t)EP_ERR_HIP, __ATOMIC_RELEASE);
@@ -242,9 +253,11 @@ public:
         courier.start(&dma);
         return true;
     }
-    // The same on engines chosen by the caller.
-    void init_with(hsa_agent_t gpu, hsa_agent_t cpu, uint32_t out, const std::vector<uint32_t> &in, int nslots) {
-        dma.init_with(gpu, cpu, out, in);
+    // The same on engines chosen by the caller (flag engines 0: the flags go on the engine
+    // of their data).
+    void init_with(hsa_agent_t gpu, hsa_agent_t cpu, uint32_t out, const std::vector<uint32_t> &in, int nslots,
+                   uint32_t out_flag = 0, uint32_t in_flag = 0) {
+        dma.init_with(gpu, cpu, out, in, out_flag, in_flag);
         slots.init(nslots);
         courier.start(&dma);
     }

@@ -109,11 +109,14 @@ bool SdmaLane::init(int device, int slots, std::string &err) {
         pref = 0;
     const uint32_t pick = (pref & avail) ? (pref & avail) : avail;
     const uint32_t engine = pick ? (pick & (~pick + 1u)) : 0u;  // lowest usable engine
-    init_with(gpu, cpu, engine, slots);
+    const uint32_t rest = avail & ~engine;
+    const uint32_t flag_engine = engine && rest ? (rest & (~rest + 1u)) : 0u;  // the next one, for the flags
+    init_with(gpu, cpu, engine, slots, flag_engine);
     owns_rocr_ = true;
     char name[64];
     if (engine)
-        std::snprintf(name, sizeof name, "sdma%d (available mask 0x%x)", engine_index(engine), avail);
+        std::snprintf(name, sizeof name, "sdma%d, flags sdma%d (available mask 0x%x)", engine_index(engine),
+                      engine_index(flag_engine_), avail);
     else
         std::snprintf(name, sizeof name, "runtime-chosen");
     engine_name_ = name;
@@ -142,11 +145,18 @@ bool DmaEngines::init(int device, std::string &err) {
     std::vector<uint32_t> in;
     for (uint32_t m = in_avail & ~out; m; m &= m - 1)
         in.push_back(m & (~m + 1u));
-    init_with(gpu, cpu, out, in);
+    // the flag engines: two more engines that can write host memory, apart from the data
+    // engines (none left: the flags share their data's engine)
+    std::vector<uint32_t> spare;
+    for (uint32_t m = out_avail & ~out & ~(in.empty() ? 0u : in[0]); m; m &= m - 1)
+        spare.push_back(m & (~m + 1u));
+    const uint32_t out_flag = spare.size() > 1 ? spare[1] : 0u, in_flag = spare.empty() ? 0u : spare[0];
+    init_with(gpu, cpu, out, in, out_flag, in_flag);
     owns_rocr_ = true;
-    char buf[96];
-    std::snprintf(buf, sizeof buf, "out sdma%d, in %d engines (masks out 0x%x in 0x%x)", engine_index(out_),
-                  (int)in_.size(), out_avail, in_avail);
+    char buf[128];
+    std::snprintf(buf, sizeof buf, "out sdma%d, in %d engines, flags sdma%d / sdma%d (masks out 0x%x in 0x%x)",
+                  engine_index(out_), (int)in_.size(), engine_index(out_flag_engine()),
+                  engine_index(in_flag_engine()), out_avail, in_avail);
     desc_ = buf;
     return true;
 }

@@ -9,10 +9,11 @@ namespace ep {
 
 // ---------------------------------------------------------------------- SdmaLane
 
-void SdmaLane::init_with(hsa_agent_t gpu, hsa_agent_t cpu, uint32_t engine, int slots) {
+void SdmaLane::init_with(hsa_agent_t gpu, hsa_agent_t cpu, uint32_t engine, int slots, uint32_t flag_engine) {
     gpu_ = gpu;
     cpu_ = cpu;
     engine_ = engine;
+    flag_engine_ = flag_engine ? flag_engine : engine;
     engine_name_ = engine ? "sdma (caller-chosen)" : "runtime-chosen";
     slots_.init(slots);
     owns_rocr_ = false;
@@ -48,14 +49,14 @@ bool SdmaLane::begin(Round &r, int64_t timeout_us, std::string &err) {
     return true;
 }
 
-bool SdmaLane::copy(int slot, void *dst, const void *src, size_t len, const hsa_signal_t *dep, hsa_signal_t *done,
-                    std::string &err) {
+bool SdmaLane::copy(int slot, uint32_t engine, void *dst, const void *src, size_t len, const hsa_signal_t *dep,
+                    hsa_signal_t *done, std::string &err) {
     if (!slots_.take(slot, *done, err))
         return false;
     hsa_status_t st;
-    if (engine_)
+    if (engine)
         st = hsa_amd_memory_async_copy_on_engine(dst, cpu_, src, gpu_, len, 1, dep, *done,
-                                                 (hsa_amd_sdma_engine_id_t)engine_, false);
+                                                 (hsa_amd_sdma_engine_id_t)engine, false);
     else
         st = hsa_amd_memory_async_copy(dst, cpu_, src, gpu_, len, 1, dep, *done);
     if (st != HSA_STATUS_SUCCESS) {
@@ -76,8 +77,8 @@ bool SdmaLane::submit(const Round &r, void *host_dst, const void *dev_src, int64
         const int64_t off = c * chunk_bytes;
         const size_t len = (size_t)std::min<int64_t>(chunk_bytes, bytes - off);
         hsa_signal_t data{}, flag{};
-        if (!copy(r.slot, dst + off, src + off, len, &r.start, &data, err) ||
-            !copy(r.slot, flags + c, epoch_word, sizeof(uint32_t), &data, &flag, err))
+        if (!copy(r.slot, engine_, dst + off, src + off, len, &r.start, &data, err) ||
+            !copy(r.slot, flag_engine_, flags + c, epoch_word, sizeof(uint32_t), &data, &flag, err))
             return false;
     }
     return true;
@@ -88,11 +89,13 @@ bool SdmaLane::drain(int64_t timeout_us, std::string &err) { return slots_.drain
 // ---------------------------------------------------------------------- DmaEngines
 
 void DmaEngines::init_with(hsa_agent_t gpu, hsa_agent_t cpu, uint32_t out_engine,
-                           const std::vector<uint32_t> &in_engines) {
+                           const std::vector<uint32_t> &in_engines, uint32_t out_flag_engine, uint32_t in_flag_engine) {
     gpu_ = gpu;
     cpu_ = cpu;
     out_ = out_engine;
     in_ = in_engines;
+    out_flag_ = out_flag_engine;
+    in_flag_ = in_flag_engine;
     desc_ = "caller-chosen engines";
     owns_rocr_ = false;
     ready_ = true;

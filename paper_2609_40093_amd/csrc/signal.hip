@@ -108,12 +108,15 @@ __global__ __launch_bounds__(64) void gate_kernel(GateArgs g) {
         __hip_atomic_store(g.release[0], (int64_t)0, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_SYSTEM);
 }
 
-// Stores the round's epoch into the word the DMA flag copies read, then releases a copy.
+// Stores the round's epoch into the row of words the DMA flag copies read (a merged flag
+// copy reads one word per flag), then releases the copies.
 __global__ __launch_bounds__(64) void stamp_release_kernel(uint32_t *epoch_word, uint32_t epoch, int64_t *value) {
-    if (threadIdx.x == 0) {
-        __hip_atomic_store(epoch_word, epoch, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+    static_assert(kEpochRowWords <= 64, "one lane per word of the epoch row");
+    if (threadIdx.x < kEpochRowWords)
+        __hip_atomic_store(epoch_word + threadIdx.x, epoch, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+    __syncthreads();
+    if (threadIdx.x == 0)
         __hip_atomic_store(value, (int64_t)0, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_SYSTEM);
-    }
 }
 
 // Copies n int32 values (rank offsets) to host memory, then the epoch as a tag after them.

@@ -49,7 +49,7 @@ inline bool aligned16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 
 
 constexpr int kMaxBuffers = 8;
 constexpr int64_t kDefaultChunk = 64ll << 20;
-constexpr size_t kEpochStride = 64;  // one device epoch word per buffer set, 64 B apart
+constexpr size_t kEpochStride = kEpochRowWords * sizeof(uint32_t);  // one device epoch row per buffer set
 constexpr int kSdmaSlots = 4;        // host-leg rounds in flight per staging
 
 // true: the default device->host leg goes through hipMemcpyAsync instead of the SDMA lane

@@ -365,12 +365,13 @@ const hsa_agent_t kGpu{1}, kCpu{2};
 // Rounds of the default device->host leg with a chunk count that changes from round to
 // round (so a signal's role in one round differs from its role in the last round on the
 // same slot), the host running ahead of the copies, and lanes created and released
-// between batches (destroyed handles recycled).
+// between batches (destroyed handles recycled); the chunk flags on the data engine in
+// even batches and on an engine of their own in odd ones.
 void scenario_lane(uint32_t seed) {
     std::mt19937 rng(seed);
     for (int batch = 0; batch < 6; ++batch) {
         ep::SdmaLane lane;
-        lane.init_with(kGpu, kCpu, 1u, 4);
+        lane.init_with(kGpu, kCpu, 1u, 4, batch % 2 ? 3u : 0u);
         Stream stream;
         struct R {
             std::vector<uint8_t> src, dst;
@@ -416,27 +417,32 @@ void scenario_lane(uint32_t seed) {
     }
 }
 
-// Calls of the exchange modes: outbound copies with flag copies on one engine, inbound
-// copies queued by the courier as simulated senders raise their flags at random times,
-// with the number of copies per call changing from call to call; exchanges created and
-// released between batches.
+// Calls of the exchange modes: outbound copies with their flag copies, inbound copies
+// queued by the courier as simulated senders raise their flags at random times, with the
+// number of copies per call changing from call to call; exchanges created and released
+// between batches.  Even batches put the flags on the engines of their data, odd ones on
+// two flag engines; every other call gives the courier an epoch row, so that the landed
+// flags of merged inbound copies go as one flag copy.
 void scenario_exchange(uint32_t seed) {
     std::mt19937 rng(seed);
     for (int batch = 0; batch < 6; ++batch) {
         ep::Exchange x;
-        x.init_with(kGpu, kCpu, 1u, {2u}, 4);
+        x.init_with(kGpu, kCpu, 1u, {2u}, 4, batch % 2 ? 3u : 0u, batch % 2 ? 4u : 0u);
         Stream stream;
         uint32_t status[ep::kStatusWords] = {};
         struct Call {
             std::vector<std::vector<uint8_t>> out_src, out_dst, in_src, in_dst;
             std::vector<uint32_t> out_flags, ready, landed;
             uint32_t epoch, epoch_word;
+            uint32_t epoch_row[64];
         };
         std::vector<std::unique_ptr<Call>> calls;
         std::vector<std::thread> senders;
         for (int i = 0; i < 50; ++i) {
             std::unique_ptr<Call> c(new Call);
             c->epoch = c->epoch_word = (uint32_t)(batch * 1000 + i + 1);
+            for (uint32_t &w : c->epoch_row)
+                w = c->epoch;
             const int nout = (int)(rng() % 4), nin = 1 + (int)(rng() % 6);
             for (int k = 0; k < nout; ++k) {
                 c->out_src.emplace_back(64 + rng() % 512);
@@ -467,8 +473,8 @@ void scenario_exchange(uint32_t seed) {
                 hsa_signal_t d{};
                 check(x.copy(slot, 1u, c->out_dst[(size_t)k].data(), true, c->out_src[(size_t)k].data(), false,
                              c->out_src[(size_t)k].size(), &start, 1, &d, err) &&
-                          x.copy(slot, 1u, &c->out_flags[(size_t)k], true, &c->epoch_word, false, sizeof(uint32_t),
-                                 &d, 1, nullptr, err),
+                          x.copy(slot, x.dma.out_flag_engine(), &c->out_flags[(size_t)k], true, &c->epoch_word, false,
+                                 sizeof(uint32_t), &d, 1, nullptr, err),
                       "outbound copies submitted");
                 stream.wait(&c->out_flags[(size_t)k], c->epoch);
             }
@@ -476,7 +482,8 @@ void scenario_exchange(uint32_t seed) {
             j.epoch = c->epoch;
             j.per_sender = rng() % 2;
             j.start = start;
-            j.epoch_word = &c->epoch_word;
+            j.epoch_word = i % 2 ? c->epoch_row : &c->epoch_word;
+            j.epoch_words = i % 2 ? 64 : 1;
             j.status = status;
             j.deadline = Clock::now() + std::chrono::seconds(5);
             for (int k = 0; k < nin; ++k) {
@@ -618,6 +625,49 @@ void scenario_merge() {
     check(dst == src, "every range landed");
     for (int r = 0; r < n; ++r)
         check(landed[r] == 1, "every sender's landed flag");
+
+    // with an epoch row the landed flags of the merged copies are neighbouring words and go
+    // as one flag copy (on the inbound flag engine); a landed flag that is not the next word
+    // starts another flag copy
+    {
+        ep::Exchange y;
+        y.init_with(kGpu, kCpu, 1u, {2u}, 4, 3u, 4u);
+        std::vector<uint8_t> d2((size_t)(n * part), 0);
+        uint32_t row[64], lnd[n + 1] = {0, 0, 0, 0, 0};
+        for (uint32_t &w : row)
+            w = 5;
+        uint32_t rdy[n] = {5, 5, 5, 5};
+        int s2 = y.begin(1000 * 1000, err);
+        hsa_signal_t st2{};
+        check(s2 >= 0 && y.start_signal(s2, st2, err), "slot (epoch row)");
+        stream.release(ep::DmaEngines::value_pointer(st2));
+        y.arm(s2, st2);
+        const int64_t b2 = g_copies.load();
+        ep::InJob m;
+        m.epoch = 5;
+        m.per_sender = true;
+        m.start = st2;
+        m.epoch_word = row;
+        m.epoch_words = 64;
+        m.status = status;
+        m.deadline = Clock::now() + std::chrono::seconds(5);
+        // flags of senders 0, 1, 2 are words 0, 1, 2; sender 3's is word 4 (not the next word)
+        uint32_t *where[n] = {&lnd[0], &lnd[1], &lnd[2], &lnd[4]};
+        for (int r = 0; r < n; ++r) {
+            ep::InCopy c;
+            check(y.in_copy(s2, &rdy[r], reinterpret_cast<char *>(d2.data()) + r * part,
+                            reinterpret_cast<const char *>(src.data()) + r * part, part, where[r], c, err), "copy");
+            m.copies.push_back(c);
+            stream.wait(where[r], 5);
+        }
+        y.post(s2, std::move(m));
+        stream.finish();
+        check(g_copies.load() - b2 == 3, "one data copy, one flag copy for words 0-2, one for word 4");
+        check(d2 == src, "every range landed (epoch row)");
+        check(lnd[0] == 5 && lnd[1] == 5 && lnd[2] == 5 && lnd[3] == 0 && lnd[4] == 5,
+              "the landed flags and nothing between them");
+        y.release();
+    }
 
     // all-senders job: the eager copy goes while another sender is still out
     std::vector<uint8_t> own(4096, 9), own_dst(4096, 0), other(4096, 5), other_dst(4096, 0);

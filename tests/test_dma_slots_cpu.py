@@ -9,13 +9,17 @@ since, or when a dependency drops below 0 (an engine would then never start the 
 
 Cases:
 - lane: rounds of the default device->host leg with the chunk count changing between
-  rounds (signal roles shift), lanes created and released between batches;
+  rounds (signal roles shift), lanes created and released between batches, the chunk
+  flags on the data engine or on an engine of their own;
 - exchange: calls with outbound and inbound copies (courier, per-sender and all-senders
-  jobs), senders answering in random order, exchanges recreated between batches;
+  jobs), senders answering in random order, exchanges recreated between batches, the
+  flags on the data engines or on two flag engines, the landed flags of merged inbound
+  copies as one flag copy from an epoch row;
 - order: a later call's sender answers before an earlier call's; both calls finish
   without waiting for the bound (the courier serves jobs in call order);
 - merge: inbound copies contiguous in memory whose senders have answered go down as one
-  data copy with each sender's flag after it; a rank's own rows (an eager copy) go down
+  data copy with each sender's flag after it (one flag copy for flags in neighbouring
+  words when the job has an epoch row); a rank's own rows (an eager copy) go down
   before the other senders of an all-senders job answer; the pieces of a host-side result
   (eager copies whose flags the job's host work raises) go down as each is ready, without
   their flags holding back that host work;
