@@ -45,3 +45,23 @@ def test_a_failed_pinned_mode_is_recorded_and_the_others_run(monkeypatch):
     ok = r["modes"]["default"]
     assert "error" not in ok and ok["us_per_layer"] > 0
     assert "error" not in r["dense_allgather_reducescatter"]
+
+
+@pytest.mark.gpu
+def test_bench_runs_end_to_end_on_the_tiny_layer():
+    """The HBM-staged part of bench.py on the tiny layer in a process of its own: one JSON
+    line with the value, the roofline of the dispatch and combine kernels, and the same
+    steps replayed from a HIP graph."""
+    import json
+    import subprocess
+    print("[gpu] bench.py --workload tiny --no-pinned --no-cpu-baseline", flush=True)
+    r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--workload", "tiny", "--no-pinned",
+                        "--no-cpu-baseline", "--steps", "20", "--warmup", "3"], capture_output=True, text=True,
+                       timeout=240)
+    assert r.returncode == 0, r.stderr[-3000:]
+    d = json.loads(r.stdout.strip().splitlines()[-1])
+    assert d["value"] > 0 and d["n_gpus"] == 1 and d["config"]["T"] == 128
+    assert d["roofline"]["bound"] == "hbm" and d["roofline"]["frac"] > 0
+    g = d["graph_replayed_steps"]
+    assert "error" not in g, g
+    assert g["us_per_layer"] > 0 and g["steps"] >= 20
