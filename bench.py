@@ -315,6 +315,7 @@ def main():
             "launches_averaged": dk.get("launches"),
             "measured": dk.get("measured"),
             "dispatch_and_combine": pair_roofline(kernels),
+            "streaming_ceiling": ceiling_of(dominant, dk.get("hbm_frac"), ceilings, k),
         },
         "kernels": kernels,
         "hbm_copy_probe_GBps": round(copy_gbps, 1),
@@ -837,6 +838,19 @@ def pcie_peaks(dev) -> dict:
     if unsettled:
         res["earlier_unsettled_probes"] = unsettled
     return res
+
+
+def ceiling_of(kernel: str, frac, ceilings: dict, k: int) -> dict:
+    """What plain streaming code reaches for the kernel's traffic (the faster store policy):
+    the write-only stream for the dispatch kernels (89% or more of their bytes are writes at
+    top-8, 67% at top-2), the k:1 stream for the combine."""
+    names = ([f"combine_like_{k}_to_1", f"combine_like_{k}_to_1_write_through"] if kernel == "combine"
+             else ["write_only", "write_only_write_through"])
+    got = [(ceilings[n]["frac"], n) for n in names if isinstance(ceilings.get(n), dict)]
+    if not got or not frac:
+        return {"note": "no streaming probe at this row size"}
+    best, name = max(got)
+    return {"mix": name, "frac": best, "kernel_frac_of_ceiling": round(frac / best, 3)}
 
 
 def pair_roofline(kernels: dict) -> dict:
