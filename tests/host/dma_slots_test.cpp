@@ -146,10 +146,12 @@ private:
                     break;
             }
             if (!stuck) {
-                if (c.len == sizeof(uint32_t))  // flag words: one visible store
-                    __atomic_store_n(static_cast<uint32_t *>(c.dst), *static_cast<const volatile uint32_t *>(c.src),
-                                     __ATOMIC_RELEASE);
-                else {
+                if (c.len % sizeof(uint32_t) == 0 && c.len <= 64 * sizeof(uint32_t)) {
+                    // flag words (one, or a merged run of them): one visible store each
+                    for (size_t w = 0; w < c.len / sizeof(uint32_t); ++w)
+                        __atomic_store_n(static_cast<uint32_t *>(c.dst) + w,
+                                         static_cast<const volatile uint32_t *>(c.src)[w], __ATOMIC_RELEASE);
+                } else {
                     std::memcpy(c.dst, c.src, c.len);
                     __atomic_thread_fence(__ATOMIC_RELEASE);
                 }

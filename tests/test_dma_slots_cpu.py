@@ -94,3 +94,30 @@ def test_harness_catches_the_shared_signal_rule(binary):
     rc, out = run(binary, "old_rule", 1, timeout=60)
     assert rc == 1, out
     assert "decrement landed after the signal was reset" in out
+
+
+@pytest.fixture(scope="module")
+def tsan_binary(tmp_path_factory):
+    """The same harness built with ThreadSanitizer (host code only: g++, no GPU code)."""
+    gxx = shutil.which("g++")
+    if not gxx or not os.path.exists(os.path.join(ROCM_INCLUDE, "hsa", "hsa.h")):
+        pytest.skip("needs g++ and the ROCr headers")
+    out = str(tmp_path_factory.mktemp("dma_tsan") / "dma_slots_test_tsan")
+    cmd = [gxx, "-std=c++17", "-O1", "-g", "-fsanitize=thread", "-D__HIP_PLATFORM_AMD__", "-I", ROCM_INCLUDE,
+           "-I", os.path.join(ROOT, "include"), "-I", CSRC,
+           os.path.join(ROOT, "tests", "host", "dma_slots_test.cpp"), os.path.join(CSRC, "sdma_lane.cpp"),
+           "-o", out, "-lpthread"]
+    res = subprocess.run(cmd, capture_output=True, text=True)
+    if res.returncode != 0 and "tsan" in (res.stderr + res.stdout).lower():
+        pytest.skip("ThreadSanitizer runtime not available: " + res.stderr[-300:])
+    assert res.returncode == 0, res.stderr[-4000:]
+    return out
+
+
+@pytest.mark.parametrize("scenario", ["lane", "exchange", "order", "merge"])
+def test_lane_courier_and_slots_have_no_data_race(tsan_binary, scenario):
+    """The lane, the courier thread, the signal slots and the callers' threads share flags,
+    signals and job queues: ThreadSanitizer reports no data race in any scenario."""
+    rc, out = run(tsan_binary, scenario, 2, timeout=300)
+    assert "ThreadSanitizer" not in out, out[-4000:]
+    assert rc == 0 and "violations 0 checks_failed 0" in out, out[-2000:]
