@@ -26,6 +26,8 @@ Cases:
 - bounded: a slot with a signal that never retires is refused after its bound, with a
   message; a failed copy (negative value) is reported once; nothing is destroyed while a
   decrement may still come;
+- the lane, exchange, order and merge scenarios again, built with ThreadSanitizer: no data
+  race between the courier thread, the stand-in engines and the callers' threads;
 - old_rule: the reuse rule of the earlier revision (a completion signal shared by two
   copies, reset as soon as the flags are seen) replayed against the stand-in, which must
   report the late decrement: the harness does catch the failure mode.
