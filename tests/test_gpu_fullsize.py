@@ -130,12 +130,14 @@ def test_coarse_layer_as_the_benchmark_runs_it():
     st.close()
 
 
-@pytest.mark.parametrize("k,H,T", [(8, 7176, 18720), (2, 7168, 74900), (2, 7176, 74820)])
+@pytest.mark.parametrize("k,H,T", [(8, 7176, 18720), (16, 7168, 9400), (4, 4096, 65600), (2, 7168, 74900),
+                                   (2, 7176, 74820)])
 def test_write_through_pack_instances(k, H, T):
     """Pack launches that write 2 GiB or more use the write-through store instances: the
-    per-slot kernel with rows that are not whole 64-vector groups (H = 7176), and the
-    one-wave-per-chunk kernel (k = 2) with whole-group and with ragged rows.  Every packed
-    row is compared with the pack definition."""
+    per-slot kernel with rows that are not whole 64-vector groups (H = 7176), with 16-wave
+    workgroups (k = 16) and with 4-wave ones (k = 4), and the one-wave-per-chunk kernel
+    (k = 2) with whole-group and with ragged rows.  Every packed row is compared with the
+    pack definition."""
     E, R = 64, 8
     n = T * k
     assert n * 2 * H >= 2 << 30, "the case must write at least 2 GiB"
