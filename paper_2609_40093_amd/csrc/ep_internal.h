@@ -55,9 +55,8 @@ struct RowStore<true> {
 // each wave walks `rounds` rounds of 64 entries.  W = 16 while 16 rows of per-wave
 // counters fit in LDS (E <= 512), else 4.  One tile when it covers every entry in at most
 // 4 rounds (W = 16) or 8 rounds (W = 4): one kernel then does the whole layout.  Otherwise
-// as many tiles as keep the tile counts at most 16K words (the last workgroup of the
-// count kernel reads and rewrites them all) and at most 1024 tiles, with as few rounds as
-// that allows.  No tile waits for another, so the tile count is not tied to the device.
+// as many tiles as keep the tile counts at most 16K words (every workgroup of the rank
+// kernel reads them all) and at most 1024 tiles, with as few rounds as that allows.  No tile waits for another, so the tile count is not tied to the device.
 constexpr int kMaxExperts = 2048;
 constexpr int kLayoutRankCache = 8;  // rounds whose ids and in-wave ranks stay in registers
 struct LayoutGeom {
