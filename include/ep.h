@@ -103,9 +103,8 @@ ep_status ep_layout_workspace_bytes(int64_t num_tokens, int32_t topk, int32_t nu
  *   row_src         int32 [T*k] or NULL: inverse of slot_pos (row p came from slot row_src[p]).
  *   workspace       device scratch of ep_layout_workspace_bytes() bytes, zero-filled
  *                   before its first use (e.g. hipMemset) and otherwise left alone between
- *                   calls: it holds the partial counts of the tiles of the routing array,
- *                   a counter that every call leaves at 0, and the status read by
- *                   ep_layout_validate.  Calls that share a workspace must be ordered
+ *                   calls: it holds the partial counts of the tiles of the routing array
+ *                   and the status read by ep_layout_validate.  Calls that share a workspace must be ordered
  *                   (same stream or events).  No workgroup of a layout waits for another,
  *                   so a layout completes whatever else the device runs.
  * Requires T >= 0, T*k < 2^31, 1 <= k <= E <= EP_MAX_EXPERTS, R >= 1, E % R == 0.
@@ -158,8 +157,12 @@ ep_status ep_dispatch_layout_static(const int32_t *topk_idx, int64_t num_tokens,
  * Per buffer: HBM send (packed) and recv (returned rows) buffers of max_rows*H*2 bytes;
  * with PINNED_HOST also pinned host send/recv bounce buffers of the same size, one
  * uint32 send flag per chunk and one uint32 recv flag per sender in coherent pinned host
- * memory, all zero-initialised.  Creates two non-blocking DMA streams at default
- * priority: up (device->host) and down (host->device). */
+ * memory, all zero-initialised.  Creates two non-blocking streams at default priority,
+ * up (device->host) and down (host->device), and takes SDMA engines through ROCr: one for
+ * the device->host chunks and another for their flag copies (a flag copy waits for its
+ * chunk to land, and on the chunk's own engine that wait would hold up the chunks behind
+ * it).  With the environment variable EP_HOSTLEG_COPY=hip the device->host chunks and
+ * flags go through hipMemcpyAsync on the up stream instead. */
 ep_status ep_staging_alloc(ep_staging_kind kind, int64_t max_rows, int32_t hidden,
                            int32_t num_ranks, int32_t num_buffers, int64_t chunk_bytes,
                            ep_staging **out);
