@@ -44,17 +44,46 @@ MODES = [PS, DUP, DUP | PS, DUP | RO, DUP | RO | PS]
 @pytest.mark.parametrize("mode", MODES, ids=["per_sender", "duplex", "duplex_per_sender", "duplex_remote_only",
                                              "duplex_remote_only_per_sender"])
 def test_exchange_roundtrip_exact(mode):
-    T, H, E, k, R, me = 3000, 1024, 64, 4, 8, 2
-    case = make_case("exchange", T, H, E, k, R, "skewed", seed=21, gates="uniform")
+    R = 8
+    roundtrip(3000, 1024, 64, 4, R, 2, mode, case_seed=21, rng_seed=5, chunk_bytes=1 << 20,
+              inbound_us=[(r * 7919) % 3000 for r in range(R)], return_us=[(r * 104729) % 5000 for r in range(R)])
+
+
+@pytest.mark.parametrize("seed", range(12))
+def test_exchange_roundtrip_random_shapes(seed):
+    """Seeded random groups (2 to 16 ranks, any self rank), routings, row lengths, chunk
+    sizes and modes, with senders answering at once or staggered (so that inbound copies
+    of neighbouring senders merge, with their landed flags, or go one by one): the same
+    checks as above."""
+    rng = np.random.default_rng(1000 + seed)
+    R = int(rng.choice([2, 4, 8, 16]))
+    E = R * int(rng.choice([1, 2, 8]))
+    k = int(rng.choice([kk for kk in (1, 2, 4, 8) if kk <= E]))  # 1/k gates: exact sums
+    T = int(rng.integers(1, 2000))
+    H = int(rng.choice([512, 1024, 2048]))
+    me = int(rng.integers(0, R))
+    mode = MODES[int(rng.integers(0, len(MODES)))]
+    stagger = bool(rng.integers(0, 2))
+    inbound_us = [int(rng.integers(0, 3000)) if stagger else 0 for _ in range(R)]
+    return_us = [int(rng.integers(0, 3000)) if stagger else 0 for _ in range(R)]
+    chunk = int(rng.choice([64 << 10, 1 << 20]))
+    say(f"exchange random case {seed}: T={T} H={H} E={E} k={k} R={R} me={me} mode={mode} stagger={stagger}")
+    roundtrip(T, H, E, k, R, me, mode, case_seed=2000 + seed, rng_seed=seed, chunk_bytes=chunk,
+              inbound_us=inbound_us, return_us=return_us)
+
+
+def roundtrip(T, H, E, k, R, me, mode, case_seed, rng_seed, chunk_bytes, inbound_us, return_us):
+    """Three rounds on alternating buffer sets with identity experts: combine(dispatch(x))
+    == x exactly (fp32), every leg's bytes, the offsets and every flag checked."""
+    case = make_case("exchange", T, H, E, k, R, "skewed", seed=case_seed, gates="uniform")
     rows = T * k
     lay_o = oracle.layout(case.topk_idx, E, R)
     ro = lay_o.rank_offsets
-    st = ep.Staging("pinned", rows, H, R, num_buffers=2, chunk_bytes=1 << 20)
+    st = ep.Staging("pinned", rows, H, R, num_buffers=2, chunk_bytes=chunk_bytes)
     st.set_mode(mode, self_rank=me)
     peers = ep.SimPeers(st, echo=True)
-    peers.set_delays(inbound_us=[(r * 7919) % 3000 for r in range(R)],
-                     return_us=[(r * 104729) % 5000 for r in range(R)])
-    rng = np.random.default_rng(5)
+    peers.set_delays(inbound_us=inbound_us, return_us=return_us)
+    rng = np.random.default_rng(rng_seed)
     idx = torch.from_numpy(case.topk_idx).to(DEV)
     w = torch.from_numpy(case.topk_w).to(DEV)
     lay = ep.dispatch_layout(idx, E, R)
@@ -67,7 +96,11 @@ def test_exchange_roundtrip_exact(mode):
         packed = oracle.pack(xr, lay_o.slot_pos, k)
         inbound = None
         if mode & DUP:
-            rin = [int(rng.integers(0, 900)) for _ in range(R)]
+            # inbound rows of every sender, all of them within the staging's rows
+            cap = max(0, (rows - int(ro[me + 1] - ro[me])) // max(1, R - 1))
+            rin = [int(rng.integers(0, min(900, cap) + 1)) for _ in range(R)]
+            if rnd == 1:
+                rin[(me + 1) % R] = 0   # a sender with no rows for this rank
             rin[me] = 0
             st.set_inbound(buf, rin)
             full = list(rin)
