@@ -160,7 +160,9 @@ def dispatch_layout_local(topk_idx: torch.Tensor, num_experts: int, e_lo: int, e
     if out is None or (out.num_tokens, out.topk, out.num_experts, out.e_lo, out.e_hi) != (N, k, num_experts, e_lo,
                                                                                           e_hi):
         i32 = dict(dtype=torch.int32, device=dev)
-        ws = workspace_bytes(N, k, L) if 1 <= k <= L <= _lib.EP_MAX_EXPERTS else 256
+        # the window layout sorts all N*k entries over its L experts (k may exceed L: a token's
+        # experts span several windows), so its workspace is that of N*k entries of top-1
+        ws = workspace_bytes(N * k, 1, L) if N * k >= 1 and 1 <= L <= _lib.EP_MAX_EXPERTS else 256
         out = LocalLayout(N, k, num_experts, e_lo, e_hi, torch.empty(max(L, 1), **i32),
                           torch.empty(max(L, 0) + 1, **i32), torch.empty(N * k, **i32),
                           torch.empty(N * k, **i32) if with_row_src else None,

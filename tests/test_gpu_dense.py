@@ -36,9 +36,10 @@ def bits_dev(a):
 
 
 @pytest.mark.parametrize("N,E,k,window", [(4096, 16, 4, (4, 8)), (3000, 64, 8, (0, 8)), (20000, 256, 8, (224, 256)),
-                                          (700, 2048, 4, (1000, 1700)), (5, 8, 2, (7, 8)), (0, 8, 2, (0, 2))],
+                                          (700, 2048, 4, (1000, 1700)), (5, 8, 2, (7, 8)), (0, 8, 2, (0, 2)),
+                                          (6000, 64, 8, (16, 20)), (2000, 4, 4, (2, 3))],
                          ids=["coarse_window", "first_window", "many_tiles_last_window", "wide_window",
-                              "tiny", "empty"])
+                              "tiny", "empty", "topk_above_window_many_tiles", "one_expert_window"])
 def test_window_layout_pack_partials(N, E, k, window):
     e_lo, e_hi = window
     say(f"window layout N={N} E={E} k={k} [{e_lo},{e_hi})")
@@ -175,6 +176,26 @@ def test_dense_layer_exact_f32_blocks(per_sender, on_host):
         rs = oracle.pcie_volume("reduce_scatter", "cpu" if on_host else "gpu", R, Sb)
         assert res["ag_bytes"] == (ag["up"], ag["down"])
         assert res["rs_bytes"] == (rs["up"], rs["down"])
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_dense_layer_random_groups_exact(seed):
+    """Seeded random groups (2 to 8 ranks, any self rank, either waiting policy and either
+    reduction placement, token counts and row lengths): with fp32 blocks and identity
+    experts the layer returns the rank's own shard exactly, the All-Gather every shard."""
+    rng = np.random.default_rng(3000 + seed)
+    R = int(rng.choice([2, 4, 8]))
+    me = int(rng.integers(0, R))
+    E = R * int(rng.choice([1, 2, 4]))
+    k = int(rng.choice([kk for kk in (1, 2, 4) if kk <= E]))
+    T = int(rng.integers(1, 1500))
+    H = int(rng.choice([256, 512, 1024]))
+    per_sender, on_host = bool(rng.integers(0, 2)), bool(rng.integers(0, 2))
+    say(f"dense random group {seed}: R={R} me={me} E={E} k={k} T={T} H={H} per_sender={per_sender} host={on_host}")
+    for res in run_dense_layer(R, me, T, H, E, k, torch.float32, per_sender, on_host, seed=seed):
+        assert np.array_equal(res["gathered"], np.concatenate(res["shards"])), "All-Gather rows differ"
+        xf = (res["shards"][me].astype(np.uint32) << 16).view(np.float32)
+        assert np.array_equal(res["out"], xf), "Reduce-Scatter of identity experts != own shard"
 
 
 @pytest.mark.parametrize("on_host", [False, True], ids=["gpu_reduce", "host_reduce"])
