@@ -253,6 +253,57 @@ def test_accumulate_equals_single_reduction(mode, arrival):
     st.close()
 
 
+@pytest.mark.parametrize("seed", range(8))
+def test_accumulate_random_shapes(seed):
+    """Seeded random groups, routings, row lengths (any multiple of 8 elements), top-k and
+    arrival delays through the accumulation as senders land: the output equals the single
+    reduction of the same landed rows bit for bit, and the oracle within tolerance."""
+    rng = np.random.default_rng(5000 + seed)
+    R = int(rng.choice([2, 4, 8, 16]))
+    E = R * int(rng.choice([1, 2, 8]))
+    k = int(rng.integers(1, min(8, E) + 1))
+    T = int(rng.integers(1, 1500))
+    H = int(rng.choice([8, 264, 512, 1032, 2048]))
+    me = int(rng.integers(0, R))
+    mode = [PS | ACC, DUP | PS | ACC, DUP | RO | PS | ACC][int(rng.integers(0, 3))]
+    delays = [int(rng.integers(0, 20_000)) for _ in range(R)]
+    say(f"accumulate random case {seed}: T={T} H={H} E={E} k={k} R={R} me={me} mode={mode}")
+    case = make_case("accumulate_random", T, H, E, k, R, "random", seed=6000 + seed)
+    rows = T * k
+    lay_o = oracle.layout(case.topk_idx, E, R)
+    ro = lay_o.rank_offsets
+    st = ep.Staging("pinned", rows, H, R, num_buffers=2, chunk_bytes=1 << 20)
+    st.set_mode(mode, self_rank=me)
+    peers = ep.SimPeers(st, echo=True)
+    peers.set_delays(inbound_us=[0] * R, return_us=delays)
+    idx = torch.from_numpy(case.topk_idx).to(DEV)
+    w = torch.from_numpy(case.topk_w).to(DEV)
+    lay = ep.dispatch_layout(idx, E, R)
+    for rnd in range(2):
+        buf, epoch = rnd % 2, 70 + rnd
+        xr = case.x ^ np.uint16(rnd + 1)
+        if mode & DUP:
+            cap = max(0, (rows - int(ro[me + 1] - ro[me])) // max(1, R - 1))
+            rin = [int(rng.integers(0, min(300, cap) + 1)) for _ in range(R)]
+            rin[me] = 0
+            st.set_inbound(buf, rin)
+            n_in = sum(rin) + int(ro[me + 1] - ro[me])
+            st.host_array("in", buf)[:n_in] = synth.normal_bf16_rows(np.random.SeedSequence([19, seed, rnd]), n_in, H)
+        peers.post(buf, epoch, rows)
+        ep.dispatch(bits(xr), lay.slot_pos, st, topk=k, buf=buf, epoch=epoch, rank_offsets=lay.rank_offsets)
+        out = ep.combine(st, lay.slot_pos, w, buf=buf, epoch=epoch, rank_offsets=lay.rank_offsets)
+        st.status()
+        peers.drain()
+        ref = torch.empty_like(out)
+        ep.combine_rows(st.read_device("recv", rows, buf), lay.slot_pos, w, ref)
+        assert torch.equal(out.view(torch.int16), ref.view(torch.int16)), "accumulated combine != single reduction"
+        exact, _, _ = oracle.combine(oracle.pack(xr, lay_o.slot_pos, k), lay_o.slot_pos, case.topk_w)
+        err = np.abs(out.float().cpu().numpy().astype(np.float64) - exact)
+        assert err.max() <= 2e-2 and err.mean() <= 2e-3
+    peers.close()
+    st.close()
+
+
 def test_accumulate_reduces_before_a_late_sender_lands():
     """Sender 1 is held back 0.6 s.  Meanwhile every token none of whose rows comes from it
     is already final in the output (read from another stream while the combine still waits),

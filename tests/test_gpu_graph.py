@@ -73,6 +73,35 @@ def test_graph_rounds_eager():
     st.close()
 
 
+@pytest.mark.parametrize("seed", range(6))
+def test_graph_rounds_eager_random_shapes(seed):
+    """Seeded random layers through the graph-round path (rows of any multiple of 8
+    elements, so also the guarded pack and combine instances; 2 to 8 ranks; top-1 to top-8
+    with 1/k gates): three eager rounds, each returning x exactly, with the pinned send
+    rows equal to the oracle's pack."""
+    rng = np.random.default_rng(4000 + seed)
+    R = int(rng.choice([2, 4, 8]))
+    E = R * int(rng.choice([1, 2, 8]))
+    k = int(rng.choice([kk for kk in (1, 2, 4, 8) if kk <= E]))
+    T = int(rng.integers(1, 600))
+    H = int(rng.choice([8, 520, 1024, 1032, 7168]))
+    say(f"graph rounds random case {seed}: T={T} H={H} E={E} k={k} R={R}")
+    case, st, peers, idx, w, x, out, lay = setup(T=T, H=H, E=E, k=k, R=R, seed=100 + seed)
+    packed_slots = oracle.layout(case.topk_idx, case.E, case.R).slot_pos
+    for r in range(1, 4):
+        xr = payload(case, r)
+        x.copy_(torch.from_numpy(xr.view(np.int16)))
+        one_round(st, idx, w, x, out, lay, case)
+        torch.cuda.synchronize()
+        peers.wait_round(r)
+        st.status()
+        assert np.array_equal(out.cpu().numpy(), as_f32(xr)), f"round {r}"
+        sent = st.host_array("send", r % 2)[:case.slots]
+        assert np.array_equal(sent, oracle.pack(xr, packed_slots, case.k)), f"pinned send rows of round {r}"
+    peers.close()
+    st.close()
+
+
 def test_graph_capture_replay():
     case, st, peers, idx, w, x, out, lay = setup(seed=32)
     # one eager round first (the layout's device state, kernels loaded)
