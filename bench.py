@@ -30,6 +30,7 @@ METRIC = "dispatch & combine GB/s token payload (μs/MoE layer) + % HBM/PCIe roo
 HBM_PEAK_GBPS = 8000.0      # MI355X HBM3E
 PCIE_PEAK_GBPS = 64.0       # PCIe Gen5 x16, per direction
 MALL_BYTES = 256 << 20
+SPIN_CYCLES = 240_000       # a device spin of about 100 us at 2.4 GHz (torch.cuda._sleep)
 _T0 = time.perf_counter()
 
 
@@ -167,16 +168,17 @@ def main():
     step(args.warmup)
     torch.cuda.synchronize()
     probe_us = (time.perf_counter() - probe0) * 1e6
-    # Events cost the stream ~2 us per traced launch: on layers of a few hundred us or
-    # more, every kernel of every timed step carries them (< 1% of the step); on shorter
-    # layers one step in eight does, alternating between the dispatch and the combine.
+    # A launch bracketed by timing events costs the stream about 2 us and the host 10-25 us
+    # (binding the start event to the kernel).  On layers of a few hundred us or more every
+    # kernel of every timed step carries them (< 1% of the step, and the host stays far
+    # ahead of the device); shorter layers would become bound by that host time, so their
+    # timed steps run without events and the kernel averages come from the breakdown pass.
     every = probe_us > 300.0
-    cadence = ("both",) if every else ("dispatch", None, None, None, "combine", None, None, None)
     ep.trace_reset()
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for i in range(args.steps):
-        step(args.warmup + i, trace=cadence[i % len(cadence)])
+        step(args.warmup + i, trace="both" if every else None)
     t_issue = time.perf_counter()
     torch.cuda.synchronize()
     t1 = time.perf_counter()
@@ -198,11 +200,17 @@ def main():
             step((args.warmup + i) * nsets)
         torch.cuda.synchronize()
         warm = (time.perf_counter() - w0) * 1e3 / args.steps
-    # breakdown pass (not timed): every kernel of at least 50 steps bracketed by events
+    # breakdown pass (not timed): every kernel of at least 50 steps bracketed by events.
+    # On short layers the host, at 10-25 us per launch with events, falls behind the
+    # device, whose kernels would then start on an idle queue (measured longer than the same
+    # kernels behind queued work); a spin of the device (~100 us) queued ahead of each step
+    # keeps its kernels behind queued work, as in the timed steps.
     breakdown_steps = max(args.steps, 50)
     ep.trace_reset()
     ep.trace_enable(True)
     for i in range(breakdown_steps):
+        if not every:
+            torch.cuda._sleep(SPIN_CYCLES)
         step(args.warmup + args.steps + i)
     torch.cuda.synchronize()
     ep.trace_enable(False)
@@ -214,9 +222,8 @@ def main():
     # issue time show their kernel-bound time
     graph = graph_replayed_steps(step, nsets, max(2, -(-args.steps // nsets)), payload)
     progress("graph-replayed steps done")
-    # the roofline's launch averages come from the timed region (every launch of it on long
-    # layers; one step in eight on short ones, where events on every launch would stretch
-    # the kernels they bracket); other kernels from the breakdown pass
+    # the roofline's launch averages come from the timed region on long layers (every launch
+    # of it), from the breakdown pass on short ones; other kernels from the breakdown pass
     kstats = dict(timed_stats)
     for name, st_ in breakdown.items():
         kstats.setdefault(name, st_)
@@ -250,8 +257,9 @@ def main():
         entry = {"launches": st["count"], "avg_us": round(us, 3),
                  "p10_us": round(st["p10_ms"] * 1e3, 3), "p50_us": round(st["p50_ms"] * 1e3, 3),
                  "p90_us": round(st["p90_ms"] * 1e3, 3),
-                 "measured": ("timed region, every launch" if every else "timed region, one step in eight")
-                 if name in timed_stats else "breakdown pass"}
+                 "measured": "timed region, every launch" if name in timed_stats else
+                 ("breakdown pass, every launch" if every else
+                  "breakdown pass, every launch (the timed steps of layers under 300 us run without events)")}
         if name in abytes and us > 0:
             entry["algorithmic_bytes"] = abytes[name]
             entry["GBps"] = round(abytes[name] / (us * 1e-6) / 1e9, 1)
