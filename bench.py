@@ -168,17 +168,18 @@ def main():
     step(args.warmup)
     torch.cuda.synchronize()
     probe_us = (time.perf_counter() - probe0) * 1e6
-    # A launch bracketed by timing events costs the stream about 2 us and the host 10-25 us
-    # (binding the start event to the kernel).  On layers of a few hundred us or more every
-    # kernel of every timed step carries them (< 1% of the step, and the host stays far
-    # ahead of the device); shorter layers would become bound by that host time, so their
-    # timed steps run without events and the kernel averages come from the breakdown pass.
+    # A launch bracketed by timing events costs the stream about 4 us and the host 10-25 us
+    # (binding the start event to the kernel).  On layers of a few hundred us or more the
+    # timed steps carry them, the dispatch's kernels on one step and the combine's on the
+    # next (about 0.4% of the step; the host stays far ahead of the device); shorter layers
+    # would become bound by that host time, so their timed steps run without events and the
+    # kernel averages come from the breakdown pass.
     every = probe_us > 300.0
     ep.trace_reset()
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for i in range(args.steps):
-        step(args.warmup + i, trace="both" if every else None)
+        step(args.warmup + i, trace=("dispatch", "combine")[i % 2] if every else None)
     t_issue = time.perf_counter()
     torch.cuda.synchronize()
     t1 = time.perf_counter()
@@ -222,8 +223,9 @@ def main():
     # issue time show their kernel-bound time
     graph = graph_replayed_steps(step, nsets, max(2, -(-args.steps // nsets)), payload)
     progress("graph-replayed steps done")
-    # the roofline's launch averages come from the timed region on long layers (every launch
-    # of it), from the breakdown pass on short ones; other kernels from the breakdown pass
+    # the roofline's launch averages come from the timed region on long layers (the traced
+    # launches of it), from the breakdown pass on short ones; other kernels from the
+    # breakdown pass
     kstats = dict(timed_stats)
     for name, st_ in breakdown.items():
         kstats.setdefault(name, st_)
@@ -257,7 +259,8 @@ def main():
         entry = {"launches": st["count"], "avg_us": round(us, 3),
                  "p10_us": round(st["p10_ms"] * 1e3, 3), "p50_us": round(st["p50_ms"] * 1e3, 3),
                  "p90_us": round(st["p90_ms"] * 1e3, 3),
-                 "measured": "timed region, every launch" if name in timed_stats else
+                 "measured": "timed region, every other step (dispatch and combine alternate)"
+                 if name in timed_stats else
                  ("breakdown pass, every launch" if every else
                   "breakdown pass, every launch (the timed steps of layers under 300 us run without events)")}
         if name in abytes and us > 0:
