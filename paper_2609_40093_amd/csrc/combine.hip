@@ -16,7 +16,12 @@
 // unchanged (signs of zero included) -- a branch around it would let the compiler sink
 // the slot's loads into the branch and serialize them behind the previous slot's.  In
 // EXACT instances (rows a whole number of chunks) no lane carries a bounds mask either.
-// Rows are read once: loads and stores are non-temporal.
+// Rows are read once: loads are non-temporal.  Stores are device-scope write-through
+// buffer stores when the output is under 128 MiB and non-temporal from there up (RowStore):
+// measured on MI355X with inputs outside the memory-side cache, write-through stores made
+// the combine 2-7% faster up to 112 MiB of output (top-8 of 14 KiB rows, 2K-8K tokens;
+// 4 KiB rows, 8K tokens; top-2 of 8 KiB rows, 4K tokens) and 0.5-2% slower from 128 MiB
+// up (top-2, 16K tokens of 8 KiB rows; 16K and 32K tokens of 14 KiB rows).
 #include "ep_internal.h"
 
 namespace ep {
@@ -36,7 +41,7 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
 // FIXED_K: k == KC (one batch of slots, its bounds known at compile time).  SEL: the
 // receive buffer is chosen by a round counter in device memory (graph-replayed rounds);
 // without it the kernel loads nothing before the slot positions.
-template <int U, int KC, bool F32_OUT, bool EXACT, bool FIXED_K, bool SEL>
+template <int U, int KC, bool F32_OUT, bool EXACT, bool FIXED_K, bool SEL, bool WT>
 __global__ __launch_bounds__(256) void combine_kernel(const u32x4 *__restrict__ recv,
                                                       const int32_t *__restrict__ slot_pos,
                                                       const float *__restrict__ topk_w, int64_t T,
@@ -101,24 +106,25 @@ __global__ __launch_bounds__(256) void combine_kernel(const u32x4 *__restrict__ 
                 }
     }
 
+    // the token's output row: V 16-byte vectors (bf16) or 2V (fp32)
+    constexpr int kVecs = F32_OUT ? 2 : 1;
+    const RowStore<WT> dst((u32x4 *)out + t * V * kVecs, (uint32_t)V * kVecs * 16u);
 #pragma unroll
     for (int u = 0; u < U; ++u) {
         const int32_t v = v0 + u * kWave + lane;
         if (!EXACT && v >= V)
             continue;
-        const int64_t o = t * V + v;
         if constexpr (F32_OUT) {
-            u32x4 *dst = (u32x4 *)out + 2 * o;
             const u32x4 a = {__float_as_uint(acc[u][0]), __float_as_uint(acc[u][1]),
                              __float_as_uint(acc[u][2]), __float_as_uint(acc[u][3])};
             const u32x4 b = {__float_as_uint(acc[u][4]), __float_as_uint(acc[u][5]),
                              __float_as_uint(acc[u][6]), __float_as_uint(acc[u][7])};
-            __builtin_nontemporal_store(a, dst);
-            __builtin_nontemporal_store(b, dst + 1);
+            dst.put(a, 2u * (uint32_t)v);
+            dst.put(b, 2u * (uint32_t)v + 1u);
         } else {
             const u32x4 r = {pack_bf16x2(acc[u][0], acc[u][1]), pack_bf16x2(acc[u][2], acc[u][3]),
                              pack_bf16x2(acc[u][4], acc[u][5]), pack_bf16x2(acc[u][6], acc[u][7])};
-            __builtin_nontemporal_store(r, (u32x4 *)out + o);
+            dst.put(r, (uint32_t)v);
         }
     }
 }
@@ -127,6 +133,32 @@ __global__ __launch_bounds__(256) void combine_kernel(const u32x4 *__restrict__ 
 __global__ __launch_bounds__(256) void zero_fill_kernel(u32x4 *__restrict__ out, int64_t n) {
     for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n; i += (int64_t)gridDim.x * 256)
         out[i] = u32x4{0u, 0u, 0u, 0u};
+}
+
+constexpr int64_t kCombineWriteThroughBelow = 128ll << 20;  // output bytes
+
+template <int U, int KC, bool WT>
+void launch_ukw(dim3 grid, dim3 block, hipStream_t stream, TraceSlot ts, const u32x4 *rv, const int32_t *slot_pos,
+                const float *topk_w, int64_t T, int32_t V, int32_t chunks, int32_t k, void *out, bool out_f32,
+                bool exact, int64_t max_rows, RoundSel sel) {
+#define EP_COMBINE_ARGS grid, block, 0, stream, ts.start, ts.stop, 0, rv, slot_pos, topk_w, T, V, chunks, k, out, max_rows, sel
+#define EP_COMBINE_LAUNCH(F32, EX)                                                                      \
+    (k == KC ? hipExtLaunchKernelGGL((combine_kernel<U, KC, F32, EX, true, false, WT>), EP_COMBINE_ARGS) \
+             : hipExtLaunchKernelGGL((combine_kernel<U, KC, F32, EX, false, false, WT>), EP_COMBINE_ARGS))
+    if (sel.round && out_f32)  // graph-replayed rounds: the general instance reading the round
+        hipExtLaunchKernelGGL((combine_kernel<U, KC, true, false, false, true, WT>), EP_COMBINE_ARGS);
+    else if (sel.round)
+        hipExtLaunchKernelGGL((combine_kernel<U, KC, false, false, false, true, WT>), EP_COMBINE_ARGS);
+    else if (out_f32 && exact)
+        EP_COMBINE_LAUNCH(true, true);
+    else if (out_f32)
+        EP_COMBINE_LAUNCH(true, false);
+    else if (exact)
+        EP_COMBINE_LAUNCH(false, true);
+    else
+        EP_COMBINE_LAUNCH(false, false);
+#undef EP_COMBINE_LAUNCH
+#undef EP_COMBINE_ARGS
 }
 
 template <int U, int KC>
@@ -144,24 +176,13 @@ hipError_t launch_uk(const void *recv, const int32_t *slot_pos, const float *top
     const u32x4 *rv = static_cast<const u32x4 *>(recv);
     (void)hipGetLastError();  // drop an error left by an earlier, already reported call
     TraceSlot ts = trace_acquire();
-#define EP_COMBINE_ARGS grid, block, 0, stream, ts.start, ts.stop, 0, rv, slot_pos, topk_w, T, V, chunks, k, out, max_rows, sel
-#define EP_COMBINE_LAUNCH(F32, EX)                                                             \
-    (k == KC ? hipExtLaunchKernelGGL((combine_kernel<U, KC, F32, EX, true, false>), EP_COMBINE_ARGS) \
-             : hipExtLaunchKernelGGL((combine_kernel<U, KC, F32, EX, false, false>), EP_COMBINE_ARGS))
-    if (sel.round && out_f32)  // graph-replayed rounds: the general instance reading the round
-        hipExtLaunchKernelGGL((combine_kernel<U, KC, true, false, false, true>), EP_COMBINE_ARGS);
-    else if (sel.round)
-        hipExtLaunchKernelGGL((combine_kernel<U, KC, false, false, false, true>), EP_COMBINE_ARGS);
-    else if (out_f32 && exact)
-        EP_COMBINE_LAUNCH(true, true);
-    else if (out_f32)
-        EP_COMBINE_LAUNCH(true, false);
-    else if (exact)
-        EP_COMBINE_LAUNCH(false, true);
+    const bool wt = T * (int64_t)V * 16 * (out_f32 ? 2 : 1) < kCombineWriteThroughBelow;
+    if (wt)
+        launch_ukw<U, KC, true>(grid, block, stream, ts, rv, slot_pos, topk_w, T, V, chunks, k, out, out_f32, exact,
+                                max_rows, sel);
     else
-        EP_COMBINE_LAUNCH(false, false);
-#undef EP_COMBINE_LAUNCH
-#undef EP_COMBINE_ARGS
+        launch_ukw<U, KC, false>(grid, block, stream, ts, rv, slot_pos, topk_w, T, V, chunks, k, out, out_f32, exact,
+                                 max_rows, sel);
     hipError_t err = hipGetLastError();
     if (err == hipSuccess)
         trace_submit("combine", ts);

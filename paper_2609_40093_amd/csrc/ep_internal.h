@@ -17,16 +17,18 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int kWave = 64;
 
-// Stores of one packed row (the dispatch's write stream) from a wave-uniform base, under
-// one of two policies picked by the bytes a launch writes (measured on MI355X, rows of 4 and
-// 14 KiB, inputs rotated past the memory-side cache):
-//   WT = false: non-temporal stores -- faster below 2 GiB per launch (up to 20% at 0.1-1 GiB);
+// Stores of one row (a packed row of the dispatch, an output row of the combine) from a
+// wave-uniform base, under one of two policies that each kernel picks by the bytes a launch
+// writes (measured on MI355X, inputs rotated past the memory-side cache):
+//   WT = false: non-temporal stores;
 //   WT = true:  16-byte buffer stores at device scope (sc1: written through the XCD's L2
-//               rather than held there dirty) -- 1.5-2.5% faster from 2 GiB up, where the
-//               non-temporal rate falls with the size of the stream.
+//               rather than held there dirty).
+// The pack (rows of 4 and 14 KiB) writes through from 2 GiB per launch up, where the
+// non-temporal rate falls with the size of the stream (1.5-2.5% faster; non-temporal is up
+// to 20% faster at 0.1-1 GiB).  The combine's thresholds are beside it.
 // The buffer range of a write-through row is the `bytes` from `base` on: a store past it is
 // dropped by the hardware.
-constexpr int64_t kWriteThroughBytes = 2ll << 30;
+constexpr int64_t kWriteThroughBytes = 2ll << 30;  // the pack's
 template <bool WT>
 struct RowStore;
 template <>
