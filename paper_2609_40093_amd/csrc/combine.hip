@@ -17,7 +17,8 @@
 // the slot's loads into the branch and serialize them behind the previous slot's.  In
 // EXACT instances (rows a whole number of chunks) no lane carries a bounds mask either.
 // Rows are read once: loads are non-temporal.  Stores are device-scope write-through
-// buffer stores when the output is under 128 MiB and non-temporal from there up (RowStore):
+// buffer stores when the output is under 128 MiB and non-temporal from there up (RowStore),
+// where the call runs as launches of about 64 MiB of output each (see the launcher):
 // measured on MI355X with inputs outside the memory-side cache, write-through stores made
 // the combine 2-7% faster up to 112 MiB of output (top-8 of 14 KiB rows, 2K-8K tokens;
 // 4 KiB rows, 8K tokens; top-2 of 8 KiB rows, 4K tokens) and 0.5-2% slower from 128 MiB
@@ -136,6 +137,14 @@ __global__ __launch_bounds__(256) void zero_fill_kernel(u32x4 *__restrict__ out,
 }
 
 constexpr int64_t kCombineWriteThroughBelow = 128ll << 20;  // output bytes
+// From 128 MiB of output up the combine runs as several launches over consecutive token
+// ranges of about 64 MiB of output each (measured on MI355X, top-8 of 14 KiB rows, 32K
+// tokens, non-temporal stores: one launch 747 us, 2 / 4 / 8 / 16 / 32 / 64 launches 733 /
+// 727 / 718 / 719 / 748 / 801 us, and the layer's pack after it unchanged; the
+// write-through stores of the smaller outputs made the following pack slower when applied
+// to such launches).
+constexpr int64_t kCombineSplitAbove = 128ll << 20;
+constexpr int64_t kCombineLaunchBytes = 64ll << 20;
 
 template <int U, int KC, bool WT>
 void launch_ukw(dim3 grid, dim3 block, hipStream_t stream, TraceSlot ts, const u32x4 *rv, const int32_t *slot_pos,
@@ -166,23 +175,39 @@ hipError_t launch_uk(const void *recv, const int32_t *slot_pos, const float *top
                      int32_t V, int32_t k, void *out, bool out_f32, int64_t max_rows,
                      hipStream_t stream, RoundSel sel) {
     const int32_t chunks = (V + U * kWave - 1) / (U * kWave);
-    const int64_t items = T * chunks;
     const int waves_per_block = 4;
-    const int64_t blocks = (items + waves_per_block - 1) / waves_per_block;
-    if (blocks > INT32_MAX)
+    const int64_t row_bytes = (int64_t)V * 16 * (out_f32 ? 2 : 1);  // one output row
+    const int64_t out_bytes = T * row_bytes;
+    // token ranges of the launches: one below kCombineSplitAbove bytes of output, else
+    // about kCombineLaunchBytes each
+    const int64_t launches = out_bytes < kCombineSplitAbove
+                                 ? 1
+                                 : std::min<int64_t>(T, (out_bytes + kCombineLaunchBytes - 1) / kCombineLaunchBytes);
+    const int64_t per = (T + launches - 1) / launches;
+    if ((per * chunks + waves_per_block - 1) / waves_per_block > INT32_MAX)
         return hipErrorInvalidValue;
     const bool exact = V % (U * kWave) == 0;
-    const dim3 grid((unsigned)blocks), block(waves_per_block * kWave);
+    const dim3 block(waves_per_block * kWave);
     const u32x4 *rv = static_cast<const u32x4 *>(recv);
     (void)hipGetLastError();  // drop an error left by an earlier, already reported call
-    TraceSlot ts = trace_acquire();
-    const bool wt = T * (int64_t)V * 16 * (out_f32 ? 2 : 1) < kCombineWriteThroughBelow;
-    if (wt)
-        launch_ukw<U, KC, true>(grid, block, stream, ts, rv, slot_pos, topk_w, T, V, chunks, k, out, out_f32, exact,
-                                max_rows, sel);
-    else
-        launch_ukw<U, KC, false>(grid, block, stream, ts, rv, slot_pos, topk_w, T, V, chunks, k, out, out_f32, exact,
-                                 max_rows, sel);
+    const TraceSlot ts = trace_acquire();  // one pair of events around every launch of the call
+    const bool wt = out_bytes < kCombineWriteThroughBelow;
+    for (int64_t t0 = 0; t0 < T; t0 += per) {
+        const int64_t n = std::min(per, T - t0);
+        const dim3 grid((unsigned)((n * chunks + waves_per_block - 1) / waves_per_block));
+        TraceSlot part;
+        part.start = t0 == 0 ? ts.start : nullptr;
+        part.stop = t0 + n == T ? ts.stop : nullptr;
+        const int32_t *sp = slot_pos + t0 * k;
+        const float *gw = topk_w + t0 * k;
+        void *o = static_cast<char *>(out) + t0 * row_bytes;
+        if (wt)
+            launch_ukw<U, KC, true>(grid, block, stream, part, rv, sp, gw, n, V, chunks, k, o, out_f32, exact,
+                                    max_rows, sel);
+        else
+            launch_ukw<U, KC, false>(grid, block, stream, part, rv, sp, gw, n, V, chunks, k, o, out_f32, exact,
+                                     max_rows, sel);
+    }
     hipError_t err = hipGetLastError();
     if (err == hipSuccess)
         trace_submit("combine", ts);
