@@ -852,11 +852,11 @@ def pcie_peaks(dev) -> dict:
 
 
 def ceiling_of(kernel: str, frac, ceilings: dict, k: int) -> dict:
-    """What plain streaming code reaches for the kernel's traffic (the faster store policy):
+    """What plain streaming code reaches for the kernel's traffic (the fastest store policy):
     the write-only stream for the dispatch kernels (89% or more of their bytes are writes at
     top-8, 67% at top-2), the k:1 stream for the combine."""
-    names = ([f"combine_like_{k}_to_1", f"combine_like_{k}_to_1_write_through"] if kernel == "combine"
-             else ["write_only", "write_only_write_through"])
+    base = f"combine_like_{k}_to_1" if kernel == "combine" else "write_only"
+    names = [base, base + "_write_through", base + "_write_through_nt"]
     got = [(ceilings[n]["frac"], n) for n in names if isinstance(ceilings.get(n), dict)]
     if not got or not frac:
         return {"note": "no streaming probe at this row size"}
@@ -925,14 +925,14 @@ def streaming_ceilings(cfg, dev, launches: int = 10) -> dict:
              "copy_1_to_1": (rows // 2, 1, 1), "read_only": (rows, 1, 0), "write_only": (rows, 0, 1)}
     runs = []
     for name, (units, r, w) in mixes.items():
-        runs.append((name, units, r, w, False))
-        if w:  # the same mix with the pack's other store policy
-            runs.append((name + "_write_through", units, r, w, True))
+        runs.append((name, units, r, w, 0))
+        if w:  # the same mix with the path's other store policies
+            runs += [(name + "_write_through", units, r, w, 1), (name + "_write_through_nt", units, r, w, 2)]
     res = {}
-    for name, units, r, w, wt in runs:
+    for name, units, r, w, pol in runs:
         def launch(j):
             off = (j % nsets) * set_bytes
-            ep.stream_probe(dst[off:], src[off:], units, row, r, w, write_through=wt)
+            ep.stream_probe(dst[off:], src[off:], units, row, r, w, store_policy=pol)
         for j in range(2):
             launch(j)
         torch.cuda.synchronize()
@@ -952,7 +952,8 @@ def streaming_ceilings(cfg, dev, launches: int = 10) -> dict:
                      "frac": round(gbps / HBM_PEAK_GBPS, 4)}
     del src, dst
     res["note"] = ("ep_stream_probe over sequential addresses, 16-byte vectors, one wave per unit, non-temporal "
-                   "stores (names ending _write_through: device-scope write-through stores); buffer sets rotated "
+                   "stores (names ending _write_through: device-scope write-through buffer stores; _write_through_nt: "
+                   "the same with the non-temporal hint); buffer sets rotated "
                    "past the 256 MB memory-side cache")
     return res
 

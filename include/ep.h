@@ -470,11 +470,12 @@ ep_status ep_copy_probe(void *dst_dev, const void *src_dev, size_t bytes, hipStr
  * read-only, 0:1 write-only: what plain streaming code attains, beside which the path's
  * kernels are judged.  row_bytes = 1024 * g, g in {1, 2, 4, 8, 14, 16}; reads, writes in
  * 0..64, not both 0.  src: units*reads*row_bytes bytes (may be NULL when reads == 0);
- * dst: units*writes*row_bytes bytes, or 1 KiB when writes == 0.  write_through = 0 stores
- * with non-temporal 16-byte stores, 1 with device-scope write-through buffer stores (the
- * pack's two store policies).  Traced as "stream_probe". */
+ * dst: units*writes*row_bytes bytes, or 1 KiB when writes == 0.  store_policy (the path's
+ * three): 0 non-temporal 16-byte stores, 1 device-scope write-through buffer stores (the
+ * combine below 128 MiB of output), 2 the same with the non-temporal hint (the pack from
+ * 2 GiB per launch); any other value is EP_ERR_INVALID_ARG.  Traced as "stream_probe". */
 ep_status ep_stream_probe(void *dst_dev, const void *src_dev, int64_t units, int32_t row_bytes, int32_t reads,
-                          int32_t writes, int32_t write_through, hipStream_t stream);
+                          int32_t writes, int32_t store_policy, hipStream_t stream);
 
 /* PCIe probe on the SDMA engines the exchange uses: `dirs` bit 0 moves `bytes`
  * device->host (dev -> host), bit 1 host->device (host + bytes -> dev + bytes), both

@@ -606,15 +606,15 @@ def copy_probe(dst: torch.Tensor, src: torch.Tensor, stream=None) -> None:
 
 
 def stream_probe(dst: torch.Tensor, src: Optional[torch.Tensor], units: int, row_bytes: int, reads: int, writes: int,
-                 write_through: bool = False, stream=None) -> None:
+                 store_policy: int = 0, stream=None) -> None:
     """ep_stream_probe: `units` units each reading `reads` rows and writing `writes` rows of
-    row_bytes (sequential addresses), on device tensors large enough for them; stores
-    non-temporal, or device-scope write-through with write_through=True."""
+    row_bytes (sequential addresses), on device tensors large enough for them; store_policy
+    0 non-temporal, 1 device-scope write-through, 2 write-through with the non-temporal hint."""
     need_src, need_dst = units * reads * row_bytes, units * writes * row_bytes if writes else 1024
     if dst.nbytes < need_dst or (reads and (src is None or src.nbytes < need_src)):
         raise ValueError("stream_probe: buffers too small for the units asked for")
     _check(_lib_handle().ep_stream_probe(_ptr(dst), _ptr(src) if reads else None, units, row_bytes, reads, writes,
-                                         1 if write_through else 0, _stream_ptr(stream)), "ep_stream_probe")
+                                         int(store_policy), _stream_ptr(stream)), "ep_stream_probe")
 
 
 def pcie_probe(host: torch.Tensor, dev: torch.Tensor, nbytes: int, dirs: int) -> float:

@@ -109,7 +109,7 @@ __global__ __launch_bounds__(256) void combine_kernel(const u32x4 *__restrict__ 
 
     // the token's output row: V 16-byte vectors (bf16) or 2V (fp32)
     constexpr int kVecs = F32_OUT ? 2 : 1;
-    const RowStore<WT> dst((u32x4 *)out + t * V * kVecs, (uint32_t)V * kVecs * 16u);
+    const RowStore<WT ? kStoreWT : kStoreNT> dst((u32x4 *)out + t * V * kVecs, (uint32_t)V * kVecs * 16u);
 #pragma unroll
     for (int u = 0; u < U; ++u) {
         const int32_t v = v0 + u * kWave + lane;

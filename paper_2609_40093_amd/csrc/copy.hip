@@ -7,8 +7,8 @@
 //                  consecutive rows (each written row the XOR of the rows read), so the
 //                  traffic has the read:write mix of a kernel of the path with none of its
 //                  routing -- 1:k like the dispatch's pack, k:1 like the combine, 1:0
-//                  read-only, 0:1 write-only -- over sequential addresses, with either of
-//                  the pack's two store policies (RowStore).
+//                  read-only, 0:1 write-only -- over sequential addresses, with any of the
+//                  path's three store policies (RowStore).
 #include "ep_internal.h"
 
 namespace ep {
@@ -40,7 +40,7 @@ constexpr int kStreamMaxGroups = 16;  // 64-vector groups per row the probe hold
 // With no row to write, the XOR of everything read is stored (one 16-byte vector per
 // wave, into dst[unit % 64]) only if it equals a value that normal data does not give, so
 // the loads cannot be dropped.
-template <int G, bool WT>
+template <int G, int SP>
 __global__ __launch_bounds__(256) void stream_kernel(u32x4 *__restrict__ dst, const u32x4 *__restrict__ src,
                                                      int64_t units, int32_t reads, int32_t writes) {
     const int lane = threadIdx.x & 63;
@@ -73,7 +73,7 @@ __global__ __launch_bounds__(256) void stream_kernel(u32x4 *__restrict__ dst, co
     }
     u32x4 *out = dst + unit * writes * kRow;
     for (int w = 0; w < writes; ++w) {
-        const RowStore<WT> row(out + w * kRow, (uint32_t)(kRow * 16));
+        const RowStore<SP> row(out + w * kRow, (uint32_t)(kRow * 16));
 #pragma unroll
         for (int g = 0; g < G; ++g)
             row.put(acc[g], g * 64 + lane);
@@ -83,24 +83,25 @@ __global__ __launch_bounds__(256) void stream_kernel(u32x4 *__restrict__ dst, co
 }  // namespace
 
 hipError_t launch_stream_probe(void *dst, const void *src, int64_t units, int32_t row_bytes, int32_t reads,
-                               int32_t writes, bool write_through, hipStream_t stream) {
+                               int32_t writes, int store_policy, hipStream_t stream) {
     const int groups = row_bytes / 1024;
     if (units <= 0)
         return hipSuccess;
     const unsigned blocks = (unsigned)((units * 64 + 255) / 256);
     (void)hipGetLastError();
     TraceSlot ts = trace_acquire();
-    auto go = [&](auto nt_kern, auto wt_kern) {
-        hipExtLaunchKernelGGL(write_through ? wt_kern : nt_kern, dim3(blocks), dim3(256), 0, stream, ts.start, ts.stop,
-                              0, (u32x4 *)dst, (const u32x4 *)src, units, reads, writes);
+    auto go = [&](auto nt_kern, auto wt_kern, auto wts_kern) {
+        auto kern = store_policy == kStoreWTStream ? wts_kern : store_policy == kStoreWT ? wt_kern : nt_kern;
+        hipExtLaunchKernelGGL(kern, dim3(blocks), dim3(256), 0, stream, ts.start, ts.stop, 0, (u32x4 *)dst,
+                              (const u32x4 *)src, units, reads, writes);
     };
     switch (groups) {
-    case 1: go(stream_kernel<1, false>, stream_kernel<1, true>); break;
-    case 2: go(stream_kernel<2, false>, stream_kernel<2, true>); break;
-    case 4: go(stream_kernel<4, false>, stream_kernel<4, true>); break;
-    case 8: go(stream_kernel<8, false>, stream_kernel<8, true>); break;
-    case 14: go(stream_kernel<14, false>, stream_kernel<14, true>); break;
-    case 16: go(stream_kernel<16, false>, stream_kernel<16, true>); break;
+    case 1: go(stream_kernel<1, kStoreNT>, stream_kernel<1, kStoreWT>, stream_kernel<1, kStoreWTStream>); break;
+    case 2: go(stream_kernel<2, kStoreNT>, stream_kernel<2, kStoreWT>, stream_kernel<2, kStoreWTStream>); break;
+    case 4: go(stream_kernel<4, kStoreNT>, stream_kernel<4, kStoreWT>, stream_kernel<4, kStoreWTStream>); break;
+    case 8: go(stream_kernel<8, kStoreNT>, stream_kernel<8, kStoreWT>, stream_kernel<8, kStoreWTStream>); break;
+    case 14: go(stream_kernel<14, kStoreNT>, stream_kernel<14, kStoreWT>, stream_kernel<14, kStoreWTStream>); break;
+    case 16: go(stream_kernel<16, kStoreNT>, stream_kernel<16, kStoreWT>, stream_kernel<16, kStoreWTStream>); break;
     default: return hipErrorInvalidValue;
     }
     hipError_t err = hipGetLastError();

@@ -1027,17 +1027,17 @@ extern "C" ep_status ep_copy_probe(void *dst_dev, const void *src_dev, size_t by
 }
 
 extern "C" ep_status ep_stream_probe(void *dst_dev, const void *src_dev, int64_t units, int32_t row_bytes,
-                                     int32_t reads, int32_t writes, int32_t write_through, hipStream_t stream) {
+                                     int32_t reads, int32_t writes, int32_t store_policy, hipStream_t stream) {
     const int g = row_bytes / 1024;
     const bool shape = row_bytes > 0 && row_bytes % 1024 == 0 &&
                        (g == 1 || g == 2 || g == 4 || g == 8 || g == 14 || g == 16);
     if (units < 0 || !shape || reads < 0 || writes < 0 || reads + writes == 0 || reads > 64 || writes > 64 ||
-        (write_through != 0 && write_through != 1))
+        store_policy < 0 || store_policy > 2)
         return fail(EP_ERR_INVALID_ARG, "ep_stream_probe: need units >= 0, row_bytes = 1024 * {1,2,4,8,14,16}, "
-                                        "0 <= reads, writes <= 64, reads + writes > 0, write_through 0 or 1");
+                                        "0 <= reads, writes <= 64, reads + writes > 0, store_policy 0, 1 or 2");
     if (units > 0 && (!dst_dev || !aligned16(dst_dev) || (reads > 0 && (!src_dev || !aligned16(src_dev)))))
         return fail(EP_ERR_INVALID_ARG, "ep_stream_probe: 16-byte aligned src (when reading) and dst are required");
-    EP_HIP(ep::launch_stream_probe(dst_dev, src_dev, units, row_bytes, reads, writes, write_through != 0, stream));
+    EP_HIP(ep::launch_stream_probe(dst_dev, src_dev, units, row_bytes, reads, writes, store_policy, stream));
     return EP_OK;
 }
 

@@ -18,27 +18,24 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 constexpr int kWave = 64;
 
 // Stores of one row (a packed row of the dispatch, an output row of the combine) from a
-// wave-uniform base, under one of two policies that each kernel picks by the bytes a launch
-// writes (measured on MI355X, inputs rotated past the memory-side cache):
-//   WT = false: non-temporal stores;
-//   WT = true:  16-byte buffer stores at device scope (sc1: written through the XCD's L2
-//               rather than held there dirty).
-// The pack (rows of 4 and 14 KiB) writes through from 2 GiB per launch up, where the
-// non-temporal rate falls with the size of the stream (1.5-2.5% faster; non-temporal is up
-// to 20% faster at 0.1-1 GiB).  The combine's thresholds are beside it.
-// The buffer range of a write-through row is the `bytes` from `base` on: a store past it is
-// dropped by the hardware.
+// wave-uniform base, under one of three policies that each kernel picks by the bytes a
+// launch writes (measured on MI355X, inputs rotated past the memory-side cache):
+//   kStoreNT:        non-temporal stores;
+//   kStoreWT:        16-byte buffer stores at device scope (sc1: written through the XCD's
+//                    L2 rather than held there dirty);
+//   kStoreWTStream:  the same with the non-temporal hint as well (sc1 nt).
+// The pack (rows of 4 and 14 KiB) stores with kStoreWTStream from 2 GiB per launch up,
+// where the non-temporal rate falls with the size of the stream: at the prefill pack
+// (3.76 GB written) 764 us against 772 us with kStoreWT and 778 us non-temporal;
+// non-temporal is up to 20% faster at 0.1-1 GiB.  The combine writes through with kStoreWT
+// below 128 MiB of output (there kStoreWTStream measured 5-8% slower); its thresholds are
+// beside it.  The buffer range of a buffer-store row is the `bytes` from `base` on: a store
+// past it is dropped by the hardware.
+constexpr int kStoreNT = 0, kStoreWT = 1, kStoreWTStream = 2;
 constexpr int64_t kWriteThroughBytes = 2ll << 30;  // the pack's
-template <bool WT>
-struct RowStore;
-template <>
-struct RowStore<false> {
-    u32x4 *base;
-    __device__ __forceinline__ RowStore(u32x4 *b, uint32_t) : base(b) {}
-    __device__ __forceinline__ void put(u32x4 v, uint32_t vec) const { __builtin_nontemporal_store(v, base + vec); }
-};
-template <>
-struct RowStore<true> {
+template <int POL>
+struct RowStore {
+    static_assert(POL == kStoreWT || POL == kStoreWTStream, "buffer-store policies");
     __amdgpu_buffer_rsrc_t rsrc;
     __device__ __forceinline__ RowStore(u32x4 *b, uint32_t bytes) {
         const uint64_t a = reinterpret_cast<uint64_t>(b);
@@ -48,8 +45,15 @@ struct RowStore<true> {
                                                  (int)__builtin_amdgcn_readfirstlane(bytes), 0x00020000);
     }
     __device__ __forceinline__ void put(u32x4 v, uint32_t vec) const {
-        __builtin_amdgcn_raw_buffer_store_b128(v, rsrc, vec * 16u, 0, 16 /* sc1 */);
+        // cache-policy operand: 16 = sc1 (device scope), 2 = nt
+        __builtin_amdgcn_raw_buffer_store_b128(v, rsrc, vec * 16u, 0, POL == kStoreWT ? 16 : 16 | 2);
     }
+};
+template <>
+struct RowStore<kStoreNT> {
+    u32x4 *base;
+    __device__ __forceinline__ RowStore(u32x4 *b, uint32_t) : base(b) {}
+    __device__ __forceinline__ void put(u32x4 v, uint32_t vec) const { __builtin_nontemporal_store(v, base + vec); }
 };
 
 // ---- layout geometry -----------------------------------------------------------
@@ -246,6 +250,6 @@ hipError_t launch_copy(void *dst, const void *src, size_t bytes, hipStream_t str
 // Streaming probe of a given read:write mix (copy.hip); row_bytes = 1024 * g with g in
 // {1, 2, 4, 8, 14, 16}.
 hipError_t launch_stream_probe(void *dst, const void *src, int64_t units, int32_t row_bytes, int32_t reads,
-                               int32_t writes, bool write_through, hipStream_t stream);
+                               int32_t writes, int store_policy, hipStream_t stream);
 
 }  // namespace ep

@@ -362,7 +362,7 @@ __global__ __launch_bounds__(kFMaxThreads) void layout_pack_kernel(FusedArgs a, 
             const int64_t p = s_pos[(t - tok0) * K + j];
             if (p < 0 || p >= a.max_rows)
                 continue;
-            const RowStore<false> dst(packed + p * V + col, (uint32_t)(V - col) * 16u);
+            const RowStore<kStoreNT> dst(packed + p * V + col, (uint32_t)(V - col) * 16u);
 #pragma unroll
             for (int u = 0; u < U; ++u)
                 dst.put(d[u], u * kWave + lane);

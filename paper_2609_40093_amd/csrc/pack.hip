@@ -27,7 +27,8 @@
 //           16-group chunks with guarded tails.  Rows with no divisor of at least 4 groups
 //           (G a prime above 16) use the generic 16-group instance.
 // Stores: non-temporal below 2 GiB written per launch, device-scope write-through buffer
-// stores from 2 GiB up (RowStore: each policy is the faster one at its sizes).  Rows carry
+// stores with the non-temporal hint from 2 GiB up (RowStore: each policy is the faster one
+// at its sizes).  Rows carry
 // no reuse across workgroups, so the workgroup-to-XCD placement needs no remapping.
 #include "ep_internal.h"
 
@@ -53,7 +54,7 @@ __device__ __forceinline__ bool store_ok(int32_t g0, int u, int32_t ng, int lane
 }
 
 // One wave per (token, chunk): the chunk is loaded once and stored to the k rows.
-template <int U, bool EXACT, bool WT>
+template <int U, bool EXACT, int SP>
 __global__ __launch_bounds__(256) void pack_kernel(const u32x4 *__restrict__ x, int64_t T, PackGeom pg, int32_t k,
                                                    const int32_t *__restrict__ slot_pos,
                                                    u32x4 *__restrict__ packed, int64_t max_rows,
@@ -81,7 +82,7 @@ __global__ __launch_bounds__(256) void pack_kernel(const u32x4 *__restrict__ x, 
         const int64_t p = sp[j];
         if (p < 0 || p >= max_rows)
             continue;
-        const RowStore<WT> dst(packed + p * pg.V + g0 * kWave, (uint32_t)(pg.V - g0 * kWave) * 16u);
+        const RowStore<SP> dst(packed + p * pg.V + g0 * kWave, (uint32_t)(pg.V - g0 * kWave) * 16u);
 #pragma unroll
         for (int u = 0; u < U; ++u)
             if (EXACT || store_ok(g0, u, ng, lane, pg.V))
@@ -93,7 +94,7 @@ __global__ __launch_bounds__(256) void pack_kernel(const u32x4 *__restrict__ x, 
 
 // One wave per (token, chunk, slot), the k waves of a chunk adjacent: each wave writes a
 // single destination row.
-template <int U, bool EXACT, bool WT>
+template <int U, bool EXACT, int SP>
 __global__ __launch_bounds__(1024) void pack_slot_kernel(const u32x4 *__restrict__ x, int64_t T, PackGeom pg, int32_t k,
                                                         const int32_t *__restrict__ slot_pos,
                                                         u32x4 *__restrict__ packed, int64_t max_rows,
@@ -117,7 +118,7 @@ __global__ __launch_bounds__(1024) void pack_slot_kernel(const u32x4 *__restrict
     if (p < 0 || p >= max_rows)
         return;
     const u32x4 *src = x + t * pg.V;
-    const RowStore<WT> dst(packed + p * pg.V + g0 * kWave, (uint32_t)(pg.V - g0 * kWave) * 16u);
+    const RowStore<SP> dst(packed + p * pg.V + g0 * kWave, (uint32_t)(pg.V - g0 * kWave) * 16u);
     u32x4 d[U];
 #pragma unroll
     for (int u = 0; u < U; ++u)
@@ -130,49 +131,49 @@ __global__ __launch_bounds__(1024) void pack_slot_kernel(const u32x4 *__restrict
         __threadfence_system();
 }
 
-template <int U, bool EXACT, bool WT>
+template <int U, bool EXACT, int SP>
 void launch_pack_u(bool per_slot, dim3 grid, dim3 block, hipStream_t stream, TraceSlot ts, const u32x4 *x, int64_t T,
                    const PackGeom &pg, int32_t k, const int32_t *slot_pos, u32x4 *packed, int64_t max_rows,
                    uint32_t *epoch_word, uint32_t epoch, RoundSel sel, bool fence_system) {
     if (per_slot)
-        hipExtLaunchKernelGGL(pack_slot_kernel<U, EXACT, WT>, grid, block, 0, stream, ts.start, ts.stop, 0, x, T, pg,
+        hipExtLaunchKernelGGL(pack_slot_kernel<U, EXACT, SP>, grid, block, 0, stream, ts.start, ts.stop, 0, x, T, pg,
                               k, slot_pos, packed, max_rows, epoch_word, epoch, sel, fence_system);
     else
-        hipExtLaunchKernelGGL(pack_kernel<U, EXACT, WT>, grid, dim3(256), 0, stream, ts.start, ts.stop, 0, x, T, pg, k,
+        hipExtLaunchKernelGGL(pack_kernel<U, EXACT, SP>, grid, dim3(256), 0, stream, ts.start, ts.stop, 0, x, T, pg, k,
                               slot_pos, packed, max_rows, epoch_word, epoch, sel, fence_system);
 }
 
 // Chunk lengths with an EXACT instance (groups of 64 vectors), longest first.
 constexpr int kExactU[] = {16, 15, 14, 13, 12, 11, 10, 9, 8, 7, 6, 5, 4, 3, 2, 1};
 
-// Launches the instance for chunk length `exact` (0: generic) under store policy WT.
-template <bool WT>
+// Launches the instance for chunk length `exact` (0: generic) under store policy SP.
+template <int SP>
 void launch_chunk(int exact, bool per_slot, dim3 grid, dim3 block, hipStream_t stream, TraceSlot ts, const u32x4 *x,
                   int64_t T, const PackGeom &pg, int32_t k, const int32_t *slot_pos, u32x4 *packed, int64_t max_rows,
                   uint32_t *epoch_word, uint32_t epoch, RoundSel sel, bool fence_system) {
 #define EP_PACK_ARGS per_slot, grid, block, stream, ts, x, T, pg, k, slot_pos, packed, max_rows, epoch_word, epoch, sel, fence_system
     switch (exact) {
-    case 16: launch_pack_u<16, true, WT>(EP_PACK_ARGS); break;
-    case 15: launch_pack_u<15, true, WT>(EP_PACK_ARGS); break;
-    case 14: launch_pack_u<14, true, WT>(EP_PACK_ARGS); break;
-    case 13: launch_pack_u<13, true, WT>(EP_PACK_ARGS); break;
-    case 12: launch_pack_u<12, true, WT>(EP_PACK_ARGS); break;
-    case 11: launch_pack_u<11, true, WT>(EP_PACK_ARGS); break;
-    case 10: launch_pack_u<10, true, WT>(EP_PACK_ARGS); break;
-    case 9: launch_pack_u<9, true, WT>(EP_PACK_ARGS); break;
-    case 8: launch_pack_u<8, true, WT>(EP_PACK_ARGS); break;
-    case 7: launch_pack_u<7, true, WT>(EP_PACK_ARGS); break;
-    case 6: launch_pack_u<6, true, WT>(EP_PACK_ARGS); break;
-    case 5: launch_pack_u<5, true, WT>(EP_PACK_ARGS); break;
-    case 4: launch_pack_u<4, true, WT>(EP_PACK_ARGS); break;
-    case 3: launch_pack_u<3, true, WT>(EP_PACK_ARGS); break;
-    case 2: launch_pack_u<2, true, WT>(EP_PACK_ARGS); break;
-    case 1: launch_pack_u<1, true, WT>(EP_PACK_ARGS); break;
+    case 16: launch_pack_u<16, true, SP>(EP_PACK_ARGS); break;
+    case 15: launch_pack_u<15, true, SP>(EP_PACK_ARGS); break;
+    case 14: launch_pack_u<14, true, SP>(EP_PACK_ARGS); break;
+    case 13: launch_pack_u<13, true, SP>(EP_PACK_ARGS); break;
+    case 12: launch_pack_u<12, true, SP>(EP_PACK_ARGS); break;
+    case 11: launch_pack_u<11, true, SP>(EP_PACK_ARGS); break;
+    case 10: launch_pack_u<10, true, SP>(EP_PACK_ARGS); break;
+    case 9: launch_pack_u<9, true, SP>(EP_PACK_ARGS); break;
+    case 8: launch_pack_u<8, true, SP>(EP_PACK_ARGS); break;
+    case 7: launch_pack_u<7, true, SP>(EP_PACK_ARGS); break;
+    case 6: launch_pack_u<6, true, SP>(EP_PACK_ARGS); break;
+    case 5: launch_pack_u<5, true, SP>(EP_PACK_ARGS); break;
+    case 4: launch_pack_u<4, true, SP>(EP_PACK_ARGS); break;
+    case 3: launch_pack_u<3, true, SP>(EP_PACK_ARGS); break;
+    case 2: launch_pack_u<2, true, SP>(EP_PACK_ARGS); break;
+    case 1: launch_pack_u<1, true, SP>(EP_PACK_ARGS); break;
     default:
         if (pg.gpc > 4)
-            launch_pack_u<16, false, WT>(EP_PACK_ARGS);
+            launch_pack_u<16, false, SP>(EP_PACK_ARGS);
         else
-            launch_pack_u<4, false, WT>(EP_PACK_ARGS);
+            launch_pack_u<4, false, SP>(EP_PACK_ARGS);
     }
 #undef EP_PACK_ARGS
 }
@@ -225,10 +226,10 @@ hipError_t launch_pack(const void *x, int64_t T, int32_t H, int32_t k, const int
     TraceSlot ts = trace_acquire();
     const bool wt = T * k * (int64_t)pg.V * 16 >= kWriteThroughBytes;
     if (wt)
-        launch_chunk<true>(exact, per_slot, grid, dim3(per_slot ? waves * kWave : 256), stream, ts, xv, T, pg, k,
+        launch_chunk<kStoreWTStream>(exact, per_slot, grid, dim3(per_slot ? waves * kWave : 256), stream, ts, xv, T, pg, k,
                            slot_pos, pv, max_rows, epoch_word, epoch, sel, fence_system);
     else
-        launch_chunk<false>(exact, per_slot, grid, dim3(per_slot ? waves * kWave : 256), stream, ts, xv, T, pg, k,
+        launch_chunk<kStoreNT>(exact, per_slot, grid, dim3(per_slot ? waves * kWave : 256), stream, ts, xv, T, pg, k,
                             slot_pos, pv, max_rows, epoch_word, epoch, sel, fence_system);
     hipError_t err = hipGetLastError();
     if (err == hipSuccess)

@@ -143,9 +143,10 @@ def test_null_staging_calls(lib):
     assert lib.ep_sim_peers_start(None, 0, ctypes.byref(ctypes.c_void_p())) == _lib.EP_ERR_INVALID_ARG
     assert lib.ep_sim_peers_stop(None) == 0
     assert lib.ep_copy_probe(ctypes.c_void_p(16), ctypes.c_void_p(16), 15, None) == _lib.EP_ERR_INVALID_ARG
-    # store policy 0 or 1 only; a row size with no probe instance
-    assert lib.ep_stream_probe(ctypes.c_void_p(16), None, 4, 1024, 0, 1, 2, None) == _lib.EP_ERR_INVALID_ARG
-    assert b"write_through" in lib.ep_last_error()
+    # store policy 0, 1 or 2 only; a row size with no probe instance
+    for pol in (3, -1):
+        assert lib.ep_stream_probe(ctypes.c_void_p(16), None, 4, 1024, 0, 1, pol, None) == _lib.EP_ERR_INVALID_ARG
+        assert b"store_policy" in lib.ep_last_error()
     assert lib.ep_stream_probe(ctypes.c_void_p(16), None, 4, 3072, 0, 1, 0, None) == _lib.EP_ERR_INVALID_ARG
 
 

@@ -146,10 +146,14 @@ def test_pattern_bound_takes_the_slowest_direction_of_each_phase():
 
 def test_streaming_ceiling_takes_the_faster_store_policy_of_the_kernels_mix():
     ceil = {"write_only": {"frac": 0.68}, "write_only_write_through": {"frac": 0.69},
+            "write_only_write_through_nt": {"frac": 0.685},
             "combine_like_8_to_1": {"frac": 0.73}, "combine_like_8_to_1_write_through": {"frac": 0.70},
-            "note": "probe"}
+            "combine_like_8_to_1_write_through_nt": {"frac": 0.69}, "note": "probe"}
     got = bench.ceiling_of("pack", 0.69, ceil, 8)
     assert got["mix"] == "write_only_write_through" and got["frac"] == 0.69 and got["kernel_frac_of_ceiling"] == 1.0
+    ceil["write_only_write_through_nt"] = {"frac": 0.70}
+    got = bench.ceiling_of("pack", 0.69, ceil, 8)
+    assert got["mix"] == "write_only_write_through_nt" and got["kernel_frac_of_ceiling"] == round(0.69 / 0.70, 3)
     got = bench.ceiling_of("combine", 0.711, ceil, 8)
     assert got["mix"] == "combine_like_8_to_1" and got["kernel_frac_of_ceiling"] == round(0.711 / 0.73, 3)
     assert "note" in bench.ceiling_of("layout_pack", 0.69, {"note": "no instance"}, 2)
