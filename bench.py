@@ -737,9 +737,12 @@ def bench_dense(cfg, inp, args, dev, peaks) -> dict:
 
 def bench_graph(names, args, dev, peaks) -> dict:
     """Graph-replayed rounds (the decode path, Sec. 4.5): one round -- round counter,
-    layout, dispatch into pinned memory, combine from pinned memory -- captured once in a
-    HIP graph and replayed back to back.  The simulated peers only raise flags and credits
-    (their returned rows are seeded data already in the pinned receive buffers)."""
+    layout, dispatch, combine -- captured once in a HIP graph and replayed back to back,
+    with each of the two kinds of host legs: the compute units storing the rows to and
+    loading them from pinned memory (`compute_unit_legs`), or SDMA engines driven by the
+    library's host-leg thread, the captured kernels packing into and reducing from device
+    memory (`sdma_legs`, ep_graph_legs_sdma).  The simulated peers only raise flags and
+    credits (their returned rows are seeded data already in the pinned receive buffers)."""
     import numpy as np
     import torch
 
@@ -751,53 +754,61 @@ def bench_graph(names, args, dev, peaks) -> dict:
         cfg = synth.config(name)
         inp = synth.make_inputs(cfg)
         T, H, E, k, R, n = cfg.T, cfg.H, cfg.E, cfg.k, cfg.R, cfg.slots
-        st = ep.Staging("pinned", n, H, R, num_buffers=2)
         y = inp.expert_outputs()
-        for b in range(2):
-            st.host_array("recv", b)[:n] = y
-        peers = ep.SimPeers(st, echo=False, graph_rows=n)
         x = torch.from_numpy(inp.x.view(np.int16)).to(dev)
         idx = torch.from_numpy(inp.topk_idx).to(dev)
         w = torch.from_numpy(inp.topk_w).to(dev)
         out = torch.empty((T, H), dtype=torch.bfloat16, device=dev)
-        lay = ep.dispatch_layout(idx, E, R)
+        res[name] = {}
+        for legs in ("compute_unit_legs", "sdma_legs"):
+            st = ep.Staging("pinned", n, H, R, num_buffers=2)
+            for b in range(2):
+                st.host_array("recv", b)[:n] = y
+            peers = ep.SimPeers(st, echo=False, graph_rows=n)
+            if legs == "sdma_legs":
+                ep.graph_legs_sdma(st, True)
+            lay = ep.dispatch_layout(idx, E, R)
 
-        def one_round():
-            ep.round_advance(st)
-            ep.dispatch_layout(idx, E, R, out=lay)
-            ep.dispatch_graph(x, lay.slot_pos, st, topk=k)
-            ep.combine_graph(st, lay.slot_pos, w, out)
+            def one_round():
+                ep.round_advance(st)
+                ep.dispatch_layout(idx, E, R, out=lay)
+                ep.dispatch_graph(x, lay.slot_pos, st, topk=k)
+                ep.combine_graph(st, lay.slot_pos, w, out)
 
-        one_round()
-        torch.cuda.synchronize()
-        g = torch.cuda.CUDAGraph()
-        s = torch.cuda.Stream()
-        s.wait_stream(torch.cuda.current_stream())
-        with torch.cuda.stream(s):
-            with torch.cuda.graph(g, stream=s):
-                one_round()
-        torch.cuda.current_stream().wait_stream(s)
-        for _ in range(args.warmup):
-            g.replay()
-        torch.cuda.synchronize()
-        steps = max(10, min(args.steps, 100))
-        t0 = time.perf_counter()
-        for _ in range(steps):
-            g.replay()
-        torch.cuda.synchronize()
-        t1 = time.perf_counter()
-        st.status()
-        rounds = ep.round_read(st)
-        peers.wait_round(rounds)
-        peers.close()
-        st.close()
-        us = (t1 - t0) * 1e6 / steps
-        pcie = 2 * n * 2 * H
-        gbps = pcie / (us * 1e-6) / 1e9
-        res[name] = {"us_per_round": round(us, 1), "pcie_bytes_per_round": pcie, "pcie_GBps": round(gbps, 2),
-                     "frac_of_one_way_pcie_peak": round(gbps / peaks["d2h_alone"], 3), "replays": steps}
-    res["note"] = ("rows stored to and loaded from pinned memory by the compute units; the two directions run one "
-                   "after the other within a round, so the one-way peak bounds the rate")
+            one_round()
+            torch.cuda.synchronize()
+            g = torch.cuda.CUDAGraph()
+            s = torch.cuda.Stream()
+            s.wait_stream(torch.cuda.current_stream())
+            with torch.cuda.stream(s):
+                with torch.cuda.graph(g, stream=s):
+                    one_round()
+            torch.cuda.current_stream().wait_stream(s)
+            for _ in range(args.warmup):
+                g.replay()
+            torch.cuda.synchronize()
+            steps = max(10, min(args.steps, 100))
+            t0 = time.perf_counter()
+            for _ in range(steps):
+                g.replay()
+            torch.cuda.synchronize()
+            t1 = time.perf_counter()
+            st.status()
+            rounds = ep.round_read(st)
+            peers.wait_round(rounds)
+            peers.close()
+            del g
+            st.close()
+            us = (t1 - t0) * 1e6 / steps
+            pcie = 2 * n * 2 * H
+            gbps = pcie / (us * 1e-6) / 1e9
+            res[name][legs] = {"us_per_round": round(us, 1), "pcie_bytes_per_round": pcie,
+                               "pcie_GBps": round(gbps, 2),
+                               "frac_of_one_way_pcie_peak": round(gbps / peaks["d2h_alone"], 3), "replays": steps}
+    res["note"] = ("compute_unit_legs: rows stored to and loaded from pinned memory by the compute units; sdma_legs: "
+                   "rows packed into and reduced from device memory by the captured kernels and moved by SDMA "
+                   "engines (the library's host-leg thread); the two directions run one after the other within a "
+                   "round, so the one-way peak bounds the rate")
     return res
 
 

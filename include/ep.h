@@ -54,7 +54,7 @@
 extern "C" {
 #endif
 
-#define EP_ABI_VERSION 5
+#define EP_ABI_VERSION 6
 #define EP_MAX_EXPERTS 2048 /* largest E the layout kernels accept */
 
 typedef enum {
@@ -342,6 +342,25 @@ ep_status ep_dispatch_graph(const void *x_dev, int64_t num_tokens, int32_t hidde
                             const int32_t *slot_pos, ep_staging *s, hipStream_t stream);
 ep_status ep_combine_graph(ep_staging *s, const int32_t *slot_pos, const float *topk_w, int64_t num_tokens,
                            int32_t hidden, int32_t topk, void *out_dev, ep_out_dtype out_dtype, hipStream_t stream);
+/* Host legs of graph-replayed rounds on SDMA engines instead of the compute units (Sec. 4.3:
+ * the DMA engines move the bulk data, so no compute unit is spent on it; Sec. 4.4: flags
+ * raised only after their data).  on = 1 starts a library thread (call it outside graph
+ * capture, before capturing the rounds: it reads the round counter); on = 0 stops it,
+ * after synchronizing the device.  With the thread running, ep_dispatch_graph packs into
+ * the device send buffer of set round % 2 and stamps that set's ready word in host memory;
+ * the thread sees it, copies the T*topk rows to host_send on the device->host engine, and
+ * sets the set's send_flags to the round once they have landed; it then waits for every
+ * sender's recv flag of the set and for this rank's recv_credit of round - 2, copies the
+ * returned rows from host_recv to the device recv buffer on the host->device engine and
+ * sets the set's landed word; ep_combine_graph waits (bounded) for that word and reduces
+ * from the device recv buffer.  The other ranks (simulated peers) see the same flags,
+ * credits and pinned buffers as with the compute-unit legs.  No copy depends on a signal
+ * released by the device: each is queued once its source is complete.  The thread's
+ * waits for the peers and for its copies are bounded by the staging's timeout; an expired
+ * one is recorded in the status block (ep_staging_status) and the round goes on.
+ * ep_staging_free stops the thread.  EP_ERR_INVALID_ARG for a staging that graph rounds
+ * cannot use; EP_ERR_HIP if no SDMA engine can be taken. */
+ep_status ep_graph_legs_sdma(ep_staging *s, int32_t on);
 
 /* ------------------------------------------------------- dense collectives (Sec. 4.2)
  *

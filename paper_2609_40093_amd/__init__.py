@@ -11,7 +11,7 @@ _API = ("EPError", "Layout", "Staging", "SimPeers", "dispatch_layout", "layout_v
         "pcie_probe",
         "MODE_PER_SENDER", "MODE_DUPLEX", "MODE_REMOTE_ONLY", "MODE_ACCUMULATE", "LocalLayout", "dispatch_layout_local", "pack",
         "combine_rows", "Dense", "allgather", "reducescatter", "round_advance", "round_read", "dispatch_graph",
-        "combine_graph")
+        "combine_graph", "graph_legs_sdma")
 
 __all__ = list(_API)
 

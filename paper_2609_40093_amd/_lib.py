@@ -15,7 +15,7 @@ EP_STAGING_HBM, EP_STAGING_PINNED_HOST = 0, 1
 EP_OUT_BF16, EP_OUT_F32 = 0, 1
 EP_SIM_FLAGS_ONLY, EP_SIM_ECHO = 0, 1
 EP_MODE_PER_SENDER, EP_MODE_DUPLEX, EP_MODE_REMOTE_ONLY, EP_MODE_ACCUMULATE = 1, 2, 4, 8
-ABI_VERSION = 5
+ABI_VERSION = 6
 EP_MAX_EXPERTS = 2048
 
 c_i32, c_i64, c_u32, c_size, c_vp = ctypes.c_int32, ctypes.c_int64, ctypes.c_uint32, ctypes.c_size_t, ctypes.c_void_p
@@ -73,6 +73,7 @@ SIGNATURES = {
     "ep_round_read": (c_i32, [c_vp, ctypes.POINTER(c_u32)]),
     "ep_dispatch_graph": (c_i32, [c_vp, c_i64, c_i32, c_i32, c_vp, c_vp, c_vp]),
     "ep_combine_graph": (c_i32, [c_vp, c_vp, c_vp, c_i64, c_i32, c_i32, c_vp, c_i32, c_vp]),
+    "ep_graph_legs_sdma": (c_i32, [c_vp, c_i32]),
     "ep_sim_graph_start": (c_i32, [c_vp, c_i64, c_i64, c_i32, ctypes.POINTER(c_vp)]),
     "ep_sim_graph_wait": (c_i32, [c_vp, c_u32, c_i64]),
     "ep_dense_alloc": (c_i32, [c_i64, c_i32, c_i32, c_i32, c_i32, c_i32, ctypes.POINTER(c_vp)]),

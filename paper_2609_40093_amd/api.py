@@ -25,7 +25,7 @@ __all__ = ["EPError", "Layout", "Staging", "SimPeers", "dispatch_layout", "layou
            "combine", "trace_enable", "trace_read", "trace_reset", "copy_probe", "stream_probe", "workspace_bytes",
            "pcie_probe", "MODE_PER_SENDER", "MODE_DUPLEX", "MODE_REMOTE_ONLY", "MODE_ACCUMULATE", "LocalLayout",
            "dispatch_layout_local", "pack", "combine_rows", "Dense", "allgather", "reducescatter",
-           "round_advance", "round_read", "dispatch_graph", "combine_graph"]
+           "round_advance", "round_read", "dispatch_graph", "combine_graph", "graph_legs_sdma"]
 
 _PAYLOAD_DTYPES = (torch.bfloat16, torch.int16, torch.uint16)
 
@@ -491,6 +491,12 @@ def round_read(staging: Staging) -> int:
     r = ctypes.c_uint32()
     _check(_lib_handle().ep_round_read(staging.handle, ctypes.byref(r)), "ep_round_read")
     return r.value
+
+
+def graph_legs_sdma(staging: Staging, on: bool = True) -> None:
+    """ep_graph_legs_sdma: the host legs of graph-replayed rounds on SDMA engines (a library
+    thread) instead of the compute units; call before capturing the rounds."""
+    _check(_lib_handle().ep_graph_legs_sdma(staging.handle, 1 if on else 0), "ep_graph_legs_sdma")
 
 
 def dispatch_graph(x: torch.Tensor, slot_pos: torch.Tensor, staging: Staging, *, topk: int, stream=None) -> None:

@@ -334,6 +334,8 @@ namespace {
 
 void staging_release(ep_staging *s) {
     // first the SDMA copies (each waits until its copies have landed), then their buffers
+    ep::graph_legs_destroy(s->graph_legs);
+    s->graph_legs = nullptr;
     if (s->lane) {
         s->lane->release();
         delete s->lane;
@@ -621,7 +623,9 @@ struct StagingFlagNamer : ep::FlagNamer {
                             {"in_landed", "rank", &ep_staging::in_landed, R},
                             {"recv_landed", "rank", &ep_staging::recv_landed, R},
                             {"send_credits", "rank", &ep_staging::send_credit, R},
-                            {"recv_credit", "word", &ep_staging::recv_credit, 1}};
+                            {"recv_credit", "word", &ep_staging::recv_credit, 1},
+                            {"graph_ready", "word", &ep_staging::graph_ready, 1},
+                            {"graph_landed", "word", &ep_staging::graph_landed, 1}};
         for (const Arr &a : arrs)
             for (int b = 0; b < s->num_buffers; ++b) {
                 const uint32_t *base = (s->*a.at)(b);
@@ -912,6 +916,29 @@ extern "C" ep_status ep_round_read(ep_staging *s, uint32_t *round) {
     return EP_OK;
 }
 
+extern "C" ep_status ep_graph_legs_sdma(ep_staging *s, int32_t on) {
+    ep_status st = check_graph(s, "ep_graph_legs_sdma");
+    if (st != EP_OK)
+        return st;
+    if (!on) {
+        EP_HIP(hipDeviceSynchronize());  // no captured round may still wait for the thread
+        ep::graph_legs_destroy(s->graph_legs);
+        s->graph_legs = nullptr;
+        return EP_OK;
+    }
+    if (s->graph_legs)
+        return EP_OK;
+    // the thread starts at the round the device counter reaches next
+    EP_HIP(hipDeviceSynchronize());
+    uint32_t round = 0;
+    EP_HIP(hipMemcpy(&round, s->dev_round, sizeof round, hipMemcpyDeviceToHost));
+    std::string err;
+    s->graph_legs = ep::graph_legs_create(s, round + 1u, err);
+    if (!s->graph_legs)
+        return fail(EP_ERR_HIP, "ep_graph_legs_sdma: %s", err.c_str());
+    return EP_OK;
+}
+
 extern "C" ep_status ep_dispatch_graph(const void *x_dev, int64_t num_tokens, int32_t hidden, int32_t topk,
                                        const int32_t *slot_pos, ep_staging *s, hipStream_t stream) {
     ep_status st = check_graph(s, "ep_dispatch_graph");
@@ -925,12 +952,21 @@ extern "C" ep_status ep_dispatch_graph(const void *x_dev, int64_t num_tokens, in
     // buffer set round % 2 is free once every receiver credited its contents of two rounds ago
     EP_HIP(ep::launch_round_gate("wait_credits", s->dev_round, s->send_credit(0), s->num_ranks, s->num_ranks, -2,
                                  ticks, s->sleep_units, s->status(), stream));
+    // the rows go to pinned memory from the compute units, or with SDMA legs to the device
+    // send buffer, from which the legs' thread copies them once the ready word holds the round
+    const bool sdma = s->graph_legs != nullptr;
+    if (sdma)
+        ep::graph_legs_set_rows(s->graph_legs, num_tokens * topk);
+    void *const *dst = sdma ? s->dev_send : s->host_send;
     ep::RoundSel sel;
-    sel.alt = s->host_send[1];
+    sel.alt = dst[1];
     sel.round = s->dev_round;
-    EP_HIP(ep::launch_pack(x_dev, num_tokens, hidden, topk, slot_pos, s->host_send[0], s->max_rows, nullptr, 0, stream,
-                           sel, true));
-    EP_HIP(ep::launch_round_stamp(s->dev_round, s->send_flags(0), s->max_chunks, 1, stream));
+    EP_HIP(ep::launch_pack(x_dev, num_tokens, hidden, topk, slot_pos, dst[0], s->max_rows, nullptr, 0, stream, sel,
+                           true));
+    if (sdma)
+        EP_HIP(ep::launch_round_stamp(s->dev_round, s->graph_ready(0), 1, 1, stream));
+    else
+        EP_HIP(ep::launch_round_stamp(s->dev_round, s->send_flags(0), s->max_chunks, 1, stream));
     return EP_OK;
 }
 
@@ -947,13 +983,21 @@ extern "C" ep_status ep_combine_graph(ep_staging *s, const int32_t *slot_pos, co
     if (num_tokens > 0 && (!topk_w || !out_dev || !aligned16(out_dev)))
         return fail(EP_ERR_INVALID_ARG, "ep_combine_graph: topk_w and a 16-byte aligned out are required");
     const int64_t ticks = s->timeout_us * s->wall_clock_khz / 1000;
-    EP_HIP(ep::launch_round_gate("wait_returned", s->dev_round, s->recv_flags(0), s->num_ranks, s->num_ranks, 0,
-                                 ticks, s->sleep_units, s->status(), stream));
+    // the rows are read from pinned memory by the compute units, or with SDMA legs from the
+    // device receive buffer once the legs' thread has copied every sender's rows there
+    const bool sdma = s->graph_legs != nullptr;
+    if (sdma)
+        EP_HIP(ep::launch_round_gate("wait_graph_landed", s->dev_round, s->graph_landed(0), 1, 1, 0, ticks,
+                                     s->sleep_units, s->status(), stream));
+    else
+        EP_HIP(ep::launch_round_gate("wait_returned", s->dev_round, s->recv_flags(0), s->num_ranks, s->num_ranks, 0,
+                                     ticks, s->sleep_units, s->status(), stream));
+    void *const *src = sdma ? s->dev_recv : s->host_recv;
     ep::RoundSel sel;
-    sel.alt = s->host_recv[1];
+    sel.alt = src[1];
     sel.round = s->dev_round;
-    EP_HIP(ep::launch_combine(s->host_recv[0], slot_pos, topk_w, num_tokens, hidden, topk, out_dev,
-                              out_dtype == EP_OUT_F32, s->max_rows, stream, sel));
+    EP_HIP(ep::launch_combine(src[0], slot_pos, topk_w, num_tokens, hidden, topk, out_dev, out_dtype == EP_OUT_F32,
+                              s->max_rows, stream, sel));
     // the returned rows of this round are consumed: credit the buffer set to the senders
     EP_HIP(ep::launch_round_stamp(s->dev_round, s->recv_credit(0), 1, 1, stream));
     return EP_OK;

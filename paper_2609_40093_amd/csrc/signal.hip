@@ -346,6 +346,7 @@ namespace {
 constexpr const char *kSiteNames[kSiteCount] = {
     "unknown wait",  "wait_d2h",      "wait_recv",    "wait_dispatch",  "wait_combine",       "wait_returned_out",
     "landed_set",    "wait_credits",  "wait_returned", "wait_allgather", "wait_reducescatter", "the inbound-copy courier",
+    "wait_graph_landed", "the graph rounds' host-leg thread",
 };
 }  // namespace
 

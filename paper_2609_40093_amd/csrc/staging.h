@@ -56,6 +56,15 @@ constexpr int kSdmaSlots = 4;        // host-leg rounds in flight per staging
 // (environment EP_HOSTLEG_COPY=hip; kept as a measured comparison).
 bool d2h_through_hip();
 
+// ---- host legs of graph-replayed rounds on SDMA engines (graph_legs.cpp)
+class GraphLegs;
+// Starts the legs' thread at round `first_round`; nullptr with `err` on failure.
+GraphLegs *graph_legs_create(ep_staging *s, uint32_t first_round, std::string &err);
+// Stops the thread and waits for its copies in flight (null: no-op).
+void graph_legs_destroy(GraphLegs *g);
+// Rows each round moves (T * top-k of the dispatch last captured or run).
+void graph_legs_set_rows(GraphLegs *g, int64_t rows);
+
 // ---- exchange modes (exchange.cpp)
 class Exchange;
 constexpr int kMaxExchangeRanks = 32;  // 2R flags fit one polling wave; a sender set fits 32 bits
@@ -102,12 +111,13 @@ struct ep_staging {
     // (ep::kStatusWords words, status_block.h), then
     // inbound [nbuf][R], returned-out [nbuf][R], inbound-landed [nbuf][R],
     // recv-landed [nbuf][R], offsets mirror [nbuf][R+2], send credits [nbuf][R],
-    // recv credits [nbuf]
+    // recv credits [nbuf], graph-round ready [nbuf], graph-round landed [nbuf]
     uint32_t *flags = nullptr;
     size_t flag_words = 0;
     char *dev_epoch = nullptr;       // device: the epoch of each buffer set's current round
     uint32_t *dev_round = nullptr;   // device: round counter of graph-replayed rounds
     ep::SdmaLane *lane = nullptr;    // default device->host leg on one SDMA engine
+    ep::GraphLegs *graph_legs = nullptr;  // graph rounds' host legs on SDMA (ep_graph_legs_sdma)
     hipEvent_t ev_sysrel = nullptr;  // records a system-scope release before a DMA engine reads
     hipStream_t up = nullptr, down = nullptr;
     hipEvent_t ev_up_in[ep::kMaxBuffers] = {}, ev_up_done[ep::kMaxBuffers] = {};
@@ -147,9 +157,13 @@ struct ep_staging {
     uint32_t *mirror(int b) const { return ext_base() + 4 * nb() * R() + (size_t)b * (R() + 2); }
     uint32_t *send_credit(int b) const { return mirror(0) + nb() * (R() + 2) + (size_t)b * R(); }
     uint32_t *recv_credit(int b) const { return send_credit(0) + nb() * R() + (size_t)b; }
+    // graph rounds with SDMA legs: the dispatch's rows are in dev_send (set by the device),
+    // the returned rows are in dev_recv (set by the legs' thread)
+    uint32_t *graph_ready(int b) const { return recv_credit(0) + nb() + (size_t)b; }
+    uint32_t *graph_landed(int b) const { return graph_ready(0) + nb() + (size_t)b; }
     static size_t flag_words_for(int nbuf, int max_chunks, int R) {
         return (size_t)nbuf * (max_chunks + R) + ep::kStatusWords + 4 * (size_t)nbuf * R + (size_t)nbuf * (R + 2) +
-               (size_t)nbuf * R + (size_t)nbuf;
+               (size_t)nbuf * R + 3 * (size_t)nbuf;
     }
     uint32_t *epoch_word(int b) const { return reinterpret_cast<uint32_t *>(dev_epoch + b * ep::kEpochStride); }
 };

@@ -25,6 +25,8 @@ enum WaitSite : uint32_t {
     kSiteAllgather,       // wait_allgather
     kSiteReducescatter,   // wait_reducescatter
     kSiteCourier,         // the host thread gave up waiting for a sender's flag
+    kSiteGraphLanded,     // wait_graph_landed: graph rounds with SDMA legs, the returned rows landed
+    kSiteGraphLegs,       // the graph rounds' host-leg thread gave up on a flag or a copy
     kSiteCount
 };
 // The site of a wait kernel's launch name, and the name of a site.

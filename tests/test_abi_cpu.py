@@ -67,7 +67,7 @@ def test_binding_covers_every_symbol():
 
 
 def test_status_names(lib):
-    assert lib.ep_abi_version() == _lib.ABI_VERSION == 5
+    assert lib.ep_abi_version() == _lib.ABI_VERSION == 6
     assert lib.ep_status_name(0) == b"EP_OK"
     assert lib.ep_status_name(5) == b"EP_ERR_TIMEOUT"
     assert lib.ep_status_name(99) == b"EP_ERR_UNKNOWN"
@@ -135,6 +135,8 @@ def test_null_staging_calls(lib):
     assert lib.ep_combine(None, 0, 1, None, None, None, 4, 64, 2, None, 0, None) == _lib.EP_ERR_INVALID_ARG
     assert lib.ep_staging_set_mode(None, 0, 0) == _lib.EP_ERR_INVALID_ARG
     assert lib.ep_staging_set_inbound(None, 0, None) == _lib.EP_ERR_INVALID_ARG
+    assert lib.ep_graph_legs_sdma(None, 1) == _lib.EP_ERR_INVALID_ARG
+    assert lib.ep_graph_legs_sdma(None, 0) == _lib.EP_ERR_INVALID_ARG
     g = ctypes.c_double()
     assert lib.ep_pcie_probe(None, None, 16, 1, ctypes.byref(g)) == _lib.EP_ERR_INVALID_ARG
     assert lib.ep_pcie_probe(ctypes.c_void_p(16), ctypes.c_void_p(16), 16, 4, ctypes.byref(g)) == \
