@@ -356,8 +356,9 @@ ep_status ep_combine_graph(ep_staging *s, const int32_t *slot_pos, const float *
  * from the device recv buffer.  The other ranks (simulated peers) see the same flags,
  * credits and pinned buffers as with the compute-unit legs.  No copy depends on a signal
  * released by the device: each is queued once its source is complete.  The thread's
- * waits for the peers and for its copies are bounded by the staging's timeout; an expired
- * one is recorded in the status block (ep_staging_status) and the round goes on.
+ * waits for the peers and for its copies are bounded by the staging's timeout as set when
+ * the thread starts (ep_staging_set_wait); an expired one is recorded in the status block
+ * (ep_staging_status) and the round goes on.
  * ep_staging_free stops the thread.  EP_ERR_INVALID_ARG for a staging that graph rounds
  * cannot use; EP_ERR_HIP if no SDMA engine can be taken. */
 ep_status ep_graph_legs_sdma(ep_staging *s, int32_t on);

@@ -12,6 +12,7 @@
 // runtime's own choice of engine, kept as a measured comparison).
 #include "ep.h"
 #include "ep_internal.h"
+#include "graph_legs.h"
 #include "staging.h"
 
 #include <algorithm>
@@ -334,8 +335,11 @@ namespace {
 
 void staging_release(ep_staging *s) {
     // first the SDMA copies (each waits until its copies have landed), then their buffers
-    ep::graph_legs_destroy(s->graph_legs);
-    s->graph_legs = nullptr;
+    if (s->graph_legs) {
+        s->graph_legs->stop();
+        delete s->graph_legs;
+        s->graph_legs = nullptr;
+    }
     if (s->lane) {
         s->lane->release();
         delete s->lane;
@@ -921,9 +925,12 @@ extern "C" ep_status ep_graph_legs_sdma(ep_staging *s, int32_t on) {
     if (st != EP_OK)
         return st;
     if (!on) {
-        EP_HIP(hipDeviceSynchronize());  // no captured round may still wait for the thread
-        ep::graph_legs_destroy(s->graph_legs);
-        s->graph_legs = nullptr;
+        if (s->graph_legs) {
+            EP_HIP(hipDeviceSynchronize());  // no captured round may still wait for the thread
+            s->graph_legs->stop();
+            delete s->graph_legs;
+            s->graph_legs = nullptr;
+        }
         return EP_OK;
     }
     if (s->graph_legs)
@@ -932,10 +939,32 @@ extern "C" ep_status ep_graph_legs_sdma(ep_staging *s, int32_t on) {
     EP_HIP(hipDeviceSynchronize());
     uint32_t round = 0;
     EP_HIP(hipMemcpy(&round, s->dev_round, sizeof round, hipMemcpyDeviceToHost));
+    ep::GraphLegsIO io{};
+    for (int b = 0; b < 2; ++b) {
+        io.ready[b] = s->graph_ready(b);
+        io.landed[b] = s->graph_landed(b);
+        io.send_flags[b] = s->send_flags(b);
+        io.recv_flags[b] = s->recv_flags(b);
+        io.recv_credit[b] = s->recv_credit(b);
+        io.dev_send[b] = s->dev_send[b];
+        io.dev_recv[b] = s->dev_recv[b];
+        io.host_send[b] = s->host_send[b];
+        io.host_recv[b] = s->host_recv[b];
+    }
+    io.send_flag_words = s->max_chunks;
+    io.senders = s->num_ranks;
+    io.status = s->status();
+    io.row_bytes = s->row_bytes;
+    io.timeout_us = s->timeout_us;
+    ep::GraphLegs *g = new ep::GraphLegs();
     std::string err;
-    s->graph_legs = ep::graph_legs_create(s, round + 1u, err);
-    if (!s->graph_legs)
+    if (!g->dma.init(s->device, err)) {
+        g->dma.release();  // drops the ROCr reference init may have taken
+        delete g;
         return fail(EP_ERR_HIP, "ep_graph_legs_sdma: %s", err.c_str());
+    }
+    g->start(io, round + 1u);
+    s->graph_legs = g;
     return EP_OK;
 }
 
@@ -956,7 +985,7 @@ extern "C" ep_status ep_dispatch_graph(const void *x_dev, int64_t num_tokens, in
     // send buffer, from which the legs' thread copies them once the ready word holds the round
     const bool sdma = s->graph_legs != nullptr;
     if (sdma)
-        ep::graph_legs_set_rows(s->graph_legs, num_tokens * topk);
+        s->graph_legs->set_rows(num_tokens * topk);
     void *const *dst = sdma ? s->dev_send : s->host_send;
     ep::RoundSel sel;
     sel.alt = dst[1];

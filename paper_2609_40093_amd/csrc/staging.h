@@ -56,14 +56,8 @@ constexpr int kSdmaSlots = 4;        // host-leg rounds in flight per staging
 // (environment EP_HOSTLEG_COPY=hip; kept as a measured comparison).
 bool d2h_through_hip();
 
-// ---- host legs of graph-replayed rounds on SDMA engines (graph_legs.cpp)
+// ---- host legs of graph-replayed rounds on SDMA engines (graph_legs.h)
 class GraphLegs;
-// Starts the legs' thread at round `first_round`; nullptr with `err` on failure.
-GraphLegs *graph_legs_create(ep_staging *s, uint32_t first_round, std::string &err);
-// Stops the thread and waits for its copies in flight (null: no-op).
-void graph_legs_destroy(GraphLegs *g);
-// Rows each round moves (T * top-k of the dispatch last captured or run).
-void graph_legs_set_rows(GraphLegs *g, int64_t rows);
 
 // ---- exchange modes (exchange.cpp)
 class Exchange;

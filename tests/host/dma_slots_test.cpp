@@ -1,5 +1,6 @@
-// dma_slots_test.cpp -- host-only test of the SDMA lane's and the exchange's signal
-// handling (sdma.h, exchange.h, signal_slots.h) against a stand-in for the ROCr runtime.
+// dma_slots_test.cpp -- host-only test of the SDMA lane's, the exchange's and the graph
+// rounds' host legs (sdma.h, exchange.h, graph_legs.h, signal_slots.h) against a stand-in
+// for the ROCr runtime.
 //
 // The stand-in keeps the documented contract of an async copy: it starts once every
 // dependency signal reads exactly 0, it writes its bytes, and afterwards it decrements
@@ -13,12 +14,15 @@
 //   - an engine waiting longer than the test allows.
 // Destroyed handles are recycled last-in first-out, as a signal pool would.
 //
-// Usage: dma_slots_test lane|exchange|order|merge|bounded|old_rule [seed]; prints
-// "violations N" and exits 0 when N == 0 and every check of the scenario held.
+// Usage: dma_slots_test lane|exchange|order|merge|bounded|graph|graph_timeout|old_rule
+// [seed]; prints "violations N" and exits 0 when N == 0 and every check of the scenario
+// held.
 #include "exchange.h"
+#include "graph_legs.h"
 #include "sdma.h"
 #include "signal_slots.h"
 
+#include <algorithm>
 #include <atomic>
 #include <chrono>
 #include <condition_variable>
@@ -787,6 +791,167 @@ void scenario_bounded() {
     check(g_destroyed.load() == before, "no signal destroyed while one may still be decremented");
 }
 
+// Waits (at most 5 s) until (int32)(*w - want) >= 0.
+bool wait_for(const uint32_t *w, uint32_t want) {
+    const auto t0 = Clock::now();
+    while ((int32_t)(__atomic_load_n(w, __ATOMIC_ACQUIRE) - want) < 0) {
+        if (Clock::now() - t0 > std::chrono::seconds(5))
+            return false;
+        std::this_thread::yield();
+    }
+    return true;
+}
+
+// The two buffer sets of graph-replayed rounds with SDMA legs, in host memory (the
+// stand-in engines copy between any two buffers).
+constexpr int kGraphSenders = 4, kGraphFlagWords = 3;
+constexpr int64_t kGraphRowBytes = 64, kGraphMaxRows = 64;
+struct GraphSet {
+    std::vector<uint8_t> dev_send, dev_recv, host_send, host_recv;
+    uint32_t ready = 0, landed = 0, recv_credit = 0;
+    uint32_t send_flags[kGraphFlagWords] = {}, recv_flags[kGraphSenders] = {}, send_credits[kGraphSenders] = {};
+    GraphSet() {
+        for (auto *v : {&dev_send, &dev_recv, &host_send, &host_recv})
+            v->assign((size_t)(kGraphMaxRows * kGraphRowBytes), 0);
+    }
+};
+ep::GraphLegsIO graph_io(GraphSet *sets, uint32_t *status, int64_t timeout_us) {
+    ep::GraphLegsIO io{};
+    for (int b = 0; b < 2; ++b) {
+        GraphSet &g = sets[b];
+        io.ready[b] = &g.ready;
+        io.landed[b] = &g.landed;
+        io.send_flags[b] = g.send_flags;
+        io.recv_flags[b] = g.recv_flags;
+        io.recv_credit[b] = &g.recv_credit;
+        io.dev_send[b] = g.dev_send.data();
+        io.dev_recv[b] = g.dev_recv.data();
+        io.host_send[b] = g.host_send.data();
+        io.host_recv[b] = g.host_recv.data();
+    }
+    io.send_flag_words = kGraphFlagWords;
+    io.senders = kGraphSenders;
+    io.status = status;
+    io.row_bytes = kGraphRowBytes;
+    io.timeout_us = timeout_us;
+    return io;
+}
+uint8_t sent_byte(uint32_t r, size_t i) { return (uint8_t)(r * 7u + i); }
+
+// Graph-replayed rounds with SDMA legs (graph_legs.h), 200 rounds: a device stand-in (this
+// thread) waits for the receivers' credits of round r - 2, packs a number of rows that
+// changes from round to round into the device send buffer of set r % 2 and stamps the
+// set's ready word; simulated peers wait for the last send flag, check the rows in the
+// host send buffer, wait for this rank's receive credit of round r - 2, write their
+// returned rows (each sent byte plus r), credit the send buffer and raise their flags in
+// a random order after random delays; the device stand-in waits for the landed word,
+// checks the rows in the device receive buffer and credits the set.  The stand-in engines
+// apply completion decrements late.
+void scenario_graph(uint32_t seed) {
+    static GraphSet sets[2];
+    uint32_t status[ep::kStatusWords] = {};
+    ep::GraphLegs legs;
+    legs.dma.init_with(kGpu, kCpu, 1u, {2u});
+    legs.start(graph_io(sets, status, 5ll * 1000 * 1000), 1);
+    constexpr uint32_t kRounds = 200;
+    std::vector<int64_t> rows(kRounds + 1);
+    std::mt19937 rng(seed);
+    for (auto &n : rows)
+        n = 1 + (int64_t)(rng() % kGraphMaxRows);
+    std::atomic<int> peer_failures{0};
+    std::thread peers([&] {
+        std::mt19937 prng(seed + 1);
+        for (uint32_t r = 1; r <= kRounds; ++r) {
+            GraphSet &g = sets[r & 1u];
+            if (!wait_for(&g.send_flags[kGraphFlagWords - 1], r)) {
+                ++peer_failures;
+                return;
+            }
+            const size_t n = (size_t)(rows[r] * kGraphRowBytes);
+            for (size_t i = 0; i < n; ++i)
+                if (g.host_send[i] != sent_byte(r, i)) {
+                    ++peer_failures;  // a send flag came before its rows
+                    break;
+                }
+            for (int c = 0; c < kGraphFlagWords; ++c)
+                if (__atomic_load_n(&g.send_flags[c], __ATOMIC_ACQUIRE) != r)
+                    ++peer_failures;
+            if (!wait_for(&g.recv_credit, r - 2u)) {
+                ++peer_failures;
+                return;
+            }
+            for (size_t i = 0; i < n; ++i)
+                g.host_recv[i] = (uint8_t)(g.host_send[i] + r);
+            for (int i = 0; i < kGraphSenders; ++i)
+                __atomic_store_n(&g.send_credits[i], r, __ATOMIC_RELEASE);
+            int order[kGraphSenders] = {0, 1, 2, 3};
+            std::shuffle(order, order + kGraphSenders, prng);
+            for (int i : order) {
+                std::this_thread::sleep_for(std::chrono::microseconds(prng() % 100));
+                __atomic_store_n(&g.recv_flags[i], r, __ATOMIC_RELEASE);
+            }
+        }
+    });
+    bool rows_ok = true, landed_ok = true, credits_ok = true;
+    for (uint32_t r = 1; r <= kRounds; ++r) {
+        GraphSet &g = sets[r & 1u];
+        for (int i = 0; i < kGraphSenders; ++i)
+            credits_ok = credits_ok && wait_for(&g.send_credits[i], r - 2u);
+        const size_t n = (size_t)(rows[r] * kGraphRowBytes);
+        for (size_t i = 0; i < n; ++i)
+            g.dev_send[i] = sent_byte(r, i);
+        legs.set_rows(rows[r]);
+        __atomic_store_n(&g.ready, r, __ATOMIC_RELEASE);
+        if (!wait_for(&g.landed, r)) {
+            landed_ok = false;
+            break;
+        }
+        for (size_t i = 0; i < n; ++i)
+            rows_ok = rows_ok && g.dev_recv[i] == (uint8_t)(sent_byte(r, i) + r);
+        __atomic_store_n(&g.recv_credit, r, __ATOMIC_RELEASE);
+    }
+    peers.join();
+    legs.stop();
+    check(credits_ok, "the peers credited every send buffer");
+    check(landed_ok, "every round landed");
+    check(rows_ok, "every round's returned rows were in the device receive buffer when it landed");
+    check(peer_failures == 0, "every send flag came after its rows, with every flag word of the set");
+    check(status[0] == 0, "no wait of the legs' thread expired");
+}
+
+// Graph rounds with SDMA legs and peers that never answer: the thread copies the rows out
+// and raises the send flags, gives up on the senders after its bound (20 ms), records the
+// wait in the status block and still lands the round; a thread waiting for a round the
+// device never reaches stops at once.
+void scenario_graph_timeout() {
+    static GraphSet sets[2];
+    uint32_t status[ep::kStatusWords] = {};
+    ep::GraphLegs legs;
+    legs.dma.init_with(kGpu, kCpu, 1u, {2u});
+    legs.start(graph_io(sets, status, 20 * 1000), 1);
+    GraphSet &g = sets[1];
+    for (size_t i = 0; i < (size_t)(8 * kGraphRowBytes); ++i)
+        g.dev_send[i] = sent_byte(1, i);
+    legs.set_rows(8);
+    const auto t0 = Clock::now();
+    __atomic_store_n(&g.ready, 1u, __ATOMIC_RELEASE);
+    check(wait_for(&g.landed, 1u), "the late round still lands");
+    check(Clock::now() - t0 >= std::chrono::milliseconds(20), "after the wait's bound");
+    check(__atomic_load_n(&g.send_flags[0], __ATOMIC_ACQUIRE) == 1u, "the send flags are up");
+    bool sent = true;
+    for (size_t i = 0; i < (size_t)(8 * kGraphRowBytes); ++i)
+        sent = sent && g.host_send[i] == sent_byte(1, i);
+    check(sent, "the rows reached the host send buffer");
+    check(__atomic_load_n(&status[0], __ATOMIC_ACQUIRE) == 5u, "the status block holds a timeout");
+    check(status[1] == ep::kSiteGraphLegs, "recorded as the legs' thread's wait");
+    const uint64_t flag = (uint64_t)status[2] | ((uint64_t)status[3] << 32);
+    check(flag == reinterpret_cast<uint64_t>(&g.recv_flags[0]), "naming the first sender's flag");
+    check(status[5] == 1u, "and the round it waited for");
+    const auto t1 = Clock::now();
+    legs.stop();  // the thread now waits for round 2, which never comes
+    check(Clock::now() - t1 < std::chrono::milliseconds(500), "a stop ends the wait for the next round");
+}
+
 // The reuse rule this library had before, replayed directly against the stand-in: one
 // completion signal shared by two flag copies, reset for the next call as soon as the
 // host sees the flags.  With late decrements the stand-in must report a violation; this
@@ -836,10 +1001,14 @@ int main(int argc, char **argv) {
         scenario_merge();
     else if (what == "bounded")
         scenario_bounded();
+    else if (what == "graph")
+        scenario_graph(seed);
+    else if (what == "graph_timeout")
+        scenario_graph_timeout();
     else if (what == "old_rule")
         scenario_old_rule(seed);
     else {
-        std::printf("usage: %s lane|exchange|order|merge|bounded|old_rule [seed]\n", argv[0]);
+        std::printf("usage: %s lane|exchange|order|merge|bounded|graph|graph_timeout|old_rule [seed]\n", argv[0]);
         return 2;
     }
     // let every queued copy finish before the engines stop

@@ -23,11 +23,18 @@ Cases:
   before the other senders of an all-senders job answer; the pieces of a host-side result
   (eager copies whose flags the job's host work raises) go down as each is ready, without
   their flags holding back that host work;
+- graph: 200 graph-replayed rounds with SDMA legs (graph_legs.h) between a device
+  stand-in and simulated peers, with the row count changing from round to round: every
+  send flag comes after its rows, every landed word after the returned rows;
+- graph_timeout: the same thread with peers that never answer records the expired wait
+  (site, flag, round) in the status block and still lands the round; a stop ends its wait
+  for a round the device never reaches;
 - bounded: a slot with a signal that never retires is refused after its bound, with a
   message; a failed copy (negative value) is reported once; nothing is destroyed while a
   decrement may still come;
-- the lane, exchange, order and merge scenarios again, built with ThreadSanitizer: no data
-  race between the courier thread, the stand-in engines and the callers' threads;
+- the lane, exchange, order, merge and graph scenarios again, built with ThreadSanitizer: no
+  data race between the courier thread, the graph legs' thread, the stand-in engines and
+  the callers' threads;
 - old_rule: the reuse rule of the earlier revision (a completion signal shared by two
   copies, reset as soon as the flags are seen) replayed against the stand-in, which must
   report the late decrement: the harness does catch the failure mode.
@@ -52,6 +59,7 @@ def binary(tmp_path_factory):
     cmd = [gxx, "-std=c++17", "-O1", "-g", "-Wall", "-D__HIP_PLATFORM_AMD__", "-I", ROCM_INCLUDE,
            "-I", os.path.join(ROOT, "include"), "-I", CSRC,
            os.path.join(ROOT, "tests", "host", "dma_slots_test.cpp"), os.path.join(CSRC, "sdma_lane.cpp"),
+           os.path.join(CSRC, "graph_legs.cpp"),
            "-o", out, "-lpthread"]
     res = subprocess.run(cmd, capture_output=True, text=True)
     assert res.returncode == 0, res.stderr[-4000:]
@@ -87,6 +95,18 @@ def test_contiguous_ready_copies_go_as_one_and_own_rows_go_first(binary):
     assert rc == 0, out
 
 
+@pytest.mark.parametrize("seed", [1, 2])
+def test_graph_legs_raise_flags_only_after_their_rows(binary, seed):
+    rc, out = run(binary, "graph", seed)
+    assert rc == 0, out
+    assert "violations 0 checks_failed 0" in out
+
+
+def test_graph_legs_report_an_expired_wait_and_stop(binary):
+    rc, out = run(binary, "graph_timeout", timeout=60)
+    assert rc == 0, out
+
+
 def test_slot_reuse_is_bounded_and_reported(binary):
     rc, out = run(binary, "bounded", timeout=60)
     assert rc == 0, out
@@ -108,6 +128,7 @@ def tsan_binary(tmp_path_factory):
     cmd = [gxx, "-std=c++17", "-O1", "-g", "-fsanitize=thread", "-D__HIP_PLATFORM_AMD__", "-I", ROCM_INCLUDE,
            "-I", os.path.join(ROOT, "include"), "-I", CSRC,
            os.path.join(ROOT, "tests", "host", "dma_slots_test.cpp"), os.path.join(CSRC, "sdma_lane.cpp"),
+           os.path.join(CSRC, "graph_legs.cpp"),
            "-o", out, "-lpthread"]
     res = subprocess.run(cmd, capture_output=True, text=True)
     if res.returncode != 0 and "tsan" in (res.stderr + res.stdout).lower():
@@ -116,7 +137,7 @@ def tsan_binary(tmp_path_factory):
     return out
 
 
-@pytest.mark.parametrize("scenario", ["lane", "exchange", "order", "merge"])
+@pytest.mark.parametrize("scenario", ["lane", "exchange", "order", "merge", "graph"])
 def test_lane_courier_and_slots_have_no_data_race(tsan_binary, scenario):
     """The lane, the courier thread, the signal slots and the callers' threads share flags,
     signals and job queues: ThreadSanitizer reports no data race in any scenario."""
