@@ -768,6 +768,7 @@ def bench_graph(names, args, dev, peaks) -> dict:
             if legs == "sdma_legs":
                 ep.graph_legs_sdma(st, True)
             lay = ep.dispatch_layout(idx, E, R)
+            unsettled = settle_h2d(dev)
 
             def one_round():
                 ep.round_advance(st)
@@ -805,10 +806,13 @@ def bench_graph(names, args, dev, peaks) -> dict:
             res[name][legs] = {"us_per_round": round(us, 1), "pcie_bytes_per_round": pcie,
                                "pcie_GBps": round(gbps, 2),
                                "frac_of_one_way_pcie_peak": round(gbps / peaks["d2h_alone"], 3), "replays": steps}
+            if unsettled:
+                res[name][legs]["earlier_unsettled_probes"] = unsettled
     res["note"] = ("compute_unit_legs: rows stored to and loaded from pinned memory by the compute units; sdma_legs: "
                    "rows packed into and reduced from device memory by the captured kernels and moved by SDMA "
                    "engines (the library's host-leg thread); the two directions run one after the other within a "
-                   "round, so the one-way peak bounds the rate")
+                   "round, so the one-way peak bounds the rate; each measurement starts once host->device copies "
+                   "run within 20% of device->host ones (settle_h2d)")
     return res
 
 
@@ -860,6 +864,29 @@ def pcie_peaks(dev) -> dict:
     if unsettled:
         res["earlier_unsettled_probes"] = unsettled
     return res
+
+
+def settle_h2d(dev, max_s: float = 10.0) -> list:
+    """Waits (up to max_s) until host->device SDMA copies run within 20% of device->host
+    ones (256 MiB probes on one pinned buffer): after a process, or an earlier section,
+    freed tens of GB of pinned memory, host->device copies run at about half their rate
+    for a few seconds.  Returns the probes taken while they had not settled."""
+    import torch
+
+    import paper_2609_40093_amd as ep
+    nbytes = 256 << 20
+    host = torch.empty(2 * nbytes, dtype=torch.uint8, pin_memory=True)
+    devb = torch.empty(2 * nbytes, dtype=torch.uint8, device=dev)
+    unsettled = []
+    deadline = time.perf_counter() + max_s
+    while True:
+        d2h, h2d = ep.pcie_probe(host, devb, nbytes, 1), ep.pcie_probe(host, devb, nbytes, 2)
+        if h2d >= 0.8 * d2h or time.perf_counter() >= deadline:
+            break
+        unsettled.append({"d2h_alone": round(d2h, 2), "h2d_alone": round(h2d, 2)})
+        time.sleep(0.5)
+    del host, devb
+    return unsettled
 
 
 def ceiling_of(kernel: str, frac, ceilings: dict, k: int) -> dict:
