@@ -359,8 +359,12 @@ ep_status ep_combine_graph(ep_staging *s, const int32_t *slot_pos, const float *
  * waits for the peers and for its copies are bounded by the staging's timeout as set when
  * the thread starts (ep_staging_set_wait); an expired one is recorded in the status block
  * (ep_staging_status) and the round goes on.
- * ep_staging_free stops the thread.  EP_ERR_INVALID_ARG for a staging that graph rounds
- * cannot use; EP_ERR_HIP if no SDMA engine can be taken. */
+ * Which legs a round uses is fixed when its ep_dispatch_graph / ep_combine_graph calls are
+ * made (or captured): replay rounds captured with the thread running only while it runs
+ * (otherwise their combine waits out its bound and reports EP_ERR_TIMEOUT), and rounds
+ * captured without it keep the compute-unit legs.  ep_staging_free stops the thread.
+ * EP_ERR_INVALID_ARG for a staging that graph rounds cannot use; EP_ERR_HIP if no SDMA
+ * engine can be taken. */
 ep_status ep_graph_legs_sdma(ep_staging *s, int32_t on);
 
 /* ------------------------------------------------------- dense collectives (Sec. 4.2)
