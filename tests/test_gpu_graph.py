@@ -253,3 +253,38 @@ def test_graph_legs_report_peers_that_never_answer():
     assert np.array_equal(st.host_array("send", 1)[:case.slots], oracle.pack(payload(case, 1), ref.slot_pos, case.k))
     ep.graph_legs_sdma(st, False)
     st.close()
+
+
+@pytest.mark.parametrize("legs", LEGS)
+def test_graph_replay_at_the_decode_layer_shape(legs):
+    """The decode layer's shape (T=256, H=7168, 256 experts top-8, R=8: 29 MB each way per
+    round) through captured rounds: every replay returns x exactly (identity experts, gates
+    1/8, fp32 output) and leaves the oracle's packed rows in the pinned send buffer."""
+    case, st, peers, idx, w, x, out, lay = setup(T=256, H=7168, E=256, k=8, R=8, seed=36, legs=legs)
+    xr = payload(case, 0)
+    x.copy_(torch.from_numpy(xr.view(np.int16)))
+    one_round(st, idx, w, x, out, lay, case)
+    torch.cuda.synchronize()
+    peers.wait_round(1)
+    g = torch.cuda.CUDAGraph()
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        with torch.cuda.graph(g, stream=s):
+            one_round(st, idx, w, x, out, lay, case)
+    torch.cuda.current_stream().wait_stream(s)
+    torch.cuda.synchronize()
+    slots = oracle.layout(case.topk_idx, case.E, case.R).slot_pos
+    for rep in range(4):
+        say(f"decode-shape graph replay {rep} ({legs} legs)")
+        xr = payload(case, 400 + rep)
+        x.copy_(torch.from_numpy(xr.view(np.int16)))
+        g.replay()
+        torch.cuda.synchronize()
+        peers.wait_round(2 + rep)
+        st.status()
+        assert np.array_equal(out.cpu().numpy(), as_f32(xr)), f"replay {rep}"
+        sent = st.host_array("send", (2 + rep) % 2)[:case.slots]
+        assert np.array_equal(sent, oracle.pack(xr, slots, case.k)), f"replay {rep}: pinned send rows"
+    peers.close()
+    st.close()
