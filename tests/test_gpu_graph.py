@@ -288,3 +288,39 @@ def test_graph_replay_at_the_decode_layer_shape(legs):
         assert np.array_equal(sent, oracle.pack(xr, slots, case.k)), f"replay {rep}: pinned send rows"
     peers.close()
     st.close()
+
+
+@pytest.mark.parametrize("legs", LEGS)
+def test_graph_replay_with_a_split_combine(legs):
+    """A combine whose fp32 output passes 128 MiB runs as token-range launches; in graph
+    rounds each of them reads the round's buffer set (pinned memory with compute-unit legs,
+    device memory with SDMA legs).  T=4700 tokens of H=7168, top-2 of 16, R=4 (132 MiB
+    each way per round): three replays return x exactly."""
+    case, st, peers, idx, w, x, out, lay = setup(T=4700, H=7168, E=16, k=2, R=4, seed=37, legs=legs)
+    assert case.T * case.H * 4 >= 128 << 20
+    xr = payload(case, 0)
+    x.copy_(torch.from_numpy(xr.view(np.int16)))
+    one_round(st, idx, w, x, out, lay, case)
+    torch.cuda.synchronize()
+    peers.wait_round(1)
+    st.status()
+    assert np.array_equal(out.cpu().numpy(), as_f32(xr)), "eager round"
+    g = torch.cuda.CUDAGraph()
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        with torch.cuda.graph(g, stream=s):
+            one_round(st, idx, w, x, out, lay, case)
+    torch.cuda.current_stream().wait_stream(s)
+    torch.cuda.synchronize()
+    for rep in range(3):
+        say(f"split-combine graph replay {rep} ({legs} legs)")
+        xr = payload(case, 500 + rep)
+        x.copy_(torch.from_numpy(xr.view(np.int16)))
+        g.replay()
+        torch.cuda.synchronize()
+        peers.wait_round(2 + rep)
+        st.status()
+        assert np.array_equal(out.cpu().numpy(), as_f32(xr)), f"replay {rep}"
+    peers.close()
+    st.close()
